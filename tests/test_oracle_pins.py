@@ -1,0 +1,395 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these compare the oracle with itself: they use hand-worked examples
+(tests/golden), invariants of BN training, adjoint identities, finite
+differences, textbook special cases (1x1 CONV = matrix product, delta filters)
+and independent library routines (numpy matmul, torch CPU fp64 conv2d /
+batch_norm / autograd, torch's bf16 cast).  Runs on the CPU only.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import compose as OC
+from oracle import prims as P
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+RNG = np.random.default_rng(1234)
+
+
+def _golden(name):
+    d = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            k, *v = line.split()
+            d[k] = np.array([float(t) for t in v])
+    return d
+
+
+def _nchw(a):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, np.float64).transpose(0, 3, 1, 2)))
+
+
+def _nhwc(t):
+    return t.detach().numpy().transpose(0, 2, 3, 1)
+
+
+def _oihw(w):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(w, np.float64).transpose(3, 2, 0, 1)))
+
+
+# ------------------------------------------------------------- golden ----
+def test_bn_worked_example():
+    g = _golden("bn_worked_example.txt")
+    x = g["x"].reshape(4, 1)
+    y, mean, var, rstd = P.bn_fwd(x, g["gamma"], g["beta"], float(g["eps"][0]))
+    np.testing.assert_allclose(mean, g["mean"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(var, g["var"], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(rstd, g["rstd"], rtol=1e-14)
+    np.testing.assert_allclose(y[:, 0], g["y"], rtol=1e-14)
+    m1, v1 = P.mvf_stats(x)
+    np.testing.assert_allclose(v1, g["var"], rtol=0, atol=1e-15)
+    dx, dgamma, dbeta = P.bn_bwd(x, g["dy"].reshape(4, 1), g["gamma"], mean, rstd)
+    np.testing.assert_allclose(dbeta, g["dbeta"], rtol=1e-14)
+    np.testing.assert_allclose(dgamma, g["dgamma"], rtol=1e-14)
+    np.testing.assert_allclose(dx[:, 0], g["dx"], rtol=1e-13, atol=1e-15)
+
+
+def test_conv_worked_example():
+    g = _golden("conv_worked_example.txt")
+    x = g["input"].reshape(1, 3, 3, 1)
+    ones = np.ones((3, 3, 1, 1))
+    np.testing.assert_array_equal(P.conv_fwd(x, ones).ravel(), g["ones"])
+    w = np.zeros((3, 3, 1, 1)); w[0, 0] = 1
+    np.testing.assert_array_equal(P.conv_fwd(x, w).ravel(), g["tap00"])
+    w = np.zeros((3, 3, 1, 1)); w[2, 1] = 1
+    np.testing.assert_array_equal(P.conv_fwd(x, w).ravel(), g["tap21"])
+
+
+# ------------------------------------------------------------ BN forward ----
+@pytest.mark.parametrize("m,C,shift", [(512, 7, 0.0), (3000, 5, 10.0), (2, 3, 0.0)])
+def test_bn_fwd_normalised_moments(m, C, shift):
+    x = RNG.standard_normal((m, C)) * RNG.uniform(0.1, 5, C) + shift
+    y, mean, var, rstd = P.bn_fwd(x, np.ones(C), np.zeros(C), 0.0)
+    assert np.max(np.abs(y.mean(0))) < 1e-12
+    assert np.max(np.abs((y * y).mean(0) - 1)) < 1e-12
+    eps = 1e-5
+    y, mean, var, rstd = P.bn_fwd(x, np.ones(C), np.zeros(C), eps)
+    assert np.max(np.abs(y.mean(0))) < 1e-12
+    np.testing.assert_allclose((y * y).mean(0), var / (var + eps), rtol=0, atol=1e-12)
+
+
+def test_bn_fwd_affine_and_special_cases():
+    C = 4
+    x = RNG.standard_normal((100, C))
+    gamma, beta = RNG.uniform(0.5, 1.5, C), RNG.normal(0, 0.1, C)
+    y0, *_ = P.bn_fwd(x, np.ones(C), np.zeros(C), 1e-5)
+    y, *_ = P.bn_fwd(x, gamma, beta, 1e-5)
+    np.testing.assert_allclose(y, gamma * y0 + beta, rtol=0, atol=1e-13)
+    # one value per channel: xhat = 0, so y = beta
+    y1, *_ = P.bn_fwd(x[:1], gamma, beta, 1e-5)
+    np.testing.assert_array_equal(y1[0], beta)
+    # a constant channel: y = beta
+    yc, mean, var, _ = P.bn_fwd(np.full((50, C), 3.25), gamma, beta, 1e-5)
+    np.testing.assert_array_equal(var, 0.0)
+    np.testing.assert_array_equal(yc, np.broadcast_to(beta, (50, C)))
+
+
+def test_bn_fwd_matches_torch_batch_norm():
+    x = RNG.standard_normal((6, 5, 7, 9)) * 2 + 1
+    gamma, beta = RNG.uniform(0.5, 1.5, 9), RNG.normal(0, 0.1, 9)
+    y, mean, var, rstd = P.bn_fwd(x, gamma, beta, 1e-5)
+    ref = F.batch_norm(_nchw(x), None, None, torch.from_numpy(gamma), torch.from_numpy(beta),
+                       training=True, eps=1e-5)
+    np.testing.assert_allclose(y, _nhwc(ref), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(var, x.reshape(-1, 9).var(0), rtol=1e-13)     # biased (ddof=0)
+
+
+def test_mvf_stats_equal_two_pass():
+    # small integers over m = 2^10 values: both forms are exact in fp64
+    x = RNG.integers(-50, 50, (1024, 6)).astype(np.float64)   # m = 2^10: every step exact
+    m1, v1 = P.mvf_stats(x)
+    m2, v2, _ = P.bn_stats(x, 0.0)
+    np.testing.assert_array_equal(m1, m2)
+    np.testing.assert_array_equal(v1, v2)
+    x = RNG.standard_normal((4096, 3)) + 3.0
+    m1, v1 = P.mvf_stats(x)
+    np.testing.assert_allclose(v1, x.var(0), rtol=1e-12)
+    np.testing.assert_allclose(m1, x.mean(0), rtol=1e-14)
+
+
+# ----------------------------------------------------------- BN backward ----
+def test_bn_bwd_invariants():
+    m, C = 777, 6
+    x = RNG.standard_normal((m, C)) * 3 - 1
+    dy = RNG.standard_normal((m, C))
+    for gamma, beta in ((np.ones(C), np.zeros(C)), (RNG.uniform(0.5, 1.5, C), RNG.normal(0, 0.1, C))):
+        for eps in (0.0, 1e-5):
+            _, mean, var, rstd = P.bn_fwd(x, gamma, beta, eps)
+            dx, dgamma, dbeta = P.bn_bwd(x, dy, gamma, mean, rstd)
+            assert np.max(np.abs(dx.sum(0))) < 1e-10
+            xhat = (x - mean) * rstd
+            if eps == 0.0:
+                assert np.max(np.abs((dx * xhat).sum(0))) < 1e-10
+    # one value per channel, and gamma = 0: dx = 0
+    _, mean, var, rstd = P.bn_fwd(x[:1], np.ones(C), np.zeros(C), 1e-5)
+    dx, _, _ = P.bn_bwd(x[:1], dy[:1], np.ones(C), mean, rstd)
+    np.testing.assert_array_equal(dx, 0.0)
+    _, mean, var, rstd = P.bn_fwd(x, np.zeros(C), np.zeros(C), 1e-5)
+    dx, _, _ = P.bn_bwd(x, dy, np.zeros(C), mean, rstd)
+    np.testing.assert_array_equal(dx, 0.0)
+
+
+def test_bn_bwd_matches_torch_autograd():
+    x = RNG.standard_normal((4, 5, 6, 7))
+    gamma, beta = RNG.uniform(0.5, 1.5, 7), RNG.normal(0, 0.1, 7)
+    g = RNG.standard_normal(x.shape)
+    xt = _nchw(x).requires_grad_()
+    gt = torch.from_numpy(gamma).requires_grad_()
+    bt = torch.from_numpy(beta).requires_grad_()
+    yt = F.batch_norm(xt, None, None, gt, bt, training=True, eps=1e-5)
+    (yt * _nchw(g)).sum().backward()
+    _, mean, var, rstd = P.bn_fwd(x, gamma, beta, 1e-5)
+    dx, dgamma, dbeta = P.bn_bwd(x, g, gamma, mean, rstd)
+    np.testing.assert_allclose(dx, _nhwc(xt.grad), rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dgamma, gt.grad.numpy(), rtol=1e-11)
+    np.testing.assert_allclose(dbeta, bt.grad.numpy(), rtol=1e-11)
+
+
+# ------------------------------------------------------------------ ReLU ----
+def test_relu():
+    y = np.array([-2.0, -0.0, 0.0, 1e-300, 3.0])
+    np.testing.assert_array_equal(P.relu_fwd(y), [0, 0, 0, 1e-300, 3.0])
+    np.testing.assert_array_equal(P.relu_bwd(np.full(5, 7.0), y), [0, 0, 0, 7.0, 7.0])
+
+
+# ------------------------------------------------------------------ CONV ----
+def test_conv1x1_is_matrix_product():
+    x = RNG.standard_normal((3, 5, 4, 11))
+    w = RNG.standard_normal((1, 1, 11, 6))
+    out = P.conv_fwd(x, w)
+    np.testing.assert_allclose(out.reshape(-1, 6), x.reshape(-1, 11) @ w[0, 0], rtol=0, atol=1e-12)
+    g = RNG.standard_normal(out.shape)
+    np.testing.assert_allclose(P.conv_dgrad(g, w, (5, 4)).reshape(-1, 11), g.reshape(-1, 6) @ w[0, 0].T,
+                               rtol=0, atol=1e-12)
+    np.testing.assert_allclose(P.conv_wgrad(x, g, 1)[0, 0], x.reshape(-1, 11).T @ g.reshape(-1, 6),
+                               rtol=0, atol=1e-11)
+
+
+def test_conv3x3_centre_delta_is_identity():
+    x = RNG.standard_normal((2, 4, 5, 3))
+    w = np.zeros((3, 3, 3, 3))
+    w[1, 1] = np.eye(3)
+    np.testing.assert_array_equal(P.conv_fwd(x, w), x)
+
+
+@pytest.mark.parametrize("K,stride,pad,H,W", [(1, 1, 0, 5, 6), (3, 1, 1, 5, 6), (3, 1, 1, 1, 1),
+                                              (7, 2, 3, 11, 10), (3, 2, 1, 7, 7)])
+def test_conv_matches_torch(K, stride, pad, H, W):
+    x = RNG.standard_normal((2, H, W, 4))
+    w = RNG.standard_normal((K, K, 4, 5))
+    g = None
+    xt = _nchw(x).requires_grad_()
+    wt = _oihw(w).requires_grad_()
+    out_t = F.conv2d(xt, wt, stride=stride, padding=pad)
+    out = P.conv_fwd(x, w, stride, pad)
+    np.testing.assert_allclose(out, _nhwc(out_t), rtol=0, atol=1e-12)
+    g = RNG.standard_normal(out.shape)
+    (out_t * _nchw(g)).sum().backward()
+    np.testing.assert_allclose(P.conv_dgrad(g, w, (H, W), stride, pad), _nhwc(xt.grad), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(P.conv_wgrad(x, g, K, stride, pad), wt.grad.numpy().transpose(2, 3, 1, 0),
+                               rtol=0, atol=1e-11)
+
+
+def test_conv_adjoint_identities():
+    x = RNG.standard_normal((2, 6, 7, 5))
+    w = RNG.standard_normal((3, 3, 5, 4))
+    out = P.conv_fwd(x, w)
+    g = RNG.standard_normal(out.shape)
+    lhs = np.sum(out * g)
+    np.testing.assert_allclose(np.sum(x * P.conv_dgrad(g, w, (6, 7))), lhs, rtol=1e-12)
+    np.testing.assert_allclose(np.sum(w * P.conv_wgrad(x, g, 3)), lhs, rtol=1e-12)
+
+
+# --------------------------------------------------------------- pooling ----
+def test_avgpool2():
+    x = RNG.standard_normal((2, 6, 4, 3))
+    out = P.avgpool2_fwd(x)
+    np.testing.assert_allclose(_nchw(out).numpy(), F.avg_pool2d(_nchw(x), 2).numpy(), rtol=0, atol=1e-14)
+    g = RNG.standard_normal(out.shape)
+    np.testing.assert_allclose(np.sum(x * P.avgpool2_bwd(g, (6, 4))), np.sum(out * g), rtol=1e-13)
+
+
+def test_maxpool():
+    x = RNG.standard_normal((2, 9, 8, 3))
+    out = P.maxpool_fwd(x)
+    xt = _nchw(x).requires_grad_()
+    ref = F.max_pool2d(xt, 3, 2, 1)
+    np.testing.assert_array_equal(out, _nhwc(ref))
+    g = RNG.standard_normal(out.shape)
+    (ref * _nchw(g)).sum().backward()
+    np.testing.assert_allclose(P.maxpool_bwd(x, g), _nhwc(xt.grad), rtol=0, atol=1e-14)
+    # ties go to the first maximum in row-major window order
+    t = np.zeros((1, 3, 3, 1))
+    gi = P.maxpool_bwd(t, np.ones((1, 2, 2, 1)))
+    # windows start at (-1,-1), (-1,1), (1,-1), (1,1): first in-image tap of each
+    expect = np.zeros((1, 3, 3, 1))
+    expect[0, 0, 0] = expect[0, 0, 1] = expect[0, 1, 0] = expect[0, 1, 1] = 1.0
+    np.testing.assert_array_equal(gi, expect)
+
+
+# ------------------------------------------------------------ bf16 cast ----
+def test_round_bf16():
+    a = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -(1 + 2.0 ** -8 + 2.0 ** -30), 0.0, 2.0 ** -140,
+                  3.0e38, 3.4e38, 1e-40])
+    r = P.round_bf16(a)
+    assert r[0] == 1.0 and r[1] == 1 + 2.0 ** -6 and r[2] == -(1 + 2.0 ** -7)
+    ref = torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(r[3:], ref[3:])
+    x = RNG.standard_normal(100000) * np.exp(RNG.uniform(-20, 20, 100000))
+    x32 = x.astype(np.float32).astype(np.float64)          # fp32 inputs: no double rounding
+    ref = torch.from_numpy(x32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(P.round_bf16(x32), ref)
+
+
+# ----------------------------------------------- finite-difference checks ----
+def _fd(f, arr, idx, h=1e-6):
+    old = arr[idx]
+    arr[idx] = old + h
+    lp = f()
+    arr[idx] = old - h
+    lm = f()
+    arr[idx] = old
+    return (lp - lm) / (2 * h)
+
+
+def _check_fd(f, arr, grad, n=12, tol=1e-6):
+    flat = arr.reshape(-1)
+    gflat = np.asarray(grad).reshape(-1)
+    picks = RNG.choice(flat.size, size=min(n, flat.size), replace=False)
+    for i in picks:
+        num = _fd(f, flat, i)
+        assert abs(num - gflat[i]) <= tol * max(1.0, abs(num)), (i, num, gflat[i])
+
+
+@pytest.mark.parametrize("K", [1, 3])
+def test_unit_gradients_finite_difference(K):
+    rnd = OC.storage(False)
+    x = RNG.standard_normal((2, 3, 3, 3))
+    gamma, beta = RNG.uniform(0.5, 1.5, 3), RNG.normal(0, 0.1, 3)
+    w = RNG.standard_normal((K, K, 3, 2))
+    g = RNG.standard_normal((2, 3, 3, 2))
+
+    def loss():
+        return np.sum(OC.unit_fwd(x, gamma, beta, w, 1e-5, rnd)["out"] * g)
+
+    c = OC.unit_fwd(x, gamma, beta, w, 1e-5, rnd)
+    b = OC.unit_bwd(c, g, rnd)
+    _check_fd(loss, x, b["dx"], n=18)
+    _check_fd(loss, gamma, b["dgamma"])
+    _check_fd(loss, beta, b["dbeta"])
+    _check_fd(loss, w, b["dw"])
+
+
+def test_bottleneck_gradients_finite_difference():
+    rnd = OC.storage(False)
+    X = RNG.standard_normal((2, 3, 4, 4))
+    p = dict(gamma1=RNG.uniform(0.5, 1.5, 4), beta1=RNG.normal(0, .1, 4), w1=RNG.standard_normal((1, 1, 4, 5)),
+             gamma2=RNG.uniform(0.5, 1.5, 5), beta2=RNG.normal(0, .1, 5), w2=RNG.standard_normal((3, 3, 5, 2)))
+    dY = RNG.standard_normal((2, 3, 4, 6))
+
+    def loss():
+        return np.sum(OC.bottleneck_fwd(X, 2, p, 1e-5, rnd)[0] * dY)
+
+    _, c = OC.bottleneck_fwd(X, 2, p, 1e-5, rnd)
+    dX, g = OC.bottleneck_bwd(c, dY, rnd)
+    _check_fd(loss, X, dX, n=20)
+    _check_fd(loss, p["w1"], g["b1"]["dw"])
+    _check_fd(loss, p["w2"], g["b2"]["dw"])
+    _check_fd(loss, p["gamma1"], g["b1"]["dgamma"])
+    _check_fd(loss, p["beta2"], g["b2"]["dbeta"])
+
+
+def _tiny_block():
+    C0, width, growth, layers = 3, 4, 2, 2
+    cpls, c = [], C0
+    for _ in range(layers):
+        cpls.append(dict(gamma1=RNG.uniform(0.5, 1.5, c), beta1=RNG.normal(0, .1, c),
+                         w1=RNG.standard_normal((1, 1, c, width)), gamma2=RNG.uniform(0.5, 1.5, width),
+                         beta2=RNG.normal(0, .1, width), w2=RNG.standard_normal((3, 3, width, growth))))
+        c += growth
+    trans = dict(gamma=RNG.uniform(0.5, 1.5, c), beta=RNG.normal(0, .1, c), w=RNG.standard_normal((1, 1, c, 3)))
+    return RNG.standard_normal((2, 4, 4, C0)), cpls, trans, c
+
+
+def test_block_gradients_finite_difference():
+    rnd = OC.storage(False)
+    X0, cpls, trans, ct = _tiny_block()
+    dp = RNG.standard_normal((2, 2, 2, 3))
+
+    def loss():
+        return np.sum(OC.block_fwd(X0, cpls, trans, 1e-5, rnd, ct)[0] * dp)
+
+    _, c = OC.block_fwd(X0, cpls, trans, 1e-5, rnd, ct)
+    dX0, g = OC.block_bwd(c, dp, rnd)
+    _check_fd(loss, X0, dX0, n=20)
+    _check_fd(loss, cpls[0]["w1"], g["cpls"][0]["b1"]["dw"])
+    _check_fd(loss, cpls[0]["gamma2"], g["cpls"][0]["b2"]["dgamma"])
+    _check_fd(loss, cpls[1]["w2"], g["cpls"][1]["b2"]["dw"])
+    _check_fd(loss, trans["w"], g["trans"]["dw"])
+    _check_fd(loss, trans["beta"], g["trans"]["dbeta"])
+
+
+def test_resnet_block_gradients_finite_difference():
+    rnd = OC.storage(False)
+    C, Wd = 4, 3
+    p = dict(w1=RNG.standard_normal((1, 1, C, Wd)), w2=RNG.standard_normal((3, 3, Wd, Wd)),
+             w3=RNG.standard_normal((1, 1, Wd, C)))
+    for i, ch in ((1, Wd), (2, Wd), (3, C)):
+        p["gamma%d" % i], p["beta%d" % i] = RNG.uniform(0.5, 1.5, ch), RNG.normal(0, .1, ch)
+    X = RNG.standard_normal((2, 3, 3, C))
+    dr = RNG.standard_normal((2, 3, 3, C))
+
+    def loss():
+        return np.sum(OC.resnet_block_fwd(X, p, 1e-5, rnd)[0] * dr)
+
+    _, c = OC.resnet_block_fwd(X, p, 1e-5, rnd)
+    dX, g = OC.resnet_block_bwd(c, dr, rnd)
+    _check_fd(loss, X, dX, n=20)
+    _check_fd(loss, p["w1"], g["dw1"])
+    _check_fd(loss, p["w2"], g["b2"]["dw"])
+    _check_fd(loss, p["gamma3"], g["dgamma3"])
+    _check_fd(loss, p["beta1"], g["b2"]["dbeta"])
+
+
+# ------------------------------------- compositions vs torch nn (forward) ----
+def test_block_forward_matches_torch():
+    rnd = OC.storage(False)
+    X0, cpls, trans, ct = _tiny_block()
+    pooled, _ = OC.block_fwd(X0, cpls, trans, 1e-5, rnd, ct)
+
+    def bn_relu_conv(t, gamma, beta, w):
+        t = F.batch_norm(t, None, None, torch.from_numpy(gamma), torch.from_numpy(beta), training=True, eps=1e-5)
+        k = w.shape[0]
+        return F.conv2d(F.relu(t), _oihw(w), padding=k // 2)
+
+    feats = _nchw(X0)
+    for p in cpls:
+        h = bn_relu_conv(feats, p["gamma1"], p["beta1"], p["w1"])
+        h = bn_relu_conv(h, p["gamma2"], p["beta2"], p["w2"])
+        feats = torch.cat([feats, h], 1)
+    ref = F.avg_pool2d(bn_relu_conv(feats, trans["gamma"], trans["beta"], trans["w"]), 2)
+    np.testing.assert_allclose(pooled, _nhwc(ref), rtol=0, atol=1e-12)
+
+
+def test_bf16_storage_model_rounds_stored_tensors():
+    rnd = OC.storage(True)
+    x = P.round_bf16(RNG.standard_normal((2, 4, 4, 3)))
+    c = OC.unit_fwd(x, np.ones(3), np.zeros(3), P.round_bf16(RNG.standard_normal((3, 3, 3, 2))), 1e-5, rnd)
+    for key in ("z", "out"):
+        np.testing.assert_array_equal(P.round_bf16(c[key]), c[key])
