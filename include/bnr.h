@@ -1,0 +1,241 @@
+/*
+ * bnr.h -- C ABI of libbnr: restructured batch normalisation (BN
+ * Fission-n-Fusion) for CNN training on AMD Instinct MI355X (gfx950).
+ *
+ * The method ("Restructuring Batch Normalization to Accelerate CNN Training",
+ * arXiv 1807.01702, Sec. 3.2, Fig. 5) splits each BN layer into
+ *   sub-BN1: the per-channel mini-batch statistics, computed in one sweep as
+ *            sum(x) and sum(x^2) (mean/variance fusion, V(X) = E(X^2) - E(X)^2)
+ *            and fused into the epilogue of the CONV that produces x, and
+ *   sub-BN2: (x - mean) * rstd * gamma + beta, fused with the following ReLU
+ *            into the input prologue of the CONV that consumes the result;
+ * and, in the backward pass, fuses the per-channel reductions sum(dy) and
+ * sum(dy * xhat) into the epilogue of the backward CONV that produces dy, and
+ * the input-gradient correction into the prologue of the next backward CONV.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensors are NHWC.  A tensor "view" is a device pointer to its first
+ *   channel at pixel 0 plus a pixel stride `ldc` in elements (a view may be a
+ *   channel slice of a wider buffer, e.g. a DenseNet concatenation buffer).
+ *   m = n*h*w pixels.  Statistics run over all m pixels of a channel.
+ * - Storage type (bnr_dtype) applies to activations, conv weights and
+ *   activation gradients.  BN parameters, statistics, dgamma/dbeta and conv
+ *   weight gradients are always float32.  All arithmetic accumulates in
+ *   float32; cross-tile statistics combine in float64.
+ * - Conv weights are [k][k][c_in][c_out] (dense, dtype); k is 1 or 3, stride
+ *   1, zero padding k/2 (padding is applied to the CONV input, i.e. after BN
+ *   and ReLU: padded taps contribute 0).
+ * - All pointers are device pointers owned by the caller, 16-byte aligned.
+ *   Channel counts, `ldc` values and channel offsets are multiples of 8 for
+ *   BNR_BF16 and of 4 for BNR_F32 (one 16-byte vector).
+ * - `stream` is a hipStream_t (NULL: the null stream).  Every call is
+ *   asynchronous on it; errors of kernels in flight surface at the caller's
+ *   next synchronisation.
+ * - Every call validates all arguments before it launches anything: a status
+ *   other than BNR_OK means nothing was launched and nothing was written.
+ *   bnr_last_error() then describes the problem (thread-local string).
+ * - Workspace: device memory the caller provides for per-tile partial sums and
+ *   staging; query its size with the matching bnr_*_workspace_size call.  The
+ *   library allocates no device memory.  Workspace contents need no
+ *   initialisation and are dead after the call's kernels complete.
+ * - Outputs must not alias inputs unless an entry point says otherwise.
+ *   Calls are stateless and thread-safe.
+ */
+#ifndef BNR_H
+#define BNR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BNR_OK = 0,
+    BNR_ERR_NULL = 1,        /* a required pointer is NULL                          */
+    BNR_ERR_SHAPE = 2,       /* a size is non-positive, inconsistent or too large   */
+    BNR_ERR_DTYPE = 3,       /* unknown storage type                                 */
+    BNR_ERR_ALIGN = 4,       /* pointer not 16-byte aligned, or channel count / ldc  */
+                             /* not a multiple of the 16-byte vector                 */
+    BNR_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than required              */
+    BNR_ERR_UNSUPPORTED = 6, /* well-formed request outside what is implemented      */
+    BNR_ERR_HIP = 7,         /* the HIP runtime rejected a launch                    */
+    BNR_ERR_ALIAS = 8        /* an output overlaps an input it may not overlap       */
+} bnr_status;
+
+typedef enum { BNR_F32 = 0, BNR_BF16 = 1 } bnr_dtype;
+
+/* One stride-1, zero-padded CONV on NHWC views. */
+typedef struct {
+    int32_t n, h, w;       /* batch size and image height/width; m = n*h*w        */
+    int32_t c_in, c_out;   /* input / output channels                            */
+    int32_t k;             /* filter size: 1 or 3 (pad k/2)                      */
+    int32_t in_ldc;        /* pixel stride (elements) of the input view           */
+    int32_t out_ldc;       /* pixel stride (elements) of the output view          */
+    bnr_dtype dtype;       /* storage type of activations, weights, gradients    */
+} bnr_conv_desc;
+
+/* Per-channel BN state of one BN layer (float32 arrays of the BN's C channels).
+ * Training-mode BN (Sec. 2.2; Sec. 3.2 for the one-sweep statistics):
+ *   mean = sum(x)/m, var = sum(x^2)/m - mean^2 (biased), rstd = 1/sqrt(var+eps),
+ *   y = gamma * (x - mean) * rstd + beta.
+ * Statistics producers write mean/var/rstd; consumers read mean/rstd. */
+typedef struct {
+    const float *gamma;    /* [C] scale                                            */
+    const float *beta;     /* [C] shift                                            */
+    float *mean;           /* [C] mini-batch mean                                  */
+    float *var;            /* [C] biased mini-batch variance (may be NULL)         */
+    float *rstd;           /* [C] 1/sqrt(var + eps)                                */
+    float eps;             /* > 0                                                  */
+} bnr_bn;
+
+/* Where the gradient of a CONV's output comes from (backward entry points). */
+typedef enum {
+    BNR_GRAD_DENSE = 0,    /* g: materialised [m][c_out] view (pixel stride g_ldc)  */
+    BNR_GRAD_BN = 1,       /* the CONV output is the input x of a BN whose output  */
+                           /* gradient dy (after its ReLU mask) and reductions     */
+                           /* dgamma = sum(dy*xhat), dbeta = sum(dy) are known:    */
+                           /* g = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m),       */
+                           /* xhat = (x - mean)*rstd, computed on the fly (Sec.3.2 */
+                           /* backward fusion); never materialised                 */
+    BNR_GRAD_AVGPOOL2 = 2  /* the CONV output feeds a 2x2/2 average pooling and g  */
+                           /* is the pooled gradient [n][h/2][w/2][c_out]; the     */
+                           /* CONV-output gradient g[p/2]/4 is formed on the fly   */
+} bnr_grad_kind;
+
+typedef struct {
+    bnr_grad_kind kind;
+    const void *g;         /* DENSE, AVGPOOL2: gradient view                        */
+    int32_t g_ldc;         /* DENSE, AVGPOOL2: its pixel stride                     */
+    const void *dy;        /* BN: [m][c_out] dense gradient of the BN output        */
+    const void *x;         /* BN: the BN input (= this CONV's output) view           */
+    int32_t x_ldc;         /* BN: its pixel stride                                   */
+    const bnr_bn *bn;      /* BN: gamma, mean, rstd of that BN                       */
+    const float *dgamma;   /* BN: [c_out]                                            */
+    const float *dbeta;    /* BN: [c_out]                                            */
+} bnr_grad_src;
+
+/* ------------------------------------------------------------ sizes ---- */
+size_t bnr_stats_workspace_size(int64_t m, int32_t c);
+/* Workspace bytes enough for every conv entry point on this descriptor. */
+size_t bnr_workspace_size(const bnr_conv_desc *d);
+
+/* ------------------------------------------------------ forward path ---- */
+
+/* Standalone sub-BN1 (Sec. 3.2, mean/variance fusion) for a BN whose producer
+ * is not a CONV (a block input, a concatenation): one read sweep of x[m][c]
+ * (pixel stride ldc) accumulating sum(x), sum(x^2) per channel (float32 per
+ * tile, float64 across tiles), then mean/var/rstd into bn (gamma/beta unused). */
+bnr_status bnr_bn_stats(int64_t m, int32_t c, int32_t ldc, bnr_dtype dtype, const void *x,
+                        bnr_bn *bn, void *ws, size_t ws_bytes, void *stream);
+
+/* Fused CONV + sub-BN1 (Sec. 3.2, CONV1-(sub-BN1) fusion): y = conv(x, w) and,
+ * in the same kernel, per-output-channel sum(y), sum(y^2) of the values as
+ * stored in y; then mean/var/rstd of y into y_bn.  x is used as is (no BN
+ * before this CONV). */
+bnr_status bnr_conv_bn_stats_fwd(const bnr_conv_desc *d, const void *x, const void *w, void *y,
+                                 bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream);
+
+/* Fused (sub-BN2)-ReLU-CONV (Sec. 3.2): y = conv(relu(gamma*(x-mean)*rstd+beta), w)
+ * with the normalisation and ReLU applied while the CONV reads x (x_bn gives
+ * gamma, beta, mean, rstd of x's c_in channels).  If y_bn is not NULL the
+ * epilogue also produces the statistics of y (CONV-(sub-BN1) fusion of the
+ * next BN) exactly as bnr_conv_bn_stats_fwd does. */
+bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn,
+                                const void *w, void *y, bnr_bn *y_bn,
+                                void *ws, size_t ws_bytes, void *stream);
+
+/* 2x2 average pooling, stride 2, of x[n][h][w][c] (pixel stride ldc) into
+ * y[n][h/2][w/2][c] (dense); h and w even.  (DenseNet transition layer.) */
+bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype,
+                            const void *x, int32_t ldc, void *y, void *stream);
+
+/* ----------------------------------------------------- backward path ---- */
+
+/* Backward of one BN-ReLU-CONV chain (or of a plain CONV when x_bn is NULL),
+ * with the paper's backward fission/fusion (Sec. 3.2, Fig. 5b):
+ *   1. dgrad: dz = conv_transpose(g, w), g from *g_src (prologue);
+ *      epilogue (x_bn != NULL): recompute y = gamma*xhat+beta from x, apply the
+ *      ReLU mask dy = dz*[y>0], store dy[m][c_in] (dense), and accumulate
+ *      per-channel sum(dy), sum(dy*xhat) over the tile;
+ *   2. combine the tiles: dbeta = sum(dy), dgamma = sum(dy*xhat)   (x_bn != NULL);
+ *   3. wgrad: dw = sum over pixels of relu(bn(x)) (x itself if x_bn is NULL),
+ *      recomputed from x in the prologue, times g;
+ *   4. optional standalone input gradient: if dx != NULL, the BN input gradient
+ *      gamma*rstd*(dy - dbeta/m - xhat*dgamma/m) (x_bn != NULL) or dz itself
+ *      (x_bn == NULL) is written to (dx_accumulate = 0) or added to
+ *      (dx_accumulate = 1) the view dx (pixel stride dx_ldc).  dx may alias x
+ *      only if x_bn is NULL and never otherwise; with dx_accumulate = 1 the old
+ *      contents of dx are read.  When dx is NULL the BN input gradient stays
+ *      deferred: a later call consumes it as BNR_GRAD_BN from (dy, x, dgamma,
+ *      dbeta).
+ * Outputs: dw [k][k][c_in][c_out] float32 (overwritten); dgamma, dbeta [c_in]
+ * float32 and dy (required when x_bn != NULL). */
+bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                         const bnr_grad_src *g_src, float *dw, float *dgamma, float *dbeta, void *dy,
+                         void *dx, int32_t dx_ldc, int32_t dx_accumulate,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* Standalone BN input gradient for a BN whose producer is not a CONV (block
+ * input, concatenation): dx = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m) from
+ * dy[m][c] (dense), x (pixel stride x_ldc), written or added into dx (pixel
+ * stride dx_ldc).  dx may alias dy's storage only if dx_accumulate = 0 and the
+ * views coincide exactly. */
+bnr_status bnr_bn_dx(int64_t m, int32_t c, bnr_dtype dtype, const void *dy, const void *x, int32_t x_ldc,
+                     const bnr_bn *bn, const float *dgamma, const float *dbeta,
+                     void *dx, int32_t dx_ldc, int32_t dx_accumulate, void *stream);
+
+/* ------------------------------------------------- unfused A/B path ---- */
+
+typedef enum {
+    BNR_MODE_BASELINE = 0, /* the paper's unfused layer chain (Sec. 3.2, upper half  */
+                           /* of Fig. 5): mean sweep, variance sweep, normalise      */
+                           /* (write y), ReLU (read y, write z), CONV (read z);      */
+                           /* backward: CONV dgrad (write dz) and wgrad (read z),    */
+                           /* ReLU backward (write dy), BN reductions sweep, BN      */
+                           /* input-gradient sweep (write dx)                        */
+    BNR_MODE_RCF = 1,      /* ReLU-CONV fusion only (Sec. 3.2): ReLU applied while   */
+                           /* the CONV reads y; mask applied in the dgrad epilogue    */
+    BNR_MODE_RCF_MVF = 2   /* RCF plus one-sweep mean/variance statistics            */
+} bnr_ref_mode;
+
+typedef struct {
+    const void *x;         /* BN input view, pixel stride desc.in_ldc               */
+    bnr_bn *bn;            /* gamma, beta in; mean, var, rstd written by forward    */
+    const void *w;         /* CONV weights                                          */
+    void *y;               /* [m][c_in] dense: BN output (materialised)             */
+    void *z;               /* [m][c_in] dense: ReLU output (BASELINE only)          */
+    void *out;             /* CONV output view, pixel stride desc.out_ldc           */
+    const void *g;         /* backward: gradient of out, [m][c_out], stride g_ldc   */
+    int32_t g_ldc;
+    void *dz;              /* backward: [m][c_in] CONV input gradient (BASELINE)    */
+    void *dy;              /* backward: [m][c_in] BN output gradient                */
+    float *dw, *dgamma, *dbeta;
+    void *dx;              /* backward: BN input gradient view, stride dx_ldc       */
+    int32_t dx_ldc;
+    int32_t dx_accumulate;
+} bnr_ref_args;
+
+/* The same training math as the fused entry points through separate,
+ * unfused kernels (same GEMM core with fusion switched off), for A/B
+ * comparison of time and HBM traffic.  backward = 0: forward of one
+ * BN-ReLU-CONV chain; backward = 1: its backward. */
+bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_conv_desc *d,
+                              const bnr_ref_args *a, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------ diagnostics ---- */
+
+/* Plain device-to-device copy of `bytes` (multiple of 16) with the same
+ * streaming kernel style as the BN sweeps: the HBM-traffic calibration
+ * reference for profiler byte counters. */
+bnr_status bnr_hbm_copy(const void *src, void *dst, size_t bytes, void *stream);
+
+const char *bnr_status_string(bnr_status s);
+const char *bnr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BNR_H */

@@ -1,0 +1,282 @@
+"""Thin ctypes binding of ``libbnr.so`` (C ABI in ``include/bnr.h``).
+
+Argument marshalling only: tensors are torch device tensors (PyTorch supplies
+device memory and the current stream); every step of the computation runs in
+the library's HIP kernels.  There is no fallback: if ``libbnr.so`` is missing
+or fails to load, importing this module raises.
+
+Tensor views.  A view argument is a torch tensor whose last dimension holds
+the channels with unit stride and whose leading dimensions collapse to one
+pixel stride (e.g. ``buf[..., c0:c0 + c]`` of a contiguous NHWC buffer): the
+binding passes its data pointer and that pixel stride (``ldc``).
+"""
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libbnr.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libbnr.so is not built (run __graft_entry__.build())")
+_lib = ctypes.CDLL(LIB_PATH)
+
+BNR_F32, BNR_BF16 = 0, 1
+GRAD_DENSE, GRAD_BN, GRAD_AVGPOOL2 = 0, 1, 2
+MODE_BASELINE, MODE_RCF, MODE_RCF_MVF = 0, 1, 2
+STATUS = ["BNR_OK", "BNR_ERR_NULL", "BNR_ERR_SHAPE", "BNR_ERR_DTYPE", "BNR_ERR_ALIGN", "BNR_ERR_WORKSPACE",
+          "BNR_ERR_UNSUPPORTED", "BNR_ERR_HIP", "BNR_ERR_ALIAS"]
+
+c_i32, c_i64, c_vp, c_sz, c_f = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("n", c_i32), ("h", c_i32), ("w", c_i32), ("c_in", c_i32), ("c_out", c_i32), ("k", c_i32),
+                ("in_ldc", c_i32), ("out_ldc", c_i32), ("dtype", ctypes.c_int)]
+
+
+class BNStruct(ctypes.Structure):
+    _fields_ = [("gamma", c_vp), ("beta", c_vp), ("mean", c_vp), ("var", c_vp), ("rstd", c_vp), ("eps", c_f)]
+
+
+class GradSrc(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("g", c_vp), ("g_ldc", c_i32), ("dy", c_vp), ("x", c_vp), ("x_ldc", c_i32),
+                ("bn", ctypes.POINTER(BNStruct)), ("dgamma", c_vp), ("dbeta", c_vp)]
+
+
+class RefArgs(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("bn", ctypes.POINTER(BNStruct)), ("w", c_vp), ("y", c_vp), ("z", c_vp), ("out", c_vp),
+                ("g", c_vp), ("g_ldc", c_i32), ("dz", c_vp), ("dy", c_vp), ("dw", c_vp), ("dgamma", c_vp),
+                ("dbeta", c_vp), ("dx", c_vp), ("dx_ldc", c_i32), ("dx_accumulate", c_i32)]
+
+
+def _sig(name, res, *args):
+    f = getattr(_lib, name)
+    f.restype = res
+    f.argtypes = list(args)
+    return f
+
+
+_P = ctypes.POINTER
+_lib_fns = dict(
+    bnr_status_string=_sig("bnr_status_string", ctypes.c_char_p, ctypes.c_int),
+    bnr_last_error=_sig("bnr_last_error", ctypes.c_char_p),
+    bnr_stats_workspace_size=_sig("bnr_stats_workspace_size", c_sz, c_i64, c_i32),
+    bnr_workspace_size=_sig("bnr_workspace_size", c_sz, _P(ConvDesc)),
+    bnr_bn_stats=_sig("bnr_bn_stats", ctypes.c_int, c_i64, c_i32, c_i32, ctypes.c_int, c_vp, _P(BNStruct), c_vp, c_sz,
+                      c_vp),
+    bnr_conv_bn_stats_fwd=_sig("bnr_conv_bn_stats_fwd", ctypes.c_int, _P(ConvDesc), c_vp, c_vp, c_vp, _P(BNStruct),
+                               c_vp, c_sz, c_vp),
+    bnr_bn_relu_conv_fwd=_sig("bnr_bn_relu_conv_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, c_vp,
+                              _P(BNStruct), c_vp, c_sz, c_vp),
+    bnr_avgpool2_fwd=_sig("bnr_avgpool2_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
+                          c_vp, c_vp),
+    bnr_bwd_fused=_sig("bnr_bwd_fused", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, _P(GradSrc), c_vp,
+                       c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_sz, c_vp),
+    bnr_bn_dx=_sig("bnr_bn_dx", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_vp, c_i32, _P(BNStruct), c_vp, c_vp,
+                   c_vp, c_i32, c_i32, c_vp),
+    bnr_reference_path=_sig("bnr_reference_path", ctypes.c_int, ctypes.c_int, c_i32, _P(ConvDesc), _P(RefArgs), c_vp,
+                            c_sz, c_vp),
+    bnr_hbm_copy=_sig("bnr_hbm_copy", ctypes.c_int, c_vp, c_vp, c_sz, c_vp),
+)
+
+
+class BnrError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("%s: %s" % (STATUS[status] if 0 <= status < len(STATUS) else status, msg))
+        self.status = status
+
+
+def _check(status):
+    if status != 0:
+        raise BnrError(status, _lib_fns["bnr_last_error"]().decode())
+
+
+def status_string(s):
+    return _lib_fns["bnr_status_string"](s).decode()
+
+
+# --------------------------------------------------------------- helpers ----
+def dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return BNR_BF16
+    if t.dtype == torch.float32:
+        return BNR_F32
+    raise TypeError("unsupported dtype %s" % t.dtype)
+
+
+def view(t):
+    """(data pointer, pixels, channels, pixel stride) of a channel view."""
+    if t.dim() < 2 or t.stride(-1) != 1:
+        raise ValueError("view needs a unit-stride channel dimension")
+    ldc = t.stride(-2)
+    for i in range(t.dim() - 2):
+        if t.shape[i] > 1 and t.stride(i) != t.stride(i + 1) * t.shape[i + 1]:
+            raise ValueError("leading dimensions of a view must collapse to one pixel stride")
+    m = 1
+    for s in t.shape[:-1]:
+        m *= s
+    return t.data_ptr(), m, t.shape[-1], ldc
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+_ws_cache = {}
+
+
+def workspace(nbytes, device=None):
+    """Grow-only per-device workspace (device memory from torch)."""
+    dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+    cur = _ws_cache.get(dev)
+    if cur is None or cur.numel() < nbytes:
+        cur = torch.empty(max(int(nbytes), 256) + 256, dtype=torch.uint8, device=dev)
+        _ws_cache[dev] = cur
+    base = cur.data_ptr()
+    aligned = (base + 255) // 256 * 256
+    return aligned, cur.numel() - (aligned - base)
+
+
+class BN:
+    """Per-channel BN state: gamma, beta (inputs), mean, var, rstd (batch statistics), eps."""
+
+    def __init__(self, gamma, beta, eps=1e-5, mean=None, var=None, rstd=None):
+        dev, c = gamma.device, gamma.shape[0]
+        self.gamma, self.beta, self.eps = gamma, beta, float(eps)
+        self.mean = mean if mean is not None else torch.empty(c, dtype=torch.float32, device=dev)
+        self.var = var if var is not None else torch.empty(c, dtype=torch.float32, device=dev)
+        self.rstd = rstd if rstd is not None else torch.empty(c, dtype=torch.float32, device=dev)
+
+    @classmethod
+    def stats_only(cls, c, device, eps=1e-5):
+        """Statistics holder for a BN whose gamma/beta are not needed (producer side)."""
+        b = cls.__new__(cls)
+        b.gamma = b.beta = None
+        b.eps = float(eps)
+        b.mean = torch.empty(c, dtype=torch.float32, device=device)
+        b.var = torch.empty(c, dtype=torch.float32, device=device)
+        b.rstd = torch.empty(c, dtype=torch.float32, device=device)
+        return b
+
+    def struct(self):
+        return BNStruct(_ptr(self.gamma), _ptr(self.beta), _ptr(self.mean), _ptr(self.var), _ptr(self.rstd),
+                        self.eps)
+
+
+def conv_desc(n, h, w, c_in, c_out, k, in_ldc, out_ldc, dtype):
+    return ConvDesc(n, h, w, c_in, c_out, k, in_ldc, out_ldc, dtype)
+
+
+def desc_for(x, y, k, n, h, w):
+    """Descriptor of a CONV from view x ([.., c_in]) to view y ([.., c_out])."""
+    _, mx, ci, ldx = view(x)
+    _, my, co, ldy = view(y)
+    assert mx == my == n * h * w, (mx, my, n, h, w)
+    return ConvDesc(n, h, w, ci, co, k, ldx, ldy, dtype_code(x))
+
+
+# ----------------------------------------------------------- entry points --
+def bnr_workspace_size(desc):
+    return _lib_fns["bnr_workspace_size"](ctypes.byref(desc))
+
+
+def bnr_stats_workspace_size(m, c):
+    return _lib_fns["bnr_stats_workspace_size"](m, c)
+
+
+def bnr_bn_stats(x, bn):
+    """Standalone sub-BN1: batch statistics of the view x into bn."""
+    p, m, c, ldc = view(x)
+    ws, wsb = workspace(bnr_stats_workspace_size(m, c), x.device)
+    s = bn.struct()
+    _check(_lib_fns["bnr_bn_stats"](m, c, ldc, dtype_code(x), p, ctypes.byref(s), ws, wsb, _stream()))
+
+
+def bnr_conv_bn_stats_fwd(desc, x, w, y, y_bn):
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    ys = y_bn.struct()
+    _check(_lib_fns["bnr_conv_bn_stats_fwd"](ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(y), ctypes.byref(ys), ws, wsb,
+                                             _stream()))
+
+
+def bnr_bn_relu_conv_fwd(desc, x, x_bn, w, y, y_bn=None):
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    xs = x_bn.struct()
+    ys = y_bn.struct() if y_bn is not None else None
+    _check(_lib_fns["bnr_bn_relu_conv_fwd"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), _ptr(y),
+                                            ctypes.byref(ys) if ys is not None else None, ws, wsb, _stream()))
+
+
+def bnr_avgpool2_fwd(x, y, n, h, w):
+    p, m, c, ldc = view(x)
+    _check(_lib_fns["bnr_avgpool2_fwd"](n, h, w, c, dtype_code(x), p, ldc, _ptr(y), _stream()))
+
+
+def grad_dense(g):
+    p, _, _, ldc = view(g)
+    return dict(kind=GRAD_DENSE, g=p, g_ldc=ldc, keep=(g,))
+
+
+def grad_avgpool2(gp):
+    p, _, _, ldc = view(gp)
+    return dict(kind=GRAD_AVGPOOL2, g=p, g_ldc=ldc, keep=(gp,))
+
+
+def grad_bn(dy, x, bn, dgamma, dbeta):
+    """Deferred gradient of a CONV output x that feeds BN `bn` (dy dense)."""
+    px, _, _, ldx = view(x)
+    return dict(kind=GRAD_BN, dy=_ptr(dy), x=px, x_ldc=ldx, bn=bn, dgamma=_ptr(dgamma), dbeta=_ptr(dbeta),
+                keep=(dy, x, dgamma, dbeta))
+
+
+def _grad_struct(g):
+    bns = g["bn"].struct() if g.get("bn") is not None else None
+    gs = GradSrc(g["kind"], g.get("g"), g.get("g_ldc", 0), g.get("dy"), g.get("x"), g.get("x_ldc", 0),
+                 ctypes.pointer(bns) if bns is not None else None, g.get("dgamma"), g.get("dbeta"))
+    return gs, bns
+
+
+def bnr_bwd_fused(desc, x, x_bn, w, g_src, dw, dgamma=None, dbeta=None, dy=None, dx=None, dx_accumulate=False):
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    gs, keep = _grad_struct(g_src)
+    xs = x_bn.struct() if x_bn is not None else None
+    dxp, dx_ldc = (None, 0)
+    if dx is not None:
+        dxp, _, _, dx_ldc = view(dx)
+    _check(_lib_fns["bnr_bwd_fused"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs) if xs is not None else None,
+                                     _ptr(w), ctypes.byref(gs), _ptr(dw), _ptr(dgamma), _ptr(dbeta), _ptr(dy), dxp,
+                                     dx_ldc, 1 if dx_accumulate else 0, ws, wsb, _stream()))
+    del keep
+
+
+def bnr_bn_dx(dy, x, bn, dgamma, dbeta, dx, dx_accumulate=False):
+    px, m, c, ldx = view(x)
+    pd, _, _, ldd = view(dx)
+    bs = bn.struct()
+    _check(_lib_fns["bnr_bn_dx"](m, c, dtype_code(x), _ptr(dy), px, ldx, ctypes.byref(bs), _ptr(dgamma), _ptr(dbeta),
+                                 pd, ldd, 1 if dx_accumulate else 0, _stream()))
+
+
+def bnr_reference_path(mode, backward, desc, x, bn, w, y, z=None, out=None, g=None, dz=None, dy=None, dw=None,
+                       dgamma=None, dbeta=None, dx=None, dx_accumulate=False):
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    bs = bn.struct()
+    g_ldc = view(g)[3] if g is not None else 0
+    dxp, dx_ldc = (None, 0)
+    if dx is not None:
+        dxp, _, _, dx_ldc = view(dx)
+    a = RefArgs(_ptr(x), ctypes.pointer(bs), _ptr(w), _ptr(y), _ptr(z), _ptr(out), _ptr(g), g_ldc, _ptr(dz), _ptr(dy),
+                _ptr(dw), _ptr(dgamma), _ptr(dbeta), dxp, dx_ldc, 1 if dx_accumulate else 0)
+    _check(_lib_fns["bnr_reference_path"](mode, 1 if backward else 0, ctypes.byref(desc), ctypes.byref(a), ws, wsb,
+                                          _stream()))
+
+
+def bnr_hbm_copy(src, dst):
+    nbytes = src.numel() * src.element_size()
+    _check(_lib_fns["bnr_hbm_copy"](_ptr(src), _ptr(dst), nbytes, _stream()))

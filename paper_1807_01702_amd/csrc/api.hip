@@ -1,0 +1,576 @@
+// api.hip -- the C ABI of libbnr (declared in include/bnr.h): argument
+// validation, workspace carving and the launch sequences of the fused
+// BN fission/fusion path and of the unfused reference path.
+//
+// Every entry point validates all of its arguments before the first launch:
+// on any error it returns without launching anything.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/bnr.h"
+#include "kernels.hpp"
+#include "tiles.hpp"
+
+using namespace bnr;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+bnr_status fail(bnr_status s, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+bnr_status ok()
+{
+    g_err[0] = 0;
+    return BNR_OK;
+}
+
+bnr_status hip_status(hipError_t e, const char *what)
+{
+    if (e == hipSuccess) return BNR_OK;
+    return fail(BNR_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define TRY(expr)                                        \
+    do {                                                 \
+        bnr_status _s = (expr);                          \
+        if (_s != BNR_OK) return _s;                     \
+    } while (0)
+#define TRY_HIP(expr, what) TRY(hip_status((expr), what))
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+inline int esize(bnr_dtype d) { return d == BNR_BF16 ? 2 : 4; }
+inline int vec_of(bnr_dtype d) { return d == BNR_BF16 ? 8 : 4; }
+
+bnr_status check_dtype(bnr_dtype d)
+{
+    if (d != BNR_F32 && d != BNR_BF16) return fail(BNR_ERR_DTYPE, "unknown dtype %d", (int)d);
+    return BNR_OK;
+}
+
+bnr_status check_ptr(const void *p, const char *name, bool required = true)
+{
+    if (!p) return required ? fail(BNR_ERR_NULL, "%s is NULL", name) : BNR_OK;
+    if (reinterpret_cast<uintptr_t>(p) % 16) return fail(BNR_ERR_ALIGN, "%s is not 16-byte aligned", name);
+    return BNR_OK;
+}
+
+bnr_status check_fptr(const float *p, const char *name)
+{
+    if (!p) return fail(BNR_ERR_NULL, "%s is NULL", name);
+    if (reinterpret_cast<uintptr_t>(p) % 4) return fail(BNR_ERR_ALIGN, "%s is not 4-byte aligned", name);
+    return BNR_OK;
+}
+
+bnr_status check_channels(int c, int ldc, bnr_dtype d, const char *what)
+{
+    if (c <= 0 || ldc <= 0) return fail(BNR_ERR_SHAPE, "%s: channels %d / ldc %d must be positive", what, c, ldc);
+    if (ldc < c) return fail(BNR_ERR_SHAPE, "%s: ldc %d < channels %d", what, ldc, c);
+    if (c % vec_of(d) || ldc % vec_of(d))
+        return fail(BNR_ERR_ALIGN, "%s: channels %d and ldc %d must be multiples of %d", what, c, ldc, vec_of(d));
+    return BNR_OK;
+}
+
+// byte range [lo, hi) of a pixel-strided view
+struct Range { uintptr_t lo, hi; };
+Range view_range(const void *p, int64_t m, int64_t c, int64_t ldc, int es)
+{
+    uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Range{lo, lo + (uintptr_t)(((m - 1) * ldc + c) * es)};
+}
+bool overlap(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+bnr_status check_bn(const bnr_bn *bn, const char *name, bool need_affine, bool need_stats_out)
+{
+    if (!bn) return fail(BNR_ERR_NULL, "%s is NULL", name);
+    if (need_affine) {
+        TRY(check_fptr(bn->gamma, "bn.gamma"));
+        TRY(check_fptr(bn->beta, "bn.beta"));
+    }
+    TRY(check_fptr(bn->mean, "bn.mean"));
+    TRY(check_fptr(bn->rstd, "bn.rstd"));
+    if (bn->var && reinterpret_cast<uintptr_t>(bn->var) % 4) return fail(BNR_ERR_ALIGN, "bn.var misaligned");
+    if (need_stats_out && !(bn->eps > 0.0f)) return fail(BNR_ERR_SHAPE, "%s.eps must be > 0", name);
+    return BNR_OK;
+}
+
+bnr_status check_desc(const bnr_conv_desc *d)
+{
+    if (!d) return fail(BNR_ERR_NULL, "desc is NULL");
+    TRY(check_dtype(d->dtype));
+    if (d->n <= 0 || d->h <= 0 || d->w <= 0) return fail(BNR_ERR_SHAPE, "n, h, w must be positive");
+    if (d->k != 1 && d->k != 3) return fail(BNR_ERR_UNSUPPORTED, "filter size %d (only 1 and 3)", d->k);
+    if (d->k == 3 && d->w > kRowsMaxW3)
+        return fail(BNR_ERR_UNSUPPORTED, "3x3 CONV with image width %d > %d", d->w, kRowsMaxW3);
+    const int64_t m = (int64_t)d->n * d->h * d->w;
+    if (m > (int64_t)1 << 31) return fail(BNR_ERR_SHAPE, "too many pixels (%lld)", (long long)m);
+    TRY(check_channels(d->c_in, d->in_ldc, d->dtype, "conv input"));
+    TRY(check_channels(d->c_out, d->out_ldc, d->dtype, "conv output"));
+    if (d->c_in > 2048 || d->c_out > 2048) return fail(BNR_ERR_UNSUPPORTED, "more than 2048 channels");
+    return BNR_OK;
+}
+
+int64_t pixels(const bnr_conv_desc *d) { return (int64_t)d->n * d->h * d->w; }
+
+// workspace regions for the conv entry points
+struct ConvWs { size_t pack, part, wg, total; };
+ConvWs conv_ws(const bnr_conv_desc *d)
+{
+    const int taps = d->k * d->k, dt = d->dtype == BNR_BF16 ? DT_BF16 : DT_F32;
+    const int64_t m = pixels(d);
+    ConvWs w;
+    size_t pf = rows_pack_bytes(dt, taps, d->c_in, d->c_out), pb = rows_pack_bytes(dt, taps, d->c_out, d->c_in);
+    w.pack = align_up(pf > pb ? pf : pb);
+    size_t sf = (size_t)rows_mtiles(dt, taps, m, d->c_out) * 2 * d->c_out * 4;
+    size_t sb = (size_t)rows_mtiles(dt, taps, m, d->c_in) * 2 * d->c_in * 4;
+    size_t ss = (size_t)stats_row_blocks(m, d->c_in, dt) * 2 * d->c_in * 4;
+    size_t part = sf > sb ? sf : sb;
+    w.part = align_up(part > ss ? part : ss);
+    w.wg = align_up(wgrad_ws_bytes(dt, m, d->c_in, d->c_out, d->k));
+    w.total = w.pack + w.part + w.wg;
+    return w;
+}
+
+size_t stats_ws(int64_t m, int c)
+{
+    size_t a = (size_t)stats_row_blocks(m, c, DT_BF16) * 2 * c * 4;
+    size_t b = (size_t)stats_row_blocks(m, c, DT_F32) * 2 * c * 4;
+    return align_up(a > b ? a : b);
+}
+
+bnr_status check_ws(void *ws, size_t have, size_t need)
+{
+    if (need == 0) return BNR_OK;
+    if (!ws) return fail(BNR_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return fail(BNR_ERR_ALIGN, "workspace not 256-byte aligned");
+    if (have < need) return fail(BNR_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", have, need);
+    return BNR_OK;
+}
+
+int dt_of(bnr_dtype d) { return d == BNR_BF16 ? DT_BF16 : DT_F32; }
+
+// statistics of a [m][c] view: partial sweep + float64 combine (MVF)
+bnr_status run_stats(int64_t m, int c, int ldc, bnr_dtype dt, const void *x, bnr_bn *bn, float *part,
+                     hipStream_t s)
+{
+    const int64_t R = stats_row_blocks(m, c, dt_of(dt));
+    TRY_HIP(launch_stats_partial(dt_of(dt), x, ldc, m, c, ST_SUMSQ, nullptr, nullptr, nullptr, 0, part, R, s),
+            "stats sweep");
+    TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MVF, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr, s),
+            "stats combine");
+    return BNR_OK;
+}
+
+bnr_status validate_grad_src(const bnr_conv_desc *d, const bnr_grad_src *g)
+{
+    if (!g) return fail(BNR_ERR_NULL, "g_src is NULL");
+    const int es = esize(d->dtype);
+    const int64_t m = pixels(d);
+    if (g->kind == BNR_GRAD_DENSE) {
+        TRY(check_ptr(g->g, "g_src.g"));
+        TRY(check_channels(d->c_out, g->g_ldc, d->dtype, "g_src.g"));
+        (void)view_range(g->g, m, d->c_out, g->g_ldc, es);
+    } else if (g->kind == BNR_GRAD_BN) {
+        TRY(check_ptr(g->dy, "g_src.dy"));
+        TRY(check_ptr(g->x, "g_src.x"));
+        TRY(check_channels(d->c_out, g->x_ldc, d->dtype, "g_src.x"));
+        TRY(check_bn(g->bn, "g_src.bn", true, false));
+        TRY(check_fptr(g->dgamma, "g_src.dgamma"));
+        TRY(check_fptr(g->dbeta, "g_src.dbeta"));
+    } else if (g->kind == BNR_GRAD_AVGPOOL2) {
+        TRY(check_ptr(g->g, "g_src.g"));
+        TRY(check_channels(d->c_out, g->g_ldc, d->dtype, "g_src.g (pooled)"));
+        if (d->h % 2 || d->w % 2) return fail(BNR_ERR_SHAPE, "average-pooling gradient needs even h, w");
+    } else {
+        return fail(BNR_ERR_UNSUPPORTED, "unknown gradient kind %d", (int)g->kind);
+    }
+    return BNR_OK;
+}
+
+void fill_rows(RowsParams &rp, const bnr_conv_desc *d, int K, int N)
+{
+    memset(&rp, 0, sizeof rp);
+    rp.dtype = dt_of(d->dtype);
+    rp.taps = d->k * d->k;
+    rp.n = d->n; rp.h = d->h; rp.w = d->w;
+    rp.m = pixels(d);
+    rp.K = K; rp.N = N;
+}
+
+// forward CONV with optional BN+ReLU prologue and optional statistics epilogue
+bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w, void *y,
+                    bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_desc(d));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(w, "w"));
+    TRY(check_ptr(y, "y"));
+    if (x_bn) TRY(check_bn(x_bn, "x_bn", true, false));
+    if (y_bn) TRY(check_bn(y_bn, "y_bn", false, true));
+    const ConvWs cw = conv_ws(d);
+    TRY(check_ws(ws, ws_bytes, cw.total));
+    const int es = esize(d->dtype);
+    const int64_t m = pixels(d);
+    Range ry = view_range(y, m, d->c_out, d->out_ldc, es);
+    if (overlap(ry, view_range(x, m, d->c_in, d->in_ldc, es))) return fail(BNR_ERR_ALIAS, "y overlaps x");
+    const int64_t wbytes = (int64_t)d->k * d->k * d->c_in * d->c_out * es;
+    Range rw{reinterpret_cast<uintptr_t>(w), reinterpret_cast<uintptr_t>(w) + (uintptr_t)wbytes};
+    if (overlap(ry, rw)) return fail(BNR_ERR_ALIAS, "y overlaps w");
+
+    hipStream_t s = (hipStream_t)stream;
+    char *base = (char *)ws;
+    void *wpack = base;
+    float *part = (float *)(base + cw.pack);
+    TRY_HIP(launch_pack_weights(dt_of(d->dtype), w, d->k, d->c_in, d->c_out, 0, wpack, s), "weight packing");
+    RowsParams rp;
+    fill_rows(rp, d, d->c_in, d->c_out);
+    rp.pro = x_bn ? PRO_BNRELU : PRO_NONE;
+    rp.a = x; rp.a_ldc = d->in_ldc;
+    if (x_bn) { rp.p_gamma = x_bn->gamma; rp.p_beta = x_bn->beta; rp.p_mean = x_bn->mean; rp.p_rstd = x_bn->rstd; }
+    rp.wpack = wpack;
+    rp.epi = y_bn ? EPI_STATS : EPI_STORE;
+    rp.y = y; rp.y_ldc = d->out_ldc;
+    rp.part = part;
+    TRY_HIP(launch_conv_rows(rp, s), "conv forward");
+    if (y_bn) {
+        const int64_t R = rows_mtiles(rp.dtype, rp.taps, m, d->c_out);
+        TRY_HIP(launch_stats_finalize(part, R, d->c_out, m, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
+                                      nullptr, nullptr, s),
+                "stats combine");
+    }
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *bnr_status_string(bnr_status s)
+{
+    switch (s) {
+    case BNR_OK: return "BNR_OK";
+    case BNR_ERR_NULL: return "BNR_ERR_NULL";
+    case BNR_ERR_SHAPE: return "BNR_ERR_SHAPE";
+    case BNR_ERR_DTYPE: return "BNR_ERR_DTYPE";
+    case BNR_ERR_ALIGN: return "BNR_ERR_ALIGN";
+    case BNR_ERR_WORKSPACE: return "BNR_ERR_WORKSPACE";
+    case BNR_ERR_UNSUPPORTED: return "BNR_ERR_UNSUPPORTED";
+    case BNR_ERR_HIP: return "BNR_ERR_HIP";
+    case BNR_ERR_ALIAS: return "BNR_ERR_ALIAS";
+    }
+    return "BNR_ERR_UNKNOWN";
+}
+
+const char *bnr_last_error(void) { return g_err; }
+
+size_t bnr_stats_workspace_size(int64_t m, int32_t c)
+{
+    if (m <= 0 || c <= 0) return 0;
+    return stats_ws(m, c);
+}
+
+size_t bnr_workspace_size(const bnr_conv_desc *d)
+{
+    if (check_desc(d) != BNR_OK) return 0;
+    return conv_ws(d).total;
+}
+
+bnr_status bnr_bn_stats(int64_t m, int32_t c, int32_t ldc, bnr_dtype dtype, const void *x, bnr_bn *bn, void *ws,
+                        size_t ws_bytes, void *stream)
+{
+    TRY(check_dtype(dtype));
+    if (m <= 0 || m > ((int64_t)1 << 31)) return fail(BNR_ERR_SHAPE, "m = %lld out of range", (long long)m);
+    TRY(check_channels(c, ldc, dtype, "x"));
+    TRY(check_ptr(x, "x"));
+    TRY(check_bn(bn, "bn", false, true));
+    TRY(check_ws(ws, ws_bytes, stats_ws(m, c)));
+    TRY(run_stats(m, c, ldc, dtype, x, bn, (float *)ws, (hipStream_t)stream));
+    return ok();
+}
+
+bnr_status bnr_conv_bn_stats_fwd(const bnr_conv_desc *d, const void *x, const void *w, void *y, bnr_bn *y_bn,
+                                 void *ws, size_t ws_bytes, void *stream)
+{
+    if (!y_bn) return fail(BNR_ERR_NULL, "y_bn is NULL");
+    return conv_fwd(d, x, nullptr, w, y, y_bn, ws, ws_bytes, stream);
+}
+
+bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w, void *y,
+                                bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!x_bn) return fail(BNR_ERR_NULL, "x_bn is NULL");
+    return conv_fwd(d, x, x_bn, w, y, y_bn, ws, ws_bytes, stream);
+}
+
+bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *x, int32_t ldc,
+                            void *y, void *stream)
+{
+    TRY(check_dtype(dtype));
+    if (n <= 0 || h <= 0 || w <= 0) return fail(BNR_ERR_SHAPE, "n, h, w must be positive");
+    if (h % 2 || w % 2) return fail(BNR_ERR_SHAPE, "h and w must be even");
+    TRY(check_channels(c, ldc, dtype, "x"));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(y, "y"));
+    const int es = esize(dtype);
+    const int64_t m = (int64_t)n * h * w;
+    if (overlap(view_range(x, m, c, ldc, es), view_range(y, m / 4, c, c, es))) return fail(BNR_ERR_ALIAS, "y overlaps x");
+    TRY_HIP(launch_avgpool2(dt_of(dtype), n, h, w, c, x, ldc, y, (hipStream_t)stream), "avgpool");
+    return ok();
+}
+
+bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                         const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy, void *dx,
+                         int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_desc(d));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(w, "w"));
+    TRY(validate_grad_src(d, g));
+    TRY(check_fptr(dw, "dw"));
+    if (x_bn) {
+        TRY(check_bn(x_bn, "x_bn", true, false));
+        TRY(check_fptr(dgamma, "dgamma"));
+        TRY(check_fptr(dbeta, "dbeta"));
+        TRY(check_ptr(dy, "dy"));
+    } else if (!dx) {
+        return fail(BNR_ERR_NULL, "dx is required when x_bn is NULL");
+    }
+    if (dx) {
+        TRY(check_ptr(dx, "dx"));
+        TRY(check_channels(d->c_in, dx_ldc, d->dtype, "dx"));
+    }
+    const ConvWs cw = conv_ws(d);
+    TRY(check_ws(ws, ws_bytes, cw.total));
+    const int es = esize(d->dtype);
+    const int64_t m = pixels(d);
+    const Range rx = view_range(x, m, d->c_in, d->in_ldc, es);
+    if (x_bn) {
+        const Range rdy = view_range(dy, m, d->c_in, d->c_in, es);
+        if (overlap(rdy, rx)) return fail(BNR_ERR_ALIAS, "dy overlaps x");
+        if (dx && overlap(view_range(dx, m, d->c_in, dx_ldc, es), rx)) return fail(BNR_ERR_ALIAS, "dx overlaps x");
+        if (dx && overlap(view_range(dx, m, d->c_in, dx_ldc, es), rdy)) return fail(BNR_ERR_ALIAS, "dx overlaps dy");
+    }
+
+    hipStream_t s = (hipStream_t)stream;
+    char *base = (char *)ws;
+    void *wpack = base;
+    float *part = (float *)(base + cw.pack);
+    float *wgpart = (float *)(base + cw.pack + cw.part);
+    const int dt = dt_of(d->dtype);
+
+    // 1. data gradient with the gradient-source prologue and the BN-backward epilogue
+    TRY_HIP(launch_pack_weights(dt, w, d->k, d->c_in, d->c_out, 1, wpack, s), "weight packing");
+    RowsParams rp;
+    fill_rows(rp, d, d->c_out, d->c_in);
+    rp.wpack = wpack;
+    if (g->kind == BNR_GRAD_DENSE) {
+        rp.pro = PRO_NONE; rp.a = g->g; rp.a_ldc = g->g_ldc;
+    } else if (g->kind == BNR_GRAD_BN) {
+        rp.pro = PRO_BNGRAD; rp.a = g->dy; rp.a_ldc = d->c_out; rp.a2 = g->x; rp.a2_ldc = g->x_ldc;
+        rp.p_gamma = g->bn->gamma; rp.p_mean = g->bn->mean; rp.p_rstd = g->bn->rstd;
+        rp.p_dgamma = g->dgamma; rp.p_dbeta = g->dbeta;
+    } else {
+        rp.pro = PRO_POOLUP; rp.a = g->g; rp.a_ldc = g->g_ldc;
+    }
+    if (x_bn) {
+        rp.epi = EPI_BNBWD; rp.y = dy; rp.y_ldc = d->c_in; rp.part = part;
+        rp.ex = x; rp.ex_ldc = d->in_ldc;
+        rp.e_gamma = x_bn->gamma; rp.e_beta = x_bn->beta; rp.e_mean = x_bn->mean; rp.e_rstd = x_bn->rstd;
+    } else {
+        rp.epi = EPI_STORE; rp.y = dx; rp.y_ldc = dx_ldc; rp.accumulate = dx_accumulate ? 1 : 0;
+    }
+    TRY_HIP(launch_conv_rows(rp, s), "conv data gradient");
+    // 2. dbeta = sum(dy), dgamma = sum(dy * xhat)
+    if (x_bn) {
+        const int64_t R = rows_mtiles(dt, rp.taps, m, d->c_in);
+        TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma, s),
+                "backward sums combine");
+    }
+    // 3. weight gradient, both operands recomputed on load
+    WgradParams wp;
+    memset(&wp, 0, sizeof wp);
+    wp.dtype = dt; wp.k = d->k; wp.n = d->n; wp.h = d->h; wp.w = d->w; wp.m = m;
+    wp.c_in = d->c_in; wp.c_out = d->c_out;
+    wp.x = x; wp.x_ldc = d->in_ldc;
+    if (x_bn) {
+        wp.a_mode = 1;
+        wp.a_gamma = x_bn->gamma; wp.a_beta = x_bn->beta; wp.a_mean = x_bn->mean; wp.a_rstd = x_bn->rstd;
+    }
+    if (g->kind == BNR_GRAD_DENSE) {
+        wp.gsrc = GB_DENSE; wp.g = g->g; wp.g_ldc = g->g_ldc;
+    } else if (g->kind == BNR_GRAD_BN) {
+        wp.gsrc = GB_BNGRAD; wp.g = g->dy; wp.g_ldc = d->c_out; wp.gx = g->x; wp.gx_ldc = g->x_ldc;
+        wp.g_gamma = g->bn->gamma; wp.g_mean = g->bn->mean; wp.g_rstd = g->bn->rstd;
+        wp.g_dgamma = g->dgamma; wp.g_dbeta = g->dbeta;
+    } else {
+        wp.gsrc = GB_POOLUP; wp.g = g->g; wp.g_ldc = g->g_ldc;
+    }
+    wp.dw = dw; wp.part = wgpart;
+    TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
+    // 4. optional standalone BN input gradient
+    if (x_bn && dx) {
+        TRY_HIP(launch_elementwise(dt, EW_DX, m, d->c_in, dy, d->c_in, x, d->in_ldc, x_bn->gamma, nullptr, x_bn->mean,
+                                   x_bn->rstd, dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, s),
+                "BN input gradient");
+    }
+    return ok();
+}
+
+bnr_status bnr_bn_dx(int64_t m, int32_t c, bnr_dtype dtype, const void *dy, const void *x, int32_t x_ldc,
+                     const bnr_bn *bn, const float *dgamma, const float *dbeta, void *dx, int32_t dx_ldc,
+                     int32_t dx_accumulate, void *stream)
+{
+    TRY(check_dtype(dtype));
+    if (m <= 0 || m > ((int64_t)1 << 31)) return fail(BNR_ERR_SHAPE, "m = %lld out of range", (long long)m);
+    TRY(check_channels(c, c, dtype, "dy"));
+    TRY(check_channels(c, x_ldc, dtype, "x"));
+    TRY(check_channels(c, dx_ldc, dtype, "dx"));
+    TRY(check_ptr(dy, "dy"));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(dx, "dx"));
+    TRY(check_bn(bn, "bn", true, false));
+    TRY(check_fptr(dgamma, "dgamma"));
+    TRY(check_fptr(dbeta, "dbeta"));
+    const int es = esize(dtype);
+    const Range rdx = view_range(dx, m, c, dx_ldc, es);
+    if (overlap(rdx, view_range(x, m, c, x_ldc, es))) return fail(BNR_ERR_ALIAS, "dx overlaps x");
+    const Range rdy = view_range(dy, m, c, c, es);
+    if (overlap(rdx, rdy) && !(dy == dx && dx_ldc == c && !dx_accumulate))
+        return fail(BNR_ERR_ALIAS, "dx overlaps dy");
+    TRY_HIP(launch_elementwise(dt_of(dtype), EW_DX, m, c, dy, c, x, x_ldc, bn->gamma, nullptr, bn->mean, bn->rstd,
+                               dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, (hipStream_t)stream),
+            "BN input gradient");
+    return ok();
+}
+
+bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_conv_desc *d, const bnr_ref_args *a,
+                              void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_desc(d));
+    if (mode != BNR_MODE_BASELINE && mode != BNR_MODE_RCF && mode != BNR_MODE_RCF_MVF)
+        return fail(BNR_ERR_UNSUPPORTED, "unknown reference mode %d", (int)mode);
+    if (!a) return fail(BNR_ERR_NULL, "args is NULL");
+    const bool base = mode == BNR_MODE_BASELINE;
+    TRY(check_ptr(a->x, "x"));
+    TRY(check_ptr(a->w, "w"));
+    TRY(check_ptr(a->y, "y"));
+    if (base) TRY(check_ptr(a->z, "z"));
+    TRY(check_bn(a->bn, "bn", true, !backward));
+    const ConvWs cw = conv_ws(d);
+    TRY(check_ws(ws, ws_bytes, cw.total));
+    const int64_t m = pixels(d);
+    const int es = esize(d->dtype);
+    const int dt = dt_of(d->dtype);
+    hipStream_t s = (hipStream_t)stream;
+    char *base_ws = (char *)ws;
+    void *wpack = base_ws;
+    float *part = (float *)(base_ws + cw.pack);
+    float *wgpart = (float *)(base_ws + cw.pack + cw.part);
+    const bnr_bn *bn = a->bn;
+
+    if (!backward) {
+        TRY(check_ptr(a->out, "out"));
+        if (overlap(view_range(a->out, m, d->c_out, d->out_ldc, es), view_range(a->x, m, d->c_in, d->in_ldc, es)))
+            return fail(BNR_ERR_ALIAS, "out overlaps x");
+        const int64_t R = stats_row_blocks(m, d->c_in, dt);
+        if (mode == BNR_MODE_RCF_MVF) {
+            TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUMSQ, nullptr, nullptr, nullptr, 0, part,
+                                         R, s), "stats sweep");
+            TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_MVF, bn->eps, bn->mean, bn->var, bn->rstd,
+                                          nullptr, nullptr, s), "stats combine");
+        } else {
+            // mean sweep, then variance sweep (two-pass, as the unfused BN layer)
+            TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUM, nullptr, nullptr, nullptr, 0, part,
+                                         R, s), "mean sweep");
+            TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_MEAN, bn->eps, bn->mean, nullptr, nullptr, nullptr,
+                                          nullptr, s), "mean combine");
+            TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SQDEV, bn->mean, nullptr, nullptr, 0,
+                                         part, R, s), "variance sweep");
+            TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_VAR, bn->eps, nullptr, bn->var, bn->rstd, nullptr,
+                                          nullptr, s), "variance combine");
+        }
+        TRY_HIP(launch_elementwise(dt, EW_APPLY, m, d->c_in, a->x, d->in_ldc, nullptr, 0, bn->gamma, bn->beta,
+                                   bn->mean, bn->rstd, nullptr, nullptr, a->y, d->c_in, 0, s), "normalise");
+        if (base)
+            TRY_HIP(launch_elementwise(dt, EW_RELU, m, d->c_in, a->y, d->c_in, nullptr, 0, nullptr, nullptr, nullptr,
+                                       nullptr, nullptr, nullptr, a->z, d->c_in, 0, s), "relu");
+        TRY_HIP(launch_pack_weights(dt, a->w, d->k, d->c_in, d->c_out, 0, wpack, s), "weight packing");
+        RowsParams rp;
+        fill_rows(rp, d, d->c_in, d->c_out);
+        rp.pro = base ? PRO_NONE : PRO_RELU;
+        rp.a = base ? a->z : a->y; rp.a_ldc = d->c_in;
+        rp.wpack = wpack;
+        rp.epi = EPI_STORE; rp.y = a->out; rp.y_ldc = d->out_ldc;
+        TRY_HIP(launch_conv_rows(rp, s), "conv forward");
+        return ok();
+    }
+
+    TRY(check_ptr(a->g, "g"));
+    TRY(check_channels(d->c_out, a->g_ldc, d->dtype, "g"));
+    if (base) TRY(check_ptr(a->dz, "dz"));
+    TRY(check_ptr(a->dy, "dy"));
+    TRY(check_fptr(a->dw, "dw"));
+    TRY(check_fptr(a->dgamma, "dgamma"));
+    TRY(check_fptr(a->dbeta, "dbeta"));
+    TRY(check_ptr(a->dx, "dx"));
+    TRY(check_channels(d->c_in, a->dx_ldc, d->dtype, "dx"));
+    if (overlap(view_range(a->dx, m, d->c_in, a->dx_ldc, es), view_range(a->x, m, d->c_in, d->in_ldc, es)))
+        return fail(BNR_ERR_ALIAS, "dx overlaps x");
+    // data gradient (BASELINE: materialise dz; RCF: ReLU mask in the epilogue)
+    TRY_HIP(launch_pack_weights(dt, a->w, d->k, d->c_in, d->c_out, 1, wpack, s), "weight packing");
+    RowsParams rp;
+    fill_rows(rp, d, d->c_out, d->c_in);
+    rp.pro = PRO_NONE; rp.a = a->g; rp.a_ldc = a->g_ldc;
+    rp.wpack = wpack;
+    if (base) {
+        rp.epi = EPI_STORE; rp.y = a->dz; rp.y_ldc = d->c_in;
+    } else {
+        rp.epi = EPI_RELUMASK; rp.y = a->dy; rp.y_ldc = d->c_in; rp.ex = a->y; rp.ex_ldc = d->c_in;
+    }
+    TRY_HIP(launch_conv_rows(rp, s), "conv data gradient");
+    // weight gradient (BASELINE reads the stored z; RCF recomputes relu(y))
+    WgradParams wp;
+    memset(&wp, 0, sizeof wp);
+    wp.dtype = dt; wp.k = d->k; wp.n = d->n; wp.h = d->h; wp.w = d->w; wp.m = m;
+    wp.c_in = d->c_in; wp.c_out = d->c_out;
+    wp.x = base ? a->z : a->y; wp.x_ldc = d->c_in; wp.a_mode = base ? 0 : 2;
+    wp.gsrc = GB_DENSE; wp.g = a->g; wp.g_ldc = a->g_ldc;
+    wp.dw = a->dw; wp.part = wgpart;
+    TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
+    if (base)
+        TRY_HIP(launch_elementwise(dt, EW_RELUBWD, m, d->c_in, a->dz, d->c_in, a->y, d->c_in, nullptr, nullptr, nullptr,
+                                   nullptr, nullptr, nullptr, a->dy, d->c_in, 0, s), "relu backward");
+    const int64_t R = stats_row_blocks(m, d->c_in, dt);
+    TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_DYX, bn->mean, bn->rstd, a->dy, d->c_in, part, R,
+                                 s), "BN backward sums sweep");
+    TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma, s),
+            "BN backward sums combine");
+    TRY_HIP(launch_elementwise(dt, EW_DX, m, d->c_in, a->dy, d->c_in, a->x, d->in_ldc, bn->gamma, nullptr, bn->mean,
+                               bn->rstd, a->dgamma, a->dbeta, a->dx, a->dx_ldc, a->dx_accumulate ? 1 : 0, s),
+            "BN input gradient");
+    return ok();
+}
+
+bnr_status bnr_hbm_copy(const void *src, void *dst, size_t bytes, void *stream)
+{
+    TRY(check_ptr(src, "src"));
+    TRY(check_ptr(dst, "dst"));
+    if (bytes == 0 || bytes % 16) return fail(BNR_ERR_SHAPE, "bytes must be a positive multiple of 16");
+    Range a{(uintptr_t)src, (uintptr_t)src + bytes}, b{(uintptr_t)dst, (uintptr_t)dst + bytes};
+    if (overlap(a, b)) return fail(BNR_ERR_ALIAS, "dst overlaps src");
+    TRY_HIP(launch_copy16(src, dst, (int64_t)(bytes / 16), (hipStream_t)stream), "copy");
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,341 @@
+// bn_kernels.hip -- HBM-streaming BN kernels: per-channel reductions (the
+// sub-BN1 statistics sweep and the backward sums), their float64 combine,
+// the standalone BN input gradient, the unfused A/B kernels (normalise, ReLU,
+// ReLU backward), 2x2 average pooling and a calibration copy.
+//
+// Layout of every sweep: a workgroup owns a block of pixel rows and up to 32
+// 16-byte channel vectors of each row; thread (tx, ty) reads vector tx of rows
+// ty, ty+RY, ... so each wave reads whole contiguous row segments (coalesced
+// NHWC) and keeps its channels' per-thread sums in registers.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "tiles.hpp"
+
+namespace bnr {
+
+// --------------------------------------------------------------------------
+// Per-channel partial sums over a row block.
+//   ST_SUMSQ : s1 = sum x,            s2 = sum x^2        (mean/variance fusion)
+//   ST_SUM   : s1 = sum x                                 (unfused mean sweep)
+//   ST_SQDEV : s1 = sum (x - mean)^2                      (unfused variance sweep)
+//   ST_DYX   : s1 = sum dy,           s2 = sum dy * xhat  (BN backward sums)
+// part[rb][0][c] = s1, part[rb][1][c] = s2 (float32).
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_stats_partial(
+    const T *__restrict__ x, int64_t ldc, int64_t m, int C, int mode,
+    const float *__restrict__ mean, const float *__restrict__ rstd,
+    const T *__restrict__ dy, int64_t dy_ldc, int64_t rows_per_block, float *__restrict__ part)
+{
+    constexpr int VEC = Elem<T>::VEC;
+    __shared__ float red[2][kThreads * VEC];
+    const int cvec = C / VEC;
+    const int vb = min(kStatsMaxVec, cvec - (int)blockIdx.y * kStatsMaxVec);
+    const int ry = kThreads / vb;
+    const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
+    const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
+    float s1[VEC], s2[VEC], mu[VEC], rs[VEC];
+    for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f; }
+    if (ty < ry && (mode == 2 || mode == 3))
+        for (int i = 0; i < VEC; i++) { mu[i] = mean[c0 + i]; rs[i] = rstd[c0 + i]; }
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r1 = min(m, r0 + rows_per_block);
+    if (ty < ry) {
+        int64_t r = r0 + ty;
+        // four rows in flight per thread
+        for (; r + 3 * ry < r1; r += 4 * ry) {
+            vec16 v[4], d[4];
+            for (int u = 0; u < 4; u++) v[u] = ldg16(x + (r + u * ry) * ldc + c0);
+            if (mode == 3)
+                for (int u = 0; u < 4; u++) d[u] = ldg16(dy + (r + u * ry) * dy_ldc + c0);
+            for (int u = 0; u < 4; u++) {
+                float f[VEC], g[VEC];
+                Elem<T>::unpack(v[u], f);
+                if (mode == 0) {
+                    for (int i = 0; i < VEC; i++) { s1[i] += f[i]; s2[i] += f[i] * f[i]; }
+                } else if (mode == 1) {
+                    for (int i = 0; i < VEC; i++) s1[i] += f[i];
+                } else if (mode == 2) {
+                    for (int i = 0; i < VEC; i++) { float e = f[i] - mu[i]; s1[i] += e * e; }
+                } else {
+                    Elem<T>::unpack(d[u], g);
+                    for (int i = 0; i < VEC; i++) { s1[i] += g[i]; s2[i] += g[i] * ((f[i] - mu[i]) * rs[i]); }
+                }
+            }
+        }
+        for (; r < r1; r += ry) {
+            float f[VEC], g[VEC];
+            Elem<T>::unpack(ldg16(x + r * ldc + c0), f);
+            if (mode == 0) {
+                for (int i = 0; i < VEC; i++) { s1[i] += f[i]; s2[i] += f[i] * f[i]; }
+            } else if (mode == 1) {
+                for (int i = 0; i < VEC; i++) s1[i] += f[i];
+            } else if (mode == 2) {
+                for (int i = 0; i < VEC; i++) { float e = f[i] - mu[i]; s1[i] += e * e; }
+            } else {
+                Elem<T>::unpack(ldg16(dy + r * dy_ldc + c0), g);
+                for (int i = 0; i < VEC; i++) { s1[i] += g[i]; s2[i] += g[i] * ((f[i] - mu[i]) * rs[i]); }
+            }
+        }
+    }
+    const int nch = vb * VEC;
+    if (ty < ry)
+        for (int i = 0; i < VEC; i++) {
+            red[0][ty * nch + tx * VEC + i] = s1[i];
+            red[1][ty * nch + tx * VEC + i] = s2[i];
+        }
+    __syncthreads();
+    if (tid < nch) {
+        float a = 0.f, b = 0.f;
+        for (int j = 0; j < ry; j++) { a += red[0][j * nch + tid]; b += red[1][j * nch + tid]; }
+        const int c = (int)blockIdx.y * kStatsMaxVec * VEC + tid;
+        float *p = part + (int64_t)blockIdx.x * 2 * C;
+        p[c] = a;
+        p[C + c] = b;
+    }
+}
+
+// --------------------------------------------------------------------------
+// float64 combine of the partial tiles.  256 threads = 16 channels x 16
+// phases; phase j adds row blocks j, j+16, ...; then the phases are added.
+//   FIN_MVF   : mean = s1/m, var = s2/m - mean^2 (clamped at 0), rstd
+//   FIN_MEAN  : mean = s1/m
+//   FIN_VAR   : var = s1/m, rstd            (two-pass variance)
+//   FIN_BWD   : dbeta = s1, dgamma = s2
+__global__ __launch_bounds__(kThreads) void k_stats_finalize(
+    const float *__restrict__ part, int64_t R, int C, int64_t m, int mode, float eps,
+    float *__restrict__ mean, float *__restrict__ var, float *__restrict__ rstd,
+    float *__restrict__ dbeta, float *__restrict__ dgamma)
+{
+    __shared__ double red[2][16][17];
+    const int tid = threadIdx.x, cl = tid % 16, ph = tid / 16;
+    const int c = blockIdx.x * 16 + cl;
+    double a = 0.0, b = 0.0;
+    if (c < C) {
+        const float *p = part + c;
+        for (int64_t r = ph; r < R; r += 16) {
+            a += (double)p[r * 2 * C];
+            b += (double)p[r * 2 * C + C];
+        }
+    }
+    red[0][ph][cl] = a;
+    red[1][ph][cl] = b;
+    __syncthreads();
+    if (ph == 0 && c < C) {
+        a = 0.0; b = 0.0;
+        for (int j = 0; j < 16; j++) { a += red[0][j][cl]; b += red[1][j][cl]; }
+        const double dm = (double)m;
+        if (mode == FIN_MVF) {
+            double mu = a / dm, v = b / dm - mu * mu;
+            if (v < 0.0) v = 0.0;
+            mean[c] = (float)mu;
+            if (var) var[c] = (float)v;
+            rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
+        } else if (mode == FIN_MEAN) {
+            mean[c] = (float)(a / dm);
+        } else if (mode == FIN_VAR) {
+            double v = a / dm;
+            if (var) var[c] = (float)v;
+            rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
+        } else {
+            dbeta[c] = (float)a;
+            dgamma[c] = (float)b;
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
+// Element-wise passes over [m][C] views with per-channel parameters.
+//   EW_DX      : out = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m)  [+ out]
+//   EW_APPLY   : out = gamma*(x-mean)*rstd + beta                  (unfused BN)
+//   EW_RELU    : out = max(x, 0)                                   (unfused ReLU)
+//   EW_RELUBWD : out = x2 > 0 ? x : 0   (x = dz, x2 = y)           (unfused ReLU bwd)
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_elementwise(
+    int mode, int64_t m, int C, const T *__restrict__ x, int64_t x_ldc, const T *__restrict__ x2,
+    int64_t x2_ldc, const float *__restrict__ gamma, const float *__restrict__ beta,
+    const float *__restrict__ mean, const float *__restrict__ rstd, const float *__restrict__ dgamma,
+    const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int accumulate,
+    int64_t rows_per_block)
+{
+    constexpr int VEC = Elem<T>::VEC;
+    const int cvec = C / VEC;
+    const int vb = min(kStatsMaxVec, cvec - (int)blockIdx.y * kStatsMaxVec);
+    const int ry = kThreads / vb;
+    const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
+    if (ty >= ry) return;
+    const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
+    float p0[VEC], p1[VEC], p2[VEC], p3[VEC];
+    const float inv_m = 1.0f / (float)m;
+    for (int i = 0; i < VEC; i++) {
+        const int c = c0 + i;
+        if (mode == EW_DX) {
+            p0[i] = gamma[c] * rstd[c];          // k
+            p1[i] = dbeta[c] * inv_m;            // a
+            p2[i] = dgamma[c] * inv_m;           // b
+            p3[i] = mean[c];
+        } else if (mode == EW_APPLY) {
+            p0[i] = gamma[c];
+            p1[i] = beta[c];
+            p2[i] = rstd[c];
+            p3[i] = mean[c];
+        } else {
+            p0[i] = p1[i] = p2[i] = p3[i] = 0.f;
+        }
+    }
+    float rsd[VEC];
+    if (mode == EW_DX)
+        for (int i = 0; i < VEC; i++) rsd[i] = rstd[c0 + i];
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r1 = min(m, r0 + rows_per_block);
+    for (int64_t r = r0 + ty; r < r1; r += ry) {
+        float f[VEC], g[VEC], o[VEC];
+        Elem<T>::unpack(ldg16(x + r * x_ldc + c0), f);
+        if (mode == EW_DX || mode == EW_RELUBWD) Elem<T>::unpack(ldg16(x2 + r * x2_ldc + c0), g);
+        T *dst = out + r * out_ldc + c0;
+        if (mode == EW_DX) {
+            // f = dy, g = x
+            for (int i = 0; i < VEC; i++) {
+                float xh = (g[i] - p3[i]) * rsd[i];
+                o[i] = p0[i] * (f[i] - p1[i] - xh * p2[i]);
+            }
+            if (accumulate) {
+                float old[VEC];
+                Elem<T>::unpack(ldg16(dst), old);
+                for (int i = 0; i < VEC; i++) o[i] += old[i];
+            }
+        } else if (mode == EW_APPLY) {
+            for (int i = 0; i < VEC; i++) o[i] = p0[i] * ((f[i] - p3[i]) * p2[i]) + p1[i];
+        } else if (mode == EW_RELU) {
+            for (int i = 0; i < VEC; i++) o[i] = f[i] > 0.f ? f[i] : 0.f;
+        } else {
+            for (int i = 0; i < VEC; i++) o[i] = g[i] > 0.f ? f[i] : 0.f;
+        }
+        stg16(dst, Elem<T>::pack(o));
+    }
+}
+
+// --------------------------------------------------------------------------
+// 2x2 / stride-2 average pooling: one thread per output 16-byte vector.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_avgpool2(int n, int h, int w, int C, const T *__restrict__ x,
+                                                       int64_t ldc, T *__restrict__ y)
+{
+    constexpr int VEC = Elem<T>::VEC;
+    const int cvec = C / VEC, ho = h / 2, wo = w / 2;
+    const int64_t total = (int64_t)n * ho * wo * cvec;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
+        const int v = (int)(i % cvec);
+        const int64_t op = i / cvec;
+        const int ox = (int)(op % wo);
+        const int64_t t = op / wo;
+        const int oy = (int)(t % ho);
+        const int64_t nn = t / ho;
+        const int64_t ip = (nn * h + 2 * oy) * w + 2 * ox;
+        float a[VEC], b[VEC], s[VEC];
+        Elem<T>::unpack(ldg16(x + ip * ldc + v * VEC), s);
+        Elem<T>::unpack(ldg16(x + (ip + 1) * ldc + v * VEC), a);
+        for (int j = 0; j < VEC; j++) s[j] += a[j];
+        Elem<T>::unpack(ldg16(x + (ip + w) * ldc + v * VEC), a);
+        Elem<T>::unpack(ldg16(x + (ip + w + 1) * ldc + v * VEC), b);
+        for (int j = 0; j < VEC; j++) s[j] = 0.25f * (s[j] + a[j] + b[j]);
+        stg16(y + op * C + v * VEC, Elem<T>::pack(s));
+    }
+}
+
+// --------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_copy16(const vec16 *__restrict__ src, vec16 *__restrict__ dst,
+                                                     int64_t nvec)
+{
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    for (; i + 3 * stride < nvec; i += 4 * stride) {
+        vec16 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        dst[i] = a; dst[i + stride] = b; dst[i + 2 * stride] = c; dst[i + 3 * stride] = d;
+    }
+    for (; i < nvec; i += stride) dst[i] = src[i];
+}
+
+// Sum of S float32 partial tiles in a fixed order (deterministic).
+__global__ __launch_bounds__(kThreads) void k_sum_partials(const float *__restrict__ part, int64_t S,
+                                                           int64_t len, float *__restrict__ out)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < len; i += (int64_t)gridDim.x * kThreads) {
+        float s = 0.f;
+        for (int64_t j = 0; j < S; j++) s += part[j * len + i];
+        out[i] = s;
+    }
+}
+
+// --------------------------------------------------------------- launchers --
+static inline int grid_cap(int64_t want) { return (int)(want < 4096 ? (want < 1 ? 1 : want) : 4096); }
+
+hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
+                                const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
+                                float *part, int64_t R, hipStream_t s)
+{
+    const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
+    const int64_t rpb = ceil_div(m, R);
+    dim3 grid((unsigned)R, (unsigned)cb);
+    if (dtype == DT_BF16)
+        hipLaunchKernelGGL(k_stats_partial<bf16_t>, grid, dim3(kThreads), 0, s, (const bf16_t *)x, ldc, m, C, mode,
+                           mean, rstd, (const bf16_t *)dy, dy_ldc, rpb, part);
+    else
+        hipLaunchKernelGGL(k_stats_partial<float>, grid, dim3(kThreads), 0, s, (const float *)x, ldc, m, C, mode,
+                           mean, rstd, (const float *)dy, dy_ldc, rpb, part);
+    return hipGetLastError();
+}
+
+hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
+                                 float *var, float *rstd, float *dbeta, float *dgamma, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_stats_finalize, dim3((unsigned)ceil_div(C, 16)), dim3(kThreads), 0, s, part, R, C, m, mode,
+                       eps, mean, var, rstd, dbeta, dgamma);
+    return hipGetLastError();
+}
+
+hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void *x, int64_t x_ldc, const void *x2,
+                              int64_t x2_ldc, const float *gamma, const float *beta, const float *mean,
+                              const float *rstd, const float *dgamma, const float *dbeta, void *out,
+                              int64_t out_ldc, int accumulate, hipStream_t s)
+{
+    const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
+    const int64_t R = stats_row_blocks(m, C, dtype) * 2;
+    const int64_t rpb = ceil_div(m, R);
+    dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
+    if (dtype == DT_BF16)
+        hipLaunchKernelGGL(k_elementwise<bf16_t>, grid, dim3(kThreads), 0, s, mode, m, C, (const bf16_t *)x, x_ldc,
+                           (const bf16_t *)x2, x2_ldc, gamma, beta, mean, rstd, dgamma, dbeta, (bf16_t *)out,
+                           out_ldc, accumulate, rpb);
+    else
+        hipLaunchKernelGGL(k_elementwise<float>, grid, dim3(kThreads), 0, s, mode, m, C, (const float *)x, x_ldc,
+                           (const float *)x2, x2_ldc, gamma, beta, mean, rstd, dgamma, dbeta, (float *)out, out_ldc,
+                           accumulate, rpb);
+    return hipGetLastError();
+}
+
+hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, hipStream_t s)
+{
+    const int64_t total = (int64_t)n * (h / 2) * (w / 2) * (C / (dtype == DT_BF16 ? 8 : 4));
+    const int grid = grid_cap(ceil_div(total, kThreads));
+    if (dtype == DT_BF16)
+        hipLaunchKernelGGL(k_avgpool2<bf16_t>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const bf16_t *)x, ldc,
+                           (bf16_t *)y);
+    else
+        hipLaunchKernelGGL(k_avgpool2<float>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const float *)x, ldc,
+                           (float *)y);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_copy16, dim3(2048), dim3(kThreads), 0, s, (const vec16 *)src, (vec16 *)dst, nvec);
+    return hipGetLastError();
+}
+
+hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_sum_partials, dim3(grid_cap(ceil_div(len, kThreads))), dim3(kThreads), 0, s, part, S, len, out);
+    return hipGetLastError();
+}
+
+}  // namespace bnr

@@ -1,0 +1,81 @@
+// common.hpp -- device helpers shared by the libbnr kernels (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bnr {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_t;   // bf16 storage word
+
+struct alignas(16) vec16 { uint32_t u[4]; };
+
+constexpr int kThreads = 256;   // every kernel runs 256-thread workgroups (4 waves of 64)
+
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
+// float -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+    __bf16 b = (__bf16)f;
+    bf16_t u;
+    __builtin_memcpy(&u, &b, 2);
+    return u;
+}
+__device__ __forceinline__ uint32_t pack2bf(float lo, float hi) {
+    return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+// Element traits: VEC = elements per 16-byte vector; storage <-> float.
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+    static constexpr int VEC = 4;
+    __device__ static __forceinline__ void unpack(const vec16 &v, float *f) {
+        for (int i = 0; i < 4; i++) f[i] = __uint_as_float(v.u[i]);
+    }
+    __device__ static __forceinline__ vec16 pack(const float *f) {
+        vec16 v;
+        for (int i = 0; i < 4; i++) v.u[i] = __float_as_uint(f[i]);
+        return v;
+    }
+    __device__ static __forceinline__ float round(float f) { return f; }
+    __device__ static __forceinline__ float load1(const float *p) { return *p; }
+    __device__ static __forceinline__ float from(float s) { return s; }
+};
+template <> struct Elem<bf16_t> {
+    static constexpr int VEC = 8;
+    __device__ static __forceinline__ void unpack(const vec16 &v, float *f) {
+        for (int i = 0; i < 4; i++) {
+            f[2 * i] = __uint_as_float(v.u[i] << 16);
+            f[2 * i + 1] = __uint_as_float(v.u[i] & 0xffff0000u);
+        }
+    }
+    __device__ static __forceinline__ vec16 pack(const float *f) {
+        vec16 v;
+        for (int i = 0; i < 4; i++) v.u[i] = pack2bf(f[2 * i], f[2 * i + 1]);
+        return v;
+    }
+    __device__ static __forceinline__ float round(float f) { return bf2f(f2bf(f)); }
+};
+
+__device__ __forceinline__ vec16 ldg16(const void *p) { return *reinterpret_cast<const vec16 *>(p); }
+__device__ __forceinline__ void stg16(void *p, const vec16 &v) { *reinterpret_cast<vec16 *>(p) = v; }
+__device__ __forceinline__ vec16 zero16() { vec16 v; v.u[0] = v.u[1] = v.u[2] = v.u[3] = 0; return v; }
+
+// Wave-level sum over the 64 lanes of a wave (all lanes get the result).
+__device__ __forceinline__ float wave_sum(float v) {
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Logical workgroup index for XCD-aware scheduling.  The dispatcher hands
+// consecutive workgroup ids round-robin to the 8 XCDs (each with its own L2);
+// this remap makes logically consecutive tiles land on the same XCD so that
+// data they share (halo rows, re-read operands) hits in that XCD's L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+    const int X = 8;
+    if (nblocks % X) return bid;             // keep identity when not divisible
+    int per = nblocks / X;
+    return (bid % X) * per + bid / X;
+}
+
+}  // namespace bnr

@@ -1,0 +1,375 @@
+// conv_rows.hip -- implicit-GEMM CONV over NHWC pixel rows on the gfx950
+// matrix cores, with the BN fission/fusion prologues and epilogues.
+//
+// GEMM view: M = pixels, N = output channels, K = taps x input channels.
+// The same kernel runs the forward CONV and the data gradient (the data
+// gradient of a stride-1 zero-padded CONV is a forward CONV of the output
+// gradient with the filter taps flipped and c_in/c_out swapped; the weight
+// packer produces that operand).
+//
+// Per workgroup: a BM x BN output tile.  K is consumed in chunks of 32 input
+// channels; for each chunk the workgroup stages (a) the A rows of its pixels
+// plus, for 3x3, a halo of W+1 pixel rows on each side, already transformed
+// by the prologue and rounded to the matrix-core operand type, and (b) the
+// packed weights of all taps of the chunk.  Each tap then reads its shifted
+// A rows from LDS; taps that leave the image read 0 (zero padding applies to
+// the CONV input, i.e. after BN and ReLU).
+//
+// Prologues (sub-BN2 side, Sec. 3.2):
+//   PRO_RELU   : a = max(x, 0)   (ReLU-CONV fusion alone, unfused-BN modes)
+//   PRO_BNRELU : a = max(gamma*(x-mean)*rstd + beta, 0)
+//   PRO_BNGRAD : a = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m)  (deferred BN
+//                input gradient, from dy and the BN input x)
+//   PRO_POOLUP : a = g[n][y/2][x/2] / 4   (2x2 average-pooling gradient)
+// Epilogues (sub-BN1 side):
+//   EPI_STATS  : store y, per-channel sum(y), sum(y^2) of the stored values
+//   EPI_BNBWD  : dy = dz * [gamma*xhat+beta > 0] with xhat from the BN input,
+//                store dy, per-channel sum(dy), sum(dy*xhat)
+//   EPI_RELUMASK: dy = dz * [y > 0] from a stored y (ReLU-CONV fusion alone)
+// The epilogue goes through LDS so that every global access is a 16-byte
+// vector of one pixel row.
+#include "common.hpp"
+#include "kernels.hpp"
+#include "mfma.hpp"
+#include "tiles.hpp"
+
+namespace bnr {
+
+template <typename T, int TAPS, int BM, int BN>
+struct RowsCfg {
+    static constexpr int VEC = Elem<T>::VEC;
+    static constexpr int PAD = 16 / (int)sizeof(T);
+    static constexpr int ASTR = kRowsBK + PAD;                 // staged row stride (elements)
+    static constexpr int HALO_MAX = TAPS == 9 ? kRowsMaxW3 + 1 : 0;
+    static constexpr int AROWS = BM + 2 * HALO_MAX;
+    static constexpr int A_ELEMS = AROWS * ASTR;
+    static constexpr int B_ELEMS = TAPS * BN * ASTR;
+    static constexpr int CSTR = BN + PAD;
+    static constexpr size_t STAGE_BYTES = (size_t)(A_ELEMS + B_ELEMS) * sizeof(T);
+    static constexpr size_t EPI_BYTES = (size_t)BM * CSTR * sizeof(T);
+    static constexpr int RSTEP = kThreads / (BN / VEC);
+    static constexpr size_t RED_BYTES = 2ull * RSTEP * BN * sizeof(float);
+    static constexpr size_t LDS = STAGE_BYTES > EPI_BYTES ? (STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES)
+                                                          : (EPI_BYTES > RED_BYTES ? EPI_BYTES : RED_BYTES);
+};
+
+template <typename T, int TAPS, int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
+{
+    using Cfg = RowsCfg<T, TAPS, BM, BN>;
+    using M = Mfma<T>;
+    constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
+    constexpr int VEC = Cfg::VEC, ASTR = Cfg::ASTR, VPR = kRowsBK / VEC;
+    static_assert(WM * WN == 4, "four waves");
+    static_assert(TM * WM * 16 == BM && TN * WN * 16 == BN, "tile");
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *As = reinterpret_cast<T *>(smem);
+    T *Bs = As + Cfg::A_ELEMS;
+    float *coef = reinterpret_cast<float *>(smem + Cfg::LDS);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int mt = xcd_remap(blockIdx.x, gridDim.x);
+    const int nt = blockIdx.y;
+    const int64_t m = p.m;
+    const int64_t p0 = (int64_t)mt * BM;
+    const int n0 = nt * BN;
+    const int H = p.h, W = p.w, K = p.K, N = p.N;
+    const int halo = TAPS == 9 ? W + 1 : 0;
+    const int arows = BM + 2 * halo;
+
+    // per-channel prologue coefficients for all K channels
+    if (p.pro == PRO_BNRELU) {
+        for (int c = tid; c < K; c += kThreads) {
+            coef[c] = p.p_mean[c];
+            coef[K + c] = p.p_gamma[c] * p.p_rstd[c];
+            coef[2 * K + c] = p.p_beta[c];
+        }
+    } else if (p.pro == PRO_BNGRAD) {
+        const float inv_m = 1.0f / (float)m;
+        for (int c = tid; c < K; c += kThreads) {
+            coef[c] = p.p_mean[c];
+            coef[K + c] = p.p_rstd[c];
+            coef[2 * K + c] = p.p_gamma[c] * p.p_rstd[c];
+            coef[3 * K + c] = p.p_dbeta[c] * inv_m;
+            coef[4 * K + c] = p.p_dgamma[c] * inv_m;
+        }
+    }
+
+    // geometry of this lane's output rows
+    int hh[TM], ww[TM];
+    bool rv[TM];
+    for (int rb = 0; rb < TM; rb++) {
+        const int64_t pp = p0 + wm * TM * 16 + rb * 16 + (lane & 15);
+        rv[rb] = pp < m;
+        ww[rb] = (int)(pp % W);
+        hh[rb] = (int)((pp / W) % H);
+    }
+
+    f32x4 acc[TM][TN];
+    for (int rb = 0; rb < TM; rb++)
+        for (int cb = 0; cb < TN; cb++) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nchunks = (K + kRowsBK - 1) / kRowsBK;
+    const T *asrc = reinterpret_cast<const T *>(p.a);
+    const T *asrc2 = reinterpret_cast<const T *>(p.a2);
+    __syncthreads();
+
+    for (int ch = 0; ch < nchunks; ch++) {
+        const int c0 = ch * kRowsBK;
+        // ---- stage A (prologue applied, zero outside the tensor) ----
+        for (int i = tid; i < arows * VPR; i += kThreads) {
+            const int r = i / VPR, v = i % VPR;
+            const int64_t pp = p0 - halo + r;
+            const int c = c0 + v * VEC;
+            vec16 out = zero16();
+            if (pp >= 0 && pp < m && c < K) {
+                if (p.pro == PRO_NONE) {
+                    out = ldg16(asrc + pp * p.a_ldc + c);
+                } else if (p.pro == PRO_BNRELU) {
+                    float f[VEC];
+                    Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
+                    for (int e = 0; e < VEC; e++) {
+                        float t = (f[e] - coef[c + e]) * coef[K + c + e] + coef[2 * K + c + e];
+                        f[e] = t > 0.f ? t : 0.f;
+                    }
+                    out = Elem<T>::pack(f);
+                } else if (p.pro == PRO_BNGRAD) {
+                    float d[VEC], x[VEC];
+                    Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), d);
+                    Elem<T>::unpack(ldg16(asrc2 + pp * p.a2_ldc + c), x);
+                    for (int e = 0; e < VEC; e++) {
+                        const float xh = (x[e] - coef[c + e]) * coef[K + c + e];
+                        d[e] = coef[2 * K + c + e] * (d[e] - coef[3 * K + c + e] - xh * coef[4 * K + c + e]);
+                    }
+                    out = Elem<T>::pack(d);
+                } else if (p.pro == PRO_RELU) {
+                    float f[VEC];
+                    Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
+                    for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
+                    out = Elem<T>::pack(f);
+                } else {  // PRO_POOLUP
+                    const int64_t img = pp / ((int64_t)H * W);
+                    const int rem = (int)(pp - img * H * W);
+                    const int y = rem / W, x = rem - y * W;
+                    const int64_t q = (img * (H / 2) + y / 2) * (W / 2) + x / 2;
+                    float f[VEC];
+                    Elem<T>::unpack(ldg16(asrc + q * p.a_ldc + c), f);
+                    for (int e = 0; e < VEC; e++) f[e] *= 0.25f;
+                    out = Elem<T>::pack(f);
+                }
+            }
+            *reinterpret_cast<vec16 *>(As + r * ASTR + v * VEC) = out;
+        }
+        // ---- stage B: all taps of this chunk (packed, zero-padded) ----
+        const T *wsrc = reinterpret_cast<const T *>(p.wpack) + ((int64_t)nt * nchunks + ch) * (TAPS * BN * kRowsBK);
+        for (int i = tid; i < TAPS * BN * VPR; i += kThreads) {
+            const int row = i / VPR, v = i % VPR;
+            *reinterpret_cast<vec16 *>(Bs + row * ASTR + v * VEC) = ldg16(wsrc + row * kRowsBK + v * VEC);
+        }
+        __syncthreads();
+        // ---- matrix cores ----
+        for (int tap = 0; tap < TAPS; tap++) {
+            const int dh = TAPS == 9 ? tap / 3 - 1 : 0, dw = TAPS == 9 ? tap % 3 - 1 : 0;
+            const int off = dh * W + dw;
+            for (int ks = 0; ks < kRowsBK / M::KSTEP; ks++) {
+                const int kofs = ks * M::KSTEP + (lane >> 4) * M::KPL;
+                typename M::frag b[TN];
+                for (int cb = 0; cb < TN; cb++)
+                    b[cb] = M::load(Bs + (tap * BN + wn * TN * 16 + cb * 16 + (lane & 15)) * ASTR + kofs);
+                for (int rb = 0; rb < TM; rb++) {
+                    const bool ok = rv[rb] && (unsigned)(hh[rb] + dh) < (unsigned)H &&
+                                    (unsigned)(ww[rb] + dw) < (unsigned)W;
+                    const int lrow = wm * TM * 16 + rb * 16 + (lane & 15) + halo + off;
+                    typename M::frag a = M::load(As + lrow * ASTR + kofs);
+                    if (!ok) a = M::zero();
+                    for (int cb = 0; cb < TN; cb++) M::mma(acc[rb][cb], a, b[cb]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: accumulators -> LDS tile (storage type) ----
+    T *Cs = reinterpret_cast<T *>(smem);
+    for (int rb = 0; rb < TM; rb++)
+        for (int cb = 0; cb < TN; cb++)
+            for (int i = 0; i < 4; i++) {
+                const int row = wm * TM * 16 + rb * 16 + (lane >> 4) * 4 + i;
+                const int col = wn * TN * 16 + cb * 16 + (lane & 15);
+                Cs[row * Cfg::CSTR + col] = to_store<T>(acc[rb][cb][i]);
+            }
+    __syncthreads();
+
+    constexpr int VPRO = BN / VEC, RSTEP = Cfg::RSTEP;
+    const int v = tid % VPRO, r0 = tid / VPRO;
+    const int n = n0 + v * VEC;
+    const bool col_ok = n < N;
+    float s1[VEC], s2[VEC], emu[VEC], ers[VEC], eg[VEC], eb[VEC];
+    for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
+    if (p.epi == EPI_BNBWD && col_ok)
+        for (int e = 0; e < VEC; e++) {
+            emu[e] = p.e_mean[n + e]; ers[e] = p.e_rstd[n + e];
+            eg[e] = p.e_gamma[n + e]; eb[e] = p.e_beta[n + e];
+        }
+    T *yout = reinterpret_cast<T *>(p.y);
+    const T *exs = reinterpret_cast<const T *>(p.ex);
+    if (col_ok) {
+        for (int r = r0; r < BM; r += RSTEP) {
+            const int64_t pp = p0 + r;
+            if (pp >= m) break;
+            const vec16 cv = *reinterpret_cast<const vec16 *>(Cs + r * Cfg::CSTR + v * VEC);
+            T *dst = yout + pp * p.y_ldc + n;
+            if (p.epi == EPI_STORE) {
+                if (p.accumulate) {
+                    float f[VEC], old[VEC];
+                    Elem<T>::unpack(cv, f);
+                    Elem<T>::unpack(ldg16(dst), old);
+                    for (int e = 0; e < VEC; e++) f[e] += old[e];
+                    stg16(dst, Elem<T>::pack(f));
+                } else {
+                    stg16(dst, cv);
+                }
+            } else if (p.epi == EPI_STATS) {
+                float f[VEC];
+                Elem<T>::unpack(cv, f);
+                stg16(dst, cv);
+                for (int e = 0; e < VEC; e++) { s1[e] += f[e]; s2[e] += f[e] * f[e]; }
+            } else if (p.epi == EPI_RELUMASK) {
+                float f[VEC], yv[VEC];
+                Elem<T>::unpack(cv, f);
+                Elem<T>::unpack(ldg16(exs + pp * p.ex_ldc + n), yv);
+                for (int e = 0; e < VEC; e++) f[e] = yv[e] > 0.f ? f[e] : 0.f;
+                stg16(dst, Elem<T>::pack(f));
+            } else {
+                float f[VEC], x[VEC];
+                Elem<T>::unpack(cv, f);
+                Elem<T>::unpack(ldg16(exs + pp * p.ex_ldc + n), x);
+                for (int e = 0; e < VEC; e++) {
+                    const float xh = (x[e] - emu[e]) * ers[e];
+                    const float yv = eg[e] * xh + eb[e];
+                    const float d = yv > 0.f ? f[e] : 0.f;
+                    f[e] = d;
+                    s1[e] += d;
+                    s2[e] += d * xh;
+                }
+                stg16(dst, Elem<T>::pack(f));
+            }
+        }
+    }
+    if (p.epi == EPI_STATS || p.epi == EPI_BNBWD) {
+        __syncthreads();
+        float *red = reinterpret_cast<float *>(smem);
+        for (int e = 0; e < VEC; e++) {
+            red[r0 * BN + v * VEC + e] = s1[e];
+            red[(RSTEP + r0) * BN + v * VEC + e] = s2[e];
+        }
+        __syncthreads();
+        if (tid < BN && n0 + tid < N) {
+            float a = 0.f, b = 0.f;
+            for (int j = 0; j < RSTEP; j++) { a += red[j * BN + tid]; b += red[(RSTEP + j) * BN + tid]; }
+            p.part[(int64_t)mt * 2 * N + n0 + tid] = a;
+            p.part[(int64_t)mt * 2 * N + N + n0 + tid] = b;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Weight packing: W[kh][kw][ci][co] -> [ntile][chunk][tap][n][32] (GEMM order),
+// zero outside the real K/N ranges.  transpose = 1 flips the taps and swaps
+// ci/co (data-gradient operand).
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_pack_weights(const T *__restrict__ w, int taps, int c_in, int c_out,
+                                                           int transpose, int bn, int nchunks, int64_t total,
+                                                           T *__restrict__ out)
+{
+    for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * kThreads) {
+        const int kk = (int)(idx % kRowsBK);
+        int64_t t = idx / kRowsBK;
+        const int nl = (int)(t % bn); t /= bn;
+        const int tap = (int)(t % taps); t /= taps;
+        const int ch = (int)(t % nchunks);
+        const int ntile = (int)(t / nchunks);
+        const int kc = ch * kRowsBK + kk, nn = ntile * bn + nl;
+        T val = T(0);
+        if (!transpose) {
+            if (kc < c_in && nn < c_out) val = w[((int64_t)tap * c_in + kc) * c_out + nn];
+        } else {
+            if (kc < c_out && nn < c_in) val = w[((int64_t)(taps - 1 - tap) * c_in + nn) * c_out + kc];
+        }
+        out[idx] = val;
+    }
+}
+
+// ------------------------------------------------------------- launchers ---
+int64_t rows_mtiles(int dtype, int taps, int64_t m, int n_out)
+{
+    return ceil_div(m, rows_tile(dtype, taps, n_out).bm);
+}
+
+size_t rows_pack_bytes(int dtype, int taps, int K, int N)
+{
+    const RowsTile t = rows_tile(dtype, taps, N);
+    const int64_t ntiles = ceil_div(N, t.bn), nchunks = ceil_div(K, kRowsBK);
+    return (size_t)(ntiles * nchunks * taps * t.bn * kRowsBK) * (dtype == DT_BF16 ? 2 : 4);
+}
+
+hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_out, int transpose, void *wpack,
+                               hipStream_t s)
+{
+    const int taps = k * k;
+    const int K = transpose ? c_out : c_in, N = transpose ? c_in : c_out;
+    const RowsTile t = rows_tile(dtype, taps, N);
+    const int64_t ntiles = ceil_div(N, t.bn), nchunks = ceil_div(K, kRowsBK);
+    const int64_t total = ntiles * nchunks * taps * t.bn * kRowsBK;
+    const int grid = (int)(ceil_div(total, kThreads) < 1024 ? ceil_div(total, kThreads) : 1024);
+    if (dtype == DT_BF16)
+        hipLaunchKernelGGL(k_pack_weights<bf16_t>, dim3(grid), dim3(kThreads), 0, s, (const bf16_t *)w, taps, c_in,
+                           c_out, transpose, t.bn, (int)nchunks, total, (bf16_t *)wpack);
+    else
+        hipLaunchKernelGGL(k_pack_weights<float>, dim3(grid), dim3(kThreads), 0, s, (const float *)w, taps, c_in,
+                           c_out, transpose, t.bn, (int)nchunks, total, (float *)wpack);
+    return hipGetLastError();
+}
+
+template <typename T, int TAPS, int BM, int BN, int WM, int WN>
+static hipError_t run_rows(const RowsParams &p, hipStream_t s)
+{
+    using Cfg = RowsCfg<T, TAPS, BM, BN>;
+    const int P = p.pro == PRO_BNRELU ? 3 : (p.pro == PRO_BNGRAD ? 5 : 0);
+    const size_t lds = Cfg::LDS + (size_t)P * p.K * sizeof(float);
+    auto kern = k_conv_rows<T, TAPS, BM, BN, WM, WN>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    dim3 grid((unsigned)ceil_div(p.m, BM), (unsigned)ceil_div(p.N, BN));
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s)
+{
+    const RowsTile t = rows_tile(p.dtype, p.taps, p.N);
+    if (p.dtype == DT_BF16) {
+        if (p.taps == 1) {
+            if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1>(p, s);
+            if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1>(p, s);
+            return run_rows<bf16_t, 1, 128, 128, 2, 2>(p, s);
+        }
+        if (t.bn == 32) return run_rows<bf16_t, 9, 128, 32, 4, 1>(p, s);
+        return run_rows<bf16_t, 9, 128, 64, 4, 1>(p, s);
+    }
+    if (p.taps == 1) {
+        if (t.bn == 32) return run_rows<float, 1, 64, 32, 4, 1>(p, s);
+        return run_rows<float, 1, 64, 64, 4, 1>(p, s);
+    }
+    if (t.bn == 32) return run_rows<float, 9, 64, 32, 4, 1>(p, s);
+    return run_rows<float, 9, 64, 64, 4, 1>(p, s);
+}
+
+}  // namespace bnr

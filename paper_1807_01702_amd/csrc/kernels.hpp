@@ -1,0 +1,83 @@
+// kernels.hpp -- launcher interfaces between the C ABI (api.hip) and the
+// HIP kernels.  Launchers assume validated arguments.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bnr {
+
+// k_stats_partial modes
+enum { ST_SUMSQ = 0, ST_SUM = 1, ST_SQDEV = 2, ST_DYX = 3 };
+// k_stats_finalize modes
+enum { FIN_MVF = 0, FIN_MEAN = 1, FIN_VAR = 2, FIN_BWD = 3 };
+// k_elementwise modes
+enum { EW_DX = 0, EW_APPLY = 1, EW_RELU = 2, EW_RELUBWD = 3 };
+
+hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
+                                const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
+                                float *part, int64_t R, hipStream_t s);
+hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
+                                 float *var, float *rstd, float *dbeta, float *dgamma, hipStream_t s);
+hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void *x, int64_t x_ldc, const void *x2,
+                              int64_t x2_ldc, const float *gamma, const float *beta, const float *mean,
+                              const float *rstd, const float *dgamma, const float *dbeta, void *out,
+                              int64_t out_ldc, int accumulate, hipStream_t s);
+hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, hipStream_t s);
+hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s);
+hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, hipStream_t s);
+
+// ---- implicit-GEMM CONV over pixel rows (forward / data gradient) ---------
+enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 4 };
+enum { EPI_STORE = 0, EPI_STATS = 1, EPI_BNBWD = 2, EPI_RELUMASK = 3 };
+
+struct RowsParams {
+    int dtype, taps, n, h, w;
+    int64_t m;
+    int K, N;                     // GEMM reduction channels (A channels), output channels
+    int pro;
+    const void *a;                // A source: conv input / dy (BNGRAD) / pooled gradient (POOLUP)
+    int64_t a_ldc;
+    const void *a2;               // BNGRAD: the BN input x (same pixels, K channels)
+    int64_t a2_ldc;
+    const float *p_gamma, *p_beta, *p_mean, *p_rstd, *p_dgamma, *p_dbeta;
+    const void *wpack;            // weights packed by launch_pack_weights
+    int epi;
+    void *y;                      // output view (EPI_BNBWD: dy, dense)
+    int64_t y_ldc;
+    int accumulate;               // EPI_STORE only
+    float *part;                  // EPI_STATS / EPI_BNBWD: [mtiles][2][N]
+    const void *ex;               // EPI_BNBWD: BN input (N channels); EPI_RELUMASK: ReLU input
+    int64_t ex_ldc;
+    const float *e_gamma, *e_beta, *e_mean, *e_rstd;
+};
+int64_t rows_mtiles(int dtype, int taps, int64_t m, int n_out);
+size_t rows_pack_bytes(int dtype, int taps, int K, int N);
+// transpose = 0: forward packing of W[kh][kw][ci][co] (GEMM K = ci, N = co);
+// transpose = 1: data-gradient packing, flipped taps, GEMM K = co, N = ci.
+hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_out, int transpose, void *wpack,
+                               hipStream_t s);
+hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s);
+
+// ---- weight gradient -------------------------------------------------------
+enum { GB_DENSE = 0, GB_BNGRAD = 1, GB_POOLUP = 2 };
+struct WgradParams {
+    int dtype, k, n, h, w;
+    int64_t m;
+    int c_in, c_out;
+    const void *x;                // conv input view
+    int64_t x_ldc;
+    int a_mode;                   // 0: x as is, 1: relu(bn(x)) recomputed on load, 2: relu(x)
+    const float *a_gamma, *a_beta, *a_mean, *a_rstd;
+    int gsrc;                     // GB_*
+    const void *g;                // DENSE: [m][c_out] view; POOLUP: pooled gradient; BNGRAD: dy (dense)
+    int64_t g_ldc;
+    const void *gx;               // BNGRAD: BN input x view
+    int64_t gx_ldc;
+    const float *g_gamma, *g_mean, *g_rstd, *g_dgamma, *g_dbeta;
+    float *dw;                    // [k][k][c_in][c_out]
+    float *part;                  // workspace for split partial tiles
+};
+size_t wgrad_ws_bytes(int dtype, int64_t m, int c_in, int c_out, int k);
+hipError_t launch_wgrad(const WgradParams &p, hipStream_t s);
+
+}  // namespace bnr

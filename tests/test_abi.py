@@ -1,0 +1,105 @@
+"""Host-side checks of the C ABI (CPU only, no kernel launches): the library
+loads, exports every entry point that include/bnr.h declares, and rejects bad
+arguments with the documented status before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "bnr.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(bnr_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_1807_01702_amd import bnr
+    return bnr
+
+
+def test_exports_every_declared_symbol(B):
+    names = _declared()
+    assert len(names) >= 12, names
+    lib = ctypes.CDLL(B.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_status_strings(B):
+    for i, name in enumerate(B.STATUS):
+        assert B.status_string(i) == name
+
+
+def _desc(B, **kw):
+    d = dict(n=2, h=4, w=4, c_in=16, c_out=8, k=1, in_ldc=16, out_ldc=8, dtype=B.BNR_BF16)
+    d.update(kw)
+    return B.ConvDesc(**d)
+
+
+def test_workspace_sizes(B):
+    assert B.bnr_workspace_size(_desc(B)) > 0
+    assert B.bnr_workspace_size(_desc(B, k=5)) == 0
+    assert B.bnr_stats_workspace_size(100, 64) > 0
+    assert B.bnr_stats_workspace_size(0, 64) == 0
+
+
+# fake, 16-byte aligned, never dereferenced addresses (validation fails first)
+A = 0x10000
+WS = 0x100000
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=5), "BNR_ERR_UNSUPPORTED"),
+    (dict(n=0), "BNR_ERR_SHAPE"),
+    (dict(c_in=12), "BNR_ERR_ALIGN"),
+    (dict(in_ldc=8), "BNR_ERR_SHAPE"),
+    (dict(dtype=7), "BNR_ERR_DTYPE"),
+    (dict(k=3, w=65), "BNR_ERR_UNSUPPORTED"),
+])
+def test_conv_fwd_rejects_bad_descriptor(B, kw, status):
+    d = _desc(B, **kw)
+    bn = B.BNStruct(None, None, A, A, A, 1e-5)
+    r = B._lib_fns["bnr_conv_bn_stats_fwd"](ctypes.byref(d), A, A + 0x1000, A + 0x2000, ctypes.byref(bn), WS, 1 << 30, None)
+    assert B.STATUS[r] == status, B._lib_fns["bnr_last_error"]()
+
+
+def test_conv_fwd_rejects_pointers_workspace_alias(B):
+    d = _desc(B)
+    bn = B.BNStruct(None, None, A, A, A, 1e-5)
+    f = B._lib_fns["bnr_conv_bn_stats_fwd"]
+    assert B.STATUS[f(ctypes.byref(d), None, A, A + 0x2000, ctypes.byref(bn), WS, 1 << 30, None)] == "BNR_ERR_NULL"
+    assert B.STATUS[f(ctypes.byref(d), A + 8, A, A + 0x2000, ctypes.byref(bn), WS, 1 << 30, None)] == "BNR_ERR_ALIGN"
+    assert B.STATUS[f(ctypes.byref(d), A, A + 0x1000, A + 0x2000, ctypes.byref(bn), WS, 16, None)] == "BNR_ERR_WORKSPACE"
+    assert B.STATUS[f(ctypes.byref(d), A, A + 0x1000, A + 0x2000, ctypes.byref(bn), None, 0, None)] == "BNR_ERR_WORKSPACE"
+    assert B.STATUS[f(ctypes.byref(d), A, A + 0x1000, A + 0x40, ctypes.byref(bn), WS, 1 << 30, None)] == "BNR_ERR_ALIAS"
+    bad = B.BNStruct(None, None, A, A, A, 0.0)
+    assert B.STATUS[f(ctypes.byref(d), A, A + 0x1000, A + 0x2000, ctypes.byref(bad), WS, 1 << 30, None)] == "BNR_ERR_SHAPE"
+
+
+def test_other_entry_points_validate(B):
+    bn = B.BNStruct(A, A, A, A, A, 1e-5)
+    st = B._lib_fns["bnr_bn_stats"]
+    assert B.STATUS[st(0, 8, 8, B.BNR_BF16, A, ctypes.byref(bn), WS, 1 << 20, None)] == "BNR_ERR_SHAPE"
+    assert B.STATUS[st(10, 12, 16, B.BNR_BF16, A, ctypes.byref(bn), WS, 1 << 20, None)] == "BNR_ERR_ALIGN"
+    assert B.STATUS[st(10, 8, 8, B.BNR_BF16, A, None, WS, 1 << 20, None)] == "BNR_ERR_NULL"
+    d = _desc(B)
+    g = B.GradSrc(9, A, 8, None, None, 0, None, None, None)
+    r = B._lib_fns["bnr_bwd_fused"](ctypes.byref(d), A, ctypes.byref(bn), A, ctypes.byref(g), A, A, A, A, None, 0, 0,
+                                     WS, 1 << 30, None)
+    assert B.STATUS[r] == "BNR_ERR_UNSUPPORTED"
+    g = B.GradSrc(B.GRAD_DENSE, A + 0x4000, 8, None, None, 0, None, None, None)
+    r = B._lib_fns["bnr_bwd_fused"](ctypes.byref(d), A, None, A, ctypes.byref(g), A, None, None, None, None, 0, 0,
+                                     WS, 1 << 30, None)
+    assert B.STATUS[r] == "BNR_ERR_NULL"          # no BN and no dx
+    pool = B._lib_fns["bnr_avgpool2_fwd"]
+    assert B.STATUS[pool(1, 3, 4, 8, B.BNR_BF16, A, 8, A + 0x1000, None)] == "BNR_ERR_SHAPE"
+    assert B.STATUS[B._lib_fns["bnr_hbm_copy"](A, A + 0x1000, 24, None)] == "BNR_ERR_SHAPE"
+    assert B.STATUS[B._lib_fns["bnr_hbm_copy"](A, A + 0x8, 64, None)] == "BNR_ERR_ALIGN"
+    a = B.RefArgs()
+    assert B.STATUS[B._lib_fns["bnr_reference_path"](5, 0, ctypes.byref(d), ctypes.byref(a), WS, 1 << 30, None)] \
+        == "BNR_ERR_UNSUPPORTED"

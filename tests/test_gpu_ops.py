@@ -1,0 +1,248 @@
+"""Per-entry-point parity of the HIP path against the CPU oracle (GPU).
+
+Each test feeds identical seeded synthetic inputs to one C-ABI call and to
+the fp64 oracle, at sizes the oracle finishes in seconds that still span
+several tiles, a ragged pixel tail and channel counts that are not multiples
+of the tile.
+"""
+import numpy as np
+import pytest
+import torch
+
+from helpers import RTOL, assert_close, assert_stats, dev, f32dev, host, relu_ambiguous
+from oracle import prims as P
+from paper_1807_01702_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_1807_01702_amd import bnr
+    return bnr
+
+
+def _bn_dev(gamma, beta, eps=1e-5):
+    from paper_1807_01702_amd import bnr
+    return bnr.BN(f32dev(gamma), f32dev(beta), eps)
+
+
+# ------------------------------------------------------ standalone stats ----
+@pytest.mark.parametrize("m,c,ldc,bf16,shift", [
+    (512, 64, 64, False, 0.0),          # single-layer input, fp32
+    (6272, 256, 288, True, 0.0),        # bottleneck input view of a 288-channel buffer
+    (1, 8, 8, True, 0.0),               # one pixel: var = 0
+    (7, 24, 40, False, 0.0),            # ragged
+    (3001, 200, 256, True, 3.0),        # channel block tail, shifted mean
+    (20000, 64, 64, False, 30.0),       # |mean| / sigma = 30 (one-pass statistics precision)
+])
+def test_bn_stats(B, m, c, ldc, bf16, shift):
+    full = synth.normal(0, "stats", (m, ldc), bf16=bf16) + np.float32(shift)
+    full = synth.round_to_bf16(full) if bf16 else full
+    x = dev(full, bf16)
+    bn = B.BN.stats_only(c, x.device)
+    B.bnr_bn_stats(x[:, :c], bn)
+    torch.cuda.synchronize()
+    mean_r, var_r, rstd_r = P.bn_stats(full[:, :c].astype(np.float64), 1e-5)
+    if m == 1:
+        assert np.all(host(bn.var) == 0) and np.allclose(host(bn.mean), full[0, :c])
+        return
+    assert_stats("stats", host(bn.mean), host(bn.var), mean_r, var_r, RTOL[bf16])
+    np.testing.assert_allclose(host(bn.rstd), rstd_r, rtol=RTOL[bf16])
+
+
+# --------------------------------------------------------- fused forward ----
+FWD_CASES = [
+    # dtype, k, n, h, w, c_in, c_out, in_ldc, out_ldc
+    (False, 1, 8, 8, 8, 64, 32, 64, 32),         # single layer
+    (False, 3, 2, 5, 7, 12, 20, 16, 24),         # fp32 3x3, ragged
+    (True, 1, 2, 14, 14, 256, 128, 288, 128),    # bottleneck 1x1 on a concat view
+    (True, 3, 2, 14, 14, 128, 32, 128, 288),     # growth 3x3 into a concat slice
+    (True, 1, 1, 9, 11, 40, 136, 48, 136),       # ragged channels / pixels
+    (True, 3, 3, 1, 1, 64, 64, 64, 64),          # H = W = 1: only the centre tap
+    (True, 3, 1, 56, 56, 64, 64, 64, 64),        # full-width rows (W = 56)
+    (True, 3, 2, 6, 64, 32, 8, 32, 8),           # widest supported 3x3 rows
+]
+
+
+@pytest.mark.parametrize("case", FWD_CASES)
+@pytest.mark.parametrize("mode", ["bnrelu_stats", "bnrelu", "plain_stats"])
+def test_conv_fwd(B, case, mode):
+    bf16, k, n, h, w, ci, co, ildc, oldc = case
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    xf = synth.normal(1, "x", (n, h, w, ildc), bf16=bf16)
+    wt = synth.conv_weight(1, "w", k, ci, co, bf16)
+    bp = synth.bn_params(1, "bn", ci)
+    beta = bp["beta"] + (np.float32(2.0) if k == 3 else np.float32(0))   # large beta: padding semantics
+    x = dev(xf, bf16)
+    y = torch.zeros((n, h, w, oldc), dtype=x.dtype, device=x.device)
+    desc = B.desc_for(x[..., :ci], y[..., :co], k, n, h, w)
+    wd = dev(wt, bf16)
+    x64 = xf[..., :ci].astype(np.float64)
+    ybn = B.BN.stats_only(co, x.device)
+    if mode.startswith("bnrelu"):
+        xbn = _bn_dev(bp["gamma"], beta)
+        B.bnr_bn_stats(x[..., :ci], xbn)
+        B.bnr_bn_relu_conv_fwd(desc, x[..., :ci], xbn, wd, y[..., :co], ybn if mode.endswith("stats") else None)
+        yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], beta, 1e-5)
+        z = rnd(P.relu_fwd(yr))
+    else:
+        B.bnr_conv_bn_stats_fwd(desc, x[..., :ci], wd, y[..., :co], ybn)
+        z = x64
+    torch.cuda.synchronize()
+    out_r = rnd(P.conv_fwd(z, wt.astype(np.float64)))
+    assert_close("conv out", host(y[..., :co]), out_r, RTOL[bf16])
+    assert np.all(host(y[..., co:]) == 0), "wrote outside the output view"
+    if mode.endswith("stats"):
+        mr, vr, _ = P.bn_stats(out_r, 1e-5)
+        assert_stats("output stats", host(ybn.mean), host(ybn.var), mr, vr, RTOL[bf16])
+
+
+# -------------------------------------------------------- fused backward ----
+BWD_CASES = [
+    (False, 1, 8, 8, 8, 64, 32),
+    (False, 3, 2, 5, 6, 12, 20),
+    (True, 1, 2, 14, 14, 256, 128),
+    (True, 3, 2, 14, 14, 128, 32),
+    (True, 1, 1, 9, 11, 40, 136),
+    (True, 3, 3, 1, 1, 16, 24),
+    (True, 3, 1, 12, 56, 64, 64),
+]
+
+
+def _bwd_inputs(bf16, k, n, h, w, ci, co, seed=2):
+    xf = synth.normal(seed, "x", (n, h, w, ci), bf16=bf16)
+    wt = synth.conv_weight(seed, "w", k, ci, co, bf16)
+    bp = synth.bn_params(seed, "bn", ci)
+    g = synth.normal(seed, "g", (n, h, w, co), bf16=bf16)
+    return xf, wt, bp, g
+
+
+@pytest.mark.parametrize("case", BWD_CASES)
+@pytest.mark.parametrize("dxmode", ["none", "write", "accumulate"])
+def test_bwd_fused_dense(B, case, dxmode):
+    bf16, k, n, h, w, ci, co = case
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    xf, wt, bp, gf = _bwd_inputs(bf16, k, n, h, w, ci, co)
+    x, wd, g = dev(xf, bf16), dev(wt, bf16), dev(gf, bf16)
+    xbn = _bn_dev(bp["gamma"], bp["beta"])
+    B.bnr_bn_stats(x, xbn)
+    dw = torch.empty(wt.shape, dtype=torch.float32, device=x.device)
+    dgamma = torch.empty(ci, dtype=torch.float32, device=x.device)
+    dbeta = torch.empty_like(dgamma)
+    dy = torch.empty_like(x)
+    old = synth.normal(3, "old", (n, h, w, ci), bf16=bf16)
+    dx = dev(old, bf16) if dxmode != "none" else None
+    desc = B.desc_for(x, g, k, n, h, w)
+    B.bnr_bwd_fused(desc, x, xbn, wd, B.grad_dense(g), dw, dgamma, dbeta, dy, dx, dxmode == "accumulate")
+    torch.cuda.synchronize()
+    # oracle
+    x64 = xf.astype(np.float64)
+    yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    z = rnd(P.relu_fwd(yr))
+    dz = P.conv_dgrad(gf.astype(np.float64), wt.astype(np.float64), (h, w))
+    dyr = rnd(P.relu_bwd(dz, yr))
+    dwr = P.conv_wgrad(z, gf.astype(np.float64), k)
+    dxr, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd)
+    amb = relu_ambiguous(yr, bf16)
+    rt = RTOL[bf16]
+    assert_close("dy", host(dy), dyr, rt, exclude=amb)
+    assert_close("dW", host(dw), dwr, rt)
+    assert_close("dgamma", host(dgamma), dgr, rt)
+    assert_close("dbeta", host(dbeta), dbr, rt)
+    if dxmode == "write":
+        assert_close("dx", host(dx), rnd(dxr), rt, exclude=amb)
+    elif dxmode == "accumulate":
+        assert_close("dx (accumulated)", host(dx), rnd(old.astype(np.float64) + dxr), rt, exclude=amb)
+
+
+@pytest.mark.parametrize("case", [(False, 1, 8, 8, 8, 32, 64), (True, 1, 2, 14, 14, 128, 256),
+                                  (True, 3, 2, 10, 12, 64, 32), (True, 1, 1, 9, 11, 136, 40)])
+def test_bwd_fused_deferred_bn_gradient(B, case):
+    """Gradient source = the deferred input gradient of the next BN (the
+    next-prologue backward fusion)."""
+    bf16, k, n, h, w, ci, co = case
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    xf, wt, bp, _ = _bwd_inputs(bf16, k, n, h, w, ci, co, seed=4)
+    # the CONV output x2 feeds BN2, whose masked output gradient dy2 is known
+    x2f = synth.normal(4, "x2", (n, h, w, co), bf16=bf16) * np.float32(1.5) + np.float32(0.25)
+    x2f = synth.round_to_bf16(x2f) if bf16 else x2f
+    dy2f = synth.normal(4, "dy2", (n, h, w, co), bf16=bf16)
+    bp2 = synth.bn_params(4, "bn2", co)
+    x, wd, x2, dy2 = dev(xf, bf16), dev(wt, bf16), dev(x2f, bf16), dev(dy2f, bf16)
+    xbn, bn2 = _bn_dev(bp["gamma"], bp["beta"]), _bn_dev(bp2["gamma"], bp2["beta"])
+    B.bnr_bn_stats(x, xbn)
+    B.bnr_bn_stats(x2, bn2)
+    # dgamma2 / dbeta2 of BN2 from the oracle's own definition, uploaded as inputs
+    x2_64, dy2_64 = x2f.astype(np.float64), dy2f.astype(np.float64)
+    _, mu2, var2, rstd2 = P.bn_fwd(x2_64, bp2["gamma"], bp2["beta"], 1e-5)
+    _, dg2, db2 = P.bn_bwd(x2_64, dy2_64, bp2["gamma"], mu2, rstd2, want_dx=False)
+    dg2d, db2d = f32dev(dg2), f32dev(db2)
+    dw = torch.empty(wt.shape, dtype=torch.float32, device=x.device)
+    dgamma = torch.empty(ci, dtype=torch.float32, device=x.device)
+    dbeta = torch.empty_like(dgamma)
+    dy = torch.empty_like(x)
+    desc = B.desc_for(x, x2, k, n, h, w)
+    B.bnr_bwd_fused(desc, x, xbn, wd, B.grad_bn(dy2, x2, bn2, dg2d, db2d), dw, dgamma, dbeta, dy)
+    torch.cuda.synchronize()
+    g_r = rnd(P.bn_bwd(x2_64, dy2_64, bp2["gamma"], mu2, rstd2)[0])
+    x64 = xf.astype(np.float64)
+    yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    z = rnd(P.relu_fwd(yr))
+    dz = P.conv_dgrad(g_r, wt.astype(np.float64), (h, w))
+    dyr = rnd(P.relu_bwd(dz, yr))
+    dwr = P.conv_wgrad(z, g_r, k)
+    _, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd, want_dx=False)
+    rt = RTOL[bf16]
+    amb = relu_ambiguous(yr, bf16)
+    assert_close("dy", host(dy), dyr, rt, exclude=amb)
+    assert_close("dW", host(dw), dwr, rt)
+    assert_close("dgamma", host(dgamma), dgr, rt)
+    assert_close("dbeta", host(dbeta), dbr, rt)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_bwd_fused_pooled_gradient_plain_input(B, bf16):
+    """Transition-style backward: gradient from a 2x2 average pooling, and a
+    CONV without a BN in front (x_bn = NULL: dx = dz written and accumulated)."""
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    n, h, w, ci, co = 2, 8, 12, 64, 32
+    xf = synth.normal(5, "x", (n, h, w, ci), bf16=bf16)
+    wt = synth.conv_weight(5, "w", 1, ci, co, bf16)
+    gpf = synth.normal(5, "gp", (n, h // 2, w // 2, co), bf16=bf16)
+    old = synth.normal(5, "old", (n, h, w, ci), bf16=bf16)
+    x, wd, gp, dx = dev(xf, bf16), dev(wt, bf16), dev(gpf, bf16), dev(old, bf16)
+    dw = torch.empty(wt.shape, dtype=torch.float32, device=x.device)
+    desc = B.conv_desc(n, h, w, ci, co, 1, ci, co, B.dtype_code(x))
+    B.bnr_bwd_fused(desc, x, None, wd, B.grad_avgpool2(gp), dw, dx=dx, dx_accumulate=True)
+    torch.cuda.synchronize()
+    g_r = P.avgpool2_bwd(gpf.astype(np.float64), (h, w))
+    dz = P.conv_dgrad(g_r, wt.astype(np.float64), (h, w))
+    rt = RTOL[bf16]
+    assert_close("dx", host(dx), rnd(old.astype(np.float64) + dz), rt)
+    assert_close("dW", host(dw), P.conv_wgrad(xf.astype(np.float64), g_r, 1), rt)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_bn_dx_and_avgpool(B, bf16):
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    n, h, w, c, ldc = 3, 6, 10, 48, 64
+    xf = synth.normal(6, "x", (n, h, w, ldc), bf16=bf16)
+    dyf = synth.normal(6, "dy", (n, h, w, c), bf16=bf16)
+    bp = synth.bn_params(6, "bn", c)
+    x, dy = dev(xf, bf16), dev(dyf, bf16)
+    bn = _bn_dev(bp["gamma"], bp["beta"])
+    B.bnr_bn_stats(x[..., :c], bn)
+    x64 = xf[..., :c].astype(np.float64)
+    _, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    dxr, dg, db = P.bn_bwd(x64, dyf.astype(np.float64), bp["gamma"], mu, rstd)
+    G = torch.zeros((n, h, w, ldc), dtype=x.dtype, device=x.device)
+    B.bnr_bn_dx(dy, x[..., :c], bn, f32dev(dg), f32dev(db), G[..., :c])
+    B.bnr_bn_dx(dy, x[..., :c], bn, f32dev(dg), f32dev(db), G[..., :c], dx_accumulate=True)
+    pooled = torch.empty((n, h // 2, w // 2, c), dtype=x.dtype, device=x.device)
+    B.bnr_avgpool2_fwd(x[..., :c], pooled, n, h, w)
+    torch.cuda.synchronize()
+    rt = RTOL[bf16]
+    assert_close("dx twice", host(G[..., :c]), rnd(rnd(dxr) + dxr), rt)
+    assert np.all(host(G[..., c:]) == 0)
+    assert_close("avgpool", host(pooled), rnd(P.avgpool2_fwd(x64)), rt)
