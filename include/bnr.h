@@ -154,6 +154,12 @@ bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtyp
 
 /* ----------------------------------------------------- backward path ---- */
 
+/* Backward of bnr_avgpool2_fwd as a separate sweep (used by the unfused
+ * path): gx[n][y][x][c] = g[n][y/2][x/2][c] / 4, written to the view gx
+ * (pixel stride gx_ldc) from the dense pooled gradient g. */
+bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *g,
+                            void *gx, int32_t gx_ldc, void *stream);
+
 /* Backward of one BN-ReLU-CONV chain (or of a plain CONV when x_bn is NULL),
  * with the paper's backward fission/fusion (Sec. 3.2, Fig. 5b):
  *   1. dgrad: dz = conv_transpose(g, w), g from *g_src (prologue);

@@ -72,6 +72,8 @@ _lib_fns = dict(
                               _P(BNStruct), c_vp, c_sz, c_vp),
     bnr_avgpool2_fwd=_sig("bnr_avgpool2_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
                           c_vp, c_vp),
+    bnr_avgpool2_bwd=_sig("bnr_avgpool2_bwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_vp,
+                          c_i32, c_vp),
     bnr_bwd_fused=_sig("bnr_bwd_fused", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, _P(GradSrc), c_vp,
                        c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_sz, c_vp),
     bnr_bn_dx=_sig("bnr_bn_dx", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_vp, c_i32, _P(BNStruct), c_vp, c_vp,
@@ -216,6 +218,11 @@ def bnr_bn_relu_conv_fwd(desc, x, x_bn, w, y, y_bn=None):
 def bnr_avgpool2_fwd(x, y, n, h, w):
     p, m, c, ldc = view(x)
     _check(_lib_fns["bnr_avgpool2_fwd"](n, h, w, c, dtype_code(x), p, ldc, _ptr(y), _stream()))
+
+
+def bnr_avgpool2_bwd(g, gx, n, h, w):
+    pd, _, c, ldc = view(gx)
+    _check(_lib_fns["bnr_avgpool2_bwd"](n, h, w, c, dtype_code(gx), _ptr(g), pd, ldc, _stream()))
 
 
 def grad_dense(g):

@@ -1,0 +1,140 @@
+"""Algorithmic HBM bytes of one training step, fused vs unfused.
+
+"Algorithmic" = every kernel reads each of its input tensors once and writes
+each output once (halo re-reads, weight re-reads from cache and the tiny
+per-tile partial sums are not counted).  The unit of the model is the paper's
+"memory sweep": reading or writing one feature-map tensor over the whole
+mini-batch (Sec. 3.2, Fig. 5).  Per BN of C channels with S = m*C*bytes:
+
+  forward   unfused: CONV1 writes x, mean and variance sweeps read x, the
+                     normalisation reads x and writes y, ReLU reads y and writes
+                     z, CONV2 reads z                           -> 8 S
+            fused:   CONV1 writes x (statistics in its epilogue), CONV2 reads x
+                     (normalise + ReLU in its prologue)         -> 2 S
+  backward  unfused: CONV2 dgrad writes dz, wgrad reads z, ReLU backward reads
+                     dz, y and writes dy, the reductions read dy and x, the
+                     input gradient reads dy and x and writes dx, CONV1 dgrad and
+                     wgrad read dx                              -> 12 S
+            fused:   CONV2 dgrad reads x and writes dy (mask + sums in its
+                     epilogue), wgrad reads x, CONV1 dgrad and wgrad each read
+                     dy and x (deferred input gradient in their prologues)
+                                                                -> 7 S
+i.e. the backward restructuring removes 5 sweeps per BN, as the paper states.
+``sweeps_per_bn()`` returns these counts; ``for_workload()`` sums the exact
+byte traffic of each driver's kernel sequence.
+"""
+
+
+def sweeps_per_bn():
+    return {"fwd_unfused": 8, "fwd_fused": 2, "bwd_unfused": 12, "bwd_fused": 7}
+
+
+class _Acc:
+    def __init__(self):
+        self.total = 0
+
+    def __iadd__(self, v):
+        self.total += int(v)
+        return self
+
+
+def _unit_fused_fwd(a, m, ci, co, k, e, stats_sweep, out_stats=True):
+    if stats_sweep:
+        a += m * ci * e                       # standalone sub-BN1: one read sweep
+    a += m * ci * e + k * k * ci * co * e     # CONV reads x (normalise + ReLU on load) and weights
+    a += m * co * e                           # writes its output (statistics of it in the epilogue)
+
+
+def _unit_fused_bwd(a, m, ci, co, k, e, g_bytes, dx_mode):
+    """g_bytes: bytes of one read of the gradient source.  dx_mode: None
+    (deferred), 'write' or 'accumulate'."""
+    a += g_bytes + k * k * ci * co * e        # dgrad: gradient source, weights
+    a += m * ci * e + m * ci * e              # epilogue: read x, write dy
+    a += m * ci * e + g_bytes                 # wgrad: x (recomputed relu(bn(x))) and the gradient source
+    a += k * k * ci * co * 4                  # dW (fp32)
+    if dx_mode is not None:
+        a += 2 * m * ci * e + m * ci * e      # read dy, x; write dx
+        if dx_mode == "accumulate":
+            a += m * ci * e
+
+
+def _unit_ref_fwd(a, m, ci, co, k, e):
+    a += 2 * m * ci * e                       # mean sweep, variance sweep
+    a += 2 * m * ci * e                       # normalise: read x, write y
+    a += 2 * m * ci * e                       # ReLU: read y, write z
+    a += m * ci * e + k * k * ci * co * e + m * co * e   # CONV: read z, weights, write out
+
+
+def _unit_ref_bwd(a, m, ci, co, k, e, g_bytes, accumulate):
+    a += g_bytes + k * k * ci * co * e + m * ci * e      # dgrad: read g, weights, write dz
+    a += m * ci * e + g_bytes + k * k * ci * co * 4      # wgrad: read z, g, write dW
+    a += 3 * m * ci * e                                  # ReLU backward: read dz, y, write dy
+    a += 2 * m * ci * e                                  # reductions: read dy, x
+    a += 3 * m * ci * e + (m * ci * e if accumulate else 0)   # dx: read dy, x (+dx), write dx
+
+
+def single_layer(m, ci, co, e):
+    f, u = _Acc(), _Acc()
+    _unit_fused_fwd(f, m, ci, co, 1, e, True)
+    _unit_fused_bwd(f, m, ci, co, 1, e, m * co * e, "write")
+    _unit_ref_fwd(u, m, ci, co, 1, e)
+    _unit_ref_bwd(u, m, ci, co, 1, e, m * co * e, False)
+    return {"fused": f.total, "unfused": u.total}
+
+
+def bottleneck(m, ci, width, k, e):
+    f, u = _Acc(), _Acc()
+    ct = ci + k
+    for a in (f, u):
+        a += 2 * m * ct * e                   # G = dY (split backward starts from the upstream gradient)
+    _unit_fused_fwd(f, m, ci, width, 1, e, True)
+    _unit_fused_fwd(f, m, width, k, 3, e, False)
+    _unit_fused_bwd(f, m, width, k, 3, e, m * k * e, None)
+    _unit_fused_bwd(f, m, ci, width, 1, e, 2 * m * width * e, "accumulate")
+    _unit_ref_fwd(u, m, ci, width, 1, e)
+    _unit_ref_fwd(u, m, width, k, 3, e)
+    _unit_ref_bwd(u, m, width, k, 3, e, m * k * e, False)
+    _unit_ref_bwd(u, m, ci, width, 1, e, m * width * e, True)
+    return {"fused": f.total, "unfused": u.total}
+
+
+def dense_block(m, c0, layers, width, k, trans_out, e):
+    f, u = _Acc(), _Acc()
+    c = c0
+    for _ in range(layers):
+        _unit_fused_fwd(f, m, c, width, 1, e, True)
+        _unit_fused_fwd(f, m, width, k, 3, e, False)
+        _unit_ref_fwd(u, m, c, width, 1, e)
+        _unit_ref_fwd(u, m, width, k, 3, e)
+        c += k
+    ct = c
+    _unit_fused_fwd(f, m, ct, trans_out, 1, e, True)
+    _unit_ref_fwd(u, m, ct, trans_out, 1, e)
+    for a in (f, u):
+        a += m * trans_out * e + m // 4 * trans_out * e          # avgpool forward
+    # backward: transition first
+    _unit_fused_bwd(f, m, ct, trans_out, 1, e, m // 4 * trans_out * e, "write")
+    u += m // 4 * trans_out * e + m * trans_out * e              # unfused: materialised pooling gradient
+    _unit_ref_bwd(u, m, ct, trans_out, 1, e, m * trans_out * e, False)
+    for layer in reversed(range(layers)):
+        c = c0 + layer * k
+        _unit_fused_bwd(f, m, width, k, 3, e, m * k * e, None)
+        _unit_fused_bwd(f, m, c, width, 1, e, 2 * m * width * e, "accumulate")
+        _unit_ref_bwd(u, m, width, k, 3, e, m * k * e, False)
+        _unit_ref_bwd(u, m, c, width, 1, e, m * width * e, True)
+    return {"fused": f.total, "unfused": u.total}
+
+
+def for_workload(name, data):
+    e = 2 if data.get("bf16") else 4
+    if name == "single_layer":
+        n, h, w, ci = data["x"].shape
+        return single_layer(n * h * w, ci, data["w"].shape[3], e)
+    if name == "bottleneck":
+        n, h, w, ci = data["x"].shape
+        p = data["p"]
+        return bottleneck(n * h * w, ci, p["w1"].shape[3], p["w2"].shape[3], e)
+    n, h, w, c0 = data["x"].shape
+    cp = data["cpls"]
+    return dense_block(n * h * w, c0, len(cp), cp[0]["w1"].shape[3], cp[0]["w2"].shape[3],
+                       data["trans"]["w"].shape[3], e)

@@ -329,6 +329,23 @@ bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtyp
     return ok();
 }
 
+bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *g, void *gx,
+                            int32_t gx_ldc, void *stream)
+{
+    TRY(check_dtype(dtype));
+    if (n <= 0 || h <= 0 || w <= 0) return fail(BNR_ERR_SHAPE, "n, h, w must be positive");
+    if (h % 2 || w % 2) return fail(BNR_ERR_SHAPE, "h and w must be even");
+    TRY(check_channels(c, gx_ldc, dtype, "gx"));
+    TRY(check_ptr(g, "g"));
+    TRY(check_ptr(gx, "gx"));
+    const int es = esize(dtype);
+    const int64_t m = (int64_t)n * h * w;
+    if (overlap(view_range(gx, m, c, gx_ldc, es), view_range(g, m / 4, c, c, es)))
+        return fail(BNR_ERR_ALIAS, "gx overlaps g");
+    TRY_HIP(launch_avgpool2_bwd(dt_of(dtype), n, h, w, c, g, gx, gx_ldc, (hipStream_t)stream), "avgpool backward");
+    return ok();
+}
+
 bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
                          const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy, void *dx,
                          int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream)

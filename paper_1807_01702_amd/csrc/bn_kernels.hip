@@ -35,8 +35,10 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
     float s1[VEC], s2[VEC], mu[VEC], rs[VEC];
     for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f; }
-    if (ty < ry && (mode == 2 || mode == 3))
-        for (int i = 0; i < VEC; i++) { mu[i] = mean[c0 + i]; rs[i] = rstd[c0 + i]; }
+    if (ty < ry && (mode == ST_SQDEV || mode == ST_DYX))
+        for (int i = 0; i < VEC; i++) mu[i] = mean[c0 + i];
+    if (ty < ry && mode == ST_DYX)
+        for (int i = 0; i < VEC; i++) rs[i] = rstd[c0 + i];
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
     const int64_t r1 = min(m, r0 + rows_per_block);
     if (ty < ry) {
@@ -242,6 +244,30 @@ __global__ __launch_bounds__(kThreads) void k_avgpool2(int n, int h, int w, int 
     }
 }
 
+// Backward of the 2x2 pooling: every input pixel receives a quarter of its
+// window's gradient.  One thread per input 16-byte vector.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_avgpool2_bwd(int n, int h, int w, int C, const T *__restrict__ g,
+                                                           T *__restrict__ gx, int64_t ldc)
+{
+    constexpr int VEC = Elem<T>::VEC;
+    const int cvec = C / VEC;
+    const int64_t total = (int64_t)n * h * w * cvec;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < total; i += (int64_t)gridDim.x * kThreads) {
+        const int v = (int)(i % cvec);
+        const int64_t ip = i / cvec;
+        const int x = (int)(ip % w);
+        const int64_t t = ip / w;
+        const int y = (int)(t % h);
+        const int64_t nn = t / h;
+        const int64_t op = (nn * (h / 2) + y / 2) * (w / 2) + x / 2;
+        float f[VEC];
+        Elem<T>::unpack(ldg16(g + op * C + v * VEC), f);
+        for (int j = 0; j < VEC; j++) f[j] *= 0.25f;
+        stg16(gx + ip * ldc + v * VEC, Elem<T>::pack(f));
+    }
+}
+
 // --------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_copy16(const vec16 *__restrict__ src, vec16 *__restrict__ dst,
                                                      int64_t nvec)
@@ -273,6 +299,9 @@ hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m
                                 const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
                                 float *part, int64_t R, hipStream_t s)
 {
+    // operands each mode reads: refuse a launch that would dereference NULL
+    if (!x || !part || ((mode == ST_SQDEV || mode == ST_DYX) && !mean) || (mode == ST_DYX && (!rstd || !dy)))
+        return hipErrorInvalidValue;
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
     const int64_t rpb = ceil_div(m, R);
     dim3 grid((unsigned)R, (unsigned)cb);
@@ -288,6 +317,9 @@ hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m
 hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
                                  float *var, float *rstd, float *dbeta, float *dgamma, hipStream_t s)
 {
+    if (!part || (mode == FIN_MVF && (!mean || !rstd)) || (mode == FIN_MEAN && !mean) || (mode == FIN_VAR && !rstd) ||
+        (mode == FIN_BWD && (!dbeta || !dgamma)))
+        return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_stats_finalize, dim3((unsigned)ceil_div(C, 16)), dim3(kThreads), 0, s, part, R, C, m, mode,
                        eps, mean, var, rstd, dbeta, dgamma);
     return hipGetLastError();
@@ -298,6 +330,10 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
                               int64_t out_ldc, int accumulate, hipStream_t s)
 {
+    if (!x || !out || ((mode == EW_DX || mode == EW_RELUBWD) && !x2) ||
+        (mode == EW_DX && (!gamma || !rstd || !mean || !dgamma || !dbeta)) ||
+        (mode == EW_APPLY && (!gamma || !beta || !mean || !rstd)))
+        return hipErrorInvalidValue;
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
     const int64_t R = stats_row_blocks(m, C, dtype) * 2;
     const int64_t rpb = ceil_div(m, R);
@@ -323,6 +359,20 @@ hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x,
     else
         hipLaunchKernelGGL(k_avgpool2<float>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const float *)x, ldc,
                            (float *)y);
+    return hipGetLastError();
+}
+
+hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, void *gx, int64_t ldc,
+                               hipStream_t s)
+{
+    const int64_t total = (int64_t)n * h * w * (C / (dtype == DT_BF16 ? 8 : 4));
+    const int grid = grid_cap(ceil_div(total, kThreads));
+    if (dtype == DT_BF16)
+        hipLaunchKernelGGL(k_avgpool2_bwd<bf16_t>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const bf16_t *)g,
+                           (bf16_t *)gx, ldc);
+    else
+        hipLaunchKernelGGL(k_avgpool2_bwd<float>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const float *)g,
+                           (float *)gx, ldc);
     return hipGetLastError();
 }
 

@@ -352,8 +352,23 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     return hipGetLastError();
 }
 
+// Operands each prologue / epilogue mode reads must be present.
+static bool rows_operands_ok(const RowsParams &p)
+{
+    if (!p.a || !p.wpack || !p.y) return false;
+    if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return false;
+    if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd || !p.p_gamma || !p.p_dbeta || !p.p_dgamma))
+        return false;
+    if ((p.epi == EPI_STATS || p.epi == EPI_BNBWD) && !p.part) return false;
+    if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return false;
+    if (p.epi == EPI_RELUMASK && !p.ex) return false;
+    if (p.taps == 9 && p.w > kRowsMaxW3) return false;
+    return true;
+}
+
 hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s)
 {
+    if (!rows_operands_ok(p)) return hipErrorInvalidValue;
     const RowsTile t = rows_tile(p.dtype, p.taps, p.N);
     if (p.dtype == DT_BF16) {
         if (p.taps == 1) {

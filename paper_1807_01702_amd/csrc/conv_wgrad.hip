@@ -253,7 +253,13 @@ static hipError_t run_wgrad(const WgradParams &p, const WgradPlan &pl, hipStream
 
 hipError_t launch_wgrad(const WgradParams &p, hipStream_t s)
 {
+    if (!p.x || !p.g || !p.dw) return hipErrorInvalidValue;
+    if (p.a_mode == 1 && (!p.a_mean || !p.a_gamma || !p.a_rstd || !p.a_beta)) return hipErrorInvalidValue;
+    if (p.gsrc == GB_BNGRAD && (!p.gx || !p.g_mean || !p.g_rstd || !p.g_gamma || !p.g_dbeta || !p.g_dgamma))
+        return hipErrorInvalidValue;
+    if (p.k == 3 && p.w > kRowsMaxW3) return hipErrorInvalidValue;
     const WgradPlan pl = wgrad_plan(p.m, p.c_in, p.c_out, p.k, p.dtype == DT_BF16 ? 2 : 4);
+    if (pl.splits > 1 && !p.part) return hipErrorInvalidValue;
     hipError_t e;
     if (p.dtype == DT_BF16) {
         if (p.k == 1)

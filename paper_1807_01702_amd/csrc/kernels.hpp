@@ -23,6 +23,8 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
                               int64_t out_ldc, int accumulate, hipStream_t s);
 hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, hipStream_t s);
+hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, void *gx, int64_t ldc,
+                               hipStream_t s);
 hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s);
 hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, hipStream_t s);
 

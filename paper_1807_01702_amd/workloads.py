@@ -1,0 +1,264 @@
+"""Training-step drivers for the synthetic workloads, fused and unfused.
+
+Each driver owns its device buffers (allocated once), sequences C-ABI calls of
+``libbnr`` for one training step (forward + backward, no optimizer update) and
+exposes the results for parity checks.  ``fused=True`` runs the BN
+fission/fusion path (Sec. 3.2 of the paper); ``fused=False`` runs the same math
+through ``bnr_reference_path`` (the unfused BN -> ReLU -> CONV chain with
+materialised intermediates, Sec. 3.2 "before" picture).
+
+Workloads (shapes of the paper's DenseNet-121 / ResNet-50 training):
+* ``SingleLayer``  -- one BN-ReLU-CONV1x1 layer.
+* ``Bottleneck``   -- one DenseNet composite layer BN-ReLU-CONV1x1(4k)-BN-ReLU-
+                      CONV3x3(k) whose k new channels are concatenated (Sec. 2.3).
+* ``DenseBlock``   -- dense block 1 (6 composite layers, growth 32, width 128,
+                      64 -> 256 channels) + transition BN-ReLU-CONV1x1 + 2x2
+                      average pooling.  Concat is a channel-offset buffer
+                      (pointer passing, as the paper's reference does for
+                      Split); Split's backward is the accumulation of every
+                      reader's input gradient into that buffer's gradient.
+"""
+import numpy as np
+import torch
+
+from . import bnr as B
+
+MODE = B.MODE_BASELINE
+
+
+def _t(a, dev, bf16):
+    t = torch.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.float32))).to(dev)
+    return t.to(torch.bfloat16) if bf16 else t
+
+
+def _dense(flat, n, h, w, c):
+    """Dense [n, h, w, c] tensor on the front of a flat scratch buffer."""
+    return flat[:n * h * w * c].view(n, h, w, c)
+
+
+def _f32(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.float32))).to(dev)
+
+
+class _Grads:
+    def __init__(self, c, dev):
+        self.dgamma = torch.empty(c, dtype=torch.float32, device=dev)
+        self.dbeta = torch.empty(c, dtype=torch.float32, device=dev)
+
+
+class _Unit:
+    """One BN -> ReLU -> CONV chain on views x (BN input) -> out (CONV output)."""
+
+    def __init__(self, n, h, w, x, out, k, gamma, beta, wt, eps, dev, bf16, fused, ref_mode=MODE):
+        self.n, self.h, self.w, self.k = n, h, w, k
+        self.x, self.out = x, out
+        self.desc = B.desc_for(x, out, k, n, h, w)
+        self.bn = B.BN(_f32(gamma, dev), _f32(beta, dev), eps)
+        self.wt = _t(wt, dev, bf16)
+        ci, co = x.shape[-1], out.shape[-1]
+        self.dw = torch.empty(tuple(wt.shape), dtype=torch.float32, device=dev)
+        self.g = _Grads(ci, dev)
+        self.fused, self.ref_mode = fused, ref_mode
+        dt = torch.bfloat16 if bf16 else torch.float32
+        if not fused:   # materialised intermediates of the unfused chain, kept from forward to backward
+            self.y = torch.empty(x.shape[:-1] + (ci,), dtype=dt, device=dev)
+            self.z = torch.empty_like(self.y) if ref_mode == B.MODE_BASELINE else None
+
+    # unfused forward / backward through the reference path
+    def ref_fwd(self):
+        B.bnr_reference_path(self.ref_mode, False, self.desc, self.x, self.bn, self.wt, self.y, z=self.z,
+                             out=self.out)
+
+    def ref_bwd(self, g, dz, dy, dx, accumulate):
+        B.bnr_reference_path(self.ref_mode, True, self.desc, self.x, self.bn, self.wt, self.y, z=self.z, g=g,
+                             dz=dz if self.ref_mode == B.MODE_BASELINE else None, dy=dy, dw=self.dw,
+                             dgamma=self.g.dgamma, dbeta=self.g.dbeta, dx=dx, dx_accumulate=accumulate)
+
+
+class SingleLayer:
+    """BN-ReLU-CONV1x1 (fp32 by default): x [n,h,w,c_in] -> out [n,h,w,c_out],
+    upstream gradient dy of out given."""
+
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE):
+        bf16 = data["bf16"]
+        dev = torch.device(device)
+        n, h, w, ci = data["x"].shape
+        co = data["w"].shape[3]
+        self.x = _t(data["x"], dev, bf16)
+        self.out = torch.empty((n, h, w, co), dtype=self.x.dtype, device=dev)
+        self.gout = _t(data["dy"], dev, bf16)
+        self.u = _Unit(n, h, w, self.x, self.out, 1, data["gamma"], data["beta"], data["w"], data["eps"], dev, bf16,
+                       fused, ref_mode)
+        self.out_bn = B.BN.stats_only(co, dev, data["eps"])     # statistics of the CONV output (CONV-sub-BN1)
+        self.dy = torch.empty_like(self.x)
+        self.dx = torch.empty_like(self.x)
+        self.dz = torch.empty_like(self.x) if not fused else None
+        self.fused = fused
+        self.images = n
+
+    def forward(self):
+        u = self.u
+        if self.fused:
+            B.bnr_bn_stats(u.x, u.bn)
+            B.bnr_bn_relu_conv_fwd(u.desc, u.x, u.bn, u.wt, u.out, self.out_bn)
+        else:
+            u.ref_fwd()
+
+    def backward(self):
+        u = self.u
+        if self.fused:
+            B.bnr_bwd_fused(u.desc, u.x, u.bn, u.wt, B.grad_dense(self.gout), u.dw, u.g.dgamma, u.g.dbeta, self.dy,
+                            self.dx)
+        else:
+            u.ref_bwd(self.gout, self.dz, self.dy, self.dx, False)
+
+    def step(self):
+        self.forward()
+        self.backward()
+
+
+class Bottleneck:
+    """One DenseNet composite layer with concatenated output Y = [X, CPL(X)].
+    The upstream gradient dY covers all of Y; dX = dY[..., :c_in] + dx."""
+
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE):
+        bf16 = data["bf16"]
+        dev = torch.device(device)
+        p = data["p"]
+        n, h, w, ci = data["x"].shape
+        width, k = p["w1"].shape[3], p["w2"].shape[3]
+        dt = torch.bfloat16 if bf16 else torch.float32
+        self.n, self.h, self.w, self.ci, self.k = n, h, w, ci, k
+        self.buf = torch.empty((n, h, w, ci + k), dtype=dt, device=dev)
+        self.buf[..., :ci] = _t(data["x"], dev, bf16)
+        self.x1 = torch.empty((n, h, w, width), dtype=dt, device=dev)
+        eps = data["eps"]
+        self.u1 = _Unit(n, h, w, self.buf[..., :ci], self.x1, 1, p["gamma1"], p["beta1"], p["w1"], eps, dev, bf16,
+                        fused, ref_mode)
+        self.u2 = _Unit(n, h, w, self.x1, self.buf[..., ci:], 3, p["gamma2"], p["beta2"], p["w2"], eps, dev, bf16,
+                        fused, ref_mode)
+        self.dY = _t(data["dy"], dev, bf16)
+        self.G = torch.empty_like(self.dY)          # gradient of the concatenated buffer
+        self.dy1 = torch.empty((n, h, w, ci), dtype=dt, device=dev)
+        self.dy2 = torch.empty((n, h, w, width), dtype=dt, device=dev)
+        if not fused:
+            self.dz1 = torch.empty_like(self.dy1)
+            self.dz2 = torch.empty_like(self.dy2) if ref_mode == B.MODE_BASELINE else None
+            self.dx2 = torch.empty_like(self.dy2)
+        self.fused = fused
+        self.images = n
+
+    def forward(self):
+        if self.fused:
+            u1, u2 = self.u1, self.u2
+            B.bnr_bn_stats(u1.x, u1.bn)
+            B.bnr_bn_relu_conv_fwd(u1.desc, u1.x, u1.bn, u1.wt, u1.out, u2.bn)     # BN2 statistics in the epilogue
+            B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out)
+        else:
+            self.u1.ref_fwd()
+            self.u2.ref_fwd()
+
+    def backward(self):
+        B.bnr_hbm_copy(self.dY, self.G)             # Split backward starts from the upstream gradient
+        ci = self.ci
+        u1, u2 = self.u1, self.u2
+        if self.fused:
+            B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt, B.grad_dense(self.G[..., ci:]), u2.dw, u2.g.dgamma,
+                            u2.g.dbeta, self.dy2)
+            B.bnr_bwd_fused(u1.desc, u1.x, u1.bn, u1.wt,
+                            B.grad_bn(self.dy2, u2.x, u2.bn, u2.g.dgamma, u2.g.dbeta),
+                            u1.dw, u1.g.dgamma, u1.g.dbeta, self.dy1, self.G[..., :ci], dx_accumulate=True)
+        else:
+            u2.ref_bwd(self.G[..., ci:], self.dz2, self.dy2, self.dx2, False)
+            u1.ref_bwd(self.dx2, self.dz1, self.dy1, self.G[..., :ci], True)
+
+    def step(self):
+        self.forward()
+        self.backward()
+
+
+class DenseBlock:
+    """Dense block 1 of DenseNet-121 + transition layer.  Block buffer X holds
+    the block input in channels [0, c0) and composite layer l writes channels
+    [c0 + l*k, c0 + (l+1)*k).  Upstream gradient: dpool of the pooled output."""
+
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE):
+        bf16 = data["bf16"]
+        dev = torch.device(device)
+        dt = torch.bfloat16 if bf16 else torch.float32
+        n, h, w, c0 = data["x"].shape
+        ct = data["c_total"]
+        eps = data["eps"]
+        self.n, self.h, self.w, self.c0, self.ct = n, h, w, c0, ct
+        self.X = torch.zeros((n, h, w, ct), dtype=dt, device=dev)
+        self.X[..., :c0] = _t(data["x"], dev, bf16)
+        self.cpl = []
+        c_l = c0
+        width = data["cpls"][0]["w1"].shape[3]
+        for p in data["cpls"]:
+            k = p["w2"].shape[3]
+            x1 = torch.empty((n, h, w, width), dtype=dt, device=dev)
+            u1 = _Unit(n, h, w, self.X[..., :c_l], x1, 1, p["gamma1"], p["beta1"], p["w1"], eps, dev, bf16, fused,
+                       ref_mode)
+            u2 = _Unit(n, h, w, x1, self.X[..., c_l:c_l + k], 3, p["gamma2"], p["beta2"], p["w2"], eps, dev, bf16,
+                       fused, ref_mode)
+            self.cpl.append((c_l, k, u1, u2))
+            c_l += k
+        to = data["trans"]["w"].shape[3]
+        self.t = torch.empty((n, h, w, to), dtype=dt, device=dev)
+        self.ut = _Unit(n, h, w, self.X, self.t, 1, data["trans"]["gamma"], data["trans"]["beta"], data["trans"]["w"],
+                        eps, dev, bf16, fused, ref_mode)
+        self.pooled = torch.empty((n, h // 2, w // 2, to), dtype=dt, device=dev)
+        self.dpool = _t(data["dpool"], dev, bf16)
+        self.G = torch.empty((n, h, w, ct), dtype=dt, device=dev)
+        self.dy_t = torch.empty((n, h, w, ct), dtype=dt, device=dev)
+        self.dy1_flat = torch.empty(n * h * w * ct, dtype=dt, device=dev)    # dense [m][c_l] scratch, c_l < ct
+        self.dy2 = torch.empty((n, h, w, width), dtype=dt, device=dev)
+        if not fused:
+            self.dt = torch.empty_like(self.t)
+            self.dz_flat = torch.empty(n * h * w * max(ct, width), dtype=dt, device=dev)
+            self.dx2 = torch.empty_like(self.dy2)
+        self.fused = fused
+        self.images = n
+
+    def forward(self):
+        if self.fused:
+            for c_l, k, u1, u2 in self.cpl:
+                B.bnr_bn_stats(u1.x, u1.bn)                                    # sub-BN1 of a concat: own sweep
+                B.bnr_bn_relu_conv_fwd(u1.desc, u1.x, u1.bn, u1.wt, u1.out, u2.bn)
+                B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out)
+            ut = self.ut
+            B.bnr_bn_stats(ut.x, ut.bn)
+            B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
+        else:
+            for c_l, k, u1, u2 in self.cpl:
+                u1.ref_fwd()
+                u2.ref_fwd()
+            self.ut.ref_fwd()
+        B.bnr_avgpool2_fwd(self.t, self.pooled, self.n, self.h, self.w)
+
+    def backward(self):
+        ut = self.ut
+        n, h, w = self.n, self.h, self.w
+        if self.fused:
+            B.bnr_bwd_fused(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(self.dpool), ut.dw, ut.g.dgamma, ut.g.dbeta,
+                            self.dy_t, self.G)
+            for c_l, k, u1, u2 in reversed(self.cpl):
+                B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt, B.grad_dense(self.G[..., c_l:c_l + k]), u2.dw,
+                                u2.g.dgamma, u2.g.dbeta, self.dy2)
+                B.bnr_bwd_fused(u1.desc, u1.x, u1.bn, u1.wt,
+                                B.grad_bn(self.dy2, u2.x, u2.bn, u2.g.dgamma, u2.g.dbeta),
+                                u1.dw, u1.g.dgamma, u1.g.dbeta, _dense(self.dy1_flat, n, h, w, c_l),
+                                self.G[..., :c_l], dx_accumulate=True)
+        else:
+            B.bnr_avgpool2_bwd(self.dpool, self.dt, n, h, w)
+            ut.ref_bwd(self.dt, _dense(self.dz_flat, n, h, w, self.ct), self.dy_t, self.G, False)
+            for c_l, k, u1, u2 in reversed(self.cpl):
+                width = u2.x.shape[-1]
+                u2.ref_bwd(self.G[..., c_l:c_l + k], _dense(self.dz_flat, n, h, w, width), self.dy2, self.dx2, False)
+                u1.ref_bwd(self.dx2, _dense(self.dz_flat, n, h, w, c_l), _dense(self.dy1_flat, n, h, w, c_l),
+                           self.G[..., :c_l], True)
+
+    def step(self):
+        self.forward()
+        self.backward()
