@@ -123,8 +123,13 @@ bnr_status check_desc(const bnr_conv_desc *d)
 
 int64_t pixels(const bnr_conv_desc *d) { return (int64_t)d->n * d->h * d->w; }
 
-// workspace regions for the conv entry points
-struct ConvWs { size_t pack, part, wg, total; };
+// workspace regions for the conv entry points:
+//   pack  | packed weights (forward or data-gradient layout)
+//   part  | per-tile statistics partial sums [tiles][2][C]
+//   red   | statistics combine scratch (ticket counters + float64 level 1)
+//   wg    | weight-gradient split partial tiles
+//   wgred | split-K sum scratch
+struct ConvWs { size_t pack, part, red, wg, wgred, total; };
 ConvWs conv_ws(const bnr_conv_desc *d)
 {
     const int taps = d->k * d->k, dt = d->dtype == BNR_BF16 ? DT_BF16 : DT_F32;
@@ -137,17 +142,29 @@ ConvWs conv_ws(const bnr_conv_desc *d)
     size_t ss = (size_t)stats_row_blocks(m, d->c_in, dt) * 2 * d->c_in * 4;
     size_t part = sf > sb ? sf : sb;
     w.part = align_up(part > ss ? part : ss);
-    w.wg = align_up(wgrad_ws_bytes(dt, m, d->c_in, d->c_out, d->k));
-    w.total = w.pack + w.part + w.wg;
+    w.red = align_up(stats_red_bytes(d->c_in > d->c_out ? d->c_in : d->c_out));
+    w.wg = align_up(wgrad_ws_bytes(dt, m, d->n, d->h, d->w, d->c_in, d->c_out, d->k));
+    w.wgred = align_up(sum_partials_red_bytes((int64_t)d->k * d->k * d->c_in * d->c_out));
+    w.total = w.pack + w.part + w.red + w.wg + w.wgred;
     return w;
 }
 
-size_t stats_ws(int64_t m, int c)
+struct ConvPtrs { void *pack; float *part; void *red; float *wg; void *wgred; };
+ConvPtrs conv_ptrs(void *ws, const ConvWs &w)
+{
+    char *b = (char *)ws;
+    return ConvPtrs{b, (float *)(b + w.pack), b + w.pack + w.part, (float *)(b + w.pack + w.part + w.red),
+                    b + w.pack + w.part + w.red + w.wg};
+}
+
+size_t stats_part_bytes(int64_t m, int c)
 {
     size_t a = (size_t)stats_row_blocks(m, c, DT_BF16) * 2 * c * 4;
     size_t b = (size_t)stats_row_blocks(m, c, DT_F32) * 2 * c * 4;
     return align_up(a > b ? a : b);
 }
+
+size_t stats_ws(int64_t m, int c) { return stats_part_bytes(m, c) + align_up(stats_red_bytes(c)); }
 
 bnr_status check_ws(void *ws, size_t have, size_t need)
 {
@@ -161,13 +178,15 @@ bnr_status check_ws(void *ws, size_t have, size_t need)
 int dt_of(bnr_dtype d) { return d == BNR_BF16 ? DT_BF16 : DT_F32; }
 
 // statistics of a [m][c] view: partial sweep + float64 combine (MVF)
-bnr_status run_stats(int64_t m, int c, int ldc, bnr_dtype dt, const void *x, bnr_bn *bn, float *part,
-                     hipStream_t s)
+bnr_status run_stats(int64_t m, int c, int ldc, bnr_dtype dt, const void *x, bnr_bn *bn, void *ws, hipStream_t s)
 {
     const int64_t R = stats_row_blocks(m, c, dt_of(dt));
+    float *part = (float *)ws;
+    void *red = (char *)ws + stats_part_bytes(m, c);
     TRY_HIP(launch_stats_partial(dt_of(dt), x, ldc, m, c, ST_SUMSQ, nullptr, nullptr, nullptr, 0, part, R, s),
             "stats sweep");
-    TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MVF, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr, s),
+    TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MVF, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr, red,
+                                  s),
             "stats combine");
     return BNR_OK;
 }
@@ -229,9 +248,9 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     if (overlap(ry, rw)) return fail(BNR_ERR_ALIAS, "y overlaps w");
 
     hipStream_t s = (hipStream_t)stream;
-    char *base = (char *)ws;
-    void *wpack = base;
-    float *part = (float *)(base + cw.pack);
+    const ConvPtrs wp = conv_ptrs(ws, cw);
+    void *wpack = wp.pack;
+    float *part = wp.part;
     TRY_HIP(launch_pack_weights(dt_of(d->dtype), w, d->k, d->c_in, d->c_out, 0, wpack, s), "weight packing");
     RowsParams rp;
     fill_rows(rp, d, d->c_in, d->c_out);
@@ -246,7 +265,7 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     if (y_bn) {
         const int64_t R = rows_mtiles(rp.dtype, rp.taps, m, d->c_out);
         TRY_HIP(launch_stats_finalize(part, R, d->c_out, m, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
-                                      nullptr, nullptr, s),
+                                      nullptr, nullptr, wp.red, s),
                 "stats combine");
     }
     return ok();
@@ -295,7 +314,7 @@ bnr_status bnr_bn_stats(int64_t m, int32_t c, int32_t ldc, bnr_dtype dtype, cons
     TRY(check_ptr(x, "x"));
     TRY(check_bn(bn, "bn", false, true));
     TRY(check_ws(ws, ws_bytes, stats_ws(m, c)));
-    TRY(run_stats(m, c, ldc, dtype, x, bn, (float *)ws, (hipStream_t)stream));
+    TRY(run_stats(m, c, ldc, dtype, x, bn, ws, (hipStream_t)stream));
     return ok();
 }
 
@@ -380,10 +399,9 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     }
 
     hipStream_t s = (hipStream_t)stream;
-    char *base = (char *)ws;
-    void *wpack = base;
-    float *part = (float *)(base + cw.pack);
-    float *wgpart = (float *)(base + cw.pack + cw.part);
+    const ConvPtrs cp = conv_ptrs(ws, cw);
+    void *wpack = cp.pack;
+    float *part = cp.part;
     const int dt = dt_of(d->dtype);
 
     // 1. data gradient with the gradient-source prologue and the BN-backward epilogue
@@ -411,7 +429,8 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     // 2. dbeta = sum(dy), dgamma = sum(dy * xhat)
     if (x_bn) {
         const int64_t R = rows_mtiles(dt, rp.taps, m, d->c_in);
-        TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma, s),
+        TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma,
+                                      cp.red, s),
                 "backward sums combine");
     }
     // 3. weight gradient, both operands recomputed on load
@@ -433,7 +452,7 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     } else {
         wp.gsrc = GB_POOLUP; wp.g = g->g; wp.g_ldc = g->g_ldc;
     }
-    wp.dw = dw; wp.part = wgpart;
+    wp.dw = dw; wp.part = cp.wg; wp.red = cp.wgred;
     TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
     // 4. optional standalone BN input gradient
     if (x_bn && dx) {
@@ -490,10 +509,10 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
     const int es = esize(d->dtype);
     const int dt = dt_of(d->dtype);
     hipStream_t s = (hipStream_t)stream;
-    char *base_ws = (char *)ws;
-    void *wpack = base_ws;
-    float *part = (float *)(base_ws + cw.pack);
-    float *wgpart = (float *)(base_ws + cw.pack + cw.part);
+    const ConvPtrs cp = conv_ptrs(ws, cw);
+    void *wpack = cp.pack;
+    float *part = cp.part;
+    void *red = cp.red;
     const bnr_bn *bn = a->bn;
 
     if (!backward) {
@@ -505,17 +524,17 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
             TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUMSQ, nullptr, nullptr, nullptr, 0, part,
                                          R, s), "stats sweep");
             TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_MVF, bn->eps, bn->mean, bn->var, bn->rstd,
-                                          nullptr, nullptr, s), "stats combine");
+                                          nullptr, nullptr, red, s), "stats combine");
         } else {
             // mean sweep, then variance sweep (two-pass, as the unfused BN layer)
             TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUM, nullptr, nullptr, nullptr, 0, part,
                                          R, s), "mean sweep");
             TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_MEAN, bn->eps, bn->mean, nullptr, nullptr, nullptr,
-                                          nullptr, s), "mean combine");
+                                          nullptr, red, s), "mean combine");
             TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SQDEV, bn->mean, nullptr, nullptr, 0,
                                          part, R, s), "variance sweep");
             TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_VAR, bn->eps, nullptr, bn->var, bn->rstd, nullptr,
-                                          nullptr, s), "variance combine");
+                                          nullptr, red, s), "variance combine");
         }
         TRY_HIP(launch_elementwise(dt, EW_APPLY, m, d->c_in, a->x, d->in_ldc, nullptr, 0, bn->gamma, bn->beta,
                                    bn->mean, bn->rstd, nullptr, nullptr, a->y, d->c_in, 0, s), "normalise");
@@ -563,7 +582,7 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
     wp.c_in = d->c_in; wp.c_out = d->c_out;
     wp.x = base ? a->z : a->y; wp.x_ldc = d->c_in; wp.a_mode = base ? 0 : 2;
     wp.gsrc = GB_DENSE; wp.g = a->g; wp.g_ldc = a->g_ldc;
-    wp.dw = a->dw; wp.part = wgpart;
+    wp.dw = a->dw; wp.part = cp.wg; wp.red = cp.wgred;
     TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
     if (base)
         TRY_HIP(launch_elementwise(dt, EW_RELUBWD, m, d->c_in, a->dz, d->c_in, a->y, d->c_in, nullptr, nullptr, nullptr,
@@ -571,7 +590,8 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
     const int64_t R = stats_row_blocks(m, d->c_in, dt);
     TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_DYX, bn->mean, bn->rstd, a->dy, d->c_in, part, R,
                                  s), "BN backward sums sweep");
-    TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma, s),
+    TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma,
+                                  red, s),
             "BN backward sums combine");
     TRY_HIP(launch_elementwise(dt, EW_DX, m, d->c_in, a->dy, d->c_in, a->x, d->in_ldc, bn->gamma, nullptr, bn->mean,
                                bn->rstd, a->dgamma, a->dbeta, a->dx, a->dx_ldc, a->dx_accumulate ? 1 : 0, s),

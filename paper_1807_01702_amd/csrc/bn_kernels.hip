@@ -97,51 +97,76 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
 }
 
 // --------------------------------------------------------------------------
-// float64 combine of the partial tiles.  256 threads = 16 channels x 16
-// phases; phase j adds row blocks j, j+16, ...; then the phases are added.
+// float64 combine of the partial tiles, in two kernels (the kernel boundary
+// makes level 1 visible to level 2; no in-kernel fences).
+// Level 1, grid (C/64, RS): workgroup (cg, rs) adds row blocks
+// [rs*R/RS, (rs+1)*R/RS) of 64 channels (lane = channel, the 4 waves take
+// interleaved rows, 8 loads in flight per lane) into float64 sums lvl1[rs].
+__global__ __launch_bounds__(kThreads) void k_stats_combine1(const float *__restrict__ part, int64_t R, int C,
+                                                             double *__restrict__ lvl1)
+{
+    __shared__ double red[2][4][64];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int c = blockIdx.x * 64 + lane;
+    const int RS = gridDim.y, rs = blockIdx.y;
+    const int64_t r0 = rs * R / RS, r1 = (rs + 1) * R / RS;
+    double a = 0.0, b = 0.0;
+    if (c < C) {
+        const float *p = part + c;
+        for (int64_t r = r0 + wv; r < r1; r += 32) {
+            float va[8], vb[8];
+            for (int u = 0; u < 8; u++) {
+                const int64_t rr = r + 4 * u;
+                va[u] = rr < r1 ? p[rr * 2 * C] : 0.f;
+                vb[u] = rr < r1 ? p[rr * 2 * C + C] : 0.f;
+            }
+            for (int u = 0; u < 8; u++) { a += (double)va[u]; b += (double)vb[u]; }
+        }
+    }
+    red[0][wv][lane] = a;
+    red[1][wv][lane] = b;
+    __syncthreads();
+    if (wv == 0 && c < C) {
+        lvl1[((int64_t)rs * 2) * C + c] = red[0][0][lane] + red[0][1][lane] + red[0][2][lane] + red[0][3][lane];
+        lvl1[((int64_t)rs * 2 + 1) * C + c] = red[1][0][lane] + red[1][1][lane] + red[1][2][lane] + red[1][3][lane];
+    }
+}
+
+// Level 2: adds the RS level-1 sums of a channel in a fixed order
+// (deterministic) and writes
 //   FIN_MVF   : mean = s1/m, var = s2/m - mean^2 (clamped at 0), rstd
 //   FIN_MEAN  : mean = s1/m
 //   FIN_VAR   : var = s1/m, rstd            (two-pass variance)
 //   FIN_BWD   : dbeta = s1, dgamma = s2
-__global__ __launch_bounds__(kThreads) void k_stats_finalize(
-    const float *__restrict__ part, int64_t R, int C, int64_t m, int mode, float eps,
-    float *__restrict__ mean, float *__restrict__ var, float *__restrict__ rstd,
-    float *__restrict__ dbeta, float *__restrict__ dgamma)
+__global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__restrict__ lvl1, int RS, int C, int64_t m,
+                                                             int mode, float eps, float *__restrict__ mean,
+                                                             float *__restrict__ var, float *__restrict__ rstd,
+                                                             float *__restrict__ dbeta, float *__restrict__ dgamma)
 {
-    __shared__ double red[2][16][17];
-    const int tid = threadIdx.x, cl = tid % 16, ph = tid / 16;
-    const int c = blockIdx.x * 16 + cl;
+    const int c = blockIdx.x * kThreads + threadIdx.x;
+    if (c >= C) return;
     double a = 0.0, b = 0.0;
-    if (c < C) {
-        const float *p = part + c;
-        for (int64_t r = ph; r < R; r += 16) {
-            a += (double)p[r * 2 * C];
-            b += (double)p[r * 2 * C + C];
-        }
+    for (int j = 0; j < RS; j++) {
+        a += lvl1[((int64_t)j * 2) * C + c];
+        b += lvl1[((int64_t)j * 2 + 1) * C + c];
     }
-    red[0][ph][cl] = a;
-    red[1][ph][cl] = b;
-    __syncthreads();
-    if (ph == 0 && c < C) {
-        a = 0.0; b = 0.0;
-        for (int j = 0; j < 16; j++) { a += red[0][j][cl]; b += red[1][j][cl]; }
-        const double dm = (double)m;
-        if (mode == FIN_MVF) {
-            double mu = a / dm, v = b / dm - mu * mu;
-            if (v < 0.0) v = 0.0;
-            mean[c] = (float)mu;
-            if (var) var[c] = (float)v;
-            rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
-        } else if (mode == FIN_MEAN) {
-            mean[c] = (float)(a / dm);
-        } else if (mode == FIN_VAR) {
-            double v = a / dm;
-            if (var) var[c] = (float)v;
-            rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
-        } else {
-            dbeta[c] = (float)a;
-            dgamma[c] = (float)b;
-        }
+    const double dm = (double)m;
+    if (mode == FIN_MVF) {
+        const double mu = a / dm;
+        double v = b / dm - mu * mu;
+        if (v < 0.0) v = 0.0;
+        mean[c] = (float)mu;
+        if (var) var[c] = (float)v;
+        rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
+    } else if (mode == FIN_MEAN) {
+        mean[c] = (float)(a / dm);
+    } else if (mode == FIN_VAR) {
+        const double v = a / dm;
+        if (var) var[c] = (float)v;
+        rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
+    } else {
+        dbeta[c] = (float)a;
+        dgamma[c] = (float)b;
     }
 }
 
@@ -281,19 +306,58 @@ __global__ __launch_bounds__(kThreads) void k_copy16(const vec16 *__restrict__ s
     for (; i < nvec; i += stride) dst[i] = src[i];
 }
 
-// Sum of S float32 partial tiles in a fixed order (deterministic).
-__global__ __launch_bounds__(kThreads) void k_sum_partials(const float *__restrict__ part, int64_t S,
-                                                           int64_t len, float *__restrict__ out)
+// Sum of S float32 partial tiles, in two kernels.  Level 1, grid
+// (len/1024, SG): workgroup (i, g) adds splits [g*S/SG, (g+1)*S/SG) of 1024
+// outputs (a float4 per thread, 4 loads in flight); level 2 adds the SG
+// level-1 rows in a fixed order (deterministic).  With SG = 1 level 1 writes
+// the result directly.
+__global__ __launch_bounds__(kThreads) void k_sum_partials1(const float *__restrict__ part, int64_t S, int64_t len,
+                                                            float *__restrict__ dst)
 {
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < len; i += (int64_t)gridDim.x * kThreads) {
-        float s = 0.f;
-        for (int64_t j = 0; j < S; j++) s += part[j * len + i];
-        out[i] = s;
+    const int SG = gridDim.y, g = blockIdx.y;
+    const int64_t i4 = (int64_t)blockIdx.x * kThreads + threadIdx.x;     // float4 index
+    if (i4 * 4 >= len) return;
+    const int64_t s0 = g * S / SG, s1 = (g + 1) * S / SG;
+    const float4 *p = reinterpret_cast<const float4 *>(part) + i4;
+    const int64_t st = len / 4;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    int64_t s = s0;
+    for (; s + 3 < s1; s += 4) {
+        const float4 a = p[s * st], b = p[(s + 1) * st], c = p[(s + 2) * st], d = p[(s + 3) * st];
+        acc.x += a.x; acc.y += a.y; acc.z += a.z; acc.w += a.w;
+        acc.x += b.x; acc.y += b.y; acc.z += b.z; acc.w += b.w;
+        acc.x += c.x; acc.y += c.y; acc.z += c.z; acc.w += c.w;
+        acc.x += d.x; acc.y += d.y; acc.z += d.z; acc.w += d.w;
     }
+    for (; s < s1; s++) {
+        const float4 a = p[s * st];
+        acc.x += a.x; acc.y += a.y; acc.z += a.z; acc.w += a.w;
+    }
+    reinterpret_cast<float4 *>(dst)[(int64_t)g * st + i4] = acc;
+}
+
+__global__ __launch_bounds__(kThreads) void k_sum_partials2(const float *__restrict__ lvl1, int SG, int64_t len,
+                                                            float *__restrict__ out)
+{
+    const int64_t i4 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i4 * 4 >= len) return;
+    const int64_t st = len / 4;
+    float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int j = 0; j < SG; j++) {
+        const float4 a = reinterpret_cast<const float4 *>(lvl1)[(int64_t)j * st + i4];
+        t.x += a.x; t.y += a.y; t.z += a.z; t.w += a.w;
+    }
+    reinterpret_cast<float4 *>(out)[i4] = t;
 }
 
 // --------------------------------------------------------------- launchers --
 static inline int grid_cap(int64_t want) { return (int)(want < 4096 ? (want < 1 ? 1 : want) : 4096); }
+
+int stats_finalize_splits(int64_t R)
+{
+    int64_t rs = R / 64;
+    return (int)(rs < 1 ? 1 : (rs > kRedMaxRS ? kRedMaxRS : rs));
+}
 
 hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
                                 const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
@@ -314,14 +378,24 @@ hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m
     return hipGetLastError();
 }
 
-hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
-                                 float *var, float *rstd, float *dbeta, float *dgamma, hipStream_t s)
+int stats_combine_splits(int64_t R)
 {
-    if (!part || (mode == FIN_MVF && (!mean || !rstd)) || (mode == FIN_MEAN && !mean) || (mode == FIN_VAR && !rstd) ||
-        (mode == FIN_BWD && (!dbeta || !dgamma)))
+    int64_t rs = R / 64;
+    return (int)(rs < 1 ? 1 : (rs > kRedMaxRS ? kRedMaxRS : rs));
+}
+
+hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
+                                 float *var, float *rstd, float *dbeta, float *dgamma, void *red, hipStream_t s)
+{
+    if (!part || !red || (mode == FIN_MVF && (!mean || !rstd)) || (mode == FIN_MEAN && !mean) ||
+        (mode == FIN_VAR && !rstd) || (mode == FIN_BWD && (!dbeta || !dgamma)))
         return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_stats_finalize, dim3((unsigned)ceil_div(C, 16)), dim3(kThreads), 0, s, part, R, C, m, mode,
-                       eps, mean, var, rstd, dbeta, dgamma);
+    double *lvl1 = reinterpret_cast<double *>(red);
+    const int RS = stats_combine_splits(R);
+    hipLaunchKernelGGL(k_stats_combine1, dim3((unsigned)ceil_div(C, 64), (unsigned)RS), dim3(kThreads), 0, s, part, R,
+                       C, lvl1);
+    hipLaunchKernelGGL(k_stats_combine2, dim3((unsigned)ceil_div(C, kThreads)), dim3(kThreads), 0, s, lvl1, RS, C, m,
+                       mode, eps, mean, var, rstd, dbeta, dgamma);
     return hipGetLastError();
 }
 
@@ -382,9 +456,16 @@ hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s
     return hipGetLastError();
 }
 
-hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, hipStream_t s)
+int sum_partials_groups(int64_t S) { return (int)(S < 8 ? S : 8); }
+
+hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, void *red, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_sum_partials, dim3(grid_cap(ceil_div(len, kThreads))), dim3(kThreads), 0, s, part, S, len, out);
+    const int SG = sum_partials_groups(S);
+    if (!part || !out || (len % 4) || (SG > 1 && !red)) return hipErrorInvalidValue;
+    const unsigned gx = (unsigned)ceil_div(len, 4 * kThreads);
+    float *lvl1 = SG > 1 ? reinterpret_cast<float *>(red) : out;
+    hipLaunchKernelGGL(k_sum_partials1, dim3(gx, (unsigned)SG), dim3(kThreads), 0, s, part, S, len, lvl1);
+    if (SG > 1) hipLaunchKernelGGL(k_sum_partials2, dim3(gx), dim3(kThreads), 0, s, lvl1, SG, len, out);
     return hipGetLastError();
 }
 

@@ -69,13 +69,14 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // Logical workgroup index for XCD-aware scheduling.  The dispatcher hands
 // consecutive workgroup ids round-robin to the 8 XCDs (each with its own L2);
-// this remap makes logically consecutive tiles land on the same XCD so that
-// data they share (halo rows, re-read operands) hits in that XCD's L2.
+// this bijective remap gives every XCD a contiguous range of logical ids, so
+// logically neighbouring tiles (halo rows, operands re-read by several output
+// tiles) land on the same XCD and share its L2.
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     const int X = 8;
-    if (nblocks % X) return bid;             // keep identity when not divisible
-    int per = nblocks / X;
-    return (bid % X) * per + bid / X;
+    const int q = nblocks / X, r = nblocks % X;
+    const int x = bid % X, k = bid / X;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + k;
 }
 
 }  // namespace bnr

@@ -1,22 +1,27 @@
 // conv_wgrad.hip -- CONV weight gradient on the gfx950 matrix cores with the
 // fission/fusion prologues on both operands.
 //
-//   dW[kh][kw][ci][co] = sum over pixels q of Z[q][ci] * G[q - off][co] * valid
+//   dW[kh][kw][ci][co] = sum over pixels q of Z[q][ci] * G[q - off][co]
 //
-// with off = (kh-1)*W + (kw-1) for 3x3 (0 for 1x1): the tap shift is applied
-// to the gradient operand, so the Z operand is read unshifted.  valid is 1 when
-// pixel q - off is the in-image neighbour of q for that tap (zero padding).
-// Z is relu(bn(x)) recomputed from x (sub-BN2 recomputation, no stored
-// activation), or x itself; G is a dense gradient, the deferred BN input
-// gradient k*(dy - a - xhat*b) formed from (dy, x) on the fly, or the
-// average-pooling gradient formed from the pooled gradient.
+// Z is relu(bn(x)) recomputed from x on load (no stored activation), relu(x)
+// or x itself; G is a dense gradient, the deferred BN input gradient
+// k*(dy - a - xhat*b) formed from (dy, x) on load, or the 2x2 average-pooling
+// gradient formed from the pooled gradient.  For 3x3 the tap shift is applied
+// to G, so Z is read unshifted.
 //
-// GEMM view: M = 64 input channels (one 16-row block per wave) x taps of one
-// filter row, N = output channels, K = pixels.  Pixels come in chunks of 64,
-// staged transposed in LDS (channel-major, pixel-contiguous) so that a lane's
-// 8 consecutive k values are one 16-byte read.  The pixel range is split S
-// ways; each split writes a float32 partial tile and a fixed-order sum
-// produces dW (deterministic).
+// GEMM view: M = 64 input channels x taps, N = output channels, K = pixels.
+// K comes in chunks of 64 positions staged transposed in LDS (channel-major,
+// pixel-contiguous) so that a lane's 8 consecutive k values are one 16-byte
+// read.  3x3 chunks are R whole image rows in a zero-padded layout (one zero
+// column on the left, zeros up to the padded width PW).  A workgroup owns one
+// filter row kh, so the G operand of a chunk is the same R rows shifted by
+// dh = kh - 1 (zero outside the image), laid out the same way: tap kw then
+// reads G at offset 1 - kw from the Z position, out-of-image neighbours read
+// the zeros, and only kw = 0 / 2 need a 2-byte realignment (four alignbyte
+// ops on five dword reads).
+// The next chunk's global loads are issued before the current chunk's matrix
+// work.  S pixel splits write float32 partial tiles; a fixed-order sum gives
+// dW (deterministic).
 #include "common.hpp"
 #include "kernels.hpp"
 #include "mfma.hpp"
@@ -24,44 +29,104 @@
 
 namespace bnr {
 
-template <typename T, int TPW, int COT>
+template <typename T, int TAPS, int COT>
 struct WgCfg {
     static constexpr int VEC = Elem<T>::VEC;
     static constexpr int PAD = 16 / (int)sizeof(T);
-    static constexpr int ZSTR = kWgBKP + PAD;
-    static constexpr int HALO_MAX = TPW == 3 ? kRowsMaxW3 + 1 : 0;
-    static constexpr int GCOLS = kWgBKP + 2 * HALO_MAX;
-    static constexpr int GSTR = GCOLS + PAD;
-    static constexpr size_t Z_BYTES = (size_t)kWgCIT * ZSTR * sizeof(T);
-    static constexpr size_t G_BYTES = (size_t)COT * GSTR * sizeof(T);
+    static constexpr int ZSTR = kWgKC + PAD;
+    static constexpr int GOFF = 8;                                    // zero guard in front of a G row
+    static constexpr int GCOLS = kWgKC;                               // R * PW = 64
+    static constexpr int GSTR = GOFF + GCOLS + 8 + PAD;
+    static constexpr int ZITEMS = (kWgKC / 2) * (kWgCIT / VEC);       // pixel pairs x vectors
+    static constexpr int GITEMS = (GCOLS / 2) * (COT / VEC);
+    static constexpr int ZI = (ZITEMS + kThreads - 1) / kThreads;
+    static constexpr int GI = (GITEMS + kThreads - 1) / kThreads;
 };
 
-template <typename T, int TPW, int COT>
-__global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, int ci_tiles, int kh_tiles, int co_tiles,
-                                                   int64_t chunks_per_split, int64_t nchunks, int splits)
+// 8 consecutive storage elements starting at element s of an LDS row whose
+// base is 16-byte aligned; s % 8 is the same for every lane of the call.
+template <typename T> struct Shifted;
+template <> struct Shifted<bf16_t> {
+    __device__ static __forceinline__ bf16x8 load(const bf16_t *row, int s) {
+        if ((s & 7) == 0) return Mfma<bf16_t>::load(row + s);
+        uint32_t w[4];
+        if ((s & 1) == 0) {
+            const uint32_t *p = reinterpret_cast<const uint32_t *>(row + s);
+            for (int i = 0; i < 4; i++) w[i] = p[i];
+        } else {
+            const uint32_t *p = reinterpret_cast<const uint32_t *>(row + s - 1);
+            uint32_t v[5];
+            for (int i = 0; i < 5; i++) v[i] = p[i];
+            for (int i = 0; i < 4; i++) w[i] = __builtin_amdgcn_alignbyte(v[i + 1], v[i], 2);
+        }
+        return Mfma<bf16_t>::from_words(w);
+    }
+};
+template <> struct Shifted<float> {
+    __device__ static __forceinline__ float load(const float *row, int s) { return row[s]; }
+};
+
+// two pixels' values of one channel -> one LDS store
+template <typename T> __device__ __forceinline__ void st_pair(T *dst, float a, float b);
+template <> __device__ __forceinline__ void st_pair<bf16_t>(bf16_t *dst, float a, float b) {
+    *reinterpret_cast<uint32_t *>(dst) = pack2bf(a, b);
+}
+template <> __device__ __forceinline__ void st_pair<float>(float *dst, float a, float b) {
+    *reinterpret_cast<float2 *>(dst) = make_float2(a, b);
+}
+
+// K position of a chunk -> pixel index (or -1: a zero position)
+struct ChunkGeo {
+    int taps, H, W, R, PW;
+    int64_t m, q0;     // 1x1: first pixel of the chunk
+    int64_t img;       // 3x3: image of the chunk
+    int h0;            // 3x3: first image row of the chunk
+    __device__ int64_t zpix(int kp) const {
+        if (taps == 1) {
+            const int64_t q = q0 + kp;
+            return q < m ? q : -1;
+        }
+        const int r = kp / PW, c = kp - r * PW;
+        const int h = h0 + r;
+        if (r >= R || h >= H || c < 1 || c > W) return -1;
+        return (img * H + h) * W + (c - 1);
+    }
+    // G position (row r of the chunk, column c) -> pixel (h0 + r - dh, c - 1) or -1
+    __device__ int64_t gpix(int gp, int dh) const {
+        if (taps == 1) return zpix(gp);
+        const int r = gp / PW, c = gp - r * PW;
+        const int h = h0 + r - dh;
+        if (r >= R || h < 0 || h >= H || c < 1 || c > W) return -1;
+        return (img * H + h) * W + (c - 1);
+    }
+};
+
+template <typename T, int TAPS, int COT, int WR, int WC>
+__global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
 {
-    using Cfg = WgCfg<T, TPW, COT>;
+    using Cfg = WgCfg<T, TAPS, COT>;
     using M = Mfma<T>;
-    constexpr int VEC = Cfg::VEC, ZSTR = Cfg::ZSTR, GSTR = Cfg::GSTR;
-    constexpr int TN = COT / 16;
+    constexpr int VEC = Cfg::VEC, ZSTR = Cfg::ZSTR, GSTR = Cfg::GSTR, GOFF = Cfg::GOFF;
+    constexpr int RB = kWgCIT / 16 / WR;      // 16-row blocks of ci per wave
+    constexpr int CB = COT / 16 / WC;         // 16-column blocks of co per wave
+    static_assert(WR * WC == 4, "four waves");
     __shared__ __align__(16) T Zt[kWgCIT * ZSTR];
     __shared__ __align__(16) T Gt[COT * GSTR];
-    __shared__ uint8_t flags[kWgBKP];
     __shared__ float zc[3][kWgCIT];
     __shared__ float gc[5][COT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int n_out = ci_tiles * kh_tiles * co_tiles;
+    const int wr = wave / WC, wc = wave % WC;
+    const int n_out = pl.ci_tiles * pl.kh_tiles * pl.co_tiles;
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
     const int ot = lid % n_out, split = lid / n_out;
-    const int co_t = ot % co_tiles, kh_t = (ot / co_tiles) % kh_tiles, ci_t = ot / (co_tiles * kh_tiles);
+    const int co_t = ot % pl.co_tiles, kh_t = (ot / pl.co_tiles) % pl.kh_tiles, ci_t = ot / (pl.co_tiles * pl.kh_tiles);
     const int ci0 = ci_t * kWgCIT, co0 = co_t * COT;
-    const int H = p.h, W = p.w, C_in = p.c_in, C_out = p.c_out;
+    const int C_in = p.c_in, C_out = p.c_out;
     const int64_t m = p.m;
-    const int halo = TPW == 3 ? W + 1 : 0;
-    const int dh = TPW == 3 ? kh_t - 1 : 0;
+    const int gcols = kWgKC;
+    const int dh = TAPS == 3 ? kh_t - 1 : 0;
 
-    // operand prologue coefficients for this tile's channels
     if (tid < kWgCIT) {
         const int c = ci0 + tid;
         if (p.a_mode == 1 && c < C_in) {
@@ -81,139 +146,139 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, int ci_tiles,
             gc[4][tid] = p.g_dgamma[c] * inv_m;
         }
     }
+    // zero the G guards and the columns beyond gcols once; staging never writes them
+    for (int i = tid; i < COT * GSTR; i += kThreads) {
+        const int col = i % GSTR;
+        if (col < GOFF || col >= GOFF + gcols) Gt[i] = T(0);
+    }
 
-    f32x4 acc[TPW][TN];
-    for (int t = 0; t < TPW; t++)
-        for (int cb = 0; cb < TN; cb++) acc[t][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[TAPS][RB][CB];
+    for (int t = 0; t < TAPS; t++)
+        for (int rb = 0; rb < RB; rb++)
+            for (int cb = 0; cb < CB; cb++) acc[t][rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const T *xs = reinterpret_cast<const T *>(p.x);
     const T *gs = reinterpret_cast<const T *>(p.g);
     const T *gxs = reinterpret_cast<const T *>(p.gx);
-    const int64_t ch_begin = (int64_t)split * chunks_per_split;
-    const int64_t ch_end = min(nchunks, ch_begin + chunks_per_split);
-    const int gcols = kWgBKP + 2 * halo;
-    __syncthreads();
+    const int64_t ch_begin = (int64_t)split * pl.chunks_per_split;
+    const int64_t ch_end = min(pl.nchunks, ch_begin + pl.chunks_per_split);
+    const int zitems = Cfg::ZITEMS;
+    const int gitems = (gcols / 2) * (COT / VEC);
 
+    // ---- register stage of one chunk (raw loads; transforms at LDS store) ----
+    vec16 zr[Cfg::ZI][2], gr[Cfg::GI][2], gx[Cfg::GI][2];
+    auto geo_of = [&](int64_t ch) {
+        ChunkGeo g;
+        g.taps = TAPS; g.H = p.h; g.W = p.w; g.R = pl.R; g.PW = pl.PW; g.m = m;
+        if (TAPS == 1) { g.q0 = ch * kWgKC; g.img = 0; g.h0 = 0; }
+        else {
+            g.q0 = 0;
+            g.img = ch / pl.chunks_per_image;
+            g.h0 = (int)(ch - g.img * pl.chunks_per_image) * pl.R;
+        }
+        return g;
+    };
+    auto load_chunk = [&](int64_t ch) {
+        const ChunkGeo g = geo_of(ch);
+        for (int j = 0; j < Cfg::ZI; j++) {
+            const int i = tid + j * kThreads;
+            const int v = i % (kWgCIT / VEC), pr = i / (kWgCIT / VEC);
+            const int c = ci0 + v * VEC;
+            for (int h2 = 0; h2 < 2; h2++) {
+                const int64_t q = i < zitems ? g.zpix(2 * pr + h2) : -1;
+                zr[j][h2] = (q >= 0 && c < C_in) ? ldg16(xs + q * p.x_ldc + c) : zero16();
+            }
+        }
+        for (int j = 0; j < Cfg::GI; j++) {
+            const int i = tid + j * kThreads;
+            const int v = i % (COT / VEC), pr = i / (COT / VEC);
+            const int c = co0 + v * VEC;
+            for (int h2 = 0; h2 < 2; h2++) {
+                const int64_t q = i < gitems ? g.gpix(2 * pr + h2, dh) : -1;
+                vec16 a = zero16(), b = zero16();
+                if (q >= 0 && c < C_out) {
+                    if (p.gsrc == GB_DENSE) {
+                        a = ldg16(gs + q * p.g_ldc + c);
+                    } else if (p.gsrc == GB_BNGRAD) {
+                        a = ldg16(gs + q * p.g_ldc + c);
+                        b = ldg16(gxs + q * p.gx_ldc + c);
+                    } else {
+                        const int64_t img = q / ((int64_t)p.h * p.w);
+                        const int rem = (int)(q - img * p.h * p.w);
+                        const int y = rem / p.w, xx = rem - y * p.w;
+                        const int64_t qq = (img * (p.h / 2) + y / 2) * (p.w / 2) + xx / 2;
+                        a = ldg16(gs + qq * p.g_ldc + c);
+                    }
+                }
+                gr[j][h2] = a;
+                gx[j][h2] = b;
+            }
+        }
+    };
+    auto store_chunk = [&](int64_t ch) {
+        const ChunkGeo g = geo_of(ch);
+        for (int j = 0; j < Cfg::ZI; j++) {
+            const int i = tid + j * kThreads;
+            if (i >= zitems) break;
+            const int v = i % (kWgCIT / VEC), pr = i / (kWgCIT / VEC);
+            const int cl = v * VEC;
+            float f[2][VEC];
+            for (int h2 = 0; h2 < 2; h2++) {
+                Elem<T>::unpack(zr[j][h2], f[h2]);
+                const bool valid = g.zpix(2 * pr + h2) >= 0 && ci0 + cl < C_in;
+                if (p.a_mode == 1)
+                    for (int e = 0; e < VEC; e++) {
+                        const float t = (f[h2][e] - zc[0][cl + e]) * zc[1][cl + e] + zc[2][cl + e];
+                        f[h2][e] = valid && t > 0.f ? t : 0.f;
+                    }
+                else if (p.a_mode == 2)
+                    for (int e = 0; e < VEC; e++) f[h2][e] = f[h2][e] > 0.f ? f[h2][e] : 0.f;
+            }
+            for (int e = 0; e < VEC; e++) st_pair<T>(Zt + (cl + e) * ZSTR + 2 * pr, f[0][e], f[1][e]);
+        }
+        for (int j = 0; j < Cfg::GI; j++) {
+            const int i = tid + j * kThreads;
+            if (i >= gitems) break;
+            const int v = i % (COT / VEC), pr = i / (COT / VEC);
+            const int cl = v * VEC;
+            float f[2][VEC];
+            for (int h2 = 0; h2 < 2; h2++) {
+                Elem<T>::unpack(gr[j][h2], f[h2]);
+                if (p.gsrc == GB_BNGRAD) {
+                    const bool valid = g.gpix(2 * pr + h2, dh) >= 0 && co0 + cl < C_out;
+                    float x[VEC];
+                    Elem<T>::unpack(gx[j][h2], x);
+                    for (int e = 0; e < VEC; e++) {
+                        const float xh = (x[e] - gc[0][cl + e]) * gc[1][cl + e];
+                        const float d = gc[2][cl + e] * (f[h2][e] - gc[3][cl + e] - xh * gc[4][cl + e]);
+                        f[h2][e] = valid ? d : 0.f;
+                    }
+                } else if (p.gsrc == GB_POOLUP) {
+                    for (int e = 0; e < VEC; e++) f[h2][e] *= 0.25f;
+                }
+            }
+            for (int e = 0; e < VEC; e++) st_pair<T>(Gt + (cl + e) * GSTR + GOFF + 2 * pr, f[0][e], f[1][e]);
+        }
+    };
+
+    if (ch_begin < ch_end) load_chunk(ch_begin);
+    __syncthreads();
     for (int64_t ch = ch_begin; ch < ch_end; ch++) {
-        const int64_t q0 = ch * kWgBKP;
-        // ---- stage Z^T: 64 channels x 64 pixels, two pixels per item ----
-        {
-            constexpr int VPP = kWgCIT / VEC;                 // vectors per pixel
-            constexpr int ITEMS = (kWgBKP / 2) * VPP;
-            for (int i = tid; i < ITEMS; i += kThreads) {
-                const int v = i % VPP, pr = i / VPP;
-                const int cl = v * VEC, c = ci0 + cl;
-                float f0[VEC], f1[VEC];
-                for (int h2 = 0; h2 < 2; h2++) {
-                    float *f = h2 ? f1 : f0;
-                    const int64_t q = q0 + 2 * pr + h2;
-                    if (q < m && c < C_in) {
-                        Elem<T>::unpack(ldg16(xs + q * p.x_ldc + c), f);
-                        if (p.a_mode == 1)
-                            for (int e = 0; e < VEC; e++) {
-                                const float t = (f[e] - zc[0][cl + e]) * zc[1][cl + e] + zc[2][cl + e];
-                                f[e] = Elem<T>::round(t > 0.f ? t : 0.f);
-                            }
-                        else if (p.a_mode == 2)
-                            for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
-                    } else {
-                        for (int e = 0; e < VEC; e++) f[e] = 0.f;
-                    }
-                }
-                for (int e = 0; e < VEC; e++) {
-                    T *dst = Zt + (cl + e) * ZSTR + 2 * pr;
-                    dst[0] = to_store<T>(f0[e]);
-                    dst[1] = to_store<T>(f1[e]);
-                }
-            }
-        }
-        // ---- stage G^T with the tap halo: COT channels x gcols pixels ----
-        {
-            constexpr int VPP = COT / VEC;
-            const int items = (gcols / 2) * VPP;
-            for (int i = tid; i < items; i += kThreads) {
-                const int v = i % VPP, pr = i / VPP;
-                const int cl = v * VEC, c = co0 + cl;
-                float f0[VEC], f1[VEC];
-                for (int h2 = 0; h2 < 2; h2++) {
-                    float *f = h2 ? f1 : f0;
-                    const int64_t q = q0 - halo + 2 * pr + h2;
-                    if (q >= 0 && q < m && c < C_out) {
-                        if (p.gsrc == GB_DENSE) {
-                            Elem<T>::unpack(ldg16(gs + q * p.g_ldc + c), f);
-                        } else if (p.gsrc == GB_BNGRAD) {
-                            float x[VEC];
-                            Elem<T>::unpack(ldg16(gs + q * p.g_ldc + c), f);
-                            Elem<T>::unpack(ldg16(gxs + q * p.gx_ldc + c), x);
-                            for (int e = 0; e < VEC; e++) {
-                                const float xh = (x[e] - gc[0][cl + e]) * gc[1][cl + e];
-                                f[e] = Elem<T>::round(gc[2][cl + e] * (f[e] - gc[3][cl + e] - xh * gc[4][cl + e]));
-                            }
-                        } else {
-                            const int64_t img = q / ((int64_t)H * W);
-                            const int rem = (int)(q - img * H * W);
-                            const int y = rem / W, xx = rem - y * W;
-                            const int64_t qq = (img * (H / 2) + y / 2) * (W / 2) + xx / 2;
-                            Elem<T>::unpack(ldg16(gs + qq * p.g_ldc + c), f);
-                            for (int e = 0; e < VEC; e++) f[e] *= 0.25f;
-                        }
-                    } else {
-                        for (int e = 0; e < VEC; e++) f[e] = 0.f;
-                    }
-                }
-                for (int e = 0; e < VEC; e++) {
-                    T *dst = Gt + (cl + e) * GSTR + 2 * pr;
-                    dst[0] = to_store<T>(f0[e]);
-                    dst[1] = to_store<T>(f1[e]);
-                }
-            }
-        }
-        // ---- border flags of the chunk's pixels (3x3 only) ----
-        if (TPW == 3 && tid < kWgBKP) {
-            const int64_t q = q0 + tid;
-            uint8_t f = 0;
-            if (q < m) {
-                const int wq = (int)(q % W), hq = (int)((q / W) % H);
-                f = 1 | (hq == 0 ? 2 : 0) | (hq == H - 1 ? 4 : 0) | (wq == 0 ? 8 : 0) | (wq == W - 1 ? 16 : 0);
-            }
-            flags[tid] = f;
-        }
+        store_chunk(ch);
         __syncthreads();
+        if (ch + 1 < ch_end) load_chunk(ch + 1);
         // ---- matrix cores ----
-        for (int ks = 0; ks < kWgBKP / M::KSTEP; ks++) {
+        for (int ks = 0; ks < kWgKC / M::KSTEP; ks++) {
             const int kq = ks * M::KSTEP + (lane >> 4) * M::KPL;
-            const typename M::frag a = M::load(Zt + (wave * 16 + (lane & 15)) * ZSTR + kq);
-            for (int t = 0; t < TPW; t++) {
-                if (TPW == 1) {
-                    for (int cb = 0; cb < TN; cb++) {
-                        const typename M::frag b = M::load(Gt + (cb * 16 + (lane & 15)) * GSTR + kq);
-                        M::mma(acc[t][cb], a, b);
-                    }
-                } else {
-                    const int dw = t - 1;
-                    const int off = dh * W + dw;
-                    const int bad = (dh == 1 ? 2 : (dh == -1 ? 4 : 0)) | (dw == 1 ? 8 : (dw == -1 ? 16 : 0));
-                    bool ok[M::KPL];
-                    for (int e = 0; e < M::KPL; e++) {
-                        const int f = flags[kq + e];
-                        ok[e] = (f & 1) && !(f & bad);
-                    }
-                    for (int cb = 0; cb < TN; cb++) {
-                        const T *src = Gt + (cb * 16 + (lane & 15)) * GSTR + halo - off + kq;
-                        typename M::frag b;
-                        if constexpr (M::KPL == 8) {
-                            uint32_t wv[4];
-                            for (int e2 = 0; e2 < 4; e2++) {
-                                const uint32_t lo = ok[2 * e2] ? (uint32_t)src[2 * e2] : 0u;
-                                const uint32_t hi = ok[2 * e2 + 1] ? (uint32_t)src[2 * e2 + 1] : 0u;
-                                wv[e2] = lo | (hi << 16);
-                            }
-                            b = M::from_words(wv);
-                        } else {
-                            b = ok[0] ? M::load(src) : M::zero();
-                        }
-                        M::mma(acc[t][cb], a, b);
-                    }
+            typename M::frag a[RB];
+            for (int rb = 0; rb < RB; rb++) a[rb] = M::load(Zt + ((wr * RB + rb) * 16 + (lane & 15)) * ZSTR + kq);
+            for (int t = 0; t < TAPS; t++) {
+                // G position of Z position kq for tap (kh_t, kw = t): 1 - kw
+                const int off = TAPS == 3 ? 1 - t : 0;
+                for (int cb = 0; cb < CB; cb++) {
+                    const T *row = Gt + ((wc * CB + cb) * 16 + (lane & 15)) * GSTR;
+                    const typename M::frag b = Shifted<T>::load(row, GOFF + off + kq);
+                    for (int rb = 0; rb < RB; rb++) M::mma(acc[t][rb][cb], a[rb], b);
                 }
             }
         }
@@ -221,34 +286,42 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, int ci_tiles,
     }
 
     // ---- partial tile (or dW directly when there is one split) ----
-    float *dst = splits == 1 ? p.dw : p.part + (int64_t)split * p.k * p.k * C_in * C_out;
-    for (int t = 0; t < TPW; t++) {
-        const int tap = TPW == 3 ? kh_t * 3 + t : 0;
-        for (int cb = 0; cb < TN; cb++)
-            for (int i = 0; i < 4; i++) {
-                const int ci = ci0 + wave * 16 + (lane >> 4) * 4 + i;
-                const int co = co0 + cb * 16 + (lane & 15);
-                if (ci < C_in && co < C_out) dst[((int64_t)tap * C_in + ci) * C_out + co] = acc[t][cb][i];
-            }
+    float *dst = pl.splits == 1 ? p.dw : p.part + (int64_t)split * p.k * p.k * C_in * C_out;
+    for (int t = 0; t < TAPS; t++) {
+        const int tap = TAPS == 3 ? kh_t * 3 + t : 0;
+        for (int rb = 0; rb < RB; rb++)
+            for (int cb = 0; cb < CB; cb++)
+                for (int i = 0; i < 4; i++) {
+                    const int ci = ci0 + (wr * RB + rb) * 16 + (lane >> 4) * 4 + i;
+                    const int co = co0 + (wc * CB + cb) * 16 + (lane & 15);
+                    if (ci < C_in && co < C_out) dst[((int64_t)tap * C_in + ci) * C_out + co] = acc[t][rb][cb][i];
+                }
     }
 }
 
 // ------------------------------------------------------------- launchers ---
-size_t wgrad_ws_bytes(int dtype, int64_t m, int c_in, int c_out, int k)
+size_t wgrad_ws_bytes(int dtype, int64_t m, int n, int h, int w, int c_in, int c_out, int k)
 {
-    const WgradPlan pl = wgrad_plan(m, c_in, c_out, k, dtype == DT_BF16 ? 2 : 4);
+    const WgradPlan pl = wgrad_plan(m, n, h, w, c_in, c_out, k, dtype == DT_BF16 ? 2 : 4);
     if (pl.splits <= 1) return 0;
     return (size_t)pl.splits * k * k * c_in * c_out * sizeof(float);
 }
 
-template <typename T, int TPW, int COT>
+template <typename T, int TAPS, int COT, int WR, int WC>
 static hipError_t run_wgrad(const WgradParams &p, const WgradPlan &pl, hipStream_t s)
 {
-    const int64_t nchunks = ceil_div(p.m, kWgBKP);
     const int64_t blocks = (int64_t)pl.ci_tiles * pl.kh_tiles * pl.co_tiles * pl.splits;
-    hipLaunchKernelGGL((k_wgrad<T, TPW, COT>), dim3((unsigned)blocks), dim3(kThreads), 0, s, p, pl.ci_tiles,
-                       pl.kh_tiles, pl.co_tiles, pl.chunks_per_split, nchunks, (int)pl.splits);
+    hipLaunchKernelGGL((k_wgrad<T, TAPS, COT, WR, WC>), dim3((unsigned)blocks), dim3(kThreads), 0, s, p, pl);
     return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t dispatch_wgrad(const WgradParams &p, const WgradPlan &pl, hipStream_t s)
+{
+    if (p.k == 3) return pl.cot == 32 ? run_wgrad<T, 3, 32, 4, 1>(p, pl, s) : run_wgrad<T, 3, 64, 4, 1>(p, pl, s);
+    if (pl.cot == 32) return run_wgrad<T, 1, 32, 4, 1>(p, pl, s);
+    if (pl.cot == 64) return run_wgrad<T, 1, 64, 2, 2>(p, pl, s);
+    return run_wgrad<T, 1, 128, 1, 4>(p, pl, s);
 }
 
 hipError_t launch_wgrad(const WgradParams &p, hipStream_t s)
@@ -257,27 +330,12 @@ hipError_t launch_wgrad(const WgradParams &p, hipStream_t s)
     if (p.a_mode == 1 && (!p.a_mean || !p.a_gamma || !p.a_rstd || !p.a_beta)) return hipErrorInvalidValue;
     if (p.gsrc == GB_BNGRAD && (!p.gx || !p.g_mean || !p.g_rstd || !p.g_gamma || !p.g_dbeta || !p.g_dgamma))
         return hipErrorInvalidValue;
-    if (p.k == 3 && p.w > kRowsMaxW3) return hipErrorInvalidValue;
-    const WgradPlan pl = wgrad_plan(p.m, p.c_in, p.c_out, p.k, p.dtype == DT_BF16 ? 2 : 4);
-    if (pl.splits > 1 && !p.part) return hipErrorInvalidValue;
-    hipError_t e;
-    if (p.dtype == DT_BF16) {
-        if (p.k == 1)
-            e = pl.cot == 32 ? run_wgrad<bf16_t, 1, 32>(p, pl, s)
-              : pl.cot == 64 ? run_wgrad<bf16_t, 1, 64>(p, pl, s) : run_wgrad<bf16_t, 1, 128>(p, pl, s);
-        else
-            e = pl.cot == 32 ? run_wgrad<bf16_t, 3, 32>(p, pl, s)
-              : pl.cot == 64 ? run_wgrad<bf16_t, 3, 64>(p, pl, s) : run_wgrad<bf16_t, 3, 128>(p, pl, s);
-    } else {
-        if (p.k == 1)
-            e = pl.cot == 32 ? run_wgrad<float, 1, 32>(p, pl, s)
-              : pl.cot == 64 ? run_wgrad<float, 1, 64>(p, pl, s) : run_wgrad<float, 1, 128>(p, pl, s);
-        else
-            e = pl.cot == 32 ? run_wgrad<float, 3, 32>(p, pl, s)
-              : pl.cot == 64 ? run_wgrad<float, 3, 64>(p, pl, s) : run_wgrad<float, 3, 128>(p, pl, s);
-    }
+    if (p.k == 3 && p.w > kWgMaxW3) return hipErrorInvalidValue;
+    const WgradPlan pl = wgrad_plan(p.m, p.n, p.h, p.w, p.c_in, p.c_out, p.k, p.dtype == DT_BF16 ? 2 : 4);
+    if (pl.splits > 1 && (!p.part || !p.red)) return hipErrorInvalidValue;
+    const hipError_t e = p.dtype == DT_BF16 ? dispatch_wgrad<bf16_t>(p, pl, s) : dispatch_wgrad<float>(p, pl, s);
     if (e != hipSuccess || pl.splits <= 1) return e;
-    return launch_sum_partials(p.part, pl.splits, (int64_t)p.k * p.k * p.c_in * p.c_out, p.dw, s);
+    return launch_sum_partials(p.part, pl.splits, (int64_t)p.k * p.k * p.c_in * p.c_out, p.dw, p.red, s);
 }
 
 }  // namespace bnr

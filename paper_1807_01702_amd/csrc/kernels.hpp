@@ -13,11 +13,16 @@ enum { FIN_MVF = 0, FIN_MEAN = 1, FIN_VAR = 2, FIN_BWD = 3 };
 // k_elementwise modes
 enum { EW_DX = 0, EW_APPLY = 1, EW_RELU = 2, EW_RELUBWD = 3 };
 
+// Reduction scratch ("red") of a statistics combine: the float64 level-1
+// sums [RS][2][C] (RS <= kRedMaxRS row splits).
+constexpr int kRedMaxRS = 32;
+inline size_t stats_red_bytes(int C) { return (size_t)kRedMaxRS * 2 * C * sizeof(double); }
+int stats_combine_splits(int64_t R);
 hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
                                 const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
                                 float *part, int64_t R, hipStream_t s);
 hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
-                                 float *var, float *rstd, float *dbeta, float *dgamma, hipStream_t s);
+                                 float *var, float *rstd, float *dbeta, float *dgamma, void *red, hipStream_t s);
 hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void *x, int64_t x_ldc, const void *x2,
                               int64_t x2_ldc, const float *gamma, const float *beta, const float *mean,
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
@@ -26,7 +31,10 @@ hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x,
 hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, void *gx, int64_t ldc,
                                hipStream_t s);
 hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s);
-hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, hipStream_t s);
+// Split-K sum scratch: up to 8 level-1 float32 rows of len.
+inline size_t sum_partials_red_bytes(int64_t len) { return 8 * (size_t)len * 4; }
+int sum_partials_groups(int64_t S);
+hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, void *red, hipStream_t s);
 
 // ---- implicit-GEMM CONV over pixel rows (forward / data gradient) ---------
 enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 4 };
@@ -78,8 +86,9 @@ struct WgradParams {
     const float *g_gamma, *g_mean, *g_rstd, *g_dgamma, *g_dbeta;
     float *dw;                    // [k][k][c_in][c_out]
     float *part;                  // workspace for split partial tiles
+    void *red;                    // split-K sum scratch (sum_partials_red_bytes)
 };
-size_t wgrad_ws_bytes(int dtype, int64_t m, int c_in, int c_out, int k);
+size_t wgrad_ws_bytes(int dtype, int64_t m, int n, int h, int w, int c_in, int c_out, int k);
 hipError_t launch_wgrad(const WgradParams &p, hipStream_t s);
 
 }  // namespace bnr

@@ -27,7 +27,7 @@ inline int64_t stats_row_blocks(int64_t m, int c, int dtype) {
 // Tile: BM pixel rows x BN output channels, K consumed in chunks of 32 input
 // channels (all taps of a chunk resident in LDS).
 constexpr int kRowsBK = 32;
-constexpr int kRowsMaxW3 = 64;             // largest image width for 3x3 (halo = W+1 rows)
+constexpr int kRowsMaxW3 = 62;             // largest image width for 3x3 (halo = W+1 rows)
 struct RowsTile { int bm, bn; };
 inline RowsTile rows_tile(int dtype, int taps, int n_out) {
     if (dtype == DT_F32) return RowsTile{64, n_out <= 32 ? 32 : 64};
@@ -36,37 +36,53 @@ inline RowsTile rows_tile(int dtype, int taps, int n_out) {
 }
 
 // ---- weight gradient (reduction over pixels, split-K) ----------------------
-// Workgroup tile: 64 input channels x (1 or 3 taps) x COT output channels,
-// pixels in chunks of kWgBKP; S pixel splits write float32 partial tiles.
-constexpr int kWgBKP = 64;
-constexpr int kWgCIT = 64;
-inline int wgrad_cot(int n_out) { return n_out <= 32 ? 32 : (n_out <= 64 ? 64 : 128); }
+// Workgroup tile: 64 input channels x (1x1: the tap; 3x3: the 3 taps of one
+// filter row) x COT output channels; K (pixels) in chunks of 64 positions.
+// 3x3 chunks are R whole image rows laid out with a zero column on the left
+// and zero padding to a width PW in {16, 32, 64}, so R * PW = 64.  The chunk
+// range is split S ways; each split writes a float32 partial tile.
+constexpr int kWgKC = 64;                  // K positions per chunk
+constexpr int kWgCIT = 64;                 // input channels per tile
+constexpr int kWgMaxW3 = 62;               // widest 3x3 image row (PW <= 64)
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct WgradPlan {
-    int ci_tiles, kh_tiles, co_tiles, cot, taps_per_wg;
-    int64_t splits, chunks_per_split;
+    int k, cot, ci_tiles, kh_tiles, co_tiles;
+    int R, PW;                             // 3x3 only
+    int64_t chunks_per_image, nchunks, splits, chunks_per_split;
 };
-inline WgradPlan wgrad_plan(int64_t m, int c_in, int c_out, int k, int elem_bytes) {
+inline WgradPlan wgrad_plan(int64_t m, int n, int h, int w, int c_in, int c_out, int k, int elem_bytes)
+{
     WgradPlan p;
-    p.cot = wgrad_cot(c_out);
+    p.k = k;
+    p.cot = c_out <= 32 ? 32 : (c_out <= 64 || k == 3 ? 64 : 128);
     p.ci_tiles = (int)ceil_div(c_in, kWgCIT);
     p.kh_tiles = k == 3 ? 3 : 1;
-    p.taps_per_wg = k == 3 ? 3 : 1;
     p.co_tiles = (int)ceil_div(c_out, p.cot);
-    int64_t n_out = (int64_t)p.ci_tiles * p.kh_tiles * p.co_tiles;
-    int64_t chunks = ceil_div(m, kWgBKP);
+    if (k == 3) {
+        p.PW = w + 2 <= 16 ? 16 : (w + 2 <= 32 ? 32 : 64);
+        p.R = kWgKC / p.PW;
+        p.chunks_per_image = ceil_div(h, p.R);
+        p.nchunks = (int64_t)n * p.chunks_per_image;
+    } else {
+        p.PW = 0;
+        p.R = 0;
+        p.chunks_per_image = 0;
+        p.nchunks = ceil_div(m, kWgKC);
+    }
+    const int64_t n_out = (int64_t)p.ci_tiles * p.kh_tiles * p.co_tiles;
     int64_t s = ceil_div(512, n_out);
-    // keep the partial tiles (S * |dW| floats) small next to the operand bytes
-    int64_t dw_bytes = (int64_t)k * k * c_in * c_out * 4;
-    int64_t in_bytes = m * (int64_t)(c_in + c_out) * elem_bytes;
-    int64_t cap = (in_bytes / 12) / (dw_bytes > 0 ? dw_bytes : 1);
+    // partial tiles (S * |dW| float32, written and read once) kept below a
+    // third of the operand bytes
+    const int64_t dw_bytes = (int64_t)k * k * c_in * c_out * 4;
+    const int64_t in_bytes = m * (int64_t)(c_in + c_out) * elem_bytes;
+    int64_t cap = (in_bytes / 3) / (dw_bytes > 0 ? dw_bytes : 1);
     if (cap < 1) cap = 1;
     if (s > cap) s = cap;
-    if (s > chunks) s = chunks;
+    if (s > p.nchunks) s = p.nchunks;
     if (s < 1) s = 1;
-    p.chunks_per_split = ceil_div(chunks, s);
-    p.splits = ceil_div(chunks, p.chunks_per_split);
+    p.chunks_per_split = ceil_div(p.nchunks, s);
+    p.splits = ceil_div(p.nchunks, p.chunks_per_split);
     return p;
 }
 

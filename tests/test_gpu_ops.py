@@ -61,7 +61,7 @@ FWD_CASES = [
     (True, 1, 1, 9, 11, 40, 136, 48, 136),       # ragged channels / pixels
     (True, 3, 3, 1, 1, 64, 64, 64, 64),          # H = W = 1: only the centre tap
     (True, 3, 1, 56, 56, 64, 64, 64, 64),        # full-width rows (W = 56)
-    (True, 3, 2, 6, 64, 32, 8, 32, 8),           # widest supported 3x3 rows
+    (True, 3, 2, 6, 62, 32, 8, 32, 8),           # widest supported 3x3 rows
 ]
 
 
@@ -107,6 +107,9 @@ BWD_CASES = [
     (True, 1, 1, 9, 11, 40, 136),
     (True, 3, 3, 1, 1, 16, 24),
     (True, 3, 1, 12, 56, 64, 64),
+    (True, 3, 2, 7, 7, 128, 32),                # 7x7 rows: four image rows per K chunk
+    (True, 3, 1, 5, 30, 64, 96),                # two rows per chunk, two output-channel tiles
+    (False, 3, 2, 3, 62, 8, 12),                # widest rows, fp32
 ]
 
 
