@@ -86,6 +86,53 @@ def timed_steps(torch, wl, steps, warmup, use_graph):
     return start.elapsed_time(end) / steps, wall, graph
 
 
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+PEAK_MFMA_TFS = {"bf16": 2500.0, "f32": 157.3}
+
+
+def traced_kernels(torch, wl, steps):
+    """Per-kernel totals over `steps` eager steps, each launch bracketed by
+    HIP events on its own stream inside the library."""
+    from paper_1807_01702_amd import bnr as B
+    wl.step()
+    torch.cuda.synchronize()
+    B.bnr_trace_begin(0xF, 200000)
+    for _ in range(steps):
+        wl.step()
+    torch.cuda.synchronize()
+    recs = B.bnr_trace_end(200000)
+    agg = {}
+    for name, ms, by, fl in recs:
+        a = agg.setdefault(name, [0, 0.0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += ms
+        a[2] += by
+        a[3] += fl
+    out = {}
+    for name, (n, ms, by, fl) in agg.items():
+        out[name] = dict(launches_per_step=n / steps, ms_per_step=ms / steps, avg_launch_us=1e3 * ms / n,
+                         algorithmic_bytes_per_launch=by / n, flops_per_launch=fl / n,
+                         achieved_GBps=by / (ms * 1e-3) / 1e9 if ms > 0 else None)
+    return out
+
+
+def roofline(kernels, dtype):
+    name = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    k = kernels[name]
+    t = k["avg_launch_us"] * 1e-6
+    bytes_t = k["algorithmic_bytes_per_launch"] / (PEAK_HBM_GBS * 1e9)
+    flops_t = k["flops_per_launch"] / (PEAK_MFMA_TFS[dtype] * 1e12)
+    if flops_t > bytes_t:
+        ach = k["flops_per_launch"] / t / 1e12
+        return dict(bound="mfma", achieved=ach, peak=PEAK_MFMA_TFS[dtype], unit="TFLOP/s",
+                    frac=ach / PEAK_MFMA_TFS[dtype], traffic=None, kernel=name,
+                    avg_launch_us=k["avg_launch_us"], flops_per_launch=k["flops_per_launch"])
+    ach = k["algorithmic_bytes_per_launch"] / t / 1e9
+    return dict(bound="hbm", achieved=ach, peak=PEAK_HBM_GBS, unit="GB/s", frac=ach / PEAK_HBM_GBS, traffic=None,
+                kernel=name, avg_launch_us=k["avg_launch_us"],
+                algorithmic_bytes_per_launch=k["algorithmic_bytes_per_launch"])
+
+
 def cpu_baseline(args):
     """The fp64 oracle, as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -95,13 +142,13 @@ def cpu_baseline(args):
     os.environ.setdefault("OMP_NUM_THREADS", str(threads))
     rnd = OC.storage(True)
     if args.workload == "dense_block":
-        n = 8
+        n = 64
         d = synth.dense_block(seed=0, n=n)
         t0 = time.perf_counter()
         _, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"])
         OC.block_bwd(c, d["dpool"].astype(np.float64), rnd)
     elif args.workload == "bottleneck":
-        n = 4
+        n = 32
         d = synth.bottleneck(seed=0, n=n)
         t0 = time.perf_counter()
         _, c = OC.bottleneck_fwd(d["x"], d["p"]["w2"].shape[3], d["p"], d["eps"], rnd)
@@ -115,8 +162,8 @@ def cpu_baseline(args):
         OC.unit_bwd(c, d["dy"].astype(np.float64), rnd)
     dt = time.perf_counter() - t0
     return {"value": n / dt, "unit": "images/s", "cores": threads, "kind": "oracle",
-            "sample": "%s training step (fwd+bwd) at batch %d instead of the full batch, fp64 oracle with the "
-                      "bf16 storage model; %.1f s" % (args.workload, n, dt)}
+            "sample": "one %s training step (fwd+bwd) at batch %d, fp64 oracle with the configuration's storage "
+                      "model; %.1f s on %d threads" % (args.workload, n, dt, threads)}
 
 
 def main():
@@ -135,6 +182,8 @@ def main():
     if args.profile_only:
         print(json.dumps({k: v["ms"] for k, v in res.items()}))
         return
+    dtype = "bf16" if data.get("bf16") else "f32"
+    kernels = traced_kernels(torch, wls["fused"], args.steps) if "fused" in wls else None
     fused = res.get("fused")
     unf = res.get("unfused")
     model = bytes_model.for_workload(args.workload, data)
@@ -145,7 +194,7 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": fused["ms"] if fused else None,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if data.get("bf16") else "f32",
+        "dtype": dtype,
         "data": "synthetic (seeded N(0,1) activations and gradients, He-normal weights)",
         "config": {"workload": {"dense_block": "DenseNet-121 dense block 1 (6 composite layers, growth 32, width "
                                                "128, 64->256 ch) + transition BN-ReLU-CONV1x1 256->128 + avgpool2",
@@ -156,7 +205,8 @@ def main():
         "unfused": {"images_per_s": unf["images"] / (unf["ms"] / 1e3), "ms_per_step": unf["ms"]} if unf else None,
         "speedup_vs_unfused": (unf["ms"] / fused["ms"]) if (fused and unf) else None,
         "hbm_bytes_per_step": {"algorithmic_fused": model["fused"], "algorithmic_unfused": model["unfused"]},
-        "roofline": None,
+        "roofline": roofline(kernels, dtype) if kernels else None,
+        "kernels": kernels,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(args),
     }
     print(json.dumps(line))

@@ -238,6 +238,21 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
  * reference for profiler byte counters. */
 bnr_status bnr_hbm_copy(const void *src, void *dst, size_t bytes, void *stream);
 
+/* Launch timing (diagnostic).  Between bnr_trace_begin and bnr_trace_end,
+ * every launch of a kernel whose class is in `kernel_classes` (bit mask:
+ * 1 implicit-GEMM CONV, 2 weight gradient, 4 BN sweeps and element-wise
+ * passes, 8 combines / weight packing / split-K sums), up to `capacity`
+ * launches, is bracketed by two HIP events recorded on the launch's own
+ * stream.  bnr_trace_end waits for those events and fills, per launch, the
+ * duration in ms, the algorithmic HBM bytes (each input tensor read once, each
+ * output written once), the floating-point operations and a kernel id
+ * (1 CONV 1x1, 2 CONV 3x3, 3 weight gradient 1x1, 4 weight gradient 3x3,
+ * 5 statistics sweep, 6 element-wise pass, 7 statistics combine, 8 weight
+ * packing, 9 split-K sum, 10 pooling, 11 copy); it returns the number of
+ * launches written.  Not meant for graph capture. */
+bnr_status bnr_trace_begin(int32_t kernel_classes, int32_t capacity);
+int32_t bnr_trace_end(double *ms, double *bytes, double *flops, int32_t *kernel_id, int32_t capacity);
+
 const char *bnr_status_string(bnr_status s);
 const char *bnr_last_error(void);
 

@@ -81,7 +81,13 @@ _lib_fns = dict(
     bnr_reference_path=_sig("bnr_reference_path", ctypes.c_int, ctypes.c_int, c_i32, _P(ConvDesc), _P(RefArgs), c_vp,
                             c_sz, c_vp),
     bnr_hbm_copy=_sig("bnr_hbm_copy", ctypes.c_int, c_vp, c_vp, c_sz, c_vp),
+    bnr_trace_begin=_sig("bnr_trace_begin", ctypes.c_int, c_i32, c_i32),
+    bnr_trace_end=_sig("bnr_trace_end", c_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                       ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i32), c_i32),
 )
+
+KERNEL_IDS = {1: "conv1x1", 2: "conv3x3", 3: "wgrad1x1", 4: "wgrad3x3", 5: "stats_sweep", 6: "elementwise",
+              7: "stats_combine", 8: "weight_pack", 9: "splitk_sum", 10: "pool", 11: "copy"}
 
 
 class BnrError(RuntimeError):
@@ -287,3 +293,17 @@ def bnr_reference_path(mode, backward, desc, x, bn, w, y, z=None, out=None, g=No
 def bnr_hbm_copy(src, dst):
     nbytes = src.numel() * src.element_size()
     _check(_lib_fns["bnr_hbm_copy"](_ptr(src), _ptr(dst), nbytes, _stream()))
+
+
+def bnr_trace_begin(kernel_classes=0xF, capacity=100000):
+    _check(_lib_fns["bnr_trace_begin"](kernel_classes, capacity))
+
+
+def bnr_trace_end(capacity=100000):
+    """[(kernel name, ms, algorithmic bytes, flops)] of the traced launches."""
+    ms = (ctypes.c_double * capacity)()
+    by = (ctypes.c_double * capacity)()
+    fl = (ctypes.c_double * capacity)()
+    kid = (c_i32 * capacity)()
+    n = _lib_fns["bnr_trace_end"](ms, by, fl, kid, capacity)
+    return [(KERNEL_IDS.get(kid[i], str(kid[i])), ms[i], by[i], fl[i]) for i in range(n)]

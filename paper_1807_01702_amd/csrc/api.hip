@@ -140,7 +140,10 @@ ConvWs conv_ws(const bnr_conv_desc *d)
     size_t sf = (size_t)rows_mtiles(dt, taps, m, d->c_out) * 2 * d->c_out * 4;
     size_t sb = (size_t)rows_mtiles(dt, taps, m, d->c_in) * 2 * d->c_in * 4;
     size_t ss = (size_t)stats_row_blocks(m, d->c_in, dt) * 2 * d->c_in * 4;
+    const int cmax = d->c_in > d->c_out ? d->c_in : d->c_out;
+    const size_t sp = (size_t)conv1x1_partial_rows(m) * 2 * cmax * 4;
     size_t part = sf > sb ? sf : sb;
+    if (sp > part) part = sp;
     w.part = align_up(part > ss ? part : ss);
     w.red = align_up(stats_red_bytes(d->c_in > d->c_out ? d->c_in : d->c_out));
     w.wg = align_up(wgrad_ws_bytes(dt, m, d->n, d->h, d->w, d->c_in, d->c_out, d->k));
@@ -227,6 +230,26 @@ void fill_rows(RowsParams &rp, const bnr_conv_desc *d, int K, int N)
     rp.K = K; rp.N = N;
 }
 
+// Runs the CONV GEMM of rp (forward when transpose = 0, data gradient when 1)
+// with the persistent 1x1 kernel when it applies, else packs the weights and
+// runs the tiled kernel.  *rows = statistics partial rows written.
+bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w, int transpose, void *wpack,
+                           int64_t *rows, hipStream_t s)
+{
+    if (rp.taps == 1 && conv1x1_supported(rp.dtype, rp.K, rp.N)) {
+        rp.wraw = w;
+        rp.wtrans = transpose;
+        *rows = conv1x1_partial_rows(rp.m);
+        TRY_HIP(launch_conv1x1(rp, s), transpose ? "conv data gradient" : "conv forward");
+        return BNR_OK;
+    }
+    TRY_HIP(launch_pack_weights(rp.dtype, w, d->k, d->c_in, d->c_out, transpose, wpack, s), "weight packing");
+    rp.wpack = wpack;
+    *rows = rows_mtiles(rp.dtype, rp.taps, rp.m, rp.N);
+    TRY_HIP(launch_conv_rows(rp, s), transpose ? "conv data gradient" : "conv forward");
+    return BNR_OK;
+}
+
 // forward CONV with optional BN+ReLU prologue and optional statistics epilogue
 bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w, void *y,
                     bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream)
@@ -251,19 +274,17 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     const ConvPtrs wp = conv_ptrs(ws, cw);
     void *wpack = wp.pack;
     float *part = wp.part;
-    TRY_HIP(launch_pack_weights(dt_of(d->dtype), w, d->k, d->c_in, d->c_out, 0, wpack, s), "weight packing");
     RowsParams rp;
     fill_rows(rp, d, d->c_in, d->c_out);
     rp.pro = x_bn ? PRO_BNRELU : PRO_NONE;
     rp.a = x; rp.a_ldc = d->in_ldc;
     if (x_bn) { rp.p_gamma = x_bn->gamma; rp.p_beta = x_bn->beta; rp.p_mean = x_bn->mean; rp.p_rstd = x_bn->rstd; }
-    rp.wpack = wpack;
     rp.epi = y_bn ? EPI_STATS : EPI_STORE;
     rp.y = y; rp.y_ldc = d->out_ldc;
     rp.part = part;
-    TRY_HIP(launch_conv_rows(rp, s), "conv forward");
+    int64_t R = 0;
+    TRY(launch_conv_any(rp, d, w, 0, wpack, &R, s));
     if (y_bn) {
-        const int64_t R = rows_mtiles(rp.dtype, rp.taps, m, d->c_out);
         TRY_HIP(launch_stats_finalize(part, R, d->c_out, m, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
                                       nullptr, nullptr, wp.red, s),
                 "stats combine");
@@ -405,10 +426,8 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     const int dt = dt_of(d->dtype);
 
     // 1. data gradient with the gradient-source prologue and the BN-backward epilogue
-    TRY_HIP(launch_pack_weights(dt, w, d->k, d->c_in, d->c_out, 1, wpack, s), "weight packing");
     RowsParams rp;
     fill_rows(rp, d, d->c_out, d->c_in);
-    rp.wpack = wpack;
     if (g->kind == BNR_GRAD_DENSE) {
         rp.pro = PRO_NONE; rp.a = g->g; rp.a_ldc = g->g_ldc;
     } else if (g->kind == BNR_GRAD_BN) {
@@ -425,10 +444,10 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     } else {
         rp.epi = EPI_STORE; rp.y = dx; rp.y_ldc = dx_ldc; rp.accumulate = dx_accumulate ? 1 : 0;
     }
-    TRY_HIP(launch_conv_rows(rp, s), "conv data gradient");
+    int64_t R = 0;
+    TRY(launch_conv_any(rp, d, w, 1, wpack, &R, s));
     // 2. dbeta = sum(dy), dgamma = sum(dy * xhat)
     if (x_bn) {
-        const int64_t R = rows_mtiles(dt, rp.taps, m, d->c_in);
         TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma,
                                       cp.red, s),
                 "backward sums combine");
@@ -541,14 +560,13 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
         if (base)
             TRY_HIP(launch_elementwise(dt, EW_RELU, m, d->c_in, a->y, d->c_in, nullptr, 0, nullptr, nullptr, nullptr,
                                        nullptr, nullptr, nullptr, a->z, d->c_in, 0, s), "relu");
-        TRY_HIP(launch_pack_weights(dt, a->w, d->k, d->c_in, d->c_out, 0, wpack, s), "weight packing");
         RowsParams rp;
         fill_rows(rp, d, d->c_in, d->c_out);
         rp.pro = base ? PRO_NONE : PRO_RELU;
         rp.a = base ? a->z : a->y; rp.a_ldc = d->c_in;
-        rp.wpack = wpack;
         rp.epi = EPI_STORE; rp.y = a->out; rp.y_ldc = d->out_ldc;
-        TRY_HIP(launch_conv_rows(rp, s), "conv forward");
+        int64_t Rf = 0;
+        TRY(launch_conv_any(rp, d, a->w, 0, wpack, &Rf, s));
         return ok();
     }
 
@@ -564,17 +582,16 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
     if (overlap(view_range(a->dx, m, d->c_in, a->dx_ldc, es), view_range(a->x, m, d->c_in, d->in_ldc, es)))
         return fail(BNR_ERR_ALIAS, "dx overlaps x");
     // data gradient (BASELINE: materialise dz; RCF: ReLU mask in the epilogue)
-    TRY_HIP(launch_pack_weights(dt, a->w, d->k, d->c_in, d->c_out, 1, wpack, s), "weight packing");
     RowsParams rp;
     fill_rows(rp, d, d->c_out, d->c_in);
     rp.pro = PRO_NONE; rp.a = a->g; rp.a_ldc = a->g_ldc;
-    rp.wpack = wpack;
     if (base) {
         rp.epi = EPI_STORE; rp.y = a->dz; rp.y_ldc = d->c_in;
     } else {
         rp.epi = EPI_RELUMASK; rp.y = a->dy; rp.y_ldc = d->c_in; rp.ex = a->y; rp.ex_ldc = d->c_in;
     }
-    TRY_HIP(launch_conv_rows(rp, s), "conv data gradient");
+    int64_t Rd = 0;
+    TRY(launch_conv_any(rp, d, a->w, 1, wpack, &Rd, s));
     // weight gradient (BASELINE reads the stored z; RCF recomputes relu(y))
     WgradParams wp;
     memset(&wp, 0, sizeof wp);

@@ -10,6 +10,7 @@
 #include "common.hpp"
 #include "kernels.hpp"
 #include "tiles.hpp"
+#include "trace.hpp"
 
 namespace bnr {
 
@@ -369,6 +370,8 @@ hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
     const int64_t rpb = ceil_div(m, R);
     dim3 grid((unsigned)R, (unsigned)cb);
+    const double es = dtype == DT_BF16 ? 2.0 : 4.0;
+    TraceScope tr(KC_SWEEP, KID_STATS_SWEEP, s, (mode == ST_DYX ? 2.0 : 1.0) * (double)m * C * es, 0.0);
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_stats_partial<bf16_t>, grid, dim3(kThreads), 0, s, (const bf16_t *)x, ldc, m, C, mode,
                            mean, rstd, (const bf16_t *)dy, dy_ldc, rpb, part);
@@ -392,8 +395,12 @@ hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m,
         return hipErrorInvalidValue;
     double *lvl1 = reinterpret_cast<double *>(red);
     const int RS = stats_combine_splits(R);
-    hipLaunchKernelGGL(k_stats_combine1, dim3((unsigned)ceil_div(C, 64), (unsigned)RS), dim3(kThreads), 0, s, part, R,
-                       C, lvl1);
+    {
+        TraceScope tr(KC_SMALL, KID_COMBINE, s, (double)R * 2 * C * 4 + (double)RS * 2 * C * 8, 0.0);
+        hipLaunchKernelGGL(k_stats_combine1, dim3((unsigned)ceil_div(C, 64), (unsigned)RS), dim3(kThreads), 0, s, part,
+                           R, C, lvl1);
+    }
+    TraceScope tr(KC_SMALL, KID_COMBINE, s, (double)RS * 2 * C * 8 + 3.0 * C * 4, 0.0);
     hipLaunchKernelGGL(k_stats_combine2, dim3((unsigned)ceil_div(C, kThreads)), dim3(kThreads), 0, s, lvl1, RS, C, m,
                        mode, eps, mean, var, rstd, dbeta, dgamma);
     return hipGetLastError();
@@ -412,6 +419,8 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
     const int64_t R = stats_row_blocks(m, C, dtype) * 2;
     const int64_t rpb = ceil_div(m, R);
     dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
+    const double sweeps = mode == EW_DX ? 3.0 + (accumulate ? 1.0 : 0.0) : (mode == EW_RELUBWD ? 3.0 : 2.0);
+    TraceScope tr(KC_SWEEP, KID_ELEMENTWISE, s, sweeps * (double)m * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_elementwise<bf16_t>, grid, dim3(kThreads), 0, s, mode, m, C, (const bf16_t *)x, x_ldc,
                            (const bf16_t *)x2, x2_ldc, gamma, beta, mean, rstd, dgamma, dbeta, (bf16_t *)out,
@@ -427,6 +436,7 @@ hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x,
 {
     const int64_t total = (int64_t)n * (h / 2) * (w / 2) * (C / (dtype == DT_BF16 ? 8 : 4));
     const int grid = grid_cap(ceil_div(total, kThreads));
+    TraceScope tr(KC_SWEEP, KID_POOL, s, 1.25 * (double)n * h * w * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_avgpool2<bf16_t>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const bf16_t *)x, ldc,
                            (bf16_t *)y);
@@ -441,6 +451,7 @@ hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void
 {
     const int64_t total = (int64_t)n * h * w * (C / (dtype == DT_BF16 ? 8 : 4));
     const int grid = grid_cap(ceil_div(total, kThreads));
+    TraceScope tr(KC_SWEEP, KID_POOL, s, 1.25 * (double)n * h * w * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_avgpool2_bwd<bf16_t>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const bf16_t *)g,
                            (bf16_t *)gx, ldc);
@@ -452,6 +463,7 @@ hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void
 
 hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s)
 {
+    TraceScope tr(KC_SWEEP, KID_COPY, s, 32.0 * (double)nvec, 0.0);
     hipLaunchKernelGGL(k_copy16, dim3(2048), dim3(kThreads), 0, s, (const vec16 *)src, (vec16 *)dst, nvec);
     return hipGetLastError();
 }
@@ -464,8 +476,14 @@ hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float 
     if (!part || !out || (len % 4) || (SG > 1 && !red)) return hipErrorInvalidValue;
     const unsigned gx = (unsigned)ceil_div(len, 4 * kThreads);
     float *lvl1 = SG > 1 ? reinterpret_cast<float *>(red) : out;
-    hipLaunchKernelGGL(k_sum_partials1, dim3(gx, (unsigned)SG), dim3(kThreads), 0, s, part, S, len, lvl1);
-    if (SG > 1) hipLaunchKernelGGL(k_sum_partials2, dim3(gx), dim3(kThreads), 0, s, lvl1, SG, len, out);
+    {
+        TraceScope tr(KC_SMALL, KID_SPLITK_SUM, s, 4.0 * (double)len * (S + SG), 0.0);
+        hipLaunchKernelGGL(k_sum_partials1, dim3(gx, (unsigned)SG), dim3(kThreads), 0, s, part, S, len, lvl1);
+    }
+    if (SG > 1) {
+        TraceScope tr(KC_SMALL, KID_SPLITK_SUM, s, 4.0 * (double)len * (SG + 1), 0.0);
+        hipLaunchKernelGGL(k_sum_partials2, dim3(gx), dim3(kThreads), 0, s, lvl1, SG, len, out);
+    }
     return hipGetLastError();
 }
 

@@ -32,6 +32,7 @@
 #include "kernels.hpp"
 #include "mfma.hpp"
 #include "tiles.hpp"
+#include "trace.hpp"
 
 namespace bnr {
 
@@ -325,6 +326,7 @@ hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_
     const int64_t ntiles = ceil_div(N, t.bn), nchunks = ceil_div(K, kRowsBK);
     const int64_t total = ntiles * nchunks * taps * t.bn * kRowsBK;
     const int grid = (int)(ceil_div(total, kThreads) < 1024 ? ceil_div(total, kThreads) : 1024);
+    TraceScope tr(KC_SMALL, KID_PACK, s, (double)(taps * c_in * c_out + total) * (dtype == DT_BF16 ? 2 : 4), 0.0);
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_pack_weights<bf16_t>, dim3(grid), dim3(kThreads), 0, s, (const bf16_t *)w, taps, c_in,
                            c_out, transpose, t.bn, (int)nchunks, total, (bf16_t *)wpack);
@@ -332,6 +334,20 @@ hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_
         hipLaunchKernelGGL(k_pack_weights<float>, dim3(grid), dim3(kThreads), 0, s, (const float *)w, taps, c_in,
                            c_out, transpose, t.bn, (int)nchunks, total, (float *)wpack);
     return hipGetLastError();
+}
+
+// Algorithmic HBM bytes of one launch: each operand tensor read once, each
+// output written once (weights once).
+static double rows_algorithmic_bytes(const RowsParams &p)
+{
+    const double e = p.dtype == DT_BF16 ? 2.0 : 4.0, m = (double)p.m, K = p.K, N = p.N;
+    double a = m * K;                                            // A operand
+    if (p.pro == PRO_BNGRAD) a = 2.0 * m * K;                    // dy and x
+    if (p.pro == PRO_POOLUP) a = m / 4.0 * K;                    // pooled gradient
+    double out = m * N;                                          // output write
+    if (p.epi == EPI_STORE && p.accumulate) out += m * N;        // read-modify-write
+    if (p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK) out += m * N;   // BN input / ReLU input read
+    return e * (a + out + (double)p.taps * K * N);
 }
 
 template <typename T, int TAPS, int BM, int BN, int WM, int WN>
@@ -348,6 +364,8 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
         attr_set = true;
     }
     dim3 grid((unsigned)ceil_div(p.m, BM), (unsigned)ceil_div(p.N, BN));
+    TraceScope tr(KC_CONV, TAPS == 9 ? KID_CONV_3X3 : KID_CONV_1X1, s, rows_algorithmic_bytes(p),
+                  2.0 * (double)p.m * TAPS * p.K * p.N);
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, p);
     return hipGetLastError();
 }

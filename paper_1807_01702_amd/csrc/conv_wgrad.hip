@@ -26,6 +26,7 @@
 #include "kernels.hpp"
 #include "mfma.hpp"
 #include "tiles.hpp"
+#include "trace.hpp"
 
 namespace bnr {
 
@@ -311,6 +312,13 @@ template <typename T, int TAPS, int COT, int WR, int WC>
 static hipError_t run_wgrad(const WgradParams &p, const WgradPlan &pl, hipStream_t s)
 {
     const int64_t blocks = (int64_t)pl.ci_tiles * pl.kh_tiles * pl.co_tiles * pl.splits;
+    const double e = sizeof(T), m = (double)p.m;
+    double g = m * p.c_out;                                       // gradient operand
+    if (p.gsrc == GB_BNGRAD) g *= 2.0;                            // dy and x
+    if (p.gsrc == GB_POOLUP) g /= 4.0;                            // pooled gradient
+    const double dwb = (double)p.k * p.k * p.c_in * p.c_out;
+    TraceScope tr(KC_WGRAD, TAPS == 3 ? KID_WGRAD_3X3 : KID_WGRAD_1X1, s, e * (m * p.c_in + g) + 4.0 * dwb,
+                  2.0 * m * dwb);
     hipLaunchKernelGGL((k_wgrad<T, TAPS, COT, WR, WC>), dim3((unsigned)blocks), dim3(kThreads), 0, s, p, pl);
     return hipGetLastError();
 }

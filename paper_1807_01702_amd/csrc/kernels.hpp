@@ -50,7 +50,9 @@ struct RowsParams {
     const void *a2;               // BNGRAD: the BN input x (same pixels, K channels)
     int64_t a2_ldc;
     const float *p_gamma, *p_beta, *p_mean, *p_rstd, *p_dgamma, *p_dbeta;
-    const void *wpack;            // weights packed by launch_pack_weights
+    const void *wpack;            // weights packed by launch_pack_weights (conv_rows)
+    const void *wraw;             // weights in their [k][k][c_in][c_out] layout (persistent 1x1)
+    int wtrans;                   // 1: data-gradient operand (GEMM K = c_out, N = c_in)
     int epi;
     void *y;                      // output view (EPI_BNBWD: dy, dense)
     int64_t y_ldc;
@@ -67,6 +69,11 @@ size_t rows_pack_bytes(int dtype, int taps, int K, int N);
 hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_out, int transpose, void *wpack,
                                hipStream_t s);
 hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s);
+
+// ---- persistent 1x1 CONV (weights resident in LDS, one workgroup per CU) ----
+bool conv1x1_supported(int dtype, int K, int N);
+int64_t conv1x1_partial_rows(int64_t m);      // statistics partial rows it writes
+hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s);
 
 // ---- weight gradient -------------------------------------------------------
 enum { GB_DENSE = 0, GB_BNGRAD = 1, GB_POOLUP = 2 };
