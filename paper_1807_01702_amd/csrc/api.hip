@@ -141,7 +141,9 @@ ConvWs conv_ws(const bnr_conv_desc *d)
     size_t sb = (size_t)rows_mtiles(dt, taps, m, d->c_in) * 2 * d->c_in * 4;
     size_t ss = (size_t)stats_row_blocks(m, d->c_in, dt) * 2 * d->c_in * 4;
     const int cmax = d->c_in > d->c_out ? d->c_in : d->c_out;
-    const size_t sp = (size_t)conv1x1_partial_rows(m) * 2 * cmax * 4;
+    const int64_t prow = conv1x1_partial_rows(m) > conv3x3_partial_rows(m) ? conv1x1_partial_rows(m)
+                                                                            : conv3x3_partial_rows(m);
+    const size_t sp = (size_t)prow * 2 * cmax * 4;
     size_t part = sf > sb ? sf : sb;
     if (sp > part) part = sp;
     w.part = align_up(part > ss ? part : ss);
@@ -241,6 +243,13 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
         rp.wtrans = transpose;
         *rows = conv1x1_partial_rows(rp.m);
         TRY_HIP(launch_conv1x1(rp, s), transpose ? "conv data gradient" : "conv forward");
+        return BNR_OK;
+    }
+    if (rp.taps == 9 && rp.pro != PRO_POOLUP && conv3x3_supported(rp.dtype, rp.K, rp.N, rp.w)) {
+        rp.wraw = w;
+        rp.wtrans = transpose;
+        *rows = conv3x3_partial_rows(rp.m);
+        TRY_HIP(launch_conv3x3(rp, s), transpose ? "conv data gradient" : "conv forward");
         return BNR_OK;
     }
     TRY_HIP(launch_pack_weights(rp.dtype, w, d->k, d->c_in, d->c_out, transpose, wpack, s), "weight packing");

@@ -15,19 +15,40 @@
 namespace bnr {
 
 // --------------------------------------------------------------------------
-// Per-channel partial sums over a row block.
+// Per-channel partial sums over a row block (MODE is a template argument so
+// every load of a 4-row batch is issued before any arithmetic).
 //   ST_SUMSQ : s1 = sum x,            s2 = sum x^2        (mean/variance fusion)
 //   ST_SUM   : s1 = sum x                                 (unfused mean sweep)
 //   ST_SQDEV : s1 = sum (x - mean)^2                      (unfused variance sweep)
 //   ST_DYX   : s1 = sum dy,           s2 = sum dy * xhat  (BN backward sums)
 // part[rb][0][c] = s1, part[rb][1][c] = s2 (float32).
-template <typename T>
+template <typename T, int MODE>
+__device__ __forceinline__ void stats_accum(const vec16 &v, const vec16 &d, const float *mu, const float *rs,
+                                            float *s1, float *s2)
+{
+    constexpr int VEC = Elem<T>::VEC;
+    float f[VEC];
+    Elem<T>::unpack(v, f);
+    if (MODE == ST_SUMSQ) {
+        for (int i = 0; i < VEC; i++) { s1[i] += f[i]; s2[i] += f[i] * f[i]; }
+    } else if (MODE == ST_SUM) {
+        for (int i = 0; i < VEC; i++) s1[i] += f[i];
+    } else if (MODE == ST_SQDEV) {
+        for (int i = 0; i < VEC; i++) { const float e = f[i] - mu[i]; s1[i] += e * e; }
+    } else {
+        float g[VEC];
+        Elem<T>::unpack(d, g);
+        for (int i = 0; i < VEC; i++) { s1[i] += g[i]; s2[i] += g[i] * ((f[i] - mu[i]) * rs[i]); }
+    }
+}
+
+template <typename T, int MODE>
 __global__ __launch_bounds__(kThreads) void k_stats_partial(
-    const T *__restrict__ x, int64_t ldc, int64_t m, int C, int mode,
+    const T *__restrict__ x, int64_t ldc, int64_t m, int C,
     const float *__restrict__ mean, const float *__restrict__ rstd,
     const T *__restrict__ dy, int64_t dy_ldc, int64_t rows_per_block, float *__restrict__ part)
 {
-    constexpr int VEC = Elem<T>::VEC;
+    constexpr int VEC = Elem<T>::VEC, U = 4;
     __shared__ float red[2][kThreads * VEC];
     const int cvec = C / VEC;
     const int vb = min(kStatsMaxVec, cvec - (int)blockIdx.y * kStatsMaxVec);
@@ -36,48 +57,28 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
     float s1[VEC], s2[VEC], mu[VEC], rs[VEC];
     for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f; }
-    if (ty < ry && (mode == ST_SQDEV || mode == ST_DYX))
+    if (ty < ry && (MODE == ST_SQDEV || MODE == ST_DYX))
         for (int i = 0; i < VEC; i++) mu[i] = mean[c0 + i];
-    if (ty < ry && mode == ST_DYX)
+    if (ty < ry && MODE == ST_DYX)
         for (int i = 0; i < VEC; i++) rs[i] = rstd[c0 + i];
     const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
     const int64_t r1 = min(m, r0 + rows_per_block);
     if (ty < ry) {
         int64_t r = r0 + ty;
-        // four rows in flight per thread
-        for (; r + 3 * ry < r1; r += 4 * ry) {
-            vec16 v[4], d[4];
-            for (int u = 0; u < 4; u++) v[u] = ldg16(x + (r + u * ry) * ldc + c0);
-            if (mode == 3)
-                for (int u = 0; u < 4; u++) d[u] = ldg16(dy + (r + u * ry) * dy_ldc + c0);
-            for (int u = 0; u < 4; u++) {
-                float f[VEC], g[VEC];
-                Elem<T>::unpack(v[u], f);
-                if (mode == 0) {
-                    for (int i = 0; i < VEC; i++) { s1[i] += f[i]; s2[i] += f[i] * f[i]; }
-                } else if (mode == 1) {
-                    for (int i = 0; i < VEC; i++) s1[i] += f[i];
-                } else if (mode == 2) {
-                    for (int i = 0; i < VEC; i++) { float e = f[i] - mu[i]; s1[i] += e * e; }
-                } else {
-                    Elem<T>::unpack(d[u], g);
-                    for (int i = 0; i < VEC; i++) { s1[i] += g[i]; s2[i] += g[i] * ((f[i] - mu[i]) * rs[i]); }
-                }
+        for (; r + (U - 1) * ry < r1; r += U * ry) {
+            vec16 v[U], d[U];
+            #pragma unroll
+            for (int u = 0; u < U; u++) {
+                v[u] = ldg16(x + (r + u * ry) * ldc + c0);
+                d[u] = MODE == ST_DYX ? ldg16(dy + (r + u * ry) * dy_ldc + c0) : v[u];
             }
+            #pragma unroll
+            for (int u = 0; u < U; u++) stats_accum<T, MODE>(v[u], d[u], mu, rs, s1, s2);
         }
         for (; r < r1; r += ry) {
-            float f[VEC], g[VEC];
-            Elem<T>::unpack(ldg16(x + r * ldc + c0), f);
-            if (mode == 0) {
-                for (int i = 0; i < VEC; i++) { s1[i] += f[i]; s2[i] += f[i] * f[i]; }
-            } else if (mode == 1) {
-                for (int i = 0; i < VEC; i++) s1[i] += f[i];
-            } else if (mode == 2) {
-                for (int i = 0; i < VEC; i++) { float e = f[i] - mu[i]; s1[i] += e * e; }
-            } else {
-                Elem<T>::unpack(ldg16(dy + r * dy_ldc + c0), g);
-                for (int i = 0; i < VEC; i++) { s1[i] += g[i]; s2[i] += g[i] * ((f[i] - mu[i]) * rs[i]); }
-            }
+            const vec16 v = ldg16(x + r * ldc + c0);
+            const vec16 d = MODE == ST_DYX ? ldg16(dy + r * dy_ldc + c0) : v;
+            stats_accum<T, MODE>(v, d, mu, rs, s1, s2);
         }
     }
     const int nch = vb * VEC;
@@ -94,6 +95,72 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
         float *p = part + (int64_t)blockIdx.x * 2 * C;
         p[c] = a;
         p[C + c] = b;
+    }
+}
+
+// --------------------------------------------------------------------------
+// Finalisation shared by the combine kernels: from the float64 sums a = s1,
+// b = s2 of one channel write
+//   FIN_MVF   : mean = a/m, var = b/m - mean^2 (clamped at 0), rstd
+//   FIN_MEAN  : mean = a/m
+//   FIN_VAR   : var = a/m, rstd            (two-pass variance)
+//   FIN_BWD   : dbeta = a, dgamma = b
+__device__ __forceinline__ void stats_write(int mode, int c, double a, double b, int64_t m, float eps, float *mean,
+                                            float *var, float *rstd, float *dbeta, float *dgamma)
+{
+    const double dm = (double)m;
+    if (mode == FIN_MVF) {
+        const double mu = a / dm;
+        double v = b / dm - mu * mu;
+        if (v < 0.0) v = 0.0;
+        mean[c] = (float)mu;
+        if (var) var[c] = (float)v;
+        rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
+    } else if (mode == FIN_MEAN) {
+        mean[c] = (float)(a / dm);
+    } else if (mode == FIN_VAR) {
+        const double v = a / dm;
+        if (var) var[c] = (float)v;
+        rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
+    } else {
+        dbeta[c] = (float)a;
+        dgamma[c] = (float)b;
+    }
+}
+
+// One-kernel combine for up to kCombineOneMaxRows partial rows: workgroup =
+// 8 channels x 32 row groups; thread (c, g) adds rows g, g+32, ... in float64
+// (8 loads in flight), then the 32 group sums of a channel are added in a
+// fixed order (deterministic).
+__global__ __launch_bounds__(kThreads) void k_stats_combine_one(const float *__restrict__ part, int64_t R, int C,
+                                                                int64_t m, int mode, float eps, float *mean,
+                                                                float *var, float *rstd, float *dbeta, float *dgamma)
+{
+    __shared__ double red[2][32][8];
+    const int tid = threadIdx.x, cl = tid & 7, g = tid >> 3;
+    const int c = blockIdx.x * 8 + cl;
+    double a = 0.0, b = 0.0;
+    if (c < C) {
+        const float *p = part + c;
+        for (int64_t r = g; r < R; r += 8 * 32) {
+            float va[8], vb[8];
+            #pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const int64_t rr = r + 32 * u;
+                va[u] = rr < R ? p[rr * 2 * C] : 0.f;
+                vb[u] = rr < R ? p[rr * 2 * C + C] : 0.f;
+            }
+            #pragma unroll
+            for (int u = 0; u < 8; u++) { a += (double)va[u]; b += (double)vb[u]; }
+        }
+    }
+    red[0][g][cl] = a;
+    red[1][g][cl] = b;
+    __syncthreads();
+    if (g == 0 && c < C) {
+        double sa = 0.0, sb = 0.0;
+        for (int j = 0; j < 32; j++) { sa += red[0][j][cl]; sb += red[1][j][cl]; }
+        stats_write(mode, c, sa, sb, m, eps, mean, var, rstd, dbeta, dgamma);
     }
 }
 
@@ -134,11 +201,7 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine1(const float *__rest
 }
 
 // Level 2: adds the RS level-1 sums of a channel in a fixed order
-// (deterministic) and writes
-//   FIN_MVF   : mean = s1/m, var = s2/m - mean^2 (clamped at 0), rstd
-//   FIN_MEAN  : mean = s1/m
-//   FIN_VAR   : var = s1/m, rstd            (two-pass variance)
-//   FIN_BWD   : dbeta = s1, dgamma = s2
+// (deterministic) and writes the statistics.
 __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__restrict__ lvl1, int RS, int C, int64_t m,
                                                              int mode, float eps, float *__restrict__ mean,
                                                              float *__restrict__ var, float *__restrict__ rstd,
@@ -151,94 +214,94 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__res
         a += lvl1[((int64_t)j * 2) * C + c];
         b += lvl1[((int64_t)j * 2 + 1) * C + c];
     }
-    const double dm = (double)m;
-    if (mode == FIN_MVF) {
-        const double mu = a / dm;
-        double v = b / dm - mu * mu;
-        if (v < 0.0) v = 0.0;
-        mean[c] = (float)mu;
-        if (var) var[c] = (float)v;
-        rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
-    } else if (mode == FIN_MEAN) {
-        mean[c] = (float)(a / dm);
-    } else if (mode == FIN_VAR) {
-        const double v = a / dm;
-        if (var) var[c] = (float)v;
-        rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
-    } else {
-        dbeta[c] = (float)a;
-        dgamma[c] = (float)b;
-    }
+    stats_write(mode, c, a, b, m, eps, mean, var, rstd, dbeta, dgamma);
 }
 
 // --------------------------------------------------------------------------
-// Element-wise passes over [m][C] views with per-channel parameters.
+// Element-wise passes over [m][C] views with per-channel parameters (MODE
+// and ACC are template arguments so each row batch issues all its loads,
+// including the accumulate read, before any arithmetic).
 //   EW_DX      : out = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m)  [+ out]
 //   EW_APPLY   : out = gamma*(x-mean)*rstd + beta                  (unfused BN)
 //   EW_RELU    : out = max(x, 0)                                   (unfused ReLU)
 //   EW_RELUBWD : out = x2 > 0 ? x : 0   (x = dz, x2 = y)           (unfused ReLU bwd)
-template <typename T>
+template <typename T, int MODE, bool ACC>
 __global__ __launch_bounds__(kThreads) void k_elementwise(
-    int mode, int64_t m, int C, const T *__restrict__ x, int64_t x_ldc, const T *__restrict__ x2,
+    int64_t m, int C, const T *__restrict__ x, int64_t x_ldc, const T *__restrict__ x2,
     int64_t x2_ldc, const float *__restrict__ gamma, const float *__restrict__ beta,
     const float *__restrict__ mean, const float *__restrict__ rstd, const float *__restrict__ dgamma,
-    const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int accumulate,
-    int64_t rows_per_block)
+    const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int64_t rows_per_block)
 {
-    constexpr int VEC = Elem<T>::VEC;
+    constexpr int VEC = Elem<T>::VEC, U = 2;
+    constexpr bool TWO = MODE == EW_DX || MODE == EW_RELUBWD;
     const int cvec = C / VEC;
     const int vb = min(kStatsMaxVec, cvec - (int)blockIdx.y * kStatsMaxVec);
     const int ry = kThreads / vb;
     const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
     if (ty >= ry) return;
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
-    float p0[VEC], p1[VEC], p2[VEC], p3[VEC];
+    float p0[VEC], p1[VEC], p2[VEC], p3[VEC], p4[VEC];
     const float inv_m = 1.0f / (float)m;
     for (int i = 0; i < VEC; i++) {
         const int c = c0 + i;
-        if (mode == EW_DX) {
+        p0[i] = p1[i] = p2[i] = p3[i] = p4[i] = 0.f;
+        if (MODE == EW_DX) {
             p0[i] = gamma[c] * rstd[c];          // k
             p1[i] = dbeta[c] * inv_m;            // a
             p2[i] = dgamma[c] * inv_m;           // b
             p3[i] = mean[c];
-        } else if (mode == EW_APPLY) {
+            p4[i] = rstd[c];
+        } else if (MODE == EW_APPLY) {
             p0[i] = gamma[c];
             p1[i] = beta[c];
             p2[i] = rstd[c];
             p3[i] = mean[c];
-        } else {
-            p0[i] = p1[i] = p2[i] = p3[i] = 0.f;
         }
     }
-    float rsd[VEC];
-    if (mode == EW_DX)
-        for (int i = 0; i < VEC; i++) rsd[i] = rstd[c0 + i];
-    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
-    const int64_t r1 = min(m, r0 + rows_per_block);
-    for (int64_t r = r0 + ty; r < r1; r += ry) {
+    auto row = [&](const vec16 &vx, const vec16 &v2, const vec16 &vo) __attribute__((always_inline)) {
         float f[VEC], g[VEC], o[VEC];
-        Elem<T>::unpack(ldg16(x + r * x_ldc + c0), f);
-        if (mode == EW_DX || mode == EW_RELUBWD) Elem<T>::unpack(ldg16(x2 + r * x2_ldc + c0), g);
-        T *dst = out + r * out_ldc + c0;
-        if (mode == EW_DX) {
+        Elem<T>::unpack(vx, f);
+        if (TWO) Elem<T>::unpack(v2, g);
+        if (MODE == EW_DX) {
             // f = dy, g = x
             for (int i = 0; i < VEC; i++) {
-                float xh = (g[i] - p3[i]) * rsd[i];
+                const float xh = (g[i] - p3[i]) * p4[i];
                 o[i] = p0[i] * (f[i] - p1[i] - xh * p2[i]);
             }
-            if (accumulate) {
+            if (ACC) {
                 float old[VEC];
-                Elem<T>::unpack(ldg16(dst), old);
+                Elem<T>::unpack(vo, old);
                 for (int i = 0; i < VEC; i++) o[i] += old[i];
             }
-        } else if (mode == EW_APPLY) {
+        } else if (MODE == EW_APPLY) {
             for (int i = 0; i < VEC; i++) o[i] = p0[i] * ((f[i] - p3[i]) * p2[i]) + p1[i];
-        } else if (mode == EW_RELU) {
+        } else if (MODE == EW_RELU) {
             for (int i = 0; i < VEC; i++) o[i] = f[i] > 0.f ? f[i] : 0.f;
         } else {
             for (int i = 0; i < VEC; i++) o[i] = g[i] > 0.f ? f[i] : 0.f;
         }
-        stg16(dst, Elem<T>::pack(o));
+        return Elem<T>::pack(o);
+    };
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r1 = min(m, r0 + rows_per_block);
+    int64_t r = r0 + ty;
+    for (; r + (U - 1) * ry < r1; r += U * ry) {
+        vec16 vx[U], v2[U], vo[U];
+        #pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t rr = r + u * ry;
+            vx[u] = ldg16(x + rr * x_ldc + c0);
+            v2[u] = TWO ? ldg16(x2 + rr * x2_ldc + c0) : vx[u];
+            vo[u] = ACC ? ldg16(out + rr * out_ldc + c0) : vx[u];
+        }
+        #pragma unroll
+        for (int u = 0; u < U; u++) stg16(out + (r + u * ry) * out_ldc + c0, row(vx[u], v2[u], vo[u]));
+    }
+    for (; r < r1; r += ry) {
+        const vec16 vx = ldg16(x + r * x_ldc + c0);
+        const vec16 v2 = TWO ? ldg16(x2 + r * x2_ldc + c0) : vx;
+        const vec16 vo = ACC ? ldg16(out + r * out_ldc + c0) : vx;
+        stg16(out + r * out_ldc + c0, row(vx, v2, vo));
     }
 }
 
@@ -295,16 +358,26 @@ __global__ __launch_bounds__(kThreads) void k_avgpool2_bwd(int n, int h, int w, 
 }
 
 // --------------------------------------------------------------------------
+// Streaming copy (HBM calibration): each workgroup copies one contiguous
+// range, four 16-byte vectors in flight per thread, non-temporal accesses.
 __global__ __launch_bounds__(kThreads) void k_copy16(const vec16 *__restrict__ src, vec16 *__restrict__ dst,
-                                                     int64_t nvec)
+                                                     int64_t nvec, int64_t per_block)
 {
-    const int64_t stride = (int64_t)gridDim.x * kThreads;
-    int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    for (; i + 3 * stride < nvec; i += 4 * stride) {
-        vec16 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
-        dst[i] = a; dst[i + stride] = b; dst[i + 2 * stride] = c; dst[i + 3 * stride] = d;
+    const int64_t b0 = (int64_t)blockIdx.x * per_block;
+    const int64_t b1 = b0 + per_block < nvec ? b0 + per_block : nvec;
+    int64_t i = b0 + threadIdx.x;
+    for (; i + 3 * kThreads < b1; i += 4 * kThreads) {
+        vec16 t[4];
+        #pragma unroll
+        for (int u = 0; u < 4; u++)
+            #pragma unroll
+            for (int k = 0; k < 4; k++) t[u].u[k] = __builtin_nontemporal_load(&src[i + u * kThreads].u[k]);
+        #pragma unroll
+        for (int u = 0; u < 4; u++)
+            #pragma unroll
+            for (int k = 0; k < 4; k++) __builtin_nontemporal_store(t[u].u[k], &dst[i + u * kThreads].u[k]);
     }
-    for (; i < nvec; i += stride) dst[i] = src[i];
+    for (; i < b1; i += kThreads) dst[i] = src[i];
 }
 
 // Sum of S float32 partial tiles, in two kernels.  Level 1, grid
@@ -354,12 +427,6 @@ __global__ __launch_bounds__(kThreads) void k_sum_partials2(const float *__restr
 // --------------------------------------------------------------- launchers --
 static inline int grid_cap(int64_t want) { return (int)(want < 4096 ? (want < 1 ? 1 : want) : 4096); }
 
-int stats_finalize_splits(int64_t R)
-{
-    int64_t rs = R / 64;
-    return (int)(rs < 1 ? 1 : (rs > kRedMaxRS ? kRedMaxRS : rs));
-}
-
 hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
                                 const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
                                 float *part, int64_t R, hipStream_t s)
@@ -369,15 +436,29 @@ hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m
         return hipErrorInvalidValue;
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
     const int64_t rpb = ceil_div(m, R);
-    dim3 grid((unsigned)R, (unsigned)cb);
+    dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
     const double es = dtype == DT_BF16 ? 2.0 : 4.0;
     TraceScope tr(KC_SWEEP, KID_STATS_SWEEP, s, (mode == ST_DYX ? 2.0 : 1.0) * (double)m * C * es, 0.0);
-    if (dtype == DT_BF16)
-        hipLaunchKernelGGL(k_stats_partial<bf16_t>, grid, dim3(kThreads), 0, s, (const bf16_t *)x, ldc, m, C, mode,
-                           mean, rstd, (const bf16_t *)dy, dy_ldc, rpb, part);
-    else
-        hipLaunchKernelGGL(k_stats_partial<float>, grid, dim3(kThreads), 0, s, (const float *)x, ldc, m, C, mode,
-                           mean, rstd, (const float *)dy, dy_ldc, rpb, part);
+    auto go = [&](auto kern, auto tag) {
+        using T = decltype(tag);
+        hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, (const T *)x, ldc, m, C, mean, rstd, (const T *)dy,
+                           dy_ldc, rpb, part);
+    };
+    if (dtype == DT_BF16) {
+        switch (mode) {
+        case ST_SUMSQ: go(k_stats_partial<bf16_t, ST_SUMSQ>, bf16_t()); break;
+        case ST_SUM: go(k_stats_partial<bf16_t, ST_SUM>, bf16_t()); break;
+        case ST_SQDEV: go(k_stats_partial<bf16_t, ST_SQDEV>, bf16_t()); break;
+        default: go(k_stats_partial<bf16_t, ST_DYX>, bf16_t()); break;
+        }
+    } else {
+        switch (mode) {
+        case ST_SUMSQ: go(k_stats_partial<float, ST_SUMSQ>, float()); break;
+        case ST_SUM: go(k_stats_partial<float, ST_SUM>, float()); break;
+        case ST_SQDEV: go(k_stats_partial<float, ST_SQDEV>, float()); break;
+        default: go(k_stats_partial<float, ST_DYX>, float()); break;
+        }
+    }
     return hipGetLastError();
 }
 
@@ -393,6 +474,12 @@ hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m,
     if (!part || !red || (mode == FIN_MVF && (!mean || !rstd)) || (mode == FIN_MEAN && !mean) ||
         (mode == FIN_VAR && !rstd) || (mode == FIN_BWD && (!dbeta || !dgamma)))
         return hipErrorInvalidValue;
+    if (R <= kCombineOneMaxRows) {
+        TraceScope tr(KC_SMALL, KID_COMBINE, s, (double)R * 2 * C * 4 + 3.0 * C * 4, 0.0);
+        hipLaunchKernelGGL(k_stats_combine_one, dim3((unsigned)ceil_div(C, 8)), dim3(kThreads), 0, s, part, R, C, m,
+                           mode, eps, mean, var, rstd, dbeta, dgamma);
+        return hipGetLastError();
+    }
     double *lvl1 = reinterpret_cast<double *>(red);
     const int RS = stats_combine_splits(R);
     {
@@ -416,19 +503,31 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
         (mode == EW_APPLY && (!gamma || !beta || !mean || !rstd)))
         return hipErrorInvalidValue;
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
-    const int64_t R = stats_row_blocks(m, C, dtype) * 2;
+    const int64_t R = stats_row_blocks(m, C, dtype) * 4;
     const int64_t rpb = ceil_div(m, R);
     dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
     const double sweeps = mode == EW_DX ? 3.0 + (accumulate ? 1.0 : 0.0) : (mode == EW_RELUBWD ? 3.0 : 2.0);
     TraceScope tr(KC_SWEEP, KID_ELEMENTWISE, s, sweeps * (double)m * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
-    if (dtype == DT_BF16)
-        hipLaunchKernelGGL(k_elementwise<bf16_t>, grid, dim3(kThreads), 0, s, mode, m, C, (const bf16_t *)x, x_ldc,
-                           (const bf16_t *)x2, x2_ldc, gamma, beta, mean, rstd, dgamma, dbeta, (bf16_t *)out,
-                           out_ldc, accumulate, rpb);
-    else
-        hipLaunchKernelGGL(k_elementwise<float>, grid, dim3(kThreads), 0, s, mode, m, C, (const float *)x, x_ldc,
-                           (const float *)x2, x2_ldc, gamma, beta, mean, rstd, dgamma, dbeta, (float *)out, out_ldc,
-                           accumulate, rpb);
+    auto go = [&](auto kern, auto tag) {
+        using T = decltype(tag);
+        hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, m, C, (const T *)x, x_ldc, (const T *)x2, x2_ldc, gamma,
+                           beta, mean, rstd, dgamma, dbeta, (T *)out, out_ldc, rpb);
+    };
+    if (dtype == DT_BF16) {
+        if (mode == EW_DX) {
+            if (accumulate) go(k_elementwise<bf16_t, EW_DX, true>, bf16_t());
+            else go(k_elementwise<bf16_t, EW_DX, false>, bf16_t());
+        } else if (mode == EW_APPLY) go(k_elementwise<bf16_t, EW_APPLY, false>, bf16_t());
+        else if (mode == EW_RELU) go(k_elementwise<bf16_t, EW_RELU, false>, bf16_t());
+        else go(k_elementwise<bf16_t, EW_RELUBWD, false>, bf16_t());
+    } else {
+        if (mode == EW_DX) {
+            if (accumulate) go(k_elementwise<float, EW_DX, true>, float());
+            else go(k_elementwise<float, EW_DX, false>, float());
+        } else if (mode == EW_APPLY) go(k_elementwise<float, EW_APPLY, false>, float());
+        else if (mode == EW_RELU) go(k_elementwise<float, EW_RELU, false>, float());
+        else go(k_elementwise<float, EW_RELUBWD, false>, float());
+    }
     return hipGetLastError();
 }
 
@@ -464,7 +563,9 @@ hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void
 hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s)
 {
     TraceScope tr(KC_SWEEP, KID_COPY, s, 32.0 * (double)nvec, 0.0);
-    hipLaunchKernelGGL(k_copy16, dim3(2048), dim3(kThreads), 0, s, (const vec16 *)src, (vec16 *)dst, nvec);
+    const int64_t per = ceil_div(nvec, 4096) < kThreads ? kThreads : ceil_div(nvec, 4096);
+    hipLaunchKernelGGL(k_copy16, dim3((unsigned)ceil_div(nvec, per)), dim3(kThreads), 0, s, (const vec16 *)src,
+                       (vec16 *)dst, nvec, per);
     return hipGetLastError();
 }
 

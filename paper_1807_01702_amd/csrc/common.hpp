@@ -61,6 +61,22 @@ __device__ __forceinline__ vec16 ldg16(const void *p) { return *reinterpret_cast
 __device__ __forceinline__ void stg16(void *p, const vec16 &v) { *reinterpret_cast<vec16 *>(p) = v; }
 __device__ __forceinline__ vec16 zero16() { vec16 v; v.u[0] = v.u[1] = v.u[2] = v.u[3] = 0; return v; }
 
+// Raw buffer view of [base, base + bytes) (bytes < 2^31).  A load at an
+// offset outside the range returns zeros in hardware, so operand loads need
+// neither a branch nor a zero-initialised destination (which would force the
+// compiler to wait for older memory operations before issuing them).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+constexpr uint32_t kBufOff = 0x80000000u;       // an offset that is always out of range
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_view(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ vec16 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    vec16 v;
+    v.u[0] = t.x; v.u[1] = t.y; v.u[2] = t.z; v.u[3] = t.w;
+    return v;
+}
+
 // Wave-level sum over the 64 lanes of a wave (all lanes get the result).
 __device__ __forceinline__ float wave_sum(float v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -16,6 +16,8 @@ enum { EW_DX = 0, EW_APPLY = 1, EW_RELU = 2, EW_RELUBWD = 3 };
 // Reduction scratch ("red") of a statistics combine: the float64 level-1
 // sums [RS][2][C] (RS <= kRedMaxRS row splits).
 constexpr int kRedMaxRS = 32;
+// Up to this many partial rows the combine runs as one kernel.
+constexpr int64_t kCombineOneMaxRows = 1024;
 inline size_t stats_red_bytes(int C) { return (size_t)kRedMaxRS * 2 * C * sizeof(double); }
 int stats_combine_splits(int64_t R);
 hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
@@ -39,6 +41,13 @@ hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float 
 // ---- implicit-GEMM CONV over pixel rows (forward / data gradient) ---------
 enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 4 };
 enum { EPI_STORE = 0, EPI_STATS = 1, EPI_BNBWD = 2, EPI_RELUMASK = 3 };
+// Compile-time epilogue kinds of the persistent CONV kernels (EPI_STORE splits
+// into plain store and read-add-store).
+enum { EK_STORE = 0, EK_STORE_ACC = 1, EK_STATS = 2, EK_RELUMASK = 3, EK_BNBWD = 4 };
+inline int epilogue_kind(int epi, int accumulate) {
+    return epi == EPI_STORE ? (accumulate ? EK_STORE_ACC : EK_STORE)
+                            : (epi == EPI_STATS ? EK_STATS : (epi == EPI_RELUMASK ? EK_RELUMASK : EK_BNBWD));
+}
 
 struct RowsParams {
     int dtype, taps, n, h, w;
@@ -51,7 +60,7 @@ struct RowsParams {
     int64_t a2_ldc;
     const float *p_gamma, *p_beta, *p_mean, *p_rstd, *p_dgamma, *p_dbeta;
     const void *wpack;            // weights packed by launch_pack_weights (conv_rows)
-    const void *wraw;             // weights in their [k][k][c_in][c_out] layout (persistent 1x1)
+    const void *wraw;             // weights in their [k][k][c_in][c_out] layout (persistent kernels)
     int wtrans;                   // 1: data-gradient operand (GEMM K = c_out, N = c_in)
     int epi;
     void *y;                      // output view (EPI_BNBWD: dy, dense)
@@ -74,6 +83,11 @@ hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s);
 bool conv1x1_supported(int dtype, int K, int N);
 int64_t conv1x1_partial_rows(int64_t m);      // statistics partial rows it writes
 hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s);
+
+// ---- persistent 3x3 CONV (weights and an input-row ring buffer in LDS) ----
+bool conv3x3_supported(int dtype, int K, int N, int W);
+int64_t conv3x3_partial_rows(int64_t m);      // statistics partial rows it writes
+hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s);
 
 // ---- weight gradient -------------------------------------------------------
 enum { GB_DENSE = 0, GB_BNGRAD = 1, GB_POOLUP = 2 };
