@@ -77,6 +77,12 @@ __device__ __forceinline__ vec16 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return v;
 }
 
+// Eight consecutive floats from a 32-byte aligned LDS address (two 16-byte reads).
+__device__ __forceinline__ void lds_f8(const float *p, float *f) {
+    const float4 a = reinterpret_cast<const float4 *>(p)[0], b = reinterpret_cast<const float4 *>(p)[1];
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+}
+
 // Wave-level sum over the 64 lanes of a wave (all lanes get the result).
 __device__ __forceinline__ float wave_sum(float v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

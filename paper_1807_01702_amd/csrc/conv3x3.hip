@@ -3,25 +3,29 @@
 // prologues and epilogues.
 //
 // One 512-thread workgroup per CU owns a contiguous range of pixel rows
-// [P0, P1) of the NHWC tensor (pixel = row of the GEMM) and keeps
-//   * the weights of all nine taps in LDS, read once from [kh][kw][ci][co]
-//     (transposed on load for the forward GEMM, taps flipped for the data
-//     gradient), and
-//   * a ring buffer of input rows: a 128-row output tile at p0 needs the rows
-//     [p0 - (W+1), p0 + 128 + W + 1); consecutive tiles share all but 128 of
-//     them, so each input row is read from HBM and transformed by the
-//     prologue once (no halo re-reads inside a workgroup).
+// [P0, P1) of the NHWC tensor (pixel = row of the GEMM).
+//   * Weights: each of the 8 waves owns a 32-channel slice of the GEMM K
+//     (input channels) and a 32-column slice of the outputs, and keeps the
+//     matrix-core fragments of that slice for all nine taps in registers
+//     (72 VGPRs), loaded once through LDS from [kh][kw][ci][co] (transposed for
+//     the forward GEMM, taps flipped for the data gradient).  The remaining
+//     8 / (K slices x N slices) waves split the 128 rows of a tile.
+//   * Inputs: a ring buffer of pixel rows in LDS.  A 128-row output tile at
+//     p0 needs the rows [p0 - (W+1), p0 + 128 + W + 1); consecutive tiles share
+//     all but 128 of them, so each input row is read from HBM and transformed
+//     by the prologue once (no halo re-reads inside a workgroup).
 // The 128 new rows of the next tile are loaded into registers while the
 // matrix cores work on the current tile, together with the epilogue operand
 // of the current tile.  Two waves per SIMD let one wave's prologue / epilogue
 // arithmetic overlap the other's matrix-core work.  Taps that fall outside
 // the image read a zero row of LDS: zero padding applies to the CONV input,
-// i.e. after BN and ReLU.
+// i.e. after BN and ReLU.  The float32 partial tiles of the K slices are
+// added in LDS in a fixed order.
 //
-// The epilogue stages the output tile through LDS so that every global access
-// is a 16-byte vector of one pixel row, and keeps the per-channel statistics
-// of the workgroup's rows in registers: one partial row per workgroup.
-// Prologue / epilogue modes are those of conv_rows.hip.
+// The epilogue reads whole 16-byte channel vectors of one pixel row, so every
+// global access is coalesced, and keeps the per-channel statistics of the
+// workgroup's rows in registers: one partial row per workgroup.  Prologue /
+// epilogue modes are those of conv_rows.hip.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "mfma.hpp"
@@ -34,62 +38,69 @@ constexpr int kP3Threads = 512;
 constexpr int kP3BM = 128;          // output rows per tile
 constexpr int kP3MaxW = 62;         // widest image row (ring = 128 + 2 (W + 1) rows)
 
+// LDS layout (bytes): [ring: ring rows, then copies of its first 16 rows (so
+// a 16-row fragment starting anywhere in the ring is contiguous), then one
+// zero row; lda bf16 per row]
+// [stage: weights Ws[9][NP][ldw] bf16 at the start; afterwards the float32
+// K-slice partial tiles red[WK][128][ldr] and finally the statistics scratch]
+// [coefficients: 5 KP + 4 NP floats].
 struct P3Geom {
-    int KP, NP, lda, ldw, ldc, ring;
-    size_t ring_bytes;              // ring rows + one zero row (also the final statistics scratch)
-    size_t lds;
+    int KP, NP, lda, ldw, ldr, ring;
+    size_t ring_bytes, stage_bytes, lds;
 };
 
-template <typename T>
 static P3Geom p3_geom(int K, int N, int W)
 {
-    const int PAD = 16 / (int)sizeof(T);
     P3Geom g;
     g.KP = (K + 31) / 32 * 32;
     g.NP = N <= 32 ? 32 : (N <= 64 ? 64 : 128);
-    g.lda = g.KP + PAD;
-    g.ldw = g.KP + PAD;
-    g.ldc = g.NP + PAD;
+    g.lda = g.KP + 8;
+    g.ldw = g.KP + 8;
+    g.ldr = g.NP + 4;
     g.ring = kP3BM + 2 * (W + 1);
-    const size_t red = (size_t)2 * (kP3Threads / (g.NP / (16 / sizeof(T)))) * g.NP * sizeof(float);
-    g.ring_bytes = (size_t)(g.ring + 1) * g.lda * sizeof(T);
-    if (red > g.ring_bytes) g.ring_bytes = red;
-    g.lds = (size_t)9 * g.NP * g.ldw * sizeof(T) + g.ring_bytes + (size_t)kP3BM * g.ldc * sizeof(T) +
-            (size_t)(5 * g.KP + 4 * g.NP) * sizeof(float);
+    g.ring_bytes = (size_t)(g.ring + 16 + 1) * g.lda * 2;
+    const size_t wst = (size_t)9 * g.NP * g.ldw * 2;
+    const size_t red = (size_t)(g.KP / 32) * kP3BM * g.ldr * 4;
+    const size_t stats = (size_t)2 * (kP3Threads / (g.NP / 8)) * g.NP * 4;
+    g.stage_bytes = wst > red ? wst : red;
+    if (stats > g.stage_bytes) g.stage_bytes = stats;
+    g.lds = g.ring_bytes + g.stage_bytes + (size_t)(5 * g.KP + 4 * g.NP) * 4;
     return g;
 }
 
-// NPC: output columns (32, 64 or 128); WM: waves along the 128 tile rows
-// (8 or 4; the other 8 / WM waves split the columns).  The epilogue kind EK
-// and whether the prologue reads a second operand (PRO_BNGRAD) are
-// compile-time, so the epilogue is straight-line code and the compiler can
-// keep the next tile's loads in flight while it waits for the epilogue
-// operand (a runtime mode switch makes it wait for every outstanding load at
-// each branch).
-template <typename T, int NPC, int WM, int EK, bool BNG>
+// WK x WN: 32-channel K slices x 32-column N slices (one per wave); the
+// other 8 / (WK WN) waves split the tile rows.  The epilogue kind EK and
+// whether the prologue reads a second operand (PRO_BNGRAD) are compile-time,
+// so the epilogue is straight-line code and the compiler can keep the next
+// tile's loads in flight while it waits for the epilogue operand (a runtime
+// mode switch makes it wait for every outstanding load at each branch).
+template <int WK, int WN, int EK, bool BNG>
 __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
 {
+    using T = bf16_t;
     using M = Mfma<T>;
-    constexpr int VEC = Elem<T>::VEC;
-    constexpr int WN = 8 / WM;
-    constexpr int RB = kP3BM / (16 * WM);                        // 16-row blocks per wave
-    constexpr int CBW = NPC / (16 * WN);                         // 16-column blocks per wave
+    constexpr int VEC = 8;
+    constexpr int KPC = 32 * WK, NPC = 32 * WN;
+    constexpr int WR = 8 / (WK * WN);                            // row groups
+    constexpr int RB = kP3BM / (16 * WR);                        // 16-row blocks per wave
     constexpr int VPRO = NPC / VEC, RSTEP = kP3Threads / VPRO;
-    constexpr int RPT = kP3BM / RSTEP > 0 ? kP3BM / RSTEP : 1;   // epilogue rows per thread
+    constexpr int RPT = kP3BM / RSTEP;                           // epilogue rows per thread
     constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD;
-    constexpr int NVA = kP3BM * (128 / VEC) / kP3Threads;       // up to 128 input channels
+    constexpr int NVA = (kP3BM * (KPC / VEC) + kP3Threads - 1) / kP3Threads;
     constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1;
-    static_assert(RB >= 1 && CBW >= 1, "wave layout");
+    static_assert(WR * WK * WN == 8 && RPT >= 1, "wave layout");
     extern __shared__ __align__(16) unsigned char smem[];
-    T *Ws = reinterpret_cast<T *>(smem);                         // [9][NP][ldw]
-    T *ring = Ws + (size_t)9 * NPC * g.ldw;                      // [ring + 1][lda]; row `ring` is zero
-    T *Cs = reinterpret_cast<T *>(reinterpret_cast<unsigned char *>(ring) + g.ring_bytes);   // [BM][ldc]
-    float *coef = reinterpret_cast<float *>(Cs + (size_t)kP3BM * g.ldc);
-    float *epi = coef + 5 * g.KP;
+    T *ring = reinterpret_cast<T *>(smem);                       // [ring + 16 + 1][lda]
+    unsigned char *stage = smem + g.ring_bytes;
+    T *Ws = reinterpret_cast<T *>(stage);                        // [9][NP][ldw] (start only)
+    float *red = reinterpret_cast<float *>(stage);               // [WK][BM][ldr]
+    float *coef = reinterpret_cast<float *>(stage + g.stage_bytes);
+    float *epi = coef + 5 * KPC;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave % WM, wn = wave / WM;
-    const int K = p.K, N = p.N, KP = g.KP, RING = g.ring;
+    const int wr = wave % WR, wk = (wave / WR) % WK, wn = wave / (WR * WK);
+    const int K = p.K, N = p.N, RING = g.ring, lda = g.lda, ldr = g.ldr;
+    const int ZROW = RING + 16;                                  // the zero row
     const int m = (int)p.m;                                      // launcher: m < 2^30
     const int H = p.h, W = p.w, H1 = W + 1;
     const int P0 = (int)((int64_t)blockIdx.x * m / gridDim.x), P1 = (int)((int64_t)(blockIdx.x + 1) * m / gridDim.x);
@@ -103,19 +114,18 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * ES) : 0u);
 
-    // ---- weights -> LDS as Ws[tap][n][k] (zero outside K x N) ----
+    // ---- weights -> LDS stage as Ws[tap][n][k] (zero outside K x N) ----
     if (!p.wtrans) {      // forward: W[tap][k][n] (k = c_in, n = c_out); scatter columns
-        for (int i = tid; i < 9 * KP * VPRO; i += kP3Threads) {
-            const int tap = i / (KP * VPRO), rem = i % (KP * VPRO);
+        for (int i = tid; i < 9 * KPC * VPRO; i += kP3Threads) {
+            const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
             const int k = rem / VPRO, n0 = (rem % VPRO) * VEC;
-            float f[VEC];
-            if (k < K && n0 < N) Elem<T>::unpack(ldg16(wsrc + ((int64_t)tap * K + k) * N + n0), f);
-            else for (int e = 0; e < VEC; e++) f[e] = 0.f;
+            const vec16 v = (k < K && n0 < N) ? ldg16(wsrc + ((int64_t)tap * K + k) * N + n0) : zero16();
+            const T *h = reinterpret_cast<const T *>(&v);
             #pragma unroll
-            for (int e = 0; e < VEC; e++) Ws[(tap * NPC + n0 + e) * g.ldw + k] = to_store<T>(f[e]);
+            for (int e = 0; e < VEC; e++) Ws[(tap * NPC + n0 + e) * g.ldw + k] = h[e];
         }
     } else {              // data gradient: W[8 - tap][n][k] (n = c_in, k = c_out); rows copy straight
-        const int VPK = KP / VEC;
+        constexpr int VPK = KPC / VEC;
         for (int i = tid; i < 9 * NPC * VPK; i += kP3Threads) {
             const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
             const int n = rem / VPK, k0 = (rem % VPK) * VEC;
@@ -123,12 +133,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             *reinterpret_cast<vec16 *>(Ws + (tap * NPC + n) * g.ldw + k0) = v;
         }
     }
-    for (int i = tid; i < KP / VEC; i += kP3Threads)               // the zero row
-        *reinterpret_cast<vec16 *>(ring + (size_t)RING * g.lda + i * VEC) = zero16();
+    for (int i = tid; i < KPC / VEC; i += kP3Threads)              // the zero row
+        *reinterpret_cast<vec16 *>(ring + (size_t)ZROW * lda + i * VEC) = zero16();
     // ---- per-channel prologue / epilogue parameters ----
     //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
     //   BNGRAD: d = c2 * (dy - c3 - (x - c0) * c1 * c4)
-    for (int c = tid; c < KP; c += kP3Threads) {
+    for (int c = tid; c < KPC; c += kP3Threads) {
         float c0 = 0.f, c1 = 0.f, c2 = 0.f, c3 = 0.f, c4 = 0.f;
         if (c < K && p.pro == PRO_BNRELU) {
             c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
@@ -137,20 +147,36 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             c0 = p.p_mean[c]; c1 = p.p_rstd[c]; c2 = p.p_gamma[c] * p.p_rstd[c];
             c3 = p.p_dbeta[c] * inv_m; c4 = p.p_dgamma[c] * inv_m;
         }
-        coef[c] = c0; coef[KP + c] = c1; coef[2 * KP + c] = c2; coef[3 * KP + c] = c3; coef[4 * KP + c] = c4;
+        coef[c] = c0; coef[KPC + c] = c1; coef[2 * KPC + c] = c2; coef[3 * KPC + c] = c3; coef[4 * KPC + c] = c4;
     }
     for (int c = tid; c < NPC; c += kP3Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
         if (c < N && EK == EK_BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
         epi[c] = e0; epi[NPC + c] = e1; epi[2 * NPC + c] = e2; epi[3 * NPC + c] = e3;
     }
+    __syncthreads();
+    // this wave's weight fragments: K slice wk, columns wn*32 + {0, 16}, nine taps
+    typename M::frag bfr[9][2];
+    #pragma unroll
+    for (int tap = 0; tap < 9; tap++)
+        #pragma unroll
+        for (int cb = 0; cb < 2; cb++)
+            bfr[tap][cb] = M::load(Ws + (tap * NPC + wn * 32 + cb * 16 + (lane & 15)) * g.ldw + wk * 32 +
+                                   (lane >> 4) * M::KPL);
+    // epilogue channels of this thread are fixed: BN parameters in registers
+    const int v = tid % VPRO, r0 = tid / VPRO;
+    const int n = v * VEC;
+    const bool col_ok = n < N;
+    float eM[VEC], eR[VEC], eG[VEC], eB[VEC];
+    #pragma unroll
+    for (int e = 0; e < VEC; e++) {
+        eM[e] = epi[n + e]; eR[e] = epi[NPC + n + e]; eG[e] = epi[2 * NPC + n + e]; eB[e] = epi[3 * NPC + n + e];
+    }
 
     // ---- input batches: up to 128 consecutive rows, loaded to registers ----
     // Slot j of this thread: 4 consecutive lanes cover 4 channel vectors of
     // one row, 16 lane groups 16 rows (4 distinct coefficient addresses per
     // wave: LDS broadcast).
-    const int VPR = KP / VEC;
-    const int nva = (kP3BM * VPR + kP3Threads - 1) / kP3Threads;
     int sr[NVA], sc[NVA];
     #pragma unroll
     for (int j = 0; j < NVA; j++) {
@@ -164,7 +190,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
             const int q = q0 + sr[j];
-            const bool ok = j < nva && sc[j] < K && sr[j] < cnt && q >= 0 && q < m;
+            const bool ok = sc[j] < K && sr[j] < cnt && q >= 0 && q < m;
             ra[j] = bld16(abuf, ok ? (uint32_t)(q * a_ldc + sc[j]) * ES : kBufOff);
             if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(q * a2_ldc + sc[j]) * ES : kBufOff);
         }
@@ -173,7 +199,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
             const int r = sr[j], c = sc[j];
-            if (j >= nva || c >= KP || r >= cnt) continue;
+            if (c >= KPC || r >= cnt) continue;
             const int q = q0 + r;
             const bool valid = q >= 0 && q < m && c < K;
             vec16 out = ra[j];
@@ -181,21 +207,29 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 float f[VEC];
                 Elem<T>::unpack(ra[j], f);
                 if (p.pro == PRO_BNRELU) {
+                    float ca[VEC], cb[VEC];
+                    lds_f8(coef + c, ca);
+                    lds_f8(coef + KPC + c, cb);
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) {
-                        const float t = __builtin_fmaf(f[e], coef[c + e], coef[KP + c + e]);
+                        const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
                         f[e] = valid && t > 0.f ? t : 0.f;
                     }
                 } else if (p.pro == PRO_RELU) {
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
                 } else if (BNG && p.pro == PRO_BNGRAD) {
-                    float x[VEC];
+                    float x[VEC], c0[VEC], c1[VEC], c2[VEC], c3[VEC], c4[VEC];
                     Elem<T>::unpack(rb[j < NVB ? j : 0], x);
+                    lds_f8(coef + c, c0);
+                    lds_f8(coef + KPC + c, c1);
+                    lds_f8(coef + 2 * KPC + c, c2);
+                    lds_f8(coef + 3 * KPC + c, c3);
+                    lds_f8(coef + 4 * KPC + c, c4);
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) {
-                        const float xh = (x[e] - coef[c + e]) * coef[KP + c + e];
-                        const float d = coef[2 * KP + c + e] * (f[e] - coef[3 * KP + c + e] - xh * coef[4 * KP + c + e]);
+                        const float xh = (x[e] - c0[e]) * c1[e];
+                        const float d = c2[e] * (f[e] - c3[e] - xh * c4[e]);
                         f[e] = valid ? d : 0.f;
                     }
                 }
@@ -203,14 +237,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             }
             int s = slot0 + r;
             if (s >= RING) s -= RING;
-            *reinterpret_cast<vec16 *>(ring + s * g.lda + c) = out;
+            *reinterpret_cast<vec16 *>(ring + s * lda + c) = out;
+            if (s < 16) *reinterpret_cast<vec16 *>(ring + (s + RING) * lda + c) = out;
         }
     };
 
-    // ---- epilogue mapping: thread = one channel vector of rows r0, r0+RSTEP, ... ----
-    const int v = tid % VPRO, r0 = tid / VPRO;
-    const int n = v * VEC;
-    const bool col_ok = n < N;
+    // ---- epilogue operand: thread = one channel vector of rows r0, r0+RSTEP, ... ----
     vec16 rx[NVX];
     float s1[VEC], s2[VEC];
     #pragma unroll
@@ -227,13 +259,6 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             else rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * ES : kBufOff);
         }
     };
-
-    __syncthreads();
-    float eM[VEC], eR[VEC], eG[VEC], eB[VEC];
-    #pragma unroll
-    for (int e = 0; e < VEC; e++) {
-        eM[e] = epi[n + e]; eR[e] = epi[NPC + n + e]; eG[e] = epi[2 * NPC + n + e]; eB[e] = epi[3 * NPC + n + e];
-    }
 
     // ---- ring fill: rows [P0 - H1, P0 + H1) ----
     int L = P0 - H1;                // next input row to load; its ring slot is slotL
@@ -264,58 +289,59 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         cnt = P1 + H1 - L < kP3BM ? P1 + H1 - L : kP3BM;
         if (cnt > 0) load_rows(L, cnt);
 
-        // ---- matrix cores: (16 RB) rows x (16 CBW) columns per wave, nine taps ----
-        int hh[RB], ww[RB], rw[RB];
+        // ---- matrix cores: 16 RB rows x 32 columns x 32 K per wave, nine taps ----
+        // tap validity of this lane's rows as 9-bit masks (bit 3 (dh+1) + dw+1)
+        unsigned vmask[RB];
         #pragma unroll
         for (int ib = 0; ib < RB; ib++) {
-            rw[ib] = wm * 16 * RB + ib * 16 + (lane & 15);
-            const int pp = p0 + rw[ib];
-            ww[ib] = pp % W;
-            hh[ib] = (pp / W) % H;
-        }
-        f32x4 acc[RB][CBW];
-        #pragma unroll
-        for (int ib = 0; ib < RB; ib++)
+            const int r = wr * 16 * RB + ib * 16 + (lane & 15);
+            const int pp = p0 + r;
+            const int x = pp % W, y = (pp / W) % H;
+            const unsigned rows = (y > 0 ? 1u : 0u) | 2u | (y < H - 1 ? 4u : 0u);
+            const unsigned cols = (x > 0 ? 1u : 0u) | 2u | (x < W - 1 ? 4u : 0u);
+            unsigned mk = 0;
             #pragma unroll
-            for (int cb = 0; cb < CBW; cb++) acc[ib][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int t = 0; t < 9; t++)
+                mk |= ((rows >> (t / 3)) & (cols >> (t % 3)) & 1u) << t;
+            vmask[ib] = r < nrows ? mk : 0u;
+        }
+        f32x4 acc[RB][2];
+        #pragma unroll
+        for (int ib = 0; ib < RB; ib++) {
+            acc[ib][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+            acc[ib][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        const int kofs = wk * 32 + (lane >> 4) * M::KPL;
+        // first ring row of this wave's rows (wave-uniform)
+        const int ubase = sb + __builtin_amdgcn_readfirstlane(wr) * 16 * RB;
+        #pragma unroll
         for (int tap = 0; tap < 9; tap++) {
-            const int dh = tap / 3 - 1, dw = tap % 3 - 1;
-            const int off = dh * W + dw;
-            const T *arow[RB];
+            const int off = (tap / 3 - 1) * W + (tap % 3 - 1);
             #pragma unroll
             for (int ib = 0; ib < RB; ib++) {
-                int s = sb + rw[ib] + off;
-                if (s < 0) s += RING;
-                if (s >= RING) s -= RING;
-                const bool ok = rw[ib] < nrows && (unsigned)(hh[ib] + dh) < (unsigned)H &&
-                                (unsigned)(ww[ib] + dw) < (unsigned)W;
-                arow[ib] = ring + (ok ? s : RING) * g.lda + (lane >> 4) * M::KPL;
-            }
-            const T *brow = Ws + (tap * NPC + wn * 16 * CBW + (lane & 15)) * g.ldw + (lane >> 4) * M::KPL;
-            for (int k0 = 0; k0 < KP; k0 += M::KSTEP) {
-                typename M::frag a[RB];
-                #pragma unroll
-                for (int ib = 0; ib < RB; ib++) a[ib] = M::load(arow[ib] + k0);
-                #pragma unroll
-                for (int cb = 0; cb < CBW; cb++) {
-                    const typename M::frag b = M::load(brow + cb * 16 * g.ldw + k0);
-                    #pragma unroll
-                    for (int ib = 0; ib < RB; ib++) M::mma(acc[ib][cb], a[ib], b);
-                }
+                int u = ubase + ib * 16 + off;
+                u = u < 0 ? u + RING : (u >= RING ? u - RING : u);
+                if (u >= RING) u -= RING;
+                const int s = ((vmask[ib] >> tap) & 1u) ? u + (lane & 15) : ZROW;
+                const typename M::frag a = M::load(ring + s * lda + kofs);
+                M::mma(acc[ib][0], a, bfr[tap][0]);
+                M::mma(acc[ib][1], a, bfr[tap][1]);
             }
         }
+        // ---- float32 partial tile of this K slice -> LDS ----
         #pragma unroll
         for (int ib = 0; ib < RB; ib++)
             #pragma unroll
-            for (int cb = 0; cb < CBW; cb++)
+            for (int cb = 0; cb < 2; cb++)
                 #pragma unroll
                 for (int i = 0; i < 4; i++) {
-                    const int row = wm * 16 * RB + ib * 16 + (lane >> 4) * 4 + i;
-                    const int col = wn * 16 * CBW + cb * 16 + (lane & 15);
-                    Cs[row * g.ldc + col] = to_store<T>(acc[ib][cb][i]);
+                    const int row = wr * 16 * RB + ib * 16 + (lane >> 4) * 4 + i;
+                    const int col = wn * 32 + cb * 16 + (lane & 15);
+                    red[(wk * kP3BM + row) * ldr + col] = acc[ib][cb][i];
                 }
         __syncthreads();
-        // ---- epilogue row pass: all outputs of this thread first (no branch,
+        // ---- epilogue row pass: sum of the K slices (fixed order), rounded to
+        // the storage type; all outputs of this thread first (no branch,
         // invalid rows contribute zeros), then the stores back to back ----
         {
             vec16 vo[RPT];
@@ -323,8 +349,17 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             for (int j = 0; j < RPT; j++) {
                 const int r = r0 + j * RSTEP;
                 const bool ok = col_ok && r < nrows;
-                const vec16 cv = *reinterpret_cast<const vec16 *>(Cs + (r < kP3BM ? r : 0) * g.ldc + n);
                 float f[VEC];
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] = 0.f;
+                #pragma unroll
+                for (int q = 0; q < WK; q++) {
+                    const float4 *src = reinterpret_cast<const float4 *>(red + (q * kP3BM + r) * ldr + n);
+                    const float4 lo = src[0], hi = src[1];
+                    f[0] += lo.x; f[1] += lo.y; f[2] += lo.z; f[3] += lo.w;
+                    f[4] += hi.x; f[5] += hi.y; f[6] += hi.z; f[7] += hi.w;
+                }
+                const vec16 cv = Elem<T>::pack(f);
                 Elem<T>::unpack(cv, f);
                 vo[j] = cv;
                 if (EK == EK_STORE_ACC) {
@@ -374,7 +409,6 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
 
     // ---- per-workgroup statistics partial row ----
     if (EK == EK_STATS || EK == EK_BNBWD) {
-        float *red = reinterpret_cast<float *>(ring);
         #pragma unroll
         for (int e = 0; e < VEC; e++) {
             red[r0 * NPC + n + e] = s1[e];
@@ -406,7 +440,10 @@ static int p3_cus()
 bool conv3x3_supported(int dtype, int K, int N, int W)
 {
     if (dtype != DT_BF16 || K > 128 || N > 128 || W > kP3MaxW || W < 1) return false;
-    return p3_geom<bf16_t>(K, N, W).lds <= 160 * 1024;
+    const P3Geom g = p3_geom(K, N, W);
+    const int wk = g.KP / 32, wn = g.NP / 32;
+    if (wk == 3 || wk * wn > 4) return false;      // at most 64 rows x 2 column blocks of accumulators per wave
+    return g.lds <= 160 * 1024;
 }
 
 int64_t conv3x3_partial_rows(int64_t m)
@@ -416,12 +453,10 @@ int64_t conv3x3_partial_rows(int64_t m)
     return tiles < g ? tiles : g;
 }
 
-template <int NPC, int EK, bool BNG>
+template <int WK, int WN, int EK, bool BNG>
 static hipError_t run_p3(const RowsParams &p, const P3Geom &g, hipStream_t s)
 {
-    // 32 output columns: eight waves of 16 rows; wider: 4 x 2 waves of 32 rows
-    constexpr int WM = NPC == 32 ? 8 : 4;
-    auto kern = k_conv3x3<bf16_t, NPC, WM, EK, BNG>;
+    auto kern = k_conv3x3<WK, WN, EK, BNG>;
     static bool attr_set = false;
     if (!attr_set) {
         const hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
@@ -439,13 +474,19 @@ static hipError_t run_p3(const RowsParams &p, const P3Geom &g, hipStream_t s)
     return hipGetLastError();
 }
 
+// (K slices, N slices) with WK * WN <= 4, WK in {1, 2, 4}
 template <int EK, bool BNG>
-static hipError_t run_p3_np(const RowsParams &p, const P3Geom &g, hipStream_t s)
+static hipError_t run_p3_shape(const RowsParams &p, const P3Geom &g, hipStream_t s)
 {
-    switch (g.NP) {
-    case 32: return run_p3<32, EK, BNG>(p, g, s);
-    case 64: return run_p3<64, EK, BNG>(p, g, s);
-    default: return run_p3<128, EK, BNG>(p, g, s);
+    const int wk = g.KP / 32, wn = g.NP / 32;
+    switch (wk * 8 + wn) {
+    case 1 * 8 + 1: return run_p3<1, 1, EK, BNG>(p, g, s);
+    case 1 * 8 + 2: return run_p3<1, 2, EK, BNG>(p, g, s);
+    case 1 * 8 + 4: return run_p3<1, 4, EK, BNG>(p, g, s);
+    case 2 * 8 + 1: return run_p3<2, 1, EK, BNG>(p, g, s);
+    case 2 * 8 + 2: return run_p3<2, 2, EK, BNG>(p, g, s);
+    case 4 * 8 + 1: return run_p3<4, 1, EK, BNG>(p, g, s);
+    default: return hipErrorInvalidValue;
     }
 }
 
@@ -453,11 +494,11 @@ template <bool BNG>
 static hipError_t run_p3_ek(const RowsParams &p, const P3Geom &g, int ek, hipStream_t s)
 {
     switch (ek) {
-    case EK_STORE: return run_p3_np<EK_STORE, BNG>(p, g, s);
-    case EK_STORE_ACC: return run_p3_np<EK_STORE_ACC, BNG>(p, g, s);
-    case EK_STATS: return run_p3_np<EK_STATS, BNG>(p, g, s);
-    case EK_RELUMASK: return run_p3_np<EK_RELUMASK, BNG>(p, g, s);
-    default: return run_p3_np<EK_BNBWD, BNG>(p, g, s);
+    case EK_STORE: return run_p3_shape<EK_STORE, BNG>(p, g, s);
+    case EK_STORE_ACC: return run_p3_shape<EK_STORE_ACC, BNG>(p, g, s);
+    case EK_STATS: return run_p3_shape<EK_STATS, BNG>(p, g, s);
+    case EK_RELUMASK: return run_p3_shape<EK_RELUMASK, BNG>(p, g, s);
+    default: return run_p3_shape<EK_BNBWD, BNG>(p, g, s);
     }
 }
 
@@ -477,7 +518,7 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
     if (p.m >= (lim >> 1) || (p.m * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
-    const P3Geom g = p3_geom<bf16_t>(p.K, p.N, p.w);
+    const P3Geom g = p3_geom(p.K, p.N, p.w);
     const int ek = epilogue_kind(p.epi, p.accumulate);
     if (p.pro == PRO_BNGRAD) return run_p3_ek<true>(p, g, ek, s);
     return run_p3_ek<false>(p, g, ek, s);
