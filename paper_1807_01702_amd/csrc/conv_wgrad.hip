@@ -300,12 +300,289 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 weight gradient with transposing LDS reads (gfx950 ds_read_b64_tr_b16).
+// Z and G are staged row-major exactly as they arrive from HBM (one row per K
+// position, 16-byte channel vectors), after the prologue transform; a
+// matrix-core fragment (8 consecutive K positions of one channel per lane) is
+// two transposing 8-byte reads.  Within a group of 16 lanes, lane j reads the
+// 4 channels 4 (j % 4) .. +3 of row j / 4 and lane i receives channel i of
+// rows 0..3 (layout checked on the device).  For 3x3 every tap is a row
+// offset into the staged Z, so all nine taps share the G fragments.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+__device__ __forceinline__ bf16x8 tr_frag(const bf16_t *p, int pitch)
+{
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p + 4 * pitch));
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int TAPS, int CIT, int COT, int WCI, int GS>
+__global__ __launch_bounds__(kThreads) void k_wgrad_tr(WgradParams p, WgTrPlan pl)
+{
+    using T = bf16_t;
+    using M = Mfma<T>;
+    constexpr int VEC = 8;
+    constexpr int WCO = 4 / WCI;
+    constexpr int RB = CIT / 16 / WCI, CB = COT / 16 / WCO;
+    constexpr int ZP = CIT + 8, GP = COT + 8;                     // LDS row pitches (elements)
+    constexpr int VZ = CIT / VEC, VG = COT / VEC;                 // vectors per staged row
+    constexpr int KQMAX = 128;
+    constexpr int ZRMAX = TAPS == 3 ? KQMAX + 2 * (kWgMaxW3 + 2) + 2 : KQMAX;
+    constexpr int NZ = (ZRMAX * VZ + kThreads - 1) / kThreads;
+    constexpr int NG = (KQMAX * VG + kThreads - 1) / kThreads;
+    constexpr int NGX = GS == GB_BNGRAD ? NG : 1;
+    static_assert(WCI * WCO == 4 && RB >= 1 && CB >= 1, "wave layout");
+    extern __shared__ __align__(16) unsigned char smem[];
+    T *Zs = reinterpret_cast<T *>(smem);                          // [zrows][ZP]
+    T *Gs = Zs + (size_t)pl.zrows * ZP;                           // [KQ][GP]
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wci = wave % WCI, wco = wave / WCI;
+    const int n_out = pl.ci_tiles * pl.co_tiles;
+    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    const int ot = lid % n_out, split = lid / n_out;
+    const int co_t = ot % pl.co_tiles, ci_t = ot / pl.co_tiles;
+    const int ci0 = ci_t * CIT, co0 = co_t * COT;
+    const int C_in = p.c_in, C_out = p.c_out, H = p.h, W = p.w;
+    const int64_t m = p.m;
+    const int PW = pl.PW, KQ = pl.KQ, ZR = pl.zrows;
+
+    // per-thread channel vectors (fixed: 256 is a multiple of VZ and VG)
+    const int vz = tid % VZ, vg = tid % VG;
+    const int cz = ci0 + vz * VEC, cg = co0 + vg * VEC;
+    const bool zc_ok = cz < C_in, gc_ok = cg < C_out;
+    float za[VEC], zb[VEC], gA[VEC], gB[VEC], gC[VEC];
+    #pragma unroll
+    for (int e = 0; e < VEC; e++) {
+        za[e] = 1.f; zb[e] = 0.f; gA[e] = 1.f; gB[e] = 0.f; gC[e] = 0.f;
+        if (p.a_mode == 1 && zc_ok) {
+            za[e] = p.a_gamma[cz + e] * p.a_rstd[cz + e];
+            zb[e] = p.a_beta[cz + e] - p.a_mean[cz + e] * za[e];
+        }
+        if (GS == GB_BNGRAD && gc_ok) {
+            // d = k (dy - dbeta/m - (x - mean) rstd dgamma/m) = A dy + B x + C
+            const float inv_m = 1.0f / (float)m;
+            const float k = p.g_gamma[cg + e] * p.g_rstd[cg + e];
+            const float b = p.g_dgamma[cg + e] * inv_m * p.g_rstd[cg + e];
+            gA[e] = k;
+            gB[e] = -k * b;
+            gC[e] = k * (b * p.g_mean[cg + e] - p.g_dbeta[cg + e] * inv_m);
+        }
+    }
+
+    // raw-buffer views (launcher: every span below 2^31 bytes)
+    const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.x, (uint32_t)(((m - 1) * p.x_ldc + C_in) * 2));
+    const int64_t gpix = GS == GB_POOLUP ? m / 4 : m;
+    const __amdgpu_buffer_rsrc_t gbuf = buf_view(p.g, (uint32_t)(((gpix - 1) * p.g_ldc + C_out) * 2));
+    const __amdgpu_buffer_rsrc_t gxbuf = buf_view(GS == GB_BNGRAD ? p.gx : p.g,
+                                                  GS == GB_BNGRAD ? (uint32_t)(((m - 1) * p.gx_ldc + C_out) * 2) : 0u);
+
+    // position -> pixel of a chunk (-1: zero position)
+    auto chunk_base = [&](int64_t ch, int64_t &img, int &h0) __attribute__((always_inline)) {
+        if (TAPS == 3) {
+            img = ch / pl.chunks_per_image;
+            h0 = (int)(ch - img * pl.chunks_per_image) * pl.R;
+        } else {
+            img = ch;
+            h0 = 0;
+        }
+    };
+    auto pix = [&](int64_t img, int h0, int q, bool gside) __attribute__((always_inline)) -> int64_t {
+        if (TAPS == 1) {
+            const int64_t pp = img * KQMAX + q;
+            return q < KQ && pp < m ? pp : -1;
+        }
+        const int r = (q + 2 * PW) / PW - 2;                      // floor(q / PW) for q >= -2 PW
+        const int col = q - r * PW;
+        const int h = h0 + r;
+        if (gside && r >= pl.R) return -1;
+        if (h < 0 || h >= H || col < 1 || col > W) return -1;
+        return (img * H + h) * W + (col - 1);
+    };
+
+    vec16 zr[NZ], gr[NG], gx[NGX];
+    auto load_chunk = [&](int64_t ch) __attribute__((always_inline)) {
+        int64_t img; int h0;
+        chunk_base(ch, img, h0);
+        #pragma unroll
+        for (int j = 0; j < NZ; j++) {
+            const int row = tid / VZ + j * (kThreads / VZ);
+            const int64_t q = row < ZR ? pix(img, h0, TAPS == 3 ? row - (PW + 1) : row, false) : -1;
+            zr[j] = bld16(xbuf, q >= 0 && zc_ok ? (uint32_t)((q * p.x_ldc + cz) * 2) : kBufOff);
+        }
+        #pragma unroll
+        for (int j = 0; j < NG; j++) {
+            const int row = tid / VG + j * (kThreads / VG);
+            const int64_t q = row < KQ ? pix(img, h0, row, true) : -1;
+            const bool ok = q >= 0 && gc_ok;
+            if (GS == GB_POOLUP) {
+                const int64_t im = q / ((int64_t)H * W);
+                const int rem = (int)(q - im * H * W);
+                const int y = rem / W, xx = rem - y * W;
+                const int64_t qq = (im * (H / 2) + y / 2) * (W / 2) + xx / 2;
+                gr[j] = bld16(gbuf, ok ? (uint32_t)((qq * p.g_ldc + cg) * 2) : kBufOff);
+            } else {
+                gr[j] = bld16(gbuf, ok ? (uint32_t)((q * p.g_ldc + cg) * 2) : kBufOff);
+            }
+            if (GS == GB_BNGRAD) gx[j < NGX ? j : 0] = bld16(gxbuf, ok ? (uint32_t)((q * p.gx_ldc + cg) * 2) : kBufOff);
+        }
+    };
+    auto store_chunk = [&](int64_t ch) __attribute__((always_inline)) {
+        int64_t img; int h0;
+        chunk_base(ch, img, h0);
+        #pragma unroll
+        for (int j = 0; j < NZ; j++) {
+            const int row = tid / VZ + j * (kThreads / VZ);
+            if (row >= ZR) continue;
+            vec16 out = zr[j];
+            if (p.a_mode != 0) {
+                const bool valid = pix(img, h0, TAPS == 3 ? row - (PW + 1) : row, false) >= 0 && zc_ok;
+                float f[VEC];
+                Elem<T>::unpack(zr[j], f);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) {
+                    const float t = p.a_mode == 1 ? __builtin_fmaf(f[e], za[e], zb[e]) : f[e];
+                    f[e] = valid && t > 0.f ? t : 0.f;
+                }
+                out = Elem<T>::pack(f);
+            }
+            *reinterpret_cast<vec16 *>(Zs + row * ZP + vz * VEC) = out;
+        }
+        #pragma unroll
+        for (int j = 0; j < NG; j++) {
+            const int row = tid / VG + j * (kThreads / VG);
+            if (row >= KQ) continue;
+            vec16 out = gr[j];
+            if (GS == GB_BNGRAD) {
+                const bool valid = pix(img, h0, row, true) >= 0 && gc_ok;
+                float d[VEC], x[VEC];
+                Elem<T>::unpack(gr[j], d);
+                Elem<T>::unpack(gx[j < NGX ? j : 0], x);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) {
+                    const float v = __builtin_fmaf(gA[e], d[e], __builtin_fmaf(gB[e], x[e], gC[e]));
+                    d[e] = valid ? v : 0.f;
+                }
+                out = Elem<T>::pack(d);
+            } else if (GS == GB_POOLUP) {
+                float d[VEC];
+                Elem<T>::unpack(gr[j], d);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) d[e] *= 0.25f;
+                out = Elem<T>::pack(d);
+            }
+            *reinterpret_cast<vec16 *>(Gs + row * GP + vg * VEC) = out;
+        }
+    };
+
+    f32x4 acc[TAPS * TAPS][RB][CB];
+    #pragma unroll
+    for (int t = 0; t < TAPS * TAPS; t++)
+        #pragma unroll
+        for (int rb = 0; rb < RB; rb++)
+            #pragma unroll
+            for (int cb = 0; cb < CB; cb++) acc[t][rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // this lane's transposing-read offsets (elements)
+    const int g16 = lane >> 4, j16 = lane & 15;
+    const T *za_base = Zs + (8 * g16 + (j16 >> 2)) * ZP + 4 * (j16 & 3) + wci * RB * 16;
+    const T *gb_base = Gs + (8 * g16 + (j16 >> 2)) * GP + 4 * (j16 & 3) + wco * CB * 16;
+
+    const int64_t ch_begin = (int64_t)split * pl.chunks_per_split;
+    const int64_t ch_end = min(pl.nchunks, ch_begin + pl.chunks_per_split);
+    if (ch_begin < ch_end) load_chunk(ch_begin);
+    for (int64_t ch = ch_begin; ch < ch_end; ch++) {
+        store_chunk(ch);
+        __syncthreads();
+        if (ch + 1 < ch_end) load_chunk(ch + 1);
+        for (int kq = 0; kq < KQ; kq += M::KSTEP) {
+            typename M::frag b[CB];
+            #pragma unroll
+            for (int cb = 0; cb < CB; cb++) b[cb] = tr_frag(gb_base + kq * GP + cb * 16, GP);
+            #pragma unroll
+            for (int t = 0; t < TAPS * TAPS; t++) {
+                const int toff = TAPS == 3 ? (t / 3) * PW + (t % 3) : 0;
+                #pragma unroll
+                for (int rb = 0; rb < RB; rb++) {
+                    const typename M::frag a = tr_frag(za_base + (kq + toff) * ZP + rb * 16, ZP);
+                    #pragma unroll
+                    for (int cb = 0; cb < CB; cb++) M::mma(acc[t][rb][cb], a, b[cb]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- partial tile (or dW directly when there is one split) ----
+    float *dst = pl.splits == 1 ? p.dw : p.part + (int64_t)split * p.k * p.k * C_in * C_out;
+    #pragma unroll
+    for (int t = 0; t < TAPS * TAPS; t++)
+        #pragma unroll
+        for (int rb = 0; rb < RB; rb++)
+            #pragma unroll
+            for (int cb = 0; cb < CB; cb++)
+                #pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const int ci = ci0 + (wci * RB + rb) * 16 + (lane >> 4) * 4 + i;
+                    const int co = co0 + (wco * CB + cb) * 16 + (lane & 15);
+                    if (ci < C_in && co < C_out) dst[((int64_t)t * C_in + ci) * C_out + co] = acc[t][rb][cb][i];
+                }
+}
+
 // ------------------------------------------------------------- launchers ---
+static bool wgrad_tr_ok(int dtype, int64_t m, int h, int w, int64_t x_ldc, int64_t g_ldc, int64_t gx_ldc, int k)
+{
+    if (dtype != DT_BF16 || (k == 3 && w > kWgMaxW3)) return false;
+    const int64_t lim = (int64_t)1 << 31;
+    return (m * x_ldc) * 2 < lim && (m * g_ldc) * 2 < lim && (m * gx_ldc) * 2 < lim && h >= 1 && w >= 1;
+}
+
 size_t wgrad_ws_bytes(int dtype, int64_t m, int n, int h, int w, int c_in, int c_out, int k)
 {
     const WgradPlan pl = wgrad_plan(m, n, h, w, c_in, c_out, k, dtype == DT_BF16 ? 2 : 4);
-    if (pl.splits <= 1) return 0;
-    return (size_t)pl.splits * k * k * c_in * c_out * sizeof(float);
+    const WgTrPlan tp = wgrad_tr_plan(m, n, h, w, c_in, c_out, k);
+    const int64_t s = dtype == DT_BF16 ? (pl.splits > tp.splits ? pl.splits : tp.splits) : pl.splits;
+    if (s <= 1) return 0;
+    return (size_t)s * k * k * c_in * c_out * sizeof(float);
+}
+
+template <int TAPS, int CIT, int COT, int WCI>
+static hipError_t run_wgrad_tr(const WgradParams &p, const WgTrPlan &pl, hipStream_t s)
+{
+    const int64_t blocks = (int64_t)pl.ci_tiles * pl.co_tiles * pl.splits;
+    const size_t lds = ((size_t)pl.zrows * (CIT + 8) + (size_t)pl.KQ * (COT + 8)) * 2;
+    const double m = (double)p.m;
+    double g = m * p.c_out;
+    if (p.gsrc == GB_BNGRAD) g *= 2.0;
+    if (p.gsrc == GB_POOLUP) g /= 4.0;
+    const double dwb = (double)p.k * p.k * p.c_in * p.c_out;
+    TraceScope tr(KC_WGRAD, TAPS == 3 ? KID_WGRAD_3X3 : KID_WGRAD_1X1, s, 2.0 * (m * p.c_in + g) + 4.0 * dwb,
+                  2.0 * m * dwb);
+    if (p.gsrc == GB_BNGRAD)
+        hipLaunchKernelGGL((k_wgrad_tr<TAPS, CIT, COT, WCI, GB_BNGRAD>), dim3((unsigned)blocks), dim3(kThreads), lds, s, p, pl);
+    else if (p.gsrc == GB_POOLUP)
+        hipLaunchKernelGGL((k_wgrad_tr<TAPS, CIT, COT, WCI, GB_POOLUP>), dim3((unsigned)blocks), dim3(kThreads), lds, s, p, pl);
+    else
+        hipLaunchKernelGGL((k_wgrad_tr<TAPS, CIT, COT, WCI, GB_DENSE>), dim3((unsigned)blocks), dim3(kThreads), lds, s, p, pl);
+    return hipGetLastError();
+}
+
+static hipError_t dispatch_wgrad_tr(const WgradParams &p, const WgTrPlan &pl, hipStream_t s)
+{
+    if (pl.k == 3) return pl.cot == 32 ? run_wgrad_tr<3, 64, 32, 4>(p, pl, s) : run_wgrad_tr<3, 64, 64, 4>(p, pl, s);
+    if (pl.cit == 64) {
+        if (pl.cot == 32) return run_wgrad_tr<1, 64, 32, 2>(p, pl, s);
+        if (pl.cot == 64) return run_wgrad_tr<1, 64, 64, 2>(p, pl, s);
+        return run_wgrad_tr<1, 64, 128, 1>(p, pl, s);
+    }
+    if (pl.cot == 32) return run_wgrad_tr<1, 128, 32, 4>(p, pl, s);
+    if (pl.cot == 64) return run_wgrad_tr<1, 128, 64, 2>(p, pl, s);
+    return run_wgrad_tr<1, 128, 128, 2>(p, pl, s);
 }
 
 template <typename T, int TAPS, int COT, int WR, int WC>
@@ -339,6 +616,13 @@ hipError_t launch_wgrad(const WgradParams &p, hipStream_t s)
     if (p.gsrc == GB_BNGRAD && (!p.gx || !p.g_mean || !p.g_rstd || !p.g_gamma || !p.g_dbeta || !p.g_dgamma))
         return hipErrorInvalidValue;
     if (p.k == 3 && p.w > kWgMaxW3) return hipErrorInvalidValue;
+    if (wgrad_tr_ok(p.dtype, p.m, p.h, p.w, p.x_ldc, p.g_ldc, p.gsrc == GB_BNGRAD ? p.gx_ldc : 0, p.k)) {
+        const WgTrPlan tp = wgrad_tr_plan(p.m, p.n, p.h, p.w, p.c_in, p.c_out, p.k);
+        if (tp.splits > 1 && (!p.part || !p.red)) return hipErrorInvalidValue;
+        const hipError_t e = dispatch_wgrad_tr(p, tp, s);
+        if (e != hipSuccess || tp.splits <= 1) return e;
+        return launch_sum_partials(p.part, tp.splits, (int64_t)p.k * p.k * p.c_in * p.c_out, p.dw, p.red, s);
+    }
     const WgradPlan pl = wgrad_plan(p.m, p.n, p.h, p.w, p.c_in, p.c_out, p.k, p.dtype == DT_BF16 ? 2 : 4);
     if (pl.splits > 1 && (!p.part || !p.red)) return hipErrorInvalidValue;
     const hipError_t e = p.dtype == DT_BF16 ? dispatch_wgrad<bf16_t>(p, pl, s) : dispatch_wgrad<float>(p, pl, s);

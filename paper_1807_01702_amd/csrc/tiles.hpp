@@ -86,4 +86,59 @@ inline WgradPlan wgrad_plan(int64_t m, int n, int h, int w, int c_in, int c_out,
     return p;
 }
 
+// ---- bf16 weight gradient with transposing LDS reads --------------------
+// Both operands are staged row-major (one row per K position, channels
+// contiguous) and the matrix-core fragments are read transposed.  A
+// workgroup owns CIT input channels x COT output channels (x all nine taps
+// for 3x3).  K positions come in chunks of KQ: 1x1, KQ consecutive pixels;
+// 3x3, R image rows of PW = W + 2 padded positions (a zero column at each
+// end) rounded up to a multiple of 32, with the Z operand staged for the
+// positions [-(PW + 1), KQ + PW + 1) so that tap (kh, kw) reads Z rows
+// q + kh PW + kw (zero padding is the zero positions).
+struct WgTrPlan {
+    int k, cit, cot, ci_tiles, co_tiles;
+    int R, PW, KQ, zrows;
+    int64_t chunks_per_image, nchunks, splits, chunks_per_split;
+};
+inline WgTrPlan wgrad_tr_plan(int64_t m, int n, int h, int w, int c_in, int c_out, int k)
+{
+    WgTrPlan p;
+    p.k = k;
+    p.cot = c_out <= 32 ? 32 : (c_out <= 64 ? 64 : 128);
+    if (k == 3 && p.cot > 64) p.cot = 64;
+    p.cit = (k == 1 && c_in > 64) ? 128 : 64;
+    p.ci_tiles = (int)ceil_div(c_in, p.cit);
+    p.co_tiles = (int)ceil_div(c_out, p.cot);
+    if (k == 3) {
+        p.PW = w + 2;
+        p.R = 128 / p.PW < 1 ? 1 : 128 / p.PW;
+        if (p.R > h) p.R = h;
+        p.KQ = (int)ceil_div((int64_t)p.R * p.PW, 32) * 32;
+        p.zrows = p.KQ + 2 * p.PW + 2;
+        p.chunks_per_image = ceil_div(h, p.R);
+        p.nchunks = (int64_t)n * p.chunks_per_image;
+    } else {
+        p.PW = 0;
+        p.R = 0;
+        p.KQ = 128;
+        p.zrows = 128;
+        p.chunks_per_image = 0;
+        p.nchunks = ceil_div(m, 128);
+    }
+    const int64_t n_out = (int64_t)p.ci_tiles * p.co_tiles;
+    int64_t s = ceil_div(768, n_out);
+    // partial tiles (S * |dW| float32, written and read once) kept below a
+    // third of the operand bytes
+    const int64_t dw_bytes = (int64_t)k * k * c_in * c_out * 4;
+    const int64_t in_bytes = m * (int64_t)(c_in + c_out) * 2;
+    int64_t cap = (in_bytes / 3) / (dw_bytes > 0 ? dw_bytes : 1);
+    if (cap < 1) cap = 1;
+    if (s > cap) s = cap;
+    if (s > p.nchunks) s = p.nchunks;
+    if (s < 1) s = 1;
+    p.chunks_per_split = ceil_div(p.nchunks, s);
+    p.splits = ceil_div(p.nchunks, p.chunks_per_split);
+    return p;
+}
+
 }  // namespace bnr
