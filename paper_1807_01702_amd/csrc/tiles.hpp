@@ -90,7 +90,7 @@ inline WgradPlan wgrad_plan(int64_t m, int n, int h, int w, int c_in, int c_out,
 // Both operands are staged row-major (one row per K position, channels
 // contiguous) and the matrix-core fragments are read transposed.  A
 // workgroup owns CIT input channels x COT output channels (x all nine taps
-// for 3x3).  K positions come in chunks of KQ: 1x1, KQ consecutive pixels;
+// for 3x3).  K positions come in chunks of KQ: 1x1, 64 consecutive pixels;
 // 3x3, R image rows of PW = W + 2 padded positions (a zero column at each
 // end) rounded up to a multiple of 32, with the Z operand staged for the
 // positions [-(PW + 1), KQ + PW + 1) so that tap (kh, kw) reads Z rows
@@ -120,10 +120,10 @@ inline WgTrPlan wgrad_tr_plan(int64_t m, int n, int h, int w, int c_in, int c_ou
     } else {
         p.PW = 0;
         p.R = 0;
-        p.KQ = 128;
-        p.zrows = 128;
+        p.KQ = 64;
+        p.zrows = 64;
         p.chunks_per_image = 0;
-        p.nchunks = ceil_div(m, 128);
+        p.nchunks = ceil_div(m, 64);
     }
     const int64_t n_out = (int64_t)p.ci_tiles * p.co_tiles;
     int64_t s = ceil_div(768, n_out);
