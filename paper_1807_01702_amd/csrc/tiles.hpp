@@ -126,12 +126,12 @@ inline WgTrPlan wgrad_tr_plan(int64_t m, int n, int h, int w, int c_in, int c_ou
         p.nchunks = ceil_div(m, 64);
     }
     const int64_t n_out = (int64_t)p.ci_tiles * p.co_tiles;
-    int64_t s = ceil_div(768, n_out);
-    // partial tiles (S * |dW| float32, written and read once) kept below a
-    // third of the operand bytes
+    int64_t s = ceil_div(512, n_out);                 // two workgroups per CU
+    // partial tiles (S * |dW| float32, written and read once) kept below the
+    // operand bytes
     const int64_t dw_bytes = (int64_t)k * k * c_in * c_out * 4;
     const int64_t in_bytes = m * (int64_t)(c_in + c_out) * 2;
-    int64_t cap = (in_bytes / 3) / (dw_bytes > 0 ? dw_bytes : 1);
+    int64_t cap = in_bytes / (dw_bytes > 0 ? dw_bytes : 1);
     if (cap < 1) cap = 1;
     if (s > cap) s = cap;
     if (s > p.nchunks) s = p.nchunks;
