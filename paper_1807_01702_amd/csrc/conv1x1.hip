@@ -24,42 +24,44 @@ namespace bnr {
 
 constexpr int kP1Threads = 512;
 constexpr int kP1BM = 128;     // largest tile height (rows = pixels)
-constexpr int kP1NV = 8;        // 16-byte vectors per thread for a tile operand
+constexpr int kP1NV = 8;       // 16-byte vectors per thread for a tile operand
 
 struct P1Geom {
     int KP, NP, lda, ldw, ldc;
     size_t region, lds;
 };
 
-template <typename T>
 static P1Geom p1_geom(int K, int N)
 {
-    const int PAD = 16 / (int)sizeof(T);
     P1Geom g;
-    g.KP = (int)((K + 31) / 32 * 32);
+    g.KP = (K + 31) / 32 * 32;
     g.NP = N <= 32 ? 32 : (N <= 64 ? 64 : (N <= 128 ? 128 : 256));
-    g.lda = g.KP + PAD;
-    g.ldw = g.KP + PAD;
-    g.ldc = g.NP + PAD;
+    g.lda = g.KP + 8;
+    g.ldw = g.KP + 8;
+    g.ldc = g.NP + 8;
     const size_t a = (size_t)kP1BM * g.lda, c = (size_t)kP1BM * g.ldc;
-    const size_t red = (size_t)2 * (kP1Threads / (g.NP / (16 / sizeof(T)))) * g.NP * sizeof(float) / sizeof(T);
+    const size_t red = (size_t)2 * (kP1Threads / (g.NP / 8)) * g.NP * sizeof(float) / 2;
     g.region = a > c ? (a > red ? a : red) : (c > red ? c : red);
-    g.lds = ((size_t)g.NP * g.ldw + g.region) * sizeof(T) + (size_t)(5 * g.KP + 4 * g.NP) * sizeof(float);
+    g.lds = ((size_t)g.NP * g.ldw + g.region) * 2 + (size_t)(5 * g.KP + 4 * g.NP) * sizeof(float);
     return g;
 }
 
 // NVA: upper bound of 16-byte A vectors per thread and tile (compile time, so
-// the operand registers stay in VGPRs); IO: 0 = A only, 1 = A + epilogue
-// operand, 2 = A + second prologue operand (PRO_BNGRAD) + epilogue operand.
-template <typename T, int CBW, int NVA, int IO, int BM>
+// the operand registers stay in VGPRs).  The epilogue kind EK and whether the
+// prologue reads a second operand (PRO_BNGRAD) are compile-time as well, so
+// the epilogue is straight-line code and the compiler can keep the next
+// tile's loads in flight while it waits for the epilogue operand.
+template <int CBW, int NVA, int EK, bool BNG, int BM>
 __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, int ntiles)
 {
+    using T = bf16_t;
     using M = Mfma<T>;
-    constexpr int VEC = Elem<T>::VEC;
+    constexpr int VEC = 8;
     constexpr int RPT0 = BM * (32 * CBW / VEC) / kP1Threads;
     constexpr int RPT = RPT0 > 0 ? RPT0 : 1;                     // epilogue rows per thread
     constexpr int RB = BM / 64;                                  // 16-row MFMA blocks per wave
-    constexpr int NVB = IO == 2 ? NVA : 1, NVX = IO >= 1 ? RPT : 1;
+    constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD;
+    constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1;
     extern __shared__ __align__(16) unsigned char smem[];
     T *Ws = reinterpret_cast<T *>(smem);
     T *As = Ws + (size_t)g.NP * g.ldw;
@@ -68,23 +70,29 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     float *epi = coef + 5 * g.KP;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;              // 4 x 2 waves: 32 rows x NP/2 columns each
+    const int wm = wave >> 1, wn = wave & 1;              // 4 x 2 waves: 16 RB rows x NP/2 columns each
     const int K = p.K, N = p.N, KP = g.KP, NP = g.NP;
-    const int64_t m = p.m;
+    const int m = (int)p.m;                               // launcher: m < 2^30
     const int H = p.h, W = p.w;
-    const T *asrc = reinterpret_cast<const T *>(p.a);
-    const T *asrc2 = reinterpret_cast<const T *>(p.a2);
     const T *wsrc = reinterpret_cast<const T *>(p.wraw);
+    const int a_ldc = (int)p.a_ldc, a2_ldc = (int)p.a2_ldc, y_ldc = (int)p.y_ldc, ex_ldc = (int)p.ex_ldc;
+    const bool pool = p.pro == PRO_POOLUP;
+    // operand views as raw buffers (launcher guarantees each spans < 2^31 bytes)
+    const int64_t arows = pool ? (int64_t)m / 4 : m;
+    const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((arows - 1) * a_ldc + K) * 2));
+    const __amdgpu_buffer_rsrc_t a2buf = buf_view(BNG ? p.a2 : p.a, BNG ? (uint32_t)(((int64_t)(m - 1) * a2_ldc + K) * 2) : 0u);
+    const __amdgpu_buffer_rsrc_t ybuf = buf_view(p.y, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * 2));
+    const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
+                                                 p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * 2) : 0u);
 
     // ---- weights -> LDS as Ws[n][k] (zero outside K x N) ----
     if (!p.wtrans) {      // forward: W[k][n] (k = c_in, n = c_out); read rows of n, scatter to columns
         for (int i = tid; i < KP * (NP / VEC); i += kP1Threads) {
             const int k = i / (NP / VEC), n0 = (i % (NP / VEC)) * VEC;
-            float f[VEC];
-            if (k < K && n0 < N) Elem<T>::unpack(ldg16(wsrc + (int64_t)k * N + n0), f);
-            else for (int e = 0; e < VEC; e++) f[e] = 0.f;
+            const vec16 v = (k < K && n0 < N) ? ldg16(wsrc + (int64_t)k * N + n0) : zero16();
+            const T *h = reinterpret_cast<const T *>(&v);
             #pragma unroll
-            for (int e = 0; e < VEC; e++) Ws[(n0 + e) * g.ldw + k] = to_store<T>(f[e]);
+            for (int e = 0; e < VEC; e++) Ws[(n0 + e) * g.ldw + k] = h[e];
         }
     } else {              // data gradient: W[n][k] (n = c_in, k = c_out): rows copy straight
         for (int i = tid; i < NP * (KP / VEC); i += kP1Threads) {
@@ -94,20 +102,22 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
         }
     }
     // ---- per-channel prologue / epilogue parameters ----
+    //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
+    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient, expanded)
     for (int c = tid; c < KP; c += kP1Threads) {
-        float c0 = 0.f, c1 = 0.f, c2 = 0.f, c3 = 0.f, c4 = 0.f;
+        float c0 = 0.f, c1 = 0.f, c2 = 0.f;
         if (c < K && p.pro == PRO_BNRELU) {
-            c0 = p.p_mean[c]; c1 = p.p_gamma[c] * p.p_rstd[c]; c2 = p.p_beta[c];
+            c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
         } else if (c < K && p.pro == PRO_BNGRAD) {
             const float inv_m = 1.0f / (float)m;
-            c0 = p.p_mean[c]; c1 = p.p_rstd[c]; c2 = p.p_gamma[c] * p.p_rstd[c];
-            c3 = p.p_dbeta[c] * inv_m; c4 = p.p_dgamma[c] * inv_m;
+            const float k = p.p_gamma[c] * p.p_rstd[c], b = p.p_dgamma[c] * inv_m * p.p_rstd[c];
+            c0 = k; c1 = -k * b; c2 = k * (b * p.p_mean[c] - p.p_dbeta[c] * inv_m);
         }
-        coef[c] = c0; coef[KP + c] = c1; coef[2 * KP + c] = c2; coef[3 * KP + c] = c3; coef[4 * KP + c] = c4;
+        coef[c] = c0; coef[KP + c] = c1; coef[2 * KP + c] = c2;
     }
     for (int c = tid; c < NP; c += kP1Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
-        if (c < N && p.epi == EPI_BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
+        if (c < N && EK == EK_BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
         epi[c] = e0; epi[NP + c] = e1; epi[2 * NP + c] = e2; epi[3 * NP + c] = e3;
     }
 
@@ -118,63 +128,64 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     // contiguous bytes of one pixel row), 16 lane groups cover 16 rows, so a
     // wave touches only 4 distinct prologue-coefficient addresses (LDS
     // broadcast, no bank conflicts).
-    auto a_slot = [&](int j, int &r, int &c) __attribute__((always_inline)) {
+    int sr[NVA], sc[NVA];
+    #pragma unroll
+    for (int j = 0; j < NVA; j++) {
         const int i = tid + j * kP1Threads;
         const int q = i >> 2;
-        r = q % BM;
-        c = ((q / BM) * 4 + (i & 3)) * VEC;
-    };
+        sr[j] = q % BM;
+        sc[j] = ((q / BM) * 4 + (i & 3)) * VEC;
+    }
     vec16 ra[NVA], rb[NVB];
-    const bool pool = p.pro == PRO_POOLUP;
     auto load_a = [&](int tile) __attribute__((always_inline)) {
-        const int64_t p0 = (int64_t)tile * BM;
+        const int p0 = tile * BM;
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
-            int r, c;
-            a_slot(j, r, c);
-            const int64_t pp = p0 + r;
+            const int pp = p0 + sr[j], c = sc[j];
             const bool ok = j < nva && c < K && pp < m;
-            int64_t q = pp;
+            int q = pp;
             if (pool) {
-                const int64_t img = pp / ((int64_t)H * W);
-                const int rem = (int)(pp - img * H * W);
+                const int img = pp / (H * W);
+                const int rem = pp - img * H * W;
                 const int y = rem / W, x = rem - y * W;
                 q = (img * (H / 2) + y / 2) * (W / 2) + x / 2;
             }
-            const vec16 va = ok ? ldg16(asrc + q * p.a_ldc + c) : zero16();
-            ra[j] = va;
-            if (IO == 2) rb[j < NVB ? j : 0] = ok ? ldg16(asrc2 + pp * p.a2_ldc + c) : zero16();
+            ra[j] = bld16(abuf, ok ? (uint32_t)(q * a_ldc + c) * 2u : kBufOff);
+            if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(pp * a2_ldc + c) * 2u : kBufOff);
         }
     };
     auto store_a = [&](int tile) __attribute__((always_inline)) {
-        const int64_t p0 = (int64_t)tile * BM;
+        const int p0 = tile * BM;
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
-            if (j >= nva) continue;
-            int r, c;
-            a_slot(j, r, c);
-            if (c >= KP) continue;
+            const int r = sr[j], c = sc[j];
+            if (j >= nva || c >= KP) continue;
             const bool valid = p0 + r < m && c < K;
             vec16 out = ra[j];
             if (p.pro != PRO_NONE) {
                 float f[VEC];
                 Elem<T>::unpack(ra[j], f);
                 if (p.pro == PRO_BNRELU) {
+                    float ca[VEC], cb[VEC];
+                    lds_f8(coef + c, ca);
+                    lds_f8(coef + KP + c, cb);
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) {
-                        const float t = (f[e] - coef[c + e]) * coef[KP + c + e] + coef[2 * KP + c + e];
+                        const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
                         f[e] = valid && t > 0.f ? t : 0.f;
                     }
                 } else if (p.pro == PRO_RELU) {
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
-                } else if (IO == 2 && p.pro == PRO_BNGRAD) {
-                    float x[VEC];
+                } else if (BNG && p.pro == PRO_BNGRAD) {
+                    float x[VEC], c0[VEC], c1[VEC], c2[VEC];
                     Elem<T>::unpack(rb[j < NVB ? j : 0], x);
+                    lds_f8(coef + c, c0);
+                    lds_f8(coef + KP + c, c1);
+                    lds_f8(coef + 2 * KP + c, c2);
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) {
-                        const float xh = (x[e] - coef[c + e]) * coef[KP + c + e];
-                        const float d = coef[2 * KP + c + e] * (f[e] - coef[3 * KP + c + e] - xh * coef[4 * KP + c + e]);
+                        const float d = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
                         f[e] = valid ? d : 0.f;
                     }
                 } else {  // PRO_POOLUP
@@ -197,18 +208,15 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
     T *yout = reinterpret_cast<T *>(p.y);
-    const T *exs = reinterpret_cast<const T *>(p.ex);
-    const bool epi_reads = p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK || (p.epi == EPI_STORE && p.accumulate);
     auto load_epi = [&](int tile) __attribute__((always_inline)) {
-        const int64_t p0 = (int64_t)tile * BM;
-        if (IO == 0) return;
+        if (!READS) return;
+        const int p0 = tile * BM;
         #pragma unroll
         for (int j = 0; j < NVX; j++) {
-            rx[j] = zero16();
-            if (!epi_reads || !col_ok) continue;
-            const int64_t pp = p0 + r0 + j * RSTEP;
-            if (r0 + j * RSTEP >= BM || pp >= m) continue;
-            rx[j] = p.epi == EPI_STORE ? ldg16(yout + pp * p.y_ldc + n) : ldg16(exs + pp * p.ex_ldc + n);
+            const int r = r0 + j * RSTEP, pp = p0 + r;
+            const bool ok = col_ok && r < BM && pp < m;
+            if (EK == EK_STORE_ACC) rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
+            else rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
         }
     };
 
@@ -224,22 +232,25 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     for (; tile < ntiles; tile += gridDim.x) {
         store_a(tile);
         __syncthreads();
-        if (tile + (int)gridDim.x < ntiles) load_a(tile + gridDim.x);
+        // epilogue operand first: the epilogue waits for it while the next
+        // tile's rows (issued after it) may still be in flight
         load_epi(tile);
-        // ---- matrix cores: 32 rows x NP/2 columns per wave ----
+        if (tile + (int)gridDim.x < ntiles) load_a(tile + gridDim.x);
+        // ---- matrix cores: 16 RB rows x NP/2 columns per wave ----
         f32x4 acc[RB][CBW];
         #pragma unroll
         for (int ib = 0; ib < RB; ib++)
             #pragma unroll
             for (int cb = 0; cb < CBW; cb++) acc[ib][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const T *arow = As + (wm * (16 * RB) + (lane & 15)) * g.lda + (lane >> 4) * M::KPL;
+        const T *brow = Ws + (wn * (NP / 2) + (lane & 15)) * g.ldw + (lane >> 4) * M::KPL;
         for (int k0 = 0; k0 < KP; k0 += M::KSTEP) {
-            const int kofs = k0 + (lane >> 4) * M::KPL;
             typename M::frag a[RB];
             #pragma unroll
-            for (int ib = 0; ib < RB; ib++) a[ib] = M::load(As + (wm * (16 * RB) + ib * 16 + (lane & 15)) * g.lda + kofs);
+            for (int ib = 0; ib < RB; ib++) a[ib] = M::load(arow + ib * 16 * g.lda + k0);
             #pragma unroll
             for (int cb = 0; cb < CBW; cb++) {
-                const typename M::frag b = M::load(Ws + (wn * (NP / 2) + cb * 16 + (lane & 15)) * g.ldw + kofs);
+                const typename M::frag b = M::load(brow + cb * 16 * g.ldw + k0);
                 #pragma unroll
                 for (int ib = 0; ib < RB; ib++) M::mma(acc[ib][cb], a[ib], b);
             }
@@ -253,62 +264,65 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
                 for (int i = 0; i < 4; i++) {
                     const int row = wm * (16 * RB) + ib * 16 + (lane >> 4) * 4 + i;
                     const int col = wn * (NP / 2) + cb * 16 + (lane & 15);
-                    Cs[row * g.ldc + col] = to_store<T>(acc[ib][cb][i]);
+                    Cs[row * g.ldc + col] = f2bf(acc[ib][cb][i]);
                 }
         __syncthreads();
-        // ---- epilogue row pass ----
-        const int64_t p0 = (int64_t)tile * BM;
-        if (col_ok) {
-            #pragma unroll
-            for (int j = 0; j < RPT; j++) {
-                const int r = r0 + j * RSTEP;
-                const int64_t pp = p0 + r;
-                if (r >= BM || pp >= m) continue;
-                const vec16 cv = *reinterpret_cast<const vec16 *>(Cs + r * g.ldc + n);
-                T *dst = yout + pp * p.y_ldc + n;
-                float f[VEC];
-                Elem<T>::unpack(cv, f);
-                if (p.epi == EPI_STORE) {
-                    if (IO >= 1 && p.accumulate) {
-                        float old[VEC];
-                        Elem<T>::unpack(rx[j < NVX ? j : 0], old);
-                        #pragma unroll
-                        for (int e = 0; e < VEC; e++) f[e] += old[e];
-                        stg16(dst, Elem<T>::pack(f));
-                    } else {
-                        stg16(dst, cv);
-                    }
-                } else if (p.epi == EPI_STATS) {
-                    stg16(dst, cv);
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) { s1[e] += f[e]; s2[e] += f[e] * f[e]; }
-                } else if (IO >= 1 && p.epi == EPI_RELUMASK) {
-                    float yv[VEC];
-                    Elem<T>::unpack(rx[j < NVX ? j : 0], yv);
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) f[e] = yv[e] > 0.f ? f[e] : 0.f;
-                    stg16(dst, Elem<T>::pack(f));
-                } else if (IO >= 1) {  // EPI_BNBWD
-                    float x[VEC];
-                    Elem<T>::unpack(rx[j < NVX ? j : 0], x);
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) {
-                        const float xh = (x[e] - eM[e]) * eR[e];
-                        const float yv = eG[e] * xh + eB[e];
-                        const float d = yv > 0.f ? f[e] : 0.f;
-                        f[e] = d;
-                        s1[e] += d;
-                        s2[e] += d * xh;
-                    }
-                    stg16(dst, Elem<T>::pack(f));
+        // ---- epilogue row pass: all outputs of this thread first (invalid rows
+        // contribute zeros), then the stores back to back ----
+        const int p0 = tile * BM;
+        vec16 vo[RPT];
+        #pragma unroll
+        for (int j = 0; j < RPT; j++) {
+            const int r = r0 + j * RSTEP;
+            const bool ok = col_ok && r < BM && p0 + r < m;
+            const vec16 cv = *reinterpret_cast<const vec16 *>(Cs + (r < BM ? r : 0) * g.ldc + n);
+            float f[VEC];
+            Elem<T>::unpack(cv, f);
+            vo[j] = cv;
+            if (EK == EK_STORE_ACC) {
+                float old[VEC];
+                Elem<T>::unpack(rx[j < NVX ? j : 0], old);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] += old[e];
+                vo[j] = Elem<T>::pack(f);
+            } else if (EK == EK_STATS) {
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) {
+                    const float fv = ok ? f[e] : 0.f;
+                    s1[e] += fv;
+                    s2[e] += fv * fv;
                 }
+            } else if (EK == EK_RELUMASK) {
+                float yv[VEC];
+                Elem<T>::unpack(rx[j < NVX ? j : 0], yv);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] = yv[e] > 0.f ? f[e] : 0.f;
+                vo[j] = Elem<T>::pack(f);
+            } else if (EK == EK_BNBWD) {
+                float x[VEC];
+                Elem<T>::unpack(rx[j < NVX ? j : 0], x);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) {
+                    const float xh = (x[e] - eM[e]) * eR[e];
+                    const float yv = eG[e] * xh + eB[e];
+                    const float d = ok && yv > 0.f ? f[e] : 0.f;
+                    f[e] = d;
+                    s1[e] += d;
+                    s2[e] += d * xh;
+                }
+                vo[j] = Elem<T>::pack(f);
             }
+        }
+        #pragma unroll
+        for (int j = 0; j < RPT; j++) {
+            const int r = r0 + j * RSTEP;
+            if (col_ok && r < BM && p0 + r < m) stg16(yout + (int64_t)(p0 + r) * y_ldc + n, vo[j]);
         }
         __syncthreads();
     }
 
     // ---- per-workgroup statistics partial row ----
-    if (p.epi == EPI_STATS || p.epi == EPI_BNBWD) {
+    if (EK == EK_STATS || EK == EK_BNBWD) {
         float *red = reinterpret_cast<float *>(As);
         #pragma unroll
         for (int e = 0; e < VEC; e++) {
@@ -340,12 +354,11 @@ static int device_cus()
 
 bool conv1x1_supported(int dtype, int K, int N)
 {
-    if (K > 256 || N > 256 || (dtype != DT_BF16 && N > 128)) return false;
-    const P1Geom g = dtype == DT_BF16 ? p1_geom<bf16_t>(K, N) : p1_geom<float>(K, N);
+    if (dtype != DT_BF16 || K > 256 || N > 256) return false;
+    const P1Geom g = p1_geom(K, N);
     if (g.lds > 150 * 1024) return false;
-    const int VEC = dtype == DT_BF16 ? 8 : 4;
-    if ((int64_t)kP1BM * (g.KP / VEC) > (int64_t)kP1NV * kP1Threads) return false;      // A tile registers
-    if (kP1BM / (kP1Threads / (g.NP / VEC)) > kP1NV) return false;                       // epilogue registers
+    if ((int64_t)kP1BM * (g.KP / 8) > (int64_t)kP1NV * kP1Threads) return false;      // A tile registers
+    if (kP1BM / (kP1Threads / (g.NP / 8)) > kP1NV) return false;                       // epilogue registers
     return true;
 }
 
@@ -356,10 +369,10 @@ int64_t conv1x1_partial_rows(int64_t m)
     return tiles < g ? tiles : g;
 }
 
-template <typename T, int CBW, int NVA, int IO, int BM>
+template <int CBW, int NVA, int EK, bool BNG, int BM>
 static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
 {
-    auto kern = k_conv1x1<T, CBW, NVA, IO, BM>;
+    auto kern = k_conv1x1<CBW, NVA, EK, BNG, BM>;
     static bool attr_set = false;
     if (!attr_set) {
         const hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
@@ -368,13 +381,13 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
     }
     const int ntiles = (int)ceil_div(p.m, BM);
     const int grid = (int)conv1x1_partial_rows(p.m);
-    const double e = sizeof(T), m = (double)p.m;
+    const double m = (double)p.m;
     double a = m * p.K;
-    if (p.pro == PRO_BNGRAD) a *= 2.0;
+    if (BNG) a *= 2.0;
     if (p.pro == PRO_POOLUP) a /= 4.0;
     double out = m * p.N;
-    if (p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK || (p.epi == EPI_STORE && p.accumulate)) out += m * p.N;
-    TraceScope tr(KC_CONV, KID_CONV_1X1, s, e * (a + out + (double)p.K * p.N), 2.0 * m * p.K * p.N);
+    if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD) out += m * p.N;
+    TraceScope tr(KC_CONV, KID_CONV_1X1, s, 2.0 * (a + out + (double)p.K * p.N), 2.0 * m * p.K * p.N);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kP1Threads), g.lds, s, p, g, ntiles);
     return hipGetLastError();
 }
@@ -382,39 +395,44 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
 // Tile height: 128 rows unless the operand registers of the variant would not
 // fit the 256 VGPRs a wave has at two waves per SIMD; then 64 rows, which
 // halves every per-thread operand array.
-template <typename T, int CBW, int NVA128, int IO>
+template <int CBW, int NVA128, int EK, bool BNG>
 static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s)
 {
-    constexpr bool small = (CBW == 8 && IO >= 1) || (NVA128 == 8 && IO == 2);
-    if constexpr (small) return run_p1<T, CBW, 4, IO, 64>(p, g, s);
-    else return run_p1<T, CBW, NVA128, IO, 128>(p, g, s);
+    constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD;
+    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && BNG);
+    if constexpr (small) return run_p1<CBW, 4, EK, BNG, 64>(p, g, s);
+    else return run_p1<CBW, NVA128, EK, BNG, 128>(p, g, s);
 }
 
-template <typename T, int NVA128, int IO>
+template <int NVA128, int EK, bool BNG>
 static hipError_t run_p1_cbw(const RowsParams &p, const P1Geom &g, hipStream_t s)
 {
     switch (g.NP / 32) {
-    case 1: return run_p1_bm<T, 1, NVA128, IO>(p, g, s);
-    case 2: return run_p1_bm<T, 2, NVA128, IO>(p, g, s);
-    case 4: return run_p1_bm<T, 4, NVA128, IO>(p, g, s);
-    default:
-        if constexpr (sizeof(T) == 2) return run_p1_bm<T, 8, NVA128, IO>(p, g, s);
-        else return hipErrorInvalidValue;      // float with 256 output columns exceeds LDS
+    case 1: return run_p1_bm<1, NVA128, EK, BNG>(p, g, s);
+    case 2: return run_p1_bm<2, NVA128, EK, BNG>(p, g, s);
+    case 4: return run_p1_bm<4, NVA128, EK, BNG>(p, g, s);
+    default: return run_p1_bm<8, NVA128, EK, BNG>(p, g, s);
     }
 }
 
-template <typename T>
-static hipError_t run_p1_io(const RowsParams &p, const P1Geom &g, int io, hipStream_t s)
+template <int EK, bool BNG>
+static hipError_t run_p1_nva(const RowsParams &p, const P1Geom &g, hipStream_t s)
 {
-    const int nva = (int)ceil_div((int64_t)kP1BM * (g.KP / Elem<T>::VEC), kP1Threads);
-    if (nva <= 4) {
-        if (io == 0) return run_p1_cbw<T, 4, 0>(p, g, s);
-        if (io == 1) return run_p1_cbw<T, 4, 1>(p, g, s);
-        return run_p1_cbw<T, 4, 2>(p, g, s);
+    const int nva = (int)ceil_div((int64_t)kP1BM * (g.KP / 8), kP1Threads);
+    if (nva <= 4) return run_p1_cbw<4, EK, BNG>(p, g, s);
+    return run_p1_cbw<8, EK, BNG>(p, g, s);
+}
+
+template <bool BNG>
+static hipError_t run_p1_ek(const RowsParams &p, const P1Geom &g, int ek, hipStream_t s)
+{
+    switch (ek) {
+    case EK_STORE: return run_p1_nva<EK_STORE, BNG>(p, g, s);
+    case EK_STORE_ACC: return run_p1_nva<EK_STORE_ACC, BNG>(p, g, s);
+    case EK_STATS: return run_p1_nva<EK_STATS, BNG>(p, g, s);
+    case EK_RELUMASK: return run_p1_nva<EK_RELUMASK, BNG>(p, g, s);
+    default: return run_p1_nva<EK_BNBWD, BNG>(p, g, s);
     }
-    if (io == 0) return run_p1_cbw<T, 8, 0>(p, g, s);
-    if (io == 1) return run_p1_cbw<T, 8, 1>(p, g, s);
-    return run_p1_cbw<T, 8, 2>(p, g, s);
 }
 
 hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s)
@@ -426,10 +444,16 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s)
     if ((p.epi == EPI_STATS || p.epi == EPI_BNBWD) && !p.part) return hipErrorInvalidValue;
     if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return hipErrorInvalidValue;
     if (p.epi == EPI_RELUMASK && !p.ex) return hipErrorInvalidValue;
-    const bool epi_reads = p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK || (p.epi == EPI_STORE && p.accumulate);
-    const int io = p.pro == PRO_BNGRAD ? 2 : (epi_reads ? 1 : 0);
-    if (p.dtype == DT_BF16) return run_p1_io<bf16_t>(p, p1_geom<bf16_t>(p.K, p.N), io, s);
-    return run_p1_io<float>(p, p1_geom<float>(p.K, p.N), io, s);
+    if (p.pro == PRO_POOLUP && (p.h % 2 || p.w % 2 || (int64_t)p.n * p.h * p.w != p.m)) return hipErrorInvalidValue;
+    // 32-bit pixel indices and raw-buffer operand views: every span below 2^31 bytes
+    const int64_t lim = (int64_t)1 << 31;
+    if (p.m < 1 || p.m >= (lim >> 1) || (p.m * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
+        (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
+        return hipErrorInvalidValue;
+    const P1Geom g = p1_geom(p.K, p.N);
+    const int ek = epilogue_kind(p.epi, p.accumulate);
+    if (p.pro == PRO_BNGRAD) return run_p1_ek<true>(p, g, ek, s);
+    return run_p1_ek<false>(p, g, ek, s);
 }
 
 }  // namespace bnr
