@@ -231,6 +231,59 @@ typedef struct {
 bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_conv_desc *d,
                               const bnr_ref_args *a, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------------------ residual blocks (ResNet) ---- */
+
+/* Plain CONV forward y = conv(x, w) (no BN work): a CONV whose input has no
+ * BN in front of it and whose output statistics are not needed, e.g. the
+ * first CONV of a block in the unfused A/B chain. */
+bnr_status bnr_conv_fwd(const bnr_conv_desc *d, const void *x, const void *w, void *y, void *ws, size_t ws_bytes,
+                        void *stream);
+
+/* Residual-block tail out = relu(gamma*(y-mean)*rstd + beta + id) in one
+ * element-wise sweep ([m][c] views; bn holds the statistics of y, already
+ * produced by the CONV that wrote y).  The BN here is followed by an addition
+ * and a ReLU rather than by a CONV, so sub-BN2 cannot be fused into a
+ * following CONV prologue (Sec. 3.2 fuses sub-BN2 only into a following
+ * CONV); it runs as a standalone pass.  out may alias id exactly. */
+bnr_status bnr_bn_add_relu_fwd(int64_t m, int32_t c, bnr_dtype dtype, const void *y, int32_t y_ldc,
+                               const bnr_bn *bn, const void *id, int32_t id_ldc, void *out, int32_t out_ldc,
+                               void *stream);
+
+/* Backward of bnr_bn_add_relu_fwd up to the BN reductions, in one sweep:
+ * gm = g * [out > 0] (the gradient of the identity input and of the BN
+ * output), dbeta = sum(gm), dgamma = sum(gm * xhat) with xhat from y and bn
+ * (the standard BN gradients).  The BN input gradient is not formed: the
+ * CONV that produced y consumes it deferred (BNR_GRAD_BN with dy = gm).  gm
+ * may alias g exactly.  ws: bnr_stats_workspace_size(m, c) bytes. */
+bnr_status bnr_bn_add_relu_bwd(int64_t m, int32_t c, bnr_dtype dtype, const void *g, int32_t g_ldc,
+                               const void *out, int32_t out_ldc, const void *y, int32_t y_ldc, const bnr_bn *bn,
+                               void *gm, int32_t gm_ldc, float *dgamma, float *dbeta, void *ws, size_t ws_bytes,
+                               void *stream);
+
+/* Unfused A/B counterpart of the two calls above (the reference layer
+ * chain): forward, two-pass statistics of y into bn (mean, var, rstd), a
+ * normalise sweep (write tmp, dense [m][c]) and an add + ReLU sweep (write
+ * out); backward, a ReLU-backward sweep (write gm, dense), a reductions sweep
+ * (dgamma, dbeta) and an input-gradient sweep (write dx). */
+typedef struct {
+    const void *y;       /* BN input                                      */
+    int32_t y_ldc;
+    bnr_bn *bn;
+    const void *id;      /* forward: identity input                       */
+    int32_t id_ldc;
+    void *out;           /* forward: output; backward: the forward output */
+    int32_t out_ldc;
+    void *tmp;           /* forward scratch, dense [m][c]                 */
+    const void *g;       /* backward: gradient of out                     */
+    int32_t g_ldc;
+    void *gm;            /* backward: masked gradient, dense [m][c]       */
+    float *dgamma, *dbeta;
+    void *dx;            /* backward: BN input gradient                   */
+    int32_t dx_ldc;
+} bnr_addrelu_ref_args;
+bnr_status bnr_reference_bn_add_relu(int32_t backward, int64_t m, int32_t c, bnr_dtype dtype,
+                                     const bnr_addrelu_ref_args *a, void *ws, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------ diagnostics ---- */
 
 /* Plain device-to-device copy of `bytes` (multiple of 16) with the same

@@ -51,6 +51,12 @@ class RefArgs(ctypes.Structure):
                 ("dbeta", c_vp), ("dx", c_vp), ("dx_ldc", c_i32), ("dx_accumulate", c_i32)]
 
 
+class AddReluRefArgs(ctypes.Structure):
+    _fields_ = [("y", c_vp), ("y_ldc", c_i32), ("bn", ctypes.POINTER(BNStruct)), ("id", c_vp), ("id_ldc", c_i32),
+                ("out", c_vp), ("out_ldc", c_i32), ("tmp", c_vp), ("g", c_vp), ("g_ldc", c_i32), ("gm", c_vp),
+                ("dgamma", c_vp), ("dbeta", c_vp), ("dx", c_vp), ("dx_ldc", c_i32)]
+
+
 def _sig(name, res, *args):
     f = getattr(_lib, name)
     f.restype = res
@@ -81,6 +87,13 @@ _lib_fns = dict(
     bnr_reference_path=_sig("bnr_reference_path", ctypes.c_int, ctypes.c_int, c_i32, _P(ConvDesc), _P(RefArgs), c_vp,
                             c_sz, c_vp),
     bnr_hbm_copy=_sig("bnr_hbm_copy", ctypes.c_int, c_vp, c_vp, c_sz, c_vp),
+    bnr_conv_fwd=_sig("bnr_conv_fwd", ctypes.c_int, _P(ConvDesc), c_vp, c_vp, c_vp, c_vp, c_sz, c_vp),
+    bnr_bn_add_relu_fwd=_sig("bnr_bn_add_relu_fwd", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_i32,
+                             _P(BNStruct), c_vp, c_i32, c_vp, c_i32, c_vp),
+    bnr_bn_add_relu_bwd=_sig("bnr_bn_add_relu_bwd", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_i32, c_vp, c_i32,
+                             c_vp, c_i32, _P(BNStruct), c_vp, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp),
+    bnr_reference_bn_add_relu=_sig("bnr_reference_bn_add_relu", ctypes.c_int, c_i32, c_i64, c_i32, ctypes.c_int,
+                                   _P(AddReluRefArgs), c_vp, c_sz, c_vp),
     bnr_trace_begin=_sig("bnr_trace_begin", ctypes.c_int, c_i32, c_i32),
     bnr_trace_end=_sig("bnr_trace_end", c_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i32), c_i32),
@@ -288,6 +301,45 @@ def bnr_reference_path(mode, backward, desc, x, bn, w, y, z=None, out=None, g=No
                 _ptr(dw), _ptr(dgamma), _ptr(dbeta), dxp, dx_ldc, 1 if dx_accumulate else 0)
     _check(_lib_fns["bnr_reference_path"](mode, 1 if backward else 0, ctypes.byref(desc), ctypes.byref(a), ws, wsb,
                                           _stream()))
+
+
+def bnr_conv_fwd(desc, x, w, y):
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    _check(_lib_fns["bnr_conv_fwd"](ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(y), ws, wsb, _stream()))
+
+
+def bnr_bn_add_relu_fwd(y, bn, ident, out):
+    py, m, c, ldy = view(y)
+    pi, _, _, ldi = view(ident)
+    po, _, _, ldo = view(out)
+    bs = bn.struct()
+    _check(_lib_fns["bnr_bn_add_relu_fwd"](m, c, dtype_code(y), py, ldy, ctypes.byref(bs), pi, ldi, po, ldo, _stream()))
+
+
+def bnr_bn_add_relu_bwd(g, out, y, bn, gm, dgamma, dbeta):
+    pg, m, c, ldg = view(g)
+    po, _, _, ldo = view(out)
+    py, _, _, ldy = view(y)
+    pm, _, _, ldm = view(gm)
+    ws, wsb = workspace(bnr_stats_workspace_size(m, c), y.device)
+    bs = bn.struct()
+    _check(_lib_fns["bnr_bn_add_relu_bwd"](m, c, dtype_code(y), pg, ldg, po, ldo, py, ldy, ctypes.byref(bs), pm, ldm,
+                                           _ptr(dgamma), _ptr(dbeta), ws, wsb, _stream()))
+
+
+def bnr_reference_bn_add_relu(backward, y, bn, out, ident=None, tmp=None, g=None, gm=None, dgamma=None, dbeta=None,
+                              dx=None):
+    py, m, c, ldy = view(y)
+    po, _, _, ldo = view(out)
+    pi, ldi = (view(ident)[0], view(ident)[3]) if ident is not None else (None, 0)
+    pg, ldg = (view(g)[0], view(g)[3]) if g is not None else (None, 0)
+    pdx, lddx = (view(dx)[0], view(dx)[3]) if dx is not None else (None, 0)
+    bs = bn.struct()
+    a = AddReluRefArgs(py, ldy, ctypes.pointer(bs), pi, ldi, po, ldo, _ptr(tmp), pg, ldg, _ptr(gm), _ptr(dgamma),
+                       _ptr(dbeta), pdx, lddx)
+    ws, wsb = workspace(bnr_stats_workspace_size(m, c), y.device)
+    _check(_lib_fns["bnr_reference_bn_add_relu"](1 if backward else 0, m, c, dtype_code(y), ctypes.byref(a), ws, wsb,
+                                                 _stream()))
 
 
 def bnr_hbm_copy(src, dst):

@@ -625,6 +625,133 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
     return ok();
 }
 
+bnr_status bnr_conv_fwd(const bnr_conv_desc *d, const void *x, const void *w, void *y, void *ws, size_t ws_bytes,
+                        void *stream)
+{
+    return conv_fwd(d, x, nullptr, w, y, nullptr, ws, ws_bytes, stream);
+}
+
+// shared argument checks of the residual BN-add-ReLU calls
+static bnr_status check_rows(int64_t m, int32_t c, bnr_dtype dtype)
+{
+    TRY(check_dtype(dtype));
+    if (m <= 0 || m > ((int64_t)1 << 31)) return fail(BNR_ERR_SHAPE, "m = %lld out of range", (long long)m);
+    return check_channels(c, c, dtype, "c");
+}
+
+bnr_status bnr_bn_add_relu_fwd(int64_t m, int32_t c, bnr_dtype dtype, const void *y, int32_t y_ldc, const bnr_bn *bn,
+                               const void *id, int32_t id_ldc, void *out, int32_t out_ldc, void *stream)
+{
+    TRY(check_rows(m, c, dtype));
+    TRY(check_channels(c, y_ldc, dtype, "y"));
+    TRY(check_channels(c, id_ldc, dtype, "id"));
+    TRY(check_channels(c, out_ldc, dtype, "out"));
+    TRY(check_ptr(y, "y"));
+    TRY(check_ptr(id, "id"));
+    TRY(check_ptr(out, "out"));
+    TRY(check_bn(bn, "bn", true, false));
+    const int es = esize(dtype);
+    const Range ro = view_range(out, m, c, out_ldc, es);
+    if (overlap(ro, view_range(y, m, c, y_ldc, es))) return fail(BNR_ERR_ALIAS, "out overlaps y");
+    if (overlap(ro, view_range(id, m, c, id_ldc, es)) && !(out == id && out_ldc == id_ldc))
+        return fail(BNR_ERR_ALIAS, "out overlaps id");
+    TRY_HIP(launch_elementwise(dt_of(dtype), EW_BNADDRELU, m, c, y, y_ldc, id, id_ldc, bn->gamma, bn->beta, bn->mean,
+                               bn->rstd, nullptr, nullptr, out, out_ldc, 0, (hipStream_t)stream),
+            "BN + add + ReLU");
+    return ok();
+}
+
+bnr_status bnr_bn_add_relu_bwd(int64_t m, int32_t c, bnr_dtype dtype, const void *g, int32_t g_ldc, const void *out,
+                               int32_t out_ldc, const void *y, int32_t y_ldc, const bnr_bn *bn, void *gm,
+                               int32_t gm_ldc, float *dgamma, float *dbeta, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_rows(m, c, dtype));
+    TRY(check_channels(c, g_ldc, dtype, "g"));
+    TRY(check_channels(c, out_ldc, dtype, "out"));
+    TRY(check_channels(c, y_ldc, dtype, "y"));
+    TRY(check_channels(c, gm_ldc, dtype, "gm"));
+    TRY(check_ptr(g, "g"));
+    TRY(check_ptr(out, "out"));
+    TRY(check_ptr(y, "y"));
+    TRY(check_ptr(gm, "gm"));
+    TRY(check_bn(bn, "bn", false, false));
+    TRY(check_fptr(dgamma, "dgamma"));
+    TRY(check_fptr(dbeta, "dbeta"));
+    TRY(check_ws(ws, ws_bytes, stats_ws(m, c)));
+    const int es = esize(dtype);
+    const Range rg = view_range(gm, m, c, gm_ldc, es);
+    if (overlap(rg, view_range(out, m, c, out_ldc, es))) return fail(BNR_ERR_ALIAS, "gm overlaps out");
+    if (overlap(rg, view_range(y, m, c, y_ldc, es))) return fail(BNR_ERR_ALIAS, "gm overlaps y");
+    if (overlap(rg, view_range(g, m, c, g_ldc, es)) && !(gm == g && gm_ldc == g_ldc))
+        return fail(BNR_ERR_ALIAS, "gm overlaps g");
+    hipStream_t s = (hipStream_t)stream;
+    const int dt = dt_of(dtype);
+    const int64_t R = stats_row_blocks(m, c, dt);
+    float *part = (float *)ws;
+    void *red = (char *)ws + stats_part_bytes(m, c);
+    TRY_HIP(launch_addrelu_bwd(dt, m, c, g, g_ldc, out, out_ldc, y, y_ldc, bn->mean, bn->rstd, gm, gm_ldc, part, R, s),
+            "ReLU mask + BN backward sums");
+    TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma, red, s),
+            "backward sums combine");
+    return ok();
+}
+
+bnr_status bnr_reference_bn_add_relu(int32_t backward, int64_t m, int32_t c, bnr_dtype dtype,
+                                     const bnr_addrelu_ref_args *a, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_rows(m, c, dtype));
+    if (!a) return fail(BNR_ERR_NULL, "args is NULL");
+    TRY(check_channels(c, a->y_ldc, dtype, "y"));
+    TRY(check_ptr(a->y, "y"));
+    TRY(check_ptr(a->out, "out"));
+    TRY(check_channels(c, a->out_ldc, dtype, "out"));
+    TRY(check_ws(ws, ws_bytes, stats_ws(m, c)));
+    hipStream_t s = (hipStream_t)stream;
+    const int dt = dt_of(dtype);
+    const bnr_bn *bn = a->bn;
+    const int64_t R = stats_row_blocks(m, c, dt);
+    float *part = (float *)ws;
+    void *red = (char *)ws + stats_part_bytes(m, c);
+    if (!backward) {
+        TRY(check_bn(bn, "bn", true, true));
+        TRY(check_ptr(a->id, "id"));
+        TRY(check_channels(c, a->id_ldc, dtype, "id"));
+        TRY(check_ptr(a->tmp, "tmp"));
+        // two-pass statistics, normalise (write tmp), add + ReLU (write out)
+        TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_SUM, nullptr, nullptr, nullptr, 0, part, R, s),
+                "mean sweep");
+        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MEAN, bn->eps, bn->mean, nullptr, nullptr, nullptr, nullptr,
+                                      red, s), "mean combine");
+        TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_SQDEV, bn->mean, nullptr, nullptr, 0, part, R, s),
+                "variance sweep");
+        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, nullptr, bn->var, bn->rstd, nullptr, nullptr,
+                                      red, s), "variance combine");
+        TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->y, a->y_ldc, nullptr, 0, bn->gamma, bn->beta, bn->mean,
+                                   bn->rstd, nullptr, nullptr, a->tmp, c, 0, s), "normalise");
+        TRY_HIP(launch_elementwise(dt, EW_ADDRELU, m, c, a->tmp, c, a->id, a->id_ldc, nullptr, nullptr, nullptr,
+                                   nullptr, nullptr, nullptr, a->out, a->out_ldc, 0, s), "add + ReLU");
+        return ok();
+    }
+    TRY(check_bn(bn, "bn", true, false));
+    TRY(check_ptr(a->g, "g"));
+    TRY(check_channels(c, a->g_ldc, dtype, "g"));
+    TRY(check_ptr(a->gm, "gm"));
+    TRY(check_ptr(a->dx, "dx"));
+    TRY(check_channels(c, a->dx_ldc, dtype, "dx"));
+    TRY(check_fptr(a->dgamma, "dgamma"));
+    TRY(check_fptr(a->dbeta, "dbeta"));
+    // ReLU backward (write gm), BN reductions sweep, BN input-gradient sweep (write dx)
+    TRY_HIP(launch_elementwise(dt, EW_RELUBWD, m, c, a->g, a->g_ldc, a->out, a->out_ldc, nullptr, nullptr, nullptr,
+                               nullptr, nullptr, nullptr, a->gm, c, 0, s), "ReLU backward");
+    TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_DYX, bn->mean, bn->rstd, a->gm, c, part, R, s),
+            "BN backward sums");
+    TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma, red, s),
+            "backward sums combine");
+    TRY_HIP(launch_elementwise(dt, EW_DX, m, c, a->gm, c, a->y, a->y_ldc, bn->gamma, nullptr, bn->mean, bn->rstd,
+                               a->dgamma, a->dbeta, a->dx, a->dx_ldc, 0, s), "BN input gradient");
+    return ok();
+}
+
 bnr_status bnr_hbm_copy(const void *src, void *dst, size_t bytes, void *stream)
 {
     TRY(check_ptr(src, "src"));

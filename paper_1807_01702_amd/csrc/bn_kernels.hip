@@ -225,6 +225,8 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__res
 //   EW_APPLY   : out = gamma*(x-mean)*rstd + beta                  (unfused BN)
 //   EW_RELU    : out = max(x, 0)                                   (unfused ReLU)
 //   EW_RELUBWD : out = x2 > 0 ? x : 0   (x = dz, x2 = y)           (unfused ReLU bwd)
+//   EW_BNADDRELU: out = max(gamma*(x-mean)*rstd + beta + x2, 0)    (residual BN + add + ReLU)
+//   EW_ADDRELU : out = max(x + x2, 0)                              (unfused add + ReLU)
 template <typename T, int MODE, bool ACC>
 __global__ __launch_bounds__(kThreads) void k_elementwise(
     int64_t m, int C, const T *__restrict__ x, int64_t x_ldc, const T *__restrict__ x2,
@@ -233,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
     const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int64_t rows_per_block)
 {
     constexpr int VEC = Elem<T>::VEC, U = 2;
-    constexpr bool TWO = MODE == EW_DX || MODE == EW_RELUBWD;
+    constexpr bool TWO = MODE == EW_DX || MODE == EW_RELUBWD || MODE == EW_BNADDRELU || MODE == EW_ADDRELU;
     const int cvec = C / VEC;
     const int vb = min(kStatsMaxVec, cvec - (int)blockIdx.y * kStatsMaxVec);
     const int ry = kThreads / vb;
@@ -256,6 +258,9 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
             p1[i] = beta[c];
             p2[i] = rstd[c];
             p3[i] = mean[c];
+        } else if (MODE == EW_BNADDRELU) {
+            p0[i] = gamma[c] * rstd[c];
+            p1[i] = beta[c] - mean[c] * p0[i];
         }
     }
     auto row = [&](const vec16 &vx, const vec16 &v2, const vec16 &vo) __attribute__((always_inline)) {
@@ -277,6 +282,16 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
             for (int i = 0; i < VEC; i++) o[i] = p0[i] * ((f[i] - p3[i]) * p2[i]) + p1[i];
         } else if (MODE == EW_RELU) {
             for (int i = 0; i < VEC; i++) o[i] = f[i] > 0.f ? f[i] : 0.f;
+        } else if (MODE == EW_BNADDRELU) {
+            for (int i = 0; i < VEC; i++) {
+                const float t = __builtin_fmaf(f[i], p0[i], p1[i]) + g[i];
+                o[i] = t > 0.f ? t : 0.f;
+            }
+        } else if (MODE == EW_ADDRELU) {
+            for (int i = 0; i < VEC; i++) {
+                const float t = f[i] + g[i];
+                o[i] = t > 0.f ? t : 0.f;
+            }
         } else {
             for (int i = 0; i < VEC; i++) o[i] = g[i] > 0.f ? f[i] : 0.f;
         }
@@ -302,6 +317,78 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
         const vec16 v2 = TWO ? ldg16(x2 + r * x2_ldc + c0) : vx;
         const vec16 vo = ACC ? ldg16(out + r * out_ldc + c0) : vx;
         stg16(out + r * out_ldc + c0, row(vx, v2, vo));
+    }
+}
+
+// --------------------------------------------------------------------------
+// Backward of out = relu(bn(y) + identity) up to the BN reductions, in one
+// sweep: gm = g * [out > 0] (the gradient of both the identity and the BN
+// output), s1 = sum gm, s2 = sum gm * (y - mean) * rstd.  Row blocks as in
+// k_stats_partial.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_addrelu_bwd(
+    const T *g, int64_t g_ldc, const T *__restrict__ out, int64_t out_ldc, const T *__restrict__ y,
+    int64_t y_ldc, int64_t m, int C, const float *__restrict__ mean, const float *__restrict__ rstd, T *gm,
+    int64_t gm_ldc, int64_t rows_per_block, float *__restrict__ part)
+{
+    constexpr int VEC = Elem<T>::VEC, U = 2;
+    __shared__ float red[2][kThreads * VEC];
+    const int cvec = C / VEC;
+    const int vb = min(kStatsMaxVec, cvec - (int)blockIdx.y * kStatsMaxVec);
+    const int ry = kThreads / vb;
+    const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
+    const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
+    float s1[VEC], s2[VEC], mu[VEC], rs[VEC];
+    for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 0.f; }
+    if (ty < ry)
+        for (int i = 0; i < VEC; i++) { mu[i] = mean[c0 + i]; rs[i] = rstd[c0 + i]; }
+    auto row = [&](const vec16 &vg, const vec16 &vo, const vec16 &vy, T *dst) __attribute__((always_inline)) {
+        float fg[VEC], fo[VEC], fy[VEC];
+        Elem<T>::unpack(vg, fg);
+        Elem<T>::unpack(vo, fo);
+        Elem<T>::unpack(vy, fy);
+        for (int i = 0; i < VEC; i++) {
+            const float d = fo[i] > 0.f ? fg[i] : 0.f;
+            fg[i] = d;
+            s1[i] += d;
+            s2[i] += d * ((fy[i] - mu[i]) * rs[i]);
+        }
+        stg16(dst, Elem<T>::pack(fg));
+    };
+    const int64_t r0 = (int64_t)blockIdx.x * rows_per_block;
+    const int64_t r1 = min(m, r0 + rows_per_block);
+    if (ty < ry) {
+        int64_t r = r0 + ty;
+        for (; r + (U - 1) * ry < r1; r += U * ry) {
+            vec16 vg[U], vo[U], vy[U];
+            #pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int64_t rr = r + u * ry;
+                vg[u] = ldg16(g + rr * g_ldc + c0);
+                vo[u] = ldg16(out + rr * out_ldc + c0);
+                vy[u] = ldg16(y + rr * y_ldc + c0);
+            }
+            #pragma unroll
+            for (int u = 0; u < U; u++) row(vg[u], vo[u], vy[u], gm + (r + u * ry) * gm_ldc + c0);
+        }
+        for (; r < r1; r += ry)
+            row(ldg16(g + r * g_ldc + c0), ldg16(out + r * out_ldc + c0), ldg16(y + r * y_ldc + c0),
+                gm + r * gm_ldc + c0);
+    }
+    const int nch = vb * VEC;
+    if (ty < ry)
+        for (int i = 0; i < VEC; i++) {
+            red[0][ty * nch + tx * VEC + i] = s1[i];
+            red[1][ty * nch + tx * VEC + i] = s2[i];
+        }
+    __syncthreads();
+    if (tid < nch) {
+        float a = 0.f, b = 0.f;
+        for (int j = 0; j < ry; j++) { a += red[0][j * nch + tid]; b += red[1][j * nch + tid]; }
+        const int c = (int)blockIdx.y * kStatsMaxVec * VEC + tid;
+        float *p = part + (int64_t)blockIdx.x * 2 * C;
+        p[c] = a;
+        p[C + c] = b;
     }
 }
 
@@ -498,15 +585,15 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
                               int64_t out_ldc, int accumulate, hipStream_t s)
 {
-    if (!x || !out || ((mode == EW_DX || mode == EW_RELUBWD) && !x2) ||
-        (mode == EW_DX && (!gamma || !rstd || !mean || !dgamma || !dbeta)) ||
-        (mode == EW_APPLY && (!gamma || !beta || !mean || !rstd)))
+    const bool two = mode == EW_DX || mode == EW_RELUBWD || mode == EW_BNADDRELU || mode == EW_ADDRELU;
+    if (!x || !out || (two && !x2) || (mode == EW_DX && (!gamma || !rstd || !mean || !dgamma || !dbeta)) ||
+        ((mode == EW_APPLY || mode == EW_BNADDRELU) && (!gamma || !beta || !mean || !rstd)))
         return hipErrorInvalidValue;
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
     const int64_t R = stats_row_blocks(m, C, dtype) * 4;
     const int64_t rpb = ceil_div(m, R);
     dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
-    const double sweeps = mode == EW_DX ? 3.0 + (accumulate ? 1.0 : 0.0) : (mode == EW_RELUBWD ? 3.0 : 2.0);
+    const double sweeps = mode == EW_DX ? 3.0 + (accumulate ? 1.0 : 0.0) : (two ? 3.0 : 2.0);
     TraceScope tr(KC_SWEEP, KID_ELEMENTWISE, s, sweeps * (double)m * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
     auto go = [&](auto kern, auto tag) {
         using T = decltype(tag);
@@ -519,6 +606,8 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
             else go(k_elementwise<bf16_t, EW_DX, false>, bf16_t());
         } else if (mode == EW_APPLY) go(k_elementwise<bf16_t, EW_APPLY, false>, bf16_t());
         else if (mode == EW_RELU) go(k_elementwise<bf16_t, EW_RELU, false>, bf16_t());
+        else if (mode == EW_BNADDRELU) go(k_elementwise<bf16_t, EW_BNADDRELU, false>, bf16_t());
+        else if (mode == EW_ADDRELU) go(k_elementwise<bf16_t, EW_ADDRELU, false>, bf16_t());
         else go(k_elementwise<bf16_t, EW_RELUBWD, false>, bf16_t());
     } else {
         if (mode == EW_DX) {
@@ -526,8 +615,30 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
             else go(k_elementwise<float, EW_DX, false>, float());
         } else if (mode == EW_APPLY) go(k_elementwise<float, EW_APPLY, false>, float());
         else if (mode == EW_RELU) go(k_elementwise<float, EW_RELU, false>, float());
+        else if (mode == EW_BNADDRELU) go(k_elementwise<float, EW_BNADDRELU, false>, float());
+        else if (mode == EW_ADDRELU) go(k_elementwise<float, EW_ADDRELU, false>, float());
         else go(k_elementwise<float, EW_RELUBWD, false>, float());
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_addrelu_bwd(int dtype, int64_t m, int C, const void *g, int64_t g_ldc, const void *out,
+                              int64_t out_ldc, const void *y, int64_t y_ldc, const float *mean, const float *rstd,
+                              void *gm, int64_t gm_ldc, float *part, int64_t R, hipStream_t s)
+{
+    if (!g || !out || !y || !mean || !rstd || !gm || !part) return hipErrorInvalidValue;
+    const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
+    const int64_t rpb = ceil_div(m, R);
+    dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
+    TraceScope tr(KC_SWEEP, KID_ELEMENTWISE, s, 4.0 * (double)m * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
+    if (dtype == DT_BF16)
+        hipLaunchKernelGGL(k_addrelu_bwd<bf16_t>, grid, dim3(kThreads), 0, s, (const bf16_t *)g, g_ldc,
+                           (const bf16_t *)out, out_ldc, (const bf16_t *)y, y_ldc, m, C, mean, rstd, (bf16_t *)gm,
+                           gm_ldc, rpb, part);
+    else
+        hipLaunchKernelGGL(k_addrelu_bwd<float>, grid, dim3(kThreads), 0, s, (const float *)g, g_ldc,
+                           (const float *)out, out_ldc, (const float *)y, y_ldc, m, C, mean, rstd, (float *)gm, gm_ldc,
+                           rpb, part);
     return hipGetLastError();
 }
 

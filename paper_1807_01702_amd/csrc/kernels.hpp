@@ -11,7 +11,7 @@ enum { ST_SUMSQ = 0, ST_SUM = 1, ST_SQDEV = 2, ST_DYX = 3 };
 // k_stats_finalize modes
 enum { FIN_MVF = 0, FIN_MEAN = 1, FIN_VAR = 2, FIN_BWD = 3 };
 // k_elementwise modes
-enum { EW_DX = 0, EW_APPLY = 1, EW_RELU = 2, EW_RELUBWD = 3 };
+enum { EW_DX = 0, EW_APPLY = 1, EW_RELU = 2, EW_RELUBWD = 3, EW_BNADDRELU = 4, EW_ADDRELU = 5 };
 
 // Reduction scratch ("red") of a statistics combine: the float64 level-1
 // sums [RS][2][C] (RS <= kRedMaxRS row splits).
@@ -29,6 +29,11 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
                               int64_t x2_ldc, const float *gamma, const float *beta, const float *mean,
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
                               int64_t out_ldc, int accumulate, hipStream_t s);
+// Residual-block backward sweep: gm = g * [out > 0], per-channel sum(gm) and
+// sum(gm * (y - mean) * rstd) partials [R][2][C].
+hipError_t launch_addrelu_bwd(int dtype, int64_t m, int C, const void *g, int64_t g_ldc, const void *out,
+                              int64_t out_ldc, const void *y, int64_t y_ldc, const float *mean, const float *rstd,
+                              void *gm, int64_t gm_ldc, float *part, int64_t R, hipStream_t s);
 hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, hipStream_t s);
 hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, void *gx, int64_t ldc,
                                hipStream_t s);

@@ -13,7 +13,9 @@ Workloads (shapes of the paper's DenseNet-121 / ResNet-50 training):
                       CONV3x3(k) whose k new channels are concatenated (Sec. 2.3).
 * ``DenseBlock``   -- dense block 1 (6 composite layers, growth 32, width 128,
                       64 -> 256 channels) + transition BN-ReLU-CONV1x1 + 2x2
-                      average pooling.  Concat is a channel-offset buffer
+                      average pooling.
+* ``ResNetStack``  -- ResNet-50 conv2_x bottleneck blocks with identity
+                      shortcuts.  Concat is a channel-offset buffer
                       (pointer passing, as the paper's reference does for
                       Split); Split's backward is the accumulation of every
                       reader's input gradient into that buffer's gradient.
@@ -258,6 +260,105 @@ class DenseBlock:
                 u2.ref_bwd(self.G[..., c_l:c_l + k], _dense(self.dz_flat, n, h, w, width), self.dy2, self.dx2, False)
                 u1.ref_bwd(self.dx2, _dense(self.dz_flat, n, h, w, c_l), _dense(self.dy1_flat, n, h, w, c_l),
                            self.G[..., :c_l], True)
+
+    def step(self):
+        self.forward()
+        self.backward()
+
+
+class ResNetStack:
+    """ResNet-50 conv2_x: bottleneck blocks CONV1x1(c -> width) - BN - ReLU -
+    CONV3x3(width -> width) - BN - ReLU - CONV1x1(width -> c) - BN, + identity,
+    ReLU (He et al., as used in the paper's ResNet-50 evaluation).
+
+    Fused: every BN's statistics come from the epilogue of the CONV that
+    produces its input; BN1/BN2 + ReLU run in the next CONV's prologue; the
+    last BN of a block is followed by the residual addition, so it runs with
+    the addition and the ReLU as one element-wise sweep, and its input
+    gradient is consumed deferred by the third CONV's backward.  Unfused: the
+    reference chain (two-pass statistics, materialised normalised / ReLU
+    tensors and gradients)."""
+
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE):
+        bf16 = data["bf16"]
+        dev = torch.device(device)
+        dt = torch.bfloat16 if bf16 else torch.float32
+        n, h, w, c = data["x"].shape
+        width = data["blocks"][0]["w1"].shape[3]
+        self.n, self.h, self.w, self.c, self.width = n, h, w, c, width
+        self.fused, self.images = fused, n
+        eps = data["eps"]
+        self.x0 = _t(data["x"], dev, bf16)
+        self.gout = _t(data["dy"], dev, bf16)
+        self.blocks = []
+        xin = self.x0
+        for p in data["blocks"]:
+            b = dict(xin=xin)
+            b["y1"] = torch.empty((n, h, w, width), dtype=dt, device=dev)
+            b["y2"] = torch.empty_like(b["y1"])
+            b["y3"] = torch.empty((n, h, w, c), dtype=dt, device=dev)
+            b["out"] = torch.empty_like(b["y3"])
+            b["w1"] = _t(p["w1"], dev, bf16)
+            b["dw1"] = torch.empty(tuple(p["w1"].shape), dtype=torch.float32, device=dev)
+            b["desc1"] = B.desc_for(xin, b["y1"], 1, n, h, w)
+            # BN1 -> ReLU -> CONV3x3 and BN2 -> ReLU -> CONV1x1 as units
+            b["u2"] = _Unit(n, h, w, b["y1"], b["y2"], 3, p["gamma1"], p["beta1"], p["w2"], eps, dev, bf16, fused,
+                            ref_mode)
+            b["u3"] = _Unit(n, h, w, b["y2"], b["y3"], 1, p["gamma2"], p["beta2"], p["w3"], eps, dev, bf16, fused,
+                            ref_mode)
+            b["bn3"] = B.BN(_f32(p["gamma3"], dev), _f32(p["beta3"], dev), eps)
+            b["g3"] = _Grads(c, dev)
+            self.blocks.append(b)
+            xin = b["out"]
+        self.out = xin
+        self.gbuf = torch.empty_like(self.x0)                      # gradient of the current block input
+        self.dyw = torch.empty((n, h, w, width), dtype=dt, device=dev)
+        self.dyw2 = torch.empty_like(self.dyw)
+        if not fused:
+            self.tmp = torch.empty_like(self.x0)
+            self.dx3 = torch.empty_like(self.x0)
+            self.dyw3 = torch.empty_like(self.dyw)
+            self.dzw = torch.empty_like(self.dyw)
+
+    def forward(self):
+        for b in self.blocks:
+            u2, u3 = b["u2"], b["u3"]
+            if self.fused:
+                B.bnr_conv_bn_stats_fwd(b["desc1"], b["xin"], b["w1"], b["y1"], u2.bn)
+                B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out, u3.bn)
+                B.bnr_bn_relu_conv_fwd(u3.desc, u3.x, u3.bn, u3.wt, u3.out, b["bn3"])
+                B.bnr_bn_add_relu_fwd(b["y3"], b["bn3"], b["xin"], b["out"])
+            else:
+                B.bnr_conv_fwd(b["desc1"], b["xin"], b["w1"], b["y1"])
+                u2.ref_fwd()
+                u3.ref_fwd()
+                B.bnr_reference_bn_add_relu(False, b["y3"], b["bn3"], b["out"], ident=b["xin"], tmp=self.tmp)
+
+    def backward(self):
+        g = self.gout
+        for b in reversed(self.blocks):
+            u2, u3, g3 = b["u2"], b["u3"], b["g3"]
+            if self.fused:
+                # gm = g * [out > 0] into gbuf (in place from the second block on), BN3 sums
+                B.bnr_bn_add_relu_bwd(g, b["out"], b["y3"], b["bn3"], self.gbuf, g3.dgamma, g3.dbeta)
+                B.bnr_bwd_fused(u3.desc, u3.x, u3.bn, u3.wt, B.grad_bn(self.gbuf, b["y3"], b["bn3"], g3.dgamma,
+                                                                       g3.dbeta),
+                                u3.dw, u3.g.dgamma, u3.g.dbeta, self.dyw)
+                B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt, B.grad_bn(self.dyw, u3.x, u3.bn, u3.g.dgamma,
+                                                                       u3.g.dbeta),
+                                u2.dw, u2.g.dgamma, u2.g.dbeta, self.dyw2)
+                # first CONV: its input has no BN in front; identity gradient + data gradient
+                B.bnr_bwd_fused(b["desc1"], b["xin"], None, b["w1"], B.grad_bn(self.dyw2, u2.x, u2.bn,
+                                                                               u2.g.dgamma, u2.g.dbeta),
+                                b["dw1"], dx=self.gbuf, dx_accumulate=True)
+            else:
+                B.bnr_reference_bn_add_relu(True, b["y3"], b["bn3"], b["out"], g=g, gm=self.gbuf,
+                                            dgamma=g3.dgamma, dbeta=g3.dbeta, dx=self.dx3)
+                u3.ref_bwd(self.dx3, self.dzw, self.dyw, self.dyw2, False)
+                u2.ref_bwd(self.dyw2, self.dzw, self.dyw, self.dyw3, False)
+                B.bnr_bwd_fused(b["desc1"], b["xin"], None, b["w1"], B.grad_dense(self.dyw3), b["dw1"],
+                                dx=self.gbuf, dx_accumulate=True)
+            g = self.gbuf
 
     def step(self):
         self.forward()

@@ -17,6 +17,11 @@ the CPU oracle run on the same seeded inputs.
     unfused GPU paths differ from each other as much as from the oracle).  The
     test therefore requires the fused path's backward to be as accurate as the
     unfused path's (relative L2 distance to the oracle within 25%).
+* ResNet-50 conv2_x stack (bottleneck blocks with identity shortcuts):
+  - fp32 storage, small shapes: every tensor of two blocks, fused and
+    unfused, rtol 1e-4 (same ReLU-margin precondition);
+  - bf16 operands, the conv2_x channel shapes at reduced batch: forward and
+    statistics at rtol 2e-2, backward accuracy equivalence as for the block.
 """
 import numpy as np
 import pytest
@@ -53,6 +58,8 @@ def _step_twice(wl):
 
 
 def _grad_tensors(wl):
+    if hasattr(wl, "blocks"):
+        return [wl.gbuf] + [t for b in wl.blocks for t in (b["dw1"], b["u2"].dw, b["u3"].dw)]
     if hasattr(wl, "cpl"):
         return [wl.G, wl.ut.dw] + [u.dw for _, _, u1, u2 in wl.cpl for u in (u1, u2)]
     if hasattr(wl, "u1"):
@@ -221,3 +228,80 @@ def test_full_batch_dense_block_forward_and_invariants():
     np.testing.assert_allclose(dy.sum(0), db, rtol=0, atol=1e-5 * np.abs(dy).sum(0).max())
     np.testing.assert_allclose((dy * xh).sum(0), dg, rtol=0, atol=1e-5 * np.abs(dy * xh).sum(0).max())
     assert np.max(np.abs(xh.sum(0))) <= 1e-5 * len(xh)
+
+
+# ------------------------------------------------------------ ResNet stack ----
+def _resnet_oracle(d):
+    rnd = OC.storage(d["bf16"])
+    X = np.asarray(d["x"], np.float64)
+    outs, caches = [], []
+    for p in d["blocks"]:
+        X, c = OC.resnet_block_fwd(X, p, d["eps"], rnd)
+        outs.append(X)
+        caches.append(c)
+    g = np.asarray(d["dy"], np.float64)
+    grads = [None] * len(caches)
+    for i in reversed(range(len(caches))):
+        g, grads[i] = OC.resnet_block_bwd(caches[i], g, rnd)
+    return outs, caches, g, grads
+
+
+def _resnet_margin(caches):
+    ys = []
+    for c in caches:
+        ys += [c["u2"]["y"], c["u3"]["y"], c["s"]]
+    return min(float(np.min(np.abs(y)) / np.max(np.abs(y))) for y in ys)
+
+
+def _check_resnet_forward(wl, outs, caches, rt):
+    for i, (b, o, c) in enumerate(zip(wl.blocks, outs, caches)):
+        assert_close("out%d" % i, host(b["out"]), o, rt)
+        assert_stats("bn1 b%d" % i, host(b["u2"].bn.mean), host(b["u2"].bn.var), c["u2"]["mean"], c["u2"]["var"], rt)
+        assert_stats("bn2 b%d" % i, host(b["u3"].bn.mean), host(b["u3"].bn.var), c["u3"]["mean"], c["u3"]["var"], rt)
+        assert_stats("bn3 b%d" % i, host(b["bn3"].mean), host(b["bn3"].var), c["mean3"], c["var3"], rt)
+
+
+def _resnet_grads(wl, grads):
+    """(name, gpu tensor, oracle value) of every backward output."""
+    out = []
+    for i, (b, g) in enumerate(zip(wl.blocks, grads)):
+        out += [("dW1 b%d" % i, b["dw1"], g["dw1"]), ("dW2 b%d" % i, b["u2"].dw, g["b2"]["dw"]),
+                ("dW3 b%d" % i, b["u3"].dw, g["b3"]["dw"]),
+                ("dgamma1 b%d" % i, b["u2"].g.dgamma, g["b2"]["dgamma"]),
+                ("dbeta1 b%d" % i, b["u2"].g.dbeta, g["b2"]["dbeta"]),
+                ("dgamma2 b%d" % i, b["u3"].g.dgamma, g["b3"]["dgamma"]),
+                ("dbeta2 b%d" % i, b["u3"].g.dbeta, g["b3"]["dbeta"]),
+                ("dgamma3 b%d" % i, b["g3"].dgamma, g["dgamma3"]), ("dbeta3 b%d" % i, b["g3"].dbeta, g["dbeta3"])]
+    return out
+
+
+@pytest.mark.parametrize("mode", ["fused", "baseline"])
+def test_resnet_stack_fp32_all_tensors(mode):
+    d = synth.resnet_stack(seed=0, n=2, h=8, w=8, c=64, width=16, blocks=2, bf16=False)
+    outs, caches, dX, grads = _resnet_oracle(d)
+    assert _resnet_margin(caches) >= 1e-6, "precondition: ReLU decisions must be unique at fp32 accuracy"
+    wl = _make("ResNetStack", d, mode)
+    _step_twice(wl)
+    rt = RTOL[False]
+    _check_resnet_forward(wl, outs, caches, rt)
+    assert_close("dX", host(wl.gbuf), dX, rt)
+    for name, t, ref in _resnet_grads(wl, grads):
+        assert_close(name, host(t), ref, rt)
+
+
+def test_resnet_stack_bf16():
+    d = synth.resnet_stack(seed=0, n=2, blocks=3)
+    outs, caches, dX, grads = _resnet_oracle(d)
+    rt = RTOL[True]
+    errs = {}
+    for mode in ("fused", "baseline"):
+        wl = _make("ResNetStack", d, mode)
+        _step_twice(wl)
+        _check_resnet_forward(wl, outs, caches, rt)
+        # the last block's BN3 sums and third-CONV weight gradient precede every ReLU decision but one
+        e = [_l2(host(wl.gbuf), dX)] + [_l2(host(t), ref) for _, t, ref in _resnet_grads(wl, grads)]
+        errs[mode] = np.array(e)
+        del wl
+    fused, unfused = errs["fused"], errs["baseline"]
+    assert np.all(fused <= 1.25 * unfused + 2e-3), (fused, unfused)
+    assert np.all(fused <= 0.2), fused
