@@ -7,7 +7,7 @@ layers + transition) over one batch of synthetic inputs already resident in
 HBM.  Both steps are captured once in a HIP graph and replayed.
 
 Prints one JSON line (rank 0).  Options: --gpus (1 only), --steps, --warmup,
---workload {dense_block,bottleneck,single_layer}, --no-graph,
+--workload {dense_block,bottleneck,single_layer,resnet_stack}, --no-graph,
 --no-cpu-baseline, --profile-only (steps only, for rocprofv3 runs).
 """
 import argparse
@@ -23,6 +23,7 @@ WORKLOADS = {
     "dense_block": ("DenseBlock", "dense_block", dict(n=64)),
     "bottleneck": ("Bottleneck", "bottleneck", dict(n=32)),
     "single_layer": ("SingleLayer", "single_layer", dict()),
+    "resnet_stack": ("ResNetStack", "resnet_stack", dict(n=128)),
 }
 
 
@@ -153,6 +154,17 @@ def cpu_baseline(args):
         t0 = time.perf_counter()
         _, c = OC.bottleneck_fwd(d["x"], d["p"]["w2"].shape[3], d["p"], d["eps"], rnd)
         OC.bottleneck_bwd(c, d["dy"].astype(np.float64), rnd)
+    elif args.workload == "resnet_stack":
+        n = 4                     # bounded sample: the stack at batch 4 (per-image cost is batch independent)
+        d = synth.resnet_stack(seed=0, n=n)
+        t0 = time.perf_counter()
+        X, cs = d["x"], []
+        for p in d["blocks"]:
+            X, c = OC.resnet_block_fwd(X, p, d["eps"], rnd)
+            cs.append(c)
+        g = d["dy"].astype(np.float64)
+        for c in reversed(cs):
+            g, _ = OC.resnet_block_bwd(c, g, rnd)
     else:
         d = synth.single_layer(seed=0)
         n = d["x"].shape[0]
@@ -199,7 +211,9 @@ def main():
         "config": {"workload": {"dense_block": "DenseNet-121 dense block 1 (6 composite layers, growth 32, width "
                                                "128, 64->256 ch) + transition BN-ReLU-CONV1x1 256->128 + avgpool2",
                                 "bottleneck": "DenseNet-121 bottleneck layer 256->128->32 + concat",
-                                "single_layer": "BN-ReLU-CONV1x1 64->32"}[args.workload],
+                                "single_layer": "BN-ReLU-CONV1x1 64->32",
+                                "resnet_stack": "ResNet-50 conv2_x: 3 bottleneck blocks 256->64->64->256 with "
+                                                "identity shortcuts"}[args.workload],
                    "global_batch": fused["images"] if fused else unf["images"], "image_hw": 56,
                    "graph": not args.no_graph},
         "unfused": {"images_per_s": unf["images"] / (unf["ms"] / 1e3), "ms_per_step": unf["ms"]} if unf else None,

@@ -125,6 +125,34 @@ def dense_block(m, c0, layers, width, k, trans_out, e):
     return {"fused": f.total, "unfused": u.total}
 
 
+def resnet_stack(m, c, width, blocks, e):
+    """Bottleneck blocks CONV1x1(c->width)-BN-ReLU-CONV3x3-BN-ReLU-CONV1x1(width->c)-BN, + id, ReLU."""
+    f, u = _Acc(), _Acc()
+    S, Sw = m * c * e, m * width * e
+    w1, w2, w3 = c * width * e, 9 * width * width * e, width * c * e
+    for _ in range(blocks):
+        # forward: first CONV reads X and writes y1 with BN1's statistics (fused) / without (unfused)
+        for a in (f, u):
+            a += S + w1 + Sw
+        _unit_fused_fwd(f, m, width, width, 3, e, False)
+        _unit_fused_fwd(f, m, width, c, 1, e, False)
+        f += 3 * S                            # BN3 + add + ReLU: read y3, X; write out
+        _unit_ref_fwd(u, m, width, width, 3, e)
+        _unit_ref_fwd(u, m, width, c, 1, e)
+        u += 2 * S + 2 * S + 3 * S            # two-pass statistics, normalise (r, w), add + ReLU (r, r, w)
+    for _ in range(blocks):
+        f += 4 * S                            # mask + BN3 sums: read g, out, y3; write gm
+        _unit_fused_bwd(f, m, width, c, 1, e, 2 * S, None)
+        _unit_fused_bwd(f, m, width, width, 3, e, 2 * Sw, None)
+        f += 2 * Sw + w1 + 2 * S              # first CONV dgrad: (dy1, y1) in, accumulate into gm
+        f += S + 2 * Sw + 4 * c * width       # its wgrad: X and (dy1, y1)
+        u += 3 * S + 2 * S + 3 * S            # ReLU backward (r, r, w), BN3 sums (r, r), BN3 dx (r, r, w)
+        _unit_ref_bwd(u, m, width, c, 1, e, S, False)
+        _unit_ref_bwd(u, m, width, width, 3, e, Sw, False)
+        u += Sw + w1 + 2 * S + S + Sw + 4 * c * width
+    return {"fused": f.total, "unfused": u.total}
+
+
 def for_workload(name, data):
     e = 2 if data.get("bf16") else 4
     if name == "single_layer":
@@ -134,6 +162,9 @@ def for_workload(name, data):
         n, h, w, ci = data["x"].shape
         p = data["p"]
         return bottleneck(n * h * w, ci, p["w1"].shape[3], p["w2"].shape[3], e)
+    if name == "resnet_stack":
+        n, h, w, c = data["x"].shape
+        return resnet_stack(n * h * w, c, data["blocks"][0]["w1"].shape[3], len(data["blocks"]), e)
     n, h, w, c0 = data["x"].shape
     cp = data["cpls"]
     return dense_block(n * h * w, c0, len(cp), cp[0]["w1"].shape[3], cp[0]["w2"].shape[3],
