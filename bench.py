@@ -4,7 +4,10 @@ fission/fusion path vs the unfused path, on one MI355X.
 
 A step is one forward + backward pass of the whole block (six composite
 layers + transition) over one batch of synthetic inputs already resident in
-HBM.  Both steps are captured once in a HIP graph and replayed.
+HBM.  Each variant's step is captured once in a HIP graph and replayed.
+Variants: fused (BN fission/fusion + inter-composite-layer fusion: the
+headline value), fused_no_icf (fission/fusion inside composite layers only)
+and unfused (the reference layer chain).
 
 Prints one JSON line (rank 0).  Options: --gpus (1 only), --steps, --warmup,
 --workload {dense_block,bottleneck,single_layer,resnet_stack}, --no-graph,
@@ -36,7 +39,7 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true")
-    ap.add_argument("--only", choices=["fused", "unfused"], default=None)
+    ap.add_argument("--only", choices=["fused", "fused_no_icf", "unfused"], default=None)
     return ap.parse_args()
 
 
@@ -45,11 +48,14 @@ def build_workloads(args, torch):
     from paper_1807_01702_amd import workloads as W
     cls, recipe, kw = WORKLOADS[args.workload]
     data = getattr(synth, recipe)(seed=0, **kw)
+    variants = [("fused", dict(fused=True)), ("unfused", dict(fused=False))]
+    if args.workload == "dense_block":          # fused = BNFF + inter-composite-layer fusion; BNFF alone beside it
+        variants.insert(1, ("fused_no_icf", dict(fused=True, icf=False)))
     out = {}
-    for name, fused in (("fused", True), ("unfused", False)):
+    for name, kw in variants:
         if args.only and args.only != name:
             continue
-        out[name] = getattr(W, cls)(data, fused=fused)
+        out[name] = getattr(W, cls)(data, **kw)
     return data, out
 
 
@@ -198,6 +204,7 @@ def main():
     kernels = traced_kernels(torch, wls["fused"], args.steps) if "fused" in wls else None
     fused = res.get("fused")
     unf = res.get("unfused")
+    noicf = res.get("fused_no_icf")
     model = bytes_model.for_workload(args.workload, data)
     line = {
         "metric": "training images/sec + HBM bytes/step, DenseNet-121 block (fused vs unfused)",
@@ -217,6 +224,8 @@ def main():
                    "global_batch": fused["images"] if fused else unf["images"], "image_hw": 56,
                    "graph": not args.no_graph},
         "unfused": {"images_per_s": unf["images"] / (unf["ms"] / 1e3), "ms_per_step": unf["ms"]} if unf else None,
+        "fused_no_icf": ({"images_per_s": noicf["images"] / (noicf["ms"] / 1e3), "ms_per_step": noicf["ms"],
+                          "algorithmic_bytes": model.get("fused_no_icf")} if noicf else None),
         "speedup_vs_unfused": (unf["ms"] / fused["ms"]) if (fused and unf) else None,
         "hbm_bytes_per_step": {"algorithmic_fused": model["fused"], "algorithmic_unfused": model["unfused"]},
         "roofline": roofline(kernels, dtype) if kernels else None,

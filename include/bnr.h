@@ -100,21 +100,31 @@ typedef enum {
                            /* g = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m),       */
                            /* xhat = (x - mean)*rstd, computed on the fly (Sec.3.2 */
                            /* backward fusion); never materialised                 */
-    BNR_GRAD_AVGPOOL2 = 2  /* the CONV output feeds a 2x2/2 average pooling and g  */
+    BNR_GRAD_AVGPOOL2 = 2, /* the CONV output feeds a 2x2/2 average pooling and g  */
                            /* is the pooled gradient [n][h/2][w/2][c_out]; the     */
                            /* CONV-output gradient g[p/2]/4 is formed on the fly   */
+    BNR_GRAD_SPLIT = 3     /* the CONV output x is read by several BN layers that  */
+                           /* share its statistics (DenseNet concatenation, Sec.   */
+                           /* 3.2 inter-composite-layer fusion) and their input    */
+                           /* gradients were left in summed form by                */
+                           /* bnr_bwd_fused_split: g view holds                    */
+                           /* D = sum_l gamma_l*rstd*dy_l, alpha/betap the per-    */
+                           /* channel sums; g = D + alpha + betap*xhat, xhat =      */
+                           /* (x - mean)*rstd from bn, formed on the fly           */
 } bnr_grad_kind;
 
 typedef struct {
     bnr_grad_kind kind;
-    const void *g;         /* DENSE, AVGPOOL2: gradient view                        */
-    int32_t g_ldc;         /* DENSE, AVGPOOL2: its pixel stride                     */
+    const void *g;         /* DENSE, AVGPOOL2, SPLIT (D): gradient view             */
+    int32_t g_ldc;         /* DENSE, AVGPOOL2, SPLIT: its pixel stride              */
     const void *dy;        /* BN: [m][c_out] dense gradient of the BN output        */
-    const void *x;         /* BN: the BN input (= this CONV's output) view           */
-    int32_t x_ldc;         /* BN: its pixel stride                                   */
-    const bnr_bn *bn;      /* BN: gamma, mean, rstd of that BN                       */
+    const void *x;         /* BN, SPLIT: the BN input (= this CONV's output) view    */
+    int32_t x_ldc;         /* BN, SPLIT: its pixel stride                            */
+    const bnr_bn *bn;      /* BN: gamma, mean, rstd of that BN; SPLIT: mean, rstd    */
     const float *dgamma;   /* BN: [c_out]                                            */
     const float *dbeta;    /* BN: [c_out]                                            */
+    const float *alpha;    /* SPLIT: [c_out]                                         */
+    const float *betap;    /* SPLIT: [c_out]                                         */
 } bnr_grad_src;
 
 /* ------------------------------------------------------------ sizes ---- */
@@ -192,6 +202,47 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
 bnr_status bnr_bn_dx(int64_t m, int32_t c, bnr_dtype dtype, const void *dy, const void *x, int32_t x_ldc,
                      const bnr_bn *bn, const float *dgamma, const float *dbeta,
                      void *dx, int32_t dx_ldc, int32_t dx_accumulate, void *stream);
+
+/* ------------------------- concatenation BNs (DenseNet, ICF) ---------- */
+
+/* Inter-composite-layer fusion (Sec. 3.2, last paragraph; the paper leaves it
+ * to future work and estimates its gain in Sec. 5).  In a dense block every
+ * BN1 reads channels of one concatenation buffer, and all BN layers that read
+ * a channel see the same values, hence the same mini-batch mean and rstd.
+ * Forward: each channel's statistics are produced once, by the epilogue of the
+ * CONV that writes it (bnr_bn_relu_conv_fwd with y_bn viewing the shared
+ * per-channel arrays at the channel offset) or by one bnr_bn_stats sweep over
+ * the block input; every BN1 then reads them, so no BN1 sweeps its input.
+ * Backward: the input gradient of channel c summed over its BN consumers l is
+ *   sum_l gamma_l*rstd*(dy_l - dbeta_l/m - xhat*dgamma_l/m)
+ *     = D + alpha + betap*xhat,  D = sum_l gamma_l*rstd*dy_l,
+ *   alpha = -sum_l gamma_l*rstd*dbeta_l/m,  betap = -sum_l gamma_l*rstd*dgamma_l/m,
+ * so each consumer's backward adds its term to D in its data-gradient
+ * epilogue and to alpha/betap in its reductions combine, and the producer's
+ * backward forms the gradient on load (BNR_GRAD_SPLIT).  (This factorisation
+ * is this library's reading of the fused Split-layer backward.) */
+
+/* bnr_bwd_fused for a BN whose input x is a concatenation slice: the same
+ * steps 1-3 (dgrad with the BN-backward epilogue, dbeta/dgamma combine,
+ * wgrad), except that the epilogue does not store dy but writes
+ * (accumulate = 0) or adds (accumulate = 1) gamma*rstd*dy into the view gsum
+ * (D above; [m][c_in], pixel stride gsum_ldc), and the combine also writes or
+ * adds alpha and betap ([c_in] float32).  x_bn is required.  gsum must not
+ * overlap x or any view g_src reads; with accumulate = 1 its old contents are
+ * read.  Outputs: dw, dgamma, dbeta (overwritten), gsum, alpha, betap. */
+bnr_status bnr_bwd_fused_split(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                               const bnr_grad_src *g_src, float *dw, float *dgamma, float *dbeta,
+                               void *gsum, int32_t gsum_ldc, int32_t accumulate, float *alpha, float *betap,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/* Materialise a summed BN input gradient: dx = gsum + alpha + betap*xhat with
+ * xhat = (x - mean)*rstd (mean, rstd from bn), written to (dx_accumulate = 0)
+ * or added into (1) the view dx.  All views [m][c] with their pixel strides.
+ * dx may alias gsum only if the views coincide exactly and dx_accumulate = 0;
+ * dx must not overlap x. */
+bnr_status bnr_split_dx(int64_t m, int32_t c, bnr_dtype dtype, const void *gsum, int32_t gsum_ldc,
+                        const void *x, int32_t x_ldc, const bnr_bn *bn, const float *alpha, const float *betap,
+                        void *dx, int32_t dx_ldc, int32_t dx_accumulate, void *stream);
 
 /* ------------------------------------------------- unfused A/B path ---- */
 

@@ -23,7 +23,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 BNR_F32, BNR_BF16 = 0, 1
-GRAD_DENSE, GRAD_BN, GRAD_AVGPOOL2 = 0, 1, 2
+GRAD_DENSE, GRAD_BN, GRAD_AVGPOOL2, GRAD_SPLIT = 0, 1, 2, 3
 MODE_BASELINE, MODE_RCF, MODE_RCF_MVF = 0, 1, 2
 STATUS = ["BNR_OK", "BNR_ERR_NULL", "BNR_ERR_SHAPE", "BNR_ERR_DTYPE", "BNR_ERR_ALIGN", "BNR_ERR_WORKSPACE",
           "BNR_ERR_UNSUPPORTED", "BNR_ERR_HIP", "BNR_ERR_ALIAS"]
@@ -42,7 +42,7 @@ class BNStruct(ctypes.Structure):
 
 class GradSrc(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int), ("g", c_vp), ("g_ldc", c_i32), ("dy", c_vp), ("x", c_vp), ("x_ldc", c_i32),
-                ("bn", ctypes.POINTER(BNStruct)), ("dgamma", c_vp), ("dbeta", c_vp)]
+                ("bn", ctypes.POINTER(BNStruct)), ("dgamma", c_vp), ("dbeta", c_vp), ("alpha", c_vp), ("betap", c_vp)]
 
 
 class RefArgs(ctypes.Structure):
@@ -82,6 +82,10 @@ _lib_fns = dict(
                           c_i32, c_vp),
     bnr_bwd_fused=_sig("bnr_bwd_fused", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, _P(GradSrc), c_vp,
                        c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_sz, c_vp),
+    bnr_bwd_fused_split=_sig("bnr_bwd_fused_split", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
+                             _P(GradSrc), c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp),
+    bnr_split_dx=_sig("bnr_split_dx", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_i32, c_vp, c_i32,
+                      _P(BNStruct), c_vp, c_vp, c_vp, c_i32, c_i32, c_vp),
     bnr_bn_dx=_sig("bnr_bn_dx", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_vp, c_i32, _P(BNStruct), c_vp, c_vp,
                    c_vp, c_i32, c_i32, c_vp),
     bnr_reference_path=_sig("bnr_reference_path", ctypes.c_int, ctypes.c_int, c_i32, _P(ConvDesc), _P(RefArgs), c_vp,
@@ -185,6 +189,16 @@ class BN:
         b.rstd = torch.empty(c, dtype=torch.float32, device=device)
         return b
 
+    @classmethod
+    def stats_view(cls, eps, mean, var, rstd):
+        """Statistics holder on caller-provided arrays (e.g. channel slices of
+        per-channel arrays shared by several BN layers)."""
+        b = cls.__new__(cls)
+        b.gamma = b.beta = None
+        b.eps = float(eps)
+        b.mean, b.var, b.rstd = mean, var, rstd
+        return b
+
     def struct(self):
         return BNStruct(_ptr(self.gamma), _ptr(self.beta), _ptr(self.mean), _ptr(self.var), _ptr(self.rstd),
                         self.eps)
@@ -261,10 +275,20 @@ def grad_bn(dy, x, bn, dgamma, dbeta):
                 keep=(dy, x, dgamma, dbeta))
 
 
+def grad_split(gsum, x, bn, alpha, betap):
+    """Summed gradient of a concatenation slice x read by several BNs with the
+    statistics in bn: g = gsum + alpha + betap * (x - mean) * rstd."""
+    pg, _, _, ldg = view(gsum)
+    px, _, _, ldx = view(x)
+    return dict(kind=GRAD_SPLIT, g=pg, g_ldc=ldg, x=px, x_ldc=ldx, bn=bn, alpha=_ptr(alpha), betap=_ptr(betap),
+                keep=(gsum, x, alpha, betap))
+
+
 def _grad_struct(g):
     bns = g["bn"].struct() if g.get("bn") is not None else None
     gs = GradSrc(g["kind"], g.get("g"), g.get("g_ldc", 0), g.get("dy"), g.get("x"), g.get("x_ldc", 0),
-                 ctypes.pointer(bns) if bns is not None else None, g.get("dgamma"), g.get("dbeta"))
+                 ctypes.pointer(bns) if bns is not None else None, g.get("dgamma"), g.get("dbeta"), g.get("alpha"),
+                 g.get("betap"))
     return gs, bns
 
 
@@ -279,6 +303,29 @@ def bnr_bwd_fused(desc, x, x_bn, w, g_src, dw, dgamma=None, dbeta=None, dy=None,
                                      _ptr(w), ctypes.byref(gs), _ptr(dw), _ptr(dgamma), _ptr(dbeta), _ptr(dy), dxp,
                                      dx_ldc, 1 if dx_accumulate else 0, ws, wsb, _stream()))
     del keep
+
+
+def bnr_bwd_fused_split(desc, x, x_bn, w, g_src, dw, dgamma, dbeta, gsum, alpha, betap, accumulate=False):
+    """bnr_bwd_fused for a concatenation-slice BN input: gamma*rstd*dy goes to
+    (or is added into) the view gsum and the combine writes (adds) alpha, betap."""
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    gs, keep = _grad_struct(g_src)
+    xs = x_bn.struct()
+    pg, _, _, ldg = view(gsum)
+    _check(_lib_fns["bnr_bwd_fused_split"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), ctypes.byref(gs),
+                                           _ptr(dw), _ptr(dgamma), _ptr(dbeta), pg, ldg, 1 if accumulate else 0,
+                                           _ptr(alpha), _ptr(betap), ws, wsb, _stream()))
+    del keep
+
+
+def bnr_split_dx(gsum, x, bn, alpha, betap, dx, dx_accumulate=False):
+    """dx = gsum + alpha + betap * (x - mean) * rstd (views [.., c])."""
+    pg, m, c, ldg = view(gsum)
+    px, _, _, ldx = view(x)
+    pd, _, _, ldd = view(dx)
+    bs = bn.struct()
+    _check(_lib_fns["bnr_split_dx"](m, c, dtype_code(x), pg, ldg, px, ldx, ctypes.byref(bs), _ptr(alpha), _ptr(betap),
+                                    pd, ldd, 1 if dx_accumulate else 0, _stream()))
 
 
 def bnr_bn_dx(dy, x, bn, dgamma, dbeta, dx, dx_accumulate=False):

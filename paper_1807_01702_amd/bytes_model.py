@@ -20,6 +20,14 @@ mini-batch (Sec. 3.2, Fig. 5).  Per BN of C channels with S = m*C*bytes:
                      dy and x (deferred input gradient in their prologues)
                                                                 -> 7 S
 i.e. the backward restructuring removes 5 sweeps per BN, as the paper states.
+
+Inter-composite-layer fusion (dense block, Sec. 3.2 last paragraph): the BN1
+statistics come from the producers' epilogues (no sweep per layer, one sweep
+of the block input), and each BN1's input gradient is added in summed form
+into the concatenation gradient inside its data-gradient epilogue (read x, read
+and write the sum: 3 S instead of writing dy and a separate read dy, x, G /
+write G pass: 5 S); a slice's producer reads the sum and x (2 S of k channels
+instead of 1).
 ``sweeps_per_bn()`` returns these counts; ``for_workload()`` sums the exact
 byte traffic of each driver's kernel sequence.
 """
@@ -56,6 +64,17 @@ def _unit_fused_bwd(a, m, ci, co, k, e, g_bytes, dx_mode):
         a += 2 * m * ci * e + m * ci * e      # read dy, x; write dx
         if dx_mode == "accumulate":
             a += m * ci * e
+
+
+def _unit_split_bwd(a, m, ci, co, k, e, g_bytes, accumulate):
+    """Backward of a concatenation-slice BN reader leaving its input gradient in
+    summed form: the epilogue reads x and writes (or reads and writes) the sum."""
+    a += g_bytes + k * k * ci * co * e        # dgrad: gradient source, weights
+    a += m * ci * e + m * ci * e              # epilogue: read x, write the sum
+    if accumulate:
+        a += m * ci * e                       # ... and read its old contents
+    a += m * ci * e + g_bytes                 # wgrad: x and the gradient source
+    a += k * k * ci * co * 4                  # dW (fp32)
 
 
 def _unit_ref_fwd(a, m, ci, co, k, e):
@@ -122,7 +141,23 @@ def dense_block(m, c0, layers, width, k, trans_out, e):
         _unit_fused_bwd(f, m, c, width, 1, e, 2 * m * width * e, "accumulate")
         _unit_ref_bwd(u, m, width, k, 3, e, m * k * e, False)
         _unit_ref_bwd(u, m, c, width, 1, e, m * width * e, True)
-    return {"fused": f.total, "unfused": u.total}
+    # with inter-composite-layer fusion
+    i = _Acc()
+    i += m * c0 * e                                              # the one statistics sweep (block input)
+    c = c0
+    for _ in range(layers):
+        _unit_fused_fwd(i, m, c, width, 1, e, False)
+        _unit_fused_fwd(i, m, width, k, 3, e, False)
+        c += k
+    _unit_fused_fwd(i, m, ct, trans_out, 1, e, False)
+    i += m * trans_out * e + m // 4 * trans_out * e              # avgpool forward
+    _unit_split_bwd(i, m, ct, trans_out, 1, e, m // 4 * trans_out * e, False)
+    for layer in reversed(range(layers)):
+        c = c0 + layer * k
+        _unit_fused_bwd(i, m, width, k, 3, e, 2 * m * k * e, None)   # summed gradient + slice on load
+        _unit_split_bwd(i, m, c, width, 1, e, 2 * m * width * e, True)
+    i += 3 * m * c0 * e                                          # block-input gradient: read sum, x; write
+    return {"fused": i.total, "fused_no_icf": f.total, "unfused": u.total}
 
 
 def resnet_stack(m, c, width, blocks, e):

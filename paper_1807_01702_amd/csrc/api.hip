@@ -216,6 +216,14 @@ bnr_status validate_grad_src(const bnr_conv_desc *d, const bnr_grad_src *g)
         TRY(check_ptr(g->g, "g_src.g"));
         TRY(check_channels(d->c_out, g->g_ldc, d->dtype, "g_src.g (pooled)"));
         if (d->h % 2 || d->w % 2) return fail(BNR_ERR_SHAPE, "average-pooling gradient needs even h, w");
+    } else if (g->kind == BNR_GRAD_SPLIT) {
+        TRY(check_ptr(g->g, "g_src.g"));
+        TRY(check_channels(d->c_out, g->g_ldc, d->dtype, "g_src.g (summed)"));
+        TRY(check_ptr(g->x, "g_src.x"));
+        TRY(check_channels(d->c_out, g->x_ldc, d->dtype, "g_src.x"));
+        TRY(check_bn(g->bn, "g_src.bn", false, false));
+        TRY(check_fptr(g->alpha, "g_src.alpha"));
+        TRY(check_fptr(g->betap, "g_src.betap"));
     } else {
         return fail(BNR_ERR_UNSUPPORTED, "unknown gradient kind %d", (int)g->kind);
     }
@@ -245,7 +253,7 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
         TRY_HIP(launch_conv1x1(rp, s), transpose ? "conv data gradient" : "conv forward");
         return BNR_OK;
     }
-    if (rp.taps == 9 && rp.pro != PRO_POOLUP && conv3x3_supported(rp.dtype, rp.K, rp.N, rp.w)) {
+    if (rp.taps == 9 && rp.pro != PRO_POOLUP && !rp.e_scale && conv3x3_supported(rp.dtype, rp.K, rp.N, rp.w)) {
         rp.wraw = w;
         rp.wtrans = transpose;
         *rows = conv3x3_partial_rows(rp.m);
@@ -395,6 +403,91 @@ bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtyp
     return ok();
 }
 
+// Steps 1-3 of the fused backward on validated arguments: data gradient with
+// the gradient-source prologue and (x_bn) the BN-backward epilogue into y
+// (dy, or with y_scale the summed-gradient term gamma*rstd*dy, y_acc: added),
+// the dbeta/dgamma combine (with split: also alpha/betap), the weight gradient.
+static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                            const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *y, int64_t y_ldc,
+                            int y_scale, int y_acc, const SplitTerms *split, void *ws, hipStream_t s)
+{
+    const ConvWs cw = conv_ws(d);
+    const ConvPtrs cp = conv_ptrs(ws, cw);
+    const int64_t m = pixels(d);
+    const int dt = dt_of(d->dtype);
+
+    // 1. data gradient
+    RowsParams rp;
+    fill_rows(rp, d, d->c_out, d->c_in);
+    if (g->kind == BNR_GRAD_DENSE) {
+        rp.pro = PRO_NONE; rp.a = g->g; rp.a_ldc = g->g_ldc;
+    } else if (g->kind == BNR_GRAD_BN) {
+        rp.pro = PRO_BNGRAD; rp.a = g->dy; rp.a_ldc = d->c_out; rp.a2 = g->x; rp.a2_ldc = g->x_ldc;
+        rp.p_gamma = g->bn->gamma; rp.p_mean = g->bn->mean; rp.p_rstd = g->bn->rstd;
+        rp.p_dgamma = g->dgamma; rp.p_dbeta = g->dbeta;
+    } else if (g->kind == BNR_GRAD_SPLIT) {
+        rp.pro = PRO_BNGRAD; rp.p_split = 1; rp.a = g->g; rp.a_ldc = g->g_ldc; rp.a2 = g->x; rp.a2_ldc = g->x_ldc;
+        rp.p_mean = g->bn->mean; rp.p_rstd = g->bn->rstd; rp.p_alpha = g->alpha; rp.p_betap = g->betap;
+    } else {
+        rp.pro = PRO_POOLUP; rp.a = g->g; rp.a_ldc = g->g_ldc;
+    }
+    if (x_bn) {
+        rp.epi = EPI_BNBWD; rp.y = y; rp.y_ldc = y_ldc; rp.part = cp.part;
+        rp.e_scale = y_scale; rp.accumulate = y_scale && y_acc ? 1 : 0;
+        rp.ex = x; rp.ex_ldc = d->in_ldc;
+        rp.e_gamma = x_bn->gamma; rp.e_beta = x_bn->beta; rp.e_mean = x_bn->mean; rp.e_rstd = x_bn->rstd;
+    } else {
+        rp.epi = EPI_STORE; rp.y = y; rp.y_ldc = y_ldc; rp.accumulate = y_acc ? 1 : 0;
+    }
+    int64_t R = 0;
+    TRY(launch_conv_any(rp, d, w, 1, cp.pack, &R, s));
+    // 2. dbeta = sum(dy), dgamma = sum(dy * xhat)
+    if (x_bn) {
+        TRY_HIP(launch_stats_finalize(cp.part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma,
+                                      cp.red, s, split),
+                "backward sums combine");
+    }
+    // 3. weight gradient, both operands recomputed on load
+    WgradParams wp;
+    memset(&wp, 0, sizeof wp);
+    wp.dtype = dt; wp.k = d->k; wp.n = d->n; wp.h = d->h; wp.w = d->w; wp.m = m;
+    wp.c_in = d->c_in; wp.c_out = d->c_out;
+    wp.x = x; wp.x_ldc = d->in_ldc;
+    if (x_bn) {
+        wp.a_mode = 1;
+        wp.a_gamma = x_bn->gamma; wp.a_beta = x_bn->beta; wp.a_mean = x_bn->mean; wp.a_rstd = x_bn->rstd;
+    }
+    if (g->kind == BNR_GRAD_DENSE) {
+        wp.gsrc = GB_DENSE; wp.g = g->g; wp.g_ldc = g->g_ldc;
+    } else if (g->kind == BNR_GRAD_BN) {
+        wp.gsrc = GB_BNGRAD; wp.g = g->dy; wp.g_ldc = d->c_out; wp.gx = g->x; wp.gx_ldc = g->x_ldc;
+        wp.g_gamma = g->bn->gamma; wp.g_mean = g->bn->mean; wp.g_rstd = g->bn->rstd;
+        wp.g_dgamma = g->dgamma; wp.g_dbeta = g->dbeta;
+    } else if (g->kind == BNR_GRAD_SPLIT) {
+        wp.gsrc = GB_BNGRAD; wp.g_split = 1; wp.g = g->g; wp.g_ldc = g->g_ldc; wp.gx = g->x; wp.gx_ldc = g->x_ldc;
+        wp.g_mean = g->bn->mean; wp.g_rstd = g->bn->rstd; wp.g_alpha = g->alpha; wp.g_betap = g->betap;
+    } else {
+        wp.gsrc = GB_POOLUP; wp.g = g->g; wp.g_ldc = g->g_ldc;
+    }
+    wp.dw = dw; wp.part = cp.wg; wp.red = cp.wgred;
+    TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
+    return BNR_OK;
+}
+
+// byte ranges a gradient source reads
+static bool grad_src_overlaps(const bnr_conv_desc *d, const bnr_grad_src *g, Range r)
+{
+    const int es = esize(d->dtype);
+    const int64_t m = pixels(d);
+    if (g->kind == BNR_GRAD_DENSE || g->kind == BNR_GRAD_SPLIT)
+        if (overlap(r, view_range(g->g, m, d->c_out, g->g_ldc, es))) return true;
+    if (g->kind == BNR_GRAD_AVGPOOL2 && overlap(r, view_range(g->g, m / 4, d->c_out, g->g_ldc, es))) return true;
+    if (g->kind == BNR_GRAD_BN && overlap(r, view_range(g->dy, m, d->c_out, d->c_out, es))) return true;
+    if ((g->kind == BNR_GRAD_BN || g->kind == BNR_GRAD_SPLIT) && overlap(r, view_range(g->x, m, d->c_out, g->x_ldc, es)))
+        return true;
+    return false;
+}
+
 bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
                          const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy, void *dx,
                          int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream)
@@ -429,65 +522,70 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     }
 
     hipStream_t s = (hipStream_t)stream;
-    const ConvPtrs cp = conv_ptrs(ws, cw);
-    void *wpack = cp.pack;
-    float *part = cp.part;
-    const int dt = dt_of(d->dtype);
-
-    // 1. data gradient with the gradient-source prologue and the BN-backward epilogue
-    RowsParams rp;
-    fill_rows(rp, d, d->c_out, d->c_in);
-    if (g->kind == BNR_GRAD_DENSE) {
-        rp.pro = PRO_NONE; rp.a = g->g; rp.a_ldc = g->g_ldc;
-    } else if (g->kind == BNR_GRAD_BN) {
-        rp.pro = PRO_BNGRAD; rp.a = g->dy; rp.a_ldc = d->c_out; rp.a2 = g->x; rp.a2_ldc = g->x_ldc;
-        rp.p_gamma = g->bn->gamma; rp.p_mean = g->bn->mean; rp.p_rstd = g->bn->rstd;
-        rp.p_dgamma = g->dgamma; rp.p_dbeta = g->dbeta;
-    } else {
-        rp.pro = PRO_POOLUP; rp.a = g->g; rp.a_ldc = g->g_ldc;
-    }
-    if (x_bn) {
-        rp.epi = EPI_BNBWD; rp.y = dy; rp.y_ldc = d->c_in; rp.part = part;
-        rp.ex = x; rp.ex_ldc = d->in_ldc;
-        rp.e_gamma = x_bn->gamma; rp.e_beta = x_bn->beta; rp.e_mean = x_bn->mean; rp.e_rstd = x_bn->rstd;
-    } else {
-        rp.epi = EPI_STORE; rp.y = dx; rp.y_ldc = dx_ldc; rp.accumulate = dx_accumulate ? 1 : 0;
-    }
-    int64_t R = 0;
-    TRY(launch_conv_any(rp, d, w, 1, wpack, &R, s));
-    // 2. dbeta = sum(dy), dgamma = sum(dy * xhat)
-    if (x_bn) {
-        TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma,
-                                      cp.red, s),
-                "backward sums combine");
-    }
-    // 3. weight gradient, both operands recomputed on load
-    WgradParams wp;
-    memset(&wp, 0, sizeof wp);
-    wp.dtype = dt; wp.k = d->k; wp.n = d->n; wp.h = d->h; wp.w = d->w; wp.m = m;
-    wp.c_in = d->c_in; wp.c_out = d->c_out;
-    wp.x = x; wp.x_ldc = d->in_ldc;
-    if (x_bn) {
-        wp.a_mode = 1;
-        wp.a_gamma = x_bn->gamma; wp.a_beta = x_bn->beta; wp.a_mean = x_bn->mean; wp.a_rstd = x_bn->rstd;
-    }
-    if (g->kind == BNR_GRAD_DENSE) {
-        wp.gsrc = GB_DENSE; wp.g = g->g; wp.g_ldc = g->g_ldc;
-    } else if (g->kind == BNR_GRAD_BN) {
-        wp.gsrc = GB_BNGRAD; wp.g = g->dy; wp.g_ldc = d->c_out; wp.gx = g->x; wp.gx_ldc = g->x_ldc;
-        wp.g_gamma = g->bn->gamma; wp.g_mean = g->bn->mean; wp.g_rstd = g->bn->rstd;
-        wp.g_dgamma = g->dgamma; wp.g_dbeta = g->dbeta;
-    } else {
-        wp.gsrc = GB_POOLUP; wp.g = g->g; wp.g_ldc = g->g_ldc;
-    }
-    wp.dw = dw; wp.part = cp.wg; wp.red = cp.wgred;
-    TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
+    if (x_bn) TRY(bwd_steps(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, d->c_in, 0, 0, nullptr, ws, s));
+    else TRY(bwd_steps(d, x, nullptr, w, g, dw, nullptr, nullptr, dx, dx_ldc, 0, dx_accumulate, nullptr, ws, s));
     // 4. optional standalone BN input gradient
     if (x_bn && dx) {
-        TRY_HIP(launch_elementwise(dt, EW_DX, m, d->c_in, dy, d->c_in, x, d->in_ldc, x_bn->gamma, nullptr, x_bn->mean,
-                                   x_bn->rstd, dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, s),
+        TRY_HIP(launch_elementwise(dt_of(d->dtype), EW_DX, m, d->c_in, dy, d->c_in, x, d->in_ldc, x_bn->gamma, nullptr,
+                                   x_bn->mean, x_bn->rstd, dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, s),
                 "BN input gradient");
     }
+    return ok();
+}
+
+bnr_status bnr_bwd_fused_split(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                               const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *gsum,
+                               int32_t gsum_ldc, int32_t accumulate, float *alpha, float *betap, void *ws,
+                               size_t ws_bytes, void *stream)
+{
+    TRY(check_desc(d));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(w, "w"));
+    TRY(validate_grad_src(d, g));
+    TRY(check_fptr(dw, "dw"));
+    TRY(check_bn(x_bn, "x_bn", true, false));
+    TRY(check_fptr(dgamma, "dgamma"));
+    TRY(check_fptr(dbeta, "dbeta"));
+    TRY(check_fptr(alpha, "alpha"));
+    TRY(check_fptr(betap, "betap"));
+    TRY(check_ptr(gsum, "gsum"));
+    TRY(check_channels(d->c_in, gsum_ldc, d->dtype, "gsum"));
+    const ConvWs cw = conv_ws(d);
+    TRY(check_ws(ws, ws_bytes, cw.total));
+    const int es = esize(d->dtype);
+    const int64_t m = pixels(d);
+    const Range rs = view_range(gsum, m, d->c_in, gsum_ldc, es);
+    if (overlap(rs, view_range(x, m, d->c_in, d->in_ldc, es))) return fail(BNR_ERR_ALIAS, "gsum overlaps x");
+    if (grad_src_overlaps(d, g, rs)) return fail(BNR_ERR_ALIAS, "gsum overlaps a view g_src reads");
+    const SplitTerms st{x_bn->gamma, x_bn->rstd, alpha, betap, accumulate ? 1 : 0};
+    TRY(bwd_steps(d, x, x_bn, w, g, dw, dgamma, dbeta, gsum, gsum_ldc, 1, accumulate ? 1 : 0, &st, ws,
+                  (hipStream_t)stream));
+    return ok();
+}
+
+bnr_status bnr_split_dx(int64_t m, int32_t c, bnr_dtype dtype, const void *gsum, int32_t gsum_ldc, const void *x,
+                        int32_t x_ldc, const bnr_bn *bn, const float *alpha, const float *betap, void *dx,
+                        int32_t dx_ldc, int32_t dx_accumulate, void *stream)
+{
+    TRY(check_dtype(dtype));
+    if (m <= 0 || m > ((int64_t)1 << 31)) return fail(BNR_ERR_SHAPE, "m = %lld out of range", (long long)m);
+    TRY(check_channels(c, gsum_ldc, dtype, "gsum"));
+    TRY(check_channels(c, x_ldc, dtype, "x"));
+    TRY(check_channels(c, dx_ldc, dtype, "dx"));
+    TRY(check_ptr(gsum, "gsum"));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(dx, "dx"));
+    TRY(check_bn(bn, "bn", false, false));
+    TRY(check_fptr(alpha, "alpha"));
+    TRY(check_fptr(betap, "betap"));
+    const int es = esize(dtype);
+    const Range rdx = view_range(dx, m, c, dx_ldc, es);
+    if (overlap(rdx, view_range(x, m, c, x_ldc, es))) return fail(BNR_ERR_ALIAS, "dx overlaps x");
+    if (overlap(rdx, view_range(gsum, m, c, gsum_ldc, es)) && !(gsum == dx && dx_ldc == gsum_ldc && !dx_accumulate))
+        return fail(BNR_ERR_ALIAS, "dx overlaps gsum");
+    TRY_HIP(launch_elementwise(dt_of(dtype), EW_SPLITDX, m, c, gsum, gsum_ldc, x, x_ldc, nullptr, nullptr, bn->mean,
+                               bn->rstd, betap, alpha, dx, dx_ldc, dx_accumulate ? 1 : 0, (hipStream_t)stream),
+            "summed BN input gradient");
     return ok();
 }
 

@@ -104,9 +104,11 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
 //   FIN_MVF   : mean = a/m, var = b/m - mean^2 (clamped at 0), rstd
 //   FIN_MEAN  : mean = a/m
 //   FIN_VAR   : var = a/m, rstd            (two-pass variance)
-//   FIN_BWD   : dbeta = a, dgamma = b
+//   FIN_BWD   : dbeta = a, dgamma = b, and the summed-gradient terms of st
+//               (SplitTerms) when st.alpha is set
 __device__ __forceinline__ void stats_write(int mode, int c, double a, double b, int64_t m, float eps, float *mean,
-                                            float *var, float *rstd, float *dbeta, float *dgamma)
+                                            float *var, float *rstd, float *dbeta, float *dgamma,
+                                            const SplitTerms &st)
 {
     const double dm = (double)m;
     if (mode == FIN_MVF) {
@@ -125,6 +127,13 @@ __device__ __forceinline__ void stats_write(int mode, int c, double a, double b,
     } else {
         dbeta[c] = (float)a;
         dgamma[c] = (float)b;
+        if (st.alpha) {
+            const double k = (double)st.gamma[c] * (double)st.rstd[c];
+            float al = (float)(-k * a / dm), bp = (float)(-k * b / dm);
+            if (st.accumulate) { al += st.alpha[c]; bp += st.betap[c]; }
+            st.alpha[c] = al;
+            st.betap[c] = bp;
+        }
     }
 }
 
@@ -134,7 +143,8 @@ __device__ __forceinline__ void stats_write(int mode, int c, double a, double b,
 // fixed order (deterministic).
 __global__ __launch_bounds__(kThreads) void k_stats_combine_one(const float *__restrict__ part, int64_t R, int C,
                                                                 int64_t m, int mode, float eps, float *mean,
-                                                                float *var, float *rstd, float *dbeta, float *dgamma)
+                                                                float *var, float *rstd, float *dbeta, float *dgamma,
+                                                                SplitTerms st)
 {
     __shared__ double red[2][32][8];
     const int tid = threadIdx.x, cl = tid & 7, g = tid >> 3;
@@ -160,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine_one(const float *__r
     if (g == 0 && c < C) {
         double sa = 0.0, sb = 0.0;
         for (int j = 0; j < 32; j++) { sa += red[0][j][cl]; sb += red[1][j][cl]; }
-        stats_write(mode, c, sa, sb, m, eps, mean, var, rstd, dbeta, dgamma);
+        stats_write(mode, c, sa, sb, m, eps, mean, var, rstd, dbeta, dgamma, st);
     }
 }
 
@@ -205,7 +215,8 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine1(const float *__rest
 __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__restrict__ lvl1, int RS, int C, int64_t m,
                                                              int mode, float eps, float *__restrict__ mean,
                                                              float *__restrict__ var, float *__restrict__ rstd,
-                                                             float *__restrict__ dbeta, float *__restrict__ dgamma)
+                                                             float *__restrict__ dbeta, float *__restrict__ dgamma,
+                                                             SplitTerms st)
 {
     const int c = blockIdx.x * kThreads + threadIdx.x;
     if (c >= C) return;
@@ -214,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__res
         a += lvl1[((int64_t)j * 2) * C + c];
         b += lvl1[((int64_t)j * 2 + 1) * C + c];
     }
-    stats_write(mode, c, a, b, m, eps, mean, var, rstd, dbeta, dgamma);
+    stats_write(mode, c, a, b, m, eps, mean, var, rstd, dbeta, dgamma, st);
 }
 
 // --------------------------------------------------------------------------
@@ -227,6 +238,8 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__res
 //   EW_RELUBWD : out = x2 > 0 ? x : 0   (x = dz, x2 = y)           (unfused ReLU bwd)
 //   EW_BNADDRELU: out = max(gamma*(x-mean)*rstd + beta + x2, 0)    (residual BN + add + ReLU)
 //   EW_ADDRELU : out = max(x + x2, 0)                              (unfused add + ReLU)
+//   EW_SPLITDX : out = x + alpha + betap*(x2-mean)*rstd  [+ out]   (summed BN input
+//                gradient; alpha is passed in dbeta's place, betap in dgamma's)
 template <typename T, int MODE, bool ACC>
 __global__ __launch_bounds__(kThreads) void k_elementwise(
     int64_t m, int C, const T *__restrict__ x, int64_t x_ldc, const T *__restrict__ x2,
@@ -235,7 +248,8 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
     const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int64_t rows_per_block)
 {
     constexpr int VEC = Elem<T>::VEC, U = 2;
-    constexpr bool TWO = MODE == EW_DX || MODE == EW_RELUBWD || MODE == EW_BNADDRELU || MODE == EW_ADDRELU;
+    constexpr bool TWO = MODE == EW_DX || MODE == EW_RELUBWD || MODE == EW_BNADDRELU || MODE == EW_ADDRELU ||
+                         MODE == EW_SPLITDX;
     const int cvec = C / VEC;
     const int vb = min(kStatsMaxVec, cvec - (int)blockIdx.y * kStatsMaxVec);
     const int ry = kThreads / vb;
@@ -261,6 +275,9 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
         } else if (MODE == EW_BNADDRELU) {
             p0[i] = gamma[c] * rstd[c];
             p1[i] = beta[c] - mean[c] * p0[i];
+        } else if (MODE == EW_SPLITDX) {
+            p0[i] = dgamma[c] * rstd[c];         // betap * rstd
+            p1[i] = dbeta[c] - p0[i] * mean[c];  // alpha - betap * rstd * mean
         }
     }
     auto row = [&](const vec16 &vx, const vec16 &v2, const vec16 &vo) __attribute__((always_inline)) {
@@ -291,6 +308,14 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
             for (int i = 0; i < VEC; i++) {
                 const float t = f[i] + g[i];
                 o[i] = t > 0.f ? t : 0.f;
+            }
+        } else if (MODE == EW_SPLITDX) {
+            // f = summed gradient, g = x
+            for (int i = 0; i < VEC; i++) o[i] = f[i] + __builtin_fmaf(p0[i], g[i], p1[i]);
+            if (ACC) {
+                float old[VEC];
+                Elem<T>::unpack(vo, old);
+                for (int i = 0; i < VEC; i++) o[i] += old[i];
             }
         } else {
             for (int i = 0; i < VEC; i++) o[i] = g[i] > 0.f ? f[i] : 0.f;
@@ -556,15 +581,21 @@ int stats_combine_splits(int64_t R)
 }
 
 hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
-                                 float *var, float *rstd, float *dbeta, float *dgamma, void *red, hipStream_t s)
+                                 float *var, float *rstd, float *dbeta, float *dgamma, void *red, hipStream_t s,
+                                 const SplitTerms *split)
 {
     if (!part || !red || (mode == FIN_MVF && (!mean || !rstd)) || (mode == FIN_MEAN && !mean) ||
         (mode == FIN_VAR && !rstd) || (mode == FIN_BWD && (!dbeta || !dgamma)))
         return hipErrorInvalidValue;
+    SplitTerms st{nullptr, nullptr, nullptr, nullptr, 0};
+    if (split && split->alpha) {
+        if (mode != FIN_BWD || !split->gamma || !split->rstd || !split->betap) return hipErrorInvalidValue;
+        st = *split;
+    }
     if (R <= kCombineOneMaxRows) {
         TraceScope tr(KC_SMALL, KID_COMBINE, s, (double)R * 2 * C * 4 + 3.0 * C * 4, 0.0);
         hipLaunchKernelGGL(k_stats_combine_one, dim3((unsigned)ceil_div(C, 8)), dim3(kThreads), 0, s, part, R, C, m,
-                           mode, eps, mean, var, rstd, dbeta, dgamma);
+                           mode, eps, mean, var, rstd, dbeta, dgamma, st);
         return hipGetLastError();
     }
     double *lvl1 = reinterpret_cast<double *>(red);
@@ -576,7 +607,7 @@ hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m,
     }
     TraceScope tr(KC_SMALL, KID_COMBINE, s, (double)RS * 2 * C * 8 + 3.0 * C * 4, 0.0);
     hipLaunchKernelGGL(k_stats_combine2, dim3((unsigned)ceil_div(C, kThreads)), dim3(kThreads), 0, s, lvl1, RS, C, m,
-                       mode, eps, mean, var, rstd, dbeta, dgamma);
+                       mode, eps, mean, var, rstd, dbeta, dgamma, st);
     return hipGetLastError();
 }
 
@@ -585,15 +616,17 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
                               int64_t out_ldc, int accumulate, hipStream_t s)
 {
-    const bool two = mode == EW_DX || mode == EW_RELUBWD || mode == EW_BNADDRELU || mode == EW_ADDRELU;
+    const bool two = mode == EW_DX || mode == EW_RELUBWD || mode == EW_BNADDRELU || mode == EW_ADDRELU ||
+                     mode == EW_SPLITDX;
     if (!x || !out || (two && !x2) || (mode == EW_DX && (!gamma || !rstd || !mean || !dgamma || !dbeta)) ||
+        (mode == EW_SPLITDX && (!rstd || !mean || !dgamma || !dbeta)) ||
         ((mode == EW_APPLY || mode == EW_BNADDRELU) && (!gamma || !beta || !mean || !rstd)))
         return hipErrorInvalidValue;
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
     const int64_t R = stats_row_blocks(m, C, dtype) * 4;
     const int64_t rpb = ceil_div(m, R);
     dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
-    const double sweeps = mode == EW_DX ? 3.0 + (accumulate ? 1.0 : 0.0) : (two ? 3.0 : 2.0);
+    const double sweeps = mode == EW_DX || mode == EW_SPLITDX ? 3.0 + (accumulate ? 1.0 : 0.0) : (two ? 3.0 : 2.0);
     TraceScope tr(KC_SWEEP, KID_ELEMENTWISE, s, sweeps * (double)m * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
     auto go = [&](auto kern, auto tag) {
         using T = decltype(tag);
@@ -604,6 +637,9 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
         if (mode == EW_DX) {
             if (accumulate) go(k_elementwise<bf16_t, EW_DX, true>, bf16_t());
             else go(k_elementwise<bf16_t, EW_DX, false>, bf16_t());
+        } else if (mode == EW_SPLITDX) {
+            if (accumulate) go(k_elementwise<bf16_t, EW_SPLITDX, true>, bf16_t());
+            else go(k_elementwise<bf16_t, EW_SPLITDX, false>, bf16_t());
         } else if (mode == EW_APPLY) go(k_elementwise<bf16_t, EW_APPLY, false>, bf16_t());
         else if (mode == EW_RELU) go(k_elementwise<bf16_t, EW_RELU, false>, bf16_t());
         else if (mode == EW_BNADDRELU) go(k_elementwise<bf16_t, EW_BNADDRELU, false>, bf16_t());
@@ -613,6 +649,9 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
         if (mode == EW_DX) {
             if (accumulate) go(k_elementwise<float, EW_DX, true>, float());
             else go(k_elementwise<float, EW_DX, false>, float());
+        } else if (mode == EW_SPLITDX) {
+            if (accumulate) go(k_elementwise<float, EW_SPLITDX, true>, float());
+            else go(k_elementwise<float, EW_SPLITDX, false>, float());
         } else if (mode == EW_APPLY) go(k_elementwise<float, EW_APPLY, false>, float());
         else if (mode == EW_RELU) go(k_elementwise<float, EW_RELU, false>, float());
         else if (mode == EW_BNADDRELU) go(k_elementwise<float, EW_BNADDRELU, false>, float());

@@ -77,6 +77,31 @@ __device__ __forceinline__ vec16 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return v;
 }
 
+// Deferred input gradient of a BN-fed tensor, formed on load as
+//   d = A dy + B x + C  per channel (dy the loaded gradient, x the BN input).
+// One BN (split = 0):  d = gamma rstd (dy - dbeta/m - xhat dgamma/m), i.e.
+//   A = gamma rstd, B = -A rstd dgamma/m, C = A (rstd dgamma/m mean - dbeta/m).
+// Several BNs reading the same channels with the same statistics (the
+// consumers of a concatenated feature map, split = 1): the gradient buffer
+// holds D = sum_l gamma_l rstd dy_l and the per-channel sums
+// alpha = -sum_l gamma_l rstd dbeta_l/m, betap = -sum_l gamma_l rstd dgamma_l/m,
+// so d = D + alpha + betap xhat: A = 1, B = betap rstd, C = alpha - B mean.
+__device__ __forceinline__ void deferred_coef(int split, int c, float inv_m, const float *gamma, const float *mean,
+                                              const float *rstd, const float *dgamma, const float *dbeta,
+                                              const float *alpha, const float *betap, float &A, float &B, float &C)
+{
+    if (split) {
+        A = 1.f;
+        B = betap[c] * rstd[c];
+        C = alpha[c] - B * mean[c];
+    } else {
+        const float k = gamma[c] * rstd[c], b = dgamma[c] * inv_m * rstd[c];
+        A = k;
+        B = -k * b;
+        C = k * (b * mean[c] - dbeta[c] * inv_m);
+    }
+}
+
 // Eight consecutive floats from a 32-byte aligned LDS address (two 16-byte reads).
 __device__ __forceinline__ void lds_f8(const float *p, float *f) {
     const float4 a = reinterpret_cast<const float4 *>(p)[0], b = reinterpret_cast<const float4 *>(p)[1];

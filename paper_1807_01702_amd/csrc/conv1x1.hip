@@ -42,7 +42,7 @@ static P1Geom p1_geom(int K, int N)
     const size_t a = (size_t)kP1BM * g.lda, c = (size_t)kP1BM * g.ldc;
     const size_t red = (size_t)2 * (kP1Threads / (g.NP / 8)) * g.NP * sizeof(float) / 2;
     g.region = a > c ? (a > red ? a : red) : (c > red ? c : red);
-    g.lds = ((size_t)g.NP * g.ldw + g.region) * 2 + (size_t)(5 * g.KP + 4 * g.NP) * sizeof(float);
+    g.lds = ((size_t)g.NP * g.ldw + g.region) * 2 + (size_t)(3 * g.KP + 4 * g.NP) * sizeof(float);
     return g;
 }
 
@@ -60,14 +60,15 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     constexpr int RPT0 = BM * (32 * CBW / VEC) / kP1Threads;
     constexpr int RPT = RPT0 > 0 ? RPT0 : 1;                     // epilogue rows per thread
     constexpr int RB = BM / 64;                                  // 16-row MFMA blocks per wave
-    constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD;
-    constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1;
+    constexpr bool BNBWD = EK == EK_BNBWD || EK == EK_BNBWD_SC || EK == EK_BNBWD_SCACC;
+    constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || BNBWD;
+    constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1, NVD = EK == EK_BNBWD_SCACC ? RPT : 1;
     extern __shared__ __align__(16) unsigned char smem[];
     T *Ws = reinterpret_cast<T *>(smem);
     T *As = Ws + (size_t)g.NP * g.ldw;
     T *Cs = As;                                           // output staging reuses the A tile
     float *coef = reinterpret_cast<float *>(As + g.region);
-    float *epi = coef + 5 * g.KP;
+    float *epi = coef + 3 * g.KP;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;              // 4 x 2 waves: 16 RB rows x NP/2 columns each
@@ -103,21 +104,20 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     }
     // ---- per-channel prologue / epilogue parameters ----
     //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
-    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient, expanded)
+    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef)
     for (int c = tid; c < KP; c += kP1Threads) {
         float c0 = 0.f, c1 = 0.f, c2 = 0.f;
         if (c < K && p.pro == PRO_BNRELU) {
             c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
         } else if (c < K && p.pro == PRO_BNGRAD) {
-            const float inv_m = 1.0f / (float)m;
-            const float k = p.p_gamma[c] * p.p_rstd[c], b = p.p_dgamma[c] * inv_m * p.p_rstd[c];
-            c0 = k; c1 = -k * b; c2 = k * (b * p.p_mean[c] - p.p_dbeta[c] * inv_m);
+            deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
+                          p.p_alpha, p.p_betap, c0, c1, c2);
         }
         coef[c] = c0; coef[KP + c] = c1; coef[2 * KP + c] = c2;
     }
     for (int c = tid; c < NP; c += kP1Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
-        if (c < N && EK == EK_BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
+        if (c < N && BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
         epi[c] = e0; epi[NP + c] = e1; epi[2 * NP + c] = e2; epi[3 * NP + c] = e3;
     }
 
@@ -203,7 +203,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     const int v = tid % VPRO, r0 = tid / VPRO;
     const int n = v * VEC;
     const bool col_ok = n < N;
-    vec16 rx[NVX];
+    vec16 rx[NVX], rd[NVD];
     float s1[VEC], s2[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
@@ -217,6 +217,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
             const bool ok = col_ok && r < BM && pp < m;
             if (EK == EK_STORE_ACC) rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
             else rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
+            if (EK == EK_BNBWD_SCACC) rd[j < NVD ? j : 0] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
         }
     };
 
@@ -298,17 +299,20 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) f[e] = yv[e] > 0.f ? f[e] : 0.f;
                 vo[j] = Elem<T>::pack(f);
-            } else if (EK == EK_BNBWD) {
-                float x[VEC];
+            } else if (BNBWD) {
+                float x[VEC], old[VEC];
                 Elem<T>::unpack(rx[j < NVX ? j : 0], x);
+                if (EK == EK_BNBWD_SCACC) Elem<T>::unpack(rd[j < NVD ? j : 0], old);
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) {
                     const float xh = (x[e] - eM[e]) * eR[e];
                     const float yv = eG[e] * xh + eB[e];
                     const float d = ok && yv > 0.f ? f[e] : 0.f;
-                    f[e] = d;
                     s1[e] += d;
                     s2[e] += d * xh;
+                    if (EK == EK_BNBWD) f[e] = d;
+                    else if (EK == EK_BNBWD_SC) f[e] = d * (eG[e] * eR[e]);
+                    else f[e] = __builtin_fmaf(d, eG[e] * eR[e], old[e]);
                 }
                 vo[j] = Elem<T>::pack(f);
             }
@@ -322,7 +326,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     }
 
     // ---- per-workgroup statistics partial row ----
-    if (EK == EK_STATS || EK == EK_BNBWD) {
+    if (EK == EK_STATS || BNBWD) {
         float *red = reinterpret_cast<float *>(As);
         #pragma unroll
         for (int e = 0; e < VEC; e++) {
@@ -386,7 +390,8 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
     if (BNG) a *= 2.0;
     if (p.pro == PRO_POOLUP) a /= 4.0;
     double out = m * p.N;
-    if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD) out += m * p.N;
+    if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD || EK == EK_BNBWD_SC) out += m * p.N;
+    if (EK == EK_BNBWD_SCACC) out += 2.0 * m * p.N;
     TraceScope tr(KC_CONV, KID_CONV_1X1, s, 2.0 * (a + out + (double)p.K * p.N), 2.0 * m * p.K * p.N);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kP1Threads), g.lds, s, p, g, ntiles);
     return hipGetLastError();
@@ -398,7 +403,7 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
 template <int CBW, int NVA128, int EK, bool BNG>
 static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s)
 {
-    constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD;
+    constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK >= EK_BNBWD;
     constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && BNG);
     if constexpr (small) return run_p1<CBW, 4, EK, BNG, 64>(p, g, s);
     else return run_p1<CBW, NVA128, EK, BNG, 128>(p, g, s);
@@ -431,6 +436,8 @@ static hipError_t run_p1_ek(const RowsParams &p, const P1Geom &g, int ek, hipStr
     case EK_STORE_ACC: return run_p1_nva<EK_STORE_ACC, BNG>(p, g, s);
     case EK_STATS: return run_p1_nva<EK_STATS, BNG>(p, g, s);
     case EK_RELUMASK: return run_p1_nva<EK_RELUMASK, BNG>(p, g, s);
+    case EK_BNBWD_SC: return run_p1_nva<EK_BNBWD_SC, BNG>(p, g, s);
+    case EK_BNBWD_SCACC: return run_p1_nva<EK_BNBWD_SCACC, BNG>(p, g, s);
     default: return run_p1_nva<EK_BNBWD, BNG>(p, g, s);
     }
 }
@@ -439,7 +446,8 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s)
 {
     if (!p.a || !p.wraw || !p.y || p.taps != 1 || !conv1x1_supported(p.dtype, p.K, p.N)) return hipErrorInvalidValue;
     if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return hipErrorInvalidValue;
-    if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd || !p.p_gamma || !p.p_dbeta || !p.p_dgamma))
+    if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd ||
+                                (p.p_split ? (!p.p_alpha || !p.p_betap) : (!p.p_gamma || !p.p_dbeta || !p.p_dgamma))))
         return hipErrorInvalidValue;
     if ((p.epi == EPI_STATS || p.epi == EPI_BNBWD) && !p.part) return hipErrorInvalidValue;
     if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return hipErrorInvalidValue;
@@ -451,7 +459,7 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s)
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
     const P1Geom g = p1_geom(p.K, p.N);
-    const int ek = epilogue_kind(p.epi, p.accumulate);
+    const int ek = epilogue_kind(p.epi, p.accumulate, p.e_scale);
     if (p.pro == PRO_BNGRAD) return run_p1_ek<true>(p, g, ek, s);
     return run_p1_ek<false>(p, g, ek, s);
 }

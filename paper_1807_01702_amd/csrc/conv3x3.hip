@@ -43,7 +43,7 @@ constexpr int kP3MaxW = 62;         // widest image row (ring = 128 + 2 (W + 1) 
 // zero row; lda bf16 per row]
 // [stage: weights Ws[9][NP][ldw] bf16 at the start; afterwards the float32
 // K-slice partial tiles red[WK][128][ldr] and finally the statistics scratch]
-// [coefficients: 5 KP + 4 NP floats].
+// [coefficients: 3 KP + 4 NP floats].
 struct P3Geom {
     int KP, NP, lda, ldw, ldr, ring;
     size_t ring_bytes, stage_bytes, lds;
@@ -64,7 +64,7 @@ static P3Geom p3_geom(int K, int N, int W)
     const size_t stats = (size_t)2 * (kP3Threads / (g.NP / 8)) * g.NP * 4;
     g.stage_bytes = wst > red ? wst : red;
     if (stats > g.stage_bytes) g.stage_bytes = stats;
-    g.lds = g.ring_bytes + g.stage_bytes + (size_t)(5 * g.KP + 4 * g.NP) * 4;
+    g.lds = g.ring_bytes + g.stage_bytes + (size_t)(3 * g.KP + 4 * g.NP) * 4;
     return g;
 }
 
@@ -95,7 +95,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     T *Ws = reinterpret_cast<T *>(stage);                        // [9][NP][ldw] (start only)
     float *red = reinterpret_cast<float *>(stage);               // [WK][BM][ldr]
     float *coef = reinterpret_cast<float *>(stage + g.stage_bytes);
-    float *epi = coef + 5 * KPC;
+    float *epi = coef + 3 * KPC;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave % WR, wk = (wave / WR) % WK, wn = wave / (WR * WK);
@@ -137,17 +137,16 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         *reinterpret_cast<vec16 *>(ring + (size_t)ZROW * lda + i * VEC) = zero16();
     // ---- per-channel prologue / epilogue parameters ----
     //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
-    //   BNGRAD: d = c2 * (dy - c3 - (x - c0) * c1 * c4)
+    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef)
     for (int c = tid; c < KPC; c += kP3Threads) {
-        float c0 = 0.f, c1 = 0.f, c2 = 0.f, c3 = 0.f, c4 = 0.f;
+        float c0 = 0.f, c1 = 0.f, c2 = 0.f;
         if (c < K && p.pro == PRO_BNRELU) {
             c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
         } else if (c < K && p.pro == PRO_BNGRAD) {
-            const float inv_m = 1.0f / (float)m;
-            c0 = p.p_mean[c]; c1 = p.p_rstd[c]; c2 = p.p_gamma[c] * p.p_rstd[c];
-            c3 = p.p_dbeta[c] * inv_m; c4 = p.p_dgamma[c] * inv_m;
+            deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
+                          p.p_alpha, p.p_betap, c0, c1, c2);
         }
-        coef[c] = c0; coef[KPC + c] = c1; coef[2 * KPC + c] = c2; coef[3 * KPC + c] = c3; coef[4 * KPC + c] = c4;
+        coef[c] = c0; coef[KPC + c] = c1; coef[2 * KPC + c] = c2;
     }
     for (int c = tid; c < NPC; c += kP3Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
@@ -219,17 +218,14 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
                 } else if (BNG && p.pro == PRO_BNGRAD) {
-                    float x[VEC], c0[VEC], c1[VEC], c2[VEC], c3[VEC], c4[VEC];
+                    float x[VEC], c0[VEC], c1[VEC], c2[VEC];
                     Elem<T>::unpack(rb[j < NVB ? j : 0], x);
                     lds_f8(coef + c, c0);
                     lds_f8(coef + KPC + c, c1);
                     lds_f8(coef + 2 * KPC + c, c2);
-                    lds_f8(coef + 3 * KPC + c, c3);
-                    lds_f8(coef + 4 * KPC + c, c4);
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) {
-                        const float xh = (x[e] - c0[e]) * c1[e];
-                        const float d = c2[e] * (f[e] - c3[e] - xh * c4[e]);
+                        const float d = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
                         f[e] = valid ? d : 0.f;
                     }
                 }
@@ -507,9 +503,11 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
     if (!p.a || !p.wraw || !p.y || p.taps != 9 || p.pro == PRO_POOLUP || !conv3x3_supported(p.dtype, p.K, p.N, p.w))
         return hipErrorInvalidValue;
     if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return hipErrorInvalidValue;
-    if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd || !p.p_gamma || !p.p_dbeta || !p.p_dgamma))
+    if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd ||
+                                (p.p_split ? (!p.p_alpha || !p.p_betap) : (!p.p_gamma || !p.p_dbeta || !p.p_dgamma))))
         return hipErrorInvalidValue;
     if ((p.epi == EPI_STATS || p.epi == EPI_BNBWD) && !p.part) return hipErrorInvalidValue;
+    if (p.epi == EPI_BNBWD && p.e_scale) return hipErrorInvalidValue;     // summed-gradient form: conv_rows
     if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return hipErrorInvalidValue;
     if (p.epi == EPI_RELUMASK && !p.ex) return hipErrorInvalidValue;
     if ((int64_t)p.n * p.h * p.w != p.m || p.m < 1) return hipErrorInvalidValue;
@@ -519,7 +517,7 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
     const P3Geom g = p3_geom(p.K, p.N, p.w);
-    const int ek = epilogue_kind(p.epi, p.accumulate);
+    const int ek = epilogue_kind(p.epi, p.accumulate, 0);
     if (p.pro == PRO_BNGRAD) return run_p3_ek<true>(p, g, ek, s);
     return run_p3_ek<false>(p, g, ek, s);
 }

@@ -18,13 +18,14 @@
 // Prologues (sub-BN2 side, Sec. 3.2):
 //   PRO_RELU   : a = max(x, 0)   (ReLU-CONV fusion alone, unfused-BN modes)
 //   PRO_BNRELU : a = max(gamma*(x-mean)*rstd + beta, 0)
-//   PRO_BNGRAD : a = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m)  (deferred BN
-//                input gradient, from dy and the BN input x)
+//   PRO_BNGRAD : a = A dy + B x + C  (deferred BN input gradient from dy and
+//                the BN input x; coefficients by deferred_coef)
 //   PRO_POOLUP : a = g[n][y/2][x/2] / 4   (2x2 average-pooling gradient)
 // Epilogues (sub-BN1 side):
 //   EPI_STATS  : store y, per-channel sum(y), sum(y^2) of the stored values
 //   EPI_BNBWD  : dy = dz * [gamma*xhat+beta > 0] with xhat from the BN input,
-//                store dy, per-channel sum(dy), sum(dy*xhat)
+//                store dy (e_scale: store or add gamma*rstd*dy), per-channel
+//                sum(dy), sum(dy*xhat)
 //   EPI_RELUMASK: dy = dz * [y > 0] from a stored y (ReLU-CONV fusion alone)
 // The epilogue goes through LDS so that every global access is a 16-byte
 // vector of one pixel row.
@@ -89,13 +90,9 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
         }
     } else if (p.pro == PRO_BNGRAD) {
         const float inv_m = 1.0f / (float)m;
-        for (int c = tid; c < K; c += kThreads) {
-            coef[c] = p.p_mean[c];
-            coef[K + c] = p.p_rstd[c];
-            coef[2 * K + c] = p.p_gamma[c] * p.p_rstd[c];
-            coef[3 * K + c] = p.p_dbeta[c] * inv_m;
-            coef[4 * K + c] = p.p_dgamma[c] * inv_m;
-        }
+        for (int c = tid; c < K; c += kThreads)
+            deferred_coef(p.p_split, c, inv_m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta, p.p_alpha,
+                          p.p_betap, coef[c], coef[K + c], coef[2 * K + c]);
     }
 
     // geometry of this lane's output rows
@@ -140,10 +137,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     float d[VEC], x[VEC];
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), d);
                     Elem<T>::unpack(ldg16(asrc2 + pp * p.a2_ldc + c), x);
-                    for (int e = 0; e < VEC; e++) {
-                        const float xh = (x[e] - coef[c + e]) * coef[K + c + e];
-                        d[e] = coef[2 * K + c + e] * (d[e] - coef[3 * K + c + e] - xh * coef[4 * K + c + e]);
-                    }
+                    for (int e = 0; e < VEC; e++)
+                        d[e] = __builtin_fmaf(coef[c + e], d[e], __builtin_fmaf(coef[K + c + e], x[e], coef[2 * K + c + e]));
                     out = Elem<T>::pack(d);
                 } else if (p.pro == PRO_RELU) {
                     float f[VEC];
@@ -244,16 +239,18 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 for (int e = 0; e < VEC; e++) f[e] = yv[e] > 0.f ? f[e] : 0.f;
                 stg16(dst, Elem<T>::pack(f));
             } else {
-                float f[VEC], x[VEC];
+                float f[VEC], x[VEC], old[VEC];
                 Elem<T>::unpack(cv, f);
                 Elem<T>::unpack(ldg16(exs + pp * p.ex_ldc + n), x);
+                if (p.e_scale && p.accumulate) Elem<T>::unpack(ldg16(dst), old);
                 for (int e = 0; e < VEC; e++) {
                     const float xh = (x[e] - emu[e]) * ers[e];
                     const float yv = eg[e] * xh + eb[e];
                     const float d = yv > 0.f ? f[e] : 0.f;
-                    f[e] = d;
                     s1[e] += d;
                     s2[e] += d * xh;
+                    // summed-gradient form: gamma*rstd*dy, stored or added
+                    f[e] = !p.e_scale ? d : (p.accumulate ? __builtin_fmaf(d, eg[e] * ers[e], old[e]) : d * (eg[e] * ers[e]));
                 }
                 stg16(dst, Elem<T>::pack(f));
             }
@@ -347,6 +344,7 @@ static double rows_algorithmic_bytes(const RowsParams &p)
     double out = m * N;                                          // output write
     if (p.epi == EPI_STORE && p.accumulate) out += m * N;        // read-modify-write
     if (p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK) out += m * N;   // BN input / ReLU input read
+    if (p.epi == EPI_BNBWD && p.e_scale && p.accumulate) out += m * N;  // summed gradient read
     return e * (a + out + (double)p.taps * K * N);
 }
 
@@ -354,7 +352,7 @@ template <typename T, int TAPS, int BM, int BN, int WM, int WN>
 static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 {
     using Cfg = RowsCfg<T, TAPS, BM, BN>;
-    const int P = p.pro == PRO_BNRELU ? 3 : (p.pro == PRO_BNGRAD ? 5 : 0);
+    const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD ? 3 : 0;
     const size_t lds = Cfg::LDS + (size_t)P * p.K * sizeof(float);
     auto kern = k_conv_rows<T, TAPS, BM, BN, WM, WN>;
     static bool attr_set = false;
@@ -375,7 +373,8 @@ static bool rows_operands_ok(const RowsParams &p)
 {
     if (!p.a || !p.wpack || !p.y) return false;
     if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return false;
-    if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd || !p.p_gamma || !p.p_dbeta || !p.p_dgamma))
+    if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd ||
+                                (p.p_split ? (!p.p_alpha || !p.p_betap) : (!p.p_gamma || !p.p_dbeta || !p.p_dgamma))))
         return false;
     if ((p.epi == EPI_STATS || p.epi == EPI_BNBWD) && !p.part) return false;
     if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return false;

@@ -114,7 +114,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
     __shared__ __align__(16) T Zt[kWgCIT * ZSTR];
     __shared__ __align__(16) T Gt[COT * GSTR];
     __shared__ float zc[3][kWgCIT];
-    __shared__ float gc[5][COT];
+    __shared__ float gc[3][COT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave / WC, wc = wave % WC;
@@ -138,14 +138,9 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
     }
     if (tid < COT) {
         const int c = co0 + tid;
-        if (p.gsrc == GB_BNGRAD && c < C_out) {
-            const float inv_m = 1.0f / (float)m;
-            gc[0][tid] = p.g_mean[c];
-            gc[1][tid] = p.g_rstd[c];
-            gc[2][tid] = p.g_gamma[c] * p.g_rstd[c];
-            gc[3][tid] = p.g_dbeta[c] * inv_m;
-            gc[4][tid] = p.g_dgamma[c] * inv_m;
-        }
+        if (p.gsrc == GB_BNGRAD && c < C_out)
+            deferred_coef(p.g_split, c, 1.0f / (float)m, p.g_gamma, p.g_mean, p.g_rstd, p.g_dgamma, p.g_dbeta,
+                          p.g_alpha, p.g_betap, gc[0][tid], gc[1][tid], gc[2][tid]);
     }
     // zero the G guards and the columns beyond gcols once; staging never writes them
     for (int i = tid; i < COT * GSTR; i += kThreads) {
@@ -250,8 +245,8 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
                     float x[VEC];
                     Elem<T>::unpack(gx[j][h2], x);
                     for (int e = 0; e < VEC; e++) {
-                        const float xh = (x[e] - gc[0][cl + e]) * gc[1][cl + e];
-                        const float d = gc[2][cl + e] * (f[h2][e] - gc[3][cl + e] - xh * gc[4][cl + e]);
+                        const float d = __builtin_fmaf(gc[0][cl + e], f[h2][e],
+                                                       __builtin_fmaf(gc[1][cl + e], x[e], gc[2][cl + e]));
                         f[h2][e] = valid ? d : 0.f;
                     }
                 } else if (p.gsrc == GB_POOLUP) {
@@ -321,8 +316,11 @@ __device__ __forceinline__ bf16x8 tr_frag(const bf16_t *p, int pitch)
     return __builtin_bit_cast(bf16x8, v);
 }
 
+// Two workgroups per CU wherever the operand registers allow it without
+// spilling (all but the 64-channel 3x3 tiles, whose nine accumulator sets
+// need one workgroup's whole register file).
 template <int TAPS, int CIT, int COT, int WCI, int GS>
-__global__ __launch_bounds__(kThreads) void k_wgrad_tr(WgradParams p, WgTrPlan pl)
+__global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_wgrad_tr(WgradParams p, WgTrPlan pl)
 {
     using T = bf16_t;
     using M = Mfma<T>;
@@ -340,6 +338,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_tr(WgradParams p, WgTrPlan p
     extern __shared__ __align__(16) unsigned char smem[];
     T *Zs = reinterpret_cast<T *>(smem);                          // [zrows][ZP]
     T *Gs = Zs + (size_t)pl.zrows * ZP;                           // [KQ][GP]
+    float *gco = reinterpret_cast<float *>(Gs + (size_t)pl.KQ * GP);   // BNGRAD coefficients [3][COT]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wci = wave % WCI, wco = wave / WCI;
@@ -356,24 +355,24 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_tr(WgradParams p, WgTrPlan p
     const int vz = tid % VZ, vg = tid % VG;
     const int cz = ci0 + vz * VEC, cg = co0 + vg * VEC;
     const bool zc_ok = cz < C_in, gc_ok = cg < C_out;
-    float za[VEC], zb[VEC], gA[VEC], gB[VEC], gC[VEC];
+    float za[VEC], zb[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) {
-        za[e] = 1.f; zb[e] = 0.f; gA[e] = 1.f; gB[e] = 0.f; gC[e] = 0.f;
+        za[e] = 1.f; zb[e] = 0.f;
         if (p.a_mode == 1 && zc_ok) {
             za[e] = p.a_gamma[cz + e] * p.a_rstd[cz + e];
             zb[e] = p.a_beta[cz + e] - p.a_mean[cz + e] * za[e];
         }
-        if (GS == GB_BNGRAD && gc_ok) {
-            // d = k (dy - dbeta/m - (x - mean) rstd dgamma/m) = A dy + B x + C
-            const float inv_m = 1.0f / (float)m;
-            const float k = p.g_gamma[cg + e] * p.g_rstd[cg + e];
-            const float b = p.g_dgamma[cg + e] * inv_m * p.g_rstd[cg + e];
-            gA[e] = k;
-            gB[e] = -k * b;
-            gC[e] = k * (b * p.g_mean[cg + e] - p.g_dbeta[cg + e] * inv_m);
-        }
     }
+    // deferred-gradient coefficients in LDS (registers are the occupancy limit of the 3x3 variants)
+    if (GS == GB_BNGRAD && tid < COT) {
+        float A = 0.f, Bc = 0.f, Cc = 0.f;
+        if (co0 + tid < C_out)
+            deferred_coef(p.g_split, co0 + tid, 1.0f / (float)m, p.g_gamma, p.g_mean, p.g_rstd, p.g_dgamma,
+                          p.g_dbeta, p.g_alpha, p.g_betap, A, Bc, Cc);
+        gco[tid] = A; gco[COT + tid] = Bc; gco[2 * COT + tid] = Cc;
+    }
+    __syncthreads();
 
     // raw-buffer views (launcher: every span below 2^31 bytes)
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.x, (uint32_t)(((m - 1) * p.x_ldc + C_in) * 2));
@@ -460,9 +459,12 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_tr(WgradParams p, WgTrPlan p
             vec16 out = gr[j];
             if (GS == GB_BNGRAD) {
                 const bool valid = pix(img, h0, row, true) >= 0 && gc_ok;
-                float d[VEC], x[VEC];
+                float d[VEC], x[VEC], gA[VEC], gB[VEC], gC[VEC];
                 Elem<T>::unpack(gr[j], d);
                 Elem<T>::unpack(gx[j < NGX ? j : 0], x);
+                lds_f8(gco + vg * VEC, gA);
+                lds_f8(gco + COT + vg * VEC, gB);
+                lds_f8(gco + 2 * COT + vg * VEC, gC);
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) {
                     const float v = __builtin_fmaf(gA[e], d[e], __builtin_fmaf(gB[e], x[e], gC[e]));
@@ -555,7 +557,7 @@ template <int TAPS, int CIT, int COT, int WCI>
 static hipError_t run_wgrad_tr(const WgradParams &p, const WgTrPlan &pl, hipStream_t s)
 {
     const int64_t blocks = (int64_t)pl.ci_tiles * pl.co_tiles * pl.splits;
-    const size_t lds = ((size_t)pl.zrows * (CIT + 8) + (size_t)pl.KQ * (COT + 8)) * 2;
+    const size_t lds = ((size_t)pl.zrows * (CIT + 8) + (size_t)pl.KQ * (COT + 8)) * 2 + 3 * COT * sizeof(float);
     const double m = (double)p.m;
     double g = m * p.c_out;
     if (p.gsrc == GB_BNGRAD) g *= 2.0;
@@ -613,7 +615,8 @@ hipError_t launch_wgrad(const WgradParams &p, hipStream_t s)
 {
     if (!p.x || !p.g || !p.dw) return hipErrorInvalidValue;
     if (p.a_mode == 1 && (!p.a_mean || !p.a_gamma || !p.a_rstd || !p.a_beta)) return hipErrorInvalidValue;
-    if (p.gsrc == GB_BNGRAD && (!p.gx || !p.g_mean || !p.g_rstd || !p.g_gamma || !p.g_dbeta || !p.g_dgamma))
+    if (p.gsrc == GB_BNGRAD && (!p.gx || !p.g_mean || !p.g_rstd ||
+                                (p.g_split ? (!p.g_alpha || !p.g_betap) : (!p.g_gamma || !p.g_dbeta || !p.g_dgamma))))
         return hipErrorInvalidValue;
     if (p.k == 3 && p.w > kWgMaxW3) return hipErrorInvalidValue;
     if (wgrad_tr_ok(p.dtype, p.m, p.h, p.w, p.x_ldc, p.g_ldc, p.gsrc == GB_BNGRAD ? p.gx_ldc : 0, p.k)) {

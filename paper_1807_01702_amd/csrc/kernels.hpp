@@ -11,7 +11,16 @@ enum { ST_SUMSQ = 0, ST_SUM = 1, ST_SQDEV = 2, ST_DYX = 3 };
 // k_stats_finalize modes
 enum { FIN_MVF = 0, FIN_MEAN = 1, FIN_VAR = 2, FIN_BWD = 3 };
 // k_elementwise modes
-enum { EW_DX = 0, EW_APPLY = 1, EW_RELU = 2, EW_RELUBWD = 3, EW_BNADDRELU = 4, EW_ADDRELU = 5 };
+enum { EW_DX = 0, EW_APPLY = 1, EW_RELU = 2, EW_RELUBWD = 3, EW_BNADDRELU = 4, EW_ADDRELU = 5, EW_SPLITDX = 6 };
+
+// Summed-gradient terms a FIN_BWD combine also writes (or adds to) for a BN
+// whose input channels have several BN consumers with shared statistics:
+//   alpha[c] = -gamma[c] rstd[c] dbeta[c] / m,  betap[c] = -gamma[c] rstd[c] dgamma[c] / m.
+struct SplitTerms {
+    const float *gamma, *rstd;
+    float *alpha, *betap;         // NULL: none
+    int accumulate;
+};
 
 // Reduction scratch ("red") of a statistics combine: the float64 level-1
 // sums [RS][2][C] (RS <= kRedMaxRS row splits).
@@ -24,7 +33,8 @@ hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m
                                 const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
                                 float *part, int64_t R, hipStream_t s);
 hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
-                                 float *var, float *rstd, float *dbeta, float *dgamma, void *red, hipStream_t s);
+                                 float *var, float *rstd, float *dbeta, float *dgamma, void *red, hipStream_t s,
+                                 const SplitTerms *split = nullptr);
 hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void *x, int64_t x_ldc, const void *x2,
                               int64_t x2_ldc, const float *gamma, const float *beta, const float *mean,
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
@@ -48,10 +58,13 @@ enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 
 enum { EPI_STORE = 0, EPI_STATS = 1, EPI_BNBWD = 2, EPI_RELUMASK = 3 };
 // Compile-time epilogue kinds of the persistent CONV kernels (EPI_STORE splits
 // into plain store and read-add-store).
-enum { EK_STORE = 0, EK_STORE_ACC = 1, EK_STATS = 2, EK_RELUMASK = 3, EK_BNBWD = 4 };
-inline int epilogue_kind(int epi, int accumulate) {
-    return epi == EPI_STORE ? (accumulate ? EK_STORE_ACC : EK_STORE)
-                            : (epi == EPI_STATS ? EK_STATS : (epi == EPI_RELUMASK ? EK_RELUMASK : EK_BNBWD));
+// EK_BNBWD_SC / EK_BNBWD_SCACC: the BN-backward epilogue storing (adding)
+// gamma*rstd*dy instead of dy (summed-gradient form, RowsParams::e_scale).
+enum { EK_STORE = 0, EK_STORE_ACC = 1, EK_STATS = 2, EK_RELUMASK = 3, EK_BNBWD = 4, EK_BNBWD_SC = 5,
+       EK_BNBWD_SCACC = 6 };
+inline int epilogue_kind(int epi, int accumulate, int scale) {
+    if (epi == EPI_BNBWD) return scale ? (accumulate ? EK_BNBWD_SCACC : EK_BNBWD_SC) : EK_BNBWD;
+    return epi == EPI_STORE ? (accumulate ? EK_STORE_ACC : EK_STORE) : (epi == EPI_STATS ? EK_STATS : EK_RELUMASK);
 }
 
 struct RowsParams {
@@ -64,13 +77,16 @@ struct RowsParams {
     const void *a2;               // BNGRAD: the BN input x (same pixels, K channels)
     int64_t a2_ldc;
     const float *p_gamma, *p_beta, *p_mean, *p_rstd, *p_dgamma, *p_dbeta;
+    int p_split;                  // PRO_BNGRAD: 1 = summed gradient of several BNs (deferred_coef)
+    const float *p_alpha, *p_betap;
     const void *wpack;            // weights packed by launch_pack_weights (conv_rows)
     const void *wraw;             // weights in their [k][k][c_in][c_out] layout (persistent kernels)
     int wtrans;                   // 1: data-gradient operand (GEMM K = c_out, N = c_in)
     int epi;
-    void *y;                      // output view (EPI_BNBWD: dy, dense)
+    void *y;                      // output view (EPI_BNBWD: dy)
     int64_t y_ldc;
-    int accumulate;               // EPI_STORE only
+    int accumulate;               // EPI_STORE; EPI_BNBWD with e_scale: add to y's old contents
+    int e_scale;                  // EPI_BNBWD: y receives gamma*rstd*dy (the summed-gradient term)
     float *part;                  // EPI_STATS / EPI_BNBWD: [mtiles][2][N]
     const void *ex;               // EPI_BNBWD: BN input (N channels); EPI_RELUMASK: ReLU input
     int64_t ex_ldc;
@@ -110,6 +126,8 @@ struct WgradParams {
     const void *gx;               // BNGRAD: BN input x view
     int64_t gx_ldc;
     const float *g_gamma, *g_mean, *g_rstd, *g_dgamma, *g_dbeta;
+    int g_split;                  // GB_BNGRAD: 1 = summed gradient of several BNs (deferred_coef)
+    const float *g_alpha, *g_betap;
     float *dw;                    // [k][k][c_in][c_out]
     float *part;                  // workspace for split partial tiles
     void *red;                    // split-K sum scratch (sum_partials_red_bytes)

@@ -182,9 +182,21 @@ class Bottleneck:
 class DenseBlock:
     """Dense block 1 of DenseNet-121 + transition layer.  Block buffer X holds
     the block input in channels [0, c0) and composite layer l writes channels
-    [c0 + l*k, c0 + (l+1)*k).  Upstream gradient: dpool of the pooled output."""
+    [c0 + l*k, c0 + (l+1)*k).  Upstream gradient: dpool of the pooled output.
 
-    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE):
+    ``icf`` (fused only, default on): inter-composite-layer fusion (Sec. 3.2,
+    last paragraph).  Every BN reading a channel of X sees the same values,
+    so the statistics live once per channel in shared arrays: one sweep for
+    the block input, the 3x3 CONV epilogues for every new slice; no BN1 sweeps
+    its input.  Backward: the concatenation gradient G holds the summed form
+    D = sum_l gamma_l rstd dy_l (written by the transition's and added by each
+    BN1's data-gradient epilogue) plus per-channel alpha/betap; each 3x3
+    CONV's backward forms its slice's gradient on load, and one pass
+    materialises the block input's gradient at the end.  Without ICF each BN1
+    sweeps its input for statistics and its input gradient is formed by a
+    separate pass accumulating into G."""
+
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None):
         bf16 = data["bf16"]
         dev = torch.device(device)
         dt = torch.bfloat16 if bf16 else torch.float32
@@ -221,10 +233,31 @@ class DenseBlock:
             self.dz_flat = torch.empty(n * h * w * max(ct, width), dtype=dt, device=dev)
             self.dx2 = torch.empty_like(self.dy2)
         self.fused = fused
+        self.icf = fused if icf is None else bool(icf)
+        if self.icf and not fused:
+            raise ValueError("inter-composite-layer fusion needs the fused path")
+        if self.icf:
+            f32 = dict(dtype=torch.float32, device=dev)
+            self.mu, self.var, self.rstd = (torch.empty(ct, **f32) for _ in range(3))
+            self.alpha, self.betap = torch.empty(ct, **f32), torch.empty(ct, **f32)
+            shared = lambda lo, hi: dict(mean=self.mu[lo:hi], var=self.var[lo:hi], rstd=self.rstd[lo:hi])
+            self.in_stats = B.BN.stats_view(eps, **shared(0, c0))       # block input channels
+            self.slice_stats = []
+            for c_l, k, u1, u2 in self.cpl:
+                u1.bn = B.BN(u1.bn.gamma, u1.bn.beta, eps, **shared(0, c_l))
+                self.slice_stats.append(B.BN.stats_view(eps, **shared(c_l, c_l + k)))
+            self.ut.bn = B.BN(self.ut.bn.gamma, self.ut.bn.beta, eps, **shared(0, ct))
         self.images = n
 
     def forward(self):
-        if self.fused:
+        if self.icf:
+            B.bnr_bn_stats(self.X[..., :self.c0], self.in_stats)               # the one statistics sweep
+            for (c_l, k, u1, u2), st in zip(self.cpl, self.slice_stats):
+                B.bnr_bn_relu_conv_fwd(u1.desc, u1.x, u1.bn, u1.wt, u1.out, u2.bn)
+                B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out, st)   # the new slice's statistics
+            ut = self.ut
+            B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
+        elif self.fused:
             for c_l, k, u1, u2 in self.cpl:
                 B.bnr_bn_stats(u1.x, u1.bn)                                    # sub-BN1 of a concat: own sweep
                 B.bnr_bn_relu_conv_fwd(u1.desc, u1.x, u1.bn, u1.wt, u1.out, u2.bn)
@@ -242,7 +275,22 @@ class DenseBlock:
     def backward(self):
         ut = self.ut
         n, h, w = self.n, self.h, self.w
-        if self.fused:
+        if self.icf:
+            c0 = self.c0
+            B.bnr_bwd_fused_split(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(self.dpool), ut.dw, ut.g.dgamma,
+                                  ut.g.dbeta, self.G, self.alpha, self.betap)
+            for (c_l, k, u1, u2), st in zip(reversed(self.cpl), reversed(self.slice_stats)):
+                sl = slice(c_l, c_l + k)
+                B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt,
+                                B.grad_split(self.G[..., sl], self.X[..., sl], st, self.alpha[sl], self.betap[sl]),
+                                u2.dw, u2.g.dgamma, u2.g.dbeta, self.dy2)
+                B.bnr_bwd_fused_split(u1.desc, u1.x, u1.bn, u1.wt,
+                                      B.grad_bn(self.dy2, u2.x, u2.bn, u2.g.dgamma, u2.g.dbeta),
+                                      u1.dw, u1.g.dgamma, u1.g.dbeta, self.G[..., :c_l], self.alpha[:c_l],
+                                      self.betap[:c_l], accumulate=True)
+            B.bnr_split_dx(self.G[..., :c0], self.X[..., :c0], self.in_stats, self.alpha[:c0], self.betap[:c0],
+                           self.G[..., :c0])
+        elif self.fused:
             B.bnr_bwd_fused(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(self.dpool), ut.dw, ut.g.dgamma, ut.g.dbeta,
                             self.dy_t, self.G)
             for c_l, k, u1, u2 in reversed(self.cpl):

@@ -249,3 +249,92 @@ def test_bn_dx_and_avgpool(B, bf16):
     assert_close("dx twice", host(G[..., :c]), rnd(rnd(dxr) + dxr), rt)
     assert np.all(host(G[..., c:]) == 0)
     assert_close("avgpool", host(pooled), rnd(P.avgpool2_fwd(x64)), rt)
+
+
+# ------------------------------------- concatenation BNs: summed gradient ----
+@pytest.mark.parametrize("case", [
+    # bf16, k of the producer, n, h, w, c (slice), ldc of the buffer, c_out of the two readers, producer c_in
+    (False, 3, 2, 6, 7, 24, 40, (16, 40), 12),     # fp32: tiled kernels, ragged
+    (True, 3, 2, 10, 12, 32, 96, (128, 64), 128),  # bf16: persistent 1x1 readers, 3x3 producer
+    (True, 1, 1, 9, 11, 136, 160, (128, 256), 64),  # bf16: wide slice, 1x1 producer
+])
+def test_split_fusion_two_readers(B, case):
+    """A concatenation slice x read by two BN-ReLU-CONV1x1 layers that share
+    its statistics (inter-composite-layer fusion, Sec. 3.2): each reader's
+    backward leaves its BN input gradient in summed form (gsum, alpha, betap);
+    the CONV that produced x consumes the sum on load (BNR_GRAD_SPLIT), and
+    bnr_split_dx materialises it.  Oracle: the plain sum of the two readers'
+    BN input gradients."""
+    bf16, kp, n, h, w, c, ldc, cos, cp = case
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    buf_f = synth.normal(7, "buf", (n, h, w, ldc), bf16=bf16) * np.float32(1.3) + np.float32(0.2)
+    buf_f = synth.round_to_bf16(buf_f) if bf16 else buf_f
+    buf = dev(buf_f, bf16)
+    x = buf[..., :c]
+    shared = B.BN.stats_only(c, buf.device)
+    B.bnr_bn_stats(x, shared)                       # the channels' one statistics sweep
+    x64 = buf_f[..., :c].astype(np.float64)
+    G = dev(synth.normal(7, "garbage", (n, h, w, ldc), bf16=bf16), bf16)     # overwritten by the first reader
+    alpha = f32dev(synth.normal(7, "ga", (c,)))
+    betap = f32dev(synth.normal(7, "gb", (c,)))
+    dx_true = np.zeros_like(x64)
+    readers = []
+    for i, co in enumerate(cos):
+        wt = synth.conv_weight(7, "w%d" % i, 1, c, co, bf16)
+        bp = synth.bn_params(7, "bn%d" % i, c)
+        gf = synth.normal(7, "g%d" % i, (n, h, w, co), bf16=bf16)
+        bn = B.BN(f32dev(bp["gamma"]), f32dev(bp["beta"]), 1e-5, mean=shared.mean, var=shared.var, rstd=shared.rstd)
+        dw = torch.empty(wt.shape, dtype=torch.float32, device=buf.device)
+        dgamma = torch.empty(c, dtype=torch.float32, device=buf.device)
+        dbeta = torch.empty_like(dgamma)
+        g = dev(gf, bf16)
+        desc = B.desc_for(x, g, 1, n, h, w)
+        B.bnr_bwd_fused_split(desc, x, bn, dev(wt, bf16), B.grad_dense(g), dw, dgamma, dbeta, G[..., :c], alpha,
+                              betap, accumulate=i > 0)
+        yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+        dz = P.conv_dgrad(gf.astype(np.float64), wt.astype(np.float64), (h, w))
+        dyr = rnd(P.relu_bwd(dz, yr))
+        dxr, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd)
+        dx_true += dxr
+        readers.append((dw, dgamma, dbeta, P.conv_wgrad(rnd(P.relu_fwd(yr)), gf.astype(np.float64), 1), dgr, dbr,
+                        relu_ambiguous(yr, bf16)))
+    # the producer CONV of x (plain input): its backward takes the summed gradient on load
+    xin_f = synth.normal(7, "xin", (n, h, w, cp), bf16=bf16)
+    wp = synth.conv_weight(7, "wp", kp, cp, c, bf16)
+    xin = dev(xin_f, bf16)
+    dwp = torch.empty(wp.shape, dtype=torch.float32, device=buf.device)
+    dxin = torch.empty_like(xin)
+    descp = B.desc_for(xin, x, kp, n, h, w)
+    B.bnr_bwd_fused(descp, xin, None, dev(wp, bf16), B.grad_split(G[..., :c], x, shared, alpha, betap), dwp,
+                    dx=dxin)
+    torch.cuda.synchronize()
+    rest = host(G[..., c:])
+    B.bnr_split_dx(G[..., :c], x, shared, alpha, betap, G[..., :c])
+    torch.cuda.synchronize()
+    rt = RTOL[bf16]
+    amb = np.zeros(x64.shape, bool)
+    for dw, dgamma, dbeta, dwr, dgr, dbr, a in readers:
+        assert_close("reader dW", host(dw), dwr, rt)
+        assert_close("reader dgamma", host(dgamma), dgr, rt)
+        assert_close("reader dbeta", host(dbeta), dbr, rt)
+        amb |= a
+    assert_close("summed dx", host(G[..., :c]), dx_true, rt, exclude=amb)
+    np.testing.assert_array_equal(host(G[..., c:]), rest)          # channels beyond the slice untouched
+    g_true = rnd(dx_true)
+    amb_px = np.broadcast_to(np.any(amb, axis=-1, keepdims=True), x64.shape)
+    assert np.mean(amb_px) <= 3e-2
+    dz_p = P.conv_dgrad(g_true, wp.astype(np.float64), (h, w))
+    # a flipped reader decision changes g at that pixel only; the producer's
+    # outputs are compared where no such pixel is within reach of the filter
+    reach = amb_px[..., :1]
+    if kp == 3:
+        pad = np.pad(reach, ((0, 0), (1, 1), (1, 1), (0, 0)))
+        reach = np.zeros_like(reach)
+        for dy_ in range(3):
+            for dx_ in range(3):
+                reach |= pad[:, dy_:dy_ + h, dx_:dx_ + w]
+    if not np.any(amb_px):
+        assert_close("producer dW (summed gradient on load)", host(dwp), P.conv_wgrad(xin_f.astype(np.float64),
+                                                                                      g_true, kp), rt)
+    assert_close("producer dx", host(dxin), dz_p, rt, exclude=np.broadcast_to(reach, dz_p.shape),
+                 max_excluded_frac=0.3)
