@@ -249,8 +249,7 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
     if (rp.taps == 1 && conv1x1_supported(rp.dtype, rp.K, rp.N)) {
         rp.wraw = w;
         rp.wtrans = transpose;
-        *rows = conv1x1_partial_rows(rp.m);
-        TRY_HIP(launch_conv1x1(rp, s), transpose ? "conv data gradient" : "conv forward");
+        TRY_HIP(launch_conv1x1(rp, s, rows), transpose ? "conv data gradient" : "conv forward");
         return BNR_OK;
     }
     if (rp.taps == 9 && rp.pro != PRO_POOLUP && !rp.e_scale && conv3x3_supported(rp.dtype, rp.K, rp.N, rp.w)) {

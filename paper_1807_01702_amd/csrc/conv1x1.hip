@@ -86,20 +86,41 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * 2) : 0u);
 
-    // ---- weights -> LDS as Ws[n][k] (zero outside K x N) ----
-    if (!p.wtrans) {      // forward: W[k][n] (k = c_in, n = c_out); read rows of n, scatter to columns
-        for (int i = tid; i < KP * (NP / VEC); i += kP1Threads) {
-            const int k = i / (NP / VEC), n0 = (i % (NP / VEC)) * VEC;
-            const vec16 v = (k < K && n0 < N) ? ldg16(wsrc + (int64_t)k * N + n0) : zero16();
-            const T *h = reinterpret_cast<const T *>(&v);
+    // ---- weights -> LDS as Ws[n][k] (zero outside K x N), in batches of
+    // kWB vectors per thread whose loads are all in flight before any write ----
+    {
+        constexpr int kWB = 8;
+        const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(K * N * 2));
+        const int total = KP * NP / VEC;
+        for (int base = 0; base < total; base += kWB * kP1Threads) {
+            vec16 v[kWB];
             #pragma unroll
-            for (int e = 0; e < VEC; e++) Ws[(n0 + e) * g.ldw + k] = h[e];
-        }
-    } else {              // data gradient: W[n][k] (n = c_in, k = c_out): rows copy straight
-        for (int i = tid; i < NP * (KP / VEC); i += kP1Threads) {
-            const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
-            const vec16 v = (n < N && k0 < K) ? ldg16(wsrc + (int64_t)n * K + k0) : zero16();
-            *reinterpret_cast<vec16 *>(Ws + n * g.ldw + k0) = v;
+            for (int u = 0; u < kWB; u++) {
+                const int i = base + u * kP1Threads + tid;
+                int off;
+                if (!p.wtrans) {  // forward: W[k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k
+                    const int n0 = (i / KP) * VEC, k = i % KP;
+                    off = i < total && k < K && n0 < N ? (k * N + n0) * 2 : (int)kBufOff;
+                } else {          // data gradient: W[n][k] (n = c_in, k = c_out), rows of k
+                    const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
+                    off = i < total && n < N && k0 < K ? (n * K + k0) * 2 : (int)kBufOff;
+                }
+                v[u] = bld16(wbuf, (uint32_t)off);
+            }
+            #pragma unroll
+            for (int u = 0; u < kWB; u++) {
+                const int i = base + u * kP1Threads + tid;
+                if (i >= total) break;
+                if (!p.wtrans) {  // scatter the n row to columns (a wave writes 64 consecutive k of a column)
+                    const int n0 = (i / KP) * VEC, k = i % KP;
+                    #pragma unroll
+                    for (int e = 0; e < VEC; e++)
+                        Ws[(n0 + e) * g.ldw + k] = (T)((e & 1) ? (v[u].u[e >> 1] >> 16) : (v[u].u[e >> 1] & 0xffffu));
+                } else {          // rows copy straight
+                    const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
+                    *reinterpret_cast<vec16 *>(Ws + n * g.ldw + k0) = v[u];
+                }
+            }
         }
     }
     // ---- per-channel prologue / epilogue parameters ----
@@ -137,64 +158,90 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
         sc[j] = ((q / BM) * 4 + (i & 3)) * VEC;
     }
     vec16 ra[NVA], rb[NVB];
+    // the wave-uniform mode switches sit outside the slot loops, so each
+    // mode's slots are straight-line code
     auto load_a = [&](int tile) __attribute__((always_inline)) {
         const int p0 = tile * BM;
-        #pragma unroll
-        for (int j = 0; j < NVA; j++) {
-            const int pp = p0 + sr[j], c = sc[j];
-            const bool ok = j < nva && c < K && pp < m;
-            int q = pp;
-            if (pool) {
+        if (!BNG && pool) {             // (the deferred-gradient variants never read a pooled gradient)
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int pp = p0 + sr[j], c = sc[j];
+                const bool ok = j < nva && c < K && pp < m;
                 const int img = pp / (H * W);
                 const int rem = pp - img * H * W;
                 const int y = rem / W, x = rem - y * W;
-                q = (img * (H / 2) + y / 2) * (W / 2) + x / 2;
+                const int q = (img * (H / 2) + y / 2) * (W / 2) + x / 2;
+                ra[j] = bld16(abuf, ok ? (uint32_t)(q * a_ldc + c) * 2u : kBufOff);
             }
-            ra[j] = bld16(abuf, ok ? (uint32_t)(q * a_ldc + c) * 2u : kBufOff);
-            if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(pp * a2_ldc + c) * 2u : kBufOff);
+        } else {
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int pp = p0 + sr[j], c = sc[j];
+                const bool ok = j < nva && c < K && pp < m;
+                ra[j] = bld16(abuf, ok ? (uint32_t)(pp * a_ldc + c) * 2u : kBufOff);
+                if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(pp * a2_ldc + c) * 2u : kBufOff);
+            }
         }
     };
+    // Prologue transforms.  A 1x1 output row depends on its own input row
+    // only, so rows past the end need no masking (their outputs are never
+    // stored or counted); channels past K read zeros and have zero
+    // coefficients and zero weights.
     auto store_a = [&](int tile) __attribute__((always_inline)) {
-        const int p0 = tile * BM;
-        #pragma unroll
-        for (int j = 0; j < NVA; j++) {
-            const int r = sr[j], c = sc[j];
-            if (j >= nva || c >= KP) continue;
-            const bool valid = p0 + r < m && c < K;
-            vec16 out = ra[j];
-            if (p.pro != PRO_NONE) {
+        (void)tile;
+        auto put = [&](int j, const vec16 &v) __attribute__((always_inline)) {
+            if (j < nva && sc[j] < KP) *reinterpret_cast<vec16 *>(As + sr[j] * g.lda + sc[j]) = v;
+        };
+        if (BNG) {                                        // PRO_BNGRAD: d = c0 dy + c1 x + c2
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = sc[j] < KP ? sc[j] : 0;
+                float f[VEC], x[VEC], c0[VEC], c1[VEC], c2[VEC];
+                Elem<T>::unpack(ra[j], f);
+                Elem<T>::unpack(rb[j < NVB ? j : 0], x);
+                lds_f8(coef + c, c0);
+                lds_f8(coef + KP + c, c1);
+                lds_f8(coef + 2 * KP + c, c2);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
+                put(j, Elem<T>::pack(f));
+            }
+        } else if (p.pro == PRO_BNRELU) {                 // z = max(x c0 + c1, 0)
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = sc[j] < KP ? sc[j] : 0;
+                float f[VEC], ca[VEC], cb[VEC];
+                Elem<T>::unpack(ra[j], f);
+                lds_f8(coef + c, ca);
+                lds_f8(coef + KP + c, cb);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) {
+                    const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
+                    f[e] = t > 0.f ? t : 0.f;
+                }
+                put(j, Elem<T>::pack(f));
+            }
+        } else if (p.pro == PRO_RELU) {
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
                 float f[VEC];
                 Elem<T>::unpack(ra[j], f);
-                if (p.pro == PRO_BNRELU) {
-                    float ca[VEC], cb[VEC];
-                    lds_f8(coef + c, ca);
-                    lds_f8(coef + KP + c, cb);
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) {
-                        const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
-                        f[e] = valid && t > 0.f ? t : 0.f;
-                    }
-                } else if (p.pro == PRO_RELU) {
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
-                } else if (BNG && p.pro == PRO_BNGRAD) {
-                    float x[VEC], c0[VEC], c1[VEC], c2[VEC];
-                    Elem<T>::unpack(rb[j < NVB ? j : 0], x);
-                    lds_f8(coef + c, c0);
-                    lds_f8(coef + KP + c, c1);
-                    lds_f8(coef + 2 * KP + c, c2);
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) {
-                        const float d = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
-                        f[e] = valid ? d : 0.f;
-                    }
-                } else {  // PRO_POOLUP
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) f[e] *= 0.25f;
-                }
-                out = Elem<T>::pack(f);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
+                put(j, Elem<T>::pack(f));
             }
-            *reinterpret_cast<vec16 *>(As + r * g.lda + c) = out;
+        } else if (!BNG && pool) {                        // PRO_POOLUP: g[p/2] / 4
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                float f[VEC];
+                Elem<T>::unpack(ra[j], f);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] *= 0.25f;
+                put(j, Elem<T>::pack(f));
+            }
+        } else {
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) put(j, ra[j]);
         }
     };
 
@@ -366,15 +413,17 @@ bool conv1x1_supported(int dtype, int K, int N)
     return true;
 }
 
+// Up to two workgroups per CU (when a variant's LDS and registers allow it,
+// the second hides the first's load / epilogue latency).
 int64_t conv1x1_partial_rows(int64_t m)
 {
-    const int64_t tiles = ceil_div(m, kP1BM);
-    const int64_t g = device_cus();
+    const int64_t tiles = ceil_div(m, 64);
+    const int64_t g = 2 * (int64_t)device_cus();
     return tiles < g ? tiles : g;
 }
 
 template <int CBW, int NVA, int EK, bool BNG, int BM>
-static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
+static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     auto kern = k_conv1x1<CBW, NVA, EK, BNG, BM>;
     static bool attr_set = false;
@@ -384,7 +433,13 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
         attr_set = true;
     }
     const int ntiles = (int)ceil_div(p.m, BM);
-    const int grid = (int)conv1x1_partial_rows(p.m);
+    int per_cu = 1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)kern, kP1Threads, g.lds) != hipSuccess ||
+        per_cu < 1)
+        per_cu = 1;
+    const int64_t gmax = (int64_t)device_cus() * (per_cu < 2 ? per_cu : 2);
+    const int grid = (int)(ntiles < gmax ? ntiles : gmax);
+    *rows = grid;
     const double m = (double)p.m;
     double a = m * p.K;
     if (BNG) a *= 2.0;
@@ -401,48 +456,48 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s)
 // fit the 256 VGPRs a wave has at two waves per SIMD; then 64 rows, which
 // halves every per-thread operand array.
 template <int CBW, int NVA128, int EK, bool BNG>
-static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s)
+static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK >= EK_BNBWD;
     constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && BNG);
-    if constexpr (small) return run_p1<CBW, 4, EK, BNG, 64>(p, g, s);
-    else return run_p1<CBW, NVA128, EK, BNG, 128>(p, g, s);
+    if constexpr (small) return run_p1<CBW, 4, EK, BNG, 64>(p, g, s, rows);
+    else return run_p1<CBW, NVA128, EK, BNG, 128>(p, g, s, rows);
 }
 
 template <int NVA128, int EK, bool BNG>
-static hipError_t run_p1_cbw(const RowsParams &p, const P1Geom &g, hipStream_t s)
+static hipError_t run_p1_cbw(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     switch (g.NP / 32) {
-    case 1: return run_p1_bm<1, NVA128, EK, BNG>(p, g, s);
-    case 2: return run_p1_bm<2, NVA128, EK, BNG>(p, g, s);
-    case 4: return run_p1_bm<4, NVA128, EK, BNG>(p, g, s);
-    default: return run_p1_bm<8, NVA128, EK, BNG>(p, g, s);
+    case 1: return run_p1_bm<1, NVA128, EK, BNG>(p, g, s, rows);
+    case 2: return run_p1_bm<2, NVA128, EK, BNG>(p, g, s, rows);
+    case 4: return run_p1_bm<4, NVA128, EK, BNG>(p, g, s, rows);
+    default: return run_p1_bm<8, NVA128, EK, BNG>(p, g, s, rows);
     }
 }
 
 template <int EK, bool BNG>
-static hipError_t run_p1_nva(const RowsParams &p, const P1Geom &g, hipStream_t s)
+static hipError_t run_p1_nva(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     const int nva = (int)ceil_div((int64_t)kP1BM * (g.KP / 8), kP1Threads);
-    if (nva <= 4) return run_p1_cbw<4, EK, BNG>(p, g, s);
-    return run_p1_cbw<8, EK, BNG>(p, g, s);
+    if (nva <= 4) return run_p1_cbw<4, EK, BNG>(p, g, s, rows);
+    return run_p1_cbw<8, EK, BNG>(p, g, s, rows);
 }
 
 template <bool BNG>
-static hipError_t run_p1_ek(const RowsParams &p, const P1Geom &g, int ek, hipStream_t s)
+static hipError_t run_p1_ek(const RowsParams &p, const P1Geom &g, int ek, hipStream_t s, int64_t *rows)
 {
     switch (ek) {
-    case EK_STORE: return run_p1_nva<EK_STORE, BNG>(p, g, s);
-    case EK_STORE_ACC: return run_p1_nva<EK_STORE_ACC, BNG>(p, g, s);
-    case EK_STATS: return run_p1_nva<EK_STATS, BNG>(p, g, s);
-    case EK_RELUMASK: return run_p1_nva<EK_RELUMASK, BNG>(p, g, s);
-    case EK_BNBWD_SC: return run_p1_nva<EK_BNBWD_SC, BNG>(p, g, s);
-    case EK_BNBWD_SCACC: return run_p1_nva<EK_BNBWD_SCACC, BNG>(p, g, s);
-    default: return run_p1_nva<EK_BNBWD, BNG>(p, g, s);
+    case EK_STORE: return run_p1_nva<EK_STORE, BNG>(p, g, s, rows);
+    case EK_STORE_ACC: return run_p1_nva<EK_STORE_ACC, BNG>(p, g, s, rows);
+    case EK_STATS: return run_p1_nva<EK_STATS, BNG>(p, g, s, rows);
+    case EK_RELUMASK: return run_p1_nva<EK_RELUMASK, BNG>(p, g, s, rows);
+    case EK_BNBWD_SC: return run_p1_nva<EK_BNBWD_SC, BNG>(p, g, s, rows);
+    case EK_BNBWD_SCACC: return run_p1_nva<EK_BNBWD_SCACC, BNG>(p, g, s, rows);
+    default: return run_p1_nva<EK_BNBWD, BNG>(p, g, s, rows);
     }
 }
 
-hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s)
+hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
 {
     if (!p.a || !p.wraw || !p.y || p.taps != 1 || !conv1x1_supported(p.dtype, p.K, p.N)) return hipErrorInvalidValue;
     if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return hipErrorInvalidValue;
@@ -460,8 +515,8 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s)
         return hipErrorInvalidValue;
     const P1Geom g = p1_geom(p.K, p.N);
     const int ek = epilogue_kind(p.epi, p.accumulate, p.e_scale);
-    if (p.pro == PRO_BNGRAD) return run_p1_ek<true>(p, g, ek, s);
-    return run_p1_ek<false>(p, g, ek, s);
+    if (p.pro == PRO_BNGRAD) return run_p1_ek<true>(p, g, ek, s, rows);
+    return run_p1_ek<false>(p, g, ek, s, rows);
 }
 
 }  // namespace bnr

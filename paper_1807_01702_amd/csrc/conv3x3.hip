@@ -2,25 +2,32 @@
 // data gradient, on the gfx950 matrix cores with the BN fission/fusion
 // prologues and epilogues.
 //
-// One 512-thread workgroup per CU owns a contiguous range of pixel rows
-// [P0, P1) of the NHWC tensor (pixel = row of the GEMM).
+// The GEMM rows are the positions of the zero-padded image grid,
+// P = (img (H + 2) + hp) (W + 2) + wp: a 3x3 tap is then the constant row
+// offset (dh (W + 2) + dw) for every output row, padding taps read zero rows,
+// and an A fragment is one LDS read at a wave-uniform row plus a fixed lane
+// offset (no per-lane masks or address arithmetic in the matrix-core loop).
+// Outputs at padding positions are computed and discarded (2 (H + W + 2) of
+// every (H + 2)(W + 2) positions).
+// One 512-thread workgroup per CU owns a contiguous range of positions
+// [P0, P1).
 //   * Weights: each of the 8 waves owns a 32-channel slice of the GEMM K
 //     (input channels) and a 32-column slice of the outputs, and keeps the
 //     matrix-core fragments of that slice for all nine taps in registers
 //     (72 VGPRs), loaded once through LDS from [kh][kw][ci][co] (transposed for
 //     the forward GEMM, taps flipped for the data gradient).  The remaining
 //     8 / (K slices x N slices) waves split the 128 rows of a tile.
-//   * Inputs: a ring buffer of pixel rows in LDS.  A 128-row output tile at
-//     p0 needs the rows [p0 - (W+1), p0 + 128 + W + 1); consecutive tiles share
-//     all but 128 of them, so each input row is read from HBM and transformed
-//     by the prologue once (no halo re-reads inside a workgroup).
+//   * Inputs: a ring buffer of position rows in LDS.  A 128-row output tile
+//     at p0 needs the rows [p0 - (W+3), p0 + 128 + W + 3); consecutive tiles
+//     share all but 128 of them, so each input pixel is read from HBM and
+//     transformed by the prologue once (no halo re-reads inside a workgroup);
+//     padding positions are written as zeros.
 // The 128 new rows of the next tile are loaded into registers while the
 // matrix cores work on the current tile, together with the epilogue operand
 // of the current tile.  Two waves per SIMD let one wave's prologue / epilogue
-// arithmetic overlap the other's matrix-core work.  Taps that fall outside
-// the image read a zero row of LDS: zero padding applies to the CONV input,
-// i.e. after BN and ReLU.  The float32 partial tiles of the K slices are
-// added in LDS in a fixed order.
+// arithmetic overlap the other's matrix-core work.  Zero padding applies to
+// the CONV input, i.e. after BN and ReLU.  The float32 partial tiles of the K
+// slices are added in LDS in a fixed order.
 //
 // The epilogue reads whole 16-byte channel vectors of one pixel row, so every
 // global access is coalesced, and keeps the per-channel statistics of the
@@ -36,16 +43,18 @@ namespace bnr {
 
 constexpr int kP3Threads = 512;
 constexpr int kP3BM = 128;          // output rows per tile
-constexpr int kP3MaxW = 62;         // widest image row (ring = 128 + 2 (W + 1) rows)
+constexpr int kP3MaxW = 62;         // widest image row (ring = 128 + 2 (W + 3) rows)
 
 // LDS layout (bytes): [ring: ring rows, then copies of its first 16 rows (so
-// a 16-row fragment starting anywhere in the ring is contiguous), then one
-// zero row; lda bf16 per row]
+// a 16-row fragment starting anywhere in the ring is contiguous); lda bf16
+// per row]
 // [stage: weights Ws[9][NP][ldw] bf16 at the start; afterwards the float32
 // K-slice partial tiles red[WK][128][ldr] and finally the statistics scratch]
 // [coefficients: 3 KP + 4 NP floats].
 struct P3Geom {
     int KP, NP, lda, ldw, ldr, ring;
+    int PW, PH, MP;                 // padded row length W + 2, image height H + 2, positions n PH PW
+    double inv_pw, inv_ph;
     size_t ring_bytes, stage_bytes, lds;
 };
 
@@ -57,8 +66,10 @@ static P3Geom p3_geom(int K, int N, int W)
     g.lda = g.KP + 8;
     g.ldw = g.KP + 8;
     g.ldr = g.NP + 4;
-    g.ring = kP3BM + 2 * (W + 1);
-    g.ring_bytes = (size_t)(g.ring + 16 + 1) * g.lda * 2;
+    g.ring = kP3BM + 2 * (W + 3);
+    g.ring_bytes = (size_t)(g.ring + 16) * g.lda * 2;
+    g.PW = W + 2;
+    g.PH = 0; g.MP = 0; g.inv_pw = 1.0 / g.PW; g.inv_ph = 0.0;   // set by the launcher
     const size_t wst = (size_t)9 * g.NP * g.ldw * 2;
     const size_t red = (size_t)(g.KP / 32) * kP3BM * g.ldr * 4;
     const size_t stats = (size_t)2 * (kP3Threads / (g.NP / 8)) * g.NP * 4;
@@ -66,6 +77,21 @@ static P3Geom p3_geom(int K, int N, int W)
     if (stats > g.stage_bytes) g.stage_bytes = stats;
     g.lds = g.ring_bytes + g.stage_bytes + (size_t)(3 * g.KP + 4 * g.NP) * 4;
     return g;
+}
+
+// Pixel of padded position P, or -1 for a padding position or one outside
+// [0, MP).  The float64 quotient is within one of the exact one (P < 2^30).
+__device__ __forceinline__ int p3_pixel(int P, const P3Geom &g, int H, int W)
+{
+    if (P < 0 || P >= g.MP) return -1;
+    int t = (int)((double)P * g.inv_pw);
+    int wp = P - t * g.PW;
+    if (wp < 0) { t--; wp += g.PW; } else if (wp >= g.PW) { t++; wp -= g.PW; }
+    int img = (int)((double)t * g.inv_ph);
+    int hp = t - img * g.PH;
+    if (hp < 0) { img--; hp += g.PH; } else if (hp >= g.PH) { img++; hp -= g.PH; }
+    if (wp == 0 || wp > W || hp == 0 || hp > H) return -1;
+    return (img * H + hp - 1) * W + wp - 1;
 }
 
 // WK x WN: 32-channel K slices x 32-column N slices (one per wave); the
@@ -90,7 +116,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1;
     static_assert(WR * WK * WN == 8 && RPT >= 1, "wave layout");
     extern __shared__ __align__(16) unsigned char smem[];
-    T *ring = reinterpret_cast<T *>(smem);                       // [ring + 16 + 1][lda]
+    T *ring = reinterpret_cast<T *>(smem);                       // [ring + 16][lda]
     unsigned char *stage = smem + g.ring_bytes;
     T *Ws = reinterpret_cast<T *>(stage);                        // [9][NP][ldw] (start only)
     float *red = reinterpret_cast<float *>(stage);               // [WK][BM][ldr]
@@ -100,10 +126,10 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave % WR, wk = (wave / WR) % WK, wn = wave / (WR * WK);
     const int K = p.K, N = p.N, RING = g.ring, lda = g.lda, ldr = g.ldr;
-    const int ZROW = RING + 16;                                  // the zero row
     const int m = (int)p.m;                                      // launcher: m < 2^30
-    const int H = p.h, W = p.w, H1 = W + 1;
-    const int P0 = (int)((int64_t)blockIdx.x * m / gridDim.x), P1 = (int)((int64_t)(blockIdx.x + 1) * m / gridDim.x);
+    const int H = p.h, W = p.w, PW = g.PW, H1 = PW + 1;
+    const int P0 = (int)((int64_t)blockIdx.x * g.MP / gridDim.x);
+    const int P1 = (int)((int64_t)(blockIdx.x + 1) * g.MP / gridDim.x);
     const T *wsrc = reinterpret_cast<const T *>(p.wraw);
     constexpr uint32_t ES = sizeof(T);
     // operand views as raw buffers (launcher guarantees each spans < 2^31 bytes)
@@ -114,27 +140,50 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * ES) : 0u);
 
-    // ---- weights -> LDS stage as Ws[tap][n][k] (zero outside K x N) ----
-    if (!p.wtrans) {      // forward: W[tap][k][n] (k = c_in, n = c_out); scatter columns
-        for (int i = tid; i < 9 * KPC * VPRO; i += kP3Threads) {
-            const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
-            const int k = rem / VPRO, n0 = (rem % VPRO) * VEC;
-            const vec16 v = (k < K && n0 < N) ? ldg16(wsrc + ((int64_t)tap * K + k) * N + n0) : zero16();
-            const T *h = reinterpret_cast<const T *>(&v);
-            #pragma unroll
-            for (int e = 0; e < VEC; e++) Ws[(tap * NPC + n0 + e) * g.ldw + k] = h[e];
-        }
-    } else {              // data gradient: W[8 - tap][n][k] (n = c_in, k = c_out); rows copy straight
+    // ---- weights -> LDS stage as Ws[tap][n][k] (zero outside K x N), in
+    // batches of kWB vectors per thread whose loads are all in flight before
+    // any write ----
+    {
+        constexpr int kWB = 8;
+        const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(9 * K * N * ES));
+        constexpr int total = 9 * KPC * NPC / VEC;
         constexpr int VPK = KPC / VEC;
-        for (int i = tid; i < 9 * NPC * VPK; i += kP3Threads) {
-            const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
-            const int n = rem / VPK, k0 = (rem % VPK) * VEC;
-            const vec16 v = (n < N && k0 < K) ? ldg16(wsrc + ((int64_t)(8 - tap) * N + n) * K + k0) : zero16();
-            *reinterpret_cast<vec16 *>(Ws + (tap * NPC + n) * g.ldw + k0) = v;
+        for (int base = 0; base < total; base += kWB * kP3Threads) {
+            vec16 v[kWB];
+            #pragma unroll
+            for (int u = 0; u < kWB; u++) {
+                const int i = base + u * kP3Threads + tid;
+                int off;
+                if (!p.wtrans) {  // forward: W[tap][k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k
+                    const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
+                    const int n0 = (rem / KPC) * VEC, k = rem % KPC;
+                    off = i < total && k < K && n0 < N ? ((tap * K + k) * N + n0) * (int)ES : (int)kBufOff;
+                } else {          // data gradient: W[8 - tap][n][k] (n = c_in, k = c_out), rows of k
+                    const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
+                    const int n = rem / VPK, k0 = (rem % VPK) * VEC;
+                    off = i < total && n < N && k0 < K ? (((8 - tap) * N + n) * K + k0) * (int)ES : (int)kBufOff;
+                }
+                v[u] = bld16(wbuf, (uint32_t)off);
+            }
+            #pragma unroll
+            for (int u = 0; u < kWB; u++) {
+                const int i = base + u * kP3Threads + tid;
+                if (i >= total) break;
+                if (!p.wtrans) {  // scatter the n row to columns (a wave writes 64 consecutive k of a column)
+                    const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
+                    const int n0 = (rem / KPC) * VEC, k = rem % KPC;
+                    #pragma unroll
+                    for (int e = 0; e < VEC; e++)
+                        Ws[(tap * NPC + n0 + e) * g.ldw + k] =
+                            (T)((e & 1) ? (v[u].u[e >> 1] >> 16) : (v[u].u[e >> 1] & 0xffffu));
+                } else {          // rows copy straight
+                    const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
+                    const int n = rem / VPK, k0 = (rem % VPK) * VEC;
+                    *reinterpret_cast<vec16 *>(Ws + (tap * NPC + n) * g.ldw + k0) = v[u];
+                }
+            }
         }
     }
-    for (int i = tid; i < KPC / VEC; i += kP3Threads)              // the zero row
-        *reinterpret_cast<vec16 *>(ring + (size_t)ZROW * lda + i * VEC) = zero16();
     // ---- per-channel prologue / epilogue parameters ----
     //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
     //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef)
@@ -172,156 +221,176 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         eM[e] = epi[n + e]; eR[e] = epi[NPC + n + e]; eG[e] = epi[2 * NPC + n + e]; eB[e] = epi[3 * NPC + n + e];
     }
 
-    // ---- input batches: up to 128 consecutive rows, loaded to registers ----
-    // Slot j of this thread: 4 consecutive lanes cover 4 channel vectors of
-    // one row, 16 lane groups 16 rows (4 distinct coefficient addresses per
+    // ---- input batches: up to 128 consecutive positions, loaded to registers ----
+    // This thread loads and transforms row arow of a batch, channel vectors
+    // 4 j + (tid & 3): 4 consecutive lanes cover 64 contiguous bytes of one
+    // pixel, 16 lane groups 16 rows (4 distinct coefficient addresses per
     // wave: LDS broadcast).
-    int sr[NVA], sc[NVA];
-    #pragma unroll
-    for (int j = 0; j < NVA; j++) {
-        const int i = tid + j * kP3Threads;
-        const int q = i >> 2;
-        sr[j] = q % kP3BM;
-        sc[j] = ((q / kP3BM) * 4 + (i & 3)) * VEC;
-    }
+    const int arow = tid >> 2;
+    int apix = -1;                  // pixel of this thread's row of the batch in flight
     vec16 ra[NVA], rb[NVB];
     auto load_rows = [&](int q0, int cnt) __attribute__((always_inline)) {
+        apix = arow < cnt ? p3_pixel(q0 + arow, g, H, W) : -1;
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
-            const int q = q0 + sr[j];
-            const bool ok = sc[j] < K && sr[j] < cnt && q >= 0 && q < m;
-            ra[j] = bld16(abuf, ok ? (uint32_t)(q * a_ldc + sc[j]) * ES : kBufOff);
-            if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(q * a2_ldc + sc[j]) * ES : kBufOff);
+            const int c = (4 * j + (tid & 3)) * VEC;
+            const bool ok = apix >= 0 && c < K;
+            ra[j] = bld16(abuf, ok ? (uint32_t)(apix * a_ldc + c) * ES : kBufOff);
+            if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(apix * a2_ldc + c) * ES : kBufOff);
         }
     };
-    auto store_rows = [&](int q0, int cnt, int slot0) __attribute__((always_inline)) {
-        #pragma unroll
-        for (int j = 0; j < NVA; j++) {
-            const int r = sr[j], c = sc[j];
-            if (c >= KPC || r >= cnt) continue;
-            const int q = q0 + r;
-            const bool valid = q >= 0 && q < m && c < K;
-            vec16 out = ra[j];
-            if (p.pro != PRO_NONE) {
+    // prologue transform of the batch in registers, then the ring writes; the
+    // mode switch is wave-uniform and outside the vector loop, so each mode's
+    // vectors are straight-line code
+    auto store_rows = [&](int cnt, int slot0) __attribute__((always_inline)) {
+        if (arow >= cnt) return;
+        int s = slot0 + arow;
+        if (s >= RING) s -= RING;
+        const bool vrow = apix >= 0;                      // padding rows: zeros
+        vec16 outv[NVA];
+        if (BNG) {                                        // PRO_BNGRAD: d = c0 dy + c1 x + c2
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = (4 * j + (tid & 3)) * VEC;
+                const bool valid = vrow && c < K;
+                float f[VEC], x[VEC], c0[VEC], c1[VEC], c2[VEC];
+                Elem<T>::unpack(ra[j], f);
+                Elem<T>::unpack(rb[j < NVB ? j : 0], x);
+                lds_f8(coef + c, c0);
+                lds_f8(coef + KPC + c, c1);
+                lds_f8(coef + 2 * KPC + c, c2);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) {
+                    const float d = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
+                    f[e] = valid ? d : 0.f;
+                }
+                outv[j] = Elem<T>::pack(f);
+            }
+        } else if (p.pro == PRO_BNRELU) {                 // z = max(x c0 + c1, 0)
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = (4 * j + (tid & 3)) * VEC;
+                const bool valid = vrow && c < K;
+                float f[VEC], ca[VEC], cb[VEC];
+                Elem<T>::unpack(ra[j], f);
+                lds_f8(coef + c, ca);
+                lds_f8(coef + KPC + c, cb);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) {
+                    const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
+                    f[e] = valid && t > 0.f ? t : 0.f;
+                }
+                outv[j] = Elem<T>::pack(f);
+            }
+        } else if (p.pro == PRO_RELU) {
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
                 float f[VEC];
                 Elem<T>::unpack(ra[j], f);
-                if (p.pro == PRO_BNRELU) {
-                    float ca[VEC], cb[VEC];
-                    lds_f8(coef + c, ca);
-                    lds_f8(coef + KPC + c, cb);
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) {
-                        const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
-                        f[e] = valid && t > 0.f ? t : 0.f;
-                    }
-                } else if (p.pro == PRO_RELU) {
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
-                } else if (BNG && p.pro == PRO_BNGRAD) {
-                    float x[VEC], c0[VEC], c1[VEC], c2[VEC];
-                    Elem<T>::unpack(rb[j < NVB ? j : 0], x);
-                    lds_f8(coef + c, c0);
-                    lds_f8(coef + KPC + c, c1);
-                    lds_f8(coef + 2 * KPC + c, c2);
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++) {
-                        const float d = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
-                        f[e] = valid ? d : 0.f;
-                    }
-                }
-                out = Elem<T>::pack(f);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
+                outv[j] = Elem<T>::pack(f);
             }
-            int s = slot0 + r;
-            if (s >= RING) s -= RING;
-            *reinterpret_cast<vec16 *>(ring + s * lda + c) = out;
-            if (s < 16) *reinterpret_cast<vec16 *>(ring + (s + RING) * lda + c) = out;
+        } else {
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) outv[j] = ra[j];     // out-of-range loads read zero
+        }
+        #pragma unroll
+        for (int j = 0; j < NVA; j++) {
+            const int c = (4 * j + (tid & 3)) * VEC;
+            if (c < KPC) *reinterpret_cast<vec16 *>(ring + s * lda + c) = outv[j];
+        }
+        if (s < 16) {
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = (4 * j + (tid & 3)) * VEC;
+                if (c < KPC) *reinterpret_cast<vec16 *>(ring + (s + RING) * lda + c) = outv[j];
+            }
         }
     };
 
     // ---- epilogue operand: thread = one channel vector of rows r0, r0+RSTEP, ... ----
     vec16 rx[NVX];
+    int epix[RPT];                  // pixels of this thread's epilogue rows (-1: padding / past the end)
     float s1[VEC], s2[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
     T *yout = reinterpret_cast<T *>(p.y);
     auto load_epi = [&](int p0, int nrows) __attribute__((always_inline)) {
+        #pragma unroll
+        for (int j = 0; j < RPT; j++) {
+            const int r = r0 + j * RSTEP;
+            epix[j] = col_ok && r < nrows ? p3_pixel(p0 + r, g, H, W) : -1;
+        }
         if (!READS) return;
         #pragma unroll
         for (int j = 0; j < NVX; j++) {
-            const int r = r0 + j * RSTEP;
-            const int pp = p0 + r;
-            const bool ok = col_ok && r < nrows;
+            const int pp = epix[j];
+            const bool ok = pp >= 0;
             if (EK == EK_STORE_ACC) rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * ES : kBufOff);
             else rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * ES : kBufOff);
         }
     };
 
-    // ---- ring fill: rows [P0 - H1, P0 + H1) ----
-    int L = P0 - H1;                // next input row to load; its ring slot is slotL
+    // ---- ring fill: the first tile's window, positions [P0 - H1, P0 + 128 + H1) ----
+    int L = P0 - H1;                // next position to load; its ring slot is slotL
     int slotL = 0;
-    while (L < P0 + H1) {
-        const int cnt = P0 + H1 - L < kP3BM ? P0 + H1 - L : kP3BM;
-        load_rows(L, cnt);
-        store_rows(L, cnt, slotL);
-        L += cnt;
-        slotL += cnt;
+    while (L < P0 + kP3BM + H1) {
+        const int c0n = P0 + kP3BM + H1 - L < kP3BM ? P0 + kP3BM + H1 - L : kP3BM;
+        load_rows(L, c0n);
+        store_rows(c0n, slotL);
+        L += c0n;
+        slotL += c0n;
         if (slotL >= RING) slotL -= RING;
     }
-    // prefetch the batch of the first tile
-    int cnt = P1 + H1 - L < kP3BM ? P1 + H1 - L : kP3BM;
-    load_rows(L, cnt);
+    // prefetch the batch stored while the first tile's epilogue runs, and
+    // the first tile's epilogue operand
+    int cnt = P1 + H1 - L < kP3BM ? (P1 + H1 - L > 0 ? P1 + H1 - L : 0) : kP3BM;
+    if (cnt > 0) load_rows(L, cnt);
+    load_epi(P0, P1 - P0 < kP3BM ? P1 - P0 : kP3BM);
     int sb = H1;                    // ring slot of the first row of the current tile
+    __syncthreads();
 
+    // Per tile two phases separated by barriers: (A) matrix cores on the
+    // tile's ring window, partial tiles to LDS; (B) the ring rows of the tile
+    // after next's window replace the rows only this tile needed, the
+    // epilogue of this tile runs, and the next batch and epilogue operand are
+    // loaded.
     for (int p0 = P0; p0 < P1; p0 += kP3BM) {
         const int nrows = P1 - p0 < kP3BM ? P1 - p0 : kP3BM;
-        store_rows(L, cnt, slotL);
-        L += cnt;
-        slotL += cnt;
-        if (slotL >= RING) slotL -= RING;
-        __syncthreads();
-        // epilogue operand first: the epilogue waits for it while the next
-        // tile's rows (issued after it) may still be in flight
-        load_epi(p0, nrows);
-        cnt = P1 + H1 - L < kP3BM ? P1 + H1 - L : kP3BM;
-        if (cnt > 0) load_rows(L, cnt);
 
-        // ---- matrix cores: 16 RB rows x 32 columns x 32 K per wave, nine taps ----
-        // tap validity of this lane's rows as 9-bit masks (bit 3 (dh+1) + dw+1)
-        unsigned vmask[RB];
-        #pragma unroll
-        for (int ib = 0; ib < RB; ib++) {
-            const int r = wr * 16 * RB + ib * 16 + (lane & 15);
-            const int pp = p0 + r;
-            const int x = pp % W, y = (pp / W) % H;
-            const unsigned rows = (y > 0 ? 1u : 0u) | 2u | (y < H - 1 ? 4u : 0u);
-            const unsigned cols = (x > 0 ? 1u : 0u) | 2u | (x < W - 1 ? 4u : 0u);
-            unsigned mk = 0;
-            #pragma unroll
-            for (int t = 0; t < 9; t++)
-                mk |= ((rows >> (t / 3)) & (cols >> (t % 3)) & 1u) << t;
-            vmask[ib] = r < nrows ? mk : 0u;
-        }
+        // ---- (A) matrix cores: 16 RB rows x 32 columns x 32 K per wave, nine taps ----
         f32x4 acc[RB][2];
         #pragma unroll
         for (int ib = 0; ib < RB; ib++) {
             acc[ib][0] = f32x4{0.f, 0.f, 0.f, 0.f};
             acc[ib][1] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
-        const int kofs = wk * 32 + (lane >> 4) * M::KPL;
-        // first ring row of this wave's rows (wave-uniform)
+        // A fragment = ring row u (wave-uniform) + this lane's fixed offset;
+        // the next tap's fragments are read while this tap's are multiplied
+        const int lane_off = (lane & 15) * lda + wk * 32 + (lane >> 4) * M::KPL;
         const int ubase = sb + __builtin_amdgcn_readfirstlane(wr) * 16 * RB;
-        #pragma unroll
-        for (int tap = 0; tap < 9; tap++) {
-            const int off = (tap / 3 - 1) * W + (tap % 3 - 1);
+        // (double-buffered unless the 128-column variants' registers cannot hold it)
+        constexpr int NB = WN == 4 ? 1 : 2;
+        typename M::frag af[NB][RB];
+        auto load_tap = [&](int tap, typename M::frag *dst) __attribute__((always_inline)) {
+            const int off = (tap / 3 - 1) * PW + (tap % 3 - 1);
             #pragma unroll
             for (int ib = 0; ib < RB; ib++) {
-                int u = ubase + ib * 16 + off;
+                int u = ubase + ib * 16 + off;           // in [-(PW + 1), 2 RING)
                 u = u < 0 ? u + RING : (u >= RING ? u - RING : u);
-                if (u >= RING) u -= RING;
-                const int s = ((vmask[ib] >> tap) & 1u) ? u + (lane & 15) : ZROW;
-                const typename M::frag a = M::load(ring + s * lda + kofs);
-                M::mma(acc[ib][0], a, bfr[tap][0]);
-                M::mma(acc[ib][1], a, bfr[tap][1]);
+                dst[ib] = M::load(ring + u * lda + lane_off);
+            }
+        };
+        if (NB == 2) load_tap(0, af[0]);
+        #pragma unroll
+        for (int tap = 0; tap < 9; tap++) {
+            if (NB == 1) load_tap(tap, af[0]);
+            else if (tap + 1 < 9) load_tap(tap + 1, af[(tap + 1) % NB]);
+            #pragma unroll
+            for (int ib = 0; ib < RB; ib++) {
+                M::mma(acc[ib][0], af[tap % NB][ib], bfr[tap][0]);
+                M::mma(acc[ib][1], af[tap % NB][ib], bfr[tap][1]);
             }
         }
         // ---- float32 partial tile of this K slice -> LDS ----
@@ -336,6 +405,11 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                     red[(wk * kP3BM + row) * ldr + col] = acc[ib][cb][i];
                 }
         __syncthreads();
+        // ---- (B) ring rows of the tile after next, then this tile's epilogue ----
+        store_rows(cnt, slotL);
+        L += cnt;
+        slotL += cnt;
+        if (slotL >= RING) slotL -= RING;
         // ---- epilogue row pass: sum of the K slices (fixed order), rounded to
         // the storage type; all outputs of this thread first (no branch,
         // invalid rows contribute zeros), then the stores back to back ----
@@ -344,7 +418,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             #pragma unroll
             for (int j = 0; j < RPT; j++) {
                 const int r = r0 + j * RSTEP;
-                const bool ok = col_ok && r < nrows;
+                const bool ok = epix[j] >= 0;
                 float f[VEC];
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) f[e] = 0.f;
@@ -393,11 +467,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 }
             }
             #pragma unroll
-            for (int j = 0; j < RPT; j++) {
-                const int r = r0 + j * RSTEP;
-                if (col_ok && r < nrows) stg16(yout + (int64_t)(p0 + r) * y_ldc + n, vo[j]);
-            }
+            for (int j = 0; j < RPT; j++)
+                if (epix[j] >= 0) stg16(yout + (int64_t)epix[j] * y_ldc + n, vo[j]);
         }
+        cnt = P1 + H1 - L < kP3BM ? (P1 + H1 - L > 0 ? P1 + H1 - L : 0) : kP3BM;
+        if (cnt > 0) load_rows(L, cnt);
+        if (p0 + kP3BM < P1) load_epi(p0 + kP3BM, P1 - p0 - kP3BM < kP3BM ? P1 - p0 - kP3BM : kP3BM);
         sb += kP3BM;
         if (sb >= RING) sb -= RING;
         __syncthreads();
@@ -516,7 +591,12 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
     if (p.m >= (lim >> 1) || (p.m * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
-    const P3Geom g = p3_geom(p.K, p.N, p.w);
+    P3Geom g = p3_geom(p.K, p.N, p.w);
+    g.PH = p.h + 2;
+    g.inv_ph = 1.0 / g.PH;
+    const int64_t mp = (int64_t)p.n * g.PH * g.PW;                // padded positions
+    if (mp >= (lim >> 1)) return hipErrorInvalidValue;
+    g.MP = (int)mp;
     const int ek = epilogue_kind(p.epi, p.accumulate, 0);
     if (p.pro == PRO_BNGRAD) return run_p3_ek<true>(p, g, ek, s);
     return run_p3_ek<false>(p, g, ek, s);

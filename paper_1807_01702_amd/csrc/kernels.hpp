@@ -102,8 +102,8 @@ hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s);
 
 // ---- persistent 1x1 CONV (weights resident in LDS, one workgroup per CU) ----
 bool conv1x1_supported(int dtype, int K, int N);
-int64_t conv1x1_partial_rows(int64_t m);      // statistics partial rows it writes
-hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s);
+int64_t conv1x1_partial_rows(int64_t m);      // upper bound of the statistics partial rows it writes
+hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows);   // *rows: partial rows written
 
 // ---- persistent 3x3 CONV (weights and an input-row ring buffer in LDS) ----
 bool conv3x3_supported(int dtype, int K, int N, int W);
