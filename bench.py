@@ -11,11 +11,25 @@ and unfused (the reference layer chain).
 
 Prints one JSON line (rank 0).  Options: --gpus (1 only), --steps, --warmup,
 --workload {dense_block,bottleneck,single_layer,resnet_stack}, --no-graph,
---no-cpu-baseline, --profile-only (steps only, for rocprofv3 runs).
+--no-cpu-baseline, --profile-only (steps only, for rocprofv3 runs),
+--calib-copy-mb M (with --profile-only: one bnr_hbm_copy of M MiB after the
+steps, the byte-counter calibration reference).
+
+HBM traffic of the dominant kernel (`roofline.traffic`): two rocprofv3
+counter runs of the profile-only command, one with FETCH_SIZE and one with
+WRITE_SIZE, are summarised by `python bench.py --summarize-pmc FETCH_DIR
+WRITE_DIR --calib-copy-mb M` into profiles/hbm_traffic_<workload>.json: per kernel class the
+counter bytes per launch, each scaled by expected / counted bytes of the
+calibration copy, and the SHA-256 of the sources the class is built from.
+The bench line reports that figure only while those sources are unchanged.
 """
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -40,6 +54,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true")
     ap.add_argument("--only", choices=["fused", "fused_no_icf", "unfused"], default=None)
+    ap.add_argument("--calib-copy-mb", type=int, default=0)
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None)
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("KERNEL_STATS_CSV", "STEPS"), default=None)
+    ap.add_argument("--bench-json", default=None)
     return ap.parse_args()
 
 
@@ -123,8 +141,9 @@ def traced_kernels(torch, wl, steps):
     return out
 
 
-def roofline(kernels, dtype):
+def roofline(kernels, dtype, workload):
     name = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    traffic = traffic_for(workload, name)
     k = kernels[name]
     t = k["avg_launch_us"] * 1e-6
     bytes_t = k["algorithmic_bytes_per_launch"] / (PEAK_HBM_GBS * 1e9)
@@ -132,12 +151,155 @@ def roofline(kernels, dtype):
     if flops_t > bytes_t:
         ach = k["flops_per_launch"] / t / 1e12
         return dict(bound="mfma", achieved=ach, peak=PEAK_MFMA_TFS[dtype], unit="TFLOP/s",
-                    frac=ach / PEAK_MFMA_TFS[dtype], traffic=None, kernel=name,
+                    frac=ach / PEAK_MFMA_TFS[dtype], traffic=traffic, kernel=name,
                     avg_launch_us=k["avg_launch_us"], flops_per_launch=k["flops_per_launch"])
     ach = k["algorithmic_bytes_per_launch"] / t / 1e9
-    return dict(bound="hbm", achieved=ach, peak=PEAK_HBM_GBS, unit="GB/s", frac=ach / PEAK_HBM_GBS, traffic=None,
+    return dict(bound="hbm", achieved=ach, peak=PEAK_HBM_GBS, unit="GB/s", frac=ach / PEAK_HBM_GBS, traffic=traffic,
                 kernel=name, avg_launch_us=k["avg_launch_us"],
                 algorithmic_bytes_per_launch=k["algorithmic_bytes_per_launch"])
+
+
+# ---------------------------------------------------- HBM byte counters ----
+CSRC = os.path.join(ROOT, "paper_1807_01702_amd", "csrc")
+SHARED_SOURCES = ["common.hpp", "kernels.hpp", "mfma.hpp", "tiles.hpp"]
+CLASS_SOURCES = {"conv1x1": ["conv1x1.hip", "conv_rows.hip"], "conv3x3": ["conv3x3.hip", "conv_rows.hip"],
+                 "wgrad1x1": ["conv_wgrad.hip"], "wgrad3x3": ["conv_wgrad.hip"],
+                 "stats_sweep": ["bn_kernels.hip"], "elementwise": ["bn_kernels.hip"],
+                 "stats_combine": ["bn_kernels.hip"], "splitk_sum": ["bn_kernels.hip"], "pool": ["bn_kernels.hip"],
+                 "copy": ["bn_kernels.hip"], "weight_pack": ["conv_rows.hip"]}
+
+
+def kernel_class(name):
+    """Kernel class (as in the launch trace) of a profiler kernel name."""
+    n = name.replace("void ", "")
+    m = re.search(r"bnr::(k_\w+)(<([^>]*)>)?", n)
+    if not m:
+        return None
+    k, targs = m.group(1), [t.strip() for t in (m.group(3) or "").split(",")]
+    if k == "k_conv1x1":
+        return "conv1x1"
+    if k == "k_conv3x3":
+        return "conv3x3"
+    if k == "k_conv_rows":
+        return "conv1x1" if len(targs) > 1 and targs[1] == "1" else "conv3x3"
+    if k in ("k_wgrad_tr", "k_wgrad"):
+        taps = targs[0] if k == "k_wgrad_tr" else (targs[1] if len(targs) > 1 else "")
+        return "wgrad1x1" if taps == "1" else "wgrad3x3"
+    return {"k_stats_partial": "stats_sweep", "k_elementwise": "elementwise", "k_addrelu_bwd": "elementwise",
+            "k_stats_combine_one": "stats_combine", "k_stats_combine1": "stats_combine",
+            "k_stats_combine2": "stats_combine", "k_sum_partials1": "splitk_sum", "k_sum_partials2": "splitk_sum",
+            "k_avgpool2": "pool", "k_avgpool2_bwd": "pool", "k_copy16": "copy",
+            "k_pack_weights": "weight_pack"}.get(k)
+
+
+def sources_sha(cls):
+    h = hashlib.sha256()
+    for f in CLASS_SOURCES.get(cls, []) + SHARED_SOURCES:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def _counter_rows(d, counter):
+    out = []
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    out.append((r["Kernel_Name"], float(r["Counter_Value"]) * 1024.0))   # KiB -> bytes
+    return out
+
+
+def summarize_pmc(fetch_dir, write_dir, workload, copy_mb):
+    """Per kernel class: counter bytes per launch, scaled by the calibration copy."""
+    fetch, write = _counter_rows(fetch_dir, "FETCH_SIZE"), _counter_rows(write_dir, "WRITE_SIZE")
+    expected = copy_mb * 1024.0 * 1024.0
+    fc = [v for n, v in fetch if kernel_class(n) == "copy"]
+    wc = [v for n, v in write if kernel_class(n) == "copy"]
+    if not fc or not wc:
+        raise SystemExit("no calibration copy in the counter runs (use --calib-copy-mb)")
+    f_scale, w_scale = expected / fc[-1], expected / wc[-1]
+    agg = {}
+    for rows, key in ((fetch, "fetch"), (write, "write")):
+        for n, v in rows:
+            c = kernel_class(n)
+            if c is None or c == "copy":
+                continue
+            a = agg.setdefault(c, {"fetch": [], "write": []})
+            a[key].append(v)
+    classes = {}
+    for c, a in sorted(agg.items()):
+        if not a["fetch"] or not a["write"]:
+            continue
+        fb = sum(a["fetch"]) / len(a["fetch"]) * f_scale
+        wb = sum(a["write"]) / len(a["write"]) * w_scale
+        classes[c] = {"launches": len(a["fetch"]), "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                      "bytes_per_launch": fb + wb, "sources_sha256": sources_sha(c)}
+    return {"workload": workload, "calibration": {"copy_bytes": expected, "fetch_counted": fc[-1],
+                                                  "write_counted": wc[-1], "fetch_scale": f_scale,
+                                                  "write_scale": w_scale},
+            "classes": classes}
+
+
+def traffic_for(workload, cls):
+    """Counter bytes per launch of a kernel class, if measured on the current sources."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % workload)
+    try:
+        with open(path) as fh:
+            d = json.load(fh)
+        c = d["classes"][cls]
+    except (OSError, KeyError, ValueError):
+        return None
+    return c["bytes_per_launch"] if c.get("sources_sha256") == sources_sha(cls) else None
+
+
+def _short(n):
+    n = re.sub(r"\(.*", "", n)
+    return n.replace("void ", "").replace("unsigned short", "bf16")
+
+
+def summarize_trace(stats_csv, steps, workload, bench_json=None):
+    """Markdown tables: rocprofv3 --stats per kernel, per class, and the byte
+    counters of profiles/hbm_traffic_<workload>.json against the algorithmic
+    bytes of a bench line (if given)."""
+    with open(stats_csv) as fh:
+        rows = list(csv.DictReader(fh))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    out = ["Steps in the trace: %d (warm-up included). Kernel time per step: %.3f ms." % (steps, tot / steps / 1e6),
+           "", "| kernel | launches/step | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        out.append("| `%s` | %.1f | %.1f | %.1f | %.1f | %.1f%% |" % (
+            _short(r["Name"]), int(r["Calls"]) / steps, float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+            float(r["MaxNs"]) / 1e3, 100 * float(r["TotalDurationNs"]) / tot))
+    groups = {}
+    for r in rows:
+        a = groups.setdefault(kernel_class(r["Name"]) or _short(r["Name"])[:40], [0, 0.0])
+        a[0] += int(r["Calls"])
+        a[1] += float(r["TotalDurationNs"])
+    out += ["", "By kernel class (the classes of the bench line's `kernels`):", "",
+            "| class | launches/step | avg us | ms/step |", "|---|---|---|---|"]
+    for g, (n, t) in sorted(groups.items(), key=lambda kv: -kv[1][1]):
+        out.append("| %s | %.1f | %.1f | %.3f |" % (g, n / steps, t / n / 1e3, t / steps / 1e6))
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % workload)
+    if os.path.exists(path):
+        with open(path) as fh:
+            tr = json.load(fh)
+        alg = {}
+        if bench_json:
+            with open(bench_json) as fh:
+                alg = {k: v["algorithmic_bytes_per_launch"] for k, v in json.loads(fh.read())["kernels"].items()}
+        cal = tr["calibration"]
+        out += ["", "HBM bytes per launch from the FETCH_SIZE and WRITE_SIZE counter runs, each scaled by "
+                "expected / counted bytes of a %d MiB `bnr_hbm_copy` in the same run (fetch x%.3f, write x%.3f):"
+                % (cal["copy_bytes"] / 2 ** 20, cal["fetch_scale"], cal["write_scale"]), "",
+                "| class | fetch MB | write MB | total MB | algorithmic MB | total / algorithmic |",
+                "|---|---|---|---|---|---|"]
+        for c, v in sorted(tr["classes"].items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
+            a = alg.get(c)
+            out.append("| %s | %.1f | %.1f | %.1f | %s | %s |" % (
+                c, v["fetch_bytes_per_launch"] / 1e6, v["write_bytes_per_launch"] / 1e6, v["bytes_per_launch"] / 1e6,
+                "%.1f" % (a / 1e6) if a else "-", "%.2f" % (v["bytes_per_launch"] / a) if a else "-"))
+    return "\n".join(out)
 
 
 def cpu_baseline(args):
@@ -186,6 +348,18 @@ def cpu_baseline(args):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        if args.calib_copy_mb <= 0:
+            raise SystemExit("--summarize-pmc needs the --calib-copy-mb value the counter runs used")
+        out = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload, args.calib_copy_mb)
+        path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % args.workload)
+        with open(path, "w") as fh:
+            json.dump(out, fh, indent=1, sort_keys=True)
+        print(json.dumps(out["classes"]))
+        return
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace[0], int(args.summarize_trace[1]), args.workload, args.bench_json))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
@@ -198,6 +372,14 @@ def main():
         ms, wall, _ = timed_steps(torch, wl, args.steps, args.warmup, not args.no_graph)
         res[name] = dict(ms=ms, wall=wall, images=wl.images)
     if args.profile_only:
+        if args.calib_copy_mb > 0:
+            from paper_1807_01702_amd import bnr as B
+            nb = args.calib_copy_mb * 1024 * 1024
+            src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
+            dst = torch.empty_like(src)
+            torch.cuda.synchronize()
+            B.bnr_hbm_copy(src, dst)
+            torch.cuda.synchronize()
         print(json.dumps({k: v["ms"] for k, v in res.items()}))
         return
     dtype = "bf16" if data.get("bf16") else "f32"
@@ -228,7 +410,7 @@ def main():
                           "algorithmic_bytes": model.get("fused_no_icf")} if noicf else None),
         "speedup_vs_unfused": (unf["ms"] / fused["ms"]) if (fused and unf) else None,
         "hbm_bytes_per_step": {"algorithmic_fused": model["fused"], "algorithmic_unfused": model["unfused"]},
-        "roofline": roofline(kernels, dtype) if kernels else None,
+        "roofline": roofline(kernels, dtype, args.workload) if kernels else None,
         "kernels": kernels,
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(args),
     }
