@@ -12,6 +12,8 @@ describes and nothing else:
   (one tensor read by several later layers) is a sum over its readers.
 * ``block_*`` -- dense block 1 of DenseNet-121 followed by its transition
   layer BN-ReLU-CONV1x1 + 2x2 average pooling (Sec. 2.3).
+* ``densenet_*`` -- a whole DenseNet: 7x7 stem, dense blocks joined by
+  transitions, and the classifier head (Sec. 2.2, Sec. 2.3, Sec. 3.1).
 * ``resnet_*`` -- a ResNet bottleneck block CONV1x1-BN-ReLU-CONV3x3-BN-ReLU-
   CONV1x1-BN, element-wise sum with its input, ReLU (Sec. 2.2).
 
@@ -93,10 +95,10 @@ def bottleneck_bwd(c, dY, rnd):
     return G[..., :c["c_l"]], g
 
 
-# ------------------------------------------- dense block 1 + transition ----
-def block_fwd(X0, cpls, trans, eps, rnd, c_total):
-    """X0: block input [N,H,W,C0]; cpls: list of composite-layer params;
-    trans: gamma, beta, w (1x1) of the transition.  Returns pooled output."""
+# ------------------------------------------- dense block (+ transition) ----
+def dense_layers_fwd(X0, cpls, eps, rnd, c_total):
+    """The composite layers of one dense block on a buffer holding the block
+    input X0 in channels [0, C0); returns (buffer, per-layer caches)."""
     N, H, W, C0 = X0.shape
     buf = np.zeros((N, H, W, c_total))
     buf[..., :C0] = X0
@@ -105,9 +107,24 @@ def block_fwd(X0, cpls, trans, eps, rnd, c_total):
         caches.append(cpl_fwd(buf, c_l, p, eps, rnd))
         c_l += p["w2"].shape[3]
     assert c_l == c_total
+    return buf, caches
+
+
+def dense_layers_bwd(caches, G, rnd):
+    """Backward of ``dense_layers_fwd`` on the complete gradient G of the
+    block buffer (in place); returns the per-layer parameter gradients."""
+    grads = [cpl_bwd(cc, G, rnd) for cc in reversed(caches)]
+    grads.reverse()
+    return grads
+
+
+def block_fwd(X0, cpls, trans, eps, rnd, c_total):
+    """X0: block input [N,H,W,C0]; cpls: list of composite-layer params;
+    trans: gamma, beta, w (1x1) of the transition.  Returns pooled output."""
+    buf, caches = dense_layers_fwd(X0, cpls, eps, rnd, c_total)
     ut = unit_fwd(buf, trans["gamma"], trans["beta"], trans["w"], eps, rnd)
     pooled = rnd(P.avgpool2_fwd(ut["out"]))
-    return pooled, dict(buf=buf, cpls=caches, ut=ut, C0=C0)
+    return pooled, dict(buf=buf, cpls=caches, ut=ut, C0=X0.shape[3])
 
 
 def block_bwd(c, dpool, rnd):
@@ -115,10 +132,7 @@ def block_bwd(c, dpool, rnd):
     gt = rnd(P.avgpool2_bwd(dpool, ut["x"].shape[1:3]))
     bt = unit_bwd(ut, gt, rnd)
     G = rnd(bt["dx"])
-    grads = []
-    for cc in reversed(c["cpls"]):
-        grads.append(cpl_bwd(cc, G, rnd))
-    grads.reverse()
+    grads = dense_layers_bwd(c["cpls"], G, rnd)
     return G[..., :c["C0"]], dict(trans=bt, cpls=grads, G=G)
 
 
@@ -146,3 +160,67 @@ def resnet_block_bwd(c, dr, rnd):
     dX = rnd(ds + P.conv_dgrad(g1, p["w1"], c["X"].shape[1:3]))
     dw1 = P.conv_wgrad(c["X"], g1, p["w1"].shape[0])
     return dX, dict(dw1=dw1, b2=b2, b3=b3, dgamma3=dgamma3, dbeta3=dbeta3)
+
+
+# ------------------------------------------------ full DenseNet(-121) ----
+def densenet_fwd(d, eps, rnd):
+    """One training forward pass of a DenseNet (Sec. 2.3: dense blocks joined
+    by transition layers; Sec. 3.1: a first 7x7 CONV):
+      stem   CONV7x7/2 pad 3 -> BN -> ReLU -> max pooling 3x3/2 pad 1,
+      blocks dense layers, then (all but the last) transition BN-ReLU-CONV1x1
+             + 2x2 average pooling whose output is the next block's input,
+      head   BN -> ReLU -> global average pooling -> FC -> softmax
+             cross-entropy (mean over the batch).
+    d: img [N,H,W,Ci], stem {w, gamma, beta}, blocks [{cpls, trans or None,
+    c_total}], head {gamma, beta, w [C,K], b [K]}, labels [N].
+    Returns (loss, cache)."""
+    st = d["stem"]
+    img = np.asarray(d["img"], np.float64)
+    s = rnd(P.conv_fwd(img, st["w"], stride=2, pad=3))
+    y0, m0, v0, r0 = P.bn_fwd(s, st["gamma"], st["beta"], eps)
+    z0 = P.relu_fwd(y0)
+    X = rnd(P.maxpool_fwd(z0, 3, 2, 1))
+    stem = dict(img=img, s=s, y=y0, z=z0, mean=m0, var=v0, rstd=r0, out=X)
+    blocks = []
+    for b in d["blocks"]:
+        if b["trans"] is not None:
+            X, cb = block_fwd(X, b["cpls"], b["trans"], eps, rnd, b["c_total"])
+        else:
+            buf, caches = dense_layers_fwd(X, b["cpls"], eps, rnd, b["c_total"])
+            cb = dict(buf=buf, cpls=caches, C0=X.shape[3])
+            X = buf
+        blocks.append(cb)
+    hp = d["head"]
+    y5, m5, v5, r5 = P.bn_fwd(X, hp["gamma"], hp["beta"], eps)
+    z5 = P.relu_fwd(y5)
+    f = P.global_avgpool_fwd(z5)
+    logits = P.fc_fwd(f, hp["w"], hp["b"])
+    loss, dlogits = P.softmax_ce(logits, d["labels"])
+    head = dict(x=X, y=y5, z=z5, mean=m5, var=v5, rstd=r5, f=f, logits=logits, dlogits=dlogits)
+    return loss, dict(stem=stem, blocks=blocks, head=head, d=d)
+
+
+def densenet_bwd(c, rnd):
+    """Backward of ``densenet_fwd`` for the loss itself.  Returns the
+    parameter gradients and the intermediate gradients the fused path
+    materialises (stored ones rounded by ``rnd``)."""
+    d, hd, st = c["d"], c["head"], c["stem"]
+    hp = d["head"]
+    df, dwfc, dbfc = P.fc_bwd(hd["f"], hp["w"], hd["dlogits"])
+    dz5 = P.global_avgpool_bwd(df, hd["x"].shape[1:3])
+    dy5 = P.relu_bwd(dz5, hd["y"])
+    dx5, dg5, db5 = P.bn_bwd(hd["x"], dy5, hp["gamma"], hd["mean"], hd["rstd"])
+    head = dict(df=df, dw=dwfc, db=dbfc, dgamma=dg5, dbeta=db5)
+    blocks = [None] * len(c["blocks"])
+    cb = c["blocks"][-1]
+    G = rnd(dx5)
+    blocks[-1] = dict(cpls=dense_layers_bwd(cb["cpls"], G, rnd), G=G)
+    dX = G[..., :cb["C0"]]
+    for i in range(len(c["blocks"]) - 2, -1, -1):
+        dX, blocks[i] = block_bwd(c["blocks"][i], dX, rnd)
+    dz0 = P.maxpool_bwd(st["z"], dX, 3, 2, 1)
+    dy0 = rnd(P.relu_bwd(dz0, st["y"]))
+    dx0, dg0, db0 = P.bn_bwd(st["s"], dy0, d["stem"]["gamma"], st["mean"], st["rstd"])
+    dw0 = P.conv_wgrad(st["img"], rnd(dx0), d["stem"]["w"].shape[0], stride=2, pad=3)
+    stem = dict(dX=dX, dy=dy0, dw=dw0, dgamma=dg0, dbeta=db0)
+    return dict(head=head, blocks=blocks, stem=stem)

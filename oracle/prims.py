@@ -166,3 +166,46 @@ def round_bf16(a):
     a = np.array(a, dtype=np.float64, copy=True)
     lib().orc_round_bf16(ctypes.c_long(a.size), _p(a))
     return a
+
+
+# ------------------------------------------------------- network head ----
+# The paper names the network's single fully connected layer (Sec. 2.2: 120
+# CONV layers plus one FC layer) but gives no equations for the head; these
+# are the standard classifier: global average pooling, an affine layer and
+# the softmax cross-entropy averaged over the mini-batch.  numpy fp64.
+def global_avgpool_fwd(x):
+    """[N, H, W, C] -> [N, C]: mean over the H*W positions of each image."""
+    x = _f64(x)
+    return x.sum(axis=(1, 2)) / (x.shape[1] * x.shape[2])
+
+
+def global_avgpool_bwd(gout, hw):
+    """Every position of image n receives gout[n, c] / (H*W)."""
+    gout = _f64(gout)
+    H, W = hw
+    return np.broadcast_to((gout / (H * W))[:, None, None, :], (gout.shape[0], H, W, gout.shape[1])).copy()
+
+
+def fc_fwd(f, wt, bias):
+    """logits[n, j] = sum_c f[n, c] * wt[c, j] + bias[j]."""
+    return _f64(f) @ _f64(wt) + _f64(bias)[None, :]
+
+
+def fc_bwd(f, wt, glogits):
+    """(df, dwt, dbias) of L = sum(logits * glogits)."""
+    f, wt, gl = _f64(f), _f64(wt), _f64(glogits)
+    return gl @ wt.T, f.T @ gl, gl.sum(axis=0)
+
+
+def softmax_ce(logits, labels):
+    """Mean over the batch of -log softmax(logits)[n, label[n]], and its
+    gradient with respect to the logits: (softmax - onehot) / N."""
+    z = _f64(logits)
+    N, K = z.shape
+    lab = np.asarray(labels, dtype=np.int64)
+    s = z - z.max(axis=1, keepdims=True)
+    lse = np.log(np.exp(s).sum(axis=1))
+    loss = float(np.mean(lse - s[np.arange(N), lab]))
+    p = np.exp(s - lse[:, None])
+    p[np.arange(N), lab] -= 1.0
+    return loss, p / N

@@ -111,3 +111,36 @@ def resnet_stack(seed=0, n=128, h=56, w=56, c=256, width=64, blocks=3, bf16=True
         ps.append(d)
     return dict(x=normal(seed, "x", (n, h, w, c), bf16=bf16), blocks=ps,
                 dy=normal(seed, "dy", (n, h, w, c), bf16=bf16), eps=EPS, bf16=bf16)
+
+
+def densenet(seed=0, n=128, hw=224, c_img=3, c_stem=64, growth=32, width=128, blocks=(6, 12, 24, 16),
+             classes=1000, bf16=True):
+    """A whole DenseNet training step: image [n, hw, hw, c_img] ~ N(0, 1),
+    uniform random labels in [0, classes), 7x7 stem CONV (He-normal), BN
+    parameters as everywhere, dense blocks of `blocks` composite layers with
+    compression-1/2 transitions between them, and the classifier FC
+    (weight N(0, 1/C), bias N(0, 0.1)).  Defaults: DenseNet-121 at 224x224."""
+    stem_bn = bn_params(seed, "stem.bn", c_stem)
+    d = dict(img=normal(seed, "img", (n, hw, hw, c_img), bf16=bf16),
+             labels=_gen(seed, "labels").integers(0, classes, size=n).astype(np.int32),
+             stem=dict(w=conv_weight(seed, "stem.w", 7, c_img, c_stem, bf16), gamma=stem_bn["gamma"],
+                       beta=stem_bn["beta"]),
+             blocks=[], eps=EPS, bf16=bf16)
+    c0 = c_stem
+    for b, layers in enumerate(blocks):
+        cpls, c_l = [], c0
+        for l in range(layers):
+            cpls.append(cpl_params(seed, "b%d.cpl%d" % (b, l), c_l, width, growth, bf16))
+            c_l += growth
+        trans = None
+        if b + 1 < len(blocks):
+            tb = bn_params(seed, "b%d.trans.bn" % b, c_l)
+            trans = dict(gamma=tb["gamma"], beta=tb["beta"],
+                         w=conv_weight(seed, "b%d.trans.w" % b, 1, c_l, c_l // 2, bf16))
+        d["blocks"].append(dict(cpls=cpls, trans=trans, c_total=c_l, c0=c0))
+        c0 = c_l // 2
+    hb = bn_params(seed, "head.bn", c_l)
+    d["head"] = dict(gamma=hb["gamma"], beta=hb["beta"],
+                     w=normal(seed, "head.w", (c_l, classes), std=float(1.0 / np.sqrt(c_l)), bf16=bf16),
+                     b=normal(seed, "head.b", (classes,), 0.1))
+    return d

@@ -1,7 +1,8 @@
 """Plants plausible mistakes in a copy of the CPU oracle and checks that the
 pins in test_oracle_pins.py catch every one of them (CPU only).
 
-Each mutant is a one-spot text edit of oracle/oracle.c or oracle/compose.py:
+Each mutant is a one-spot text edit of oracle/oracle.c, oracle/compose.py or
+oracle/prims.py:
 a flipped filter tap, a transposed weight index, an unbiased variance, a
 dropped or sign-flipped term of the BN gradient, a wrong ReLU tie rule, a lost
 concat-gradient accumulation, ...  The mutated copy (with the pins and the
@@ -52,6 +53,13 @@ MUTANTS = [
     ("transition backward skips the pooling gradient", "compose.py",
      'gt = rnd(P.avgpool2_bwd(dpool, ut["x"].shape[1:3]))', 'gt = rnd(np.repeat(np.repeat(dpool, 2, 1), 2, 2))'),
     ("residual gradient not added", "compose.py", 'dX = rnd(ds + P.conv_dgrad(', 'dX = rnd(0 * ds + P.conv_dgrad('),
+    ("cross-entropy gradient not averaged over the batch", "prims.py", "return loss, p / N", "return loss, p"),
+    ("FC bias dropped", "prims.py", "return _f64(f) @ _f64(wt) + _f64(bias)[None, :]", "return _f64(f) @ _f64(wt)"),
+    ("global pooling gradient scaled by 1/H only", "prims.py", "(gout / (H * W))", "(gout / H)"),
+    ("head ReLU mask taken on the BN input", "compose.py", 'dy5 = P.relu_bwd(dz5, hd["y"])',
+     'dy5 = P.relu_bwd(dz5, hd["x"])'),
+    ("stem weight gradient with the wrong padding", "compose.py",
+     'd["stem"]["w"].shape[0], stride=2, pad=3)', 'd["stem"]["w"].shape[0], stride=2, pad=2)'),
 ]
 
 
@@ -62,6 +70,10 @@ def _run_mutant(tmp_root, idx, fname, old, new):
     os.makedirs(os.path.join(d, "tests"))
     shutil.copy(os.path.join(ROOT, "tests", "test_oracle_pins.py"), os.path.join(d, "tests"))
     shutil.copytree(os.path.join(ROOT, "tests", "golden"), os.path.join(d, "tests", "golden"))
+    pkg = os.path.join(d, "paper_1807_01702_amd")        # the seeded input generator the pins draw from
+    os.makedirs(pkg)
+    for f in ("__init__.py", "synth.py"):
+        shutil.copy(os.path.join(ROOT, "paper_1807_01702_amd", f), pkg)
     path = os.path.join(d, "oracle", fname)
     src = open(path).read()
     assert src.count(old) == 1, "mutation site not unique/found: %r" % old
