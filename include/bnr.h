@@ -157,18 +157,20 @@ bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr
                                 const void *w, void *y, bnr_bn *y_bn,
                                 void *ws, size_t ws_bytes, void *stream);
 
-/* 2x2 average pooling, stride 2, of x[n][h][w][c] (pixel stride ldc) into
- * y[n][h/2][w/2][c] (dense); h and w even.  (DenseNet transition layer.) */
+/* 2x2 average pooling, stride 2, of x[n][h][w][c] (pixel stride ldc) into the
+ * view y[n][h/2][w/2][c] (pixel stride y_ldc, e.g. the first channels of the
+ * next dense block's concatenation buffer); h and w even.  (DenseNet
+ * transition layer, Sec. 2.3.) */
 bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype,
-                            const void *x, int32_t ldc, void *y, void *stream);
+                            const void *x, int32_t ldc, void *y, int32_t y_ldc, void *stream);
 
 /* ----------------------------------------------------- backward path ---- */
 
 /* Backward of bnr_avgpool2_fwd as a separate sweep (used by the unfused
  * path): gx[n][y][x][c] = g[n][y/2][x/2][c] / 4, written to the view gx
- * (pixel stride gx_ldc) from the dense pooled gradient g. */
+ * (pixel stride gx_ldc) from the pooled gradient view g (pixel stride g_ldc). */
 bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *g,
-                            void *gx, int32_t gx_ldc, void *stream);
+                            int32_t g_ldc, void *gx, int32_t gx_ldc, void *stream);
 
 /* Backward of one BN-ReLU-CONV chain (or of a plain CONV when x_bn is NULL),
  * with the paper's backward fission/fusion (Sec. 3.2, Fig. 5b):
@@ -335,6 +337,125 @@ typedef struct {
 bnr_status bnr_reference_bn_add_relu(int32_t backward, int64_t m, int32_t c, bnr_dtype dtype,
                                      const bnr_addrelu_ref_args *a, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------------ network ends (whole DenseNet) ---- */
+
+/* The first CONV of the network: 7x7, stride 2, zero padding 3 (Sec. 3.1
+ * notes DenseNet-121's first CONV is 7x7), c_in image channels -> 64.
+ *   img [n][h][w][4] (dtype): channels 0..c_in-1 are used, the rest are read
+ *       as 0 (one 8-byte bf16 / 16-byte float32 pixel);  w <= 256.
+ *   w   [7][7][c_in][64] (dtype).
+ *   s   [n][ho][wo][64] dense output, ho = (h-1)/2 + 1, wo = (w-1)/2 + 1. */
+typedef struct {
+    int32_t n, h, w;       /* batch size, image height and width                 */
+    int32_t c_in;          /* image channels, 1..4                               */
+    bnr_dtype dtype;
+} bnr_stem_desc;
+
+/* Workspace bytes for bnr_stem_conv_fwd and bnr_stem_wgrad on d. */
+size_t bnr_stem_workspace_size(const bnr_stem_desc *d);
+
+/* First CONV with the sub-BN1 statistics epilogue of the BN after it (Sec.
+ * 3.2 CONV-(sub-BN1) fusion): s = conv(img, w) and, when s_bn is not NULL,
+ * the mean/var/rstd of s's 64 channels (float32 per-workgroup sums of the
+ * stored values, float64 combine) into s_bn.  (The float32 storage type runs
+ * a direct CONV and a statistics sweep: it is the parity configuration.) */
+bnr_status bnr_stem_conv_fwd(const bnr_stem_desc *d, const void *img, const void *w, void *s,
+                             bnr_bn *s_bn, void *ws, size_t ws_bytes, void *stream);
+
+/* Weight gradient of the first CONV: dw[7][7][c_in][64] (float32, overwritten)
+ * = sum over output pixels of the image patch times g, g the gradient of s
+ * from g_src: BNR_GRAD_DENSE (view g, pixel stride g_ldc) or BNR_GRAD_BN (the
+ * BN after the CONV: g = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m) formed on
+ * load from dy [m][64] dense and x = s, Sec. 3.2 backward fusion; rounded to
+ * the storage type before the product as a stored gradient would be).  The
+ * image needs no gradient. */
+bnr_status bnr_stem_wgrad(const bnr_stem_desc *d, const void *img, const bnr_grad_src *g_src, float *dw,
+                          void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for the two max-pooling calls below on x[n][h][w][c]. */
+size_t bnr_pool_workspace_size(int32_t n, int32_t h, int32_t w, int32_t c);
+
+/* BN -> ReLU -> 3x3 / stride 2 / pad 1 max pooling (the layer after the first
+ * CONV; padded taps never win), with sub-BN2 + ReLU applied while the pooling
+ * reads x (Sec. 3.2 places sub-BN2 and ReLU in the reader of the BN output):
+ * y[n][ho][wo][c] = max over the window of relu(gamma*(x-mean)*rstd + beta)
+ * (x_bn: gamma, beta, mean, rstd of x), or of x itself when x_bn is NULL.
+ * When y_bn is not NULL the statistics of y (as stored) go to y_bn in the
+ * same pass (the sub-BN1 of the next BN: a dense block's input).  Views x
+ * (pixel stride x_ldc), y (pixel stride y_ldc); ho = (h-1)/2+1, wo likewise.
+ * ws: bnr_pool_workspace_size bytes (may be NULL when y_bn is NULL). */
+bnr_status bnr_bn_relu_maxpool_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype,
+                                   const void *x, int32_t x_ldc, const bnr_bn *x_bn, void *y, int32_t y_ldc,
+                                   bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream);
+
+/* Backward of bnr_bn_relu_maxpool_fwd: each gradient gy[n][oh][ow][c] (view,
+ * pixel stride gy_ldc) goes to the first maximum of its window (row-major
+ * tap order).  With x_bn: the ReLU mask is applied (dy = dz [y > 0], y
+ * recomputed from x), dy is stored to dy [n*h*w][c] (dense) and the BN
+ * reductions dbeta = sum(dy), dgamma = sum(dy*xhat) of the stored dy are
+ * written (Sec. 3.2 backward fusion); the BN input gradient stays deferred
+ * (the first CONV's weight gradient consumes it as BNR_GRAD_BN).  Without
+ * x_bn: dy receives the pooling input gradient.  c <= 64 with a power-of-two
+ * number of 16-byte vectors; wo <= 64.  ws: bnr_pool_workspace_size bytes
+ * (may be NULL without x_bn). */
+bnr_status bnr_maxpool_bn_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *x,
+                              int32_t x_ldc, const bnr_bn *x_bn, const void *gy, int32_t gy_ldc, void *dy,
+                              float *dgamma, float *dbeta, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes for bnr_head_bwd on x[n][h][w][c]. */
+size_t bnr_head_workspace_size(int32_t n, int32_t h, int32_t w, int32_t c);
+
+/* Classifier head (the network's one FC layer, Sec. 2.2): BN -> ReLU ->
+ * global average pooling -> FC -> softmax cross-entropy over the batch.
+ *   x [n*h*w][c] view (pixel stride x_ldc) with its BN x_bn (gamma, beta and
+ *   the statistics of x, already produced); wfc [c][classes] (dtype);
+ *   bfc [classes]; labels [n] int32 (device; a label outside [0, classes)
+ *   makes the loss NaN).  Outputs (float32, device): f [n][c] pooled
+ *   features, logits [n][classes], dlogits = (softmax - onehot)/n, and
+ *   loss[0] = mean over the batch of -log softmax(logits)[label]. */
+bnr_status bnr_head_fwd(int32_t n, int32_t h, int32_t w, int32_t c, int32_t classes, bnr_dtype dtype,
+                        const void *x, int32_t x_ldc, const bnr_bn *x_bn, const void *wfc, const float *bfc,
+                        const int32_t *labels, float *f, float *logits, float *dlogits, float *loss,
+                        void *stream);
+
+/* Backward of bnr_head_fwd from its dlogits: df = dlogits wfc^T [n][c],
+ * dwfc = f^T dlogits [c][classes], dbfc = column sums [classes] (all float32,
+ * overwritten), and the head BN's backward: dy = [y > 0] df/(h*w) (not
+ * stored), dbeta = sum(dy), dgamma = sum(dy*xhat).  The BN input gradient:
+ *   alpha, betap not NULL (x is a DenseNet concatenation, Sec. 3.2 ICF): gx
+ *     receives gamma*rstd*dy and alpha/betap are written, the summed form of
+ *     bnr_bwd_fused_split (accumulate = 0);
+ *   alpha, betap NULL: gx receives gamma*rstd*(dy - dbeta/m - xhat*dgamma/m).
+ * gx: view (pixel stride gx_ldc), must not overlap x. */
+bnr_status bnr_head_bwd(int32_t n, int32_t h, int32_t w, int32_t c, int32_t classes, bnr_dtype dtype,
+                        const void *x, int32_t x_ldc, const bnr_bn *x_bn, const void *wfc, const float *f,
+                        const float *dlogits, float *df, float *dwfc, float *dbfc, float *dgamma, float *dbeta,
+                        void *gx, int32_t gx_ldc, float *alpha, float *betap, void *ws, size_t ws_bytes,
+                        void *stream);
+
+/* Unfused A/B counterpart of a BN -> ReLU pair whose reader is not a CONV
+ * (the max pooling after the first CONV): forward, two-pass statistics of
+ * x[m][c] (pixel stride x_ldc) into bn (mean, var, rstd), a normalise sweep
+ * (write y, dense [m][c]) and a ReLU sweep (write z, dense); backward, a
+ * ReLU-backward sweep dy = gz [y > 0] (write dy, dense), a reductions sweep
+ * (dgamma, dbeta) and an input-gradient sweep (write dx, pixel stride
+ * dx_ldc).  ws: bnr_stats_workspace_size(m, c) bytes. */
+typedef struct {
+    const void *x;       /* BN input                                      */
+    int32_t x_ldc;
+    bnr_bn *bn;
+    void *y;             /* BN output, dense [m][c] (written forward)     */
+    void *z;             /* forward: ReLU output, dense [m][c]            */
+    const void *gz;      /* backward: gradient of z                       */
+    int32_t gz_ldc;
+    void *dy;            /* backward: masked gradient, dense [m][c]       */
+    float *dgamma, *dbeta;
+    void *dx;            /* backward: BN input gradient                   */
+    int32_t dx_ldc;
+} bnr_bnrelu_ref_args;
+bnr_status bnr_reference_bn_relu(int32_t backward, int64_t m, int32_t c, bnr_dtype dtype,
+                                 const bnr_bnrelu_ref_args *a, void *ws, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------ diagnostics ---- */
 
 /* Plain device-to-device copy of `bytes` (multiple of 16) with the same
@@ -352,7 +473,8 @@ bnr_status bnr_hbm_copy(const void *src, void *dst, size_t bytes, void *stream);
  * output written once), the floating-point operations and a kernel id
  * (1 CONV 1x1, 2 CONV 3x3, 3 weight gradient 1x1, 4 weight gradient 3x3,
  * 5 statistics sweep, 6 element-wise pass, 7 statistics combine, 8 weight
- * packing, 9 split-K sum, 10 pooling, 11 copy); it returns the number of
+ * packing, 9 split-K sum, 10 pooling, 11 copy, 12 first CONV, 13 first-CONV
+ * weight gradient, 14 max pooling, 15 classifier head); it returns the number of
  * launches written.  Not meant for graph capture. */
 bnr_status bnr_trace_begin(int32_t kernel_classes, int32_t capacity);
 int32_t bnr_trace_end(double *ms, double *bytes, double *flops, int32_t *kernel_id, int32_t capacity);

@@ -45,6 +45,16 @@ class GradSrc(ctypes.Structure):
                 ("bn", ctypes.POINTER(BNStruct)), ("dgamma", c_vp), ("dbeta", c_vp), ("alpha", c_vp), ("betap", c_vp)]
 
 
+class BnReluRefArgs(ctypes.Structure):
+    _fields_ = [("x", c_vp), ("x_ldc", c_i32), ("bn", ctypes.POINTER(BNStruct)), ("y", c_vp), ("z", c_vp),
+                ("gz", c_vp), ("gz_ldc", c_i32), ("dy", c_vp), ("dgamma", c_vp), ("dbeta", c_vp), ("dx", c_vp),
+                ("dx_ldc", c_i32)]
+
+
+class StemDesc(ctypes.Structure):
+    _fields_ = [("n", c_i32), ("h", c_i32), ("w", c_i32), ("c_in", c_i32), ("dtype", ctypes.c_int)]
+
+
 class RefArgs(ctypes.Structure):
     _fields_ = [("x", c_vp), ("bn", ctypes.POINTER(BNStruct)), ("w", c_vp), ("y", c_vp), ("z", c_vp), ("out", c_vp),
                 ("g", c_vp), ("g_ldc", c_i32), ("dz", c_vp), ("dy", c_vp), ("dw", c_vp), ("dgamma", c_vp),
@@ -77,9 +87,9 @@ _lib_fns = dict(
     bnr_bn_relu_conv_fwd=_sig("bnr_bn_relu_conv_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, c_vp,
                               _P(BNStruct), c_vp, c_sz, c_vp),
     bnr_avgpool2_fwd=_sig("bnr_avgpool2_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
-                          c_vp, c_vp),
-    bnr_avgpool2_bwd=_sig("bnr_avgpool2_bwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_vp,
-                          c_i32, c_vp),
+                          c_vp, c_i32, c_vp),
+    bnr_avgpool2_bwd=_sig("bnr_avgpool2_bwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
+                          c_vp, c_i32, c_vp),
     bnr_bwd_fused=_sig("bnr_bwd_fused", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, _P(GradSrc), c_vp,
                        c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_sz, c_vp),
     bnr_bwd_fused_split=_sig("bnr_bwd_fused_split", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
@@ -98,13 +108,31 @@ _lib_fns = dict(
                              c_vp, c_i32, _P(BNStruct), c_vp, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp),
     bnr_reference_bn_add_relu=_sig("bnr_reference_bn_add_relu", ctypes.c_int, c_i32, c_i64, c_i32, ctypes.c_int,
                                    _P(AddReluRefArgs), c_vp, c_sz, c_vp),
+    bnr_reference_bn_relu=_sig("bnr_reference_bn_relu", ctypes.c_int, c_i32, c_i64, c_i32, ctypes.c_int,
+                               _P(BnReluRefArgs), c_vp, c_sz, c_vp),
+    bnr_stem_workspace_size=_sig("bnr_stem_workspace_size", c_sz, _P(StemDesc)),
+    bnr_stem_conv_fwd=_sig("bnr_stem_conv_fwd", ctypes.c_int, _P(StemDesc), c_vp, c_vp, c_vp, _P(BNStruct), c_vp,
+                           c_sz, c_vp),
+    bnr_stem_wgrad=_sig("bnr_stem_wgrad", ctypes.c_int, _P(StemDesc), c_vp, _P(GradSrc), c_vp, c_vp, c_sz, c_vp),
+    bnr_pool_workspace_size=_sig("bnr_pool_workspace_size", c_sz, c_i32, c_i32, c_i32, c_i32),
+    bnr_bn_relu_maxpool_fwd=_sig("bnr_bn_relu_maxpool_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int,
+                                 c_vp, c_i32, _P(BNStruct), c_vp, c_i32, _P(BNStruct), c_vp, c_sz, c_vp),
+    bnr_maxpool_bn_bwd=_sig("bnr_maxpool_bn_bwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
+                            _P(BNStruct), c_vp, c_i32, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp),
+    bnr_head_workspace_size=_sig("bnr_head_workspace_size", c_sz, c_i32, c_i32, c_i32, c_i32),
+    bnr_head_fwd=_sig("bnr_head_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
+                      _P(BNStruct), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp),
+    bnr_head_bwd=_sig("bnr_head_bwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
+                      _P(BNStruct), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_vp, c_vp, c_vp,
+                      c_sz, c_vp),
     bnr_trace_begin=_sig("bnr_trace_begin", ctypes.c_int, c_i32, c_i32),
     bnr_trace_end=_sig("bnr_trace_end", c_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i32), c_i32),
 )
 
 KERNEL_IDS = {1: "conv1x1", 2: "conv3x3", 3: "wgrad1x1", 4: "wgrad3x3", 5: "stats_sweep", 6: "elementwise",
-              7: "stats_combine", 8: "weight_pack", 9: "splitk_sum", 10: "pool", 11: "copy"}
+              7: "stats_combine", 8: "weight_pack", 9: "splitk_sum", 10: "pool", 11: "copy", 12: "stem_conv",
+              13: "stem_wgrad", 14: "maxpool", 15: "head"}
 
 
 class BnrError(RuntimeError):
@@ -250,12 +278,14 @@ def bnr_bn_relu_conv_fwd(desc, x, x_bn, w, y, y_bn=None):
 
 def bnr_avgpool2_fwd(x, y, n, h, w):
     p, m, c, ldc = view(x)
-    _check(_lib_fns["bnr_avgpool2_fwd"](n, h, w, c, dtype_code(x), p, ldc, _ptr(y), _stream()))
+    py, _, _, ldy = view(y)
+    _check(_lib_fns["bnr_avgpool2_fwd"](n, h, w, c, dtype_code(x), p, ldc, py, ldy, _stream()))
 
 
 def bnr_avgpool2_bwd(g, gx, n, h, w):
     pd, _, c, ldc = view(gx)
-    _check(_lib_fns["bnr_avgpool2_bwd"](n, h, w, c, dtype_code(gx), _ptr(g), pd, ldc, _stream()))
+    pg, _, _, ldg = view(g)
+    _check(_lib_fns["bnr_avgpool2_bwd"](n, h, w, c, dtype_code(gx), pg, ldg, pd, ldc, _stream()))
 
 
 def grad_dense(g):
@@ -406,3 +436,79 @@ def bnr_trace_end(capacity=100000):
     kid = (c_i32 * capacity)()
     n = _lib_fns["bnr_trace_end"](ms, by, fl, kid, capacity)
     return [(KERNEL_IDS.get(kid[i], str(kid[i])), ms[i], by[i], fl[i]) for i in range(n)]
+
+
+# ------------------------------------------------------ network ends ----
+def stem_desc(img, c_in):
+    """First-CONV descriptor of an image tensor [n, h, w, 4] with c_in channels used."""
+    n, h, w, pix = img.shape
+    assert pix == 4 and img.is_contiguous()
+    return StemDesc(n, h, w, c_in, dtype_code(img))
+
+
+def bnr_stem_conv_fwd(img, w, s, s_bn=None):
+    d = stem_desc(img, w.shape[2])
+    ws, wsb = workspace(_lib_fns["bnr_stem_workspace_size"](ctypes.byref(d)), img.device)
+    bs = s_bn.struct() if s_bn is not None else None
+    _check(_lib_fns["bnr_stem_conv_fwd"](ctypes.byref(d), _ptr(img), _ptr(w), _ptr(s),
+                                         ctypes.byref(bs) if bs is not None else None, ws, wsb, _stream()))
+
+
+def bnr_stem_wgrad(img, c_in, g_src, dw):
+    d = stem_desc(img, c_in)
+    ws, wsb = workspace(_lib_fns["bnr_stem_workspace_size"](ctypes.byref(d)), img.device)
+    gs, keep = _grad_struct(g_src)
+    _check(_lib_fns["bnr_stem_wgrad"](ctypes.byref(d), _ptr(img), ctypes.byref(gs), _ptr(dw), ws, wsb, _stream()))
+    del keep
+
+
+def bnr_bn_relu_maxpool_fwd(x, x_bn, y, n, h, w, y_bn=None):
+    """y = maxpool3x3/2(relu(bn(x))) (x_bn None: of x) [+ statistics of y]."""
+    px, _, c, ldx = view(x)
+    py, _, _, ldy = view(y)
+    ws, wsb = workspace(_lib_fns["bnr_pool_workspace_size"](n, h, w, c), x.device)
+    xs = x_bn.struct() if x_bn is not None else None
+    ys = y_bn.struct() if y_bn is not None else None
+    _check(_lib_fns["bnr_bn_relu_maxpool_fwd"](n, h, w, c, dtype_code(x), px, ldx,
+                                               ctypes.byref(xs) if xs is not None else None, py, ldy,
+                                               ctypes.byref(ys) if ys is not None else None, ws, wsb, _stream()))
+
+
+def bnr_maxpool_bn_bwd(x, x_bn, gy, dy, n, h, w, dgamma=None, dbeta=None):
+    px, _, c, ldx = view(x)
+    pg, _, _, ldg = view(gy)
+    ws, wsb = workspace(_lib_fns["bnr_pool_workspace_size"](n, h, w, c), x.device)
+    xs = x_bn.struct() if x_bn is not None else None
+    _check(_lib_fns["bnr_maxpool_bn_bwd"](n, h, w, c, dtype_code(x), px, ldx, ctypes.byref(xs) if xs is not None else None,
+                                          pg, ldg, _ptr(dy), _ptr(dgamma), _ptr(dbeta), ws, wsb, _stream()))
+
+
+def bnr_head_fwd(x, x_bn, wfc, bfc, labels, f, logits, dlogits, loss, n, h, w):
+    px, _, c, ldx = view(x)
+    xs = x_bn.struct()
+    _check(_lib_fns["bnr_head_fwd"](n, h, w, c, wfc.shape[1], dtype_code(x), px, ldx, ctypes.byref(xs), _ptr(wfc),
+                                    _ptr(bfc), _ptr(labels), _ptr(f), _ptr(logits), _ptr(dlogits), _ptr(loss),
+                                    _stream()))
+
+
+def bnr_head_bwd(x, x_bn, wfc, f, dlogits, df, dwfc, dbfc, dgamma, dbeta, gx, n, h, w, alpha=None, betap=None):
+    px, _, c, ldx = view(x)
+    pg, _, _, ldg = view(gx)
+    ws, wsb = workspace(_lib_fns["bnr_head_workspace_size"](n, h, w, c), x.device)
+    xs = x_bn.struct()
+    _check(_lib_fns["bnr_head_bwd"](n, h, w, c, wfc.shape[1], dtype_code(x), px, ldx, ctypes.byref(xs), _ptr(wfc),
+                                    _ptr(f), _ptr(dlogits), _ptr(df), _ptr(dwfc), _ptr(dbfc), _ptr(dgamma),
+                                    _ptr(dbeta), pg, ldg, _ptr(alpha), _ptr(betap), ws, wsb, _stream()))
+
+
+def bnr_reference_bn_relu(backward, x, bn, y, z=None, gz=None, dy=None, dgamma=None, dbeta=None, dx=None):
+    """Unfused BN -> ReLU (forward: stats, y, z; backward: dy, dgamma, dbeta, dx)."""
+    px, m, c, ldx = view(x)
+    pgz, ldgz = (view(gz)[0], view(gz)[3]) if gz is not None else (None, 0)
+    pdx, lddx = (view(dx)[0], view(dx)[3]) if dx is not None else (None, 0)
+    bs = bn.struct()
+    a = BnReluRefArgs(px, ldx, ctypes.pointer(bs), _ptr(y), _ptr(z), pgz, ldgz, _ptr(dy), _ptr(dgamma), _ptr(dbeta),
+                      pdx, lddx)
+    ws, wsb = workspace(bnr_stats_workspace_size(m, c), x.device)
+    _check(_lib_fns["bnr_reference_bn_relu"](1 if backward else 0, m, c, dtype_code(x), ctypes.byref(a), ws, wsb,
+                                             _stream()))

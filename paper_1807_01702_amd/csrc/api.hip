@@ -370,35 +370,39 @@ bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr
 }
 
 bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *x, int32_t ldc,
-                            void *y, void *stream)
+                            void *y, int32_t y_ldc, void *stream)
 {
     TRY(check_dtype(dtype));
     if (n <= 0 || h <= 0 || w <= 0) return fail(BNR_ERR_SHAPE, "n, h, w must be positive");
     if (h % 2 || w % 2) return fail(BNR_ERR_SHAPE, "h and w must be even");
     TRY(check_channels(c, ldc, dtype, "x"));
+    TRY(check_channels(c, y_ldc, dtype, "y"));
     TRY(check_ptr(x, "x"));
     TRY(check_ptr(y, "y"));
     const int es = esize(dtype);
     const int64_t m = (int64_t)n * h * w;
-    if (overlap(view_range(x, m, c, ldc, es), view_range(y, m / 4, c, c, es))) return fail(BNR_ERR_ALIAS, "y overlaps x");
-    TRY_HIP(launch_avgpool2(dt_of(dtype), n, h, w, c, x, ldc, y, (hipStream_t)stream), "avgpool");
+    if (overlap(view_range(x, m, c, ldc, es), view_range(y, m / 4, c, y_ldc, es)))
+        return fail(BNR_ERR_ALIAS, "y overlaps x");
+    TRY_HIP(launch_avgpool2(dt_of(dtype), n, h, w, c, x, ldc, y, y_ldc, (hipStream_t)stream), "avgpool");
     return ok();
 }
 
-bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *g, void *gx,
-                            int32_t gx_ldc, void *stream)
+bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *g, int32_t g_ldc,
+                            void *gx, int32_t gx_ldc, void *stream)
 {
     TRY(check_dtype(dtype));
     if (n <= 0 || h <= 0 || w <= 0) return fail(BNR_ERR_SHAPE, "n, h, w must be positive");
     if (h % 2 || w % 2) return fail(BNR_ERR_SHAPE, "h and w must be even");
+    TRY(check_channels(c, g_ldc, dtype, "g"));
     TRY(check_channels(c, gx_ldc, dtype, "gx"));
     TRY(check_ptr(g, "g"));
     TRY(check_ptr(gx, "gx"));
     const int es = esize(dtype);
     const int64_t m = (int64_t)n * h * w;
-    if (overlap(view_range(gx, m, c, gx_ldc, es), view_range(g, m / 4, c, c, es)))
+    if (overlap(view_range(gx, m, c, gx_ldc, es), view_range(g, m / 4, c, g_ldc, es)))
         return fail(BNR_ERR_ALIAS, "gx overlaps g");
-    TRY_HIP(launch_avgpool2_bwd(dt_of(dtype), n, h, w, c, g, gx, gx_ldc, (hipStream_t)stream), "avgpool backward");
+    TRY_HIP(launch_avgpool2_bwd(dt_of(dtype), n, h, w, c, g, g_ldc, gx, gx_ldc, (hipStream_t)stream),
+            "avgpool backward");
     return ok();
 }
 
@@ -849,6 +853,67 @@ bnr_status bnr_reference_bn_add_relu(int32_t backward, int64_t m, int32_t c, bnr
     return ok();
 }
 
+bnr_status bnr_reference_bn_relu(int32_t backward, int64_t m, int32_t c, bnr_dtype dtype, const bnr_bnrelu_ref_args *a,
+                                 void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_rows(m, c, dtype));
+    if (!a) return fail(BNR_ERR_NULL, "args is NULL");
+    TRY(check_channels(c, a->x_ldc, dtype, "x"));
+    TRY(check_ptr(a->x, "x"));
+    TRY(check_ptr(a->y, "y"));
+    TRY(check_ws(ws, ws_bytes, stats_ws(m, c)));
+    const int es = esize(dtype);
+    hipStream_t s = (hipStream_t)stream;
+    const int dt = dt_of(dtype);
+    const bnr_bn *bn = a->bn;
+    const int64_t R = stats_row_blocks(m, c, dt);
+    float *part = (float *)ws;
+    void *red = (char *)ws + stats_part_bytes(m, c);
+    const Range rx = view_range(a->x, m, c, a->x_ldc, es), ry = view_range(a->y, m, c, c, es);
+    if (overlap(rx, ry)) return fail(BNR_ERR_ALIAS, "y overlaps x");
+    if (!backward) {
+        TRY(check_bn(bn, "bn", true, true));
+        TRY(check_ptr(a->z, "z"));
+        const Range rz = view_range(a->z, m, c, c, es);
+        if (overlap(rz, rx) || overlap(rz, ry)) return fail(BNR_ERR_ALIAS, "z overlaps x or y");
+        // two-pass statistics, normalise (write y), ReLU (write z)
+        TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_SUM, nullptr, nullptr, nullptr, 0, part, R, s),
+                "mean sweep");
+        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MEAN, bn->eps, bn->mean, nullptr, nullptr, nullptr, nullptr,
+                                      red, s), "mean combine");
+        TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_SQDEV, bn->mean, nullptr, nullptr, 0, part, R, s),
+                "variance sweep");
+        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, nullptr, bn->var, bn->rstd, nullptr, nullptr,
+                                      red, s), "variance combine");
+        TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->x, a->x_ldc, nullptr, 0, bn->gamma, bn->beta, bn->mean,
+                                   bn->rstd, nullptr, nullptr, a->y, c, 0, s), "normalise");
+        TRY_HIP(launch_elementwise(dt, EW_RELU, m, c, a->y, c, nullptr, 0, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                   nullptr, a->z, c, 0, s), "ReLU");
+        return ok();
+    }
+    TRY(check_bn(bn, "bn", true, false));
+    TRY(check_ptr(a->gz, "gz"));
+    TRY(check_channels(c, a->gz_ldc, dtype, "gz"));
+    TRY(check_ptr(a->dy, "dy"));
+    TRY(check_ptr(a->dx, "dx"));
+    TRY(check_channels(c, a->dx_ldc, dtype, "dx"));
+    TRY(check_fptr(a->dgamma, "dgamma"));
+    TRY(check_fptr(a->dbeta, "dbeta"));
+    const Range rd = view_range(a->dy, m, c, c, es), rdx = view_range(a->dx, m, c, a->dx_ldc, es);
+    if (overlap(rd, rx) || overlap(rd, ry) || overlap(rdx, rx) || overlap(rdx, ry) || overlap(rdx, rd))
+        return fail(BNR_ERR_ALIAS, "dy / dx overlap an input");
+    // ReLU backward (write dy), BN reductions sweep, BN input-gradient sweep (write dx)
+    TRY_HIP(launch_elementwise(dt, EW_RELUBWD, m, c, a->gz, a->gz_ldc, a->y, c, nullptr, nullptr, nullptr, nullptr,
+                               nullptr, nullptr, a->dy, c, 0, s), "ReLU backward");
+    TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_DYX, bn->mean, bn->rstd, a->dy, c, part, R, s),
+            "BN backward sums");
+    TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma, red, s),
+            "backward sums combine");
+    TRY_HIP(launch_elementwise(dt, EW_DX, m, c, a->dy, c, a->x, a->x_ldc, bn->gamma, nullptr, bn->mean, bn->rstd,
+                               a->dgamma, a->dbeta, a->dx, a->dx_ldc, 0, s), "BN input gradient");
+    return ok();
+}
+
 bnr_status bnr_hbm_copy(const void *src, void *dst, size_t bytes, void *stream)
 {
     TRY(check_ptr(src, "src"));
@@ -857,6 +922,366 @@ bnr_status bnr_hbm_copy(const void *src, void *dst, size_t bytes, void *stream)
     Range a{(uintptr_t)src, (uintptr_t)src + bytes}, b{(uintptr_t)dst, (uintptr_t)dst + bytes};
     if (overlap(a, b)) return fail(BNR_ERR_ALIAS, "dst overlaps src");
     TRY_HIP(launch_copy16(src, dst, (int64_t)(bytes / 16), (hipStream_t)stream), "copy");
+    return ok();
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Network ends: first CONV, BN-ReLU-max pooling, classifier head.
+namespace {
+
+bnr_status check_stem(const bnr_stem_desc *d)
+{
+    if (!d) return fail(BNR_ERR_NULL, "desc is NULL");
+    TRY(check_dtype(d->dtype));
+    if (d->n <= 0 || d->h <= 0 || d->w <= 0) return fail(BNR_ERR_SHAPE, "n, h, w must be positive");
+    if (d->c_in < 1 || d->c_in > kStemPix) return fail(BNR_ERR_UNSUPPORTED, "c_in %d (1..%d)", d->c_in, kStemPix);
+    if (d->w > kStemMaxW) return fail(BNR_ERR_UNSUPPORTED, "image width %d > %d", d->w, kStemMaxW);
+    if ((int64_t)d->n * d->h * d->w * kStemPix >= ((int64_t)1 << 31)) return fail(BNR_ERR_SHAPE, "image too large");
+    if ((int64_t)d->n * stem_out(d->h) * stem_out(d->w) * kStemCout >= ((int64_t)1 << 31))
+        return fail(BNR_ERR_SHAPE, "output too large");
+    return BNR_OK;
+}
+
+struct StemWs { size_t part, red, wg, wgred, total; };
+StemWs stem_ws(const bnr_stem_desc *d)
+{
+    const int ho = stem_out(d->h), wo = stem_out(d->w);
+    const int64_t m = (int64_t)d->n * ho * wo;
+    const int64_t items = (int64_t)d->n * ((ho + kStemRows - 1) / kStemRows);
+    const int64_t nw = (int64_t)kStemK * kStemK * d->c_in * kStemCout;
+    StemWs w;
+    const size_t pg = (size_t)stem_groups(items) * 2 * kStemCout * 4, ps = stats_part_bytes(m, kStemCout);
+    w.part = align_up(pg > ps ? pg : ps);
+    w.red = align_up(stats_red_bytes(kStemCout));
+    w.wg = align_up((size_t)stem_wgrad_splits(DT_BF16, items) * nw * 4);
+    w.wgred = align_up(sum_partials_red_bytes(nw));
+    w.total = w.part + w.red + w.wg + w.wgred;
+    return w;
+}
+
+void stem_params(StemParams &p, const bnr_stem_desc *d)
+{
+    memset(&p, 0, sizeof p);
+    p.n = d->n; p.h = d->h; p.w = d->w;
+    p.ho = stem_out(d->h); p.wo = stem_out(d->w);
+    p.c_in = d->c_in;
+}
+
+Range bytes_range(const void *p, int64_t bytes)
+{
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Range{lo, lo + (uintptr_t)bytes};
+}
+
+size_t pool_ws(int n, int h, int w, int c)
+{
+    const int64_t m_out = (int64_t)n * ((h - 1) / 2 + 1) * ((w - 1) / 2 + 1);
+    int64_t R = maxpool_fwd_rows(DT_BF16, m_out, c);
+    if (maxpool_fwd_rows(DT_F32, m_out, c) > R) R = maxpool_fwd_rows(DT_F32, m_out, c);
+    if (maxpool_bwd_groups(n, h) > R) R = maxpool_bwd_groups(n, h);
+    return align_up((size_t)R * 2 * c * 4) + align_up(stats_red_bytes(c));
+}
+
+bnr_status check_pool_shape(int n, int h, int w, int c)
+{
+    if (n <= 0 || h <= 0 || w <= 0 || c <= 0) return fail(BNR_ERR_SHAPE, "n, h, w, c must be positive");
+    if ((int64_t)n * h * w > ((int64_t)1 << 31)) return fail(BNR_ERR_SHAPE, "too many pixels");
+    return BNR_OK;
+}
+
+size_t head_ws(int n, int h, int w, int c)
+{
+    const int64_t m = (int64_t)n * h * w;
+    int64_t R = head_rows(DT_BF16, m, c);
+    if (head_rows(DT_F32, m, c) > R) R = head_rows(DT_F32, m, c);
+    return align_up((size_t)R * 2 * c * 4) + align_up(stats_red_bytes(c));
+}
+
+bnr_status check_head(int n, int h, int w, int c, int classes, bnr_dtype dtype, const void *x, int x_ldc,
+                      const bnr_bn *x_bn, const void *wfc)
+{
+    TRY(check_dtype(dtype));
+    if (n <= 0 || h <= 0 || w <= 0 || classes <= 0) return fail(BNR_ERR_SHAPE, "n, h, w, classes must be positive");
+    if ((int64_t)n * h * w > ((int64_t)1 << 31) || (int64_t)c * classes > ((int64_t)1 << 31))
+        return fail(BNR_ERR_SHAPE, "too large");
+    TRY(check_channels(c, x_ldc, dtype, "x"));
+    TRY(check_ptr(x, "x"));
+    TRY(check_bn(x_bn, "x_bn", true, false));
+    TRY(check_ptr(wfc, "wfc"));
+    return BNR_OK;
+}
+
+void head_params(HeadParams &p, int n, int h, int w, int c, int classes, const void *x, int x_ldc, const bnr_bn *bn,
+                 const void *wfc)
+{
+    memset(&p, 0, sizeof p);
+    p.n = n; p.h = h; p.w = w; p.c = c; p.classes = classes;
+    p.x = x; p.x_ldc = x_ldc;
+    p.gamma = bn->gamma; p.beta = bn->beta; p.mean = bn->mean; p.rstd = bn->rstd;
+    p.wfc = wfc;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t bnr_stem_workspace_size(const bnr_stem_desc *d)
+{
+    if (check_stem(d) != BNR_OK) return 0;
+    return stem_ws(d).total;
+}
+
+bnr_status bnr_stem_conv_fwd(const bnr_stem_desc *d, const void *img, const void *w, void *s, bnr_bn *s_bn, void *ws,
+                             size_t ws_bytes, void *stream)
+{
+    TRY(check_stem(d));
+    TRY(check_ptr(img, "img"));
+    TRY(check_ptr(w, "w"));
+    TRY(check_ptr(s, "s"));
+    if (s_bn) TRY(check_bn(s_bn, "s_bn", false, true));
+    const StemWs sw = stem_ws(d);
+    TRY(check_ws(ws, ws_bytes, sw.total));
+    const int es = esize(d->dtype);
+    StemParams p;
+    stem_params(p, d);
+    const int64_t m = (int64_t)p.n * p.ho * p.wo;
+    const Range rs = bytes_range(s, m * kStemCout * es);
+    if (overlap(rs, bytes_range(img, (int64_t)d->n * d->h * d->w * kStemPix * es))) return fail(BNR_ERR_ALIAS, "s overlaps img");
+    if (overlap(rs, bytes_range(w, (int64_t)kStemK * kStemK * d->c_in * kStemCout * es)))
+        return fail(BNR_ERR_ALIAS, "s overlaps w");
+    p.img = img; p.wt = w; p.s = s;
+    p.part = (float *)ws;
+    hipStream_t st = (hipStream_t)stream;
+    const int dt = dt_of(d->dtype);
+    TRY_HIP(launch_stem_conv(dt, p, s_bn && dt == DT_BF16, st), "first conv");
+    if (s_bn) {
+        if (dt == DT_BF16) {
+            const int64_t R = stem_groups((int64_t)p.n * ((p.ho + kStemRows - 1) / kStemRows));
+            TRY_HIP(launch_stats_finalize(p.part, R, kStemCout, m, FIN_MVF, s_bn->eps, s_bn->mean, s_bn->var,
+                                          s_bn->rstd, nullptr, nullptr, (char *)ws + sw.part, st),
+                    "stats combine");
+        } else {
+            TRY(run_stats(m, kStemCout, kStemCout, d->dtype, s, s_bn, ws, st));
+        }
+    }
+    return ok();
+}
+
+bnr_status bnr_stem_wgrad(const bnr_stem_desc *d, const void *img, const bnr_grad_src *g, float *dw, void *ws,
+                          size_t ws_bytes, void *stream)
+{
+    TRY(check_stem(d));
+    TRY(check_ptr(img, "img"));
+    TRY(check_ptr(dw, "dw"));
+    if (!g) return fail(BNR_ERR_NULL, "g_src is NULL");
+    StemParams p;
+    stem_params(p, d);
+    if (g->kind == BNR_GRAD_DENSE) {
+        TRY(check_ptr(g->g, "g_src.g"));
+        TRY(check_channels(kStemCout, g->g_ldc, d->dtype, "g_src.g"));
+        p.g = g->g;
+        p.g_ldc = g->g_ldc;
+    } else if (g->kind == BNR_GRAD_BN) {
+        TRY(check_ptr(g->dy, "g_src.dy"));
+        TRY(check_ptr(g->x, "g_src.x"));
+        TRY(check_channels(kStemCout, g->x_ldc, d->dtype, "g_src.x"));
+        TRY(check_bn(g->bn, "g_src.bn", true, false));
+        TRY(check_fptr(g->dgamma, "g_src.dgamma"));
+        TRY(check_fptr(g->dbeta, "g_src.dbeta"));
+        p.g = g->dy;
+        p.g_ldc = kStemCout;
+        p.gx = g->x;
+        p.gx_ldc = g->x_ldc;
+        p.g_gamma = g->bn->gamma; p.g_mean = g->bn->mean; p.g_rstd = g->bn->rstd;
+        p.g_dgamma = g->dgamma; p.g_dbeta = g->dbeta;
+    } else {
+        return fail(BNR_ERR_UNSUPPORTED, "gradient kind %d (first CONV: dense or BN)", (int)g->kind);
+    }
+    const StemWs sw = stem_ws(d);
+    TRY(check_ws(ws, ws_bytes, sw.total));
+    p.img = img;
+    hipStream_t st = (hipStream_t)stream;
+    const int dt = dt_of(d->dtype);
+    const int gs = g->kind == BNR_GRAD_BN ? GB_BNGRAD : GB_DENSE;
+    if (dt == DT_BF16) {
+        const int64_t S = stem_wgrad_splits(dt, (int64_t)p.n * ((p.ho + kStemRows - 1) / kStemRows));
+        const int64_t len = (int64_t)kStemK * kStemK * d->c_in * kStemCout;
+        p.dwpart = (float *)((char *)ws + sw.part + sw.red);
+        TRY_HIP(launch_stem_wgrad(dt, p, gs, st), "first conv weight gradient");
+        TRY_HIP(launch_sum_partials(p.dwpart, S, len, dw, (char *)ws + sw.part + sw.red + sw.wg, st),
+                "weight gradient split sum");
+    } else {
+        p.dwpart = dw;
+        TRY_HIP(launch_stem_wgrad(dt, p, gs, st), "first conv weight gradient");
+    }
+    return ok();
+}
+
+size_t bnr_pool_workspace_size(int32_t n, int32_t h, int32_t w, int32_t c)
+{
+    if (check_pool_shape(n, h, w, c) != BNR_OK) return 0;
+    return pool_ws(n, h, w, c);
+}
+
+bnr_status bnr_bn_relu_maxpool_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *x,
+                                   int32_t x_ldc, const bnr_bn *x_bn, void *y, int32_t y_ldc, bnr_bn *y_bn, void *ws,
+                                   size_t ws_bytes, void *stream)
+{
+    TRY(check_dtype(dtype));
+    TRY(check_pool_shape(n, h, w, c));
+    TRY(check_channels(c, x_ldc, dtype, "x"));
+    TRY(check_channels(c, y_ldc, dtype, "y"));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(y, "y"));
+    if (x_bn) TRY(check_bn(x_bn, "x_bn", true, false));
+    if (y_bn) TRY(check_bn(y_bn, "y_bn", false, true));
+    TRY(check_ws(ws, ws_bytes, y_bn ? pool_ws(n, h, w, c) : 0));
+    MaxPoolParams p;
+    memset(&p, 0, sizeof p);
+    p.n = n; p.h = h; p.w = w; p.c = c;
+    p.ho = (h - 1) / 2 + 1; p.wo = (w - 1) / 2 + 1;
+    const int es = esize(dtype);
+    const int64_t m = (int64_t)n * h * w, m_out = (int64_t)n * p.ho * p.wo;
+    if (overlap(view_range(y, m_out, c, y_ldc, es), view_range(x, m, c, x_ldc, es)))
+        return fail(BNR_ERR_ALIAS, "y overlaps x");
+    p.x = x; p.x_ldc = x_ldc; p.y = y; p.y_ldc = y_ldc;
+    if (x_bn) { p.gamma = x_bn->gamma; p.beta = x_bn->beta; p.mean = x_bn->mean; p.rstd = x_bn->rstd; }
+    p.part = (float *)ws;
+    hipStream_t st = (hipStream_t)stream;
+    const int dt = dt_of(dtype);
+    TRY_HIP(launch_maxpool_fwd(dt, p, x_bn != nullptr, y_bn != nullptr, st), "max pooling");
+    if (y_bn) {
+        const int64_t R = (int64_t)ceil_div(m_out, ceil_div(m_out, maxpool_fwd_rows(dt, m_out, c)));
+        TRY_HIP(launch_stats_finalize(p.part, R, c, m_out, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
+                                      nullptr, nullptr, (char *)ws + align_up((size_t)pool_ws(n, h, w, c) -
+                                                                               align_up(stats_red_bytes(c))),
+                                      st),
+                "stats combine");
+    }
+    return ok();
+}
+
+bnr_status bnr_maxpool_bn_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *x,
+                              int32_t x_ldc, const bnr_bn *x_bn, const void *gy, int32_t gy_ldc, void *dy,
+                              float *dgamma, float *dbeta, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_dtype(dtype));
+    TRY(check_pool_shape(n, h, w, c));
+    TRY(check_channels(c, x_ldc, dtype, "x"));
+    TRY(check_channels(c, gy_ldc, dtype, "gy"));
+    TRY(check_ptr(x, "x"));
+    TRY(check_ptr(gy, "gy"));
+    TRY(check_ptr(dy, "dy"));
+    const int vec = vec_of(dtype), cvec = c / vec;
+    const int wo = (w - 1) / 2 + 1, ho = (h - 1) / 2 + 1;
+    if (c > kMaxPoolMaxC || (cvec & (cvec - 1)))
+        return fail(BNR_ERR_UNSUPPORTED, "max-pooling backward: %d channels (a power-of-two number of vectors, <= %d)",
+                    c, kMaxPoolMaxC);
+    if (wo > kMaxPoolMaxWo) return fail(BNR_ERR_UNSUPPORTED, "max-pooling backward: width %d too large", w);
+    if (x_bn) {
+        TRY(check_bn(x_bn, "x_bn", true, false));
+        TRY(check_fptr(dgamma, "dgamma"));
+        TRY(check_fptr(dbeta, "dbeta"));
+    }
+    TRY(check_ws(ws, ws_bytes, x_bn ? pool_ws(n, h, w, c) : 0));
+    const int es = esize(dtype);
+    const int64_t m = (int64_t)n * h * w, m_out = (int64_t)n * ho * wo;
+    const Range rd = view_range(dy, m, c, c, es);
+    if (overlap(rd, view_range(x, m, c, x_ldc, es))) return fail(BNR_ERR_ALIAS, "dy overlaps x");
+    if (overlap(rd, view_range(gy, m_out, c, gy_ldc, es))) return fail(BNR_ERR_ALIAS, "dy overlaps gy");
+    MaxPoolParams p;
+    memset(&p, 0, sizeof p);
+    p.n = n; p.h = h; p.w = w; p.c = c; p.ho = ho; p.wo = wo;
+    p.x = x; p.x_ldc = x_ldc; p.g = gy; p.g_ldc = gy_ldc; p.y = dy; p.y_ldc = c;
+    if (x_bn) { p.gamma = x_bn->gamma; p.beta = x_bn->beta; p.mean = x_bn->mean; p.rstd = x_bn->rstd; }
+    p.part = (float *)ws;
+    hipStream_t st = (hipStream_t)stream;
+    TRY_HIP(launch_maxpool_bwd(dt_of(dtype), p, x_bn != nullptr, st), "max-pooling backward");
+    if (x_bn) {
+        const size_t red_off = pool_ws(n, h, w, c) - align_up(stats_red_bytes(c));
+        TRY_HIP(launch_stats_finalize(p.part, maxpool_bwd_groups(n, h), c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr,
+                                      dbeta, dgamma, (char *)ws + red_off, st),
+                "backward sums combine");
+    }
+    return ok();
+}
+
+size_t bnr_head_workspace_size(int32_t n, int32_t h, int32_t w, int32_t c)
+{
+    if (n <= 0 || h <= 0 || w <= 0 || c <= 0) return 0;
+    return head_ws(n, h, w, c);
+}
+
+bnr_status bnr_head_fwd(int32_t n, int32_t h, int32_t w, int32_t c, int32_t classes, bnr_dtype dtype, const void *x,
+                        int32_t x_ldc, const bnr_bn *x_bn, const void *wfc, const float *bfc, const int32_t *labels,
+                        float *f, float *logits, float *dlogits, float *loss, void *stream)
+{
+    TRY(check_head(n, h, w, c, classes, dtype, x, x_ldc, x_bn, wfc));
+    TRY(check_fptr(bfc, "bfc"));
+    if (!labels) return fail(BNR_ERR_NULL, "labels is NULL");
+    TRY(check_fptr(f, "f"));
+    TRY(check_fptr(logits, "logits"));
+    TRY(check_fptr(dlogits, "dlogits"));
+    TRY(check_fptr(loss, "loss"));
+    HeadParams p;
+    head_params(p, n, h, w, c, classes, x, x_ldc, x_bn, wfc);
+    p.bfc = bfc; p.labels = labels; p.f = f; p.logits = logits; p.dlogits = dlogits; p.loss = loss;
+    TRY_HIP(launch_head_fwd(dt_of(dtype), p, (hipStream_t)stream), "classifier head");
+    return ok();
+}
+
+bnr_status bnr_head_bwd(int32_t n, int32_t h, int32_t w, int32_t c, int32_t classes, bnr_dtype dtype, const void *x,
+                        int32_t x_ldc, const bnr_bn *x_bn, const void *wfc, const float *f, const float *dlogits,
+                        float *df, float *dwfc, float *dbfc, float *dgamma, float *dbeta, void *gx, int32_t gx_ldc,
+                        float *alpha, float *betap, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_head(n, h, w, c, classes, dtype, x, x_ldc, x_bn, wfc));
+    TRY(check_fptr(f, "f"));
+    TRY(check_fptr(dlogits, "dlogits"));
+    TRY(check_fptr(df, "df"));
+    TRY(check_fptr(dwfc, "dwfc"));
+    TRY(check_fptr(dbfc, "dbfc"));
+    TRY(check_fptr(dgamma, "dgamma"));
+    TRY(check_fptr(dbeta, "dbeta"));
+    TRY(check_ptr(gx, "gx"));
+    TRY(check_channels(c, gx_ldc, dtype, "gx"));
+    const bool split = alpha || betap;
+    if (split) {
+        TRY(check_fptr(alpha, "alpha"));
+        TRY(check_fptr(betap, "betap"));
+    }
+    TRY(check_ws(ws, ws_bytes, head_ws(n, h, w, c)));
+    const int es = esize(dtype);
+    const int64_t m = (int64_t)n * h * w;
+    if (overlap(view_range(gx, m, c, gx_ldc, es), view_range(x, m, c, x_ldc, es)))
+        return fail(BNR_ERR_ALIAS, "gx overlaps x");
+    HeadParams p;
+    head_params(p, n, h, w, c, classes, x, x_ldc, x_bn, wfc);
+    p.f = const_cast<float *>(f);
+    p.dlogits = const_cast<float *>(dlogits);
+    p.df = df; p.dwfc = dwfc; p.dbfc = dbfc;
+    p.gx = gx; p.gx_ldc = gx_ldc;
+    p.dgamma = dgamma; p.dbeta = dbeta;
+    p.part = (float *)ws;
+    const int dt = dt_of(dtype);
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t R = ceil_div(m, ceil_div(m, head_rows(dt, m, c)));
+    void *red = (char *)ws + (head_ws(n, h, w, c) - align_up(stats_red_bytes(c)));
+    TRY_HIP(launch_head_bwd_fc(dt, p, st), "classifier head backward");
+    if (split) {
+        TRY_HIP(launch_head_bn_bwd(dt, p, HB_SPLIT, st), "head BN backward");
+        SplitTerms sp{x_bn->gamma, x_bn->rstd, alpha, betap, 0};
+        TRY_HIP(launch_stats_finalize(p.part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma, red, st,
+                                      &sp),
+                "backward sums combine");
+    } else {
+        TRY_HIP(launch_head_bn_bwd(dt, p, HB_SUMS, st), "head BN backward sums");
+        TRY_HIP(launch_stats_finalize(p.part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma, red, st),
+                "backward sums combine");
+        TRY_HIP(launch_head_bn_bwd(dt, p, HB_DX, st), "head BN input gradient");
+    }
     return ok();
 }
 

@@ -421,7 +421,7 @@ __global__ __launch_bounds__(kThreads) void k_addrelu_bwd(
 // 2x2 / stride-2 average pooling: one thread per output 16-byte vector.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_avgpool2(int n, int h, int w, int C, const T *__restrict__ x,
-                                                       int64_t ldc, T *__restrict__ y)
+                                                       int64_t ldc, T *__restrict__ y, int64_t y_ldc)
 {
     constexpr int VEC = Elem<T>::VEC;
     const int cvec = C / VEC, ho = h / 2, wo = w / 2;
@@ -441,7 +441,7 @@ __global__ __launch_bounds__(kThreads) void k_avgpool2(int n, int h, int w, int 
         Elem<T>::unpack(ldg16(x + (ip + w) * ldc + v * VEC), a);
         Elem<T>::unpack(ldg16(x + (ip + w + 1) * ldc + v * VEC), b);
         for (int j = 0; j < VEC; j++) s[j] = 0.25f * (s[j] + a[j] + b[j]);
-        stg16(y + op * C + v * VEC, Elem<T>::pack(s));
+        stg16(y + op * y_ldc + v * VEC, Elem<T>::pack(s));
     }
 }
 
@@ -449,7 +449,7 @@ __global__ __launch_bounds__(kThreads) void k_avgpool2(int n, int h, int w, int 
 // window's gradient.  One thread per input 16-byte vector.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_avgpool2_bwd(int n, int h, int w, int C, const T *__restrict__ g,
-                                                           T *__restrict__ gx, int64_t ldc)
+                                                           int64_t g_ldc, T *__restrict__ gx, int64_t ldc)
 {
     constexpr int VEC = Elem<T>::VEC;
     const int cvec = C / VEC;
@@ -463,7 +463,7 @@ __global__ __launch_bounds__(kThreads) void k_avgpool2_bwd(int n, int h, int w, 
         const int64_t nn = t / h;
         const int64_t op = (nn * (h / 2) + y / 2) * (w / 2) + x / 2;
         float f[VEC];
-        Elem<T>::unpack(ldg16(g + op * C + v * VEC), f);
+        Elem<T>::unpack(ldg16(g + op * g_ldc + v * VEC), f);
         for (int j = 0; j < VEC; j++) f[j] *= 0.25f;
         stg16(gx + ip * ldc + v * VEC, Elem<T>::pack(f));
     }
@@ -681,32 +681,33 @@ hipError_t launch_addrelu_bwd(int dtype, int64_t m, int C, const void *g, int64_
     return hipGetLastError();
 }
 
-hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, hipStream_t s)
+hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, int64_t y_ldc,
+                           hipStream_t s)
 {
     const int64_t total = (int64_t)n * (h / 2) * (w / 2) * (C / (dtype == DT_BF16 ? 8 : 4));
     const int grid = grid_cap(ceil_div(total, kThreads));
     TraceScope tr(KC_SWEEP, KID_POOL, s, 1.25 * (double)n * h * w * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_avgpool2<bf16_t>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const bf16_t *)x, ldc,
-                           (bf16_t *)y);
+                           (bf16_t *)y, y_ldc);
     else
         hipLaunchKernelGGL(k_avgpool2<float>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const float *)x, ldc,
-                           (float *)y);
+                           (float *)y, y_ldc);
     return hipGetLastError();
 }
 
-hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, void *gx, int64_t ldc,
-                               hipStream_t s)
+hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, int64_t g_ldc, void *gx,
+                               int64_t ldc, hipStream_t s)
 {
     const int64_t total = (int64_t)n * h * w * (C / (dtype == DT_BF16 ? 8 : 4));
     const int grid = grid_cap(ceil_div(total, kThreads));
     TraceScope tr(KC_SWEEP, KID_POOL, s, 1.25 * (double)n * h * w * C * (dtype == DT_BF16 ? 2 : 4), 0.0);
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_avgpool2_bwd<bf16_t>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const bf16_t *)g,
-                           (bf16_t *)gx, ldc);
+                           g_ldc, (bf16_t *)gx, ldc);
     else
         hipLaunchKernelGGL(k_avgpool2_bwd<float>, dim3(grid), dim3(kThreads), 0, s, n, h, w, C, (const float *)g,
-                           (float *)gx, ldc);
+                           g_ldc, (float *)gx, ldc);
     return hipGetLastError();
 }
 

@@ -44,9 +44,10 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
 hipError_t launch_addrelu_bwd(int dtype, int64_t m, int C, const void *g, int64_t g_ldc, const void *out,
                               int64_t out_ldc, const void *y, int64_t y_ldc, const float *mean, const float *rstd,
                               void *gm, int64_t gm_ldc, float *part, int64_t R, hipStream_t s);
-hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, hipStream_t s);
-hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, void *gx, int64_t ldc,
-                               hipStream_t s);
+hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, int64_t y_ldc,
+                           hipStream_t s);
+hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, int64_t g_ldc, void *gx,
+                               int64_t ldc, hipStream_t s);
 hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s);
 // Split-K sum scratch: up to 8 level-1 float32 rows of len.
 inline size_t sum_partials_red_bytes(int64_t len) { return 8 * (size_t)len * 4; }
@@ -134,5 +135,74 @@ struct WgradParams {
 };
 size_t wgrad_ws_bytes(int dtype, int64_t m, int n, int h, int w, int c_in, int c_out, int k);
 hipError_t launch_wgrad(const WgradParams &p, hipStream_t s);
+
+// ---- network ends: first CONV, max pooling, classifier head (net_ends.hip) ----
+// First CONV: 7x7, stride 2, pad 3, 64 output channels; the image is
+// [n][h][w][kStemPix] with c_in <= kStemPix channels used per pixel.
+constexpr int kStemK = 7, kStemPad = 3, kStemCout = 64, kStemPix = 4;
+constexpr int kStemMaxW = 256;            // widest image
+constexpr int kStemRows = 2;              // output rows per work item
+constexpr int64_t kStemMaxGroups = 512;   // persistent workgroups (two per CU)
+inline int stem_out(int x) { return (x + 2 * kStemPad - kStemK) / 2 + 1; }
+struct StemParams {
+    int n, h, w, ho, wo, c_in;
+    const void *img;              // [n][h][w][kStemPix]
+    const void *wt;               // [7][7][c_in][64]
+    void *s;                      // forward output [n][ho][wo][64]
+    float *part;                  // forward statistics partials [groups][2][64]
+    const void *g;                // weight gradient: DENSE g view / BNGRAD dy ([m][64] dense)
+    int64_t g_ldc;
+    const void *gx;               // BNGRAD: the BN input (the CONV output) view
+    int64_t gx_ldc;
+    const float *g_gamma, *g_mean, *g_rstd, *g_dgamma, *g_dbeta;
+    float *dwpart;                // weight-gradient partials [splits][7][7][c_in][64]
+};
+int64_t stem_groups(int64_t items);
+int64_t stem_wgrad_splits(int dtype, int64_t items);
+hipError_t launch_stem_conv(int dtype, const StemParams &p, bool stats, hipStream_t s);
+hipError_t launch_stem_wgrad(int dtype, const StemParams &p, int gsrc, hipStream_t s);
+
+// 3x3 / stride 2 / pad 1 max pooling (optionally of relu(bn(x))).
+constexpr int kMaxPoolMaxC = 64;          // backward: channels
+constexpr int kMaxPoolMaxWo = 64;         // backward: output width
+constexpr int64_t kMaxPoolBwdGroups = 2048;
+struct MaxPoolParams {
+    int n, h, w, c, ho, wo;
+    const void *x;                // input view [n][h][w][c]
+    int64_t x_ldc;
+    const float *gamma, *beta, *mean, *rstd;   // BN of x (NULL: plain pooling)
+    void *y;                      // forward: output view; backward: dy / dz (dense [n*h*w][c])
+    int64_t y_ldc;
+    const void *g;                // backward: gradient of the pooled output (view)
+    int64_t g_ldc;
+    float *part;                  // statistics / BN-backward partials [rows][2][c]
+};
+int64_t maxpool_fwd_rows(int dtype, int64_t m_out, int c);
+int64_t maxpool_bwd_groups(int n, int h);
+hipError_t launch_maxpool_fwd(int dtype, const MaxPoolParams &p, bool bn, bool stats, hipStream_t s);
+hipError_t launch_maxpool_bwd(int dtype, const MaxPoolParams &p, bool bn, hipStream_t s);
+
+// Classifier head: BN -> ReLU -> global average pooling -> FC -> softmax CE.
+enum { HB_SPLIT = 0, HB_SUMS = 1, HB_DX = 2 };
+struct HeadParams {
+    int n, h, w, c, classes;
+    const void *x;                // [n*h*w][c] view
+    int64_t x_ldc;
+    const float *gamma, *beta, *mean, *rstd;
+    float *f;                     // pooled features [n][c]
+    const void *wfc;              // [c][classes] (dtype)
+    const float *bfc;             // [classes]
+    const int32_t *labels;        // [n]
+    float *logits, *dlogits, *loss;
+    float *df, *dwfc, *dbfc;      // backward
+    void *gx;                     // backward: summed term / input gradient view
+    int64_t gx_ldc;
+    const float *dgamma, *dbeta;  // HB_DX
+    float *part;                  // BN-backward partials
+};
+int64_t head_rows(int dtype, int64_t m, int c);
+hipError_t launch_head_fwd(int dtype, const HeadParams &p, hipStream_t s);
+hipError_t launch_head_bwd_fc(int dtype, const HeadParams &p, hipStream_t s);
+hipError_t launch_head_bn_bwd(int dtype, const HeadParams &p, int mode, hipStream_t s);
 
 }  // namespace bnr

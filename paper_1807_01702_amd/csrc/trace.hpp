@@ -11,7 +11,8 @@ namespace bnr {
 enum KernelClass { KC_CONV = 1, KC_WGRAD = 2, KC_SWEEP = 4, KC_SMALL = 8 };
 enum KernelId {
     KID_CONV_1X1 = 1, KID_CONV_3X3 = 2, KID_WGRAD_1X1 = 3, KID_WGRAD_3X3 = 4, KID_STATS_SWEEP = 5,
-    KID_ELEMENTWISE = 6, KID_COMBINE = 7, KID_PACK = 8, KID_SPLITK_SUM = 9, KID_POOL = 10, KID_COPY = 11
+    KID_ELEMENTWISE = 6, KID_COMBINE = 7, KID_PACK = 8, KID_SPLITK_SUM = 9, KID_POOL = 10, KID_COPY = 11,
+    KID_STEM_CONV = 12, KID_STEM_WGRAD = 13, KID_MAXPOOL = 14, KID_HEAD = 15
 };
 
 bool trace_wants(int kernel_class);

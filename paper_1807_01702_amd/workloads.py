@@ -14,6 +14,8 @@ Workloads (shapes of the paper's DenseNet-121 / ResNet-50 training):
 * ``DenseBlock``   -- dense block 1 (6 composite layers, growth 32, width 128,
                       64 -> 256 channels) + transition BN-ReLU-CONV1x1 + 2x2
                       average pooling.
+* ``DenseNet``     -- the whole network: first CONV, max pooling, dense blocks
+                      and transitions, classifier head with its loss.
 * ``ResNetStack``  -- ResNet-50 conv2_x bottleneck blocks with identity
                       shortcuts.  Concat is a channel-offset buffer
                       (pointer passing, as the paper's reference does for
@@ -179,37 +181,33 @@ class Bottleneck:
         self.backward()
 
 
-class DenseBlock:
-    """Dense block 1 of DenseNet-121 + transition layer.  Block buffer X holds
-    the block input in channels [0, c0) and composite layer l writes channels
-    [c0 + l*k, c0 + (l+1)*k).  Upstream gradient: dpool of the pooled output.
+class _DenseStage:
+    """One dense block of composite layers over a concatenation buffer X
+    [n, h, w, ct] whose channels [0, c0) hold the block input (layer l writes
+    channels [c0 + l*k, c0 + (l+1)*k)), optionally followed by its transition
+    BN-ReLU-CONV1x1 + 2x2 average pooling into a caller-provided view.
 
-    ``icf`` (fused only, default on): inter-composite-layer fusion (Sec. 3.2,
-    last paragraph).  Every BN reading a channel of X sees the same values,
-    so the statistics live once per channel in shared arrays: one sweep for
-    the block input, the 3x3 CONV epilogues for every new slice; no BN1 sweeps
-    its input.  Backward: the concatenation gradient G holds the summed form
-    D = sum_l gamma_l rstd dy_l (written by the transition's and added by each
-    BN1's data-gradient epilogue) plus per-channel alpha/betap; each 3x3
-    CONV's backward forms its slice's gradient on load, and one pass
-    materialises the block input's gradient at the end.  Without ICF each BN1
-    sweeps its input for statistics and its input gradient is formed by a
-    separate pass accumulating into G."""
+    ``icf`` (fused only): inter-composite-layer fusion (Sec. 3.2, last
+    paragraph).  Every BN reading a channel of X sees the same values, so the
+    statistics live once per channel in shared arrays: one sweep (or the
+    producer's epilogue) for the block input, the 3x3 CONV epilogues for every
+    new slice; no BN1 sweeps its input.  Backward: the concatenation gradient
+    G holds the summed form D = sum_l gamma_l rstd dy_l (written by the BN
+    that reads the whole block -- the transition's or the classifier head's --
+    and added by each BN1's data-gradient epilogue) plus per-channel
+    alpha/betap; each 3x3 CONV's backward forms its slice's gradient on load,
+    and one pass materialises the block input's gradient at the end.  Without
+    ICF each BN1 sweeps its input for statistics and its input gradient is
+    formed by a separate pass accumulating into G."""
 
-    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None):
-        bf16 = data["bf16"]
-        dev = torch.device(device)
+    def __init__(self, n, h, w, c0, ct, cpls, trans, eps, dev, bf16, fused, icf, ref_mode=MODE):
         dt = torch.bfloat16 if bf16 else torch.float32
-        n, h, w, c0 = data["x"].shape
-        ct = data["c_total"]
-        eps = data["eps"]
         self.n, self.h, self.w, self.c0, self.ct = n, h, w, c0, ct
         self.X = torch.zeros((n, h, w, ct), dtype=dt, device=dev)
-        self.X[..., :c0] = _t(data["x"], dev, bf16)
         self.cpl = []
         c_l = c0
-        width = data["cpls"][0]["w1"].shape[3]
-        for p in data["cpls"]:
+        width = cpls[0]["w1"].shape[3]
+        for p in cpls:
             k = p["w2"].shape[3]
             x1 = torch.empty((n, h, w, width), dtype=dt, device=dev)
             u1 = _Unit(n, h, w, self.X[..., :c_l], x1, 1, p["gamma1"], p["beta1"], p["w1"], eps, dev, bf16, fused,
@@ -218,67 +216,86 @@ class DenseBlock:
                        fused, ref_mode)
             self.cpl.append((c_l, k, u1, u2))
             c_l += k
-        to = data["trans"]["w"].shape[3]
-        self.t = torch.empty((n, h, w, to), dtype=dt, device=dev)
-        self.ut = _Unit(n, h, w, self.X, self.t, 1, data["trans"]["gamma"], data["trans"]["beta"], data["trans"]["w"],
-                        eps, dev, bf16, fused, ref_mode)
-        self.pooled = torch.empty((n, h // 2, w // 2, to), dtype=dt, device=dev)
-        self.dpool = _t(data["dpool"], dev, bf16)
+        assert c_l == ct
+        self.ut = None
+        if trans is not None:
+            to = trans["w"].shape[3]
+            self.t = torch.empty((n, h, w, to), dtype=dt, device=dev)
+            self.ut = _Unit(n, h, w, self.X, self.t, 1, trans["gamma"], trans["beta"], trans["w"], eps, dev, bf16,
+                            fused, ref_mode)
+            self.dy_t = torch.empty((n, h, w, ct), dtype=dt, device=dev)
+            if not fused:
+                self.dt = torch.empty_like(self.t)
         self.G = torch.empty((n, h, w, ct), dtype=dt, device=dev)
-        self.dy_t = torch.empty((n, h, w, ct), dtype=dt, device=dev)
         self.dy1_flat = torch.empty(n * h * w * ct, dtype=dt, device=dev)    # dense [m][c_l] scratch, c_l < ct
         self.dy2 = torch.empty((n, h, w, width), dtype=dt, device=dev)
         if not fused:
-            self.dt = torch.empty_like(self.t)
             self.dz_flat = torch.empty(n * h * w * max(ct, width), dtype=dt, device=dev)
             self.dx2 = torch.empty_like(self.dy2)
         self.fused = fused
-        self.icf = fused if icf is None else bool(icf)
+        self.icf = bool(icf)
         if self.icf and not fused:
             raise ValueError("inter-composite-layer fusion needs the fused path")
         if self.icf:
             f32 = dict(dtype=torch.float32, device=dev)
             self.mu, self.var, self.rstd = (torch.empty(ct, **f32) for _ in range(3))
             self.alpha, self.betap = torch.empty(ct, **f32), torch.empty(ct, **f32)
-            shared = lambda lo, hi: dict(mean=self.mu[lo:hi], var=self.var[lo:hi], rstd=self.rstd[lo:hi])
-            self.in_stats = B.BN.stats_view(eps, **shared(0, c0))       # block input channels
+            self.in_stats = B.BN.stats_view(eps, **self.shared(0, c0))         # block input channels
             self.slice_stats = []
             for c_l, k, u1, u2 in self.cpl:
-                u1.bn = B.BN(u1.bn.gamma, u1.bn.beta, eps, **shared(0, c_l))
-                self.slice_stats.append(B.BN.stats_view(eps, **shared(c_l, c_l + k)))
-            self.ut.bn = B.BN(self.ut.bn.gamma, self.ut.bn.beta, eps, **shared(0, ct))
-        self.images = n
+                u1.bn = B.BN(u1.bn.gamma, u1.bn.beta, eps, **self.shared(0, c_l))
+                self.slice_stats.append(B.BN.stats_view(eps, **self.shared(c_l, c_l + k)))
+            if self.ut is not None:
+                self.ut.bn = B.BN(self.ut.bn.gamma, self.ut.bn.beta, eps, **self.shared(0, ct))
 
-    def forward(self):
+    def shared(self, lo, hi):
+        """Views of the shared per-channel statistics of channels [lo, hi)."""
+        return dict(mean=self.mu[lo:hi], var=self.var[lo:hi], rstd=self.rstd[lo:hi])
+
+    def forward(self, pooled=None, in_stats_done=False):
+        """Composite layers, then (with a transition) its CONV and the 2x2
+        pooling into the view `pooled`.  in_stats_done (ICF): the block
+        input's statistics are already in the shared arrays."""
         if self.icf:
-            B.bnr_bn_stats(self.X[..., :self.c0], self.in_stats)               # the one statistics sweep
+            if not in_stats_done:
+                B.bnr_bn_stats(self.X[..., :self.c0], self.in_stats)           # the one statistics sweep
             for (c_l, k, u1, u2), st in zip(self.cpl, self.slice_stats):
                 B.bnr_bn_relu_conv_fwd(u1.desc, u1.x, u1.bn, u1.wt, u1.out, u2.bn)
                 B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out, st)   # the new slice's statistics
             ut = self.ut
-            B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
+            if ut is not None:
+                B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
         elif self.fused:
             for c_l, k, u1, u2 in self.cpl:
                 B.bnr_bn_stats(u1.x, u1.bn)                                    # sub-BN1 of a concat: own sweep
                 B.bnr_bn_relu_conv_fwd(u1.desc, u1.x, u1.bn, u1.wt, u1.out, u2.bn)
                 B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out)
             ut = self.ut
-            B.bnr_bn_stats(ut.x, ut.bn)
-            B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
+            if ut is not None:
+                B.bnr_bn_stats(ut.x, ut.bn)
+                B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
         else:
             for c_l, k, u1, u2 in self.cpl:
                 u1.ref_fwd()
                 u2.ref_fwd()
-            self.ut.ref_fwd()
-        B.bnr_avgpool2_fwd(self.t, self.pooled, self.n, self.h, self.w)
+            if self.ut is not None:
+                self.ut.ref_fwd()
+        if self.ut is not None:
+            B.bnr_avgpool2_fwd(self.t, pooled, self.n, self.h, self.w)
 
-    def backward(self):
+    def backward(self, dpool=None):
+        """With a transition: dpool is the gradient view of the pooled output,
+        and the transition's backward starts G.  Without one the BN that
+        reads the whole block (the classifier head) has already written G
+        (and, with ICF, alpha/betap).  On return G[..., :c0] holds the
+        gradient of the block input."""
         ut = self.ut
         n, h, w = self.n, self.h, self.w
         if self.icf:
             c0 = self.c0
-            B.bnr_bwd_fused_split(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(self.dpool), ut.dw, ut.g.dgamma,
-                                  ut.g.dbeta, self.G, self.alpha, self.betap)
+            if ut is not None:
+                B.bnr_bwd_fused_split(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(dpool), ut.dw, ut.g.dgamma,
+                                      ut.g.dbeta, self.G, self.alpha, self.betap)
             for (c_l, k, u1, u2), st in zip(reversed(self.cpl), reversed(self.slice_stats)):
                 sl = slice(c_l, c_l + k)
                 B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt,
@@ -291,8 +308,9 @@ class DenseBlock:
             B.bnr_split_dx(self.G[..., :c0], self.X[..., :c0], self.in_stats, self.alpha[:c0], self.betap[:c0],
                            self.G[..., :c0])
         elif self.fused:
-            B.bnr_bwd_fused(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(self.dpool), ut.dw, ut.g.dgamma, ut.g.dbeta,
-                            self.dy_t, self.G)
+            if ut is not None:
+                B.bnr_bwd_fused(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(dpool), ut.dw, ut.g.dgamma,
+                                ut.g.dbeta, self.dy_t, self.G)
             for c_l, k, u1, u2 in reversed(self.cpl):
                 B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt, B.grad_dense(self.G[..., c_l:c_l + k]), u2.dw,
                                 u2.g.dgamma, u2.g.dbeta, self.dy2)
@@ -301,13 +319,169 @@ class DenseBlock:
                                 u1.dw, u1.g.dgamma, u1.g.dbeta, _dense(self.dy1_flat, n, h, w, c_l),
                                 self.G[..., :c_l], dx_accumulate=True)
         else:
-            B.bnr_avgpool2_bwd(self.dpool, self.dt, n, h, w)
-            ut.ref_bwd(self.dt, _dense(self.dz_flat, n, h, w, self.ct), self.dy_t, self.G, False)
+            if ut is not None:
+                B.bnr_avgpool2_bwd(dpool, self.dt, n, h, w)
+                ut.ref_bwd(self.dt, _dense(self.dz_flat, n, h, w, self.ct), self.dy_t, self.G, False)
             for c_l, k, u1, u2 in reversed(self.cpl):
                 width = u2.x.shape[-1]
                 u2.ref_bwd(self.G[..., c_l:c_l + k], _dense(self.dz_flat, n, h, w, width), self.dy2, self.dx2, False)
                 u1.ref_bwd(self.dx2, _dense(self.dz_flat, n, h, w, c_l), _dense(self.dy1_flat, n, h, w, c_l),
                            self.G[..., :c_l], True)
+
+
+class DenseBlock(_DenseStage):
+    """Dense block 1 of DenseNet-121 + transition layer on a given block
+    input; upstream gradient: dpool of the pooled output.  ``icf`` defaults
+    to on for the fused path (see _DenseStage)."""
+
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None):
+        bf16 = data["bf16"]
+        dev = torch.device(device)
+        dt = torch.bfloat16 if bf16 else torch.float32
+        n, h, w, c0 = data["x"].shape
+        super().__init__(n, h, w, c0, data["c_total"], data["cpls"], data["trans"], data["eps"], dev, bf16, fused,
+                         fused if icf is None else icf, ref_mode)
+        self.X[..., :c0] = _t(data["x"], dev, bf16)
+        to = data["trans"]["w"].shape[3]
+        self.pooled = torch.empty((n, h // 2, w // 2, to), dtype=dt, device=dev)
+        self.dpool = _t(data["dpool"], dev, bf16)
+        self.images = n
+
+    def forward(self):
+        super().forward(self.pooled)
+
+    def backward(self):
+        super().backward(self.dpool)
+
+    def step(self):
+        self.forward()
+        self.backward()
+
+
+class DenseNet:
+    """A whole DenseNet training step (forward and backward of the mean
+    softmax cross-entropy; no optimizer update): first CONV 7x7/2 -> BN ->
+    ReLU -> 3x3/2 max pooling, dense blocks joined by transitions
+    (_DenseStage), and the head BN -> ReLU -> global average pooling -> FC.
+
+    fused=True: BN fission/fusion with inter-composite-layer fusion in every
+    block.  The first CONV's epilogue produces its BN's statistics; the max
+    pooling applies that BN and the ReLU while reading and produces the
+    statistics of block 1's input; a transition's pooled output is written
+    into the next block's buffer and swept once for statistics; the head's BN
+    reads the shared statistics of the last block.  Backward: the head's BN
+    backward writes the last block's summed gradient (D, alpha, betap); each
+    block materialises the gradient of its input, which is the next-lower
+    transition's pooled-output gradient (formed on load by its CONV) or, for
+    block 1, the max pooling's output gradient; the pooling backward applies
+    the ReLU mask and the first BN's reductions, and the first CONV's weight
+    gradient forms that BN's input gradient on load.
+
+    fused=False: the unfused chain: first CONV, two-pass BN statistics,
+    normalise and ReLU sweeps, plain max pooling; blocks through
+    bnr_reference_path; backward with materialised pooling, ReLU and BN input
+    gradients.  (The head BN's statistics come from one sweep and its ReLU is
+    applied while the head pools in both paths: its tensors are three orders
+    of magnitude smaller than the first BN's.)"""
+
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE):
+        bf16 = data["bf16"]
+        dev = torch.device(device)
+        dt = torch.bfloat16 if bf16 else torch.float32
+        eps = data["eps"]
+        img = np.asarray(data["img"], np.float32)
+        n, H, W, ci = img.shape
+        self.n, self.H, self.W, self.ci = n, H, W, ci
+        img4 = np.zeros((n, H, W, 4), np.float32)
+        img4[..., :ci] = img
+        self.img = _t(img4, dev, bf16)
+        st = data["stem"]
+        self.w0 = _t(st["w"], dev, bf16)
+        c_stem = st["w"].shape[3]
+        self.hs, self.ws_ = (H - 1) // 2 + 1, (W - 1) // 2 + 1
+        self.s = torch.empty((n, self.hs, self.ws_, c_stem), dtype=dt, device=dev)
+        self.stem_bn = B.BN(_f32(st["gamma"], dev), _f32(st["beta"], dev), eps)
+        self.dw0 = torch.empty(tuple(st["w"].shape), dtype=torch.float32, device=dev)
+        self.g0 = _Grads(c_stem, dev)
+        self.dy0 = torch.empty_like(self.s)
+        h, w = (self.hs - 1) // 2 + 1, (self.ws_ - 1) // 2 + 1
+        self.stages, self.hw = [], []
+        for bd in data["blocks"]:
+            self.stages.append(_DenseStage(n, h, w, bd["c0"], bd["c_total"], bd["cpls"], bd["trans"], eps, dev, bf16,
+                                           fused, fused, ref_mode))
+            self.hw.append((h, w))
+            if bd["trans"] is not None:
+                h, w = h // 2, w // 2
+        last = self.stages[-1]
+        hp = data["head"]
+        C, K = hp["w"].shape
+        self.C, self.K = C, K
+        self.head_bn = B.BN(_f32(hp["gamma"], dev), _f32(hp["beta"], dev), eps,
+                            **(last.shared(0, C) if fused else {}))
+        self.wfc = _t(hp["w"], dev, bf16)
+        self.bfc = _f32(hp["b"], dev)
+        self.labels = torch.from_numpy(np.asarray(data["labels"], np.int32)).to(dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.f = torch.empty((n, C), **f32)
+        self.logits, self.dlogits = torch.empty((n, K), **f32), torch.empty((n, K), **f32)
+        self.loss = torch.empty(1, **f32)
+        self.df = torch.empty((n, C), **f32)
+        self.dwfc, self.dbfc = torch.empty((C, K), **f32), torch.empty(K, **f32)
+        self.g5 = _Grads(C, dev)
+        if not fused:
+            self.y0, self.z0 = torch.empty_like(self.s), torch.empty_like(self.s)
+            self.dz0, self.dx0 = torch.empty_like(self.s), torch.empty_like(self.s)
+        self.fused = fused
+        self.images = n
+
+    def forward(self):
+        s0 = self.stages[0]
+        n = self.n
+        if self.fused:
+            B.bnr_stem_conv_fwd(self.img, self.w0, self.s, self.stem_bn)
+            B.bnr_bn_relu_maxpool_fwd(self.s, self.stem_bn, s0.X[..., :s0.c0], n, self.hs, self.ws_,
+                                      y_bn=s0.in_stats)
+        else:
+            B.bnr_stem_conv_fwd(self.img, self.w0, self.s)
+            B.bnr_reference_bn_relu(False, self.s, self.stem_bn, self.y0, z=self.z0)
+            B.bnr_bn_relu_maxpool_fwd(self.z0, None, s0.X[..., :s0.c0], n, self.hs, self.ws_)
+        for i, st in enumerate(self.stages):
+            nxt = self.stages[i + 1] if i + 1 < len(self.stages) else None
+            st.forward(nxt.X[..., :nxt.c0] if nxt is not None else None, in_stats_done=(i == 0))
+        last = self.stages[-1]
+        h, w = self.hw[-1]
+        if not self.fused:
+            B.bnr_bn_stats(last.X, self.head_bn)
+        B.bnr_head_fwd(last.X, self.head_bn, self.wfc, self.bfc, self.labels, self.f, self.logits, self.dlogits,
+                       self.loss, n, h, w)
+
+    def backward(self):
+        n = self.n
+        last = self.stages[-1]
+        h, w = self.hw[-1]
+        if self.fused:
+            B.bnr_head_bwd(last.X, self.head_bn, self.wfc, self.f, self.dlogits, self.df, self.dwfc, self.dbfc,
+                           self.g5.dgamma, self.g5.dbeta, last.G, n, h, w, alpha=last.alpha, betap=last.betap)
+        else:
+            B.bnr_head_bwd(last.X, self.head_bn, self.wfc, self.f, self.dlogits, self.df, self.dwfc, self.dbfc,
+                           self.g5.dgamma, self.g5.dbeta, last.G, n, h, w)
+        for i in range(len(self.stages) - 1, -1, -1):
+            st = self.stages[i]
+            nxt = self.stages[i + 1] if i + 1 < len(self.stages) else None
+            st.backward(nxt.G[..., :nxt.c0] if nxt is not None else None)
+        s0 = self.stages[0]
+        dX = s0.G[..., :s0.c0]
+        c_in = self.ci
+        if self.fused:
+            B.bnr_maxpool_bn_bwd(self.s, self.stem_bn, dX, self.dy0, n, self.hs, self.ws_, self.g0.dgamma,
+                                 self.g0.dbeta)
+            B.bnr_stem_wgrad(self.img, c_in, B.grad_bn(self.dy0, self.s, self.stem_bn, self.g0.dgamma, self.g0.dbeta),
+                             self.dw0)
+        else:
+            B.bnr_maxpool_bn_bwd(self.z0, None, dX, self.dz0, n, self.hs, self.ws_)
+            B.bnr_reference_bn_relu(True, self.s, self.stem_bn, self.y0, gz=self.dz0, dy=self.dy0,
+                                    dgamma=self.g0.dgamma, dbeta=self.g0.dbeta, dx=self.dx0)
+            B.bnr_stem_wgrad(self.img, c_in, B.grad_dense(self.dx0), self.dw0)
 
     def step(self):
         self.forward()

@@ -97,9 +97,62 @@ def test_other_entry_points_validate(B):
                                      WS, 1 << 30, None)
     assert B.STATUS[r] == "BNR_ERR_NULL"          # no BN and no dx
     pool = B._lib_fns["bnr_avgpool2_fwd"]
-    assert B.STATUS[pool(1, 3, 4, 8, B.BNR_BF16, A, 8, A + 0x1000, None)] == "BNR_ERR_SHAPE"
+    assert B.STATUS[pool(1, 3, 4, 8, B.BNR_BF16, A, 8, A + 0x1000, 8, None)] == "BNR_ERR_SHAPE"
+    assert B.STATUS[pool(1, 4, 4, 8, B.BNR_BF16, A, 8, A + 0x1000, 4, None)] == "BNR_ERR_SHAPE"
     assert B.STATUS[B._lib_fns["bnr_hbm_copy"](A, A + 0x1000, 24, None)] == "BNR_ERR_SHAPE"
     assert B.STATUS[B._lib_fns["bnr_hbm_copy"](A, A + 0x8, 64, None)] == "BNR_ERR_ALIGN"
     a = B.RefArgs()
     assert B.STATUS[B._lib_fns["bnr_reference_path"](5, 0, ctypes.byref(d), ctypes.byref(a), WS, 1 << 30, None)] \
         == "BNR_ERR_UNSUPPORTED"
+
+
+def test_network_end_entry_points_validate(B):
+    f = B._lib_fns
+    sd = B.StemDesc(2, 30, 30, 3, B.BNR_BF16)
+    assert f["bnr_stem_workspace_size"](ctypes.byref(sd)) > 0
+    assert f["bnr_stem_workspace_size"](ctypes.byref(B.StemDesc(2, 30, 300, 3, B.BNR_BF16))) == 0
+    bn = B.BNStruct(None, None, A, A, A, 1e-5)
+    conv = f["bnr_stem_conv_fwd"]
+    for desc, status in ((B.StemDesc(2, 30, 30, 5, B.BNR_BF16), "BNR_ERR_UNSUPPORTED"),
+                         (B.StemDesc(2, 30, 257, 3, B.BNR_BF16), "BNR_ERR_UNSUPPORTED"),
+                         (B.StemDesc(0, 30, 30, 3, B.BNR_BF16), "BNR_ERR_SHAPE"),
+                         (B.StemDesc(2, 30, 30, 3, 9), "BNR_ERR_DTYPE")):
+        assert B.STATUS[conv(ctypes.byref(desc), A, A + 0x100000, A + 0x200000, ctypes.byref(bn), WS, 1 << 30,
+                             None)] == status
+    assert B.STATUS[conv(ctypes.byref(sd), A, A + 0x100000, A + 0x200000, ctypes.byref(bn), WS, 64, None)] \
+        == "BNR_ERR_WORKSPACE"
+    assert B.STATUS[conv(ctypes.byref(sd), A, A + 0x100000, A + 0x10, None, WS, 1 << 30, None)] == "BNR_ERR_ALIAS"
+    g = B.GradSrc(B.GRAD_AVGPOOL2, A, 64, None, None, 0, None, None, None)
+    assert B.STATUS[f["bnr_stem_wgrad"](ctypes.byref(sd), A, ctypes.byref(g), A + 0x10000, WS, 1 << 30, None)] \
+        == "BNR_ERR_UNSUPPORTED"
+    g = B.GradSrc(B.GRAD_DENSE, A, 60, None, None, 0, None, None, None)
+    assert B.STATUS[f["bnr_stem_wgrad"](ctypes.byref(sd), A, ctypes.byref(g), A + 0x10000, WS, 1 << 30, None)] \
+        == "BNR_ERR_SHAPE"
+    mp, mb = f["bnr_bn_relu_maxpool_fwd"], f["bnr_maxpool_bn_bwd"]
+    assert f["bnr_pool_workspace_size"](2, 112, 112, 64) > 0
+    assert B.STATUS[mp(2, 8, 8, 12, B.BNR_BF16, A, 16, None, A + 0x100000, 16, None, None, 0, None)] == "BNR_ERR_ALIGN"
+    assert B.STATUS[mp(2, 8, 8, 16, B.BNR_BF16, A, 16, None, A + 0x10, 16, None, None, 0, None)] == "BNR_ERR_ALIAS"
+    assert B.STATUS[mp(2, 8, 8, 16, B.BNR_BF16, A, 16, None, A + 0x100000, 16, ctypes.byref(bn), None, 0, None)] \
+        == "BNR_ERR_WORKSPACE"
+    assert B.STATUS[mb(2, 8, 8, 128, B.BNR_BF16, A, 128, None, A + 0x100000, 128, A + 0x200000, None, None, None, 0,
+                       None)] == "BNR_ERR_UNSUPPORTED"
+    assert B.STATUS[mb(2, 8, 8, 48, B.BNR_BF16, A, 48, None, A + 0x100000, 48, A + 0x200000, None, None, None, 0,
+                       None)] == "BNR_ERR_UNSUPPORTED"
+    assert B.STATUS[mb(2, 8, 300, 64, B.BNR_BF16, A, 64, None, A + 0x1000000, 64, A + 0x2000000, None, None, None, 0,
+                       None)] == "BNR_ERR_UNSUPPORTED"
+    full = B.BNStruct(A, A, A, A, A, 1e-5)
+    assert B.STATUS[mb(2, 8, 8, 64, B.BNR_BF16, A, 64, ctypes.byref(full), A + 0x100000, 64, A + 0x200000, None, None,
+                       WS, 1 << 30, None)] == "BNR_ERR_NULL"      # dgamma / dbeta required with a BN
+    hf, hb = f["bnr_head_fwd"], f["bnr_head_bwd"]
+    assert B.STATUS[hf(2, 7, 7, 64, 10, B.BNR_BF16, A, 64, ctypes.byref(full), A, A, None, A, A, A, A, None)] \
+        == "BNR_ERR_NULL"                                          # labels
+    assert B.STATUS[hf(2, 7, 7, 64, 0, B.BNR_BF16, A, 64, ctypes.byref(full), A, A, A, A, A, A, A, None)] \
+        == "BNR_ERR_SHAPE"
+    assert f["bnr_head_workspace_size"](2, 7, 7, 64) > 0
+    assert B.STATUS[hb(2, 7, 7, 64, 10, B.BNR_BF16, A, 64, ctypes.byref(full), A, A, A, A, A, A, A, A, A + 0x40, 64,
+                       None, None, WS, 1 << 30, None)] == "BNR_ERR_ALIAS"
+    assert B.STATUS[hb(2, 7, 7, 64, 10, B.BNR_BF16, A, 64, ctypes.byref(full), A, A, A, A, A, A, A, A, A + 0x100000,
+                       64, None, None, WS, 8, None)] == "BNR_ERR_WORKSPACE"
+    a = B.BnReluRefArgs()
+    assert B.STATUS[f["bnr_reference_bn_relu"](0, 100, 16, B.BNR_BF16, ctypes.byref(a), WS, 1 << 30, None)] \
+        == "BNR_ERR_SHAPE"                                         # x_ldc 0
