@@ -10,7 +10,7 @@ headline value), fused_no_icf (fission/fusion inside composite layers only)
 and unfused (the reference layer chain).
 
 Prints one JSON line (rank 0).  Options: --gpus (1 only), --steps, --warmup,
---workload {dense_block,bottleneck,single_layer,resnet_stack}, --no-graph,
+--workload {dense_block,bottleneck,single_layer,resnet_stack,densenet121}, --no-graph,
 --no-cpu-baseline, --profile-only (steps only, for rocprofv3 runs),
 --calib-copy-mb M (with --profile-only: one bnr_hbm_copy of M MiB after the
 steps, the byte-counter calibration reference).
@@ -41,6 +41,7 @@ WORKLOADS = {
     "bottleneck": ("Bottleneck", "bottleneck", dict(n=32)),
     "single_layer": ("SingleLayer", "single_layer", dict()),
     "resnet_stack": ("ResNetStack", "resnet_stack", dict(n=128)),
+    "densenet121": ("DenseNet", "densenet", dict(n=128)),
 }
 
 
@@ -166,7 +167,8 @@ CLASS_SOURCES = {"conv1x1": ["conv1x1.hip", "conv_rows.hip"], "conv3x3": ["conv3
                  "wgrad1x1": ["conv_wgrad.hip"], "wgrad3x3": ["conv_wgrad.hip"],
                  "stats_sweep": ["bn_kernels.hip"], "elementwise": ["bn_kernels.hip"],
                  "stats_combine": ["bn_kernels.hip"], "splitk_sum": ["bn_kernels.hip"], "pool": ["bn_kernels.hip"],
-                 "copy": ["bn_kernels.hip"], "weight_pack": ["conv_rows.hip"]}
+                 "copy": ["bn_kernels.hip"], "weight_pack": ["conv_rows.hip"], "stem_conv": ["net_ends.hip"],
+                 "stem_wgrad": ["net_ends.hip"], "maxpool": ["net_ends.hip"], "head": ["net_ends.hip"]}
 
 
 def kernel_class(name):
@@ -189,7 +191,10 @@ def kernel_class(name):
             "k_stats_combine_one": "stats_combine", "k_stats_combine1": "stats_combine",
             "k_stats_combine2": "stats_combine", "k_sum_partials1": "splitk_sum", "k_sum_partials2": "splitk_sum",
             "k_avgpool2": "pool", "k_avgpool2_bwd": "pool", "k_copy16": "copy",
-            "k_pack_weights": "weight_pack"}.get(k)
+            "k_pack_weights": "weight_pack", "k_stem_conv": "stem_conv", "k_stem_conv_f32": "stem_conv",
+            "k_stem_wgrad": "stem_wgrad", "k_stem_wgrad_f32": "stem_wgrad", "k_maxpool_fwd": "maxpool",
+            "k_maxpool_bwd": "maxpool", "k_head_pool": "head", "k_fc_gemm": "head", "k_softmax_ce": "head",
+            "k_colsum": "head", "k_head_bn_bwd": "head"}.get(k)
 
 
 def sources_sha(cls):
@@ -322,6 +327,12 @@ def cpu_baseline(args):
         t0 = time.perf_counter()
         _, c = OC.bottleneck_fwd(d["x"], d["p"]["w2"].shape[3], d["p"], d["eps"], rnd)
         OC.bottleneck_bwd(c, d["dy"].astype(np.float64), rnd)
+    elif args.workload == "densenet121":
+        n = 1                     # bounded sample: one image of the whole network (per-image cost is batch independent)
+        d = synth.densenet(seed=0, n=n)
+        t0 = time.perf_counter()
+        _, c = OC.densenet_fwd(d, d["eps"], rnd)
+        OC.densenet_bwd(c, rnd)
     elif args.workload == "resnet_stack":
         n = 4                     # bounded sample: the stack at batch 4 (per-image cost is batch independent)
         d = synth.resnet_stack(seed=0, n=n)
@@ -402,8 +413,12 @@ def main():
                                 "bottleneck": "DenseNet-121 bottleneck layer 256->128->32 + concat",
                                 "single_layer": "BN-ReLU-CONV1x1 64->32",
                                 "resnet_stack": "ResNet-50 conv2_x: 3 bottleneck blocks 256->64->64->256 with "
-                                                "identity shortcuts"}[args.workload],
-                   "global_batch": fused["images"] if fused else unf["images"], "image_hw": 56,
+                                                "identity shortcuts",
+                                "densenet121": "DenseNet-121 (7x7/2 CONV + 3x3/2 max pooling, dense blocks of "
+                                               "6/12/24/16 layers, growth 32, compression-1/2 transitions, "
+                                               "1000-way FC + softmax cross-entropy)"}[args.workload],
+                   "global_batch": fused["images"] if fused else unf["images"],
+                   "image_hw": 224 if args.workload == "densenet121" else 56,
                    "graph": not args.no_graph},
         "unfused": {"images_per_s": unf["images"] / (unf["ms"] / 1e3), "ms_per_step": unf["ms"]} if unf else None,
         "fused_no_icf": ({"images_per_s": noicf["images"] / (noicf["ms"] / 1e3), "ms_per_step": noicf["ms"],

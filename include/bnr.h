@@ -412,7 +412,8 @@ size_t bnr_head_workspace_size(int32_t n, int32_t h, int32_t w, int32_t c);
  *   bfc [classes]; labels [n] int32 (device; a label outside [0, classes)
  *   makes the loss NaN).  Outputs (float32, device): f [n][c] pooled
  *   features, logits [n][classes], dlogits = (softmax - onehot)/n, and
- *   loss[0] = mean over the batch of -log softmax(logits)[label]. */
+ *   loss [1 + n]: loss[1 + r] = -log softmax(logits[r])[label[r]] and
+ *   loss[0] their mean over the batch. */
 bnr_status bnr_head_fwd(int32_t n, int32_t h, int32_t w, int32_t c, int32_t classes, bnr_dtype dtype,
                         const void *x, int32_t x_ldc, const bnr_bn *x_bn, const void *wfc, const float *bfc,
                         const int32_t *labels, float *f, float *logits, float *dlogits, float *loss,

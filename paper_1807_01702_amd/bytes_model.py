@@ -117,47 +117,115 @@ def bottleneck(m, ci, width, k, e):
     return {"fused": f.total, "unfused": u.total}
 
 
-def dense_block(m, c0, layers, width, k, trans_out, e):
-    f, u = _Acc(), _Acc()
+def _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode, in_sweep=True):
+    """Forward of a dense block (+ transition) in mode 'icf' (fused with
+    inter-composite-layer fusion), 'fused' or 'unfused'; in_sweep (icf): the
+    block input's statistics need their own sweep."""
     c = c0
+    if mode == "icf" and in_sweep:
+        a += m * c0 * e                                          # the one statistics sweep (block input)
     for _ in range(layers):
-        _unit_fused_fwd(f, m, c, width, 1, e, True)
-        _unit_fused_fwd(f, m, width, k, 3, e, False)
-        _unit_ref_fwd(u, m, c, width, 1, e)
-        _unit_ref_fwd(u, m, width, k, 3, e)
+        if mode == "unfused":
+            _unit_ref_fwd(a, m, c, width, 1, e)
+            _unit_ref_fwd(a, m, width, k, 3, e)
+        else:
+            _unit_fused_fwd(a, m, c, width, 1, e, mode == "fused")
+            _unit_fused_fwd(a, m, width, k, 3, e, False)
         c += k
-    ct = c
-    _unit_fused_fwd(f, m, ct, trans_out, 1, e, True)
-    _unit_ref_fwd(u, m, ct, trans_out, 1, e)
-    for a in (f, u):
+    if trans_out:
+        if mode == "unfused":
+            _unit_ref_fwd(a, m, c, trans_out, 1, e)
+        else:
+            _unit_fused_fwd(a, m, c, trans_out, 1, e, mode == "fused")
         a += m * trans_out * e + m // 4 * trans_out * e          # avgpool forward
-    # backward: transition first
-    _unit_fused_bwd(f, m, ct, trans_out, 1, e, m // 4 * trans_out * e, "write")
-    u += m // 4 * trans_out * e + m * trans_out * e              # unfused: materialised pooling gradient
-    _unit_ref_bwd(u, m, ct, trans_out, 1, e, m * trans_out * e, False)
+    return c
+
+
+def _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode):
+    """Backward of _block_fwd; without a transition the block's gradient
+    buffer was written by the BN that reads the whole block (the head)."""
+    ct = c0 + layers * k
+    if trans_out:
+        if mode == "icf":
+            _unit_split_bwd(a, m, ct, trans_out, 1, e, m // 4 * trans_out * e, False)
+        elif mode == "fused":
+            _unit_fused_bwd(a, m, ct, trans_out, 1, e, m // 4 * trans_out * e, "write")
+        else:
+            a += m // 4 * trans_out * e + m * trans_out * e      # unfused: materialised pooling gradient
+            _unit_ref_bwd(a, m, ct, trans_out, 1, e, m * trans_out * e, False)
     for layer in reversed(range(layers)):
         c = c0 + layer * k
-        _unit_fused_bwd(f, m, width, k, 3, e, m * k * e, None)
-        _unit_fused_bwd(f, m, c, width, 1, e, 2 * m * width * e, "accumulate")
-        _unit_ref_bwd(u, m, width, k, 3, e, m * k * e, False)
-        _unit_ref_bwd(u, m, c, width, 1, e, m * width * e, True)
-    # with inter-composite-layer fusion
-    i = _Acc()
-    i += m * c0 * e                                              # the one statistics sweep (block input)
-    c = c0
-    for _ in range(layers):
-        _unit_fused_fwd(i, m, c, width, 1, e, False)
-        _unit_fused_fwd(i, m, width, k, 3, e, False)
-        c += k
-    _unit_fused_fwd(i, m, ct, trans_out, 1, e, False)
-    i += m * trans_out * e + m // 4 * trans_out * e              # avgpool forward
-    _unit_split_bwd(i, m, ct, trans_out, 1, e, m // 4 * trans_out * e, False)
-    for layer in reversed(range(layers)):
-        c = c0 + layer * k
-        _unit_fused_bwd(i, m, width, k, 3, e, 2 * m * k * e, None)   # summed gradient + slice on load
-        _unit_split_bwd(i, m, c, width, 1, e, 2 * m * width * e, True)
-    i += 3 * m * c0 * e                                          # block-input gradient: read sum, x; write
-    return {"fused": i.total, "fused_no_icf": f.total, "unfused": u.total}
+        if mode == "icf":
+            _unit_fused_bwd(a, m, width, k, 3, e, 2 * m * k * e, None)     # summed gradient + slice on load
+            _unit_split_bwd(a, m, c, width, 1, e, 2 * m * width * e, True)
+        elif mode == "fused":
+            _unit_fused_bwd(a, m, width, k, 3, e, m * k * e, None)
+            _unit_fused_bwd(a, m, c, width, 1, e, 2 * m * width * e, "accumulate")
+        else:
+            _unit_ref_bwd(a, m, width, k, 3, e, m * k * e, False)
+            _unit_ref_bwd(a, m, c, width, 1, e, m * width * e, True)
+    if mode == "icf":
+        a += 3 * m * c0 * e                                      # block-input gradient: read sum, x; write
+
+
+def dense_block(m, c0, layers, width, k, trans_out, e):
+    out = {}
+    for mode in ("icf", "fused", "unfused"):
+        a = _Acc()
+        _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode)
+        _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode)
+        out[mode] = a.total
+    return {"fused": out["icf"], "fused_no_icf": out["fused"], "unfused": out["unfused"]}
+
+
+def densenet(n, hw, c_in, c_stem, blocks, classes, e):
+    """Whole DenseNet step.  blocks: [(c0, layers, width, k, trans_out or 0)].
+    Fused: first CONV with statistics epilogue; BN-ReLU-max pooling reading s
+    and writing block 1's input with its statistics; blocks with ICF (blocks
+    after the first sweep their pooled input once for statistics); the head
+    reads the last block (BN + ReLU + pooling) and its backward writes the
+    summed gradient; max-pooling backward reads s and the block-1 input
+    gradient and writes dy; the first CONV's weight gradient reads the image,
+    dy and s.  Unfused: two-pass statistics, normalise and ReLU sweeps around
+    a plain max pooling, materialised pooling / ReLU / BN input gradients."""
+    ho = (hw - 1) // 2 + 1
+    hp = (ho - 1) // 2 + 1
+    S0 = n * ho * ho * c_stem * e
+    Sp = n * hp * hp * c_stem * e
+    img = n * hw * hw * 4 * e
+    w0 = 49 * c_in * c_stem
+    out = {}
+    for mode in ("icf", "unfused"):
+        a = _Acc()
+        a += img + w0 * e + S0                                   # first CONV (statistics in its epilogue if fused)
+        if mode == "icf":
+            a += S0 + Sp                                         # BN-ReLU-max pooling (+ block-input statistics)
+        else:
+            a += 6 * S0 + S0 + Sp                                # stats (2), normalise (2), ReLU (2), pooling
+        h, dims = hp, []
+        for i, (c0, layers, width, k, to) in enumerate(blocks):
+            m = n * h * h
+            ct = _block_fwd(a, m, c0, layers, width, k, to, e, mode, in_sweep=i > 0)
+            dims.append(m)
+            if to:
+                h //= 2
+        S4 = dims[-1] * ct * e
+        if mode == "unfused":
+            a += S4                                              # head BN statistics sweep
+        a += S4 + ct * classes * e                               # head forward: x (BN + ReLU + pooling), FC weights
+        a += ct * classes * (e + 4)                              # FC backward: weights, dW
+        a += (2 if mode == "icf" else 3) * S4                    # head BN backward (summed form / sums + dx)
+        for (c0, layers, width, k, to), m in reversed(list(zip(blocks, dims))):
+            _block_bwd(a, m, c0, layers, width, k, to, e, mode)
+        if mode == "icf":
+            a += 2 * S0 + Sp                                     # pooling backward: s, block-input gradient; dy
+            a += img + 2 * S0 + w0 * 4                           # first-CONV wgrad: image, dy, s; dW
+        else:
+            a += 2 * S0 + Sp                                     # plain pooling backward: z, gradient; dz
+            a += 8 * S0                                          # ReLU backward (3), BN sums (2), BN dx (3)
+            a += img + S0 + w0 * 4                               # first-CONV wgrad: image, dx; dW
+        out[mode] = a.total
+    return {"fused": out["icf"], "unfused": out["unfused"]}
 
 
 def resnet_stack(m, c, width, blocks, e):
@@ -200,6 +268,11 @@ def for_workload(name, data):
     if name == "resnet_stack":
         n, h, w, c = data["x"].shape
         return resnet_stack(n * h * w, c, data["blocks"][0]["w1"].shape[3], len(data["blocks"]), e)
+    if name == "densenet121":
+        n, hw, _, c_in = data["img"].shape
+        blocks = [(b["c0"], len(b["cpls"]), b["cpls"][0]["w1"].shape[3], b["cpls"][0]["w2"].shape[3],
+                   b["trans"]["w"].shape[3] if b["trans"] is not None else 0) for b in data["blocks"]]
+        return densenet(n, hw, c_in, data["stem"]["w"].shape[3], blocks, data["head"]["w"].shape[1], e)
     n, h, w, c0 = data["x"].shape
     cp = data["cpls"]
     return dense_block(n * h * w, c0, len(cp), cp[0]["w1"].shape[3], cp[0]["w2"].shape[3],

@@ -657,93 +657,99 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
 }
 
 // Small float32 GEMM for the FC layer: out[i][j] = sum_k A(i,k) B(k,j) (+ bias[j]),
-// A(i,k) = a[i*sai + k*sak] (float32), B(k,j) = b[k*sbk + j*sbj] (TB).  64x64
-// output tiles, K in chunks of 16 staged in LDS, 4x4 outputs per thread, k
-// summed in order (deterministic).
+// A(i,k) = a[i*sai + k*sak] (float32), B(k,j) = b[k*sbk + j*sbj] (TB).  16x64
+// output tiles (enough workgroups for the 128-image batch), K in chunks of 64
+// staged in LDS with the operand's contiguous index running across the
+// threads (coalesced for either orientation), 4 outputs per thread, k summed
+// in order (deterministic).
 template <typename TB>
 __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const float *__restrict__ a, int64_t sai,
                                                       int64_t sak, const TB *__restrict__ b, int64_t sbk,
                                                       int64_t sbj, const float *__restrict__ bias,
                                                       float *__restrict__ out)
 {
-    __shared__ float As[16][64 + 4], Bs[16][64 + 4];
+    constexpr int BM = 16, BN = 64, BK = 64;
+    __shared__ float As[BK][BM + 1], Bs[BK][BN + 4];
     const int tid = threadIdx.x, tr = tid / 16, tc = tid % 16;
-    const int i0 = blockIdx.y * 64, j0 = blockIdx.x * 64;
-    float acc[4][4];
-    #pragma unroll
-    for (int u = 0; u < 4; u++)
+    const int i0 = blockIdx.y * BM, j0 = blockIdx.x * BN;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int k0 = 0; k0 < K; k0 += BK) {
         #pragma unroll
-        for (int v = 0; v < 4; v++) acc[u][v] = 0.f;
-    for (int k0 = 0; k0 < K; k0 += 16) {
-        for (int e = tid; e < 16 * 64; e += kThreads) {
-            const int kk = e / 64, ii = e % 64;
+        for (int u = 0; u < BK * BM / kThreads; u++) {
+            const int e = tid + u * kThreads;
+            const int kk = sak == 1 ? e % BK : e / BM, ii = sak == 1 ? e / BK : e % BM;
             const int gi = i0 + ii, gk = k0 + kk;
             As[kk][ii] = gi < M && gk < K ? a[gi * sai + gk * sak] : 0.f;
-            const int gj = j0 + ii;
+        }
+        #pragma unroll
+        for (int u = 0; u < BK * BN / kThreads; u++) {
+            const int e = tid + u * kThreads;
+            const int kk = sbk == 1 ? e % BK : e / BN, jj = sbk == 1 ? e / BK : e % BN;
+            const int gj = j0 + jj, gk = k0 + kk;
             float bv = 0.f;
             if (gj < N && gk < K) {
                 if constexpr (sizeof(TB) == 2) bv = bf2f(b[gk * sbk + gj * sbj]);
                 else bv = b[gk * sbk + gj * sbj];
             }
-            Bs[kk][ii] = bv;
+            Bs[kk][jj] = bv;
         }
         __syncthreads();
-        #pragma unroll
-        for (int kk = 0; kk < 16; kk++)
+        #pragma unroll 16
+        for (int kk = 0; kk < BK; kk++) {
+            const float av = As[kk][tr];
             #pragma unroll
-            for (int u = 0; u < 4; u++)
-                #pragma unroll
-                for (int v = 0; v < 4; v++)
-                    acc[u][v] = __builtin_fmaf(As[kk][tr + 16 * u], Bs[kk][tc + 16 * v], acc[u][v]);
+            for (int v = 0; v < 4; v++) acc[v] = __builtin_fmaf(av, Bs[kk][tc + 16 * v], acc[v]);
+        }
         __syncthreads();
     }
     #pragma unroll
-    for (int u = 0; u < 4; u++)
-        #pragma unroll
-        for (int v = 0; v < 4; v++) {
-            const int gi = i0 + tr + 16 * u, gj = j0 + tc + 16 * v;
-            if (gi < M && gj < N) out[(int64_t)gi * N + gj] = acc[u][v] + (bias ? bias[gj] : 0.f);
-        }
+    for (int v = 0; v < 4; v++) {
+        const int gi = i0 + tr, gj = j0 + tc + 16 * v;
+        if (gi < M && gj < N) out[(int64_t)gi * N + gj] = acc[v] + (bias ? bias[gj] : 0.f);
+    }
 }
 
-// Softmax cross-entropy of logits [n][K] against labels, mean over the batch,
-// and its gradient dlogits = (softmax - onehot) / n.  One workgroup walks the
-// rows in order (deterministic loss); a label outside [0, K) gives a NaN loss.
+// Softmax cross-entropy of logits [n][K] against labels and its gradient
+// dlogits = (softmax - onehot) / n: one workgroup per row, which writes the
+// row's loss to loss[1 + r]; k_loss_mean then adds the rows in order
+// (deterministic) into loss[0].  A label outside [0, K) gives a NaN loss.
 __global__ __launch_bounds__(kThreads) void k_softmax_ce(int n, int K, const float *__restrict__ logits,
                                                          const int32_t *__restrict__ labels,
                                                          float *__restrict__ dlogits, float *__restrict__ loss)
 {
     __shared__ float red[kThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    double total = 0.0;
-    auto block_reduce = [&](float v, bool is_max) -> float {
-        for (int o = 32; o > 0; o >>= 1) {
-            const float u = __shfl_xor(v, o, 64);
-            v = is_max ? fmaxf(v, u) : v + u;
-        }
-        __syncthreads();
-        if (lane == 0) red[wave] = v;
-        __syncthreads();
-        float r = red[0];
-        for (int k = 1; k < kThreads / 64; k++) r = is_max ? fmaxf(r, red[k]) : r + red[k];
-        return r;
-    };
-    for (int r = 0; r < n; r++) {
-        const float *z = logits + (int64_t)r * K;
-        float mx = -INFINITY;
-        for (int j = tid; j < K; j += kThreads) mx = fmaxf(mx, z[j]);
-        mx = block_reduce(mx, true);
-        float se = 0.f;
-        for (int j = tid; j < K; j += kThreads) se += expf(z[j] - mx);
-        se = block_reduce(se, false);
-        const int lab = labels[r];
-        const bool ok = lab >= 0 && lab < K;
-        const float inv = 1.0f / se, invn = 1.0f / (float)n;
-        for (int j = tid; j < K; j += kThreads)
-            dlogits[(int64_t)r * K + j] = (expf(z[j] - mx) * inv - (j == lab ? 1.f : 0.f)) * invn;
-        if (tid == 0) total += ok ? (double)logf(se) + (double)mx - (double)z[lab] : (double)NAN;
-    }
-    if (tid == 0) loss[0] = (float)(total / (double)n);
+    const int r = blockIdx.x;
+    const float *z = logits + (int64_t)r * K;
+    float mx = -INFINITY;
+    for (int j = tid; j < K; j += kThreads) mx = fmaxf(mx, z[j]);
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    if (lane == 0) red[wave] = mx;
+    __syncthreads();
+    mx = red[0];
+    for (int w = 1; w < kThreads / 64; w++) mx = fmaxf(mx, red[w]);
+    __syncthreads();
+    float se = 0.f;
+    for (int j = tid; j < K; j += kThreads) se += expf(z[j] - mx);
+    se = wave_sum(se);
+    if (lane == 0) red[wave] = se;
+    __syncthreads();
+    se = red[0];
+    for (int w = 1; w < kThreads / 64; w++) se += red[w];
+    const int lab = labels[r];
+    const bool ok = lab >= 0 && lab < K;
+    const float inv = 1.0f / se, invn = 1.0f / (float)n;
+    for (int j = tid; j < K; j += kThreads)
+        dlogits[(int64_t)r * K + j] = (expf(z[j] - mx) * inv - (j == lab ? 1.f : 0.f)) * invn;
+    if (tid == 0) loss[1 + r] = ok ? logf(se) + mx - z[lab] : NAN;
+}
+
+__global__ __launch_bounds__(64) void k_loss_mean(int n, float *__restrict__ loss)
+{
+    if (threadIdx.x != 0) return;
+    double t = 0.0;
+    for (int r = 0; r < n; r++) t += (double)loss[1 + r];
+    loss[0] = (float)(t / (double)n);
 }
 
 // db[j] = sum_n dlogits[n][j] (rows in order).
@@ -964,15 +970,16 @@ hipError_t launch_head_fwd(int dtype, const HeadParams &p, hipStream_t s)
     const int nt = p.n * (p.c / vec);
     if (dtype == DT_BF16) hipLaunchKernelGGL(k_head_pool<bf16_t>, dim3((unsigned)ceil_div(nt, kThreads)), dim3(kThreads), 0, s, p);
     else hipLaunchKernelGGL(k_head_pool<float>, dim3((unsigned)ceil_div(nt, kThreads)), dim3(kThreads), 0, s, p);
-    dim3 grid((unsigned)ceil_div(p.classes, 64), (unsigned)ceil_div(p.n, 64));
+    dim3 grid((unsigned)ceil_div(p.classes, 64), (unsigned)ceil_div(p.n, 16));
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_fc_gemm<bf16_t>, grid, dim3(kThreads), 0, s, p.n, p.classes, p.c, p.f, (int64_t)p.c,
                            (int64_t)1, (const bf16_t *)p.wfc, (int64_t)p.classes, (int64_t)1, p.bfc, p.logits);
     else
         hipLaunchKernelGGL(k_fc_gemm<float>, grid, dim3(kThreads), 0, s, p.n, p.classes, p.c, p.f, (int64_t)p.c,
                            (int64_t)1, (const float *)p.wfc, (int64_t)p.classes, (int64_t)1, p.bfc, p.logits);
-    hipLaunchKernelGGL(k_softmax_ce, dim3(1), dim3(kThreads), 0, s, p.n, p.classes, p.logits, p.labels, p.dlogits,
-                       p.loss);
+    hipLaunchKernelGGL(k_softmax_ce, dim3((unsigned)p.n), dim3(kThreads), 0, s, p.n, p.classes, p.logits, p.labels,
+                       p.dlogits, p.loss);
+    hipLaunchKernelGGL(k_loss_mean, dim3(1), dim3(64), 0, s, p.n, p.loss);
     return hipGetLastError();
 }
 
@@ -984,7 +991,7 @@ hipError_t launch_head_bwd_fc(int dtype, const HeadParams &p, hipStream_t s)
     TraceScope tr(KC_SMALL, KID_HEAD, s, 4.0 * ((double)p.n * p.classes + 2.0 * p.n * p.c + (double)p.c * p.classes),
                   4.0 * p.n * p.c * p.classes);
     // df = dlogits W^T: A = dlogits [n][K], B(k=j, col=c) = W[c][j]
-    dim3 g1((unsigned)ceil_div(p.c, 64), (unsigned)ceil_div(p.n, 64));
+    dim3 g1((unsigned)ceil_div(p.c, 64), (unsigned)ceil_div(p.n, 16));
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_fc_gemm<bf16_t>, g1, dim3(kThreads), 0, s, p.n, p.c, p.classes, p.dlogits,
                            (int64_t)p.classes, (int64_t)1, (const bf16_t *)p.wfc, (int64_t)1, (int64_t)p.classes,
@@ -994,7 +1001,7 @@ hipError_t launch_head_bwd_fc(int dtype, const HeadParams &p, hipStream_t s)
                            (int64_t)p.classes, (int64_t)1, (const float *)p.wfc, (int64_t)1, (int64_t)p.classes,
                            (const float *)nullptr, p.df);
     // dW = f^T dlogits: A(i=c, k=n) = f[n][c], B(k=n, j) = dlogits[n][j]
-    dim3 g2((unsigned)ceil_div(p.classes, 64), (unsigned)ceil_div(p.c, 64));
+    dim3 g2((unsigned)ceil_div(p.classes, 64), (unsigned)ceil_div(p.c, 16));
     hipLaunchKernelGGL(k_fc_gemm<float>, g2, dim3(kThreads), 0, s, p.c, p.classes, p.n, p.f, (int64_t)1,
                        (int64_t)p.c, p.dlogits, (int64_t)p.classes, (int64_t)1, (const float *)nullptr, p.dwfc);
     hipLaunchKernelGGL(k_colsum, dim3((unsigned)ceil_div(p.classes, kThreads)), dim3(kThreads), 0, s, p.n, p.classes,

@@ -424,7 +424,7 @@ class DenseNet:
         f32 = dict(dtype=torch.float32, device=dev)
         self.f = torch.empty((n, C), **f32)
         self.logits, self.dlogits = torch.empty((n, K), **f32), torch.empty((n, K), **f32)
-        self.loss = torch.empty(1, **f32)
+        self.loss = torch.empty(1 + n, **f32)
         self.df = torch.empty((n, C), **f32)
         self.dwfc, self.dbfc = torch.empty((C, K), **f32), torch.empty(K, **f32)
         self.g5 = _Grads(C, dev)

@@ -235,11 +235,13 @@ def test_head(bf16):
     bn = B.BN(f32dev(gamma), f32dev(beta), 1e-5, mean=f32dev(mean32), rstd=f32dev(rstd32))
     xt, wt = dev(x, bf16), dev(wfc, bf16)
     f32 = dict(dtype=torch.float32, device="cuda")
-    ft, lg, dl, ls = torch.empty((n, c), **f32), torch.empty((n, K), **f32), torch.empty((n, K), **f32), torch.empty(1, **f32)
+    ft, lg, dl, ls = torch.empty((n, c), **f32), torch.empty((n, K), **f32), torch.empty((n, K), **f32), torch.empty(1 + n, **f32)
     lab = torch.from_numpy(labels).cuda()
     B.bnr_head_fwd(xt, bn, wt, f32dev(bfc), lab, ft, lg, dl, ls, n, h, w)
     torch.cuda.synchronize()
     assert abs(float(host(ls)[0]) - loss) <= 1e-5 * abs(loss)
+    rows = host(ls)[1:]
+    assert np.all(np.isfinite(rows)) and abs(rows.mean() - loss) <= 1e-5 * abs(loss)
     assert_close("f", host(ft), f, 1e-5)
     assert_close("logits", host(lg), logits, 1e-5)
     assert_close("dlogits", host(dl), dlogits, 1e-5)
