@@ -230,8 +230,9 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__res
 
 // --------------------------------------------------------------------------
 // Element-wise passes over [m][C] views with per-channel parameters (MODE
-// and ACC are template arguments so each row batch issues all its loads,
-// including the accumulate read, before any arithmetic).
+// and ACC are template arguments so each row batch of four rows issues all
+// its loads, including the accumulate read, before any arithmetic; the
+// operands are streamed once, so the loads are non-temporal).
 //   EW_DX      : out = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m)  [+ out]
 //   EW_APPLY   : out = gamma*(x-mean)*rstd + beta                  (unfused BN)
 //   EW_RELU    : out = max(x, 0)                                   (unfused ReLU)
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
     const float *__restrict__ mean, const float *__restrict__ rstd, const float *__restrict__ dgamma,
     const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int64_t rows_per_block)
 {
-    constexpr int VEC = Elem<T>::VEC, U = 2;
+    constexpr int VEC = Elem<T>::VEC, U = 4;
     constexpr bool TWO = MODE == EW_DX || MODE == EW_RELUBWD || MODE == EW_BNADDRELU || MODE == EW_ADDRELU ||
                          MODE == EW_SPLITDX;
     const int cvec = C / VEC;
@@ -330,17 +331,17 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
         #pragma unroll
         for (int u = 0; u < U; u++) {
             const int64_t rr = r + u * ry;
-            vx[u] = ldg16(x + rr * x_ldc + c0);
-            v2[u] = TWO ? ldg16(x2 + rr * x2_ldc + c0) : vx[u];
-            vo[u] = ACC ? ldg16(out + rr * out_ldc + c0) : vx[u];
+            vx[u] = ldg16_stream(x + rr * x_ldc + c0);
+            v2[u] = TWO ? ldg16_stream(x2 + rr * x2_ldc + c0) : vx[u];
+            vo[u] = ACC ? ldg16_stream(out + rr * out_ldc + c0) : vx[u];
         }
         #pragma unroll
         for (int u = 0; u < U; u++) stg16(out + (r + u * ry) * out_ldc + c0, row(vx[u], v2[u], vo[u]));
     }
     for (; r < r1; r += ry) {
-        const vec16 vx = ldg16(x + r * x_ldc + c0);
-        const vec16 v2 = TWO ? ldg16(x2 + r * x2_ldc + c0) : vx;
-        const vec16 vo = ACC ? ldg16(out + r * out_ldc + c0) : vx;
+        const vec16 vx = ldg16_stream(x + r * x_ldc + c0);
+        const vec16 v2 = TWO ? ldg16_stream(x2 + r * x2_ldc + c0) : vx;
+        const vec16 vo = ACC ? ldg16_stream(out + r * out_ldc + c0) : vx;
         stg16(out + r * out_ldc + c0, row(vx, v2, vo));
     }
 }
@@ -622,9 +623,10 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
         (mode == EW_SPLITDX && (!rstd || !mean || !dgamma || !dbeta)) ||
         ((mode == EW_APPLY || mode == EW_BNADDRELU) && (!gamma || !beta || !mean || !rstd)))
         return hipErrorInvalidValue;
+    // eight rows per thread: two four-row batches in flight per thread
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
-    const int64_t R = stats_row_blocks(m, C, dtype) * 4;
-    const int64_t rpb = ceil_div(m, R);
+    const int vb = (int)(C / stats_vec(dtype) < kStatsMaxVec ? C / stats_vec(dtype) : kStatsMaxVec);
+    const int64_t rpb = (int64_t)(kThreads / vb) * 8;
     dim3 grid((unsigned)ceil_div(m, rpb), (unsigned)cb);
     const double sweeps = mode == EW_DX || mode == EW_SPLITDX ? 3.0 + (accumulate ? 1.0 : 0.0) : (two ? 3.0 : 2.0);
     TraceScope tr(KC_SWEEP, KID_ELEMENTWISE, s, sweeps * (double)m * C * (dtype == DT_BF16 ? 2 : 4), 0.0);

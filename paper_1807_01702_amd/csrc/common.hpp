@@ -58,6 +58,13 @@ template <> struct Elem<bf16_t> {
 };
 
 __device__ __forceinline__ vec16 ldg16(const void *p) { return *reinterpret_cast<const vec16 *>(p); }
+// Streaming load of data read once (non-temporal: no reuse expected in the caches).
+__device__ __forceinline__ vec16 ldg16_stream(const void *p) {
+    const vec16 *s = reinterpret_cast<const vec16 *>(p);
+    vec16 v;
+    for (int k = 0; k < 4; k++) v.u[k] = __builtin_nontemporal_load(&s->u[k]);
+    return v;
+}
 __device__ __forceinline__ void stg16(void *p, const vec16 &v) { *reinterpret_cast<vec16 *>(p) = v; }
 __device__ __forceinline__ vec16 zero16() { vec16 v; v.u[0] = v.u[1] = v.u[2] = v.u[3] = 0; return v; }
 
