@@ -13,7 +13,13 @@ Prints one JSON line (rank 0).  Options: --gpus (1 only), --steps, --warmup,
 --workload {dense_block,bottleneck,single_layer,resnet_stack,densenet121}, --no-graph,
 --no-cpu-baseline, --profile-only (steps only, for rocprofv3 runs),
 --calib-copy-mb M (with --profile-only: one bnr_hbm_copy of M MiB after the
-steps, the byte-counter calibration reference).
+steps, the byte-counter calibration reference), --only VARIANT, --no-ablation
+(skip the unfused_rcf / unfused_rcf_mvf endpoints).
+
+Counter summaries (no GPU needed): --summarize-pmc (per-class bytes of the
+dominant-kernel roofline), --summarize-step-bytes FETCH_DIR WRITE_DIR (HBM bytes
+per step of a profile-only run), --summarize-mfma PMC_DIR (matrix-core rate and
+busy fraction per kernel class), --summarize-trace (rocprofv3 --stats tables).
 
 HBM traffic of the dominant kernel (`roofline.traffic`): two rocprofv3
 counter runs of the profile-only command, one with FETCH_SIZE and one with
@@ -54,7 +60,11 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true")
-    ap.add_argument("--only", choices=["fused", "fused_no_icf", "unfused"], default=None)
+    ap.add_argument("--only", choices=["fused", "fused_no_icf", "unfused", "unfused_rcf", "unfused_rcf_mvf"],
+                    default=None)
+    ap.add_argument("--no-ablation", action="store_true")
+    ap.add_argument("--summarize-step-bytes", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None)
+    ap.add_argument("--summarize-mfma", metavar="PMC_DIR", default=None)
     ap.add_argument("--calib-copy-mb", type=int, default=0)
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None)
     ap.add_argument("--summarize-trace", nargs=2, metavar=("KERNEL_STATS_CSV", "STEPS"), default=None)
@@ -70,6 +80,11 @@ def build_workloads(args, torch):
     variants = [("fused", dict(fused=True)), ("unfused", dict(fused=False))]
     if args.workload == "dense_block":          # fused = BNFF + inter-composite-layer fusion; BNFF alone beside it
         variants.insert(1, ("fused_no_icf", dict(fused=True, icf=False)))
+    if args.workload in ("dense_block", "resnet_stack", "densenet121") and not args.no_ablation:
+        # the paper's intermediate endpoints (Sec. 5): ReLU-CONV fusion, then + mean/variance fusion
+        from paper_1807_01702_amd import bnr as B
+        variants += [("unfused_rcf", dict(fused=False, ref_mode=B.MODE_RCF)),
+                     ("unfused_rcf_mvf", dict(fused=False, ref_mode=B.MODE_RCF_MVF))]
     out = {}
     for name, kw in variants:
         if args.only and args.only != name:
@@ -246,6 +261,66 @@ def summarize_pmc(fetch_dir, write_dir, workload, copy_mb):
             "classes": classes}
 
 
+def summarize_step_bytes(fetch_dir, write_dir, copy_mb, steps):
+    """HBM bytes per step of a profile-only run: FETCH_SIZE + WRITE_SIZE of
+    every library kernel dispatch (the calibration copy excluded), each
+    counter scaled by expected / counted bytes of the calibration copy,
+    divided by the number of steps the run made (warm-up included)."""
+    out = {}
+    for d, counter in ((fetch_dir, "FETCH_SIZE"), (write_dir, "WRITE_SIZE")):
+        rows = []
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as fh:
+                rows += [r for r in csv.DictReader(fh) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        lib = [(kernel_class(r["Kernel_Name"]), float(r["Counter_Value"]) * 1024.0) for r in rows
+               if kernel_class(r["Kernel_Name"]) is not None]
+        if not lib or lib[-1][0] != "copy":
+            raise SystemExit("the last library dispatch must be the calibration copy (--calib-copy-mb)")
+        scale = copy_mb * 1024.0 * 1024.0 / lib[-1][1]
+        out[counter] = {"bytes_per_step": sum(v for _, v in lib[:-1]) * scale / steps, "scale": scale}
+    out["total_bytes_per_step"] = out["FETCH_SIZE"]["bytes_per_step"] + out["WRITE_SIZE"]["bytes_per_step"]
+    return out
+
+
+def summarize_mfma(pmc_dir, dtype="bf16"):
+    """Markdown table per kernel class from a rocprofv3 --pmc run with
+    SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16 (or _F32) and
+    GRBM_GUI_ACTIVE: matrix-core FLOPs (MOPS x 512), their rate over the
+    dispatches' own durations (timestamps) against the dense peak, and the
+    matrix-core busy fraction busy / (GUI-active cycles per XCD x SIMDs).
+    GRBM_GUI_ACTIVE is reported summed over the 8 XCDs."""
+    mops = "SQ_INSTS_VALU_MFMA_MOPS_BF16" if dtype == "bf16" else "SQ_INSTS_VALU_MFMA_MOPS_F32"
+    disp = {}
+    for path in glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                d = disp.setdefault((path, r["Dispatch_Id"]), {"name": r["Kernel_Name"],
+                                                               "dur": (int(r["End_Timestamp"]) -
+                                                                       int(r["Start_Timestamp"])) * 1e-9})
+                d[r["Counter_Name"]] = float(r["Counter_Value"])
+    agg = {}
+    for d in disp.values():
+        c = kernel_class(d["name"])
+        if c is None or "GRBM_GUI_ACTIVE" not in d:
+            continue
+        a = agg.setdefault(c, [0, 0.0, 0.0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += d.get(mops, 0.0) * 512
+        a[2] += d["dur"]
+        a[3] += d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        a[4] += d["GRBM_GUI_ACTIVE"] / 8 * 1024
+    peak = PEAK_MFMA_TFS[dtype]
+    out = ["| class | dispatches | matrix-core TFLOP | time ms | TFLOP/s | of %.0f TFLOP/s peak | busy fraction |"
+           % peak, "|---|---|---|---|---|---|---|"]
+    for c, (n, fl, t, busy, cyc) in sorted(agg.items(), key=lambda kv: -kv[1][2]):
+        if fl <= 0:
+            continue
+        out.append("| %s | %d | %.3f | %.3f | %.1f | %.3f | %.3f |" % (c, n, fl / 1e12, t * 1e3, fl / t / 1e12,
+                                                                    fl / t / 1e12 / peak, busy / cyc))
+    return "\n".join(out)
+
+
 def traffic_for(workload, cls):
     """Counter bytes per launch of a kernel class, if measured on the current sources."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % workload)
@@ -368,6 +443,15 @@ def main():
             json.dump(out, fh, indent=1, sort_keys=True)
         print(json.dumps(out["classes"]))
         return
+    if args.summarize_mfma:
+        print(summarize_mfma(args.summarize_mfma))
+        return
+    if args.summarize_step_bytes:
+        if args.calib_copy_mb <= 0:
+            raise SystemExit("--summarize-step-bytes needs the --calib-copy-mb value the counter runs used")
+        print(json.dumps(summarize_step_bytes(args.summarize_step_bytes[0], args.summarize_step_bytes[1],
+                                              args.calib_copy_mb, args.steps + args.warmup)))
+        return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace[0], int(args.summarize_trace[1]), args.workload, args.bench_json))
         return
@@ -424,6 +508,8 @@ def main():
         "fused_no_icf": ({"images_per_s": noicf["images"] / (noicf["ms"] / 1e3), "ms_per_step": noicf["ms"],
                           "algorithmic_bytes": model.get("fused_no_icf")} if noicf else None),
         "speedup_vs_unfused": (unf["ms"] / fused["ms"]) if (fused and unf) else None,
+        "ablation": {k: {"images_per_s": v["images"] / (v["ms"] / 1e3), "ms_per_step": v["ms"]}
+                     for k, v in res.items()},
         "hbm_bytes_per_step": {"algorithmic_fused": model["fused"], "algorithmic_unfused": model["unfused"]},
         "roofline": roofline(kernels, dtype, args.workload) if kernels else None,
         "kernels": kernels,
