@@ -196,6 +196,22 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
                          void *dx, int32_t dx_ldc, int32_t dx_accumulate,
                          void *ws, size_t ws_bytes, void *stream);
 
+/* The two independent halves of bnr_bwd_fused (and of bnr_bwd_fused_split
+ * below), for callers that overlap a layer's weight gradient with the data
+ * gradients of the layers before it (e.g. on a second stream).  Step 3 reads
+ * only x, x_bn and what g_src reads -- nothing steps 1-2 write -- so the
+ * halves may run in either order or concurrently once g_src is complete.
+ *   bnr_bwd_data:    steps 1, 2 and 4 of bnr_bwd_fused (all its arguments but dw);
+ *   bnr_bwd_weights: step 3 (dw [k][k][c_in][c_out] float32, overwritten; x_bn
+ *                    NULL: the CONV input is x itself).
+ * Each call needs its own workspace while another call may be in flight. */
+bnr_status bnr_bwd_data(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                        const bnr_grad_src *g_src, float *dgamma, float *dbeta, void *dy,
+                        void *dx, int32_t dx_ldc, int32_t dx_accumulate,
+                        void *ws, size_t ws_bytes, void *stream);
+bnr_status bnr_bwd_weights(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn,
+                           const bnr_grad_src *g_src, float *dw, void *ws, size_t ws_bytes, void *stream);
+
 /* Standalone BN input gradient for a BN whose producer is not a CONV (block
  * input, concatenation): dx = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m) from
  * dy[m][c] (dense), x (pixel stride x_ldc), written or added into dx (pixel
@@ -236,6 +252,13 @@ bnr_status bnr_bwd_fused_split(const bnr_conv_desc *d, const void *x, const bnr_
                                const bnr_grad_src *g_src, float *dw, float *dgamma, float *dbeta,
                                void *gsum, int32_t gsum_ldc, int32_t accumulate, float *alpha, float *betap,
                                void *ws, size_t ws_bytes, void *stream);
+
+/* Steps 1-2 of bnr_bwd_fused_split (its arguments but dw); its weight
+ * gradient is bnr_bwd_weights on the same descriptor, x, x_bn and g_src. */
+bnr_status bnr_bwd_data_split(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                              const bnr_grad_src *g_src, float *dgamma, float *dbeta,
+                              void *gsum, int32_t gsum_ldc, int32_t accumulate, float *alpha, float *betap,
+                              void *ws, size_t ws_bytes, void *stream);
 
 /* Materialise a summed BN input gradient: dx = gsum + alpha + betap*xhat with
  * xhat = (x - mean)*rstd (mean, rstd from bn), written to (dx_accumulate = 0)

@@ -94,6 +94,12 @@ _lib_fns = dict(
                        c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_sz, c_vp),
     bnr_bwd_fused_split=_sig("bnr_bwd_fused_split", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
                              _P(GradSrc), c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp),
+    bnr_bwd_data=_sig("bnr_bwd_data", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, _P(GradSrc), c_vp, c_vp,
+                      c_vp, c_vp, c_i32, c_i32, c_vp, c_sz, c_vp),
+    bnr_bwd_data_split=_sig("bnr_bwd_data_split", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, _P(GradSrc),
+                            c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp),
+    bnr_bwd_weights=_sig("bnr_bwd_weights", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), _P(GradSrc), c_vp, c_vp,
+                         c_sz, c_vp),
     bnr_split_dx=_sig("bnr_split_dx", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_i32, c_vp, c_i32,
                       _P(BNStruct), c_vp, c_vp, c_vp, c_i32, c_i32, c_vp),
     bnr_bn_dx=_sig("bnr_bn_dx", ctypes.c_int, c_i64, c_i32, ctypes.c_int, c_vp, c_vp, c_i32, _P(BNStruct), c_vp, c_vp,
@@ -184,13 +190,15 @@ def _stream():
 _ws_cache = {}
 
 
-def workspace(nbytes, device=None):
-    """Grow-only per-device workspace (device memory from torch)."""
+def workspace(nbytes, device=None, slot=0):
+    """Grow-only per-device workspace (device memory from torch); calls that
+    may be in flight at the same time (on different streams) use different
+    slots."""
     dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
-    cur = _ws_cache.get(dev)
+    cur = _ws_cache.get((dev, slot))
     if cur is None or cur.numel() < nbytes:
         cur = torch.empty(max(int(nbytes), 256) + 256, dtype=torch.uint8, device=dev)
-        _ws_cache[dev] = cur
+        _ws_cache[(dev, slot)] = cur
     base = cur.data_ptr()
     aligned = (base + 255) // 256 * 256
     return aligned, cur.numel() - (aligned - base)
@@ -345,6 +353,42 @@ def bnr_bwd_fused_split(desc, x, x_bn, w, g_src, dw, dgamma, dbeta, gsum, alpha,
     _check(_lib_fns["bnr_bwd_fused_split"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), ctypes.byref(gs),
                                            _ptr(dw), _ptr(dgamma), _ptr(dbeta), pg, ldg, 1 if accumulate else 0,
                                            _ptr(alpha), _ptr(betap), ws, wsb, _stream()))
+    del keep
+
+
+def bnr_bwd_data(desc, x, x_bn, w, g_src, dgamma=None, dbeta=None, dy=None, dx=None, dx_accumulate=False, slot=0):
+    """Steps 1-2 (and the optional dx) of bnr_bwd_fused."""
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device, slot)
+    gs, keep = _grad_struct(g_src)
+    xs = x_bn.struct() if x_bn is not None else None
+    dxp, dx_ldc = (None, 0)
+    if dx is not None:
+        dxp, _, _, dx_ldc = view(dx)
+    _check(_lib_fns["bnr_bwd_data"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs) if xs is not None else None,
+                                    _ptr(w), ctypes.byref(gs), _ptr(dgamma), _ptr(dbeta), _ptr(dy), dxp, dx_ldc,
+                                    1 if dx_accumulate else 0, ws, wsb, _stream()))
+    del keep
+
+
+def bnr_bwd_data_split(desc, x, x_bn, w, g_src, dgamma, dbeta, gsum, alpha, betap, accumulate=False, slot=0):
+    """Steps 1-2 of bnr_bwd_fused_split."""
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device, slot)
+    gs, keep = _grad_struct(g_src)
+    xs = x_bn.struct()
+    pg, _, _, ldg = view(gsum)
+    _check(_lib_fns["bnr_bwd_data_split"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), ctypes.byref(gs),
+                                          _ptr(dgamma), _ptr(dbeta), pg, ldg, 1 if accumulate else 0, _ptr(alpha),
+                                          _ptr(betap), ws, wsb, _stream()))
+    del keep
+
+
+def bnr_bwd_weights(desc, x, x_bn, g_src, dw, slot=0):
+    """Step 3 of the fused backward: the weight gradient alone."""
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device, slot)
+    gs, keep = _grad_struct(g_src)
+    xs = x_bn.struct() if x_bn is not None else None
+    _check(_lib_fns["bnr_bwd_weights"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs) if xs is not None else None,
+                                       ctypes.byref(gs), _ptr(dw), ws, wsb, _stream()))
     del keep
 
 

@@ -410,16 +410,24 @@ bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtyp
 // the gradient-source prologue and (x_bn) the BN-backward epilogue into y
 // (dy, or with y_scale the summed-gradient term gamma*rstd*dy, y_acc: added),
 // the dbeta/dgamma combine (with split: also alpha/betap), the weight gradient.
+enum { BWD_DATA = 1, BWD_WEIGHTS = 2 };
+
 static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
                             const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *y, int64_t y_ldc,
-                            int y_scale, int y_acc, const SplitTerms *split, void *ws, hipStream_t s)
+                            int y_scale, int y_acc, const SplitTerms *split, void *ws, hipStream_t s,
+                            int parts = BWD_DATA | BWD_WEIGHTS)
 {
     const ConvWs cw = conv_ws(d);
     const ConvPtrs cp = conv_ptrs(ws, cw);
     const int64_t m = pixels(d);
     const int dt = dt_of(d->dtype);
 
-    // 1. data gradient
+    // 1. data gradient.  With both halves in this call and few enough partial
+    // rows, the dbeta/dgamma combine (step 2) rides in the launch that sums
+    // the weight gradient's split-K partials (after step 3).
+    int64_t R = 0;
+    bool tail_combine = false;
+    if (parts & BWD_DATA) {
     RowsParams rp;
     fill_rows(rp, d, d->c_out, d->c_in);
     if (g->kind == BNR_GRAD_DENSE) {
@@ -442,14 +450,16 @@ static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn 
     } else {
         rp.epi = EPI_STORE; rp.y = y; rp.y_ldc = y_ldc; rp.accumulate = y_acc ? 1 : 0;
     }
-    int64_t R = 0;
     TRY(launch_conv_any(rp, d, w, 1, cp.pack, &R, s));
     // 2. dbeta = sum(dy), dgamma = sum(dy * xhat)
-    if (x_bn) {
+    tail_combine = x_bn && (parts & BWD_WEIGHTS) && R <= kCombineOneMaxRows;
+    if (x_bn && !tail_combine) {
         TRY_HIP(launch_stats_finalize(cp.part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma,
                                       cp.red, s, split),
                 "backward sums combine");
     }
+    }
+    if (!(parts & BWD_WEIGHTS)) return BNR_OK;
     // 3. weight gradient, both operands recomputed on load
     WgradParams wp;
     memset(&wp, 0, sizeof wp);
@@ -473,7 +483,21 @@ static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn 
         wp.gsrc = GB_POOLUP; wp.g = g->g; wp.g_ldc = g->g_ldc;
     }
     wp.dw = dw; wp.part = cp.wg; wp.red = cp.wgred;
-    TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
+    if (!tail_combine) {
+        TRY_HIP(launch_wgrad(wp, s), "conv weight gradient");
+        return BNR_OK;
+    }
+    int64_t S = 1;
+    TRY_HIP(launch_wgrad(wp, s, &S), "conv weight gradient");
+    if (S > 1) {
+        TRY_HIP(launch_bwd_tail(cp.wg, S, (int64_t)d->k * d->k * d->c_in * d->c_out, dw, cp.part, R, d->c_in, m,
+                                dbeta, dgamma, split, s),
+                "weight-gradient sum + backward sums combine");
+    } else {
+        TRY_HIP(launch_stats_finalize(cp.part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma,
+                                      cp.red, s, split),
+                "backward sums combine");
+    }
     return BNR_OK;
 }
 
@@ -491,15 +515,15 @@ static bool grad_src_overlaps(const bnr_conv_desc *d, const bnr_grad_src *g, Ran
     return false;
 }
 
-bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
-                         const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy, void *dx,
-                         int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream)
+static bnr_status bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                            const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy, void *dx,
+                            int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream, int parts)
 {
     TRY(check_desc(d));
     TRY(check_ptr(x, "x"));
     TRY(check_ptr(w, "w"));
     TRY(validate_grad_src(d, g));
-    TRY(check_fptr(dw, "dw"));
+    if (parts & BWD_WEIGHTS) TRY(check_fptr(dw, "dw"));
     if (x_bn) {
         TRY(check_bn(x_bn, "x_bn", true, false));
         TRY(check_fptr(dgamma, "dgamma"));
@@ -525,10 +549,10 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     }
 
     hipStream_t s = (hipStream_t)stream;
-    if (x_bn) TRY(bwd_steps(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, d->c_in, 0, 0, nullptr, ws, s));
-    else TRY(bwd_steps(d, x, nullptr, w, g, dw, nullptr, nullptr, dx, dx_ldc, 0, dx_accumulate, nullptr, ws, s));
+    if (x_bn) TRY(bwd_steps(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, d->c_in, 0, 0, nullptr, ws, s, parts));
+    else TRY(bwd_steps(d, x, nullptr, w, g, dw, nullptr, nullptr, dx, dx_ldc, 0, dx_accumulate, nullptr, ws, s, parts));
     // 4. optional standalone BN input gradient
-    if (x_bn && dx) {
+    if ((parts & BWD_DATA) && x_bn && dx) {
         TRY_HIP(launch_elementwise(dt_of(d->dtype), EW_DX, m, d->c_in, dy, d->c_in, x, d->in_ldc, x_bn->gamma, nullptr,
                                    x_bn->mean, x_bn->rstd, dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, s),
                 "BN input gradient");
@@ -536,16 +560,32 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
     return ok();
 }
 
-bnr_status bnr_bwd_fused_split(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
-                               const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *gsum,
-                               int32_t gsum_ldc, int32_t accumulate, float *alpha, float *betap, void *ws,
-                               size_t ws_bytes, void *stream)
+bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                         const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy, void *dx,
+                         int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream)
+{
+    return bwd_fused(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, dx, dx_ldc, dx_accumulate, ws, ws_bytes, stream,
+                     BWD_DATA | BWD_WEIGHTS);
+}
+
+bnr_status bnr_bwd_data(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                        const bnr_grad_src *g, float *dgamma, float *dbeta, void *dy, void *dx, int32_t dx_ldc,
+                        int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream)
+{
+    return bwd_fused(d, x, x_bn, w, g, nullptr, dgamma, dbeta, dy, dx, dx_ldc, dx_accumulate, ws, ws_bytes, stream,
+                     BWD_DATA);
+}
+
+static bnr_status bwd_split(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                            const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *gsum,
+                            int32_t gsum_ldc, int32_t accumulate, float *alpha, float *betap, void *ws,
+                            size_t ws_bytes, void *stream, int parts)
 {
     TRY(check_desc(d));
     TRY(check_ptr(x, "x"));
     TRY(check_ptr(w, "w"));
     TRY(validate_grad_src(d, g));
-    TRY(check_fptr(dw, "dw"));
+    if (parts & BWD_WEIGHTS) TRY(check_fptr(dw, "dw"));
     TRY(check_bn(x_bn, "x_bn", true, false));
     TRY(check_fptr(dgamma, "dgamma"));
     TRY(check_fptr(dbeta, "dbeta"));
@@ -562,7 +602,40 @@ bnr_status bnr_bwd_fused_split(const bnr_conv_desc *d, const void *x, const bnr_
     if (grad_src_overlaps(d, g, rs)) return fail(BNR_ERR_ALIAS, "gsum overlaps a view g_src reads");
     const SplitTerms st{x_bn->gamma, x_bn->rstd, alpha, betap, accumulate ? 1 : 0};
     TRY(bwd_steps(d, x, x_bn, w, g, dw, dgamma, dbeta, gsum, gsum_ldc, 1, accumulate ? 1 : 0, &st, ws,
-                  (hipStream_t)stream));
+                  (hipStream_t)stream, parts));
+    return ok();
+}
+
+bnr_status bnr_bwd_fused_split(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                               const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *gsum,
+                               int32_t gsum_ldc, int32_t accumulate, float *alpha, float *betap, void *ws,
+                               size_t ws_bytes, void *stream)
+{
+    return bwd_split(d, x, x_bn, w, g, dw, dgamma, dbeta, gsum, gsum_ldc, accumulate, alpha, betap, ws, ws_bytes,
+                     stream, BWD_DATA | BWD_WEIGHTS);
+}
+
+bnr_status bnr_bwd_data_split(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                              const bnr_grad_src *g, float *dgamma, float *dbeta, void *gsum, int32_t gsum_ldc,
+                              int32_t accumulate, float *alpha, float *betap, void *ws, size_t ws_bytes,
+                              void *stream)
+{
+    return bwd_split(d, x, x_bn, w, g, nullptr, dgamma, dbeta, gsum, gsum_ldc, accumulate, alpha, betap, ws,
+                     ws_bytes, stream, BWD_DATA);
+}
+
+bnr_status bnr_bwd_weights(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const bnr_grad_src *g,
+                           float *dw, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_desc(d));
+    TRY(check_ptr(x, "x"));
+    TRY(validate_grad_src(d, g));
+    TRY(check_fptr(dw, "dw"));
+    if (x_bn) TRY(check_bn(x_bn, "x_bn", true, false));
+    const ConvWs cw = conv_ws(d);
+    TRY(check_ws(ws, ws_bytes, cw.total));
+    TRY(bwd_steps(d, x, x_bn, nullptr, g, dw, nullptr, nullptr, nullptr, 0, 0, 0, nullptr, ws, (hipStream_t)stream,
+                  BWD_WEIGHTS));
     return ok();
 }
 

@@ -141,14 +141,13 @@ __device__ __forceinline__ void stats_write(int mode, int c, double a, double b,
 // 8 channels x 32 row groups; thread (c, g) adds rows g, g+32, ... in float64
 // (8 loads in flight), then the 32 group sums of a channel are added in a
 // fixed order (deterministic).
-__global__ __launch_bounds__(kThreads) void k_stats_combine_one(const float *__restrict__ part, int64_t R, int C,
-                                                                int64_t m, int mode, float eps, float *mean,
-                                                                float *var, float *rstd, float *dbeta, float *dgamma,
-                                                                SplitTerms st)
+__device__ __forceinline__ void combine_one_block(int bid, const float *__restrict__ part, int64_t R, int C,
+                                                  int64_t m, int mode, float eps, float *mean, float *var,
+                                                  float *rstd, float *dbeta, float *dgamma, const SplitTerms &st)
 {
     __shared__ double red[2][32][8];
     const int tid = threadIdx.x, cl = tid & 7, g = tid >> 3;
-    const int c = blockIdx.x * 8 + cl;
+    const int c = bid * 8 + cl;
     double a = 0.0, b = 0.0;
     if (c < C) {
         const float *p = part + c;
@@ -171,6 +170,63 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine_one(const float *__r
         double sa = 0.0, sb = 0.0;
         for (int j = 0; j < 32; j++) { sa += red[0][j][cl]; sb += red[1][j][cl]; }
         stats_write(mode, c, sa, sb, m, eps, mean, var, rstd, dbeta, dgamma, st);
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void k_stats_combine_one(const float *__restrict__ part, int64_t R, int C,
+                                                                int64_t m, int mode, float eps, float *mean,
+                                                                float *var, float *rstd, float *dbeta, float *dgamma,
+                                                                SplitTerms st)
+{
+    combine_one_block(blockIdx.x, part, R, C, m, mode, eps, mean, var, rstd, dbeta, dgamma, st);
+}
+
+// --------------------------------------------------------------------------
+// Tail of a fused backward CONV call in one launch: the weight gradient's
+// split-K sum and the BN-backward sums' combine (independent jobs).
+//   workgroups [0, nb_sum): dw[i] = sum over the S partial tiles, one level:
+//     a workgroup owns 16 consecutive float4 outputs; its 256 threads are 16
+//     row groups x 16 outputs (row group q adds partials q, q+16, ... with
+//     eight loads in flight), and the 16 row-group sums of an output are
+//     added in a fixed order (deterministic);
+//   workgroups [nb_sum, nb_sum + ceil(C/8)): the one-kernel statistics
+//     combine (FIN_BWD, with the summed-gradient terms of st).
+constexpr int kTailF4 = 16;
+__global__ __launch_bounds__(kThreads) void k_bwd_tail(const float *__restrict__ wpart, int64_t S, int64_t len,
+                                                       float *__restrict__ dw, int nb_sum,
+                                                       const float *__restrict__ spart, int64_t R, int C, int64_t m,
+                                                       float *dbeta, float *dgamma, SplitTerms st)
+{
+    if ((int)blockIdx.x >= nb_sum) {
+        combine_one_block((int)blockIdx.x - nb_sum, spart, R, C, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta,
+                          dgamma, st);
+        return;
+    }
+    __shared__ float4 red[kThreads / kTailF4][kTailF4];
+    const int tid = threadIdx.x, f = tid % kTailF4, q = tid / kTailF4;
+    constexpr int QN = kThreads / kTailF4;
+    const int64_t i4 = (int64_t)blockIdx.x * kTailF4 + f;
+    const int64_t st4 = len / 4;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i4 < st4) {
+        const float4 *p = reinterpret_cast<const float4 *>(wpart) + i4;
+        for (int64_t r = q; r < S; r += 8 * QN) {
+            float4 v[8];
+            #pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const int64_t rr = r + (int64_t)u * QN;
+                v[u] = rr < S ? p[rr * st4] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            #pragma unroll
+            for (int u = 0; u < 8; u++) { acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w; }
+        }
+    }
+    red[q][f] = acc;
+    __syncthreads();
+    if (q == 0 && i4 < st4) {
+        float4 t = red[0][f];
+        for (int j = 1; j < QN; j++) { const float4 a = red[j][f]; t.x += a.x; t.y += a.y; t.z += a.z; t.w += a.w; }
+        reinterpret_cast<float4 *>(dw)[i4] = t;
     }
 }
 
@@ -719,6 +775,24 @@ hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s
     const int64_t per = ceil_div(nvec, 4096) < kThreads ? kThreads : ceil_div(nvec, 4096);
     hipLaunchKernelGGL(k_copy16, dim3((unsigned)ceil_div(nvec, per)), dim3(kThreads), 0, s, (const vec16 *)src,
                        (vec16 *)dst, nvec, per);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_tail(const float *wpart, int64_t S, int64_t len, float *dw, const float *spart, int64_t R,
+                           int C, int64_t m, float *dbeta, float *dgamma, const SplitTerms *split, hipStream_t s)
+{
+    if (!wpart || !dw || (len % 4) || S < 1 || !spart || !dbeta || !dgamma || R > kCombineOneMaxRows)
+        return hipErrorInvalidValue;
+    SplitTerms st{nullptr, nullptr, nullptr, nullptr, 0};
+    if (split && split->alpha) {
+        if (!split->gamma || !split->rstd || !split->betap) return hipErrorInvalidValue;
+        st = *split;
+    }
+    const int nb_sum = (int)ceil_div(len / 4, kTailF4);
+    const int nb_comb = (int)ceil_div(C, 8);
+    TraceScope tr(KC_SMALL, KID_SPLITK_SUM, s, 4.0 * (double)len * (S + 1) + (double)R * 2 * C * 4, 0.0);
+    hipLaunchKernelGGL(k_bwd_tail, dim3((unsigned)(nb_sum + nb_comb)), dim3(kThreads), 0, s, wpart, S, len, dw, nb_sum,
+                       spart, R, C, m, dbeta, dgamma, st);
     return hipGetLastError();
 }
 

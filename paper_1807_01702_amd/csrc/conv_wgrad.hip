@@ -611,7 +611,7 @@ static hipError_t dispatch_wgrad(const WgradParams &p, const WgradPlan &pl, hipS
     return run_wgrad<T, 1, 128, 1, 4>(p, pl, s);
 }
 
-hipError_t launch_wgrad(const WgradParams &p, hipStream_t s)
+hipError_t launch_wgrad(const WgradParams &p, hipStream_t s, int64_t *splits_out)
 {
     if (!p.x || !p.g || !p.dw) return hipErrorInvalidValue;
     if (p.a_mode == 1 && (!p.a_mean || !p.a_gamma || !p.a_rstd || !p.a_beta)) return hipErrorInvalidValue;
@@ -623,13 +623,15 @@ hipError_t launch_wgrad(const WgradParams &p, hipStream_t s)
         const WgTrPlan tp = wgrad_tr_plan(p.m, p.n, p.h, p.w, p.c_in, p.c_out, p.k);
         if (tp.splits > 1 && (!p.part || !p.red)) return hipErrorInvalidValue;
         const hipError_t e = dispatch_wgrad_tr(p, tp, s);
-        if (e != hipSuccess || tp.splits <= 1) return e;
+        if (splits_out) *splits_out = tp.splits;
+        if (e != hipSuccess || tp.splits <= 1 || splits_out) return e;
         return launch_sum_partials(p.part, tp.splits, (int64_t)p.k * p.k * p.c_in * p.c_out, p.dw, p.red, s);
     }
     const WgradPlan pl = wgrad_plan(p.m, p.n, p.h, p.w, p.c_in, p.c_out, p.k, p.dtype == DT_BF16 ? 2 : 4);
     if (pl.splits > 1 && (!p.part || !p.red)) return hipErrorInvalidValue;
     const hipError_t e = p.dtype == DT_BF16 ? dispatch_wgrad<bf16_t>(p, pl, s) : dispatch_wgrad<float>(p, pl, s);
-    if (e != hipSuccess || pl.splits <= 1) return e;
+    if (splits_out) *splits_out = pl.splits;
+    if (e != hipSuccess || pl.splits <= 1 || splits_out) return e;
     return launch_sum_partials(p.part, pl.splits, (int64_t)p.k * p.k * p.c_in * p.c_out, p.dw, p.red, s);
 }
 

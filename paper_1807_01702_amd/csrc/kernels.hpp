@@ -52,6 +52,12 @@ hipError_t launch_copy16(const void *src, void *dst, int64_t nvec, hipStream_t s
 // Split-K sum scratch: up to 8 level-1 float32 rows of len.
 inline size_t sum_partials_red_bytes(int64_t len) { return 8 * (size_t)len * 4; }
 int sum_partials_groups(int64_t S);
+// The tail of a fused backward CONV call in one launch: dw = sum of the S
+// split-K partial tiles (single level, deterministic) and the FIN_BWD combine
+// of R <= kCombineOneMaxRows BN-backward partial rows (dbeta, dgamma, and the
+// summed-gradient terms of split).
+hipError_t launch_bwd_tail(const float *wpart, int64_t S, int64_t len, float *dw, const float *spart, int64_t R,
+                           int C, int64_t m, float *dbeta, float *dgamma, const SplitTerms *split, hipStream_t s);
 hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, void *red, hipStream_t s);
 
 // ---- implicit-GEMM CONV over pixel rows (forward / data gradient) ---------
@@ -134,7 +140,10 @@ struct WgradParams {
     void *red;                    // split-K sum scratch (sum_partials_red_bytes)
 };
 size_t wgrad_ws_bytes(int dtype, int64_t m, int n, int h, int w, int c_in, int c_out, int k);
-hipError_t launch_wgrad(const WgradParams &p, hipStream_t s);
+// *splits_out != NULL: launch the weight-gradient kernel only and report its
+// split count (1: dw written directly; > 1: partial tiles in p.part for the
+// caller to sum); NULL: the split-K sum is launched here as well.
+hipError_t launch_wgrad(const WgradParams &p, hipStream_t s, int64_t *splits_out = nullptr);
 
 // ---- network ends: first CONV, max pooling, classifier head (net_ends.hip) ----
 // First CONV: 7x7, stride 2, pad 3, 64 output channels; the image is

@@ -200,7 +200,7 @@ class _DenseStage:
     ICF each BN1 sweeps its input for statistics and its input gradient is
     formed by a separate pass accumulating into G."""
 
-    def __init__(self, n, h, w, c0, ct, cpls, trans, eps, dev, bf16, fused, icf, ref_mode=MODE):
+    def __init__(self, n, h, w, c0, ct, cpls, trans, eps, dev, bf16, fused, icf, ref_mode=MODE, overlap=False):
         dt = torch.bfloat16 if bf16 else torch.float32
         self.n, self.h, self.w, self.c0, self.ct = n, h, w, c0, ct
         self.X = torch.zeros((n, h, w, ct), dtype=dt, device=dev)
@@ -229,6 +229,14 @@ class _DenseStage:
         self.G = torch.empty((n, h, w, ct), dtype=dt, device=dev)
         self.dy1_flat = torch.empty(n * h * w * ct, dtype=dt, device=dev)    # dense [m][c_l] scratch, c_l < ct
         self.dy2 = torch.empty((n, h, w, width), dtype=dt, device=dev)
+        # overlap (off by default: measured no faster, the persistent CONV kernels hold every CU): every
+        # layer's weight gradients run on a side stream while the data gradients of the layers before
+        # it proceed; a layer's BN2 gradient dy2 is then read after the next layer's data gradient has
+        # started, so each layer keeps its own dy2
+        self.overlap = bool(overlap) and fused
+        self.dy2s = ([torch.empty((n, h, w, width), dtype=dt, device=dev) for _ in cpls] if self.overlap
+                     else [self.dy2] * len(cpls))
+        self._side = torch.cuda.Stream(device=dev) if self.overlap else None
         if not fused:
             self.dz_flat = torch.empty(n * h * w * max(ct, width), dtype=dt, device=dev)
             self.dx2 = torch.empty_like(self.dy2)
@@ -288,7 +296,11 @@ class _DenseStage:
         and the transition's backward starts G.  Without one the BN that
         reads the whole block (the classifier head) has already written G
         (and, with ICF, alpha/betap).  On return G[..., :c0] holds the
-        gradient of the block input."""
+        gradient of the block input (and, with overlap, the side stream's
+        weight gradients are joined into the current stream)."""
+        if self.overlap:
+            self._backward_overlapped(dpool)
+            return
         ut = self.ut
         n, h, w = self.n, self.h, self.w
         if self.icf:
@@ -328,19 +340,68 @@ class _DenseStage:
                 u1.ref_bwd(self.dx2, _dense(self.dz_flat, n, h, w, c_l), _dense(self.dy1_flat, n, h, w, c_l),
                            self.G[..., :c_l], True)
 
+    def _weights(self, u, g_src):
+        """u's weight gradient on the side stream, after everything issued so
+        far on the current stream (which completes g_src)."""
+        main = torch.cuda.current_stream()
+        self._side.wait_stream(main)
+        with torch.cuda.stream(self._side):
+            B.bnr_bwd_weights(u.desc, u.x, u.bn, g_src, u.dw, slot=1)
+
+    def _backward_overlapped(self, dpool):
+        """The fused backward with every weight gradient on the side stream.
+        A weight gradient reads its layer's input and gradient source only:
+        the later data gradients on the current stream write other channels
+        of G, alpha, betap (and their own dy2), never what it reads."""
+        ut = self.ut
+        n, h, w = self.n, self.h, self.w
+        main = torch.cuda.current_stream()
+        if self.icf:
+            c0 = self.c0
+            if ut is not None:
+                g = B.grad_avgpool2(dpool)
+                self._weights(ut, g)
+                B.bnr_bwd_data_split(ut.desc, ut.x, ut.bn, ut.wt, g, ut.g.dgamma, ut.g.dbeta, self.G, self.alpha,
+                                     self.betap)
+            for (c_l, k, u1, u2), st, dy2 in zip(reversed(self.cpl), reversed(self.slice_stats), reversed(self.dy2s)):
+                sl = slice(c_l, c_l + k)
+                g2 = B.grad_split(self.G[..., sl], self.X[..., sl], st, self.alpha[sl], self.betap[sl])
+                self._weights(u2, g2)
+                B.bnr_bwd_data(u2.desc, u2.x, u2.bn, u2.wt, g2, u2.g.dgamma, u2.g.dbeta, dy2)
+                g1 = B.grad_bn(dy2, u2.x, u2.bn, u2.g.dgamma, u2.g.dbeta)
+                self._weights(u1, g1)
+                B.bnr_bwd_data_split(u1.desc, u1.x, u1.bn, u1.wt, g1, u1.g.dgamma, u1.g.dbeta, self.G[..., :c_l],
+                                     self.alpha[:c_l], self.betap[:c_l], accumulate=True)
+            B.bnr_split_dx(self.G[..., :c0], self.X[..., :c0], self.in_stats, self.alpha[:c0], self.betap[:c0],
+                           self.G[..., :c0])
+        else:
+            if ut is not None:
+                g = B.grad_avgpool2(dpool)
+                self._weights(ut, g)
+                B.bnr_bwd_data(ut.desc, ut.x, ut.bn, ut.wt, g, ut.g.dgamma, ut.g.dbeta, self.dy_t, self.G)
+            for (c_l, k, u1, u2), dy2 in zip(reversed(self.cpl), reversed(self.dy2s)):
+                g2 = B.grad_dense(self.G[..., c_l:c_l + k])
+                self._weights(u2, g2)
+                B.bnr_bwd_data(u2.desc, u2.x, u2.bn, u2.wt, g2, u2.g.dgamma, u2.g.dbeta, dy2)
+                g1 = B.grad_bn(dy2, u2.x, u2.bn, u2.g.dgamma, u2.g.dbeta)
+                self._weights(u1, g1)
+                B.bnr_bwd_data(u1.desc, u1.x, u1.bn, u1.wt, g1, u1.g.dgamma, u1.g.dbeta,
+                               _dense(self.dy1_flat, n, h, w, c_l), self.G[..., :c_l], dx_accumulate=True)
+        main.wait_stream(self._side)
+
 
 class DenseBlock(_DenseStage):
     """Dense block 1 of DenseNet-121 + transition layer on a given block
     input; upstream gradient: dpool of the pooled output.  ``icf`` defaults
     to on for the fused path (see _DenseStage)."""
 
-    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None):
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None, overlap=False):
         bf16 = data["bf16"]
         dev = torch.device(device)
         dt = torch.bfloat16 if bf16 else torch.float32
         n, h, w, c0 = data["x"].shape
         super().__init__(n, h, w, c0, data["c_total"], data["cpls"], data["trans"], data["eps"], dev, bf16, fused,
-                         fused if icf is None else icf, ref_mode)
+                         fused if icf is None else icf, ref_mode, overlap)
         self.X[..., :c0] = _t(data["x"], dev, bf16)
         to = data["trans"]["w"].shape[3]
         self.pooled = torch.empty((n, h // 2, w // 2, to), dtype=dt, device=dev)

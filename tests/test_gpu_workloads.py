@@ -35,7 +35,7 @@ from paper_1807_01702_amd import synth
 pytestmark = pytest.mark.gpu
 
 MODES = ["fused", "baseline", "rcf", "rcf_mvf"]
-BLOCK_MODES = ["fused", "fused_no_icf", "baseline", "rcf", "rcf_mvf"]     # fused = BNFF + ICF
+BLOCK_MODES = ["fused", "fused_overlap", "fused_no_icf", "baseline", "rcf", "rcf_mvf"]   # fused = BNFF + ICF
 
 
 def _make(cls, data, mode):
@@ -45,6 +45,8 @@ def _make(cls, data, mode):
         return getattr(W, cls)(data, fused=True)
     if mode == "fused_no_icf":
         return getattr(W, cls)(data, fused=True, icf=False)
+    if mode == "fused_overlap":         # weight gradients on a side stream
+        return getattr(W, cls)(data, fused=True, overlap=True)
     ref = {"baseline": B.MODE_BASELINE, "rcf": B.MODE_RCF, "rcf_mvf": B.MODE_RCF_MVF}[mode]
     return getattr(W, cls)(data, fused=False, ref_mode=ref)
 
