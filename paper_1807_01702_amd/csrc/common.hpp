@@ -21,8 +21,12 @@ __device__ __forceinline__ bf16_t f2bf(float f) {
     __builtin_memcpy(&u, &b, 2);
     return u;
 }
+// two floats -> packed bf16 pair (one v_cvt_pk_bf16_f32)
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack2bf(float lo, float hi) {
-    return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+    const f32x2_t f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
 // Element traits: VEC = elements per 16-byte vector; storage <-> float.
@@ -82,6 +86,12 @@ __device__ __forceinline__ vec16 bld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     vec16 v;
     v.u[0] = t.x; v.u[1] = t.y; v.u[2] = t.z; v.u[3] = t.w;
     return v;
+}
+// Store through a raw buffer view: an out-of-range offset (kBufOff) drops the
+// store, so a masked row needs no branch.
+__device__ __forceinline__ void bst16(__amdgpu_buffer_rsrc_t r, uint32_t off, const vec16 &v) {
+    const u32x4_t t = {v.u[0], v.u[1], v.u[2], v.u[3]};
+    __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, 0);
 }
 
 // Deferred input gradient of a BN-fed tensor, formed on load as

@@ -43,11 +43,11 @@ namespace bnr {
 
 constexpr int kP3Threads = 512;
 constexpr int kP3BM = 128;          // output rows per tile
-constexpr int kP3MaxW = 62;         // widest image row (ring = 128 + 2 (W + 3) rows)
+constexpr int kP3MaxW = 61;         // widest image row (ring = 128 + 2 (W + 3) rows: fill = two batches)
 
 // LDS layout (bytes): [ring: ring rows, then copies of its first 16 rows (so
-// a 16-row fragment starting anywhere in the ring is contiguous); lda bf16
-// per row]
+// a 16-row fragment starting anywhere in the ring is contiguous), then one
+// junk row for masked writes; lda bf16 per row]
 // [stage: weights Ws[9][NP][ldw] bf16 at the start; afterwards the float32
 // K-slice partial tiles red[WK][128][ldr] and finally the statistics scratch]
 // [coefficients: 3 KP + 4 NP floats].
@@ -67,7 +67,7 @@ static P3Geom p3_geom(int K, int N, int W)
     g.ldw = g.KP + 8;
     g.ldr = g.NP + 4;
     g.ring = kP3BM + 2 * (W + 3);
-    g.ring_bytes = (size_t)(g.ring + 16) * g.lda * 2;
+    g.ring_bytes = (size_t)(g.ring + 17) * g.lda * 2;   // + copies of the first 16 rows + a junk row
     g.PW = W + 2;
     g.PH = 0; g.MP = 0; g.inv_pw = 1.0 / g.PW; g.inv_ph = 0.0;   // set by the launcher
     const size_t wst = (size_t)9 * g.NP * g.ldw * 2;
@@ -80,18 +80,21 @@ static P3Geom p3_geom(int K, int N, int W)
 }
 
 // Pixel of padded position P, or -1 for a padding position or one outside
-// [0, MP).  The float64 quotient is within one of the exact one (P < 2^30).
+// [0, MP).  The float64 quotient is within one of the exact one (|P| < 2^30).
+// Branch-free (selects only): the persistent loops keep their loads in
+// flight across it.
 __device__ __forceinline__ int p3_pixel(int P, const P3Geom &g, int H, int W)
 {
-    if (P < 0 || P >= g.MP) return -1;
     int t = (int)((double)P * g.inv_pw);
     int wp = P - t * g.PW;
-    if (wp < 0) { t--; wp += g.PW; } else if (wp >= g.PW) { t++; wp -= g.PW; }
+    t = wp < 0 ? t - 1 : (wp >= g.PW ? t + 1 : t);
+    wp = P - t * g.PW;
     int img = (int)((double)t * g.inv_ph);
     int hp = t - img * g.PH;
-    if (hp < 0) { img--; hp += g.PH; } else if (hp >= g.PH) { img++; hp -= g.PH; }
-    if (wp == 0 || wp > W || hp == 0 || hp > H) return -1;
-    return (img * H + hp - 1) * W + wp - 1;
+    img = hp < 0 ? img - 1 : (hp >= g.PH ? img + 1 : img);
+    hp = t - img * g.PH;
+    const bool ok = P >= 0 && P < g.MP && wp > 0 && wp <= W && hp > 0 && hp <= H;
+    return ok ? (img * H + hp - 1) * W + wp - 1 : -1;
 }
 
 // WK x WN: 32-channel K slices x 32-column N slices (one per wave); the
@@ -114,6 +117,9 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD;
     constexpr int NVA = (kP3BM * (KPC / VEC) + kP3Threads - 1) / kP3Threads;
     constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1;
+    // batches in flight: one (a second register buffer is merged back into
+    // the first by the compiler, with copies that wait for its loads)
+    constexpr int AHEAD = 1;
     static_assert(WR * WK * WN == 8 && RPT >= 1, "wave layout");
     extern __shared__ __align__(16) unsigned char smem[];
     T *ring = reinterpret_cast<T *>(smem);                       // [ring + 16][lda]
@@ -127,7 +133,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const int wr = wave % WR, wk = (wave / WR) % WK, wn = wave / (WR * WK);
     const int K = p.K, N = p.N, RING = g.ring, lda = g.lda, ldr = g.ldr;
     const int m = (int)p.m;                                      // launcher: m < 2^30
-    const int H = p.h, W = p.w, PW = g.PW, H1 = PW + 1;
+    const int H = p.h, W = p.w, PW = g.PW;
     const int P0 = (int)((int64_t)blockIdx.x * g.MP / gridDim.x);
     const int P1 = (int)((int64_t)(blockIdx.x + 1) * g.MP / gridDim.x);
     const T *wsrc = reinterpret_cast<const T *>(p.wraw);
@@ -139,6 +145,34 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const __amdgpu_buffer_rsrc_t ybuf = buf_view(p.y, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * ES));
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * ES) : 0u);
+
+    // ---- input batches: up to 128 consecutive positions, loaded to registers ----
+    // This thread loads and transforms row tid / 4 of a batch, channel vectors
+    // 4 j + (tid & 3): 4 consecutive lanes cover 64 contiguous bytes of one
+    // pixel, 16 lane groups 16 rows (4 distinct coefficient addresses per
+    // wave: LDS broadcast).  Batch t (positions from P0 + 128 (t + 1) + H1)
+    // replaces ring rows in phase B of tile t; it is loaded AHEAD tiles
+    // earlier into one of two register buffers, so its loads are in flight
+    // for AHEAD tile periods.
+    struct Batch { vec16 a[NVA]; vec16 b[NVB]; int pix; };
+    auto load_rows = [&](int q0, int cnt, Batch &bt) __attribute__((always_inline)) {
+        const int arow = tid >> 2;
+        const int pp = p3_pixel(q0 + arow, g, H, W);
+        bt.pix = arow < cnt ? pp : -1;
+        #pragma unroll
+        for (int j = 0; j < NVA; j++) {
+            const int c = (4 * j + (tid & 3)) * VEC;
+            const bool ok = bt.pix >= 0 && c < K;
+            bt.a[j] = bld16(abuf, ok ? (uint32_t)(bt.pix * a_ldc + c) * ES : kBufOff);
+            if (BNG) bt.b[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(bt.pix * a2_ldc + c) * ES : kBufOff);
+        }
+    };
+    // ring fill: the first tile's window, positions [P0 - H1, P0 + 128 + H1)
+    // = RING rows in two batches, loaded before the weights are staged
+    const int H1 = g.PW + 1;
+    Batch bt0, bt1;
+    load_rows(P0 - H1, kP3BM, bt0);
+    load_rows(P0 - H1 + kP3BM, RING - kP3BM, bt1);
 
     // ---- weights -> LDS stage as Ws[tap][n][k] (zero outside K x N), in
     // batches of kWB vectors per thread whose loads are all in flight before
@@ -211,48 +245,32 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         for (int cb = 0; cb < 2; cb++)
             bfr[tap][cb] = M::load(Ws + (tap * NPC + wn * 32 + cb * 16 + (lane & 15)) * g.ldw + wk * 32 +
                                    (lane >> 4) * M::KPL);
-    // epilogue channels of this thread are fixed: BN parameters in registers
+    // epilogue channels of this thread are fixed (their BN parameters are
+    // read from LDS per tile: registers are the occupancy limit)
     const int v = tid % VPRO, r0 = tid / VPRO;
     const int n = v * VEC;
     const bool col_ok = n < N;
-    float eM[VEC], eR[VEC], eG[VEC], eB[VEC];
-    #pragma unroll
-    for (int e = 0; e < VEC; e++) {
-        eM[e] = epi[n + e]; eR[e] = epi[NPC + n + e]; eG[e] = epi[2 * NPC + n + e]; eB[e] = epi[3 * NPC + n + e];
-    }
 
-    // ---- input batches: up to 128 consecutive positions, loaded to registers ----
-    // This thread loads and transforms row arow of a batch, channel vectors
-    // 4 j + (tid & 3): 4 consecutive lanes cover 64 contiguous bytes of one
-    // pixel, 16 lane groups 16 rows (4 distinct coefficient addresses per
-    // wave: LDS broadcast).
-    const int arow = tid >> 2;
-    int apix = -1;                  // pixel of this thread's row of the batch in flight
-    vec16 ra[NVA], rb[NVB];
-    auto load_rows = [&](int q0, int cnt) __attribute__((always_inline)) {
-        apix = arow < cnt ? p3_pixel(q0 + arow, g, H, W) : -1;
-        #pragma unroll
-        for (int j = 0; j < NVA; j++) {
-            const int c = (4 * j + (tid & 3)) * VEC;
-            const bool ok = apix >= 0 && c < K;
-            ra[j] = bld16(abuf, ok ? (uint32_t)(apix * a_ldc + c) * ES : kBufOff);
-            if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(apix * a2_ldc + c) * ES : kBufOff);
-        }
-    };
-    // prologue transform of the batch in registers, then the ring writes; the
-    // mode switch is wave-uniform and outside the vector loop, so each mode's
-    // vectors are straight-line code
-    auto store_rows = [&](int cnt, int slot0) __attribute__((always_inline)) {
-        if (arow >= cnt) return;
+    // ---- prologue transform of a batch, then the ring writes.  The mode
+    // switch is wave-uniform and outside the vector loop; invalid rows are
+    // zeroed on the packed words and rows past the batch (and the copies of
+    // rows beyond the first 16) go to a junk row, so each mode's vectors are
+    // straight-line code.  32 NVA = KPC: every channel vector is in range. ----
+    static_assert(32 * NVA == KPC, "batch vectors");
+    auto store_rows = [&](int cnt, int slot0, Batch &bt) __attribute__((always_inline)) {
+        const int arow = tid >> 2;
+        const vec16 *ra = bt.a, *rb = bt.b;
         int s = slot0 + arow;
-        if (s >= RING) s -= RING;
-        const bool vrow = apix >= 0;                      // padding rows: zeros
+        s = s >= RING ? s - RING : s;
+        const bool live = arow < cnt;
+        const int s1 = live ? s : RING + 16;
+        const int s2 = live && s < 16 ? s + RING : RING + 16;
+        const uint32_t keep = bt.pix >= 0 ? 0xffffffffu : 0u;    // padding rows: zeros
         vec16 outv[NVA];
         if (BNG) {                                        // PRO_BNGRAD: d = c0 dy + c1 x + c2
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int c = (4 * j + (tid & 3)) * VEC;
-                const bool valid = vrow && c < K;
                 float f[VEC], x[VEC], c0[VEC], c1[VEC], c2[VEC];
                 Elem<T>::unpack(ra[j], f);
                 Elem<T>::unpack(rb[j < NVB ? j : 0], x);
@@ -260,35 +278,32 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 lds_f8(coef + KPC + c, c1);
                 lds_f8(coef + 2 * KPC + c, c2);
                 #pragma unroll
-                for (int e = 0; e < VEC; e++) {
-                    const float d = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
-                    f[e] = valid ? d : 0.f;
-                }
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
                 outv[j] = Elem<T>::pack(f);
+                #pragma unroll
+                for (int i = 0; i < 4; i++) outv[j].u[i] &= keep;
             }
         } else if (p.pro == PRO_BNRELU) {                 // z = max(x c0 + c1, 0)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int c = (4 * j + (tid & 3)) * VEC;
-                const bool valid = vrow && c < K;
                 float f[VEC], ca[VEC], cb[VEC];
                 Elem<T>::unpack(ra[j], f);
                 lds_f8(coef + c, ca);
                 lds_f8(coef + KPC + c, cb);
                 #pragma unroll
-                for (int e = 0; e < VEC; e++) {
-                    const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
-                    f[e] = valid && t > 0.f ? t : 0.f;
-                }
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(__builtin_fmaf(f[e], ca[e], cb[e]), 0.f);
                 outv[j] = Elem<T>::pack(f);
+                #pragma unroll
+                for (int i = 0; i < 4; i++) outv[j].u[i] &= keep;
             }
-        } else if (p.pro == PRO_RELU) {
+        } else if (p.pro == PRO_RELU) {                   // (padding rows load zeros)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 float f[VEC];
                 Elem<T>::unpack(ra[j], f);
                 #pragma unroll
-                for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(f[e], 0.f);
                 outv[j] = Elem<T>::pack(f);
             }
         } else {
@@ -298,14 +313,8 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
             const int c = (4 * j + (tid & 3)) * VEC;
-            if (c < KPC) *reinterpret_cast<vec16 *>(ring + s * lda + c) = outv[j];
-        }
-        if (s < 16) {
-            #pragma unroll
-            for (int j = 0; j < NVA; j++) {
-                const int c = (4 * j + (tid & 3)) * VEC;
-                if (c < KPC) *reinterpret_cast<vec16 *>(ring + (s + RING) * lda + c) = outv[j];
-            }
+            *reinterpret_cast<vec16 *>(ring + s1 * lda + c) = outv[j];
+            *reinterpret_cast<vec16 *>(ring + s2 * lda + c) = outv[j];
         }
     };
 
@@ -315,12 +324,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     float s1[VEC], s2[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
-    T *yout = reinterpret_cast<T *>(p.y);
     auto load_epi = [&](int p0, int nrows) __attribute__((always_inline)) {
         #pragma unroll
         for (int j = 0; j < RPT; j++) {
             const int r = r0 + j * RSTEP;
-            epix[j] = col_ok && r < nrows ? p3_pixel(p0 + r, g, H, W) : -1;
+            const int pp = p3_pixel(p0 + r, g, H, W);
+            epix[j] = col_ok && r < nrows ? pp : -1;
         }
         if (!READS) return;
         #pragma unroll
@@ -332,22 +341,18 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         }
     };
 
-    // ---- ring fill: the first tile's window, positions [P0 - H1, P0 + 128 + H1) ----
-    int L = P0 - H1;                // next position to load; its ring slot is slotL
-    int slotL = 0;
-    while (L < P0 + kP3BM + H1) {
-        const int c0n = P0 + kP3BM + H1 - L < kP3BM ? P0 + kP3BM + H1 - L : kP3BM;
-        load_rows(L, c0n);
-        store_rows(c0n, slotL);
-        L += c0n;
-        slotL += c0n;
-        if (slotL >= RING) slotL -= RING;
-    }
-    // prefetch the batch stored while the first tile's epilogue runs, and
-    // the first tile's epilogue operand
-    int cnt = P1 + H1 - L < kP3BM ? (P1 + H1 - L > 0 ? P1 + H1 - L : 0) : kP3BM;
-    if (cnt > 0) load_rows(L, cnt);
+    // ---- ring fill (slots 0 .. RING-1), then the first AHEAD batches and
+    // the first tile's epilogue operand (issued first: a wait for it then
+    // leaves the batches in flight) ----
+    store_rows(kP3BM, 0, bt0);
+    store_rows(RING - kP3BM, kP3BM, bt1);
+    auto batch_rows = [&](int t) __attribute__((always_inline)) -> int {
+        const int c = P1 + H1 - (P0 + kP3BM + H1 + t * kP3BM);
+        return c < 0 ? 0 : (c > kP3BM ? kP3BM : c);
+    };
     load_epi(P0, P1 - P0 < kP3BM ? P1 - P0 : kP3BM);
+    if (batch_rows(0) > 0) load_rows(P0 + kP3BM + H1, batch_rows(0), bt0);
+    if (AHEAD == 2 && batch_rows(1) > 0) load_rows(P0 + 2 * kP3BM + H1, batch_rows(1), bt1);
     int sb = H1;                    // ring slot of the first row of the current tile
     __syncthreads();
 
@@ -356,16 +361,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     // after next's window replace the rows only this tile needed, the
     // epilogue of this tile runs, and the next batch and epilogue operand are
     // loaded.
-    for (int p0 = P0; p0 < P1; p0 += kP3BM) {
+    auto tile = [&](int p0, Batch &bt) __attribute__((always_inline)) {
         const int nrows = P1 - p0 < kP3BM ? P1 - p0 : kP3BM;
+        const int tt = (p0 - P0) / kP3BM;
 
         // ---- (A) matrix cores: 16 RB rows x 32 columns x 32 K per wave, nine taps ----
-        f32x4 acc[RB][2];
-        #pragma unroll
-        for (int ib = 0; ib < RB; ib++) {
-            acc[ib][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-            acc[ib][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+        f32x4 acc[RB][2];               // set by the first tap's products
         // A fragment = ring row u (wave-uniform) + this lane's fixed offset;
         // the next tap's fragments are read while this tap's are multiplied
         const int lane_off = (lane & 15) * lda + wk * 32 + (lane >> 4) * M::KPL;
@@ -389,8 +390,13 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             else if (tap + 1 < 9) load_tap(tap + 1, af[(tap + 1) % NB]);
             #pragma unroll
             for (int ib = 0; ib < RB; ib++) {
-                M::mma(acc[ib][0], af[tap % NB][ib], bfr[tap][0]);
-                M::mma(acc[ib][1], af[tap % NB][ib], bfr[tap][1]);
+                if (tap == 0) {
+                    M::mma0(acc[ib][0], af[0][ib], bfr[0][0]);
+                    M::mma0(acc[ib][1], af[0][ib], bfr[0][1]);
+                } else {
+                    M::mma(acc[ib][0], af[tap % NB][ib], bfr[tap][0]);
+                    M::mma(acc[ib][1], af[tap % NB][ib], bfr[tap][1]);
+                }
             }
         }
         // ---- float32 partial tile of this K slice -> LDS ----
@@ -406,15 +412,19 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 }
         __syncthreads();
         // ---- (B) ring rows of the tile after next, then this tile's epilogue ----
-        store_rows(cnt, slotL);
-        L += cnt;
-        slotL += cnt;
-        if (slotL >= RING) slotL -= RING;
+        store_rows(batch_rows(tt), (tt * kP3BM) % RING, bt);
         // ---- epilogue row pass: sum of the K slices (fixed order), rounded to
         // the storage type; all outputs of this thread first (no branch,
         // invalid rows contribute zeros), then the stores back to back ----
         {
             vec16 vo[RPT];
+            float eM[VEC], eR[VEC], eG[VEC], eB[VEC];
+            if (EK == EK_BNBWD) {
+                lds_f8(epi + n, eM);
+                lds_f8(epi + NPC + n, eR);
+                lds_f8(epi + 2 * NPC + n, eG);
+                lds_f8(epi + 3 * NPC + n, eB);
+            }
             #pragma unroll
             for (int j = 0; j < RPT; j++) {
                 const int r = r0 + j * RSTEP;
@@ -468,14 +478,20 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             }
             #pragma unroll
             for (int j = 0; j < RPT; j++)
-                if (epix[j] >= 0) stg16(yout + (int64_t)epix[j] * y_ldc + n, vo[j]);
+                bst16(ybuf, epix[j] >= 0 ? (uint32_t)(epix[j] * y_ldc + n) * ES : kBufOff, vo[j]);
         }
-        cnt = P1 + H1 - L < kP3BM ? (P1 + H1 - L > 0 ? P1 + H1 - L : 0) : kP3BM;
-        if (cnt > 0) load_rows(L, cnt);
-        if (p0 + kP3BM < P1) load_epi(p0 + kP3BM, P1 - p0 - kP3BM < kP3BM ? P1 - p0 - kP3BM : kP3BM);
+        // unconditional (past the end: zero rows, out-of-range offsets), so the
+        // compiler's memory counters stay exact across the loop
+        load_epi(p0 + kP3BM, P1 - p0 - kP3BM < kP3BM ? (P1 - p0 - kP3BM > 0 ? P1 - p0 - kP3BM : 0) : kP3BM);
+        load_rows(P0 + kP3BM + H1 + (tt + AHEAD) * kP3BM, batch_rows(tt + AHEAD), bt);
         sb += kP3BM;
         if (sb >= RING) sb -= RING;
         __syncthreads();
+    };
+    for (int p0 = P0; p0 < P1; p0 += 2 * kP3BM) {
+        tile(p0, bt0);
+        if (p0 + kP3BM >= P1) break;
+        tile(p0 + kP3BM, AHEAD == 2 ? bt1 : bt0);
     }
 
     // ---- per-workgroup statistics partial row ----

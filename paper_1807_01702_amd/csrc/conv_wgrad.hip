@@ -337,8 +337,8 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
     static_assert(WCI * WCO == 4 && RB >= 1 && CB >= 1, "wave layout");
     extern __shared__ __align__(16) unsigned char smem[];
     T *Zs = reinterpret_cast<T *>(smem);                          // [zrows][ZP]
-    T *Gs = Zs + (size_t)pl.zrows * ZP;                           // [KQ][GP]
-    float *gco = reinterpret_cast<float *>(Gs + (size_t)pl.KQ * GP);   // BNGRAD coefficients [3][COT]
+    T *Gs = Zs + (size_t)(pl.zrows + 1) * ZP;                     // [KQ + 1][GP]
+    float *gco = reinterpret_cast<float *>(Gs + (size_t)(pl.KQ + 1) * GP);   // BNGRAD coefficients [3][COT]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wci = wave % WCI, wco = wave / WCI;
@@ -381,84 +381,108 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
     const __amdgpu_buffer_rsrc_t gxbuf = buf_view(GS == GB_BNGRAD ? p.gx : p.g,
                                                   GS == GB_BNGRAD ? (uint32_t)(((m - 1) * p.gx_ldc + C_out) * 2) : 0u);
 
-    // position -> pixel of a chunk (-1: zero position)
-    auto chunk_base = [&](int64_t ch, int64_t &img, int &h0) __attribute__((always_inline)) {
+    // The staged rows of this thread are the same in every chunk, so the
+    // 3x3 row -> pixel map is split once into a row offset r (image rows
+    // below the chunk's first row; a large negative value for a row that is
+    // never a pixel) and a pixel offset r W + col - 1; per chunk a pixel is
+    // then one add and one range test (no division in the loop).
+    constexpr int kNever = -(1 << 28);
+    int zrr[NZ], zro[NZ], grr[NG], gro[NG];
+    #pragma unroll
+    for (int j = 0; j < NZ; j++) {
+        zrr[j] = kNever; zro[j] = 0;
         if (TAPS == 3) {
-            img = ch / pl.chunks_per_image;
-            h0 = (int)(ch - img * pl.chunks_per_image) * pl.R;
-        } else {
-            img = ch;
-            h0 = 0;
+            const int row = tid / VZ + j * (kThreads / VZ);
+            const int q = row - (PW + 1);
+            const int r = (q + 2 * PW) / PW - 2;                  // floor(q / PW) for q >= -2 PW
+            const int col = q - r * PW;
+            zrr[j] = row < ZR && col >= 1 && col <= W ? r : kNever;
+            zro[j] = r * W + col - 1;
         }
-    };
-    auto pix = [&](int64_t img, int h0, int q, bool gside) __attribute__((always_inline)) -> int64_t {
+    }
+    #pragma unroll
+    for (int j = 0; j < NG; j++) {
+        grr[j] = kNever; gro[j] = 0;
+        if (TAPS == 3) {
+            const int row = tid / VG + j * (kThreads / VG);
+            const int r = row / PW, col = row - r * PW;
+            grr[j] = row < KQ && r < pl.R && col >= 1 && col <= W ? r : kNever;
+            gro[j] = r * W + col - 1;
+        }
+    }
+    // pixel of staged row j (Z side: zside) of a chunk whose first pixel is
+    // base (3x3: (img H + h0) W; 1x1: img 64), or -1; 32-bit (launcher: every
+    // pixel index below 2^30), selects only
+    auto pix = [&](int base, int h0, int j, bool zside) __attribute__((always_inline)) -> int {
         if (TAPS == 1) {
-            const int64_t pp = img * KQMAX + q;
-            return q < KQ && pp < m ? pp : -1;
+            const int q = tid / (zside ? VZ : VG) + j * (kThreads / (zside ? VZ : VG));
+            const int pp = base + q;
+            return (q < KQ) & (pp < (int)m) ? pp : -1;
         }
-        const int r = (q + 2 * PW) / PW - 2;                      // floor(q / PW) for q >= -2 PW
-        const int col = q - r * PW;
-        const int h = h0 + r;
-        if (gside && r >= pl.R) return -1;
-        if (h < 0 || h >= H || col < 1 || col > W) return -1;
-        return (img * H + h) * W + (col - 1);
+        const int r = zside ? zrr[j] : grr[j];
+        const int o = zside ? zro[j] : gro[j];
+        return (unsigned)(h0 + r) < (unsigned)H ? base + o : -1;
+    };
+    // 32-bit element offsets (launcher: every operand span below 2^31 bytes)
+    const int xl = (int)p.x_ldc, gl = (int)p.g_ldc, gxl = (int)p.gx_ldc;
+    auto chunk_pix0 = [&](int64_t img, int h0) __attribute__((always_inline)) -> int {
+        return TAPS == 3 ? (int)((img * H + h0) * W) : (int)(img * KQMAX);
     };
 
     vec16 zr[NZ], gr[NG], gx[NGX];
-    auto load_chunk = [&](int64_t ch) __attribute__((always_inline)) {
-        int64_t img; int h0;
-        chunk_base(ch, img, h0);
+    auto load_chunk = [&](int64_t img, int h0) __attribute__((always_inline)) {
+        const int base = chunk_pix0(img, h0);
         #pragma unroll
         for (int j = 0; j < NZ; j++) {
             const int row = tid / VZ + j * (kThreads / VZ);
-            const int64_t q = row < ZR ? pix(img, h0, TAPS == 3 ? row - (PW + 1) : row, false) : -1;
-            zr[j] = bld16(xbuf, q >= 0 && zc_ok ? (uint32_t)((q * p.x_ldc + cz) * 2) : kBufOff);
+            const int q = pix(base, h0, j, true);
+            const bool ok = (row < ZR) & (q >= 0) & zc_ok;
+            zr[j] = bld16(xbuf, ok ? (uint32_t)(q * xl + cz) * 2u : kBufOff);
         }
         #pragma unroll
         for (int j = 0; j < NG; j++) {
             const int row = tid / VG + j * (kThreads / VG);
-            const int64_t q = row < KQ ? pix(img, h0, row, true) : -1;
-            const bool ok = q >= 0 && gc_ok;
+            const int q = pix(base, h0, j, false);
+            const bool ok = (row < KQ) & (q >= 0) & gc_ok;
             if (GS == GB_POOLUP) {
-                const int64_t im = q / ((int64_t)H * W);
-                const int rem = (int)(q - im * H * W);
+                // 32-bit quotients (launcher: every pixel index below 2^31)
+                const int qi = q > 0 ? (int)q : 0;
+                const int im = qi / (H * W);
+                const int rem = qi - im * H * W;
                 const int y = rem / W, xx = rem - y * W;
-                const int64_t qq = (im * (H / 2) + y / 2) * (W / 2) + xx / 2;
-                gr[j] = bld16(gbuf, ok ? (uint32_t)((qq * p.g_ldc + cg) * 2) : kBufOff);
+                const int64_t qq = ((int64_t)im * (H / 2) + y / 2) * (W / 2) + xx / 2;
+                gr[j] = bld16(gbuf, ok ? (uint32_t)((int)qq * gl + cg) * 2u : kBufOff);
             } else {
-                gr[j] = bld16(gbuf, ok ? (uint32_t)((q * p.g_ldc + cg) * 2) : kBufOff);
+                gr[j] = bld16(gbuf, ok ? (uint32_t)(q * gl + cg) * 2u : kBufOff);
             }
-            if (GS == GB_BNGRAD) gx[j < NGX ? j : 0] = bld16(gxbuf, ok ? (uint32_t)((q * p.gx_ldc + cg) * 2) : kBufOff);
+            if (GS == GB_BNGRAD) gx[j < NGX ? j : 0] = bld16(gxbuf, ok ? (uint32_t)(q * gxl + cg) * 2u : kBufOff);
         }
     };
-    auto store_chunk = [&](int64_t ch) __attribute__((always_inline)) {
-        int64_t img; int h0;
-        chunk_base(ch, img, h0);
+    // Prologue transforms as straight-line code: the ReLU is max(t, zlo)
+    // (zlo = -inf without one), invalid rows are zeroed on the packed words,
+    // and rows past the staged range go to a junk row (no per-row branch).
+    const float zlo = p.a_mode != 0 ? 0.f : -__builtin_inff();
+    auto store_chunk = [&](int64_t img, int h0) __attribute__((always_inline)) {
+        const int base = chunk_pix0(img, h0);
         #pragma unroll
         for (int j = 0; j < NZ; j++) {
             const int row = tid / VZ + j * (kThreads / VZ);
-            if (row >= ZR) continue;
-            vec16 out = zr[j];
-            if (p.a_mode != 0) {
-                const bool valid = pix(img, h0, TAPS == 3 ? row - (PW + 1) : row, false) >= 0 && zc_ok;
-                float f[VEC];
-                Elem<T>::unpack(zr[j], f);
-                #pragma unroll
-                for (int e = 0; e < VEC; e++) {
-                    const float t = p.a_mode == 1 ? __builtin_fmaf(f[e], za[e], zb[e]) : f[e];
-                    f[e] = valid && t > 0.f ? t : 0.f;
-                }
-                out = Elem<T>::pack(f);
-            }
-            *reinterpret_cast<vec16 *>(Zs + row * ZP + vz * VEC) = out;
+            const bool valid = (row < ZR) & (pix(base, h0, j, true) >= 0) & zc_ok;
+            float f[VEC];
+            Elem<T>::unpack(zr[j], f);
+            #pragma unroll
+            for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(__builtin_fmaf(f[e], za[e], zb[e]), zlo);
+            vec16 out = Elem<T>::pack(f);
+            #pragma unroll
+            for (int i = 0; i < 4; i++) out.u[i] = valid ? out.u[i] : 0u;
+            *reinterpret_cast<vec16 *>(Zs + (row < ZR ? row : ZR) * ZP + vz * VEC) = out;
         }
         #pragma unroll
         for (int j = 0; j < NG; j++) {
             const int row = tid / VG + j * (kThreads / VG);
-            if (row >= KQ) continue;
             vec16 out = gr[j];
             if (GS == GB_BNGRAD) {
-                const bool valid = pix(img, h0, row, true) >= 0 && gc_ok;
+                const bool valid = (row < KQ) & (pix(base, h0, j, false) >= 0) & gc_ok;
                 float d[VEC], x[VEC], gA[VEC], gB[VEC], gC[VEC];
                 Elem<T>::unpack(gr[j], d);
                 Elem<T>::unpack(gx[j < NGX ? j : 0], x);
@@ -466,11 +490,10 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
                 lds_f8(gco + COT + vg * VEC, gB);
                 lds_f8(gco + 2 * COT + vg * VEC, gC);
                 #pragma unroll
-                for (int e = 0; e < VEC; e++) {
-                    const float v = __builtin_fmaf(gA[e], d[e], __builtin_fmaf(gB[e], x[e], gC[e]));
-                    d[e] = valid ? v : 0.f;
-                }
+                for (int e = 0; e < VEC; e++) d[e] = __builtin_fmaf(gA[e], d[e], __builtin_fmaf(gB[e], x[e], gC[e]));
                 out = Elem<T>::pack(d);
+                #pragma unroll
+                for (int i = 0; i < 4; i++) out.u[i] = valid ? out.u[i] : 0u;
             } else if (GS == GB_POOLUP) {
                 float d[VEC];
                 Elem<T>::unpack(gr[j], d);
@@ -478,7 +501,7 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
                 for (int e = 0; e < VEC; e++) d[e] *= 0.25f;
                 out = Elem<T>::pack(d);
             }
-            *reinterpret_cast<vec16 *>(Gs + row * GP + vg * VEC) = out;
+            *reinterpret_cast<vec16 *>(Gs + (row < KQ ? row : KQ) * GP + vg * VEC) = out;
         }
     };
 
@@ -495,13 +518,37 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
     const T *za_base = Zs + (8 * g16 + (j16 >> 2)) * ZP + 4 * (j16 & 3) + wci * RB * 16;
     const T *gb_base = Gs + (8 * g16 + (j16 >> 2)) * GP + 4 * (j16 & 3) + wco * CB * 16;
 
+    // chunk positions (image, first row) advanced incrementally
     const int64_t ch_begin = (int64_t)split * pl.chunks_per_split;
     const int64_t ch_end = min(pl.nchunks, ch_begin + pl.chunks_per_split);
-    if (ch_begin < ch_end) load_chunk(ch_begin);
+    struct Pos { int64_t img; int h0, cin; };
+    auto first = [&]() -> Pos {
+        Pos q;
+        if (TAPS == 3) {
+            q.img = ch_begin / pl.chunks_per_image;
+            q.cin = (int)(ch_begin - q.img * pl.chunks_per_image);
+            q.h0 = q.cin * pl.R;
+        } else {
+            q.img = ch_begin; q.cin = 0; q.h0 = 0;
+        }
+        return q;
+    };
+    auto advance = [&](Pos &q) __attribute__((always_inline)) {
+        if (TAPS == 3) {
+            q.cin++; q.h0 += pl.R;
+            if (q.cin == pl.chunks_per_image) { q.cin = 0; q.h0 = 0; q.img++; }
+        } else {
+            q.img++;
+        }
+    };
+    Pos ps = first(), pn = ps;
+    if (ch_begin < ch_end) load_chunk(pn.img, pn.h0);
     for (int64_t ch = ch_begin; ch < ch_end; ch++) {
-        store_chunk(ch);
+        store_chunk(ps.img, ps.h0);
         __syncthreads();
-        if (ch + 1 < ch_end) load_chunk(ch + 1);
+        advance(pn);
+        if (ch + 1 < ch_end) load_chunk(pn.img, pn.h0);
+        advance(ps);
         for (int kq = 0; kq < KQ; kq += M::KSTEP) {
             typename M::frag b[CB];
             #pragma unroll
@@ -557,7 +604,7 @@ template <int TAPS, int CIT, int COT, int WCI>
 static hipError_t run_wgrad_tr(const WgradParams &p, const WgTrPlan &pl, hipStream_t s)
 {
     const int64_t blocks = (int64_t)pl.ci_tiles * pl.co_tiles * pl.splits;
-    const size_t lds = ((size_t)pl.zrows * (CIT + 8) + (size_t)pl.KQ * (COT + 8)) * 2 + 3 * COT * sizeof(float);
+    const size_t lds = ((size_t)(pl.zrows + 1) * (CIT + 8) + (size_t)(pl.KQ + 1) * (COT + 8)) * 2 + 3 * COT * sizeof(float);
     const double m = (double)p.m;
     double g = m * p.c_out;
     if (p.gsrc == GB_BNGRAD) g *= 2.0;

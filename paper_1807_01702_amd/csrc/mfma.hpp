@@ -28,6 +28,11 @@ template <> struct Mfma<bf16_t> {
     __device__ static __forceinline__ void mma(f32x4 &c, frag a, frag b) {
         c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
     }
+    // c = a b (a zero accumulator as the inline constant: no register clears)
+    __device__ static __forceinline__ void mma0(f32x4 &c, frag a, frag b) {
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, z, 0, 0, 0);
+    }
 };
 
 template <> struct Mfma<float> {

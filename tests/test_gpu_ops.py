@@ -61,7 +61,8 @@ FWD_CASES = [
     (True, 1, 1, 9, 11, 40, 136, 48, 136),       # ragged channels / pixels
     (True, 3, 3, 1, 1, 64, 64, 64, 64),          # H = W = 1: only the centre tap
     (True, 3, 1, 56, 56, 64, 64, 64, 64),        # full-width rows (W = 56)
-    (True, 3, 2, 6, 62, 32, 8, 32, 8),           # widest supported 3x3 rows
+    (True, 3, 2, 6, 61, 32, 8, 32, 8),           # widest rows of the persistent 3x3 kernel
+    (True, 3, 1, 5, 62, 32, 8, 32, 8),           # one column past it (row-tile kernel)
 ]
 
 
