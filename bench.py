@@ -60,7 +60,8 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true")
-    ap.add_argument("--only", choices=["fused", "fused_no_icf", "fused_overlap", "unfused", "unfused_rcf",
+    ap.add_argument("--only", choices=["fused", "fused_no_icf", "fused_overlap", "fused_robust", "unfused",
+                                       "unfused_rcf",
                                        "unfused_rcf_mvf"],
                     default=None)
     ap.add_argument("--no-ablation", action="store_true")
@@ -83,6 +84,8 @@ def build_workloads(args, torch):
         variants.insert(1, ("fused_no_icf", dict(fused=True, icf=False)))
         # the same fused step with the weight gradients on a side stream
         variants.insert(2, ("fused_overlap", dict(fused=True, overlap=True)))
+        # the same fused step with robust one-sweep statistics (sums around the running mean)
+        variants.insert(3, ("fused_robust", dict(fused=True, robust=True)))
     if args.workload in ("dense_block", "resnet_stack", "densenet121") and not args.no_ablation:
         # the paper's intermediate endpoints (Sec. 5): ReLU-CONV fusion, then + mean/variance fusion
         from paper_1807_01702_amd import bnr as B

@@ -89,6 +89,21 @@ typedef struct {
     float *var;            /* [C] biased mini-batch variance (may be NULL)         */
     float *rstd;           /* [C] 1/sqrt(var + eps)                                */
     float eps;             /* > 0                                                  */
+    /* Robust one-sweep statistics (optional; NULL/0 leaves every result as
+     * above).  With shift K set, the one-sweep producers (statistics sweep,
+     * CONV statistics epilogues, stem CONV, max pooling) accumulate
+     * sum(x - K) and sum((x - K)^2) and the finalisation forms
+     * mean = K + S1/m, var = S2/m - (S1/m)^2: the same values in exact
+     * arithmetic (Sec. 3.2, mean/variance fusion), without the cancellation of
+     * E[x^2] - E[x]^2 when |mean| >> std (K = e.g. the running mean).  The
+     * two-pass (unfused) statistics ignore K.  With running_mean set the
+     * finalisation also updates running_mean (and running_var, unbiased
+     * m/(m-1) scaling, when set): r = (1 - momentum) r + momentum * batch
+     * value.  shift may alias running_mean (read before the update). */
+    const float *shift;    /* [C] or NULL                                          */
+    float *running_mean;   /* [C] or NULL                                          */
+    float *running_var;    /* [C] or NULL                                          */
+    float momentum;        /* in [0, 1]                                            */
 } bnr_bn;
 
 /* Where the gradient of a CONV's output comes from (backward entry points). */

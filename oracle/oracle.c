@@ -158,6 +158,34 @@ void orc_mvf_stats(long m, int C, const double *x, double *mean, double *var)
     }
 }
 
+/* Shifted one-sweep statistics: the mean/variance-fusion identity of Sec. 3.2
+ * applied to d = x - K for a per-channel constant K (the robust reading of
+ * one-sweep statistics; the paper itself names higher precision as the
+ * remedy for the cancellation of E(X^2) - E(X)^2).  With S1 = sum d and
+ * S2 = sum d^2:  mean = K + S1/m,  var = S2/m - (S1/m)^2. */
+void orc_mvf_stats_shifted(long m, int C, const double *x, const double *K, double *mean, double *var)
+{
+    #pragma omp parallel for schedule(static)
+    for (int c = 0; c < C; c++) {
+        double s = 0.0, s2 = 0.0;
+        for (long i = 0; i < m; i++) { double d = x[i * C + c] - K[c]; s += d; s2 += d * d; }
+        double d1 = s / (double)m, d2 = s2 / (double)m;
+        mean[c] = K[c] + d1;
+        var[c] = d2 - d1 * d1;
+    }
+}
+
+/* Running statistics of BN for inference (the usual exponential moving
+ * average): r = (1 - mo) r + mo * batch value, the variance taken unbiased,
+ * var * m / (m - 1). */
+void orc_running_update(int C, long m, double mo, const double *mean, const double *var, double *rmean, double *rvar)
+{
+    for (int c = 0; c < C; c++) {
+        rmean[c] = (1.0 - mo) * rmean[c] + mo * mean[c];
+        rvar[c] = (1.0 - mo) * rvar[c] + mo * var[c] * ((double)m / (double)(m - 1));
+    }
+}
+
 /* BN training backward.  With xhat = (x - mean) * rstd recomputed from x:
  *   dbeta  = sum dy,   dgamma = sum dy * xhat,
  *   dx     = gamma * rstd * (dy - dbeta/m - xhat * dgamma/m).

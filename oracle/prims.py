@@ -98,6 +98,25 @@ def mvf_stats(x):
     return mean, var
 
 
+def mvf_stats_shifted(x, K):
+    """One-sweep statistics around a per-channel shift K: (mean, var)."""
+    x2 = _f64(x).reshape(-1, x.shape[-1])
+    m, C = x2.shape
+    k = np.ascontiguousarray(np.broadcast_to(_f64(K), (C,)))
+    mean, var = np.empty(C), np.empty(C)
+    lib().orc_mvf_stats_shifted(ctypes.c_long(m), C, _p(x2), _p(k), _p(mean), _p(var))
+    return mean, var
+
+
+def running_update(rmean, rvar, mean, var, m, momentum):
+    """Exponential moving average of the batch statistics (unbiased variance); returns new arrays."""
+    C = len(mean)
+    rm, rv = _f64(rmean).copy(), _f64(rvar).copy()
+    lib().orc_running_update(C, ctypes.c_long(m), ctypes.c_double(momentum), _p(_f64(mean)), _p(_f64(var)),
+                             _p(rm), _p(rv))
+    return rm, rv
+
+
 def bn_bwd(x, dy, gamma, mean, rstd, want_dx=True):
     """Returns (dx or None, dgamma, dbeta)."""
     shape = x.shape

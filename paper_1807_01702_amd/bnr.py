@@ -37,7 +37,8 @@ class ConvDesc(ctypes.Structure):
 
 
 class BNStruct(ctypes.Structure):
-    _fields_ = [("gamma", c_vp), ("beta", c_vp), ("mean", c_vp), ("var", c_vp), ("rstd", c_vp), ("eps", c_f)]
+    _fields_ = [("gamma", c_vp), ("beta", c_vp), ("mean", c_vp), ("var", c_vp), ("rstd", c_vp), ("eps", c_f),
+                ("shift", c_vp), ("running_mean", c_vp), ("running_var", c_vp), ("momentum", c_f)]
 
 
 class GradSrc(ctypes.Structure):
@@ -205,7 +206,15 @@ def workspace(nbytes, device=None, slot=0):
 
 
 class BN:
-    """Per-channel BN state: gamma, beta (inputs), mean, var, rstd (batch statistics), eps."""
+    """Per-channel BN state: gamma, beta (inputs), mean, var, rstd (batch statistics), eps.
+
+    Optional robust one-sweep statistics: ``shift`` (per-channel K: the
+    one-sweep producers sum x - K and (x - K)^2) and running statistics
+    (``running_mean``, ``running_var``, ``momentum``) updated by the producer;
+    set them with :meth:`robust`."""
+
+    shift = running_mean = running_var = None
+    momentum = 0.0
 
     def __init__(self, gamma, beta, eps=1e-5, mean=None, var=None, rstd=None):
         dev, c = gamma.device, gamma.shape[0]
@@ -213,6 +222,12 @@ class BN:
         self.mean = mean if mean is not None else torch.empty(c, dtype=torch.float32, device=dev)
         self.var = var if var is not None else torch.empty(c, dtype=torch.float32, device=dev)
         self.rstd = rstd if rstd is not None else torch.empty(c, dtype=torch.float32, device=dev)
+
+    def robust(self, shift=None, running_mean=None, running_var=None, momentum=0.1):
+        """Sum around shift (may be running_mean itself) and/or update running statistics; returns self."""
+        self.shift, self.running_mean, self.running_var = shift, running_mean, running_var
+        self.momentum = float(momentum)
+        return self
 
     @classmethod
     def stats_only(cls, c, device, eps=1e-5):
@@ -237,7 +252,8 @@ class BN:
 
     def struct(self):
         return BNStruct(_ptr(self.gamma), _ptr(self.beta), _ptr(self.mean), _ptr(self.var), _ptr(self.rstd),
-                        self.eps)
+                        self.eps, _ptr(self.shift), _ptr(self.running_mean), _ptr(self.running_var),
+                        self.momentum)
 
 
 def conv_desc(n, h, w, c_in, c_out, k, in_ldc, out_ldc, dtype):

@@ -102,7 +102,25 @@ bnr_status check_bn(const bnr_bn *bn, const char *name, bool need_affine, bool n
     TRY(check_fptr(bn->rstd, "bn.rstd"));
     if (bn->var && reinterpret_cast<uintptr_t>(bn->var) % 4) return fail(BNR_ERR_ALIGN, "bn.var misaligned");
     if (need_stats_out && !(bn->eps > 0.0f)) return fail(BNR_ERR_SHAPE, "%s.eps must be > 0", name);
+    if (need_stats_out) {
+        const auto mis = [](const void *q) { return reinterpret_cast<uintptr_t>(q) % 4 != 0; };
+        if (mis(bn->shift) || mis(bn->running_mean) || mis(bn->running_var))
+            return fail(BNR_ERR_ALIGN, "%s shift / running statistics misaligned", name);
+        if (bn->running_var && !bn->running_mean)
+            return fail(BNR_ERR_NULL, "%s.running_var set without running_mean", name);
+        if (bn->running_mean && !(bn->momentum >= 0.0f && bn->momentum <= 1.0f))
+            return fail(BNR_ERR_SHAPE, "%s.momentum must be in [0, 1]", name);
+    }
     return BNR_OK;
+}
+
+// forward finalisation terms of a statistics producer: the one-sweep shift
+// (FIN_MVF) and the running statistics
+SplitTerms fwd_terms(const bnr_bn *bn, bool one_sweep)
+{
+    SplitTerms t{nullptr, nullptr, nullptr, nullptr, 0, one_sweep ? bn->shift : nullptr, bn->running_mean,
+                 bn->running_var, bn->momentum};
+    return t;
 }
 
 bnr_status check_desc(const bnr_conv_desc *d)
@@ -188,10 +206,11 @@ bnr_status run_stats(int64_t m, int c, int ldc, bnr_dtype dt, const void *x, bnr
     const int64_t R = stats_row_blocks(m, c, dt_of(dt));
     float *part = (float *)ws;
     void *red = (char *)ws + stats_part_bytes(m, c);
-    TRY_HIP(launch_stats_partial(dt_of(dt), x, ldc, m, c, ST_SUMSQ, nullptr, nullptr, nullptr, 0, part, R, s),
+    TRY_HIP(launch_stats_partial(dt_of(dt), x, ldc, m, c, ST_SUMSQ, bn->shift, nullptr, nullptr, 0, part, R, s),
             "stats sweep");
+    const SplitTerms ft = fwd_terms(bn, true);
     TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MVF, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr, red,
-                                  s),
+                                  s, &ft),
             "stats combine");
     return BNR_OK;
 }
@@ -252,7 +271,7 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
         TRY_HIP(launch_conv1x1(rp, s, rows), transpose ? "conv data gradient" : "conv forward");
         return BNR_OK;
     }
-    if (rp.taps == 9 && rp.pro != PRO_POOLUP && !rp.e_scale && conv3x3_supported(rp.dtype, rp.K, rp.N, rp.w)) {
+    if (rp.taps == 9 && rp.pro != PRO_POOLUP && !rp.e_scale && conv3x3_supported(rp.dtype, rp.K, rp.N, rp.h, rp.w)) {
         rp.wraw = w;
         rp.wtrans = transpose;
         *rows = conv3x3_partial_rows(rp.m);
@@ -298,11 +317,13 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     rp.epi = y_bn ? EPI_STATS : EPI_STORE;
     rp.y = y; rp.y_ldc = d->out_ldc;
     rp.part = part;
+    rp.e_shift = y_bn ? y_bn->shift : nullptr;
     int64_t R = 0;
     TRY(launch_conv_any(rp, d, w, 0, wpack, &R, s));
     if (y_bn) {
+        const SplitTerms ft = fwd_terms(y_bn, true);
         TRY_HIP(launch_stats_finalize(part, R, d->c_out, m, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
-                                      nullptr, nullptr, wp.red, s),
+                                      nullptr, nullptr, wp.red, s, &ft),
                 "stats combine");
     }
     return ok();
@@ -723,10 +744,11 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
             return fail(BNR_ERR_ALIAS, "out overlaps x");
         const int64_t R = stats_row_blocks(m, d->c_in, dt);
         if (mode == BNR_MODE_RCF_MVF) {
-            TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUMSQ, nullptr, nullptr, nullptr, 0, part,
-                                         R, s), "stats sweep");
+            TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUMSQ, bn->shift, nullptr, nullptr, 0,
+                                         part, R, s), "stats sweep");
+            const SplitTerms ft = fwd_terms(bn, true);
             TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_MVF, bn->eps, bn->mean, bn->var, bn->rstd,
-                                          nullptr, nullptr, red, s), "stats combine");
+                                          nullptr, nullptr, red, s, &ft), "stats combine");
         } else {
             // mean sweep, then variance sweep (two-pass, as the unfused BN layer)
             TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUM, nullptr, nullptr, nullptr, 0, part,
@@ -735,8 +757,9 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
                                           nullptr, red, s), "mean combine");
             TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SQDEV, bn->mean, nullptr, nullptr, 0,
                                          part, R, s), "variance sweep");
-            TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_VAR, bn->eps, nullptr, bn->var, bn->rstd, nullptr,
-                                          nullptr, red, s), "variance combine");
+            const SplitTerms ft = fwd_terms(bn, false);
+            TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_VAR, bn->eps, bn->mean, bn->var, bn->rstd, nullptr,
+                                          nullptr, red, s, &ft), "variance combine");
         }
         TRY_HIP(launch_elementwise(dt, EW_APPLY, m, d->c_in, a->x, d->in_ldc, nullptr, 0, bn->gamma, bn->beta,
                                    bn->mean, bn->rstd, nullptr, nullptr, a->y, d->c_in, 0, s), "normalise");
@@ -898,8 +921,9 @@ bnr_status bnr_reference_bn_add_relu(int32_t backward, int64_t m, int32_t c, bnr
                                       red, s), "mean combine");
         TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_SQDEV, bn->mean, nullptr, nullptr, 0, part, R, s),
                 "variance sweep");
-        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, nullptr, bn->var, bn->rstd, nullptr, nullptr,
-                                      red, s), "variance combine");
+        const SplitTerms ft = fwd_terms(bn, false);
+        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr,
+                                      red, s, &ft), "variance combine");
         TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->y, a->y_ldc, nullptr, 0, bn->gamma, bn->beta, bn->mean,
                                    bn->rstd, nullptr, nullptr, a->tmp, c, 0, s), "normalise");
         TRY_HIP(launch_elementwise(dt, EW_ADDRELU, m, c, a->tmp, c, a->id, a->id_ldc, nullptr, nullptr, nullptr,
@@ -956,8 +980,9 @@ bnr_status bnr_reference_bn_relu(int32_t backward, int64_t m, int32_t c, bnr_dty
                                       red, s), "mean combine");
         TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_SQDEV, bn->mean, nullptr, nullptr, 0, part, R, s),
                 "variance sweep");
-        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, nullptr, bn->var, bn->rstd, nullptr, nullptr,
-                                      red, s), "variance combine");
+        const SplitTerms ft = fwd_terms(bn, false);
+        TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr,
+                                      red, s, &ft), "variance combine");
         TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->x, a->x_ldc, nullptr, 0, bn->gamma, bn->beta, bn->mean,
                                    bn->rstd, nullptr, nullptr, a->y, c, 0, s), "normalise");
         TRY_HIP(launch_elementwise(dt, EW_RELU, m, c, a->y, c, nullptr, 0, nullptr, nullptr, nullptr, nullptr, nullptr,
@@ -1126,14 +1151,16 @@ bnr_status bnr_stem_conv_fwd(const bnr_stem_desc *d, const void *img, const void
         return fail(BNR_ERR_ALIAS, "s overlaps w");
     p.img = img; p.wt = w; p.s = s;
     p.part = (float *)ws;
+    p.shift = s_bn ? s_bn->shift : nullptr;
     hipStream_t st = (hipStream_t)stream;
     const int dt = dt_of(d->dtype);
     TRY_HIP(launch_stem_conv(dt, p, s_bn && dt == DT_BF16, st), "first conv");
     if (s_bn) {
         if (dt == DT_BF16) {
             const int64_t R = stem_groups((int64_t)p.n * ((p.ho + kStemRows - 1) / kStemRows));
+            const SplitTerms ft = fwd_terms(s_bn, true);
             TRY_HIP(launch_stats_finalize(p.part, R, kStemCout, m, FIN_MVF, s_bn->eps, s_bn->mean, s_bn->var,
-                                          s_bn->rstd, nullptr, nullptr, (char *)ws + sw.part, st),
+                                          s_bn->rstd, nullptr, nullptr, (char *)ws + sw.part, st, &ft),
                     "stats combine");
         } else {
             TRY(run_stats(m, kStemCout, kStemCout, d->dtype, s, s_bn, ws, st));
@@ -1222,15 +1249,17 @@ bnr_status bnr_bn_relu_maxpool_fwd(int32_t n, int32_t h, int32_t w, int32_t c, b
     p.x = x; p.x_ldc = x_ldc; p.y = y; p.y_ldc = y_ldc;
     if (x_bn) { p.gamma = x_bn->gamma; p.beta = x_bn->beta; p.mean = x_bn->mean; p.rstd = x_bn->rstd; }
     p.part = (float *)ws;
+    p.shift = y_bn ? y_bn->shift : nullptr;
     hipStream_t st = (hipStream_t)stream;
     const int dt = dt_of(dtype);
     TRY_HIP(launch_maxpool_fwd(dt, p, x_bn != nullptr, y_bn != nullptr, st), "max pooling");
     if (y_bn) {
         const int64_t R = (int64_t)ceil_div(m_out, ceil_div(m_out, maxpool_fwd_rows(dt, m_out, c)));
+        const SplitTerms ft = fwd_terms(y_bn, true);
         TRY_HIP(launch_stats_finalize(p.part, R, c, m_out, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
                                       nullptr, nullptr, (char *)ws + align_up((size_t)pool_ws(n, h, w, c) -
                                                                                align_up(stats_red_bytes(c))),
-                                      st),
+                                      st, &ft),
                 "stats combine");
     }
     return ok();

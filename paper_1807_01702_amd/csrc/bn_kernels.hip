@@ -17,7 +17,8 @@ namespace bnr {
 // --------------------------------------------------------------------------
 // Per-channel partial sums over a row block (MODE is a template argument so
 // every load of a 4-row batch is issued before any arithmetic).
-//   ST_SUMSQ : s1 = sum x,            s2 = sum x^2        (mean/variance fusion)
+//   ST_SUMSQ : s1 = sum (x - K),      s2 = sum (x - K)^2  (mean/variance fusion; K = the
+//              per-channel shift passed as `mean`, 0 if NULL)
 //   ST_SUM   : s1 = sum x                                 (unfused mean sweep)
 //   ST_SQDEV : s1 = sum (x - mean)^2                      (unfused variance sweep)
 //   ST_DYX   : s1 = sum dy,           s2 = sum dy * xhat  (BN backward sums)
@@ -30,7 +31,7 @@ __device__ __forceinline__ void stats_accum(const vec16 &v, const vec16 &d, cons
     float f[VEC];
     Elem<T>::unpack(v, f);
     if (MODE == ST_SUMSQ) {
-        for (int i = 0; i < VEC; i++) { s1[i] += f[i]; s2[i] += f[i] * f[i]; }
+        for (int i = 0; i < VEC; i++) { const float e = f[i] - mu[i]; s1[i] += e; s2[i] += e * e; }
     } else if (MODE == ST_SUM) {
         for (int i = 0; i < VEC; i++) s1[i] += f[i];
     } else if (MODE == ST_SQDEV) {
@@ -57,7 +58,7 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
     float s1[VEC], s2[VEC], mu[VEC], rs[VEC];
     for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f; }
-    if (ty < ry && (MODE == ST_SQDEV || MODE == ST_DYX))
+    if (ty < ry && (MODE == ST_SQDEV || MODE == ST_DYX || (MODE == ST_SUMSQ && mean)))
         for (int i = 0; i < VEC; i++) mu[i] = mean[c0 + i];
     if (ty < ry && MODE == ST_DYX)
         for (int i = 0; i < VEC; i++) rs[i] = rstd[c0 + i];
@@ -101,9 +102,11 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
 // --------------------------------------------------------------------------
 // Finalisation shared by the combine kernels: from the float64 sums a = s1,
 // b = s2 of one channel write
-//   FIN_MVF   : mean = a/m, var = b/m - mean^2 (clamped at 0), rstd
+//   FIN_MVF   : with K = st.shift (0 if NULL; the sums are of x - K):
+//               mean = K + a/m, var = b/m - (a/m)^2 (clamped at 0), rstd
 //   FIN_MEAN  : mean = a/m
 //   FIN_VAR   : var = a/m, rstd            (two-pass variance)
+//   (FIN_MVF, FIN_VAR: running statistics updated when st.rmean is set)
 //   FIN_BWD   : dbeta = a, dgamma = b, and the summed-gradient terms of st
 //               (SplitTerms) when st.alpha is set
 __device__ __forceinline__ void stats_write(int mode, int c, double a, double b, int64_t m, float eps, float *mean,
@@ -111,19 +114,27 @@ __device__ __forceinline__ void stats_write(int mode, int c, double a, double b,
                                             const SplitTerms &st)
 {
     const double dm = (double)m;
-    if (mode == FIN_MVF) {
-        const double mu = a / dm;
-        double v = b / dm - mu * mu;
-        if (v < 0.0) v = 0.0;
-        mean[c] = (float)mu;
+    if (mode == FIN_MVF || mode == FIN_VAR) {
+        double mu, v;
+        if (mode == FIN_MVF) {                    // sums of x - K
+            const double ms = a / dm;
+            v = b / dm - ms * ms;
+            if (v < 0.0) v = 0.0;
+            mu = (st.shift ? (double)st.shift[c] : 0.0) + ms;
+            mean[c] = (float)mu;
+        } else {                                  // two-pass: a = sum (x - mean)^2
+            v = a / dm;
+            mu = st.rmean ? (double)mean[c] : 0.0;
+        }
         if (var) var[c] = (float)v;
         rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
+        if (st.rmean) {
+            const double mo = (double)st.momentum;
+            st.rmean[c] = (float)((1.0 - mo) * (double)st.rmean[c] + mo * mu);
+            if (st.rvar) st.rvar[c] = (float)((1.0 - mo) * (double)st.rvar[c] + mo * v * (dm > 1.0 ? dm / (dm - 1.0) : 1.0));
+        }
     } else if (mode == FIN_MEAN) {
         mean[c] = (float)(a / dm);
-    } else if (mode == FIN_VAR) {
-        const double v = a / dm;
-        if (var) var[c] = (float)v;
-        rstd[c] = (float)(1.0 / sqrt(v + (double)eps));
     } else {
         dbeta[c] = (float)a;
         dgamma[c] = (float)b;
@@ -644,10 +655,16 @@ hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m,
     if (!part || !red || (mode == FIN_MVF && (!mean || !rstd)) || (mode == FIN_MEAN && !mean) ||
         (mode == FIN_VAR && !rstd) || (mode == FIN_BWD && (!dbeta || !dgamma)))
         return hipErrorInvalidValue;
-    SplitTerms st{nullptr, nullptr, nullptr, nullptr, 0};
+    SplitTerms st{nullptr, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0.f};
     if (split && split->alpha) {
         if (mode != FIN_BWD || !split->gamma || !split->rstd || !split->betap) return hipErrorInvalidValue;
         st = *split;
+    }
+    if (split && (split->shift || split->rmean)) {
+        if ((split->shift && mode != FIN_MVF) || (split->rmean && mode != FIN_MVF && mode != FIN_VAR) ||
+            (!split->rmean && split->rvar) || split->alpha || (mode == FIN_VAR && split->rmean && !mean))
+            return hipErrorInvalidValue;
+        st.shift = split->shift; st.rmean = split->rmean; st.rvar = split->rvar; st.momentum = split->momentum;
     }
     if (R <= kCombineOneMaxRows) {
         TraceScope tr(KC_SMALL, KID_COMBINE, s, (double)R * 2 * C * 4 + 3.0 * C * 4, 0.0);

@@ -94,6 +94,36 @@ __device__ __forceinline__ void bst16(__amdgpu_buffer_rsrc_t r, uint32_t off, co
     __builtin_amdgcn_raw_buffer_store_b128(t, r, off, 0, 0);
 }
 
+// Column sums of two float arrays in LDS, a = red[0 .. rows)[ld] and
+// b = red[rows .. 2 rows)[ld], columns 0 .. ncol-1, by all nthr threads of the
+// workgroup: each thread sums a strided slice of one column's rows, then
+// threads 0 .. 2 ncol-1 add the slices in order (a fixed order: the result
+// is deterministic).  Writes outa[c], outb[c] for c < nvalid.  Starts and
+// ends with a barrier; overwrites the first nthr floats of red.
+__device__ __forceinline__ void lds_colsum2(float *red, int rows, int ld, int ncol, int nthr, int tid,
+                                            float *outa, float *outb, int nvalid)
+{
+    const int lanes = 2 * ncol;
+    int S = nthr / lanes;
+    S = S < 1 ? 1 : (S > rows ? rows : S);
+    const int lane = tid % lanes, slice = tid / lanes;
+    float acc = 0.f;
+    __syncthreads();
+    if (slice < S) {
+        const float *col = red + (lane < ncol ? lane : rows * ld + lane - ncol);
+        for (int j = slice; j < rows; j += S) acc += col[j * ld];
+    }
+    __syncthreads();
+    if (slice < S) red[slice * lanes + lane] = acc;
+    __syncthreads();
+    if (tid < lanes) {
+        float t = 0.f;
+        for (int q = 0; q < S; q++) t += red[q * lanes + tid];
+        const int c = tid < ncol ? tid : tid - ncol;
+        if (c < nvalid) (tid < ncol ? outa : outb)[c] = t;
+    }
+}
+
 // Deferred input gradient of a BN-fed tensor, formed on load as
 //   d = A dy + B x + C  per channel (dy the loaded gradient, x the BN input).
 // One BN (split = 0):  d = gamma rstd (dy - dbeta/m - xhat dgamma/m), i.e.

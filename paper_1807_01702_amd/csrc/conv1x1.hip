@@ -139,6 +139,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     for (int c = tid; c < NP; c += kP1Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
         if (c < N && BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
+        if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[c];     // statistics of y - shift
         epi[c] = e0; epi[NP + c] = e1; epi[2 * NP + c] = e2; epi[3 * NP + c] = e3;
     }
 
@@ -336,7 +337,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
             } else if (EK == EK_STATS) {
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) {
-                    const float fv = ok ? f[e] : 0.f;
+                    const float fv = ok ? f[e] - eM[e] : 0.f;
                     s1[e] += fv;
                     s2[e] += fv * fv;
                 }
@@ -380,13 +381,8 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
             red[r0 * NP + n + e] = s1[e];
             red[(RSTEP + r0) * NP + n + e] = s2[e];
         }
-        __syncthreads();
-        for (int c = tid; c < N; c += kP1Threads) {
-            float a = 0.f, b = 0.f;
-            for (int j = 0; j < RSTEP; j++) { a += red[j * NP + c]; b += red[(RSTEP + j) * NP + c]; }
-            p.part[(int64_t)blockIdx.x * 2 * N + c] = a;
-            p.part[(int64_t)blockIdx.x * 2 * N + N + c] = b;
-        }
+        lds_colsum2(red, RSTEP, NP, NP, kP1Threads, tid, p.part + (int64_t)blockIdx.x * 2 * N,
+                    p.part + (int64_t)blockIdx.x * 2 * N + N, N);
     }
 }
 

@@ -44,6 +44,7 @@ namespace bnr {
 constexpr int kP3Threads = 512;
 constexpr int kP3BM = 128;          // output rows per tile
 constexpr int kP3MaxW = 61;         // widest image row (ring = 128 + 2 (W + 3) rows: fill = two batches)
+constexpr int kP3MaxH = 896;        // tallest image (exact multiply-shift row quotients)
 
 // LDS layout (bytes): [ring: ring rows, then copies of its first 16 rows (so
 // a 16-row fragment starting anywhere in the ring is contiguous), then one
@@ -55,6 +56,7 @@ struct P3Geom {
     int KP, NP, lda, ldw, ldr, ring;
     int PW, PH, MP;                 // padded row length W + 2, image height H + 2, positions n PH PW
     double inv_pw, inv_ph;
+    uint32_t rpw, rph;              // ceil(2^20 / PW), ceil(2^20 / PH): multiply-shift quotients
     size_t ring_bytes, stage_bytes, lds;
 };
 
@@ -77,6 +79,35 @@ static P3Geom p3_geom(int K, int N, int W)
     if (stats > g.stage_bytes) g.stage_bytes = stats;
     g.lds = g.ring_bytes + g.stage_bytes + (size_t)(3 * g.KP + 4 * g.NP) * 4;
     return g;
+}
+
+// Position -> pixel in two steps for the loops: a batch's first position
+// (wave-uniform) is split once, then each lane's offset from it with 24-bit
+// multiply-shift quotients, exact while x d < 2^20 for the dividend x and
+// divisor d (x < PW + 256 against PW <= 64; y < PH + 86 against PH <= kP3MaxH + 2).
+struct P3Base { int img, hp, wp, P; };
+__device__ __forceinline__ P3Base p3_base(int q0, const P3Geom &g)
+{
+    P3Base b;
+    b.P = q0 > 0 ? q0 : 0;
+    const int t = b.P / g.PW;
+    b.wp = b.P - t * g.PW;
+    b.img = t / g.PH;
+    b.hp = t - b.img * g.PH;
+    return b;
+}
+__device__ __forceinline__ int p3_pixel_at(const P3Base &b, int P, const P3Geom &g, int H, int W)
+{
+    const int o = P - b.P;                                    // < 256 (negative only for P < 0)
+    const int x = b.wp + (o > 0 ? o : 0);
+    const int t = (int)(__umul24((uint32_t)x, g.rpw) >> 20);
+    const int wp = x - __mul24(t, g.PW);
+    const int y = b.hp + t;
+    const int u = (int)(__umul24((uint32_t)y, g.rph) >> 20);
+    const int hp = y - __mul24(u, g.PH);
+    const int img = b.img + u;
+    const bool ok = (P >= 0) & (P < g.MP) & (wp > 0) & (wp <= W) & (hp > 0) & (hp <= H);
+    return ok ? (img * H + hp - 1) * W + wp - 1 : -1;
 }
 
 // Pixel of padded position P, or -1 for a padding position or one outside
@@ -157,7 +188,8 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     struct Batch { vec16 a[NVA]; vec16 b[NVB]; int pix; };
     auto load_rows = [&](int q0, int cnt, Batch &bt) __attribute__((always_inline)) {
         const int arow = tid >> 2;
-        const int pp = p3_pixel(q0 + arow, g, H, W);
+        const P3Base b = p3_base(q0, g);
+        const int pp = p3_pixel_at(b, q0 + arow, g, H, W);
         bt.pix = arow < cnt ? pp : -1;
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
@@ -234,6 +266,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     for (int c = tid; c < NPC; c += kP3Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
         if (c < N && EK == EK_BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
+        if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[c];     // statistics of y - shift
         epi[c] = e0; epi[NPC + c] = e1; epi[2 * NPC + c] = e2; epi[3 * NPC + c] = e3;
     }
     __syncthreads();
@@ -325,10 +358,11 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
     auto load_epi = [&](int p0, int nrows) __attribute__((always_inline)) {
+        const P3Base eb = p3_base(p0, g);
         #pragma unroll
         for (int j = 0; j < RPT; j++) {
             const int r = r0 + j * RSTEP;
-            const int pp = p3_pixel(p0 + r, g, H, W);
+            const int pp = p3_pixel_at(eb, p0 + r, g, H, W);
             epix[j] = col_ok && r < nrows ? pp : -1;
         }
         if (!READS) return;
@@ -419,6 +453,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         {
             vec16 vo[RPT];
             float eM[VEC], eR[VEC], eG[VEC], eB[VEC];
+            if (EK == EK_STATS) lds_f8(epi + n, eM);                  // shift
             if (EK == EK_BNBWD) {
                 lds_f8(epi + n, eM);
                 lds_f8(epi + NPC + n, eR);
@@ -451,7 +486,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 } else if (EK == EK_STATS) {
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) {
-                        const float fv = ok ? f[e] : 0.f;
+                        const float fv = ok ? f[e] - eM[e] : 0.f;
                         s1[e] += fv;
                         s2[e] += fv * fv;
                     }
@@ -501,13 +536,8 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             red[r0 * NPC + n + e] = s1[e];
             red[(RSTEP + r0) * NPC + n + e] = s2[e];
         }
-        __syncthreads();
-        for (int c = tid; c < N; c += kP3Threads) {
-            float a = 0.f, b = 0.f;
-            for (int j = 0; j < RSTEP; j++) { a += red[j * NPC + c]; b += red[(RSTEP + j) * NPC + c]; }
-            p.part[(int64_t)blockIdx.x * 2 * N + c] = a;
-            p.part[(int64_t)blockIdx.x * 2 * N + N + c] = b;
-        }
+        lds_colsum2(red, RSTEP, NPC, NPC, kP3Threads, tid, p.part + (int64_t)blockIdx.x * 2 * N,
+                    p.part + (int64_t)blockIdx.x * 2 * N + N, N);
     }
 }
 
@@ -524,9 +554,9 @@ static int p3_cus()
     return cus;
 }
 
-bool conv3x3_supported(int dtype, int K, int N, int W)
+bool conv3x3_supported(int dtype, int K, int N, int H, int W)
 {
-    if (dtype != DT_BF16 || K > 128 || N > 128 || W > kP3MaxW || W < 1) return false;
+    if (dtype != DT_BF16 || K > 128 || N > 128 || W > kP3MaxW || W < 1 || H > kP3MaxH || H < 1) return false;
     const P3Geom g = p3_geom(K, N, W);
     const int wk = g.KP / 32, wn = g.NP / 32;
     if (wk == 3 || wk * wn > 4) return false;      // at most 64 rows x 2 column blocks of accumulators per wave
@@ -591,7 +621,7 @@ static hipError_t run_p3_ek(const RowsParams &p, const P3Geom &g, int ek, hipStr
 
 hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
 {
-    if (!p.a || !p.wraw || !p.y || p.taps != 9 || p.pro == PRO_POOLUP || !conv3x3_supported(p.dtype, p.K, p.N, p.w))
+    if (!p.a || !p.wraw || !p.y || p.taps != 9 || p.pro == PRO_POOLUP || !conv3x3_supported(p.dtype, p.K, p.N, p.h, p.w))
         return hipErrorInvalidValue;
     if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return hipErrorInvalidValue;
     if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd ||
@@ -610,6 +640,8 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
     P3Geom g = p3_geom(p.K, p.N, p.w);
     g.PH = p.h + 2;
     g.inv_ph = 1.0 / g.PH;
+    g.rpw = (uint32_t)(((1u << 20) + g.PW - 1) / g.PW);
+    g.rph = (uint32_t)(((1u << 20) + g.PH - 1) / g.PH);
     const int64_t mp = (int64_t)p.n * g.PH * g.PW;                // padded positions
     if (mp >= (lim >> 1)) return hipErrorInvalidValue;
     g.MP = (int)mp;

@@ -209,6 +209,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             emu[e] = p.e_mean[n + e]; ers[e] = p.e_rstd[n + e];
             eg[e] = p.e_gamma[n + e]; eb[e] = p.e_beta[n + e];
         }
+    if (p.epi == EPI_STATS)                       // statistics of y - shift
+        for (int e = 0; e < VEC; e++) emu[e] = p.e_shift && col_ok ? p.e_shift[n + e] : 0.f;
     T *yout = reinterpret_cast<T *>(p.y);
     const T *exs = reinterpret_cast<const T *>(p.ex);
     if (col_ok) {
@@ -231,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 float f[VEC];
                 Elem<T>::unpack(cv, f);
                 stg16(dst, cv);
-                for (int e = 0; e < VEC; e++) { s1[e] += f[e]; s2[e] += f[e] * f[e]; }
+                for (int e = 0; e < VEC; e++) { const float d = f[e] - emu[e]; s1[e] += d; s2[e] += d * d; }
             } else if (p.epi == EPI_RELUMASK) {
                 float f[VEC], yv[VEC];
                 Elem<T>::unpack(cv, f);
@@ -263,13 +265,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             red[r0 * BN + v * VEC + e] = s1[e];
             red[(RSTEP + r0) * BN + v * VEC + e] = s2[e];
         }
-        __syncthreads();
-        if (tid < BN && n0 + tid < N) {
-            float a = 0.f, b = 0.f;
-            for (int j = 0; j < RSTEP; j++) { a += red[j * BN + tid]; b += red[(RSTEP + j) * BN + tid]; }
-            p.part[(int64_t)mt * 2 * N + n0 + tid] = a;
-            p.part[(int64_t)mt * 2 * N + N + n0 + tid] = b;
-        }
+        lds_colsum2(red, RSTEP, BN, BN, kThreads, tid, p.part + (int64_t)mt * 2 * N + n0,
+                    p.part + (int64_t)mt * 2 * N + N + n0, N - n0);
     }
 }
 

@@ -20,6 +20,12 @@ struct SplitTerms {
     const float *gamma, *rstd;
     float *alpha, *betap;         // NULL: none
     int accumulate;
+    // forward finalisation (FIN_MVF, FIN_VAR): the one-sweep sums were taken
+    // around shift (NULL: 0; FIN_MVF only) and the running statistics are
+    // updated when rmean is set (rvar: unbiased variance)
+    const float *shift;
+    float *rmean, *rvar;
+    float momentum;
 };
 
 // Reduction scratch ("red") of a statistics combine: the float64 level-1
@@ -98,6 +104,7 @@ struct RowsParams {
     const void *ex;               // EPI_BNBWD: BN input (N channels); EPI_RELUMASK: ReLU input
     int64_t ex_ldc;
     const float *e_gamma, *e_beta, *e_mean, *e_rstd;
+    const float *e_shift;         // EPI_STATS: the sums are of (y - e_shift) (NULL: 0)
 };
 int64_t rows_mtiles(int dtype, int taps, int64_t m, int n_out);
 size_t rows_pack_bytes(int dtype, int taps, int K, int N);
@@ -113,7 +120,7 @@ int64_t conv1x1_partial_rows(int64_t m);      // upper bound of the statistics p
 hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows);   // *rows: partial rows written
 
 // ---- persistent 3x3 CONV (weights and an input-row ring buffer in LDS) ----
-bool conv3x3_supported(int dtype, int K, int N, int W);
+bool conv3x3_supported(int dtype, int K, int N, int H, int W);
 int64_t conv3x3_partial_rows(int64_t m);      // statistics partial rows it writes
 hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s);
 
@@ -159,6 +166,7 @@ struct StemParams {
     const void *wt;               // [7][7][c_in][64]
     void *s;                      // forward output [n][ho][wo][64]
     float *part;                  // forward statistics partials [groups][2][64]
+    const float *shift;           // forward statistics: sums of (s - shift) (NULL: 0)
     const void *g;                // weight gradient: DENSE g view / BNGRAD dy ([m][64] dense)
     int64_t g_ldc;
     const void *gx;               // BNGRAD: the BN input (the CONV output) view
@@ -185,6 +193,7 @@ struct MaxPoolParams {
     const void *g;                // backward: gradient of the pooled output (view)
     int64_t g_ldc;
     float *part;                  // statistics / BN-backward partials [rows][2][c]
+    const float *shift;           // forward statistics: sums of (y - shift) (NULL: 0)
 };
 int64_t maxpool_fwd_rows(int dtype, int64_t m_out, int c);
 int64_t maxpool_bwd_groups(int n, int h);

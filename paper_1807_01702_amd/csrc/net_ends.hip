@@ -114,7 +114,9 @@ __global__ __launch_bounds__(kThreads, 2) void k_stem_conv(StemParams p)
             bw[kh][nb] = M::from_words(wd);
         }
 
-    float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
+    float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f}, sh[4] = {0.f, 0.f, 0.f, 0.f};
+    if (STATS && p.shift)                         // statistics of s - shift
+        for (int nb = 0; nb < 4; nb++) sh[nb] = p.shift[nb * 16 + (threadIdx.x & 15)];
     const int lid = xcd_remap(blockIdx.x, gridDim.x);
     for (int64_t it = lid; it < items; it += gridDim.x) {
         const StemItem t = stem_item(p, it);
@@ -153,7 +155,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_stem_conv(StemParams p)
                         const int pp = mb * 16 + 4 * g16 + i;
                         const bf16_t b = f2bf(acc[mi][nb][i]);
                         if (STATS && pp < t.pv) {
-                            const float v = bf2f(b);
+                            const float v = bf2f(b) - sh[nb];
                             s1[nb] += v;
                             s2[nb] += v * v;
                         }
@@ -403,10 +405,11 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
     const int ry = kThreads / vb;
     const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
-    float sg[VEC], k[VEC], b[VEC], s1[VEC], s2[VEC];
+    float sg[VEC], k[VEC], b[VEC], s1[VEC], s2[VEC], sh[VEC];
     #pragma unroll
     for (int i = 0; i < VEC; i++) {
         s1[i] = s2[i] = 0.f;
+        sh[i] = STATS && p.shift && ty < ry ? p.shift[c0 + i] : 0.f;     // statistics of y - shift
         sg[i] = 1.f; k[i] = 1.f; b[i] = 0.f;
         if (BN && ty < ry) {
             const float g = p.gamma[c0 + i];
@@ -459,7 +462,7 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
             if (STATS) {
                 Elem<T>::unpack(ov, o);
                 #pragma unroll
-                for (int i = 0; i < VEC; i++) { s1[i] += o[i]; s2[i] += o[i] * o[i]; }
+                for (int i = 0; i < VEC; i++) { const float d = o[i] - sh[i]; s1[i] += d; s2[i] += d * d; }
             }
         }
     }

@@ -200,7 +200,8 @@ class _DenseStage:
     ICF each BN1 sweeps its input for statistics and its input gradient is
     formed by a separate pass accumulating into G."""
 
-    def __init__(self, n, h, w, c0, ct, cpls, trans, eps, dev, bf16, fused, icf, ref_mode=MODE, overlap=False):
+    def __init__(self, n, h, w, c0, ct, cpls, trans, eps, dev, bf16, fused, icf, ref_mode=MODE, overlap=False,
+                 robust=False):
         dt = torch.bfloat16 if bf16 else torch.float32
         self.n, self.h, self.w, self.c0, self.ct = n, h, w, c0, ct
         self.X = torch.zeros((n, h, w, ct), dtype=dt, device=dev)
@@ -255,6 +256,24 @@ class _DenseStage:
                 self.slice_stats.append(B.BN.stats_view(eps, **self.shared(c_l, c_l + k)))
             if self.ut is not None:
                 self.ut.bn = B.BN(self.ut.bn.gamma, self.ut.bn.beta, eps, **self.shared(0, ct))
+        # robust one-sweep statistics: every statistics producer of the block sums
+        # around its channels' running mean (the shift, updated in place by the
+        # producer's finalisation together with the running variance)
+        self.robust = bool(robust)
+        if self.robust:
+            if not self.icf:
+                raise ValueError("robust statistics are wired for the fused path with inter-composite-layer fusion")
+            f32 = dict(dtype=torch.float32, device=dev)
+            self.run_mean, self.run_var = torch.zeros(ct, **f32), torch.ones(ct, **f32)
+
+            def rob(bn, rm, rv):
+                bn.robust(shift=rm, running_mean=rm, running_var=rv, momentum=0.1)
+
+            rob(self.in_stats, self.run_mean[:c0], self.run_var[:c0])
+            for (c_l, k, u1, u2), st in zip(self.cpl, self.slice_stats):
+                rob(st, self.run_mean[c_l:c_l + k], self.run_var[c_l:c_l + k])
+                wd = u2.bn.gamma.shape[0]
+                rob(u2.bn, torch.zeros(wd, **f32), torch.ones(wd, **f32))
 
     def shared(self, lo, hi):
         """Views of the shared per-channel statistics of channels [lo, hi)."""
@@ -395,13 +414,13 @@ class DenseBlock(_DenseStage):
     input; upstream gradient: dpool of the pooled output.  ``icf`` defaults
     to on for the fused path (see _DenseStage)."""
 
-    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None, overlap=False):
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None, overlap=False, robust=False):
         bf16 = data["bf16"]
         dev = torch.device(device)
         dt = torch.bfloat16 if bf16 else torch.float32
         n, h, w, c0 = data["x"].shape
         super().__init__(n, h, w, c0, data["c_total"], data["cpls"], data["trans"], data["eps"], dev, bf16, fused,
-                         fused if icf is None else icf, ref_mode, overlap)
+                         fused if icf is None else icf, ref_mode, overlap, robust)
         self.X[..., :c0] = _t(data["x"], dev, bf16)
         to = data["trans"]["w"].shape[3]
         self.pooled = torch.empty((n, h // 2, w // 2, to), dtype=dt, device=dev)

@@ -81,6 +81,21 @@ def test_conv_fwd_rejects_pointers_workspace_alias(B):
     assert B.STATUS[f(ctypes.byref(d), A, A + 0x1000, A + 0x2000, ctypes.byref(bad), WS, 1 << 30, None)] == "BNR_ERR_SHAPE"
 
 
+def test_robust_statistics_fields_validate(B):
+    """The shift / running-statistics fields of bnr_bn are checked before any launch."""
+    st = B._lib_fns["bnr_bn_stats"]
+    def status(**kw):
+        f = dict(shift=None, running_mean=None, running_var=None, momentum=0.0)
+        f.update(kw)
+        bn = B.BNStruct(None, None, A, A, A, 1e-5, f["shift"], f["running_mean"], f["running_var"], f["momentum"])
+        return B.STATUS[st(64, 8, 8, B.BNR_BF16, A, ctypes.byref(bn), WS, 1 << 20, None)]
+    assert status(running_mean=A, momentum=1.5) == "BNR_ERR_SHAPE"
+    assert status(running_mean=A, momentum=-0.1) == "BNR_ERR_SHAPE"
+    assert status(running_var=A) == "BNR_ERR_NULL"
+    assert status(shift=A + 2) == "BNR_ERR_ALIGN"
+    assert status(running_mean=A + 1, momentum=0.1) == "BNR_ERR_ALIGN"
+
+
 def test_other_entry_points_validate(B):
     bn = B.BNStruct(A, A, A, A, A, 1e-5)
     st = B._lib_fns["bnr_bn_stats"]

@@ -161,6 +161,35 @@ def test_dense_block_fp32_all_tensors(mode):
     _check_block(wl, d, RTOL[False])
 
 
+def test_dense_block_robust_statistics():
+    """Every statistics producer of the block sums around its channels'
+    running mean: three steps, each matching the oracle in every tensor, and
+    the running statistics after t steps equal the closed form
+    (1 - 0.9^t) mean and 0.9^t + (1 - 0.9^t) var m/(m-1) of the (fixed) batch
+    statistics."""
+    from paper_1807_01702_amd import workloads as W
+    d = synth.dense_block(seed=0, n=1, h=16, w=16, bf16=False)
+    rnd = OC.storage(False)
+    _, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"])
+    assert _margin(c) >= 1e-6, "precondition: ReLU decisions must be unique at fp32 accuracy"
+    wl = W.DenseBlock(d, fused=True, robust=True)
+    m = d["x"].shape[0] * d["x"].shape[1] * d["x"].shape[2]
+    for t in range(1, 4):
+        wl.step()
+        torch.cuda.synchronize()
+        _check_block(wl, d, RTOL[False])
+        a = 0.9 ** t
+        ct = d["c_total"]
+        mean_r, var_r = c["ut"]["mean"], c["ut"]["var"]          # the transition BN reads all block channels
+        np.testing.assert_allclose(host(wl.run_mean), (1 - a) * mean_r, rtol=2e-4, atol=1e-6)
+        np.testing.assert_allclose(host(wl.run_var), a + (1 - a) * var_r * m / (m - 1), rtol=2e-4)
+        assert wl.run_mean.shape[0] == ct
+        for (c_l, k, u1, u2), cc in zip(wl.cpl, c["cpls"]):
+            np.testing.assert_allclose(host(u2.bn.running_mean), (1 - a) * cc["u2"]["mean"], rtol=2e-4, atol=1e-6)
+            np.testing.assert_allclose(host(u2.bn.running_var), a + (1 - a) * cc["u2"]["var"] * m / (m - 1),
+                                       rtol=2e-4)
+
+
 def _l2(a, b):
     a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
     return float(np.linalg.norm(a - b) / np.linalg.norm(b))

@@ -40,6 +40,12 @@ MUTANTS = [
     ("BN backward: rstd factor dropped", "oracle.c", "dx[i * C + c] = gamma[c] * rstd[c] *", "dx[i * C + c] = gamma[c] *"),
     ("ReLU gradient passes at y == 0", "oracle.c", "dy[i] = y[i] > 0.0 ? dz[i] : 0.0;", "dy[i] = y[i] >= 0.0 ? dz[i] : 0.0;"),
     ("MVF drops the square of the mean", "oracle.c", "var[c] = e2 - e1 * e1;", "var[c] = e2 - e1;"),
+    ("shifted MVF forgets to add the shift back", "oracle.c", "mean[c] = K[c] + d1;", "mean[c] = d1;"),
+    ("shifted MVF squares the unshifted value", "oracle.c", "s += d; s2 += d * d; }",
+     "s += d; s2 += x[i * C + c] * x[i * C + c]; }"),
+    ("running variance kept biased", "oracle.c", "mo * var[c] * ((double)m / (double)(m - 1));", "mo * var[c];"),
+    ("running mean momentum reversed", "oracle.c", "rmean[c] = (1.0 - mo) * rmean[c] + mo * mean[c];",
+     "rmean[c] = mo * rmean[c] + (1.0 - mo) * mean[c];"),
     ("avgpool backward scale", "oracle.c", "gin[IDX4(n, iy, ix, c, H, W, C)] = 0.25 *", "gin[IDX4(n, iy, ix, c, H, W, C)] = 0.5 *"),
     ("maxpool backward picks the last maximum", "oracle.c", "if (in[j] > best) { best = in[j]; arg = j; }",
      "if (in[j] >= best) { best = in[j]; arg = j; }"),

@@ -123,6 +123,66 @@ def test_mvf_stats_equal_two_pass():
     np.testing.assert_allclose(m1, x.mean(0), rtol=1e-14)
 
 
+def test_mvf_shifted_statistics():
+    """One-sweep statistics around a shift K (the robust MVF reading): exact
+    small-integer data against the two-pass definition for several K; the
+    closed form mean = mu, var = sigma^2 of a +-sigma pattern; the textbook
+    two-pass mean/var of torch when K is the exact mean."""
+    x = RNG.integers(-50, 50, (1024, 5)).astype(np.float64)
+    m2, v2, _ = P.bn_stats(x, 0.0)
+    for K in (np.zeros(5), np.array([3.0, -7.0, 11.0, 0.5, -64.0]), m2):
+        m1, v1 = P.mvf_stats_shifted(x, K)
+        np.testing.assert_allclose(m1, m2, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(v1, v2, rtol=1e-13, atol=1e-12)
+    # K = 0 is the unshifted one-sweep identity
+    np.testing.assert_array_equal(P.mvf_stats_shifted(x, np.zeros(5))[1], P.mvf_stats(x)[1])
+    # x = mu + sigma * (+-1): mean mu, variance sigma^2, from a shift near mu
+    mu, sg = np.array([1.0e4, -2.5e3]), np.array([1.0, 0.25])
+    s = np.where(np.arange(2048) % 2 == 0, 1.0, -1.0)[:, None]
+    x = mu[None, :] + sg[None, :] * s
+    m1, v1 = P.mvf_stats_shifted(x, mu + np.array([0.5, -0.125]))
+    np.testing.assert_allclose(m1, mu, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(v1, sg ** 2, rtol=1e-12)
+    t = torch.from_numpy(RNG.standard_normal((3000, 4)) * 2 + 5)
+    m1, v1 = P.mvf_stats_shifted(t.numpy(), t.mean(0).numpy())
+    np.testing.assert_allclose(v1, t.var(0, unbiased=False).numpy(), rtol=1e-12)
+
+
+def test_mvf_shift_removes_single_precision_cancellation():
+    """The reason for the shift (a property of the method, not of the oracle):
+    float32 one-sweep sums of data with |mean|/std = 1e4 lose the variance,
+    the same sums around a shift near the mean keep it."""
+    r = np.random.default_rng(7)
+    x = (1.0e4 + r.standard_normal(65536)).astype(np.float32)
+    ref = P.bn_stats(x[:, None], 0.0)[1][0]
+    def one_sweep(d):
+        s1, s2 = np.float32(0), np.float32(0)
+        for blk in d.reshape(256, 256):                  # float32 partial sums per block, like the producers
+            s1 += blk.sum(dtype=np.float32)
+            s2 += (blk * blk).sum(dtype=np.float32)
+        e1 = np.float64(s1) / d.size
+        return np.float64(s2) / d.size - e1 * e1
+    assert abs(one_sweep(x) - ref) / ref > 0.5
+    assert abs(one_sweep(x - np.float32(1.0e4)) - ref) / ref < 1e-3
+
+
+def test_running_update_closed_form():
+    rm, rv = P.running_update([1.0, -2.0], [4.0, 0.5], [5.0, 2.0], [3.0, 6.0], 4, 0.1)
+    np.testing.assert_allclose(rm, [0.9 * 1.0 + 0.1 * 5.0, 0.9 * -2.0 + 0.1 * 2.0], rtol=1e-15)
+    np.testing.assert_allclose(rv, [0.9 * 4.0 + 0.1 * 3.0 * 4 / 3, 0.9 * 0.5 + 0.1 * 6.0 * 4 / 3], rtol=1e-15)
+    # momentum 1 replaces, 0 keeps; the unbiased variance of torch's BN update
+    rm, rv = P.running_update([7.0], [7.0], [1.0], [2.0], 9, 1.0)
+    assert rm[0] == 1.0 and rv[0] == 2.0 * 9 / 8
+    t = torch.randn(50, 3, 4, 4, dtype=torch.float64)
+    run_m, run_v = torch.zeros(3, dtype=torch.float64), torch.ones(3, dtype=torch.float64)
+    F.batch_norm(t, run_m, run_v, training=True, momentum=0.1)
+    x = t.permute(0, 2, 3, 1).reshape(-1, 3).numpy()
+    mean, var, _ = P.bn_stats(x, 0.0)
+    rm, rv = P.running_update(np.zeros(3), np.ones(3), mean, var, x.shape[0], 0.1)
+    np.testing.assert_allclose(rm, run_m.numpy(), rtol=1e-12)
+    np.testing.assert_allclose(rv, run_v.numpy(), rtol=1e-12)
+
+
 # ----------------------------------------------------------- BN backward ----
 def test_bn_bwd_invariants():
     m, C = 777, 6
