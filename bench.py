@@ -211,6 +211,7 @@ def kernel_class(name):
     return {"k_stats_partial": "stats_sweep", "k_elementwise": "elementwise", "k_addrelu_bwd": "elementwise",
             "k_stats_combine_one": "stats_combine", "k_stats_combine1": "stats_combine",
             "k_stats_combine2": "stats_combine", "k_sum_partials1": "splitk_sum", "k_sum_partials2": "splitk_sum",
+            "k_bwd_tail": "splitk_sum", "k_loss_mean": "head",
             "k_avgpool2": "pool", "k_avgpool2_bwd": "pool", "k_copy16": "copy",
             "k_pack_weights": "weight_pack", "k_stem_conv": "stem_conv", "k_stem_conv_f32": "stem_conv",
             "k_stem_wgrad": "stem_wgrad", "k_stem_wgrad_f32": "stem_wgrad", "k_maxpool_fwd": "maxpool",
