@@ -329,7 +329,7 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
     constexpr int RB = CIT / 16 / WCI, CB = COT / 16 / WCO;
     constexpr int ZP = CIT + 8, GP = COT + 8;                     // LDS row pitches (elements)
     constexpr int VZ = CIT / VEC, VG = COT / VEC;                 // vectors per staged row
-    constexpr int KQMAX = TAPS == 3 ? 128 : 64;                  // positions per chunk (upper bound)
+    constexpr int KQMAX = TAPS == 3 ? 128 : kWgTrKQ1;            // positions per chunk (upper bound)
     constexpr int ZRMAX = TAPS == 3 ? KQMAX + 2 * (kWgMaxW3 + 2) + 2 : KQMAX;
     constexpr int NZ = (ZRMAX * VZ + kThreads - 1) / kThreads;
     constexpr int NG = (KQMAX * VG + kThreads - 1) / kThreads;

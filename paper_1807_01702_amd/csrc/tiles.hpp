@@ -44,6 +44,7 @@ inline RowsTile rows_tile(int dtype, int taps, int n_out) {
 constexpr int kWgKC = 64;                  // K positions per chunk
 constexpr int kWgCIT = 64;                 // input channels per tile
 constexpr int kWgMaxW3 = 62;               // widest 3x3 image row (PW <= 64)
+constexpr int kWgTrKQ1 = 64;               // pixels per chunk of the bf16 1x1 weight gradient (128: slower)
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct WgradPlan {
@@ -120,10 +121,10 @@ inline WgTrPlan wgrad_tr_plan(int64_t m, int n, int h, int w, int c_in, int c_ou
     } else {
         p.PW = 0;
         p.R = 0;
-        p.KQ = 64;
-        p.zrows = 64;
+        p.KQ = kWgTrKQ1;
+        p.zrows = kWgTrKQ1;
         p.chunks_per_image = 0;
-        p.nchunks = ceil_div(m, 64);
+        p.nchunks = ceil_div(m, kWgTrKQ1);
     }
     const int64_t n_out = (int64_t)p.ci_tiles * p.co_tiles;
     int64_t s = ceil_div(512, n_out);                 // two workgroups per CU
