@@ -114,7 +114,134 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     const T *asrc2 = reinterpret_cast<const T *>(p.a2);
     __syncthreads();
 
-    for (int ch = 0; ch < nchunks; ch++) {
+    if constexpr (TAPS == 1) {
+        if (p.buf32) {
+            // 1x1 with every operand span below 2^31 bytes: the next chunk's A
+            // rows and weights are loaded into registers (raw buffer loads,
+            // out-of-range offsets read zeros) while the matrix cores work on
+            // the current chunk.  A slot j of this thread is row i / VPR,
+            // channel vector i % VPR of the chunk (i = tid + j kThreads); its
+            // source pixel is fixed for the whole tile.
+            constexpr int NA = (BM * VPR + kThreads - 1) / kThreads, NB = (BN * VPR + kThreads - 1) / kThreads;
+            const bool pool = p.pro == PRO_POOLUP;
+            const int64_t src_rows = pool ? m / 4 : m;
+            const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((src_rows - 1) * p.a_ldc + K) * sizeof(T)));
+            const __amdgpu_buffer_rsrc_t a2buf =
+                buf_view(p.pro == PRO_BNGRAD ? p.a2 : p.a,
+                         p.pro == PRO_BNGRAD ? (uint32_t)(((m - 1) * p.a2_ldc + K) * sizeof(T)) : 0u);
+            const __amdgpu_buffer_rsrc_t wbuf =
+                buf_view(p.wpack, (uint32_t)((int64_t)gridDim.y * nchunks * BN * kRowsBK * sizeof(T)));
+            const int a_ldc = (int)p.a_ldc, a2_ldc = (int)p.a2_ldc;
+            int apix[NA], arow[NA], avec[NA];
+            #pragma unroll
+            for (int j = 0; j < NA; j++) {
+                const int i = tid + j * kThreads;
+                arow[j] = i / VPR;
+                avec[j] = i % VPR;
+                const int64_t pp = p0 + arow[j];
+                int64_t q = pp;
+                if (pool) {
+                    const int64_t img = pp / ((int64_t)H * W);
+                    const int rem = (int)(pp - img * H * W);
+                    const int y = rem / W, x = rem - y * W;
+                    q = (img * (H / 2) + y / 2) * (W / 2) + x / 2;
+                }
+                apix[j] = pp < m && i < BM * VPR ? (int)q : -1;
+            }
+            vec16 ra[NA], rx[NA], rw[NB];
+            auto load_chunk = [&](int ch) __attribute__((always_inline)) {
+                const int c0 = ch * kRowsBK;
+                #pragma unroll
+                for (int j = 0; j < NA; j++) {
+                    const int c = c0 + avec[j] * VEC;
+                    const bool ok = apix[j] >= 0 && c < K;
+                    ra[j] = bld16(abuf, ok ? (uint32_t)(apix[j] * a_ldc + c) * (uint32_t)sizeof(T) : kBufOff);
+                    if (p.pro == PRO_BNGRAD)
+                        rx[j] = bld16(a2buf, ok ? (uint32_t)(apix[j] * a2_ldc + c) * (uint32_t)sizeof(T) : kBufOff);
+                }
+                const uint32_t wofs = (uint32_t)(((int64_t)nt * nchunks + ch) * (BN * kRowsBK));
+                #pragma unroll
+                for (int j = 0; j < NB; j++) {
+                    const int i = tid + j * kThreads;
+                    rw[j] = bld16(wbuf, i < BN * VPR ? (wofs + (uint32_t)((i / VPR) * kRowsBK + (i % VPR) * VEC)) *
+                                                           (uint32_t)sizeof(T)
+                                                     : kBufOff);
+                }
+            };
+            auto store_chunk = [&](int ch) __attribute__((always_inline)) {
+                const int c0 = ch * kRowsBK;
+                #pragma unroll
+                for (int j = 0; j < NA; j++) {
+                    const int c = c0 + avec[j] * VEC;
+                    vec16 out = ra[j];
+                    if (p.pro == PRO_BNRELU) {
+                        const int cc = c < K ? c : 0;
+                        float f[VEC];
+                        Elem<T>::unpack(ra[j], f);
+                        #pragma unroll
+                        for (int e = 0; e < VEC; e++) {
+                            const float t = (f[e] - coef[cc + e]) * coef[K + cc + e] + coef[2 * K + cc + e];
+                            f[e] = t > 0.f ? t : 0.f;
+                        }
+                        out = Elem<T>::pack(f);
+                    } else if (p.pro == PRO_BNGRAD) {
+                        const int cc = c < K ? c : 0;
+                        float d[VEC], x[VEC];
+                        Elem<T>::unpack(ra[j], d);
+                        Elem<T>::unpack(rx[j], x);
+                        #pragma unroll
+                        for (int e = 0; e < VEC; e++)
+                            d[e] = __builtin_fmaf(coef[cc + e], d[e], __builtin_fmaf(coef[K + cc + e], x[e], coef[2 * K + cc + e]));
+                        out = Elem<T>::pack(d);
+                    } else if (p.pro == PRO_RELU) {
+                        float f[VEC];
+                        Elem<T>::unpack(ra[j], f);
+                        #pragma unroll
+                        for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
+                        out = Elem<T>::pack(f);
+                    } else if (pool) {
+                        float f[VEC];
+                        Elem<T>::unpack(ra[j], f);
+                        #pragma unroll
+                        for (int e = 0; e < VEC; e++) f[e] *= 0.25f;
+                        out = Elem<T>::pack(f);
+                    }
+                    // rows past the tensor and channels past K are zero (not bn(0))
+                    const bool valid = apix[j] >= 0 && c < K;
+                    #pragma unroll
+                    for (int w4 = 0; w4 < 4; w4++) out.u[w4] = valid ? out.u[w4] : 0u;
+                    if (tid + j * kThreads < BM * VPR)
+                        *reinterpret_cast<vec16 *>(As + arow[j] * ASTR + avec[j] * VEC) = out;
+                }
+                #pragma unroll
+                for (int j = 0; j < NB; j++) {
+                    const int i = tid + j * kThreads;
+                    if (i < BN * VPR) *reinterpret_cast<vec16 *>(Bs + (i / VPR) * ASTR + (i % VPR) * VEC) = rw[j];
+                }
+            };
+            load_chunk(0);
+            for (int ch = 0; ch < nchunks; ch++) {
+                store_chunk(ch);
+                __syncthreads();
+                if (ch + 1 < nchunks) load_chunk(ch + 1);
+                for (int ks = 0; ks < kRowsBK / M::KSTEP; ks++) {
+                    const int kofs = ks * M::KSTEP + (lane >> 4) * M::KPL;
+                    typename M::frag b[TN];
+                    #pragma unroll
+                    for (int cb = 0; cb < TN; cb++)
+                        b[cb] = M::load(Bs + (wn * TN * 16 + cb * 16 + (lane & 15)) * ASTR + kofs);
+                    #pragma unroll
+                    for (int rb = 0; rb < TM; rb++) {
+                        const typename M::frag a = M::load(As + (wm * TM * 16 + rb * 16 + (lane & 15)) * ASTR + kofs);
+                        #pragma unroll
+                        for (int cb = 0; cb < TN; cb++) M::mma(acc[rb][cb], a, b[cb]);
+                    }
+                }
+                __syncthreads();
+            }
+        }
+    }
+    for (int ch = 0; ch < ((TAPS == 1 && p.buf32) ? 0 : nchunks); ch++) {
         const int c0 = ch * kRowsBK;
         // ---- stage A (prologue applied, zero outside the tensor) ----
         for (int i = tid; i < arows * VPR; i += kThreads) {
@@ -361,7 +488,16 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     dim3 grid((unsigned)ceil_div(p.m, BM), (unsigned)ceil_div(p.N, BN));
     TraceScope tr(KC_CONV, TAPS == 9 ? KID_CONV_3X3 : KID_CONV_1X1, s, rows_algorithmic_bytes(p),
                   2.0 * (double)p.m * TAPS * p.K * p.N);
-    hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, p);
+    RowsParams q = p;
+    if (TAPS == 1) {                    // 32-bit raw-buffer offsets for the pipelined 1x1 chunk loop
+        const int64_t lim = (int64_t)1 << 31, es = (int64_t)sizeof(T);
+        const int64_t src_rows = p.pro == PRO_POOLUP ? p.m / 4 : p.m;
+        const int64_t nchunks = ceil_div(p.K, kRowsBK);
+        q.buf32 = (src_rows * p.a_ldc + p.K) * es < lim &&
+                  (p.pro != PRO_BNGRAD || (p.m * p.a2_ldc + p.K) * es < lim) &&
+                  (int64_t)grid.y * nchunks * BN * kRowsBK * es < lim;
+    }
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, q);
     return hipGetLastError();
 }
 

@@ -105,6 +105,7 @@ struct RowsParams {
     int64_t ex_ldc;
     const float *e_gamma, *e_beta, *e_mean, *e_rstd;
     const float *e_shift;         // EPI_STATS: the sums are of (y - e_shift) (NULL: 0)
+    int buf32;                    // tiled 1x1 kernel: operand spans below 2^31 bytes (set by its launcher)
 };
 int64_t rows_mtiles(int dtype, int taps, int64_t m, int n_out);
 size_t rows_pack_bytes(int dtype, int taps, int K, int N);
