@@ -278,8 +278,14 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
         TRY_HIP(launch_conv3x3(rp, s), transpose ? "conv data gradient" : "conv forward");
         return BNR_OK;
     }
-    TRY_HIP(launch_pack_weights(rp.dtype, w, d->k, d->c_in, d->c_out, transpose, wpack, s), "weight packing");
-    rp.wpack = wpack;
+    if (rows_direct_weights(rp.dtype, rp.taps, rp.m, rp.K, rp.N, rp.a_ldc, rp.a2_ldc, rp.pro)) {
+        rp.wdirect = 1;                 // bf16 1x1: the tiled kernel reads the caller's weights, no packing
+        rp.wraw = w;
+        rp.wtrans = transpose;
+    } else {
+        TRY_HIP(launch_pack_weights(rp.dtype, w, d->k, d->c_in, d->c_out, transpose, wpack, s), "weight packing");
+        rp.wpack = wpack;
+    }
     *rows = rows_mtiles(rp.dtype, rp.taps, rp.m, rp.N);
     TRY_HIP(launch_conv_rows(rp, s), transpose ? "conv data gradient" : "conv forward");
     return BNR_OK;

@@ -29,6 +29,8 @@
 //   EPI_RELUMASK: dy = dz * [y > 0] from a stored y (ReLU-CONV fusion alone)
 // The epilogue goes through LDS so that every global access is a 16-byte
 // vector of one pixel row.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "mfma.hpp"
@@ -129,8 +131,16 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             const __amdgpu_buffer_rsrc_t a2buf =
                 buf_view(p.pro == PRO_BNGRAD ? p.a2 : p.a,
                          p.pro == PRO_BNGRAD ? (uint32_t)(((m - 1) * p.a2_ldc + K) * sizeof(T)) : 0u);
+            // weights: packed [nt][chunk][n][32 k], or (bf16, wdirect) the caller's
+            // [k][n] (forward: staged as rows of k, fragments by transposing
+            // reads) or [n][k] (data gradient: rows of n, as the packed layout)
+            constexpr bool kTr = std::is_same<T, bf16_t>::value;
+            const bool direct = kTr && p.wdirect;
+            const bool dfwd = direct && !p.wtrans;
+            constexpr int BP = BN + 8;                                // pitch of the [k][n] staging
             const __amdgpu_buffer_rsrc_t wbuf =
-                buf_view(p.wpack, (uint32_t)((int64_t)gridDim.y * nchunks * BN * kRowsBK * sizeof(T)));
+                direct ? buf_view(p.wraw, (uint32_t)((int64_t)K * N * sizeof(T)))
+                       : buf_view(p.wpack, (uint32_t)((int64_t)gridDim.y * nchunks * BN * kRowsBK * sizeof(T)));
             const int a_ldc = (int)p.a_ldc, a2_ldc = (int)p.a2_ldc;
             int apix[NA], arow[NA], avec[NA];
             #pragma unroll
@@ -163,9 +173,17 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 #pragma unroll
                 for (int j = 0; j < NB; j++) {
                     const int i = tid + j * kThreads;
-                    rw[j] = bld16(wbuf, i < BN * VPR ? (wofs + (uint32_t)((i / VPR) * kRowsBK + (i % VPR) * VEC)) *
-                                                           (uint32_t)sizeof(T)
-                                                     : kBufOff);
+                    uint32_t off = kBufOff;
+                    if (dfwd) {                       // row k = i / (BN / VEC) of [k][n]
+                        const int k = c0 + i / (BN / VEC), nn = n0 + (i % (BN / VEC)) * VEC;
+                        if (i < BN * VPR && k < K && nn < N) off = (uint32_t)(k * N + nn) * (uint32_t)sizeof(T);
+                    } else if (direct) {              // row n = i / VPR of [n][k]
+                        const int nn = n0 + i / VPR, k = c0 + (i % VPR) * VEC;
+                        if (i < BN * VPR && nn < N && k < K) off = (uint32_t)(nn * K + k) * (uint32_t)sizeof(T);
+                    } else if (i < BN * VPR) {
+                        off = (wofs + (uint32_t)((i / VPR) * kRowsBK + (i % VPR) * VEC)) * (uint32_t)sizeof(T);
+                    }
+                    rw[j] = bld16(wbuf, off);
                 }
             };
             auto store_chunk = [&](int ch) __attribute__((always_inline)) {
@@ -216,7 +234,11 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 #pragma unroll
                 for (int j = 0; j < NB; j++) {
                     const int i = tid + j * kThreads;
-                    if (i < BN * VPR) *reinterpret_cast<vec16 *>(Bs + (i / VPR) * ASTR + (i % VPR) * VEC) = rw[j];
+                    if (i < BN * VPR) {
+                        T *dst = dfwd ? Bs + (i / (BN / VEC)) * BP + (i % (BN / VEC)) * VEC
+                                      : Bs + (i / VPR) * ASTR + (i % VPR) * VEC;
+                        *reinterpret_cast<vec16 *>(dst) = rw[j];
+                    }
                 }
             };
             load_chunk(0);
@@ -227,9 +249,23 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 for (int ks = 0; ks < kRowsBK / M::KSTEP; ks++) {
                     const int kofs = ks * M::KSTEP + (lane >> 4) * M::KPL;
                     typename M::frag b[TN];
-                    #pragma unroll
-                    for (int cb = 0; cb < TN; cb++)
-                        b[cb] = M::load(Bs + (wn * TN * 16 + cb * 16 + (lane & 15)) * ASTR + kofs);
+                    if constexpr (kTr) {
+                        if (dfwd) {                   // 8 consecutive k of one column of [k][n]
+                            const bf16_t *bb = reinterpret_cast<const bf16_t *>(Bs) +
+                                               (ks * M::KSTEP + 8 * (lane >> 4) + ((lane & 15) >> 2)) * BP +
+                                               4 * (lane & 3) + wn * TN * 16;
+                            #pragma unroll
+                            for (int cb = 0; cb < TN; cb++) b[cb] = tr_frag(bb + cb * 16, BP);
+                        } else {
+                            #pragma unroll
+                            for (int cb = 0; cb < TN; cb++)
+                                b[cb] = M::load(Bs + (wn * TN * 16 + cb * 16 + (lane & 15)) * ASTR + kofs);
+                        }
+                    } else {
+                        #pragma unroll
+                        for (int cb = 0; cb < TN; cb++)
+                            b[cb] = M::load(Bs + (wn * TN * 16 + cb * 16 + (lane & 15)) * ASTR + kofs);
+                    }
                     #pragma unroll
                     for (int rb = 0; rb < TM; rb++) {
                         const typename M::frag a = M::load(As + (wm * TM * 16 + rb * 16 + (lane & 15)) * ASTR + kofs);
@@ -472,6 +508,21 @@ static double rows_algorithmic_bytes(const RowsParams &p)
     return e * (a + out + (double)p.taps * K * N);
 }
 
+// every operand span of the tiled 1x1 kernel below 2^31 bytes (32-bit raw
+// buffer offsets; the packed weights are at most ceil(N/32) * 32 * K_padded)
+static bool rows_spans_fit(int dtype, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro)
+{
+    const int64_t lim = (int64_t)1 << 31, es = dtype == DT_BF16 ? 2 : 4;
+    const int64_t src_rows = pro == PRO_POOLUP ? m / 4 : m;
+    return (src_rows * a_ldc + K) * es < lim && (pro != PRO_BNGRAD || (m * a2_ldc + K) * es < lim) &&
+           ceil_div(N, 32) * 32 * ceil_div(K, kRowsBK) * kRowsBK * es < lim;
+}
+
+bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro)
+{
+    return dtype == DT_BF16 && taps == 1 && rows_spans_fit(dtype, m, K, N, a_ldc, a2_ldc, pro);
+}
+
 template <typename T, int TAPS, int BM, int BN, int WM, int WN>
 static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 {
@@ -489,14 +540,8 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     TraceScope tr(KC_CONV, TAPS == 9 ? KID_CONV_3X3 : KID_CONV_1X1, s, rows_algorithmic_bytes(p),
                   2.0 * (double)p.m * TAPS * p.K * p.N);
     RowsParams q = p;
-    if (TAPS == 1) {                    // 32-bit raw-buffer offsets for the pipelined 1x1 chunk loop
-        const int64_t lim = (int64_t)1 << 31, es = (int64_t)sizeof(T);
-        const int64_t src_rows = p.pro == PRO_POOLUP ? p.m / 4 : p.m;
-        const int64_t nchunks = ceil_div(p.K, kRowsBK);
-        q.buf32 = (src_rows * p.a_ldc + p.K) * es < lim &&
-                  (p.pro != PRO_BNGRAD || (p.m * p.a2_ldc + p.K) * es < lim) &&
-                  (int64_t)grid.y * nchunks * BN * kRowsBK * es < lim;
-    }
+    q.buf32 = TAPS == 1 && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
+    if (q.wdirect && (!q.buf32 || !p.wraw)) return hipErrorInvalidValue;   // unpacked weights need this path
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, q);
     return hipGetLastError();
 }
@@ -504,7 +549,7 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 // Operands each prologue / epilogue mode reads must be present.
 static bool rows_operands_ok(const RowsParams &p)
 {
-    if (!p.a || !p.wpack || !p.y) return false;
+    if (!p.a || !(p.wdirect ? p.wraw : p.wpack) || !p.y) return false;
     if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return false;
     if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd ||
                                 (p.p_split ? (!p.p_alpha || !p.p_betap) : (!p.p_gamma || !p.p_dbeta || !p.p_dgamma))))

@@ -304,17 +304,6 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
 // 4 channels 4 (j % 4) .. +3 of row j / 4 and lane i receives channel i of
 // rows 0..3 (layout checked on the device).  For 3x3 every tap is a row
 // offset into the staged Z, so all nine taps share the G fragments.
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-
-__device__ __forceinline__ bf16x8 tr_frag(const bf16_t *p, int pitch)
-{
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p));
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p + 4 * pitch));
-    typedef short s16x8 __attribute__((ext_vector_type(8)));
-    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    return __builtin_bit_cast(bf16x8, v);
-}
 
 // Two workgroups per CU wherever the operand registers allow it without
 // spilling (all but the 64-channel 3x3 tiles, whose nine accumulator sets

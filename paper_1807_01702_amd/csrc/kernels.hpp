@@ -106,11 +106,13 @@ struct RowsParams {
     const float *e_gamma, *e_beta, *e_mean, *e_rstd;
     const float *e_shift;         // EPI_STATS: the sums are of (y - e_shift) (NULL: 0)
     int buf32;                    // tiled 1x1 kernel: operand spans below 2^31 bytes (set by its launcher)
+    int wdirect;                  // tiled bf16 1x1 kernel: weights read from wraw ([k][n], wtrans: [n][k]), no packing
 };
 int64_t rows_mtiles(int dtype, int taps, int64_t m, int n_out);
 size_t rows_pack_bytes(int dtype, int taps, int K, int N);
 // transpose = 0: forward packing of W[kh][kw][ci][co] (GEMM K = ci, N = co);
 // transpose = 1: data-gradient packing, flipped taps, GEMM K = co, N = ci.
+bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro);
 hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_out, int transpose, void *wpack,
                                hipStream_t s);
 hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s);

@@ -46,6 +46,24 @@ template <> struct Mfma<float> {
     }
 };
 
+// bf16 matrix-core fragment of 8 consecutive rows of one column from a
+// row-major LDS tile with the given row pitch (elements), by two transposing
+// 8-byte reads (ds_read_b64_tr_b16): within a group of 16 lanes, lane j
+// reads the 4 columns 4 (j % 4) .. +3 of row j / 4 and lane i receives
+// column i of rows 0..3; p is this lane's address of row j / 4 (+ 8 g for
+// lane group g), column 4 (j % 4).
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+__device__ __forceinline__ bf16x8 tr_frag(const bf16_t *p, int pitch)
+{
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p + 4 * pitch));
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
 // round an fp32 value to the storage type T (bf16: RNE)
 template <typename T> __device__ __forceinline__ T to_store(float f);
 template <> __device__ __forceinline__ float to_store<float>(float f) { return f; }

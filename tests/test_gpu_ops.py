@@ -63,6 +63,8 @@ FWD_CASES = [
     (True, 3, 1, 56, 56, 64, 64, 64, 64),        # full-width rows (W = 56)
     (True, 3, 2, 6, 61, 32, 8, 32, 8),           # widest rows of the persistent 3x3 kernel
     (True, 3, 1, 5, 62, 32, 8, 32, 8),           # one column past it (row-tile kernel)
+    (True, 1, 2, 7, 7, 512, 128, 520, 128),      # 1x1 with K > 256: tiled kernel, caller's weights unpacked
+    (True, 1, 1, 9, 11, 320, 96, 320, 104),      # same, partial output tile, output view
 ]
 
 
@@ -111,6 +113,8 @@ BWD_CASES = [
     (True, 3, 2, 7, 7, 128, 32),                # 7x7 rows: four image rows per K chunk
     (True, 3, 1, 5, 30, 64, 96),                # two rows per chunk, two output-channel tiles
     (False, 3, 2, 3, 62, 8, 12),                # widest rows, fp32
+    (True, 1, 2, 7, 7, 512, 128),               # tiled 1x1 forward weights [k][n] and data gradient [n][k] unpacked
+    (True, 1, 1, 9, 11, 288, 40),               # ragged: K and N past the 256-channel persistent kernel
 ]
 
 
