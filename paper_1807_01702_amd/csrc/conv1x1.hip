@@ -3,7 +3,10 @@
 //
 // One workgroup per CU (512 threads, 8 waves) keeps the whole weight matrix
 // in LDS -- read once from its [c_in][c_out] layout, transposed on load for
-// the forward GEMM -- and walks 128-pixel tiles t, t+G, t+2G, ...  For each
+// the forward GEMM -- and walks 128-pixel tiles t, t+G, t+2G, ... while every
+// workgroup of the grid G has one; the rows left over (fewer than G tiles)
+// are split evenly, one short tile per workgroup, so no workgroup runs a
+// whole extra tile while the others idle.  For each
 // tile the A rows held in registers are transformed by the prologue and
 // stored to LDS; the loads of the next tile (and the epilogue operand of this
 // tile) are issued before the matrix-core work, so HBM streams while the
@@ -52,7 +55,7 @@ static P1Geom p1_geom(int K, int N)
 // the epilogue is straight-line code and the compiler can keep the next
 // tile's loads in flight while it waits for the epilogue operand.
 template <int CBW, int NVA, int EK, bool BNG, int BM>
-__global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, int ntiles)
+__global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 {
     using T = bf16_t;
     using M = Mfma<T>;
@@ -161,13 +164,12 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     vec16 ra[NVA], rb[NVB];
     // the wave-uniform mode switches sit outside the slot loops, so each
     // mode's slots are straight-line code
-    auto load_a = [&](int tile) __attribute__((always_inline)) {
-        const int p0 = tile * BM;
+    auto load_a = [&](int p0, int lim) __attribute__((always_inline)) {
         if (!BNG && pool) {             // (the deferred-gradient variants never read a pooled gradient)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int pp = p0 + sr[j], c = sc[j];
-                const bool ok = j < nva && c < K && pp < m;
+                const bool ok = j < nva && c < K && pp < lim;
                 const int img = pp / (H * W);
                 const int rem = pp - img * H * W;
                 const int y = rem / W, x = rem - y * W;
@@ -178,7 +180,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int pp = p0 + sr[j], c = sc[j];
-                const bool ok = j < nva && c < K && pp < m;
+                const bool ok = j < nva && c < K && pp < lim;
                 ra[j] = bld16(abuf, ok ? (uint32_t)(pp * a_ldc + c) * 2u : kBufOff);
                 if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(pp * a2_ldc + c) * 2u : kBufOff);
             }
@@ -188,8 +190,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     // only, so rows past the end need no masking (their outputs are never
     // stored or counted); channels past K read zeros and have zero
     // coefficients and zero weights.
-    auto store_a = [&](int tile) __attribute__((always_inline)) {
-        (void)tile;
+    auto store_a = [&]() __attribute__((always_inline)) {
         auto put = [&](int j, const vec16 &v) __attribute__((always_inline)) {
             if (j < nva && sc[j] < KP) *reinterpret_cast<vec16 *>(As + sr[j] * g.lda + sc[j]) = v;
         };
@@ -256,13 +257,12 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
     T *yout = reinterpret_cast<T *>(p.y);
-    auto load_epi = [&](int tile) __attribute__((always_inline)) {
+    auto load_epi = [&](int p0, int lim) __attribute__((always_inline)) {
         if (!READS) return;
-        const int p0 = tile * BM;
         #pragma unroll
         for (int j = 0; j < NVX; j++) {
             const int r = r0 + j * RSTEP, pp = p0 + r;
-            const bool ok = col_ok && r < BM && pp < m;
+            const bool ok = col_ok && r < BM && pp < lim;
             if (EK == EK_STORE_ACC) rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
             else rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
             if (EK == EK_BNBWD_SCACC) rd[j < NVD ? j : 0] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
@@ -276,15 +276,25 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
     for (int e = 0; e < VEC; e++) {
         eM[e] = epi[n + e]; eR[e] = epi[NP + n + e]; eG[e] = epi[2 * NP + n + e]; eB[e] = epi[3 * NP + n + e];
     }
-    int tile = blockIdx.x;
-    if (tile < ntiles) load_a(tile);
-    for (; tile < ntiles; tile += gridDim.x) {
-        store_a(tile);
+    // work items: F rounds of whole tiles (item k < F is tile k*G + gi, rows
+    // [p0, p0 + BM)), then this workgroup's share [lo, hi) of the R rows left
+    const int G = gridDim.x, gi = blockIdx.x;
+    const int F = m / (G * BM), R = m - F * G * BM;         // R < G*BM <= 2^16, so gi*R fits
+    const int lo = F * G * BM + gi * R / G, hi = F * G * BM + (gi + 1) * R / G;
+    const int nitems = F + (hi > lo ? 1 : 0);
+    auto item = [&](int k, int &p0, int &lim) __attribute__((always_inline)) {
+        if (k < F) { p0 = (k * G + gi) * BM; lim = p0 + BM; } else { p0 = lo; lim = hi; }
+    };
+    if (nitems > 0) { int q0, ql; item(0, q0, ql); load_a(q0, ql); }
+    for (int k = 0; k < nitems; k++) {
+        int p0, lim;
+        item(k, p0, lim);
+        store_a();
         __syncthreads();
         // epilogue operand first: the epilogue waits for it while the next
         // tile's rows (issued after it) may still be in flight
-        load_epi(tile);
-        if (tile + (int)gridDim.x < ntiles) load_a(tile + gridDim.x);
+        load_epi(p0, lim);
+        if (k + 1 < nitems) { int q0, ql; item(k + 1, q0, ql); load_a(q0, ql); }
         // ---- matrix cores: 16 RB rows x NP/2 columns per wave ----
         f32x4 acc[RB][CBW];
         #pragma unroll
@@ -293,7 +303,8 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
             for (int cb = 0; cb < CBW; cb++) acc[ib][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
         const T *arow = As + (wm * (16 * RB) + (lane & 15)) * g.lda + (lane >> 4) * M::KPL;
         const T *brow = Ws + (wn * (NP / 2) + (lane & 15)) * g.ldw + (lane >> 4) * M::KPL;
-        for (int k0 = 0; k0 < KP; k0 += M::KSTEP) {
+        // (a wave whose 16*RB rows all lie past the end of a short tile skips them)
+        for (int k0 = 0; k0 < (wm * 16 * RB < lim - p0 ? KP : 0); k0 += M::KSTEP) {
             typename M::frag a[RB];
             #pragma unroll
             for (int ib = 0; ib < RB; ib++) a[ib] = M::load(arow + ib * 16 * g.lda + k0);
@@ -318,12 +329,11 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
         __syncthreads();
         // ---- epilogue row pass: all outputs of this thread first (invalid rows
         // contribute zeros), then the stores back to back ----
-        const int p0 = tile * BM;
         vec16 vo[RPT];
         #pragma unroll
         for (int j = 0; j < RPT; j++) {
             const int r = r0 + j * RSTEP;
-            const bool ok = col_ok && r < BM && p0 + r < m;
+            const bool ok = col_ok && r < BM && p0 + r < lim;
             const vec16 cv = *reinterpret_cast<const vec16 *>(Cs + (r < BM ? r : 0) * g.ldc + n);
             float f[VEC];
             Elem<T>::unpack(cv, f);
@@ -368,7 +378,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g, 
         #pragma unroll
         for (int j = 0; j < RPT; j++) {
             const int r = r0 + j * RSTEP;
-            if (col_ok && r < BM && p0 + r < m) stg16(yout + (int64_t)(p0 + r) * y_ldc + n, vo[j]);
+            if (col_ok && r < BM && p0 + r < lim) stg16(yout + (int64_t)(p0 + r) * y_ldc + n, vo[j]);
         }
         __syncthreads();
     }
@@ -444,7 +454,7 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
     if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD || EK == EK_BNBWD_SC) out += m * p.N;
     if (EK == EK_BNBWD_SCACC) out += 2.0 * m * p.N;
     TraceScope tr(KC_CONV, KID_CONV_1X1, s, 2.0 * (a + out + (double)p.K * p.N), 2.0 * m * p.K * p.N);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kP1Threads), g.lds, s, p, g, ntiles);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kP1Threads), g.lds, s, p, g);
     return hipGetLastError();
 }
 
