@@ -57,9 +57,18 @@ struct RowsCfg {
                                                           : (EPI_BYTES > RED_BYTES ? EPI_BYTES : RED_BYTES);
 };
 
-template <typename T, int TAPS, int BM, int BN, int WM, int WN>
+// SP: a compile-time case of the pipelined bf16 1x1 path (caller's weights,
+// every span below 2^31 bytes), so its chunk loop has no mode branches:
+// SP_FWD_BNRELU: forward, BN+ReLU prologue, weights [k][n] (with one
+// workgroup per CU, as in late dense blocks, the branches are on the
+// critical path: about 20% of the launch).  SP_RUNTIME: every mode, chosen at
+// run time.  (The same specialisation of the data gradient measured slower.)
+enum { SP_RUNTIME = 0, SP_FWD_BNRELU = 1 };
+
+template <typename T, int TAPS, int BM, int BN, int WM, int WN, int SP>
 __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
 {
+    static_assert(SP == SP_RUNTIME || (TAPS == 1 && sizeof(T) == 2), "specialised cases are bf16 1x1");
     using Cfg = RowsCfg<T, TAPS, BM, BN>;
     using M = Mfma<T>;
     constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
@@ -117,7 +126,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     __syncthreads();
 
     if constexpr (TAPS == 1) {
-        if (p.buf32) {
+        if (SP != SP_RUNTIME || p.buf32) {
             // 1x1 with every operand span below 2^31 bytes: the next chunk's A
             // rows and weights are loaded into registers (raw buffer loads,
             // out-of-range offsets read zeros) while the matrix cores work on
@@ -125,18 +134,19 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             // channel vector i % VPR of the chunk (i = tid + j kThreads); its
             // source pixel is fixed for the whole tile.
             constexpr int NA = (BM * VPR + kThreads - 1) / kThreads, NB = (BN * VPR + kThreads - 1) / kThreads;
-            const bool pool = p.pro == PRO_POOLUP;
+            const int pro = SP == SP_FWD_BNRELU ? PRO_BNRELU : p.pro;
+            const bool pool = pro == PRO_POOLUP;
             const int64_t src_rows = pool ? m / 4 : m;
             const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((src_rows - 1) * p.a_ldc + K) * sizeof(T)));
             const __amdgpu_buffer_rsrc_t a2buf =
-                buf_view(p.pro == PRO_BNGRAD ? p.a2 : p.a,
-                         p.pro == PRO_BNGRAD ? (uint32_t)(((m - 1) * p.a2_ldc + K) * sizeof(T)) : 0u);
+                buf_view(pro == PRO_BNGRAD ? p.a2 : p.a,
+                         pro == PRO_BNGRAD ? (uint32_t)(((m - 1) * p.a2_ldc + K) * sizeof(T)) : 0u);
             // weights: packed [nt][chunk][n][32 k], or (bf16, wdirect) the caller's
             // [k][n] (forward: staged as rows of k, fragments by transposing
             // reads) or [n][k] (data gradient: rows of n, as the packed layout)
             constexpr bool kTr = std::is_same<T, bf16_t>::value;
-            const bool direct = kTr && p.wdirect;
-            const bool dfwd = direct && !p.wtrans;
+            const bool direct = SP != SP_RUNTIME || (kTr && p.wdirect);
+            const bool dfwd = SP == SP_FWD_BNRELU || (SP == SP_RUNTIME && direct && !p.wtrans);
             constexpr int BP = BN + 8;                                // pitch of the [k][n] staging
             const __amdgpu_buffer_rsrc_t wbuf =
                 direct ? buf_view(p.wraw, (uint32_t)((int64_t)K * N * sizeof(T)))
@@ -166,7 +176,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     const int c = c0 + avec[j] * VEC;
                     const bool ok = apix[j] >= 0 && c < K;
                     ra[j] = bld16(abuf, ok ? (uint32_t)(apix[j] * a_ldc + c) * (uint32_t)sizeof(T) : kBufOff);
-                    if (p.pro == PRO_BNGRAD)
+                    if (pro == PRO_BNGRAD)
                         rx[j] = bld16(a2buf, ok ? (uint32_t)(apix[j] * a2_ldc + c) * (uint32_t)sizeof(T) : kBufOff);
                 }
                 const uint32_t wofs = (uint32_t)(((int64_t)nt * nchunks + ch) * (BN * kRowsBK));
@@ -192,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 for (int j = 0; j < NA; j++) {
                     const int c = c0 + avec[j] * VEC;
                     vec16 out = ra[j];
-                    if (p.pro == PRO_BNRELU) {
+                    if (pro == PRO_BNRELU) {
                         const int cc = c < K ? c : 0;
                         float f[VEC];
                         Elem<T>::unpack(ra[j], f);
@@ -202,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                             f[e] = t > 0.f ? t : 0.f;
                         }
                         out = Elem<T>::pack(f);
-                    } else if (p.pro == PRO_BNGRAD) {
+                    } else if (pro == PRO_BNGRAD) {
                         const int cc = c < K ? c : 0;
                         float d[VEC], x[VEC];
                         Elem<T>::unpack(ra[j], d);
@@ -211,7 +221,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                         for (int e = 0; e < VEC; e++)
                             d[e] = __builtin_fmaf(coef[cc + e], d[e], __builtin_fmaf(coef[K + cc + e], x[e], coef[2 * K + cc + e]));
                         out = Elem<T>::pack(d);
-                    } else if (p.pro == PRO_RELU) {
+                    } else if (pro == PRO_RELU) {
                         float f[VEC];
                         Elem<T>::unpack(ra[j], f);
                         #pragma unroll
@@ -277,7 +287,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             }
         }
     }
-    for (int ch = 0; ch < ((TAPS == 1 && p.buf32) ? 0 : nchunks); ch++) {
+    for (int ch = 0; ch < ((TAPS == 1 && (SP != SP_RUNTIME || p.buf32)) ? 0 : nchunks); ch++) {
         const int c0 = ch * kRowsBK;
         // ---- stage A (prologue applied, zero outside the tensor) ----
         for (int i = tid; i < arows * VPR; i += kThreads) {
@@ -523,13 +533,13 @@ bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a
     return dtype == DT_BF16 && taps == 1 && rows_spans_fit(dtype, m, K, N, a_ldc, a2_ldc, pro);
 }
 
-template <typename T, int TAPS, int BM, int BN, int WM, int WN>
+template <typename T, int TAPS, int BM, int BN, int WM, int WN, int SP = SP_RUNTIME>
 static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 {
     using Cfg = RowsCfg<T, TAPS, BM, BN>;
     const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD ? 3 : 0;
     const size_t lds = Cfg::LDS + (size_t)P * p.K * sizeof(float);
-    auto kern = k_conv_rows<T, TAPS, BM, BN, WM, WN>;
+    auto kern = k_conv_rows<T, TAPS, BM, BN, WM, WN, SP>;
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
@@ -542,6 +552,7 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     RowsParams q = p;
     q.buf32 = TAPS == 1 && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
     if (q.wdirect && (!q.buf32 || !p.wraw)) return hipErrorInvalidValue;   // unpacked weights need this path
+    if (SP == SP_FWD_BNRELU && (!q.wdirect || p.wtrans || p.pro != PRO_BNRELU)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, q);
     return hipGetLastError();
 }
@@ -567,6 +578,12 @@ hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s)
     const RowsTile t = rows_tile(p.dtype, p.taps, p.N);
     if (p.dtype == DT_BF16) {
         if (p.taps == 1) {
+            const bool dw = p.wdirect && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
+            if (dw && p.pro == PRO_BNRELU && !p.wtrans) {
+                if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1, SP_FWD_BNRELU>(p, s);
+                if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1, SP_FWD_BNRELU>(p, s);
+                return run_rows<bf16_t, 1, 128, 128, 2, 2, SP_FWD_BNRELU>(p, s);
+            }
             if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1>(p, s);
             if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1>(p, s);
             return run_rows<bf16_t, 1, 128, 128, 2, 2>(p, s);

@@ -65,6 +65,8 @@ FWD_CASES = [
     (True, 3, 1, 5, 62, 32, 8, 32, 8),           # one column past it (row-tile kernel)
     (True, 1, 2, 7, 7, 512, 128, 520, 128),      # 1x1 with K > 256: tiled kernel, caller's weights unpacked
     (True, 1, 1, 9, 11, 320, 96, 320, 104),      # same, partial output tile, output view
+    (True, 1, 1, 5, 13, 296, 24, 304, 24),       # tiled 1x1: ragged last 64-channel chunk, 32-channel output tile
+    (True, 1, 1, 3, 5, 1000, 64, 1000, 64),      # tiled 1x1: 16 chunks, 64-channel output tile
 ]
 
 
@@ -115,6 +117,7 @@ BWD_CASES = [
     (False, 3, 2, 3, 62, 8, 12),                # widest rows, fp32
     (True, 1, 2, 7, 7, 512, 128),               # tiled 1x1 forward weights [k][n] and data gradient [n][k] unpacked
     (True, 1, 1, 9, 11, 288, 40),               # ragged: K and N past the 256-channel persistent kernel
+    (True, 1, 1, 6, 7, 264, 24),                # tiled 1x1: one 8-channel tail chunk, 32-channel output tile
 ]
 
 
