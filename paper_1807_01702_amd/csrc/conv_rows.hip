@@ -59,11 +59,12 @@ struct RowsCfg {
 
 // SP: a compile-time case of the pipelined bf16 1x1 path (caller's weights,
 // every span below 2^31 bytes), so its chunk loop has no mode branches:
-// SP_FWD_BNRELU: forward, BN+ReLU prologue, weights [k][n] (with one
-// workgroup per CU, as in late dense blocks, the branches are on the
-// critical path: about 20% of the launch).  SP_RUNTIME: every mode, chosen at
-// run time.  (The same specialisation of the data gradient measured slower.)
-enum { SP_RUNTIME = 0, SP_FWD_BNRELU = 1 };
+// SP_FWD_BNRELU: forward, BN+ReLU prologue, weights [k][n];
+// SP_DGRAD_BNGRAD: data gradient, deferred-gradient prologue, weights [n][k];
+// SP_RUNTIME: every mode, chosen at run time.  With one workgroup per CU, as
+// in late dense blocks, the mode branches are on the critical path (forward
+// about 20% of the launch, data gradient about 6%).
+enum { SP_RUNTIME = 0, SP_FWD_BNRELU = 1, SP_DGRAD_BNGRAD = 2 };
 
 template <typename T, int TAPS, int BM, int BN, int WM, int WN, int SP>
 __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
@@ -134,7 +135,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             // channel vector i % VPR of the chunk (i = tid + j kThreads); its
             // source pixel is fixed for the whole tile.
             constexpr int NA = (BM * VPR + kThreads - 1) / kThreads, NB = (BN * VPR + kThreads - 1) / kThreads;
-            const int pro = SP == SP_FWD_BNRELU ? PRO_BNRELU : p.pro;
+            const int pro = SP == SP_FWD_BNRELU ? PRO_BNRELU : (SP == SP_DGRAD_BNGRAD ? PRO_BNGRAD : p.pro);
             const bool pool = pro == PRO_POOLUP;
             const int64_t src_rows = pool ? m / 4 : m;
             const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((src_rows - 1) * p.a_ldc + K) * sizeof(T)));
@@ -553,6 +554,7 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     q.buf32 = TAPS == 1 && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
     if (q.wdirect && (!q.buf32 || !p.wraw)) return hipErrorInvalidValue;   // unpacked weights need this path
     if (SP == SP_FWD_BNRELU && (!q.wdirect || p.wtrans || p.pro != PRO_BNRELU)) return hipErrorInvalidValue;
+    if (SP == SP_DGRAD_BNGRAD && (!q.wdirect || !p.wtrans || p.pro != PRO_BNGRAD)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, q);
     return hipGetLastError();
 }
@@ -583,6 +585,11 @@ hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s)
                 if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1, SP_FWD_BNRELU>(p, s);
                 if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1, SP_FWD_BNRELU>(p, s);
                 return run_rows<bf16_t, 1, 128, 128, 2, 2, SP_FWD_BNRELU>(p, s);
+            }
+            if (dw && p.pro == PRO_BNGRAD && p.wtrans) {
+                if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1, SP_DGRAD_BNGRAD>(p, s);
+                if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1, SP_DGRAD_BNGRAD>(p, s);
+                return run_rows<bf16_t, 1, 128, 128, 2, 2, SP_DGRAD_BNGRAD>(p, s);
             }
             if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1>(p, s);
             if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1>(p, s);
