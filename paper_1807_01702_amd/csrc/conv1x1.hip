@@ -54,9 +54,17 @@ static P1Geom p1_geom(int K, int N)
 // prologue reads a second operand (PRO_BNGRAD) are compile-time as well, so
 // the epilogue is straight-line code and the compiler can keep the next
 // tile's loads in flight while it waits for the epilogue operand.
-template <int CBW, int NVA, int EK, bool BNG, int BM>
+// PC: the prologue, compile-time where it pays: PC_BNGRAD (the deferred
+// BN input gradient, which reads a second operand), PC_BNRELU (the forward
+// BN+ReLU with the statistics epilogue), PC_RUNTIME (PRO_NONE / PRO_BNRELU /
+// PRO_RELU / PRO_POOLUP chosen at run time).
+enum { PC_RUNTIME = 0, PC_BNGRAD = 1, PC_BNRELU = 2 };
+
+template <int CBW, int NVA, int EK, int PC, int BM>
 __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 {
+    constexpr bool BNG = PC == PC_BNGRAD;
+    const int pro = PC == PC_BNRELU ? PRO_BNRELU : (PC == PC_BNGRAD ? PRO_BNGRAD : p.pro);
     using T = bf16_t;
     using M = Mfma<T>;
     constexpr int VEC = 8;
@@ -80,7 +88,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     const int H = p.h, W = p.w;
     const T *wsrc = reinterpret_cast<const T *>(p.wraw);
     const int a_ldc = (int)p.a_ldc, a2_ldc = (int)p.a2_ldc, y_ldc = (int)p.y_ldc, ex_ldc = (int)p.ex_ldc;
-    const bool pool = p.pro == PRO_POOLUP;
+    const bool pool = pro == PRO_POOLUP;
     // operand views as raw buffers (launcher guarantees each spans < 2^31 bytes)
     const int64_t arows = pool ? (int64_t)m / 4 : m;
     const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((arows - 1) * a_ldc + K) * 2));
@@ -131,9 +139,9 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef)
     for (int c = tid; c < KP; c += kP1Threads) {
         float c0 = 0.f, c1 = 0.f, c2 = 0.f;
-        if (c < K && p.pro == PRO_BNRELU) {
+        if (c < K && pro == PRO_BNRELU) {
             c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
-        } else if (c < K && p.pro == PRO_BNGRAD) {
+        } else if (c < K && pro == PRO_BNGRAD) {
             deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
                           p.p_alpha, p.p_betap, c0, c1, c2);
         }
@@ -208,7 +216,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
                 put(j, Elem<T>::pack(f));
             }
-        } else if (p.pro == PRO_BNRELU) {                 // z = max(x c0 + c1, 0)
+        } else if (pro == PRO_BNRELU) {                   // z = max(x c0 + c1, 0)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int c = sc[j] < KP ? sc[j] : 0;
@@ -223,7 +231,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 }
                 put(j, Elem<T>::pack(f));
             }
-        } else if (p.pro == PRO_RELU) {
+        } else if (pro == PRO_RELU) {
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 float f[VEC];
@@ -428,10 +436,11 @@ int64_t conv1x1_partial_rows(int64_t m)
     return tiles < g ? tiles : g;
 }
 
-template <int CBW, int NVA, int EK, bool BNG, int BM>
+template <int CBW, int NVA, int EK, int PC, int BM>
 static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
-    auto kern = k_conv1x1<CBW, NVA, EK, BNG, BM>;
+    constexpr bool BNG = PC == PC_BNGRAD;
+    auto kern = k_conv1x1<CBW, NVA, EK, PC, BM>;
     static bool attr_set = false;
     if (!attr_set) {
         const hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
@@ -461,45 +470,45 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
 // Tile height: 128 rows unless the operand registers of the variant would not
 // fit the 256 VGPRs a wave has at two waves per SIMD; then 64 rows, which
 // halves every per-thread operand array.
-template <int CBW, int NVA128, int EK, bool BNG>
+template <int CBW, int NVA128, int EK, int PC>
 static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK >= EK_BNBWD;
-    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && BNG);
-    if constexpr (small) return run_p1<CBW, 4, EK, BNG, 64>(p, g, s, rows);
-    else return run_p1<CBW, NVA128, EK, BNG, 128>(p, g, s, rows);
+    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && PC == PC_BNGRAD);
+    if constexpr (small) return run_p1<CBW, 4, EK, PC, 64>(p, g, s, rows);
+    else return run_p1<CBW, NVA128, EK, PC, 128>(p, g, s, rows);
 }
 
-template <int NVA128, int EK, bool BNG>
+template <int NVA128, int EK, int PC>
 static hipError_t run_p1_cbw(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     switch (g.NP / 32) {
-    case 1: return run_p1_bm<1, NVA128, EK, BNG>(p, g, s, rows);
-    case 2: return run_p1_bm<2, NVA128, EK, BNG>(p, g, s, rows);
-    case 4: return run_p1_bm<4, NVA128, EK, BNG>(p, g, s, rows);
-    default: return run_p1_bm<8, NVA128, EK, BNG>(p, g, s, rows);
+    case 1: return run_p1_bm<1, NVA128, EK, PC>(p, g, s, rows);
+    case 2: return run_p1_bm<2, NVA128, EK, PC>(p, g, s, rows);
+    case 4: return run_p1_bm<4, NVA128, EK, PC>(p, g, s, rows);
+    default: return run_p1_bm<8, NVA128, EK, PC>(p, g, s, rows);
     }
 }
 
-template <int EK, bool BNG>
+template <int EK, int PC>
 static hipError_t run_p1_nva(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     const int nva = (int)ceil_div((int64_t)kP1BM * (g.KP / 8), kP1Threads);
-    if (nva <= 4) return run_p1_cbw<4, EK, BNG>(p, g, s, rows);
-    return run_p1_cbw<8, EK, BNG>(p, g, s, rows);
+    if (nva <= 4) return run_p1_cbw<4, EK, PC>(p, g, s, rows);
+    return run_p1_cbw<8, EK, PC>(p, g, s, rows);
 }
 
-template <bool BNG>
+template <int PC>
 static hipError_t run_p1_ek(const RowsParams &p, const P1Geom &g, int ek, hipStream_t s, int64_t *rows)
 {
     switch (ek) {
-    case EK_STORE: return run_p1_nva<EK_STORE, BNG>(p, g, s, rows);
-    case EK_STORE_ACC: return run_p1_nva<EK_STORE_ACC, BNG>(p, g, s, rows);
-    case EK_STATS: return run_p1_nva<EK_STATS, BNG>(p, g, s, rows);
-    case EK_RELUMASK: return run_p1_nva<EK_RELUMASK, BNG>(p, g, s, rows);
-    case EK_BNBWD_SC: return run_p1_nva<EK_BNBWD_SC, BNG>(p, g, s, rows);
-    case EK_BNBWD_SCACC: return run_p1_nva<EK_BNBWD_SCACC, BNG>(p, g, s, rows);
-    default: return run_p1_nva<EK_BNBWD, BNG>(p, g, s, rows);
+    case EK_STORE: return run_p1_nva<EK_STORE, PC>(p, g, s, rows);
+    case EK_STORE_ACC: return run_p1_nva<EK_STORE_ACC, PC>(p, g, s, rows);
+    case EK_STATS: return run_p1_nva<EK_STATS, PC>(p, g, s, rows);
+    case EK_RELUMASK: return run_p1_nva<EK_RELUMASK, PC>(p, g, s, rows);
+    case EK_BNBWD_SC: return run_p1_nva<EK_BNBWD_SC, PC>(p, g, s, rows);
+    case EK_BNBWD_SCACC: return run_p1_nva<EK_BNBWD_SCACC, PC>(p, g, s, rows);
+    default: return run_p1_nva<EK_BNBWD, PC>(p, g, s, rows);
     }
 }
 
@@ -521,8 +530,9 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
         return hipErrorInvalidValue;
     const P1Geom g = p1_geom(p.K, p.N);
     const int ek = epilogue_kind(p.epi, p.accumulate, p.e_scale);
-    if (p.pro == PRO_BNGRAD) return run_p1_ek<true>(p, g, ek, s, rows);
-    return run_p1_ek<false>(p, g, ek, s, rows);
+    if (p.pro == PRO_BNGRAD) return run_p1_ek<PC_BNGRAD>(p, g, ek, s, rows);
+    if (p.pro == PRO_BNRELU && ek == EK_STATS) return run_p1_nva<EK_STATS, PC_BNRELU>(p, g, s, rows);
+    return run_p1_ek<PC_RUNTIME>(p, g, ek, s, rows);
 }
 
 }  // namespace bnr
