@@ -134,9 +134,17 @@ __device__ __forceinline__ int p3_pixel(int P, const P3Geom &g, int H, int W)
 // so the epilogue is straight-line code and the compiler can keep the next
 // tile's loads in flight while it waits for the epilogue operand (a runtime
 // mode switch makes it wait for every outstanding load at each branch).
-template <int WK, int WN, int EK, bool BNG>
+// PC: the prologue, compile-time where it pays: PC3_BNGRAD (the deferred
+// BN input gradient, which reads a second operand), PC3_BNRELU (the forward
+// BN+ReLU with the statistics epilogue), PC3_RUNTIME (PRO_NONE / PRO_BNRELU /
+// PRO_RELU chosen at run time).
+enum { PC3_RUNTIME = 0, PC3_BNGRAD = 1, PC3_BNRELU = 2 };
+
+template <int WK, int WN, int EK, int PC>
 __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
 {
+    constexpr bool BNG = PC == PC3_BNGRAD;
+    const int pro = PC == PC3_BNRELU ? PRO_BNRELU : (PC == PC3_BNGRAD ? PRO_BNGRAD : p.pro);
     using T = bf16_t;
     using M = Mfma<T>;
     constexpr int VEC = 8;
@@ -255,9 +263,9 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef)
     for (int c = tid; c < KPC; c += kP3Threads) {
         float c0 = 0.f, c1 = 0.f, c2 = 0.f;
-        if (c < K && p.pro == PRO_BNRELU) {
+        if (c < K && pro == PRO_BNRELU) {
             c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
-        } else if (c < K && p.pro == PRO_BNGRAD) {
+        } else if (c < K && pro == PRO_BNGRAD) {
             deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
                           p.p_alpha, p.p_betap, c0, c1, c2);
         }
@@ -316,7 +324,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 #pragma unroll
                 for (int i = 0; i < 4; i++) outv[j].u[i] &= keep;
             }
-        } else if (p.pro == PRO_BNRELU) {                 // z = max(x c0 + c1, 0)
+        } else if (pro == PRO_BNRELU) {                   // z = max(x c0 + c1, 0)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int c = (4 * j + (tid & 3)) * VEC;
@@ -330,7 +338,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 #pragma unroll
                 for (int i = 0; i < 4; i++) outv[j].u[i] &= keep;
             }
-        } else if (p.pro == PRO_RELU) {                   // (padding rows load zeros)
+        } else if (pro == PRO_RELU) {                     // (padding rows load zeros)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 float f[VEC];
@@ -570,10 +578,11 @@ int64_t conv3x3_partial_rows(int64_t m)
     return tiles < g ? tiles : g;
 }
 
-template <int WK, int WN, int EK, bool BNG>
+template <int WK, int WN, int EK, int PC>
 static hipError_t run_p3(const RowsParams &p, const P3Geom &g, hipStream_t s)
 {
-    auto kern = k_conv3x3<WK, WN, EK, BNG>;
+    constexpr bool BNG = PC == PC3_BNGRAD;
+    auto kern = k_conv3x3<WK, WN, EK, PC>;
     static bool attr_set = false;
     if (!attr_set) {
         const hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
@@ -592,30 +601,30 @@ static hipError_t run_p3(const RowsParams &p, const P3Geom &g, hipStream_t s)
 }
 
 // (K slices, N slices) with WK * WN <= 4, WK in {1, 2, 4}
-template <int EK, bool BNG>
+template <int EK, int PC>
 static hipError_t run_p3_shape(const RowsParams &p, const P3Geom &g, hipStream_t s)
 {
     const int wk = g.KP / 32, wn = g.NP / 32;
     switch (wk * 8 + wn) {
-    case 1 * 8 + 1: return run_p3<1, 1, EK, BNG>(p, g, s);
-    case 1 * 8 + 2: return run_p3<1, 2, EK, BNG>(p, g, s);
-    case 1 * 8 + 4: return run_p3<1, 4, EK, BNG>(p, g, s);
-    case 2 * 8 + 1: return run_p3<2, 1, EK, BNG>(p, g, s);
-    case 2 * 8 + 2: return run_p3<2, 2, EK, BNG>(p, g, s);
-    case 4 * 8 + 1: return run_p3<4, 1, EK, BNG>(p, g, s);
+    case 1 * 8 + 1: return run_p3<1, 1, EK, PC>(p, g, s);
+    case 1 * 8 + 2: return run_p3<1, 2, EK, PC>(p, g, s);
+    case 1 * 8 + 4: return run_p3<1, 4, EK, PC>(p, g, s);
+    case 2 * 8 + 1: return run_p3<2, 1, EK, PC>(p, g, s);
+    case 2 * 8 + 2: return run_p3<2, 2, EK, PC>(p, g, s);
+    case 4 * 8 + 1: return run_p3<4, 1, EK, PC>(p, g, s);
     default: return hipErrorInvalidValue;
     }
 }
 
-template <bool BNG>
+template <int PC>
 static hipError_t run_p3_ek(const RowsParams &p, const P3Geom &g, int ek, hipStream_t s)
 {
     switch (ek) {
-    case EK_STORE: return run_p3_shape<EK_STORE, BNG>(p, g, s);
-    case EK_STORE_ACC: return run_p3_shape<EK_STORE_ACC, BNG>(p, g, s);
-    case EK_STATS: return run_p3_shape<EK_STATS, BNG>(p, g, s);
-    case EK_RELUMASK: return run_p3_shape<EK_RELUMASK, BNG>(p, g, s);
-    default: return run_p3_shape<EK_BNBWD, BNG>(p, g, s);
+    case EK_STORE: return run_p3_shape<EK_STORE, PC>(p, g, s);
+    case EK_STORE_ACC: return run_p3_shape<EK_STORE_ACC, PC>(p, g, s);
+    case EK_STATS: return run_p3_shape<EK_STATS, PC>(p, g, s);
+    case EK_RELUMASK: return run_p3_shape<EK_RELUMASK, PC>(p, g, s);
+    default: return run_p3_shape<EK_BNBWD, PC>(p, g, s);
     }
 }
 
@@ -646,8 +655,9 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
     if (mp >= (lim >> 1)) return hipErrorInvalidValue;
     g.MP = (int)mp;
     const int ek = epilogue_kind(p.epi, p.accumulate, 0);
-    if (p.pro == PRO_BNGRAD) return run_p3_ek<true>(p, g, ek, s);
-    return run_p3_ek<false>(p, g, ek, s);
+    if (p.pro == PRO_BNGRAD) return run_p3_ek<PC3_BNGRAD>(p, g, ek, s);
+    if (p.pro == PRO_BNRELU && ek == EK_STATS) return run_p3_shape<EK_STATS, PC3_BNRELU>(p, g, s);
+    return run_p3_ek<PC3_RUNTIME>(p, g, ek, s);
 }
 
 }  // namespace bnr
