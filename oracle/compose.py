@@ -22,6 +22,18 @@ tensor (or hands it to a matrix unit) in its operand precision: identity for
 the fp32 configuration (the oracle then runs fully in fp64), bf16
 round-to-nearest-even for the bf16-operand configurations.  Everything between
 those points, including all statistics and reductions, stays fp64.
+The paper runs in fp32 only, so the rounding sites are a reading:
+  forward   z = relu(bn(x)) and every CONV output (the MFMA operand and the
+            stored activation), the pooled outputs, the residual block output;
+  backward  the masked BN output gradient dy of every unit; the gradient
+            operand a CONV's backward receives when it is a BN input gradient
+            (the deferred dx formed on load); the concatenation gradient G
+            after each reader's addition (Split backward) and its initial
+            value; the transition's unpooled gradient; the residual block's
+            masked gradient ds and its input gradient dX; the stem's BN input
+            gradient.
+  never     batch statistics, dgamma, dbeta and dW (fp32 results on the GPU,
+            fp64 here).
 """
 import numpy as np
 
@@ -47,14 +59,15 @@ def unit_fwd(x, gamma, beta, wt, eps, rnd):
 def unit_bwd(c, g, rnd):
     """Backward of ``unit_fwd`` for L = sum(out * g); g in operand precision.
 
-    Returns dz (CONV input gradient), dy (BN output gradient after the ReLU
-    mask, stored), dW, dgamma, dbeta and dx (fp64, not rounded)."""
+    Returns g (the gradient operand as received), dz (CONV input gradient),
+    dy (BN output gradient after the ReLU mask, stored), dW, dgamma, dbeta and
+    dx (fp64, not rounded)."""
     K = c["wt"].shape[0]
     dz = P.conv_dgrad(g, c["wt"], c["x"].shape[1:3])
     dy = rnd(P.relu_bwd(dz, c["y"]))
     dw = P.conv_wgrad(c["z"], g, K)
     dx, dgamma, dbeta = P.bn_bwd(c["x"], dy, c["gamma"], c["mean"], c["rstd"])
-    return dict(dz=dz, dy=dy, dw=dw, dgamma=dgamma, dbeta=dbeta, dx=dx)
+    return dict(g=np.asarray(g, np.float64), dz=dz, dy=dy, dw=dw, dgamma=dgamma, dbeta=dbeta, dx=dx)
 
 
 # ------------------------------------------------- DenseNet composite layer ----
@@ -159,7 +172,7 @@ def resnet_block_bwd(c, dr, rnd):
     g1 = rnd(b2["dx"])
     dX = rnd(ds + P.conv_dgrad(g1, p["w1"], c["X"].shape[1:3]))
     dw1 = P.conv_wgrad(c["X"], g1, p["w1"].shape[0])
-    return dX, dict(dw1=dw1, b2=b2, b3=b3, dgamma3=dgamma3, dbeta3=dbeta3)
+    return dX, dict(ds=ds, g1=g1, dw1=dw1, b2=b2, b3=b3, dgamma3=dgamma3, dbeta3=dbeta3)
 
 
 # ------------------------------------------------ full DenseNet(-121) ----
@@ -221,6 +234,7 @@ def densenet_bwd(c, rnd):
     dz0 = P.maxpool_bwd(st["z"], dX, 3, 2, 1)
     dy0 = rnd(P.relu_bwd(dz0, st["y"]))
     dx0, dg0, db0 = P.bn_bwd(st["s"], dy0, d["stem"]["gamma"], st["mean"], st["rstd"])
-    dw0 = P.conv_wgrad(st["img"], rnd(dx0), d["stem"]["w"].shape[0], stride=2, pad=3)
-    stem = dict(dX=dX, dy=dy0, dw=dw0, dgamma=dg0, dbeta=db0)
+    g0 = rnd(dx0)
+    dw0 = P.conv_wgrad(st["img"], g0, d["stem"]["w"].shape[0], stride=2, pad=3)
+    stem = dict(dX=dX, dy=dy0, g=g0, dw=dw0, dgamma=dg0, dbeta=db0)
     return dict(head=head, blocks=blocks, stem=stem)

@@ -568,11 +568,20 @@ static bnr_status bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn 
     const int es = esize(d->dtype);
     const int64_t m = pixels(d);
     const Range rx = view_range(x, m, d->c_in, d->in_ldc, es);
+    // the data gradient's workgroups read every view of g_src while others
+    // already write dy / dx, and the weight gradient reads them again: an
+    // output overlapping any of them is an inter-workgroup race
     if (x_bn) {
         const Range rdy = view_range(dy, m, d->c_in, d->c_in, es);
         if (overlap(rdy, rx)) return fail(BNR_ERR_ALIAS, "dy overlaps x");
+        if (grad_src_overlaps(d, g, rdy)) return fail(BNR_ERR_ALIAS, "dy overlaps a view g_src reads");
         if (dx && overlap(view_range(dx, m, d->c_in, dx_ldc, es), rx)) return fail(BNR_ERR_ALIAS, "dx overlaps x");
         if (dx && overlap(view_range(dx, m, d->c_in, dx_ldc, es), rdy)) return fail(BNR_ERR_ALIAS, "dx overlaps dy");
+    }
+    if (dx) {
+        const Range rdx = view_range(dx, m, d->c_in, dx_ldc, es);
+        if (grad_src_overlaps(d, g, rdx)) return fail(BNR_ERR_ALIAS, "dx overlaps a view g_src reads");
+        if (!x_bn && overlap(rdx, rx)) return fail(BNR_ERR_ALIAS, "dx overlaps x");
     }
 
     hipStream_t s = (hipStream_t)stream;

@@ -341,8 +341,7 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
             p2[i] = rstd[c];
             p3[i] = mean[c];
         } else if (MODE == EW_BNADDRELU) {
-            p0[i] = gamma[c] * rstd[c];
-            p1[i] = beta[c] - mean[c] * p0[i];
+            bn_coef(gamma[c], beta[c], mean[c], rstd[c], p0[i], p1[i]);
         } else if (MODE == EW_SPLITDX) {
             p0[i] = dgamma[c] * rstd[c];         // betap * rstd
             p1[i] = dbeta[c] - p0[i] * mean[c];  // alpha - betap * rstd * mean
@@ -369,7 +368,7 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
             for (int i = 0; i < VEC; i++) o[i] = f[i] > 0.f ? f[i] : 0.f;
         } else if (MODE == EW_BNADDRELU) {
             for (int i = 0; i < VEC; i++) {
-                const float t = __builtin_fmaf(f[i], p0[i], p1[i]) + g[i];
+                const float t = bn_lin(f[i], p0[i], p1[i]) + g[i];
                 o[i] = t > 0.f ? t : 0.f;
             }
         } else if (MODE == EW_ADDRELU) {

@@ -124,6 +124,19 @@ __device__ __forceinline__ void lds_colsum2(float *red, int rows, int ld, int nc
     }
 }
 
+// sub-BN2 (normalise, scale, shift) as one fused multiply-add per element:
+// y = x c0 + c1 with c0 = gamma rstd and c1 = beta - mean c0.  Every kernel
+// that applies it before a ReLU (CONV prologues, the weight gradient's
+// recompute, max pooling, the head) and every BN-backward epilogue that
+// rebuilds the ReLU mask [y > 0] from x goes through these two helpers, so
+// the forward output, the mask of dx and the recomputed dW operand take the
+// same decision at every pixel, bit for bit.
+__device__ __forceinline__ void bn_coef(float gamma, float beta, float mean, float rstd, float &c0, float &c1) {
+    c0 = gamma * rstd;
+    c1 = __builtin_fmaf(-mean, c0, beta);
+}
+__device__ __forceinline__ float bn_lin(float x, float c0, float c1) { return __builtin_fmaf(x, c0, c1); }
+
 // Deferred input gradient of a BN-fed tensor, formed on load as
 //   d = A dy + B x + C  per channel (dy the loaded gradient, x the BN input).
 // One BN (split = 0):  d = gamma rstd (dy - dbeta/m - xhat dgamma/m), i.e.

@@ -140,7 +140,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     for (int c = tid; c < KP; c += kP1Threads) {
         float c0 = 0.f, c1 = 0.f, c2 = 0.f;
         if (c < K && pro == PRO_BNRELU) {
-            c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
+            bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], c0, c1);
         } else if (c < K && pro == PRO_BNGRAD) {
             deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
                           p.p_alpha, p.p_betap, c0, c1, c2);
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 lds_f8(coef + KP + c, cb);
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) {
-                    const float t = __builtin_fmaf(f[e], ca[e], cb[e]);
+                    const float t = bn_lin(f[e], ca[e], cb[e]);
                     f[e] = t > 0.f ? t : 0.f;
                 }
                 put(j, Elem<T>::pack(f));
@@ -279,10 +279,11 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 
     __syncthreads();
     // this thread's epilogue channels are fixed: keep their BN parameters in registers
-    float eM[VEC], eR[VEC], eG[VEC], eB[VEC];
+    float eM[VEC], eR[VEC], eG[VEC], eB[VEC], eC0[VEC], eC1[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) {
         eM[e] = epi[n + e]; eR[e] = epi[NP + n + e]; eG[e] = epi[2 * NP + n + e]; eB[e] = epi[3 * NP + n + e];
+        bn_coef(eG[e], eB[e], eM[e], eR[e], eC0[e], eC1[e]);     // the forward prologue's y = x c0 + c1
     }
     // work items: F rounds of whole tiles (item k < F is tile k*G + gi, rows
     // [p0, p0 + BM)), then this workgroup's share [lo, hi) of the R rows left
@@ -372,13 +373,12 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) {
                     const float xh = (x[e] - eM[e]) * eR[e];
-                    const float yv = eG[e] * xh + eB[e];
-                    const float d = ok && yv > 0.f ? f[e] : 0.f;
+                    const float d = ok && bn_lin(x[e], eC0[e], eC1[e]) > 0.f ? f[e] : 0.f;
                     s1[e] += d;
                     s2[e] += d * xh;
                     if (EK == EK_BNBWD) f[e] = d;
-                    else if (EK == EK_BNBWD_SC) f[e] = d * (eG[e] * eR[e]);
-                    else f[e] = __builtin_fmaf(d, eG[e] * eR[e], old[e]);
+                    else if (EK == EK_BNBWD_SC) f[e] = d * eC0[e];
+                    else f[e] = __builtin_fmaf(d, eC0[e], old[e]);
                 }
                 vo[j] = Elem<T>::pack(f);
             }

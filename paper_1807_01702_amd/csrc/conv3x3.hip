@@ -264,7 +264,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     for (int c = tid; c < KPC; c += kP3Threads) {
         float c0 = 0.f, c1 = 0.f, c2 = 0.f;
         if (c < K && pro == PRO_BNRELU) {
-            c0 = p.p_gamma[c] * p.p_rstd[c]; c1 = p.p_beta[c] - p.p_mean[c] * c0;
+            bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], c0, c1);
         } else if (c < K && pro == PRO_BNGRAD) {
             deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
                           p.p_alpha, p.p_betap, c0, c1, c2);
@@ -273,7 +273,10 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     }
     for (int c = tid; c < NPC; c += kP3Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
-        if (c < N && EK == EK_BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
+        if (c < N && EK == EK_BNBWD) {      // mean, rstd and the forward's y = x c0 + c1
+            e0 = p.e_mean[c]; e1 = p.e_rstd[c];
+            bn_coef(p.e_gamma[c], p.e_beta[c], e0, e1, e2, e3);
+        }
         if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[c];     // statistics of y - shift
         epi[c] = e0; epi[NPC + c] = e1; epi[2 * NPC + c] = e2; epi[3 * NPC + c] = e3;
     }
@@ -333,7 +336,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 lds_f8(coef + c, ca);
                 lds_f8(coef + KPC + c, cb);
                 #pragma unroll
-                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(__builtin_fmaf(f[e], ca[e], cb[e]), 0.f);
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(bn_lin(f[e], ca[e], cb[e]), 0.f);
                 outv[j] = Elem<T>::pack(f);
                 #pragma unroll
                 for (int i = 0; i < 4; i++) outv[j].u[i] &= keep;
@@ -460,13 +463,13 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         // invalid rows contribute zeros), then the stores back to back ----
         {
             vec16 vo[RPT];
-            float eM[VEC], eR[VEC], eG[VEC], eB[VEC];
+            float eM[VEC], eR[VEC], eC0[VEC], eC1[VEC];
             if (EK == EK_STATS) lds_f8(epi + n, eM);                  // shift
             if (EK == EK_BNBWD) {
                 lds_f8(epi + n, eM);
                 lds_f8(epi + NPC + n, eR);
-                lds_f8(epi + 2 * NPC + n, eG);
-                lds_f8(epi + 3 * NPC + n, eB);
+                lds_f8(epi + 2 * NPC + n, eC0);
+                lds_f8(epi + 3 * NPC + n, eC1);
             }
             #pragma unroll
             for (int j = 0; j < RPT; j++) {
@@ -510,8 +513,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) {
                         const float xh = (x[e] - eM[e]) * eR[e];
-                        const float yv = eG[e] * xh + eB[e];
-                        const float d = ok && yv > 0.f ? f[e] : 0.f;
+                        const float d = ok && bn_lin(x[e], eC0[e], eC1[e]) > 0.f ? f[e] : 0.f;
                         f[e] = d;
                         s1[e] += d;
                         s2[e] += d * xh;

@@ -95,11 +95,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
 
     // per-channel prologue coefficients for all K channels
     if (p.pro == PRO_BNRELU) {
-        for (int c = tid; c < K; c += kThreads) {
-            coef[c] = p.p_mean[c];
-            coef[K + c] = p.p_gamma[c] * p.p_rstd[c];
-            coef[2 * K + c] = p.p_beta[c];
-        }
+        for (int c = tid; c < K; c += kThreads)             // y = x c0 + c1
+            bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], coef[K + c], coef[2 * K + c]);
     } else if (p.pro == PRO_BNGRAD) {
         const float inv_m = 1.0f / (float)m;
         for (int c = tid; c < K; c += kThreads)
@@ -209,7 +206,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                         Elem<T>::unpack(ra[j], f);
                         #pragma unroll
                         for (int e = 0; e < VEC; e++) {
-                            const float t = (f[e] - coef[cc + e]) * coef[K + cc + e] + coef[2 * K + cc + e];
+                            const float t = bn_lin(f[e], coef[K + cc + e], coef[2 * K + cc + e]);
                             f[e] = t > 0.f ? t : 0.f;
                         }
                         out = Elem<T>::pack(f);
@@ -303,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     float f[VEC];
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
                     for (int e = 0; e < VEC; e++) {
-                        float t = (f[e] - coef[c + e]) * coef[K + c + e] + coef[2 * K + c + e];
+                        const float t = bn_lin(f[e], coef[K + c + e], coef[2 * K + c + e]);
                         f[e] = t > 0.f ? t : 0.f;
                     }
                     out = Elem<T>::pack(f);
@@ -381,7 +378,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     if (p.epi == EPI_BNBWD && col_ok)
         for (int e = 0; e < VEC; e++) {
             emu[e] = p.e_mean[n + e]; ers[e] = p.e_rstd[n + e];
-            eg[e] = p.e_gamma[n + e]; eb[e] = p.e_beta[n + e];
+            bn_coef(p.e_gamma[n + e], p.e_beta[n + e], emu[e], ers[e], eg[e], eb[e]);   // the forward's c0, c1
         }
     if (p.epi == EPI_STATS)                       // statistics of y - shift
         for (int e = 0; e < VEC; e++) emu[e] = p.e_shift && col_ok ? p.e_shift[n + e] : 0.f;
@@ -421,12 +418,11 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 if (p.e_scale && p.accumulate) Elem<T>::unpack(ldg16(dst), old);
                 for (int e = 0; e < VEC; e++) {
                     const float xh = (x[e] - emu[e]) * ers[e];
-                    const float yv = eg[e] * xh + eb[e];
-                    const float d = yv > 0.f ? f[e] : 0.f;
+                    const float d = bn_lin(x[e], eg[e], eb[e]) > 0.f ? f[e] : 0.f;
                     s1[e] += d;
                     s2[e] += d * xh;
                     // summed-gradient form: gamma*rstd*dy, stored or added
-                    f[e] = !p.e_scale ? d : (p.accumulate ? __builtin_fmaf(d, eg[e] * ers[e], old[e]) : d * (eg[e] * ers[e]));
+                    f[e] = !p.e_scale ? d : (p.accumulate ? __builtin_fmaf(d, eg[e], old[e]) : d * eg[e]);
                 }
                 stg16(dst, Elem<T>::pack(f));
             }

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
     static_assert(WR * WC == 4, "four waves");
     __shared__ __align__(16) T Zt[kWgCIT * ZSTR];
     __shared__ __align__(16) T Gt[COT * GSTR];
-    __shared__ float zc[3][kWgCIT];
+    __shared__ float zc[2][kWgCIT];
     __shared__ float gc[3][COT];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -130,11 +130,8 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
 
     if (tid < kWgCIT) {
         const int c = ci0 + tid;
-        if (p.a_mode == 1 && c < C_in) {
-            zc[0][tid] = p.a_mean[c];
-            zc[1][tid] = p.a_gamma[c] * p.a_rstd[c];
-            zc[2][tid] = p.a_beta[c];
-        }
+        if (p.a_mode == 1 && c < C_in)          // the forward's y = x c0 + c1
+            bn_coef(p.a_gamma[c], p.a_beta[c], p.a_mean[c], p.a_rstd[c], zc[0][tid], zc[1][tid]);
     }
     if (tid < COT) {
         const int c = co0 + tid;
@@ -224,7 +221,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
                 const bool valid = g.zpix(2 * pr + h2) >= 0 && ci0 + cl < C_in;
                 if (p.a_mode == 1)
                     for (int e = 0; e < VEC; e++) {
-                        const float t = (f[h2][e] - zc[0][cl + e]) * zc[1][cl + e] + zc[2][cl + e];
+                        const float t = bn_lin(f[h2][e], zc[0][cl + e], zc[1][cl + e]);
                         f[h2][e] = valid && t > 0.f ? t : 0.f;
                     }
                 else if (p.a_mode == 2)
@@ -349,8 +346,7 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
     for (int e = 0; e < VEC; e++) {
         za[e] = 1.f; zb[e] = 0.f;
         if (p.a_mode == 1 && zc_ok) {
-            za[e] = p.a_gamma[cz + e] * p.a_rstd[cz + e];
-            zb[e] = p.a_beta[cz + e] - p.a_mean[cz + e] * za[e];
+            bn_coef(p.a_gamma[cz + e], p.a_beta[cz + e], p.a_mean[cz + e], p.a_rstd[cz + e], za[e], zb[e]);
         }
     }
     // deferred-gradient coefficients in LDS (registers are the occupancy limit of the 3x3 variants)
@@ -460,7 +456,7 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
             float f[VEC];
             Elem<T>::unpack(zr[j], f);
             #pragma unroll
-            for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(__builtin_fmaf(f[e], za[e], zb[e]), zlo);
+            for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(bn_lin(f[e], za[e], zb[e]), zlo);
             vec16 out = Elem<T>::pack(f);
             #pragma unroll
             for (int i = 0; i < 4; i++) out.u[i] = valid ? out.u[i] : 0u;

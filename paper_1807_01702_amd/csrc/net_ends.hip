@@ -414,8 +414,7 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
         if (BN && ty < ry) {
             const float g = p.gamma[c0 + i];
             sg[i] = g > 0.f ? 1.f : (g < 0.f ? -1.f : 0.f);
-            k[i] = g * p.rstd[c0 + i];
-            b[i] = p.beta[c0 + i] - p.mean[c0 + i] * k[i];
+            bn_coef(g, p.beta[c0 + i], p.mean[c0 + i], p.rstd[c0 + i], k[i], b[i]);
         }
     }
     const T *x = reinterpret_cast<const T *>(p.x);
@@ -453,7 +452,7 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
             for (int i = 0; i < VEC; i++) {
                 o[i] = bv[i];
                 if (BN) {
-                    const float v = __builtin_fmaf(bv[i], k[i], b[i]);
+                    const float v = bn_lin(bv[i], k[i], b[i]);
                     o[i] = v > 0.f ? v : 0.f;
                 }
             }
@@ -518,8 +517,7 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_bwd(MaxPoolParams p)
             const float g = p.gamma[c];
             mu[i] = p.mean[c];
             rs[i] = p.rstd[c];
-            k[i] = g * rs[i];
-            b[i] = p.beta[c] - mu[i] * k[i];
+            bn_coef(g, p.beta[c], mu[i], rs[i], k[i], b[i]);
         }
     }
     if (BN && tid < C) {
@@ -591,7 +589,7 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_bwd(MaxPoolParams p)
                 float f[VEC];
                 Elem<T>::unpack(ldg16(x + q * p.x_ldc + cv * VEC), f);
                 #pragma unroll
-                for (int i = 0; i < VEC; i++) o[i] = __builtin_fmaf(f[i], k[i], b[i]) > 0.f ? dz[i] : 0.f;
+                for (int i = 0; i < VEC; i++) o[i] = bn_lin(f[i], k[i], b[i]) > 0.f ? dz[i] : 0.f;
                 const vec16 ov = Elem<T>::pack(o);
                 stg16(dy + q * C + cv * VEC, ov);
                 Elem<T>::unpack(ov, o);
@@ -640,8 +638,7 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
     float k[VEC], b[VEC], acc[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) {
-        k[e] = p.gamma[c0 + e] * p.rstd[c0 + e];
-        b[e] = p.beta[c0 + e] - p.mean[c0 + e] * k[e];
+        bn_coef(p.gamma[c0 + e], p.beta[c0 + e], p.mean[c0 + e], p.rstd[c0 + e], k[e], b[e]);
         acc[e] = 0.f;
     }
     const T *x = reinterpret_cast<const T *>(p.x);
@@ -650,7 +647,7 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
         Elem<T>::unpack(ldg16(x + ((int64_t)n * hw + q) * p.x_ldc + c0), f);
         #pragma unroll
         for (int e = 0; e < VEC; e++) {
-            const float v = __builtin_fmaf(f[e], k[e], b[e]);
+            const float v = bn_lin(f[e], k[e], b[e]);
             acc[e] += v > 0.f ? v : 0.f;
         }
     }
@@ -795,8 +792,7 @@ __global__ __launch_bounds__(kThreads) void k_head_bn_bwd(HeadParams p, int64_t 
             const int c = c0 + i;
             mu[i] = p.mean[c];
             rs[i] = p.rstd[c];
-            k[i] = p.gamma[c] * rs[i];
-            b[i] = p.beta[c] - mu[i] * k[i];
+            bn_coef(p.gamma[c], p.beta[c], mu[i], rs[i], k[i], b[i]);
             gk[i] = k[i];
             if (MODE == HB_DX) { da[i] = p.dbeta[c] * inv_m; db[i] = p.dgamma[c] * inv_m; }
         }
@@ -813,7 +809,7 @@ __global__ __launch_bounds__(kThreads) void k_head_bn_bwd(HeadParams p, int64_t 
             #pragma unroll
             for (int i = 0; i < VEC; i++) {
                 const float dz = p.df[n * C + c0 + i] * inv_hw;
-                const float dyv = __builtin_fmaf(f[i], k[i], b[i]) > 0.f ? dz : 0.f;
+                const float dyv = bn_lin(f[i], k[i], b[i]) > 0.f ? dz : 0.f;
                 const float xh = (f[i] - mu[i]) * rs[i];
                 if (MODE == HB_DX) {
                     o[i] = gk[i] * (dyv - da[i] - xh * db[i]);

@@ -14,13 +14,21 @@ enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
 constexpr int kStatsMaxVec = 32;           // 16-byte vectors per row a workgroup covers
 inline int stats_vec(int dtype) { return dtype == DT_BF16 ? 8 : 4; }
 inline int stats_ch_per_block(int dtype) { return kStatsMaxVec * stats_vec(dtype); }
+// Row blocks of a sweep over m rows: the launched grid.  A block covers
+// ceil(m / target) rows, so the grid is ceil(m / rows-per-block), which can be
+// smaller than the target (m = 62720, target 512: 123 rows per block, 510
+// blocks).  Workspace sizing, the sweep launch and the combine all use this
+// count, so the combine never reads a partial row the sweep did not write.
 inline int64_t stats_row_blocks(int64_t m, int c, int dtype) {
     int64_t cb = (c + stats_ch_per_block(dtype) - 1) / stats_ch_per_block(dtype);
     int64_t target = 512 / cb;             // about two workgroups per CU
     if (target < 1) target = 1;
     int64_t minrows = 64;
     int64_t rb = (m + minrows - 1) / minrows;
-    return rb < target ? rb : target;
+    const int64_t want = rb < target ? rb : target;
+    if (m <= 0) return want;
+    const int64_t rpb = (m + want - 1) / want;
+    return (m + rpb - 1) / rpb;
 }
 
 // ---- implicit-GEMM CONV over pixel rows (forward and data gradient) -------

@@ -171,3 +171,23 @@ def test_network_end_entry_points_validate(B):
     a = B.BnReluRefArgs()
     assert B.STATUS[f["bnr_reference_bn_relu"](0, 100, 16, B.BNR_BF16, ctypes.byref(a), WS, 1 << 30, None)] \
         == "BNR_ERR_SHAPE"                                         # x_ldc 0
+
+
+def test_bwd_fused_rejects_outputs_over_gradient_source(B):
+    """dy / dx may not overlap any view the gradient source reads (the data
+    gradient's workgroups read it while others already write the outputs)."""
+    d = _desc(B)                                    # m = 32, c_in 16, c_out 8, bf16
+    bn = B.BNStruct(A, A, A, A, A, 1e-5)
+    f = B._lib_fns["bnr_bwd_fused"]
+    x, w, g = A, A + 0x1000, A + 0x4000
+    dense = B.GradSrc(B.GRAD_DENSE, g, 8, None, None, 0, None, None, None)
+    def st(gs, dy, dx, xbn=True):
+        return B.STATUS[f(ctypes.byref(d), x, ctypes.byref(bn) if xbn else None, w, ctypes.byref(gs), A + 0x8000,
+                          A + 0x9000, A + 0x9100, dy, dx, 16 if dx else 0, 0, WS, 1 << 30, None)]
+    assert st(dense, g + 0x10, None) == "BNR_ERR_ALIAS"          # dy over the dense gradient
+    assert st(dense, A + 0x10000, g + 0x20) == "BNR_ERR_ALIAS"   # dx over the dense gradient
+    assert st(dense, None, g, xbn=False) == "BNR_ERR_ALIAS"      # no BN: dx over the gradient
+    assert st(dense, None, x + 0x10, xbn=False) == "BNR_ERR_ALIAS"   # no BN: dx over x
+    gb = B.GradSrc(B.GRAD_BN, None, 0, A + 0x20000, A + 0x30000, 8, ctypes.pointer(bn), A, A, None, None)
+    assert st(gb, A + 0x20000, None) == "BNR_ERR_ALIAS"          # dy over the deferred gradient's dy
+    assert st(gb, A + 0x10000, A + 0x30010) == "BNR_ERR_ALIAS"   # dx over the deferred gradient's x

@@ -51,6 +51,66 @@ def test_bn_stats(B, m, c, ldc, bf16, shift):
     np.testing.assert_allclose(host(bn.rstd), rstd_r, rtol=RTOL[bf16])
 
 
+def _poison_workspace(B, nbytes, device):
+    """Grow the binding's workspace to nbytes and fill it with 0xFF bytes
+    (NaN as float32): a combine that read a partial row its sweep did not
+    write would return NaN."""
+    B.workspace(nbytes, device)
+    B._ws_cache[(torch.device(device), 0)].fill_(255)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_stats_rows_launched_equal_rows_combined(B, bf16):
+    """m = 20*56*56 = 62720 pixels of 64 channels: 123 rows per block give 510
+    launched row blocks, fewer than the 512 the sizing rule aims at.  The
+    standalone sweep and the unfused path's two-pass sweeps and backward sums
+    must combine exactly the launched rows (workspace poisoned with NaN)."""
+    n, h, w, c, co = 20, 56, 56, 64, 32
+    m = n * h * w
+    xf = synth.normal(7, "stats_rows", (n, h, w, c), bf16=bf16)
+    x = dev(xf, bf16)
+    bn = B.BN.stats_only(c, x.device)
+    _poison_workspace(B, B.bnr_stats_workspace_size(m, c), x.device)
+    B.bnr_bn_stats(x, bn)
+    torch.cuda.synchronize()
+    x64 = xf.reshape(m, c).astype(np.float64)
+    mean_r, var_r, _ = P.bn_stats(x64, 1e-5)
+    assert_stats("stats", host(bn.mean), host(bn.var), mean_r, var_r, RTOL[bf16])
+    if bf16:
+        return
+    # unfused chain (fp32): two-pass statistics, then the backward reductions
+    wt = synth.conv_weight(7, "w", 1, c, co, False)
+    bp = synth.bn_params(7, "bn", c)
+    gf = synth.normal(7, "g", (n, h, w, co), bf16=False)
+    out = torch.empty((n, h, w, co), dtype=torch.float32, device=x.device)
+    desc = B.desc_for(x, out, 1, n, h, w)
+    rbn = _bn_dev(bp["gamma"], bp["beta"])
+    y, z = torch.empty_like(x), torch.empty_like(x)
+    wd = dev(wt, False)
+    _poison_workspace(B, B.bnr_workspace_size(desc), x.device)
+    B.bnr_reference_path(B.MODE_BASELINE, False, desc, x, rbn, wd, y, z=z, out=out)
+    dz, dy, dx = torch.empty_like(x), torch.empty_like(x), torch.empty_like(x)
+    dw = torch.empty(tuple(wt.shape), dtype=torch.float32, device=x.device)
+    dg = torch.empty(c, dtype=torch.float32, device=x.device)
+    db = torch.empty_like(dg)
+    _poison_workspace(B, B.bnr_workspace_size(desc), x.device)
+    B.bnr_reference_path(B.MODE_BASELINE, True, desc, x, rbn, wd, y, z=z, g=dev(gf, False), dz=dz, dy=dy, dw=dw,
+                         dgamma=dg, dbeta=db, dx=dx)
+    torch.cuda.synchronize()
+    yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    assert_stats("two-pass stats", host(rbn.mean), host(rbn.var), mu, var, 1e-4)
+    dzr = P.conv_dgrad(gf.astype(np.float64), wt.astype(np.float64), (h, w)).reshape(m, c)
+    dyr = P.relu_bwd(dzr, yr)
+    dxr, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd)
+    xh = (x64 - mu) * rstd
+    amb = relu_ambiguous(yr, False)
+    scale_b = np.abs(dyr).sum(axis=0)
+    scale_g = np.abs(dyr * xh).sum(axis=0)
+    assert np.all(np.abs(host(db) - dbr) <= 1e-4 * scale_b), "dbeta"
+    assert np.all(np.abs(host(dg) - dgr) <= 1e-4 * scale_g), "dgamma"
+    assert_close("dx", host(dx).reshape(m, c), dxr, 1e-4, exclude=amb)
+
+
 # --------------------------------------------------------- fused forward ----
 FWD_CASES = [
     # dtype, k, n, h, w, c_in, c_out, in_ldc, out_ldc

@@ -66,6 +66,40 @@ MUTANTS = [
      'dy5 = P.relu_bwd(dz5, hd["x"])'),
     ("stem weight gradient with the wrong padding", "compose.py",
      'd["stem"]["w"].shape[0], stride=2, pad=3)', 'd["stem"]["w"].shape[0], stride=2, pad=2)'),
+    # the bf16 storage model's backward rounding sites (each dropped) and its
+    # fp32 results (one rounded)
+    ("bf16: masked BN output gradient dy not stored in bf16", "compose.py",
+     'dy = rnd(P.relu_bwd(dz, c["y"]))', 'dy = P.relu_bwd(dz, c["y"])'),
+    ("bf16: deferred dx of the 3x3 CONV's BN not rounded for the 1x1 backward", "compose.py",
+     'b1 = unit_bwd(c["u1"], rnd(b2["dx"]), rnd)', 'b1 = unit_bwd(c["u1"], b2["dx"], rnd)'),
+    ("bf16: Split accumulation into G not rounded", "compose.py",
+     'G[..., :c_l] = rnd(G[..., :c_l] + b1["dx"])', 'G[..., :c_l] = G[..., :c_l] + b1["dx"]'),
+    ("bf16: bottleneck upstream gradient not rounded", "compose.py",
+     'G = rnd(np.array(dY, dtype=np.float64, copy=True))', 'G = np.array(dY, dtype=np.float64, copy=True)'),
+    ("bf16: transition unpooled gradient not rounded", "compose.py",
+     'gt = rnd(P.avgpool2_bwd(dpool, ut["x"].shape[1:3]))', 'gt = P.avgpool2_bwd(dpool, ut["x"].shape[1:3])'),
+    ("bf16: block gradient G from the transition not rounded", "compose.py",
+     'G = rnd(bt["dx"])', 'G = np.array(bt["dx"])'),
+    ("bf16: residual masked gradient ds not rounded", "compose.py",
+     'ds = rnd(P.relu_bwd(dr, c["s"]))', 'ds = P.relu_bwd(dr, c["s"])'),
+    ("bf16: BN3 input gradient not rounded for the third CONV's backward", "compose.py",
+     'b3 = unit_bwd(c["u3"], rnd(dx3), rnd)', 'b3 = unit_bwd(c["u3"], dx3, rnd)'),
+    ("bf16: BN2 input gradient not rounded for the second CONV's backward", "compose.py",
+     'b2 = unit_bwd(c["u2"], rnd(b3["dx"]), rnd)', 'b2 = unit_bwd(c["u2"], b3["dx"], rnd)'),
+    ("bf16: BN1 input gradient not rounded for the first CONV's backward", "compose.py",
+     'g1 = rnd(b2["dx"])', 'g1 = b2["dx"]'),
+    ("bf16: residual block input gradient not rounded", "compose.py",
+     'dX = rnd(ds + P.conv_dgrad(g1', 'dX = (ds + P.conv_dgrad(g1'),
+    ("bf16: head BN input gradient not rounded", "compose.py", 'G = rnd(dx5)', 'G = np.array(dx5)'),
+    ("bf16: stem masked gradient not rounded", "compose.py",
+     'dy0 = rnd(P.relu_bwd(dz0, st["y"]))', 'dy0 = P.relu_bwd(dz0, st["y"])'),
+    ("bf16: stem BN input gradient not rounded for the stem weight gradient", "compose.py",
+     'g0 = rnd(dx0)', 'g0 = np.array(dx0)'),
+    ("bf16: weight gradient rounded to bf16", "compose.py",
+     'dw = P.conv_wgrad(c["z"], g, K)', 'dw = rnd(P.conv_wgrad(c["z"], g, K))'),
+    ("bf16: BN reductions rounded to bf16", "compose.py",
+     'dx, dgamma, dbeta = P.bn_bwd(c["x"], dy, c["gamma"], c["mean"], c["rstd"])',
+     'dx, dgamma, dbeta = P.bn_bwd(c["x"], dy, c["gamma"], c["mean"], c["rstd"]); dgamma = rnd(dgamma)'),
 ]
 
 

@@ -455,6 +455,104 @@ def test_bf16_storage_model_rounds_stored_tensors():
         np.testing.assert_array_equal(P.round_bf16(c[key]), c[key])
 
 
+def _is_bf16(a):
+    a = np.asarray(a, np.float64)
+    return np.array_equal(P.round_bf16(a), a)
+
+
+def _bf16_backward_runs():
+    """Every bf16 composition's backward, fed upstream gradients that are NOT
+    bf16-representable (fp64 normal draws), so that every rounding site in the
+    backward has something to round.  Returns [(name, stored, fp32_results)]:
+    the tensors the storage model stores in bf16 and those it keeps in fp32."""
+    rnd = OC.storage(True)
+    r = lambda a: P.round_bf16(a)
+    runs = []
+    # bottleneck: dY -> G (initial value), the 3x3 unit's dy, the deferred
+    # dx2 handed to the 1x1 unit, its dy, the Split accumulation into G
+    X = r(RNG.standard_normal((2, 4, 4, 4)))
+    pb = dict(gamma1=RNG.uniform(0.5, 1.5, 4), beta1=RNG.normal(0, .1, 4), w1=r(RNG.standard_normal((1, 1, 4, 5))),
+              gamma2=RNG.uniform(0.5, 1.5, 5), beta2=RNG.normal(0, .1, 5), w2=r(RNG.standard_normal((3, 3, 5, 2))))
+    _, c = OC.bottleneck_fwd(X, 2, pb, 1e-5, rnd)
+    dX, g = OC.bottleneck_bwd(c, RNG.standard_normal((2, 4, 4, 6)), rnd)
+    runs.append(("bottleneck", [dX, g["b2"]["g"], g["b2"]["dy"], g["b1"]["g"], g["b1"]["dy"]],
+                 [g[b][k] for b in ("b1", "b2") for k in ("dw", "dgamma", "dbeta")]))
+    # dense block + transition: the transition's unpooled gradient, G after the
+    # transition's BN input gradient and after every reader's addition
+    X0, cpls, trans, ct = _tiny_block()
+    X0 = r(X0)
+    for q in cpls:
+        q["w1"], q["w2"] = r(q["w1"]), r(q["w2"])
+    trans = dict(trans, w=r(trans["w"]))
+    _, c = OC.block_fwd(X0, cpls, trans, 1e-5, rnd, ct)
+    dX0, g = OC.block_bwd(c, RNG.standard_normal((2, 2, 2, 3)), rnd)
+    stored = [dX0, g["G"], g["trans"]["g"], g["trans"]["dy"]]
+    for q in g["cpls"]:
+        stored += [q["b1"]["g"], q["b1"]["dy"], q["b2"]["g"], q["b2"]["dy"]]
+    runs.append(("block", stored, [g["trans"]["dw"], g["trans"]["dgamma"], g["cpls"][0]["b1"]["dw"],
+                                   g["cpls"][1]["b2"]["dbeta"]]))
+    # ResNet block: ds, the deferred BN3 gradient, BN2's, BN1's, dX
+    C, Wd = 4, 3
+    pr = dict(w1=r(RNG.standard_normal((1, 1, C, Wd))), w2=r(RNG.standard_normal((3, 3, Wd, Wd))),
+              w3=r(RNG.standard_normal((1, 1, Wd, C))))
+    for i, ch in ((1, Wd), (2, Wd), (3, C)):
+        pr["gamma%d" % i], pr["beta%d" % i] = RNG.uniform(0.5, 1.5, ch), RNG.normal(0, .1, ch)
+    _, c = OC.resnet_block_fwd(r(RNG.standard_normal((2, 3, 3, C))), pr, 1e-5, rnd)
+    dX, g = OC.resnet_block_bwd(c, RNG.standard_normal((2, 3, 3, C)), rnd)
+    runs.append(("resnet", [dX, g["ds"], g["b3"]["g"], g["b3"]["dy"], g["b2"]["g"], g["b2"]["dy"], g["g1"]],
+                 [g["dw1"], g["dgamma3"], g["dbeta3"], g["b2"]["dw"], g["b3"]["dgamma"]]))
+    # whole DenseNet: the head BN's input gradient G, the stem BN's dy and input gradient
+    from paper_1807_01702_amd import synth
+    d = _f64_tree(synth.densenet(seed=5, n=2, hw=16, c_img=3, c_stem=4, growth=2, width=4, blocks=(2, 1),
+                                 classes=5, bf16=True))
+    _, c = OC.densenet_fwd(d, d["eps"], rnd)
+    g = OC.densenet_bwd(c, rnd)
+    runs.append(("densenet", [g["blocks"][-1]["G"], g["stem"]["dy"], g["stem"]["g"], g["stem"]["dX"]],
+                 [g["stem"]["dw"], g["stem"]["dgamma"], g["head"]["dw"], g["head"]["dgamma"]]))
+    return runs
+
+
+def test_bf16_storage_model_backward_rounding_sites():
+    """The bf16 compositions store every backward tensor that the GPU path
+    stores (dy, the deferred BN input gradient a CONV's backward consumes,
+    the concatenation gradient, dX) in bf16, and keep dW, dgamma, dbeta in
+    fp32 (here fp64: not bf16-rounded)."""
+    for name, stored, wide in _bf16_backward_runs():
+        for i, t in enumerate(stored):
+            assert np.any(t != 0), (name, i)
+            assert _is_bf16(t), "%s: stored backward tensor %d is not bf16" % (name, i)
+        for i, t in enumerate(wide):
+            assert not _is_bf16(t), "%s: fp32 result %d was rounded to bf16" % (name, i)
+
+
+def test_bf16_storage_model_backward_is_a_rounding_of_fp64():
+    """With identical bf16 inputs and ReLU decisions that keep a margin, the
+    bf16 model's backward differs from the exact composition only by the
+    storage roundings: a few bf16 half-ulps (2^-9) per stored tensor, well
+    under 2e-2 relative, and not zero (the roundings happen)."""
+    r = lambda a: P.round_bf16(a)
+    for seed in range(200):
+        rng = np.random.default_rng(100 + seed)
+        X = r(rng.standard_normal((2, 4, 4, 4)))
+        p = dict(gamma1=rng.uniform(0.5, 1.5, 4), beta1=rng.normal(0, .1, 4), w1=r(rng.standard_normal((1, 1, 4, 5))),
+                 gamma2=rng.uniform(0.5, 1.5, 5), beta2=rng.normal(0, .1, 5), w2=r(rng.standard_normal((3, 3, 5, 2))))
+        dY = r(rng.standard_normal((2, 4, 4, 6)))
+        _, ce = OC.bottleneck_fwd(X, 2, p, 1e-5, OC.storage(False))
+        _, cb = OC.bottleneck_fwd(X, 2, p, 1e-5, OC.storage(True))
+        # the first BN sees identical inputs and statistics on both sides; the
+        # second one's input differs by the rounding of the first CONV's output
+        if min(float(np.min(np.abs(y))) for y in (ce["u2"]["y"], cb["u2"]["y"])) < 0.01:
+            continue                       # a ReLU decision near 0: the two need not agree
+        dXe, ge = OC.bottleneck_bwd(ce, dY, OC.storage(False))
+        dXb, gb = OC.bottleneck_bwd(cb, dY, OC.storage(True))
+        for name, a, b in (("dX", dXb, dXe), ("dy2", gb["b2"]["dy"], ge["b2"]["dy"]),
+                           ("dy1", gb["b1"]["dy"], ge["b1"]["dy"]), ("dW1", gb["b1"]["dw"], ge["b1"]["dw"])):
+            e = np.max(np.abs(a - b)) / np.max(np.abs(b))
+            assert 0 < e < 0.02, (seed, name, e)
+        return
+    pytest.fail("no seed with a ReLU margin")
+
+
 # ------------------------------------------------- classifier head (C5) ----
 def test_softmax_ce_uniform_logits_closed_form():
     # equal logits: every class has probability 1/K, the loss is ln K and the
