@@ -37,10 +37,14 @@
  *   bnr_last_error() then describes the problem (thread-local string).
  * - Workspace: device memory the caller provides for per-tile partial sums and
  *   staging; query its size with the matching bnr_*_workspace_size call.  The
- *   library allocates no device memory.  Workspace contents need no
- *   initialisation and are dead after the call's kernels complete.
+ *   library allocates no device memory of its own, with one exception: the
+ *   fixed static scratch array of bnr_bn_relu_conv_fwd_static (one per GPU,
+ *   held until the process ends).  Workspace contents need no initialisation
+ *   and are dead after the call's kernels complete.
  * - Outputs must not alias inputs unless an entry point says otherwise.
- *   Calls are stateless and thread-safe.
+ *   Calls keep no state between them and are thread-safe, except for the
+ *   process-wide launch-timing switch of bnr_trace_begin / bnr_trace_end
+ *   (a diagnostic) and the static scratch array named above.
  */
 #ifndef BNR_H
 #define BNR_H
@@ -171,6 +175,25 @@ bnr_status bnr_conv_bn_stats_fwd(const bnr_conv_desc *d, const void *x, const vo
 bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn,
                                 const void *w, void *y, bnr_bn *y_bn,
                                 void *ws, size_t ws_bytes, void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * bnr_bn_relu_conv_fwd with the same arguments and results, but no workspace
+ * argument.  Its workspace is a static __device__ array of 16 MiB per GPU
+ * (allocated with the library's code object, held until the process ends);
+ * the call itself allocates nothing and creates no HIP events.
+ *   Limit: a CONV whose forward workspace (packed weights, statistics partial
+ *   rows, combine stage) exceeds 16 MiB returns BNR_ERR_WORKSPACE before any
+ *   launch.  Every layer of the dense block, the ResNet stack and DenseNet-121
+ *   at the shapes of this library's workloads fits.
+ *   Calls on one GPU share that GPU's array and leave their partial sums in
+ *   it: two calls whose kernels overlap in time on one GPU (different
+ *   streams, different host threads) race; serialise them on one stream.
+ *   No part of the array needs to start at zero.
+ *   The first call on each GPU looks up the array's device address on that
+ *   GPU (hipGetSymbolAddress) with the GPU current. */
+bnr_status bnr_bn_relu_conv_fwd_static(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn,
+                                       const void *w, void *y, bnr_bn *y_bn, void *stream);
 
 /* 2x2 average pooling, stride 2, of x[n][h][w][c] (pixel stride ldc) into the
  * view y[n][h/2][w/2][c] (pixel stride y_ldc, e.g. the first channels of the

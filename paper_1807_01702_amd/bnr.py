@@ -87,6 +87,8 @@ _lib_fns = dict(
                                c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_fwd=_sig("bnr_bn_relu_conv_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, c_vp,
                               _P(BNStruct), c_vp, c_sz, c_vp),
+    bnr_bn_relu_conv_fwd_static=_sig("bnr_bn_relu_conv_fwd_static", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct),
+                                     c_vp, c_vp, _P(BNStruct), c_vp),
     bnr_avgpool2_fwd=_sig("bnr_avgpool2_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
                           c_vp, c_i32, c_vp),
     bnr_avgpool2_bwd=_sig("bnr_avgpool2_bwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
@@ -298,6 +300,14 @@ def bnr_bn_relu_conv_fwd(desc, x, x_bn, w, y, y_bn=None):
     ys = y_bn.struct() if y_bn is not None else None
     _check(_lib_fns["bnr_bn_relu_conv_fwd"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), _ptr(y),
                                             ctypes.byref(ys) if ys is not None else None, ws, wsb, _stream()))
+
+
+def bnr_bn_relu_conv_fwd_static(desc, x, x_bn, w, y, y_bn=None):
+    """bnr_bn_relu_conv_fwd on the library's static per-GPU scratch (no workspace, no allocation)."""
+    xs = x_bn.struct()
+    ys = y_bn.struct() if y_bn is not None else None
+    _check(_lib_fns["bnr_bn_relu_conv_fwd_static"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), _ptr(y),
+                                                   ctypes.byref(ys) if ys is not None else None, _stream()))
 
 
 def bnr_avgpool2_fwd(x, y, n, h, w):

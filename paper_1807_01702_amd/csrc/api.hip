@@ -6,6 +6,7 @@
 // on any error it returns without launching anything.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -13,6 +14,7 @@
 #include "../../include/bnr.h"
 #include "kernels.hpp"
 #include "tiles.hpp"
+#include "trace.hpp"
 
 using namespace bnr;
 
@@ -144,7 +146,7 @@ int64_t pixels(const bnr_conv_desc *d) { return (int64_t)d->n * d->h * d->w; }
 // workspace regions for the conv entry points:
 //   pack  | packed weights (forward or data-gradient layout)
 //   part  | per-tile statistics partial sums [tiles][2][C]
-//   red   | statistics combine scratch (ticket counters + float64 level 1)
+//   red   | statistics combine scratch (float64 level 1)
 //   wg    | weight-gradient split partial tiles
 //   wgred | split-K sum scratch
 struct ConvWs { size_t pack, part, red, wg, wgred, total; };
@@ -291,9 +293,14 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
     return BNR_OK;
 }
 
+// workspace bytes a forward CONV touches: the first three regions (packed
+// weights, statistics partial rows, combine stage)
+size_t conv_fwd_ws(const ConvWs &w) { return w.pack + w.part + w.red; }
+
 // forward CONV with optional BN+ReLU prologue and optional statistics epilogue
+// (need: the workspace bytes checked; 0 = the whole conv workspace)
 bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w, void *y,
-                    bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream)
+                    bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream, size_t need = 0)
 {
     TRY(check_desc(d));
     TRY(check_ptr(x, "x"));
@@ -302,7 +309,7 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     if (x_bn) TRY(check_bn(x_bn, "x_bn", true, false));
     if (y_bn) TRY(check_bn(y_bn, "y_bn", false, true));
     const ConvWs cw = conv_ws(d);
-    TRY(check_ws(ws, ws_bytes, cw.total));
+    TRY(check_ws(ws, ws_bytes, need ? need : cw.total));
     const int es = esize(d->dtype);
     const int64_t m = pixels(d);
     Range ry = view_range(y, m, d->c_out, d->out_ldc, es);
@@ -333,6 +340,41 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
                 "stats combine");
     }
     return ok();
+}
+
+}  // namespace
+
+// ---- scratch of the entry point that allocates nothing ----
+// bnr_bn_relu_conv_fwd_static keeps its forward workspace (packed weights,
+// statistics partial rows, the combine's float64 stage) in this array: one
+// copy per GPU, alive until the process ends.  Host code never uses the
+// array's name as an address (on the host it is a stand-in symbol, not
+// device memory): the device address comes from hipGetSymbolAddress, taken
+// once per device with that device current.
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch_ptr[kMaxDevices];
+
+// device address of `scratch` on the current device (looked up on the first
+// call on that device; concurrent first calls look up the same address)
+bnr_status static_scratch(void **out)
+{
+    int dev = -1;
+    TRY_HIP(hipGetDevice(&dev), "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(BNR_ERR_UNSUPPORTED, "device ordinal %d >= %d", dev, kMaxDevices);
+    void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        TRY_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+        if (!p) return fail(BNR_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+        if (reinterpret_cast<uintptr_t>(p) % kAlign) return fail(BNR_ERR_HIP, "scratch is not 256-byte aligned");
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return BNR_OK;
 }
 
 }  // namespace
@@ -394,6 +436,21 @@ bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr
 {
     if (!x_bn) return fail(BNR_ERR_NULL, "x_bn is NULL");
     return conv_fwd(d, x, x_bn, w, y, y_bn, ws, ws_bytes, stream);
+}
+
+bnr_status bnr_bn_relu_conv_fwd_static(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                                       void *y, bnr_bn *y_bn, void *stream)
+{
+    if (!x_bn) return fail(BNR_ERR_NULL, "x_bn is NULL");
+    TRY(check_desc(d));
+    const size_t need = conv_fwd_ws(conv_ws(d));
+    if (need > kStaticScratchBytes)
+        return fail(BNR_ERR_WORKSPACE, "this CONV needs %zu bytes of scratch, more than the %zu of the static array",
+                    need, kStaticScratchBytes);
+    void *ptr = nullptr;
+    TRY(static_scratch(&ptr));
+    TraceSuppress no_events;              // launch timing would create HIP events
+    return conv_fwd(d, x, x_bn, w, y, y_bn, ptr, kStaticScratchBytes, stream, need);
 }
 
 bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *x, int32_t ldc,

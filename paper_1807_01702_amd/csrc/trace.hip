@@ -1,4 +1,5 @@
 // trace.hip -- state of the launch-timing diagnostics (bnr_trace_begin/end).
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -8,16 +9,22 @@
 namespace bnr {
 namespace {
 struct Rec { hipEvent_t a, b; double bytes, flops; int kid; };
-std::mutex g_mu;
-int g_classes = 0;
+std::mutex g_mu;                       // guards g_cap and g_recs
+std::atomic<int> g_classes{0};         // selected classes; 0 = tracing off
 size_t g_cap = 0;
 std::vector<Rec> g_recs;
+thread_local int g_suppress = 0;
 }  // namespace
 
+TraceSuppress::TraceSuppress() { g_suppress++; }
+TraceSuppress::~TraceSuppress() { g_suppress--; }
+
+// Tracing off (the normal case) costs one relaxed load per launch, no lock.
 bool trace_wants(int kernel_class)
 {
+    if (g_suppress || (g_classes.load(std::memory_order_relaxed) & kernel_class) == 0) return false;
     std::lock_guard<std::mutex> lk(g_mu);
-    return (g_classes & kernel_class) != 0 && g_recs.size() < g_cap;
+    return (g_classes.load(std::memory_order_relaxed) & kernel_class) != 0 && g_recs.size() < g_cap;
 }
 
 void trace_record(hipEvent_t a, hipEvent_t b, double bytes, double flops, int kid)
@@ -38,7 +45,7 @@ bnr_status bnr_trace_begin(int32_t kernel_classes, int32_t capacity)
     bnr::g_recs.clear();
     bnr::g_recs.reserve((size_t)capacity);
     bnr::g_cap = (size_t)capacity;
-    bnr::g_classes = kernel_classes;
+    bnr::g_classes.store(kernel_classes, std::memory_order_relaxed);
     return BNR_OK;
 }
 
@@ -48,7 +55,7 @@ int32_t bnr_trace_end(double *ms, double *bytes, double *flops, int32_t *kernel_
     {
         std::lock_guard<std::mutex> lk(bnr::g_mu);
         recs.swap(bnr::g_recs);
-        bnr::g_classes = 0;
+        bnr::g_classes.store(0, std::memory_order_relaxed);
         bnr::g_cap = 0;
     }
     int32_t n = 0;

@@ -18,6 +18,13 @@ enum KernelId {
 bool trace_wants(int kernel_class);
 void trace_record(hipEvent_t a, hipEvent_t b, double bytes, double flops, int kid);
 
+// While one of these lives on a thread, that thread's launches are not traced
+// (no events are created): the entry point that allocates nothing uses it.
+struct TraceSuppress {
+    TraceSuppress();
+    ~TraceSuppress();
+};
+
 // RAII bracket around one launch (no-op unless tracing selects its class)
 class TraceScope {
   public:

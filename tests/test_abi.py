@@ -191,3 +191,31 @@ def test_bwd_fused_rejects_outputs_over_gradient_source(B):
     gb = B.GradSrc(B.GRAD_BN, None, 0, A + 0x20000, A + 0x30000, 8, ctypes.pointer(bn), A, A, None, None)
     assert st(gb, A + 0x20000, None) == "BNR_ERR_ALIAS"          # dy over the deferred gradient's dy
     assert st(gb, A + 0x10000, A + 0x30010) == "BNR_ERR_ALIAS"   # dx over the deferred gradient's x
+
+
+def test_static_scratch_entry_point_limit(B):
+    """bnr_bn_relu_conv_fwd_static takes every forward CONV of the workloads
+    (dense block and bottleneck, ResNet-50 conv2_x, DenseNet-121 at N = 128)
+    and refuses one whose forward workspace exceeds its 16 MiB array, before
+    any launch.  y is NULL, so no call here can launch: a shape that fits
+    stops at the NULL check (or, without a GPU, at the device lookup)."""
+    f = B._lib_fns["bnr_bn_relu_conv_fwd_static"]
+    bn = B.BNStruct(A, A, A, A, A, 1e-5)
+    ybn = B.BNStruct(None, None, A, A, A, 1e-5)
+
+    def status(n, h, w, ci, co, k, dtype=B.BNR_BF16):
+        d = B.ConvDesc(n, h, w, ci, co, k, ci, co, dtype)
+        return B.STATUS[f(ctypes.byref(d), A, ctypes.byref(bn), A + 0x1000, None, ctypes.byref(ybn), None)]
+
+    shapes = [(32, 56, 56, 256, 128, 1), (32, 56, 56, 128, 32, 3), (64, 56, 56, 256, 128, 1),
+              (128, 56, 56, 256, 64, 1), (128, 56, 56, 64, 64, 3), (128, 56, 56, 64, 256, 1)]
+    shapes += [(64, 56, 56, 64 + 32 * l, 128, 1) for l in range(6)]
+    for hw, c0, layers in ((56, 64, 6), (28, 128, 12), (14, 256, 24), (7, 512, 16)):
+        shapes += [(128, hw, hw, c0 + 32 * l, 128, 1) for l in range(layers)] + [(128, hw, hw, 128, 32, 3)]
+        shapes.append((128, hw, hw, c0 + 32 * layers, (c0 + 32 * layers) // 2, 1))       # transition
+    for s in shapes:
+        assert status(*s) in ("BNR_ERR_NULL", "BNR_ERR_HIP"), s
+    assert status(8, 8, 8, 64, 32, 1, B.BNR_F32) in ("BNR_ERR_NULL", "BNR_ERR_HIP")
+    assert status(256, 64, 64, 256, 256, 1, B.BNR_F32) == "BNR_ERR_WORKSPACE"
+    d = _desc(B)
+    assert B.STATUS[f(ctypes.byref(d), A, None, A + 0x1000, A + 0x2000, None, None)] == "BNR_ERR_NULL"   # x_bn
