@@ -242,6 +242,10 @@ class _DenseStage:
             self.dz_flat = torch.empty(n * h * w * max(ct, width), dtype=dt, device=dev)
             self.dx2 = torch.empty_like(self.dy2)
         self.fused = fused
+        # called as layer_hook(i) after composite layer i's backward calls have
+        # been issued (i = 0 .. len(cpls)-1, in backward order), e.g. to take
+        # that layer's dy2 before the next layer reuses the buffer
+        self.layer_hook = None
         self.icf = bool(icf)
         if self.icf and not fused:
             raise ValueError("inter-composite-layer fusion needs the fused path")
@@ -327,7 +331,7 @@ class _DenseStage:
             if ut is not None:
                 B.bnr_bwd_fused_split(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(dpool), ut.dw, ut.g.dgamma,
                                       ut.g.dbeta, self.G, self.alpha, self.betap)
-            for (c_l, k, u1, u2), st in zip(reversed(self.cpl), reversed(self.slice_stats)):
+            for i, ((c_l, k, u1, u2), st) in reversed(list(enumerate(zip(self.cpl, self.slice_stats)))):
                 sl = slice(c_l, c_l + k)
                 B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt,
                                 B.grad_split(self.G[..., sl], self.X[..., sl], st, self.alpha[sl], self.betap[sl]),
@@ -336,6 +340,8 @@ class _DenseStage:
                                       B.grad_bn(self.dy2, u2.x, u2.bn, u2.g.dgamma, u2.g.dbeta),
                                       u1.dw, u1.g.dgamma, u1.g.dbeta, self.G[..., :c_l], self.alpha[:c_l],
                                       self.betap[:c_l], accumulate=True)
+                if self.layer_hook is not None:
+                    self.layer_hook(i)
             B.bnr_split_dx(self.G[..., :c0], self.X[..., :c0], self.in_stats, self.alpha[:c0], self.betap[:c0],
                            self.G[..., :c0])
         elif self.fused:

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from helpers import RTOL, assert_close, assert_stats, dev, f32dev, host, relu_ambiguous
+from helpers import RTOL, assert_close, assert_stats, dev, f32dev, host, rel_err, relu_ambiguous
 from oracle import prims as P
 from paper_1807_01702_amd import synth
 
@@ -272,6 +272,61 @@ def test_bwd_fused_deferred_bn_gradient(B, case):
     assert_close("dbeta", host(dbeta), dbr, rt)
 
 
+@pytest.mark.parametrize("case", [
+    # bf16, k, n, h, w, c_in (BN input), c_out (= the slice), ldc of the concatenation buffer, slice offset
+    (True, 3, 2, 10, 12, 128, 32, 64, 32),     # the dense block's 3x3 CONV backward (persistent kernels)
+    (True, 3, 1, 6, 56, 128, 32, 256, 224),    # full-width rows, last slice of a 256-channel buffer
+    (True, 1, 2, 7, 9, 64, 128, 160, 32),      # 1x1
+    (False, 3, 2, 5, 6, 16, 24, 40, 8),        # fp32 (tiled kernels)
+])
+def test_bwd_fused_summed_gradient_with_bn(B, case):
+    """Gradient source = the summed input gradient of a concatenation slice
+    (D + alpha + betap * xhat, formed on load) together with the BN-backward
+    epilogue of the CONV's own input BN: the combination the dense block's
+    3x3 CONVs run with inter-composite-layer fusion."""
+    bf16, k, n, h, w, ci, co, ldc, off = case
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    xf, wt, bp, _ = _bwd_inputs(bf16, k, n, h, w, ci, co, seed=9)
+    bufx = synth.normal(9, "slice_x", (n, h, w, ldc), bf16=bf16) * np.float32(1.4) + np.float32(0.3)
+    bufx = synth.round_to_bf16(bufx) if bf16 else bufx
+    bufd = synth.normal(9, "slice_d", (n, h, w, ldc), bf16=bf16) * np.float32(0.5)
+    bufd = synth.round_to_bf16(bufd) if bf16 else bufd
+    alpha_f = synth.normal(9, "alpha", (co,), std=0.05)
+    betap_f = synth.normal(9, "betap", (co,), std=0.05)
+    x, wd = dev(xf, bf16), dev(wt, bf16)
+    X, D = dev(bufx, bf16), dev(bufd, bf16)
+    xs, ds = X[..., off:off + co], D[..., off:off + co]
+    xbn = _bn_dev(bp["gamma"], bp["beta"])
+    B.bnr_bn_stats(x, xbn)
+    st = B.BN.stats_only(co, x.device)
+    B.bnr_bn_stats(xs, st)
+    dw = torch.empty(wt.shape, dtype=torch.float32, device=x.device)
+    dgamma = torch.empty(ci, dtype=torch.float32, device=x.device)
+    dbeta = torch.empty_like(dgamma)
+    dy = torch.empty_like(x)
+    desc = B.desc_for(x, xs, k, n, h, w)
+    B.bnr_bwd_fused(desc, x, xbn, wd, B.grad_split(ds, xs, st, f32dev(alpha_f), f32dev(betap_f)), dw, dgamma,
+                    dbeta, dy)
+    torch.cuda.synchronize()
+    xs64 = bufx[..., off:off + co].astype(np.float64)
+    mu_s, _, rstd_s = P.bn_stats(xs64, 1e-5)
+    g_r = rnd(bufd[..., off:off + co].astype(np.float64) + alpha_f.astype(np.float64) +
+              betap_f.astype(np.float64) * (xs64 - mu_s) * rstd_s)
+    x64 = xf.astype(np.float64)
+    yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    z = rnd(P.relu_fwd(yr))
+    dz = P.conv_dgrad(g_r, wt.astype(np.float64), (h, w))
+    dyr = rnd(P.relu_bwd(dz, yr))
+    dwr = P.conv_wgrad(z, g_r, k)
+    _, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd, want_dx=False)
+    rt = RTOL[bf16]
+    amb = relu_ambiguous(yr, bf16)
+    assert_close("dy", host(dy), dyr, rt, exclude=amb)
+    assert_close("dW", host(dw), dwr, rt)
+    assert_close("dgamma", host(dgamma), dgr, rt)
+    assert_close("dbeta", host(dbeta), dbr, rt)
+
+
 @pytest.mark.parametrize("bf16", [False, True])
 def test_bwd_fused_pooled_gradient_plain_input(B, bf16):
     """Transition-style backward: gradient from a 2x2 average pooling, and a
@@ -345,7 +400,6 @@ def test_split_fusion_two_readers(B, case):
     G = dev(synth.normal(7, "garbage", (n, h, w, ldc), bf16=bf16), bf16)     # overwritten by the first reader
     alpha = f32dev(synth.normal(7, "ga", (c,)))
     betap = f32dev(synth.normal(7, "gb", (c,)))
-    dx_true = np.zeros_like(x64)
     readers = []
     for i, co in enumerate(cos):
         wt = synth.conv_weight(7, "w%d" % i, 1, c, co, bf16)
@@ -359,13 +413,7 @@ def test_split_fusion_two_readers(B, case):
         desc = B.desc_for(x, g, 1, n, h, w)
         B.bnr_bwd_fused_split(desc, x, bn, dev(wt, bf16), B.grad_dense(g), dw, dgamma, dbeta, G[..., :c], alpha,
                               betap, accumulate=i > 0)
-        yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
-        dz = P.conv_dgrad(gf.astype(np.float64), wt.astype(np.float64), (h, w))
-        dyr = rnd(P.relu_bwd(dz, yr))
-        dxr, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd)
-        dx_true += dxr
-        readers.append((dw, dgamma, dbeta, P.conv_wgrad(rnd(P.relu_fwd(yr)), gf.astype(np.float64), 1), dgr, dbr,
-                        relu_ambiguous(yr, bf16)))
+        readers.append((dw, dgamma, dbeta, wt, bp, gf))
     # the producer CONV of x (plain input): its backward takes the summed gradient on load
     xin_f = synth.normal(7, "xin", (n, h, w, cp), bf16=bf16)
     wp = synth.conv_weight(7, "wp", kp, cp, c, bf16)
@@ -380,29 +428,47 @@ def test_split_fusion_two_readers(B, case):
     B.bnr_split_dx(G[..., :c], x, shared, alpha, betap, G[..., :c])
     torch.cuda.synchronize()
     rt = RTOL[bf16]
-    amb = np.zeros(x64.shape, bool)
-    for dw, dgamma, dbeta, dwr, dgr, dbr, a in readers:
-        assert_close("reader dW", host(dw), dwr, rt)
-        assert_close("reader dgamma", host(dgamma), dgr, rt)
-        assert_close("reader dbeta", host(dbeta), dbr, rt)
-        amb |= a
-    assert_close("summed dx", host(G[..., :c]), dx_true, rt, exclude=amb)
     np.testing.assert_array_equal(host(G[..., c:]), rest)          # channels beyond the slice untouched
-    g_true = rnd(dx_true)
-    amb_px = np.broadcast_to(np.any(amb, axis=-1, keepdims=True), x64.shape)
-    assert np.mean(amb_px) <= 3e-2
-    dz_p = P.conv_dgrad(g_true, wp.astype(np.float64), (h, w))
-    # a flipped reader decision changes g at that pixel only; the producer's
-    # outputs are compared where no such pixel is within reach of the filter
-    reach = amb_px[..., :1]
-    if kp == 3:
-        pad = np.pad(reach, ((0, 0), (1, 1), (1, 1), (0, 0)))
-        reach = np.zeros_like(reach)
-        for dy_ in range(3):
-            for dx_ in range(3):
-                reach |= pad[:, dy_:dy_ + h, dx_:dx_ + w]
-    if not np.any(amb_px):
-        assert_close("producer dW (summed gradient on load)", host(dwp), P.conv_wgrad(xin_f.astype(np.float64),
-                                                                                      g_true, kp), rt)
-    assert_close("producer dx", host(dxin), dz_p, rt, exclude=np.broadcast_to(reach, dz_p.shape),
-                 max_excluded_frac=0.3)
+
+    # Oracle.  A reader's ReLU decision within rounding of 0 has two correct
+    # outcomes; with k such decisions there are 2^k correct results.  Every
+    # tensor must match one and the same of them (no element excluded).
+    x_flat = x64.reshape(-1, c)
+    per_reader = []
+    for dw, dgamma, dbeta, wt, bp, gf in readers:
+        yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+        dz = P.conv_dgrad(gf.astype(np.float64), wt.astype(np.float64), (h, w))
+        amb = np.flatnonzero(relu_ambiguous(yr, bf16).reshape(-1))
+        per_reader.append((yr, mu, rstd, dz, amb))
+    k = sum(len(a) for *_, a in per_reader)
+    assert k <= 6, "%d ambiguous reader decisions" % k
+
+    def variant(bits):
+        out, dx_true, j = [], np.zeros_like(x64), 0
+        for (dw, dgamma, dbeta, wt, bp, gf), (yr, mu, rstd, dz, amb) in zip(readers, per_reader):
+            dy = P.relu_bwd(dz, yr).reshape(-1)
+            for e in amb:                                   # flip this decision if its bit is set
+                if bits >> j & 1:
+                    dy[e] = 0.0 if dy[e] != 0 or yr.reshape(-1)[e] > 0 else dz.reshape(-1)[e]
+                j += 1
+            dyr = rnd(dy.reshape(x64.shape))
+            dxr, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd)
+            dx_true += dxr
+            out.append((P.conv_wgrad(rnd(P.relu_fwd(yr)), gf.astype(np.float64), 1), dgr, dbr))
+        g_true = rnd(dx_true)
+        return out, dx_true, P.conv_dgrad(g_true, wp.astype(np.float64), (h, w)), \
+            P.conv_wgrad(xin_f.astype(np.float64), g_true, kp)
+
+    got_dx, got_dxin, got_dwp = host(G[..., :c]), host(dxin), host(dwp)
+    best = None
+    for bits in range(1 << k):
+        out, dx_true, dz_p, dwp_r = variant(bits)
+        errs = [rel_err(got_dx, dx_true), rel_err(got_dxin, dz_p), rel_err(got_dwp, dwp_r)]
+        for (dw, dgamma, dbeta, *_), (dwr, dgr, dbr) in zip(readers, out):
+            errs += [rel_err(host(dw), dwr), rel_err(host(dgamma), dgr), rel_err(host(dbeta), dbr)]
+        if best is None or max(errs) < max(best):
+            best = errs
+    names = ["summed dx", "producer dx", "producer dW (summed gradient on load)"] + \
+        ["reader%d %s" % (i, t) for i in range(len(readers)) for t in ("dW", "dgamma", "dbeta")]
+    bad = [(nm, e) for nm, e in zip(names, best) if e > rt]
+    assert not bad, "no correct outcome of the %d ambiguous decisions matches: %s" % (k, bad)
