@@ -176,6 +176,24 @@ bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr
                                 const void *w, void *y, bnr_bn *y_bn,
                                 void *ws, size_t ws_bytes, void *stream);
 
+/* DenseNet transition layer, fused (Sec. 2.3 transition layer; Sec. 3.2
+ * (sub-BN2)-ReLU-CONV fusion): y = avgpool2x2(conv1x1(relu(bn(x)))) computed
+ * as conv1x1(avgpool2x2(relu(bn(x)))) -- both operations are linear, so the
+ * 2x2 average of the normalised, rectified input is formed while the CONV
+ * reads x and the CONV runs on the n (h/2) (w/2) pooled pixels (a quarter of
+ * the multiply-adds; no full-resolution output is written).  d describes the
+ * full-resolution CONV (k = 1, h and w even, in_ldc: pixel stride of x);
+ * y is the pooled [n][h/2][w/2][c_out] view with pixel stride d->out_ldc
+ * (e.g. the first channels of the next dense block's buffer).  y_bn (may be
+ * NULL): statistics of y from the epilogue.  Workspace: bnr_workspace_size(d).
+ * The backward is bnr_bwd_fused / bnr_bwd_fused_split with a
+ * BNR_GRAD_AVGPOOL2 gradient source (the pooled gradient formed on load).
+ * Errors: BNR_ERR_UNSUPPORTED for k != 1, BNR_ERR_SHAPE for odd h or w,
+ * BNR_ERR_NULL without x_bn, BNR_ERR_ALIAS if y overlaps x. */
+bnr_status bnr_bn_relu_conv_pool_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn,
+                                     const void *w, void *y, bnr_bn *y_bn,
+                                     void *ws, size_t ws_bytes, void *stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):
  * bnr_bn_relu_conv_fwd with the same arguments and results, but no workspace

@@ -56,6 +56,21 @@ def unit_fwd(x, gamma, beta, wt, eps, rnd):
                 gamma=np.asarray(gamma, np.float64), wt=np.asarray(wt, np.float64))
 
 
+def unit_pool_fwd(x, gamma, beta, wt, eps, rnd):
+    """The transition layer BN -> ReLU -> CONV1x1 -> 2x2 average pooling with
+    the pooling applied to the CONV's input instead of its output (Sec. 2.3
+    transition; both operations are linear, so the result is the same in
+    exact arithmetic).  Storage: the pooled CONV operand and the pooled output
+    are rounded; z, the full-resolution CONV input, is kept as the backward
+    uses it.  Returns (cache as unit_fwd's without "out", pooled)."""
+    y, mean, var, rstd = P.bn_fwd(x, gamma, beta, eps)
+    z = rnd(P.relu_fwd(y))
+    zp = rnd(P.avgpool2_fwd(P.relu_fwd(y)))
+    pooled = rnd(P.conv_fwd(zp, wt))
+    return dict(x=np.asarray(x, np.float64), y=y, z=z, zp=zp, mean=mean, var=var, rstd=rstd,
+                gamma=np.asarray(gamma, np.float64), wt=np.asarray(wt, np.float64)), pooled
+
+
 def unit_bwd(c, g, rnd):
     """Backward of ``unit_fwd`` for L = sum(out * g); g in operand precision.
 
@@ -131,12 +146,16 @@ def dense_layers_bwd(caches, G, rnd):
     return grads
 
 
-def block_fwd(X0, cpls, trans, eps, rnd, c_total):
+def block_fwd(X0, cpls, trans, eps, rnd, c_total, pool_first=False):
     """X0: block input [N,H,W,C0]; cpls: list of composite-layer params;
-    trans: gamma, beta, w (1x1) of the transition.  Returns pooled output."""
+    trans: gamma, beta, w (1x1) of the transition.  Returns pooled output.
+    pool_first: the transition pools before its CONV (unit_pool_fwd)."""
     buf, caches = dense_layers_fwd(X0, cpls, eps, rnd, c_total)
-    ut = unit_fwd(buf, trans["gamma"], trans["beta"], trans["w"], eps, rnd)
-    pooled = rnd(P.avgpool2_fwd(ut["out"]))
+    if pool_first:
+        ut, pooled = unit_pool_fwd(buf, trans["gamma"], trans["beta"], trans["w"], eps, rnd)
+    else:
+        ut = unit_fwd(buf, trans["gamma"], trans["beta"], trans["w"], eps, rnd)
+        pooled = rnd(P.avgpool2_fwd(ut["out"]))
     return pooled, dict(buf=buf, cpls=caches, ut=ut, C0=X0.shape[3])
 
 
@@ -176,7 +195,7 @@ def resnet_block_bwd(c, dr, rnd):
 
 
 # ------------------------------------------------ full DenseNet(-121) ----
-def densenet_fwd(d, eps, rnd):
+def densenet_fwd(d, eps, rnd, pool_first=False):
     """One training forward pass of a DenseNet (Sec. 2.3: dense blocks joined
     by transition layers; Sec. 3.1: a first 7x7 CONV):
       stem   CONV7x7/2 pad 3 -> BN -> ReLU -> max pooling 3x3/2 pad 1,
@@ -186,6 +205,7 @@ def densenet_fwd(d, eps, rnd):
              cross-entropy (mean over the batch).
     d: img [N,H,W,Ci], stem {w, gamma, beta}, blocks [{cpls, trans or None,
     c_total}], head {gamma, beta, w [C,K], b [K]}, labels [N].
+    pool_first: every transition pools before its CONV (block_fwd).
     Returns (loss, cache)."""
     st = d["stem"]
     img = np.asarray(d["img"], np.float64)
@@ -197,7 +217,7 @@ def densenet_fwd(d, eps, rnd):
     blocks = []
     for b in d["blocks"]:
         if b["trans"] is not None:
-            X, cb = block_fwd(X, b["cpls"], b["trans"], eps, rnd, b["c_total"])
+            X, cb = block_fwd(X, b["cpls"], b["trans"], eps, rnd, b["c_total"], pool_first)
         else:
             buf, caches = dense_layers_fwd(X, b["cpls"], eps, rnd, b["c_total"])
             cb = dict(buf=buf, cpls=caches, C0=X.shape[3])

@@ -87,6 +87,8 @@ _lib_fns = dict(
                                c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_fwd=_sig("bnr_bn_relu_conv_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, c_vp,
                               _P(BNStruct), c_vp, c_sz, c_vp),
+    bnr_bn_relu_conv_pool_fwd=_sig("bnr_bn_relu_conv_pool_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
+                                   c_vp, _P(BNStruct), c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_fwd_static=_sig("bnr_bn_relu_conv_fwd_static", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct),
                                      c_vp, c_vp, _P(BNStruct), c_vp),
     bnr_avgpool2_fwd=_sig("bnr_avgpool2_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
@@ -300,6 +302,15 @@ def bnr_bn_relu_conv_fwd(desc, x, x_bn, w, y, y_bn=None):
     ys = y_bn.struct() if y_bn is not None else None
     _check(_lib_fns["bnr_bn_relu_conv_fwd"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), _ptr(y),
                                             ctypes.byref(ys) if ys is not None else None, ws, wsb, _stream()))
+
+
+def bnr_bn_relu_conv_pool_fwd(desc, x, x_bn, w, y, y_bn=None):
+    """Transition layer: y (pooled view) = avgpool2x2(conv1x1(relu(bn(x)))), pooled before the CONV."""
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    xs = x_bn.struct()
+    ys = y_bn.struct() if y_bn is not None else None
+    _check(_lib_fns["bnr_bn_relu_conv_pool_fwd"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), _ptr(y),
+                                                 ctypes.byref(ys) if ys is not None else None, ws, wsb, _stream()))
 
 
 def bnr_bn_relu_conv_fwd_static(desc, x, x_bn, w, y, y_bn=None):

@@ -135,9 +135,13 @@ def _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode, in_sweep=True):
     if trans_out:
         if mode == "unfused":
             _unit_ref_fwd(a, m, c, trans_out, 1, e)
+            a += m * trans_out * e + m // 4 * trans_out * e      # avgpool forward
         else:
-            _unit_fused_fwd(a, m, c, trans_out, 1, e, mode == "fused")
-        a += m * trans_out * e + m // 4 * trans_out * e          # avgpool forward
+            # BN, ReLU and the 2x2 average in the CONV's prologue: read x,
+            # write only the pooled output
+            if mode == "fused":
+                a += m * c * e                                   # the transition BN's statistics sweep
+            a += m * c * e + c * trans_out * e + m // 4 * trans_out * e
     return c
 
 
@@ -181,8 +185,8 @@ def dense_block(m, c0, layers, width, k, trans_out, e):
 def densenet(n, hw, c_in, c_stem, blocks, classes, e):
     """Whole DenseNet step.  blocks: [(c0, layers, width, k, trans_out or 0)].
     Fused: first CONV with statistics epilogue; BN-ReLU-max pooling reading s
-    and writing block 1's input with its statistics; blocks with ICF (blocks
-    after the first sweep their pooled input once for statistics); the head
+    and writing block 1's input with its statistics; blocks with ICF (a
+    transition writes the next block's input with its statistics); the head
     reads the last block (BN + ReLU + pooling) and its backward writes the
     summed gradient; max-pooling backward reads s and the block-1 input
     gradient and writes dy; the first CONV's weight gradient reads the image,
@@ -205,7 +209,7 @@ def densenet(n, hw, c_in, c_stem, blocks, classes, e):
         h, dims = hp, []
         for i, (c0, layers, width, k, to) in enumerate(blocks):
             m = n * h * h
-            ct = _block_fwd(a, m, c0, layers, width, k, to, e, mode, in_sweep=i > 0)
+            ct = _block_fwd(a, m, c0, layers, width, k, to, e, mode, in_sweep=False)
             dims.append(m)
             if to:
                 h //= 2

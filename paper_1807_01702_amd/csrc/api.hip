@@ -298,11 +298,16 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
 size_t conv_fwd_ws(const ConvWs &w) { return w.pack + w.part + w.red; }
 
 // forward CONV with optional BN+ReLU prologue and optional statistics epilogue
-// (need: the workspace bytes checked; 0 = the whole conv workspace)
+// (need: the workspace bytes checked; 0 = the whole conv workspace).  pool:
+// the BN+ReLU output is averaged over 2x2 windows before the 1x1 CONV, whose
+// output y is the pooled [n][h/2][w/2][c_out] view.
 bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w, void *y,
-                    bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream, size_t need = 0)
+                    bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream, size_t need = 0, bool pool = false)
 {
     TRY(check_desc(d));
+    if (pool && (d->k != 1 || d->h % 2 || d->w % 2 || !x_bn))
+        return fail(d->k != 1 ? BNR_ERR_UNSUPPORTED : BNR_ERR_SHAPE,
+                    "pooled forward: 1x1 CONV with BN, even h and w (k %d, h %d, w %d)", d->k, d->h, d->w);
     TRY(check_ptr(x, "x"));
     TRY(check_ptr(w, "w"));
     TRY(check_ptr(y, "y"));
@@ -312,7 +317,8 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     TRY(check_ws(ws, ws_bytes, need ? need : cw.total));
     const int es = esize(d->dtype);
     const int64_t m = pixels(d);
-    Range ry = view_range(y, m, d->c_out, d->out_ldc, es);
+    const int64_t my = pool ? m / 4 : m;                 // output rows
+    Range ry = view_range(y, my, d->c_out, d->out_ldc, es);
     if (overlap(ry, view_range(x, m, d->c_in, d->in_ldc, es))) return fail(BNR_ERR_ALIAS, "y overlaps x");
     const int64_t wbytes = (int64_t)d->k * d->k * d->c_in * d->c_out * es;
     Range rw{reinterpret_cast<uintptr_t>(w), reinterpret_cast<uintptr_t>(w) + (uintptr_t)wbytes};
@@ -324,7 +330,8 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     float *part = wp.part;
     RowsParams rp;
     fill_rows(rp, d, d->c_in, d->c_out);
-    rp.pro = x_bn ? PRO_BNRELU : PRO_NONE;
+    rp.pro = x_bn ? (pool ? PRO_BNRELU_POOL : PRO_BNRELU) : PRO_NONE;
+    rp.m = my;
     rp.a = x; rp.a_ldc = d->in_ldc;
     if (x_bn) { rp.p_gamma = x_bn->gamma; rp.p_beta = x_bn->beta; rp.p_mean = x_bn->mean; rp.p_rstd = x_bn->rstd; }
     rp.epi = y_bn ? EPI_STATS : EPI_STORE;
@@ -335,7 +342,7 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     TRY(launch_conv_any(rp, d, w, 0, wpack, &R, s));
     if (y_bn) {
         const SplitTerms ft = fwd_terms(y_bn, true);
-        TRY_HIP(launch_stats_finalize(part, R, d->c_out, m, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
+        TRY_HIP(launch_stats_finalize(part, R, d->c_out, my, FIN_MVF, y_bn->eps, y_bn->mean, y_bn->var, y_bn->rstd,
                                       nullptr, nullptr, wp.red, s, &ft),
                 "stats combine");
     }
@@ -451,6 +458,13 @@ bnr_status bnr_bn_relu_conv_fwd_static(const bnr_conv_desc *d, const void *x, co
     TRY(static_scratch(&ptr));
     TraceSuppress no_events;              // launch timing would create HIP events
     return conv_fwd(d, x, x_bn, w, y, y_bn, ptr, kStaticScratchBytes, stream, need);
+}
+
+bnr_status bnr_bn_relu_conv_pool_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                                     void *y, bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!x_bn) return fail(BNR_ERR_NULL, "x_bn is NULL");
+    return conv_fwd(d, x, x_bn, w, y, y_bn, ws, ws_bytes, stream, 0, true);
 }
 
 bnr_status bnr_avgpool2_fwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtype dtype, const void *x, int32_t ldc,

@@ -56,15 +56,18 @@ static P1Geom p1_geom(int K, int N)
 // tile's loads in flight while it waits for the epilogue operand.
 // PC: the prologue, compile-time where it pays: PC_BNGRAD (the deferred
 // BN input gradient, which reads a second operand), PC_BNRELU (the forward
-// BN+ReLU with the statistics epilogue), PC_RUNTIME (PRO_NONE / PRO_BNRELU /
-// PRO_RELU / PRO_POOLUP chosen at run time).
-enum { PC_RUNTIME = 0, PC_BNGRAD = 1, PC_BNRELU = 2 };
+// BN+ReLU with the statistics epilogue), PC_BNRELU_POOL (BN+ReLU and the 2x2
+// average of each window: a tile row loads four input pixels), PC_RUNTIME
+// (PRO_NONE / PRO_BNRELU / PRO_RELU / PRO_POOLUP chosen at run time).
+enum { PC_RUNTIME = 0, PC_BNGRAD = 1, PC_BNRELU = 2, PC_BNRELU_POOL = 3 };
 
 template <int CBW, int NVA, int EK, int PC, int BM>
 __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 {
     constexpr bool BNG = PC == PC_BNGRAD;
-    const int pro = PC == PC_BNRELU ? PRO_BNRELU : (PC == PC_BNGRAD ? PRO_BNGRAD : p.pro);
+    constexpr bool POOLF = PC == PC_BNRELU_POOL;          // rows are 2x2 windows of the input
+    constexpr int PF = POOLF ? 4 : 1;                      // input pixels per A row
+    const int pro = PC == PC_BNRELU || POOLF ? PRO_BNRELU : (PC == PC_BNGRAD ? PRO_BNGRAD : p.pro);
     using T = bf16_t;
     using M = Mfma<T>;
     constexpr int VEC = 8;
@@ -88,9 +91,9 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     const int H = p.h, W = p.w;
     const T *wsrc = reinterpret_cast<const T *>(p.wraw);
     const int a_ldc = (int)p.a_ldc, a2_ldc = (int)p.a2_ldc, y_ldc = (int)p.y_ldc, ex_ldc = (int)p.ex_ldc;
-    const bool pool = pro == PRO_POOLUP;
+    const bool pool = !POOLF && pro == PRO_POOLUP;
     // operand views as raw buffers (launcher guarantees each spans < 2^31 bytes)
-    const int64_t arows = pool ? (int64_t)m / 4 : m;
+    const int64_t arows = pool ? (int64_t)m / 4 : (POOLF ? (int64_t)m * 4 : m);
     const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((arows - 1) * a_ldc + K) * 2));
     const __amdgpu_buffer_rsrc_t a2buf = buf_view(BNG ? p.a2 : p.a, BNG ? (uint32_t)(((int64_t)(m - 1) * a2_ldc + K) * 2) : 0u);
     const __amdgpu_buffer_rsrc_t ybuf = buf_view(p.y, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * 2));
@@ -169,11 +172,27 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
         sr[j] = q % BM;
         sc[j] = ((q / BM) * 4 + (i & 3)) * VEC;
     }
-    vec16 ra[NVA], rb[NVB];
+    vec16 ra[NVA * PF], rb[NVB];
     // the wave-uniform mode switches sit outside the slot loops, so each
     // mode's slots are straight-line code
     auto load_a = [&](int p0, int lim) __attribute__((always_inline)) {
-        if (!BNG && pool) {             // (the deferred-gradient variants never read a pooled gradient)
+        if (POOLF) {                    // row q = window (img, y, x) of the (H/2) x (W/2) grid
+            const int ho = H / 2, wo = W / 2;
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int q = p0 + sr[j], c = sc[j];
+                const bool ok = j < nva && c < K && q < lim;
+                const int img = q / (ho * wo);
+                const int rem = q - img * ho * wo;
+                const int y = rem / wo, x = rem - y * wo;
+                const int p00 = (img * H + 2 * y) * W + 2 * x;
+                #pragma unroll
+                for (int f = 0; f < 4; f++) {
+                    const int pp = p00 + (f >> 1) * W + (f & 1);
+                    ra[j * PF + f] = bld16(abuf, ok ? (uint32_t)(pp * a_ldc + c) * 2u : kBufOff);
+                }
+            }
+        } else if (!BNG && pool) {      // (the deferred-gradient variants never read a pooled gradient)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int pp = p0 + sr[j], c = sc[j];
@@ -215,6 +234,26 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
                 put(j, Elem<T>::pack(f));
+            }
+        } else if (POOLF) {                               // z = mean over the window of max(x c0 + c1, 0)
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = sc[j] < KP ? sc[j] : 0;
+                float acc[VEC], ca[VEC], cb[VEC];
+                lds_f8(coef + c, ca);
+                lds_f8(coef + KP + c, cb);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) acc[e] = 0.f;
+                #pragma unroll
+                for (int f4 = 0; f4 < PF; f4++) {
+                    float f[VEC];
+                    Elem<T>::unpack(ra[j * PF + f4], f);
+                    #pragma unroll
+                    for (int e = 0; e < VEC; e++) acc[e] += __builtin_fmaxf(bn_lin(f[e], ca[e], cb[e]), 0.f);
+                }
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) acc[e] *= 0.25f;
+                put(j, Elem<T>::pack(acc));
             }
         } else if (pro == PRO_BNRELU) {                   // z = max(x c0 + c1, 0)
             #pragma unroll
@@ -459,6 +498,7 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
     double a = m * p.K;
     if (BNG) a *= 2.0;
     if (p.pro == PRO_POOLUP) a /= 4.0;
+    if (PC == PC_BNRELU_POOL) a *= 4.0;             // four input pixels per row
     double out = m * p.N;
     if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD || EK == EK_BNBWD_SC) out += m * p.N;
     if (EK == EK_BNBWD_SCACC) out += 2.0 * m * p.N;
@@ -474,7 +514,9 @@ template <int CBW, int NVA128, int EK, int PC>
 static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK >= EK_BNBWD;
-    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && PC == PC_BNGRAD);
+    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && PC == PC_BNGRAD) || PC == PC_BNRELU_POOL;
+    // (64-row tiles hold at most four 16-byte A vectors per thread; the
+    // pooling prologue loads four pixels for each)
     if constexpr (small) return run_p1<CBW, 4, EK, PC, 64>(p, g, s, rows);
     else return run_p1<CBW, NVA128, EK, PC, 128>(p, g, s, rows);
 }
@@ -523,13 +565,21 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
     if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return hipErrorInvalidValue;
     if (p.epi == EPI_RELUMASK && !p.ex) return hipErrorInvalidValue;
     if (p.pro == PRO_POOLUP && (p.h % 2 || p.w % 2 || (int64_t)p.n * p.h * p.w != p.m)) return hipErrorInvalidValue;
+    const bool poolf = p.pro == PRO_BNRELU_POOL;
+    if (poolf && (p.h % 2 || p.w % 2 || (int64_t)p.n * p.h * p.w != 4 * p.m || p.wtrans ||
+                  (p.epi != EPI_STORE && p.epi != EPI_STATS) || p.accumulate || !p.p_mean || !p.p_gamma ||
+                  !p.p_rstd || !p.p_beta))
+        return hipErrorInvalidValue;
     // 32-bit pixel indices and raw-buffer operand views: every span below 2^31 bytes
     const int64_t lim = (int64_t)1 << 31;
-    if (p.m < 1 || p.m >= (lim >> 1) || (p.m * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
+    const int64_t arows = poolf ? 4 * p.m : p.m;
+    if (p.m < 1 || arows >= (lim >> 1) || (arows * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
     const P1Geom g = p1_geom(p.K, p.N);
     const int ek = epilogue_kind(p.epi, p.accumulate, p.e_scale);
+    if (poolf) return ek == EK_STATS ? run_p1_nva<EK_STATS, PC_BNRELU_POOL>(p, g, s, rows)
+                                     : run_p1_nva<EK_STORE, PC_BNRELU_POOL>(p, g, s, rows);
     if (p.pro == PRO_BNGRAD) return run_p1_ek<PC_BNGRAD>(p, g, ek, s, rows);
     if (p.pro == PRO_BNRELU && ek == EK_STATS) return run_p1_nva<EK_STATS, PC_BNRELU>(p, g, s, rows);
     return run_p1_ek<PC_RUNTIME>(p, g, ek, s, rows);

@@ -21,6 +21,9 @@
 //   PRO_BNGRAD : a = A dy + B x + C  (deferred BN input gradient from dy and
 //                the BN input x; coefficients by deferred_coef)
 //   PRO_POOLUP : a = g[n][y/2][x/2] / 4   (2x2 average-pooling gradient)
+//   PRO_BNRELU_POOL: row = 2x2 window; a = mean over its four pixels of
+//                max(gamma*(x-mean)*rstd + beta, 0)  (1x1 only, general
+//                staging loop)
 // Epilogues (sub-BN1 side):
 //   EPI_STATS  : store y, per-channel sum(y), sum(y^2) of the stored values
 //   EPI_BNBWD  : dy = dz * [gamma*xhat+beta > 0] with xhat from the BN input,
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     const int arows = BM + 2 * halo;
 
     // per-channel prologue coefficients for all K channels
-    if (p.pro == PRO_BNRELU) {
+    if (p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL) {
         for (int c = tid; c < K; c += kThreads)             // y = x c0 + c1
             bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], coef[K + c], coef[2 * K + c]);
     } else if (p.pro == PRO_BNGRAD) {
@@ -316,6 +319,22 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
                     for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
                     out = Elem<T>::pack(f);
+                } else if (p.pro == PRO_BNRELU_POOL) {
+                    const int ho = H / 2, wo = W / 2;
+                    const int64_t img = pp / ((int64_t)ho * wo);
+                    const int rem = (int)(pp - img * ho * wo);
+                    const int y = rem / wo, x = rem - y * wo;
+                    const int64_t p00 = (img * H + 2 * y) * W + 2 * x;
+                    float acc[VEC];
+                    for (int e = 0; e < VEC; e++) acc[e] = 0.f;
+                    for (int f4 = 0; f4 < 4; f4++) {
+                        float f[VEC];
+                        Elem<T>::unpack(ldg16(asrc + (p00 + (f4 >> 1) * W + (f4 & 1)) * p.a_ldc + c), f);
+                        for (int e = 0; e < VEC; e++)
+                            acc[e] += __builtin_fmaxf(bn_lin(f[e], coef[K + c + e], coef[2 * K + c + e]), 0.f);
+                    }
+                    for (int e = 0; e < VEC; e++) acc[e] *= 0.25f;
+                    out = Elem<T>::pack(acc);
                 } else {  // PRO_POOLUP
                     const int64_t img = pp / ((int64_t)H * W);
                     const int rem = (int)(pp - img * H * W);
@@ -508,6 +527,7 @@ static double rows_algorithmic_bytes(const RowsParams &p)
     double a = m * K;                                            // A operand
     if (p.pro == PRO_BNGRAD) a = 2.0 * m * K;                    // dy and x
     if (p.pro == PRO_POOLUP) a = m / 4.0 * K;                    // pooled gradient
+    if (p.pro == PRO_BNRELU_POOL) a = 4.0 * m * K;               // four input pixels per window
     double out = m * N;                                          // output write
     if (p.epi == EPI_STORE && p.accumulate) out += m * N;        // read-modify-write
     if (p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK) out += m * N;   // BN input / ReLU input read
@@ -527,14 +547,14 @@ static bool rows_spans_fit(int dtype, int64_t m, int K, int N, int64_t a_ldc, in
 
 bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro)
 {
-    return dtype == DT_BF16 && taps == 1 && rows_spans_fit(dtype, m, K, N, a_ldc, a2_ldc, pro);
+    return dtype == DT_BF16 && taps == 1 && pro != PRO_BNRELU_POOL && rows_spans_fit(dtype, m, K, N, a_ldc, a2_ldc, pro);
 }
 
 template <typename T, int TAPS, int BM, int BN, int WM, int WN, int SP = SP_RUNTIME>
 static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 {
     using Cfg = RowsCfg<T, TAPS, BM, BN>;
-    const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD ? 3 : 0;
+    const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD || p.pro == PRO_BNRELU_POOL ? 3 : 0;
     const size_t lds = Cfg::LDS + (size_t)P * p.K * sizeof(float);
     auto kern = k_conv_rows<T, TAPS, BM, BN, WM, WN, SP>;
     static bool attr_set = false;
@@ -547,7 +567,7 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     TraceScope tr(KC_CONV, TAPS == 9 ? KID_CONV_3X3 : KID_CONV_1X1, s, rows_algorithmic_bytes(p),
                   2.0 * (double)p.m * TAPS * p.K * p.N);
     RowsParams q = p;
-    q.buf32 = TAPS == 1 && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
+    q.buf32 = TAPS == 1 && p.pro != PRO_BNRELU_POOL && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
     if (q.wdirect && (!q.buf32 || !p.wraw)) return hipErrorInvalidValue;   // unpacked weights need this path
     if (SP == SP_FWD_BNRELU && (!q.wdirect || p.wtrans || p.pro != PRO_BNRELU)) return hipErrorInvalidValue;
     if (SP == SP_DGRAD_BNGRAD && (!q.wdirect || !p.wtrans || p.pro != PRO_BNGRAD)) return hipErrorInvalidValue;
@@ -559,7 +579,11 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 static bool rows_operands_ok(const RowsParams &p)
 {
     if (!p.a || !(p.wdirect ? p.wraw : p.wpack) || !p.y) return false;
-    if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return false;
+    if ((p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL) && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta))
+        return false;
+    if (p.pro == PRO_BNRELU_POOL && (p.taps != 1 || p.h % 2 || p.w % 2 || (int64_t)p.n * p.h * p.w != 4 * p.m ||
+                                     p.wtrans || p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK))
+        return false;
     if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd ||
                                 (p.p_split ? (!p.p_alpha || !p.p_betap) : (!p.p_gamma || !p.p_dbeta || !p.p_dgamma))))
         return false;

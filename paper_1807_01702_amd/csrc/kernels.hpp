@@ -67,7 +67,11 @@ hipError_t launch_bwd_tail(const float *wpart, int64_t S, int64_t len, float *dw
 hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float *out, void *red, hipStream_t s);
 
 // ---- implicit-GEMM CONV over pixel rows (forward / data gradient) ---------
-enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 4 };
+// PRO_BNRELU_POOL: the GEMM rows are the 2x2 windows of the input image (h, w
+// even; m = n h w / 4 rows); a row is the average of relu(bn(x)) over its
+// window's four pixels (BN, ReLU and the transition's average pooling applied
+// before the linear 1x1 CONV)
+enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 4, PRO_BNRELU_POOL = 5 };
 enum { EPI_STORE = 0, EPI_STATS = 1, EPI_BNBWD = 2, EPI_RELUMASK = 3 };
 // Compile-time epilogue kinds of the persistent CONV kernels (EPI_STORE splits
 // into plain store and read-add-store).

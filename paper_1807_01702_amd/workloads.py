@@ -221,9 +221,15 @@ class _DenseStage:
         self.ut = None
         if trans is not None:
             to = trans["w"].shape[3]
-            self.t = torch.empty((n, h, w, to), dtype=dt, device=dev)
+            # the fused transition writes only its pooled output (BN, ReLU and
+            # the 2x2 average in the CONV's prologue): t is then a shape
+            # placeholder that no kernel touches
+            self.t = (torch.empty((n, h, w, to), dtype=dt, device=dev) if not fused else
+                      torch.empty((1, 1, 1, to), dtype=dt, device=dev).expand(n, h, w, to))
             self.ut = _Unit(n, h, w, self.X, self.t, 1, trans["gamma"], trans["beta"], trans["w"], eps, dev, bf16,
                             fused, ref_mode)
+            if fused:
+                self.ut.desc.out_ldc = to     # the backward's descriptor: a dense full-resolution output
             self.dy_t = torch.empty((n, h, w, ct), dtype=dt, device=dev)
             if not fused:
                 self.dt = torch.empty_like(self.t)
@@ -283,10 +289,18 @@ class _DenseStage:
         """Views of the shared per-channel statistics of channels [lo, hi)."""
         return dict(mean=self.mu[lo:hi], var=self.var[lo:hi], rstd=self.rstd[lo:hi])
 
-    def forward(self, pooled=None, in_stats_done=False):
+    def _pool_desc(self, pooled):
+        """Descriptor of the fused transition writing the pooled view."""
+        ut = self.ut
+        return B.conv_desc(self.n, self.h, self.w, ut.desc.c_in, ut.desc.c_out, 1, ut.desc.in_ldc, B.view(pooled)[3],
+                           ut.desc.dtype)
+
+    def forward(self, pooled=None, in_stats_done=False, pooled_bn=None):
         """Composite layers, then (with a transition) its CONV and the 2x2
-        pooling into the view `pooled`.  in_stats_done (ICF): the block
-        input's statistics are already in the shared arrays."""
+        pooling into the view `pooled` (fused: pooled before the CONV, in its
+        prologue; pooled_bn: statistics of the pooled output from the CONV's
+        epilogue).  in_stats_done (ICF): the block input's statistics are
+        already in the shared arrays."""
         if self.icf:
             if not in_stats_done:
                 B.bnr_bn_stats(self.X[..., :self.c0], self.in_stats)           # the one statistics sweep
@@ -295,7 +309,7 @@ class _DenseStage:
                 B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out, st)   # the new slice's statistics
             ut = self.ut
             if ut is not None:
-                B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
+                B.bnr_bn_relu_conv_pool_fwd(self._pool_desc(pooled), ut.x, ut.bn, ut.wt, pooled, pooled_bn)
         elif self.fused:
             for c_l, k, u1, u2 in self.cpl:
                 B.bnr_bn_stats(u1.x, u1.bn)                                    # sub-BN1 of a concat: own sweep
@@ -304,15 +318,14 @@ class _DenseStage:
             ut = self.ut
             if ut is not None:
                 B.bnr_bn_stats(ut.x, ut.bn)
-                B.bnr_bn_relu_conv_fwd(ut.desc, ut.x, ut.bn, ut.wt, ut.out)
+                B.bnr_bn_relu_conv_pool_fwd(self._pool_desc(pooled), ut.x, ut.bn, ut.wt, pooled, pooled_bn)
         else:
             for c_l, k, u1, u2 in self.cpl:
                 u1.ref_fwd()
                 u2.ref_fwd()
             if self.ut is not None:
                 self.ut.ref_fwd()
-        if self.ut is not None:
-            B.bnr_avgpool2_fwd(self.t, pooled, self.n, self.h, self.w)
+                B.bnr_avgpool2_fwd(self.t, pooled, self.n, self.h, self.w)
 
     def backward(self, dpool=None):
         """With a transition: dpool is the gradient view of the pooled output,
@@ -533,7 +546,9 @@ class DenseNet:
             B.bnr_bn_relu_maxpool_fwd(self.z0, None, s0.X[..., :s0.c0], n, self.hs, self.ws_)
         for i, st in enumerate(self.stages):
             nxt = self.stages[i + 1] if i + 1 < len(self.stages) else None
-            st.forward(nxt.X[..., :nxt.c0] if nxt is not None else None, in_stats_done=(i == 0))
+            # fused: the transition's epilogue produces the next block's input statistics
+            st.forward(nxt.X[..., :nxt.c0] if nxt is not None else None, in_stats_done=(i == 0 or self.fused),
+                       pooled_bn=nxt.in_stats if nxt is not None and self.fused else None)
         last = self.stages[-1]
         h, w = self.hw[-1]
         if not self.fused:

@@ -359,7 +359,7 @@ def test_densenet_fp32_all_tensors(fused, n, hw, seed):
     from paper_1807_01702_amd import workloads as W
     d = synth.densenet(seed=seed, n=n, hw=hw, blocks=(2, 2, 2, 2), bf16=False)
     rnd = OC.storage(False)
-    loss, c = OC.densenet_fwd(d, d["eps"], rnd)
+    loss, c = OC.densenet_fwd(d, d["eps"], rnd, pool_first=fused)     # the fused transitions pool first
     assert _margin(c) >= 1e-6, "precondition: ReLU decisions must be unique at fp32 accuracy"
     g = OC.densenet_bwd(c, rnd)
     wl = W.DenseNet(d, fused=fused)
@@ -411,11 +411,13 @@ def test_densenet_bf16_full_resolution(blocks):
     from paper_1807_01702_amd import workloads as W
     d = synth.densenet(seed=0, n=2, blocks=blocks)
     rnd = OC.storage(True)
-    loss, c = OC.densenet_fwd(d, d["eps"], rnd)
-    g = OC.densenet_bwd(c, rnd)
     rt = RTOL[True]
     errs, names = {}, []
     for fused in (True, False):
+        # each path against the oracle with its own transition order (the
+        # fused transitions pool before the CONV: rounding at other sites)
+        loss, c = OC.densenet_fwd(d, d["eps"], rnd, pool_first=fused)
+        g = OC.densenet_bwd(c, rnd)
         wl = W.DenseNet(d, fused=fused)
         wl.step()
         torch.cuda.synchronize()

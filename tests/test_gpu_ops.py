@@ -163,6 +163,42 @@ def test_conv_fwd(B, case, mode):
         assert_stats("output stats", host(ybn.mean), host(ybn.var), mr, vr, RTOL[bf16])
 
 
+# --------------------------------------- transition: BN-ReLU-pool-CONV ----
+@pytest.mark.parametrize("case", [
+    # dtype, n, h, w, c_in, c_out, in_ldc, out_ldc
+    (True, 4, 56, 56, 256, 128, 256, 128),      # dense block 1's transition (persistent 1x1 kernel)
+    (True, 2, 6, 10, 200, 64, 208, 96),         # ragged channels, output view of a wider buffer
+    (True, 2, 14, 14, 512, 256, 512, 512),      # K > 256: tiled kernel (DenseNet-121 transition 2 shape)
+    (False, 2, 4, 6, 40, 24, 48, 32),           # fp32 (tiled kernel)
+])
+@pytest.mark.parametrize("stats", [False, True])
+def test_bn_relu_conv_pool_fwd(B, case, stats):
+    """y = avgpool2x2(conv1x1(relu(bn(x)))): the fused path averages the
+    normalised, rectified input over each window and runs the CONV on the
+    pooled pixels; the oracle convolves at full resolution, then pools (equal
+    in exact arithmetic; the bf16 path rounds the pooled operand)."""
+    bf16, n, h, w, ci, co, ildc, oldc = case
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    xf = synth.normal(11, "x", (n, h, w, ildc), bf16=bf16)
+    wt = synth.conv_weight(11, "w", 1, ci, co, bf16)
+    bp = synth.bn_params(11, "bn", ci)
+    x = dev(xf, bf16)
+    y = torch.zeros((n, h // 2, w // 2, oldc), dtype=x.dtype, device=x.device)
+    xbn = _bn_dev(bp["gamma"], bp["beta"])
+    B.bnr_bn_stats(x[..., :ci], xbn)
+    desc = B.conv_desc(n, h, w, ci, co, 1, ildc, oldc, B.dtype_code(x))
+    ybn = B.BN.stats_only(co, x.device) if stats else None
+    B.bnr_bn_relu_conv_pool_fwd(desc, x[..., :ci], xbn, dev(wt, bf16), y[..., :co], ybn)
+    torch.cuda.synchronize()
+    yr, _, _, _ = P.bn_fwd(xf[..., :ci].astype(np.float64), bp["gamma"], bp["beta"], 1e-5)
+    out_r = P.avgpool2_fwd(P.conv_fwd(P.relu_fwd(yr), wt.astype(np.float64)))
+    assert_close("pooled out", host(y[..., :co]), rnd(out_r), RTOL[bf16])
+    assert np.all(host(y[..., co:]) == 0), "wrote outside the output view"
+    if stats:
+        mr, vr, _ = P.bn_stats(rnd(out_r), 1e-5)
+        assert_stats("pooled output stats", host(ybn.mean), host(ybn.var), mr, vr, RTOL[bf16])
+
+
 # -------------------------------------------------------- fused backward ----
 BWD_CASES = [
     (False, 1, 8, 8, 8, 64, 32),

@@ -126,7 +126,8 @@ def test_bottleneck_reduced_batch(mode):
 # --------------------------------------------------- dense block + transition ----
 def _check_block(wl, d, rt):
     rnd = OC.storage(d["bf16"])
-    pooled, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"])
+    # the fused transition pools before its CONV: the oracle in the same order
+    pooled, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"], pool_first=wl.fused)
     dX0, g = OC.block_bwd(c, d["dpool"].astype(np.float64), rnd)
     assert_close("pooled", host(wl.pooled), pooled, rt)
     assert_close("block buffer", host(wl.X), c["buf"], rt)
@@ -198,11 +199,12 @@ def _l2(a, b):
 def test_dense_block_bf16():
     d = synth.dense_block(seed=0, n=2)
     rnd = OC.storage(True)
-    pooled, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"])
-    dX0, g = OC.block_bwd(c, d["dpool"].astype(np.float64), rnd)
     rt = RTOL[True]
     errs = {}
     for mode in ("fused", "fused_no_icf", "baseline"):
+        pooled, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"],
+                                 pool_first=mode != "baseline")
+        dX0, g = OC.block_bwd(c, d["dpool"].astype(np.float64), rnd)
         wl = _make("DenseBlock", d, mode)
         _step_twice(wl)
         assert_close("pooled", host(wl.pooled), pooled, rt)
@@ -393,7 +395,7 @@ def test_full_size_dense_block_against_oracle():
     d = synth.dense_block(seed=0)
     n, h, w, c0 = d["x"].shape
     rnd = OC.storage(True)
-    pooled, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"])
+    pooled, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"], pool_first=True)
     dX0, g = OC.block_bwd(c, d["dpool"].astype(np.float64), rnd)
     wl = W.DenseBlock(d, fused=True)
     dy2 = {}

@@ -97,6 +97,10 @@ MUTANTS = [
      'g0 = rnd(dx0)', 'g0 = np.array(dx0)'),
     ("bf16: weight gradient rounded to bf16", "compose.py",
      'dw = P.conv_wgrad(c["z"], g, K)', 'dw = rnd(P.conv_wgrad(c["z"], g, K))'),
+    ("pool-first transition: ReLU after the pooling", "compose.py",
+     'zp = rnd(P.avgpool2_fwd(P.relu_fwd(y)))', 'zp = rnd(P.relu_fwd(P.avgpool2_fwd(y)))'),
+    ("pool-first transition: pooled CONV operand not rounded", "compose.py",
+     'zp = rnd(P.avgpool2_fwd(P.relu_fwd(y)))', 'zp = P.avgpool2_fwd(P.relu_fwd(y))'),
     ("bf16: BN reductions rounded to bf16", "compose.py",
      'dx, dgamma, dbeta = P.bn_bwd(c["x"], dy, c["gamma"], c["mean"], c["rstd"])',
      'dx, dgamma, dbeta = P.bn_bwd(c["x"], dy, c["gamma"], c["mean"], c["rstd"]); dgamma = rnd(dgamma)'),

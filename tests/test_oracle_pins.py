@@ -43,6 +43,11 @@ def _oihw(w):
     return torch.from_numpy(np.ascontiguousarray(np.asarray(w, np.float64).transpose(3, 2, 0, 1)))
 
 
+def _is_bf16(a):
+    a = np.asarray(a, np.float64)
+    return np.array_equal(P.round_bf16(a), a)
+
+
 # ------------------------------------------------------------- golden ----
 def test_bn_worked_example():
     g = _golden("bn_worked_example.txt")
@@ -445,6 +450,24 @@ def test_block_forward_matches_torch():
         feats = torch.cat([feats, h], 1)
     ref = F.avg_pool2d(bn_relu_conv(feats, trans["gamma"], trans["beta"], trans["w"]), 2)
     np.testing.assert_allclose(pooled, _nhwc(ref), rtol=0, atol=1e-12)
+    # the transition pooled before its (linear) CONV: the same result in exact arithmetic
+    pooled_pf, _ = OC.block_fwd(X0, cpls, trans, 1e-5, rnd, ct, pool_first=True)
+    np.testing.assert_allclose(pooled_pf, _nhwc(ref), rtol=0, atol=1e-12)
+
+
+def test_bf16_pool_first_transition_storage():
+    """Pooled before the CONV, the bf16 model stores the pooled CONV operand
+    and the pooled output in bf16 and stays within bf16 rounding of the
+    conv-then-pool order."""
+    rnd = OC.storage(True)
+    x = P.round_bf16(RNG.standard_normal((2, 6, 8, 16)))
+    g, b = RNG.uniform(0.5, 1.5, 16), RNG.normal(0, 0.1, 16)
+    w = P.round_bf16(RNG.standard_normal((1, 1, 16, 8)) * 0.3)
+    c, pooled = OC.unit_pool_fwd(x, g, b, w, 1e-5, rnd)
+    assert _is_bf16(c["zp"]) and _is_bf16(pooled) and _is_bf16(c["z"])
+    ref = P.round_bf16(P.avgpool2_fwd(OC.unit_fwd(x, g, b, w, 1e-5, rnd)["out"]))
+    e = np.max(np.abs(pooled - ref)) / np.max(np.abs(ref))
+    assert 0 < e < 2e-2, e
 
 
 def test_bf16_storage_model_rounds_stored_tensors():
@@ -455,9 +478,6 @@ def test_bf16_storage_model_rounds_stored_tensors():
         np.testing.assert_array_equal(P.round_bf16(c[key]), c[key])
 
 
-def _is_bf16(a):
-    a = np.asarray(a, np.float64)
-    return np.array_equal(P.round_bf16(a), a)
 
 
 def _bf16_backward_runs():
