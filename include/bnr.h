@@ -194,6 +194,22 @@ bnr_status bnr_bn_relu_conv_pool_fwd(const bnr_conv_desc *d, const void *x, cons
                                      const void *w, void *y, bnr_bn *y_bn,
                                      void *ws, size_t ws_bytes, void *stream);
 
+/* ResNet bottleneck boundary, fused (Sec. 2.2 element-wise sum; Sec. 3.2
+ * (sub-BN2)-ReLU-CONV fusion): the last BN of a block, the identity addition
+ * and the ReLU run in the prologue of the next block's first 1x1 CONV:
+ *   r = relu(gamma*(y-mean)*rstd + beta + ident)   (written to the view r:
+ *       the next block's identity and the ReLU operand of the backward),
+ *   out = conv1x1(r, w), with the statistics of out into out_bn (nullable).
+ * d describes the CONV (k = 1; c_in channels of y, ident and r; in_ldc: pixel
+ * stride of y; out_ldc of out).  y_bn: gamma, beta, mean, rstd of y.  r is
+ * exactly what bnr_bn_add_relu_fwd would write.  Workspace:
+ * bnr_workspace_size(d).  r must not overlap y, ident, w or out; out must not
+ * overlap y, ident or w (BNR_ERR_ALIAS).  k != 1: BNR_ERR_UNSUPPORTED. */
+bnr_status bnr_bn_add_relu_conv_fwd(const bnr_conv_desc *d, const void *y, const bnr_bn *y_bn,
+                                    const void *ident, int32_t ident_ldc, void *r, int32_t r_ldc,
+                                    const void *w, void *out, bnr_bn *out_bn,
+                                    void *ws, size_t ws_bytes, void *stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):
  * bnr_bn_relu_conv_fwd with the same arguments and results, but no workspace

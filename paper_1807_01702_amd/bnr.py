@@ -87,6 +87,8 @@ _lib_fns = dict(
                                c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_fwd=_sig("bnr_bn_relu_conv_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, c_vp,
                               _P(BNStruct), c_vp, c_sz, c_vp),
+    bnr_bn_add_relu_conv_fwd=_sig("bnr_bn_add_relu_conv_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
+                                  c_i32, c_vp, c_i32, c_vp, c_vp, _P(BNStruct), c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_pool_fwd=_sig("bnr_bn_relu_conv_pool_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
                                    c_vp, _P(BNStruct), c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_fwd_static=_sig("bnr_bn_relu_conv_fwd_static", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct),
@@ -302,6 +304,18 @@ def bnr_bn_relu_conv_fwd(desc, x, x_bn, w, y, y_bn=None):
     ys = y_bn.struct() if y_bn is not None else None
     _check(_lib_fns["bnr_bn_relu_conv_fwd"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), _ptr(y),
                                             ctypes.byref(ys) if ys is not None else None, ws, wsb, _stream()))
+
+
+def bnr_bn_add_relu_conv_fwd(desc, y, y_bn, ident, r, w, out, out_bn=None):
+    """r = relu(bn(y) + ident) (written), out = conv1x1(r) [+ statistics of out]."""
+    ws, wsb = workspace(bnr_workspace_size(desc), y.device)
+    pi, _, _, ldi = view(ident)
+    pr, _, _, ldr = view(r)
+    ys = y_bn.struct()
+    os_ = out_bn.struct() if out_bn is not None else None
+    _check(_lib_fns["bnr_bn_add_relu_conv_fwd"](ctypes.byref(desc), _ptr(y), ctypes.byref(ys), pi, ldi, pr, ldr,
+                                                _ptr(w), _ptr(out), ctypes.byref(os_) if os_ is not None else None,
+                                                ws, wsb, _stream()))
 
 
 def bnr_bn_relu_conv_pool_fwd(desc, x, x_bn, w, y, y_bn=None):

@@ -237,13 +237,16 @@ def resnet_stack(m, c, width, blocks, e):
     f, u = _Acc(), _Acc()
     S, Sw = m * c * e, m * width * e
     w1, w2, w3 = c * width * e, 9 * width * width * e, width * c * e
-    for _ in range(blocks):
-        # forward: first CONV reads X and writes y1 with BN1's statistics (fused) / without (unfused)
-        for a in (f, u):
-            a += S + w1 + Sw
+    for i in range(blocks):
+        # forward: first CONV reads X and writes y1 with BN1's statistics (fused) / without (unfused);
+        # fused, from the second block on it reads the previous y3 and identity and writes X itself
+        # (the previous block's BN3 + add + ReLU in its prologue)
+        f += (S if i == 0 else 3 * S) + w1 + Sw
+        u += S + w1 + Sw
         _unit_fused_fwd(f, m, width, width, 3, e, False)
         _unit_fused_fwd(f, m, width, c, 1, e, False)
-        f += 3 * S                            # BN3 + add + ReLU: read y3, X; write out
+        if i == blocks - 1:
+            f += 3 * S                        # the last block: BN3 + add + ReLU as one sweep
         _unit_ref_fwd(u, m, width, width, 3, e)
         _unit_ref_fwd(u, m, width, c, 1, e)
         u += 2 * S + 2 * S + 3 * S            # two-pass statistics, normalise (r, w), add + ReLU (r, r, w)

@@ -460,6 +460,57 @@ bnr_status bnr_bn_relu_conv_fwd_static(const bnr_conv_desc *d, const void *x, co
     return conv_fwd(d, x, x_bn, w, y, y_bn, ptr, kStaticScratchBytes, stream, need);
 }
 
+bnr_status bnr_bn_add_relu_conv_fwd(const bnr_conv_desc *d, const void *y, const bnr_bn *y_bn, const void *ident,
+                                    int32_t ident_ldc, void *r, int32_t r_ldc, const void *w, void *out,
+                                    bnr_bn *out_bn, void *ws, size_t ws_bytes, void *stream)
+{
+    TRY(check_desc(d));
+    if (d->k != 1) return fail(BNR_ERR_UNSUPPORTED, "residual prologue: 1x1 CONV only (k = %d)", d->k);
+    TRY(check_ptr(y, "y"));
+    TRY(check_ptr(ident, "ident"));
+    TRY(check_ptr(r, "r"));
+    TRY(check_ptr(w, "w"));
+    TRY(check_ptr(out, "out"));
+    TRY(check_channels(d->c_in, ident_ldc, d->dtype, "ident"));
+    TRY(check_channels(d->c_in, r_ldc, d->dtype, "r"));
+    TRY(check_bn(y_bn, "y_bn", true, false));
+    if (out_bn) TRY(check_bn(out_bn, "out_bn", false, true));
+    const ConvWs cw = conv_ws(d);
+    TRY(check_ws(ws, ws_bytes, cw.total));
+    const int es = esize(d->dtype);
+    const int64_t m = pixels(d);
+    const Range ry = view_range(y, m, d->c_in, d->in_ldc, es), ri = view_range(ident, m, d->c_in, ident_ldc, es);
+    const Range rr = view_range(r, m, d->c_in, r_ldc, es), ro = view_range(out, m, d->c_out, d->out_ldc, es);
+    const int64_t wbytes = (int64_t)d->c_in * d->c_out * es;
+    const Range rw{reinterpret_cast<uintptr_t>(w), reinterpret_cast<uintptr_t>(w) + (uintptr_t)wbytes};
+    if (overlap(rr, ry) || overlap(rr, ri) || overlap(rr, rw) || overlap(rr, ro))
+        return fail(BNR_ERR_ALIAS, "r overlaps y, ident, w or out");
+    if (overlap(ro, ry) || overlap(ro, ri) || overlap(ro, rw)) return fail(BNR_ERR_ALIAS, "out overlaps y, ident or w");
+
+    hipStream_t s = (hipStream_t)stream;
+    const ConvPtrs wp = conv_ptrs(ws, cw);
+    RowsParams rp;
+    fill_rows(rp, d, d->c_in, d->c_out);
+    rp.pro = PRO_BNADDRELU;
+    rp.a = y; rp.a_ldc = d->in_ldc;
+    rp.a2 = ident; rp.a2_ldc = ident_ldc;
+    rp.p_gamma = y_bn->gamma; rp.p_beta = y_bn->beta; rp.p_mean = y_bn->mean; rp.p_rstd = y_bn->rstd;
+    rp.side = r; rp.side_ldc = r_ldc;
+    rp.epi = out_bn ? EPI_STATS : EPI_STORE;
+    rp.y = out; rp.y_ldc = d->out_ldc;
+    rp.part = wp.part;
+    rp.e_shift = out_bn ? out_bn->shift : nullptr;
+    int64_t R = 0;
+    TRY(launch_conv_any(rp, d, w, 0, wp.pack, &R, s));
+    if (out_bn) {
+        const SplitTerms ft = fwd_terms(out_bn, true);
+        TRY_HIP(launch_stats_finalize(wp.part, R, d->c_out, m, FIN_MVF, out_bn->eps, out_bn->mean, out_bn->var,
+                                      out_bn->rstd, nullptr, nullptr, wp.red, s, &ft),
+                "stats combine");
+    }
+    return ok();
+}
+
 bnr_status bnr_bn_relu_conv_pool_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
                                      void *y, bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream)
 {

@@ -57,17 +57,21 @@ static P1Geom p1_geom(int K, int N)
 // PC: the prologue, compile-time where it pays: PC_BNGRAD (the deferred
 // BN input gradient, which reads a second operand), PC_BNRELU (the forward
 // BN+ReLU with the statistics epilogue), PC_BNRELU_POOL (BN+ReLU and the 2x2
-// average of each window: a tile row loads four input pixels), PC_RUNTIME
-// (PRO_NONE / PRO_BNRELU / PRO_RELU / PRO_POOLUP chosen at run time).
-enum { PC_RUNTIME = 0, PC_BNGRAD = 1, PC_BNRELU = 2, PC_BNRELU_POOL = 3 };
+// average of each window: a tile row loads four input pixels), PC_BNADD (the
+// residual block's BN + identity + ReLU: a second operand, and the result is
+// stored as a side output), PC_RUNTIME (PRO_NONE / PRO_BNRELU / PRO_RELU /
+// PRO_POOLUP chosen at run time).
+enum { PC_RUNTIME = 0, PC_BNGRAD = 1, PC_BNRELU = 2, PC_BNRELU_POOL = 3, PC_BNADD = 4 };
 
 template <int CBW, int NVA, int EK, int PC, int BM>
 __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 {
+    constexpr bool BNADD = PC == PC_BNADD;
     constexpr bool BNG = PC == PC_BNGRAD;
+    constexpr bool TWO = BNG || BNADD;                     // the prologue reads a second operand
     constexpr bool POOLF = PC == PC_BNRELU_POOL;          // rows are 2x2 windows of the input
     constexpr int PF = POOLF ? 4 : 1;                      // input pixels per A row
-    const int pro = PC == PC_BNRELU || POOLF ? PRO_BNRELU : (PC == PC_BNGRAD ? PRO_BNGRAD : p.pro);
+    const int pro = PC == PC_BNRELU || POOLF || BNADD ? PRO_BNRELU : (PC == PC_BNGRAD ? PRO_BNGRAD : p.pro);
     using T = bf16_t;
     using M = Mfma<T>;
     constexpr int VEC = 8;
@@ -76,7 +80,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     constexpr int RB = BM / 64;                                  // 16-row MFMA blocks per wave
     constexpr bool BNBWD = EK == EK_BNBWD || EK == EK_BNBWD_SC || EK == EK_BNBWD_SCACC;
     constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || BNBWD;
-    constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1, NVD = EK == EK_BNBWD_SCACC ? RPT : 1;
+    constexpr int NVB = TWO ? NVA : 1, NVX = READS ? RPT : 1, NVD = EK == EK_BNBWD_SCACC ? RPT : 1;
     extern __shared__ __align__(16) unsigned char smem[];
     T *Ws = reinterpret_cast<T *>(smem);
     T *As = Ws + (size_t)g.NP * g.ldw;
@@ -95,7 +99,10 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     // operand views as raw buffers (launcher guarantees each spans < 2^31 bytes)
     const int64_t arows = pool ? (int64_t)m / 4 : (POOLF ? (int64_t)m * 4 : m);
     const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((arows - 1) * a_ldc + K) * 2));
-    const __amdgpu_buffer_rsrc_t a2buf = buf_view(BNG ? p.a2 : p.a, BNG ? (uint32_t)(((int64_t)(m - 1) * a2_ldc + K) * 2) : 0u);
+    const __amdgpu_buffer_rsrc_t a2buf = buf_view(TWO ? p.a2 : p.a, TWO ? (uint32_t)(((int64_t)(m - 1) * a2_ldc + K) * 2) : 0u);
+    const int side_ldc = (int)p.side_ldc;
+    const __amdgpu_buffer_rsrc_t sbuf = buf_view(BNADD ? p.side : p.a,
+                                                 BNADD ? (uint32_t)(((int64_t)(m - 1) * side_ldc + K) * 2) : 0u);
     const __amdgpu_buffer_rsrc_t ybuf = buf_view(p.y, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * 2));
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * 2) : 0u);
@@ -209,7 +216,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 const int pp = p0 + sr[j], c = sc[j];
                 const bool ok = j < nva && c < K && pp < lim;
                 ra[j] = bld16(abuf, ok ? (uint32_t)(pp * a_ldc + c) * 2u : kBufOff);
-                if (BNG) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(pp * a2_ldc + c) * 2u : kBufOff);
+                if (TWO) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(pp * a2_ldc + c) * 2u : kBufOff);
             }
         }
     };
@@ -217,11 +224,27 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     // only, so rows past the end need no masking (their outputs are never
     // stored or counted); channels past K read zeros and have zero
     // coefficients and zero weights.
-    auto store_a = [&]() __attribute__((always_inline)) {
+    auto store_a = [&](int p0, int lim) __attribute__((always_inline)) {
         auto put = [&](int j, const vec16 &v) __attribute__((always_inline)) {
             if (j < nva && sc[j] < KP) *reinterpret_cast<vec16 *>(As + sr[j] * g.lda + sc[j]) = v;
         };
-        if (BNG) {                                        // PRO_BNGRAD: d = c0 dy + c1 x + c2
+        if (BNADD) {                                      // r = max(y c0 + c1 + identity, 0), also stored
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = sc[j] < KP ? sc[j] : 0;
+                float f[VEC], id[VEC], ca[VEC], cb[VEC];
+                Elem<T>::unpack(ra[j], f);
+                Elem<T>::unpack(rb[j < NVB ? j : 0], id);
+                lds_f8(coef + c, ca);
+                lds_f8(coef + KP + c, cb);
+                #pragma unroll
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(bn_lin(f[e], ca[e], cb[e]) + id[e], 0.f);
+                const vec16 v = Elem<T>::pack(f);
+                put(j, v);
+                const int pp = p0 + sr[j];
+                bst16(sbuf, j < nva && sc[j] < K && pp < lim ? (uint32_t)(pp * side_ldc + sc[j]) * 2u : kBufOff, v);
+            }
+        } else if (BNG) {                                        // PRO_BNGRAD: d = c0 dy + c1 x + c2
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int c = sc[j] < KP ? sc[j] : 0;
@@ -337,7 +360,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     for (int k = 0; k < nitems; k++) {
         int p0, lim;
         item(k, p0, lim);
-        store_a();
+        store_a(p0, lim);
         __syncthreads();
         // epilogue operand first: the epilogue waits for it while the next
         // tile's rows (issued after it) may still be in flight
@@ -497,6 +520,7 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
     const double m = (double)p.m;
     double a = m * p.K;
     if (BNG) a *= 2.0;
+    if (PC == PC_BNADD) a *= 3.0;                   // y and the identity read, the result written
     if (p.pro == PRO_POOLUP) a /= 4.0;
     if (PC == PC_BNRELU_POOL) a *= 4.0;             // four input pixels per row
     double out = m * p.N;
@@ -514,7 +538,8 @@ template <int CBW, int NVA128, int EK, int PC>
 static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK >= EK_BNBWD;
-    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && PC == PC_BNGRAD) || PC == PC_BNRELU_POOL;
+    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && (PC == PC_BNGRAD || PC == PC_BNADD)) ||
+                           PC == PC_BNRELU_POOL;
     // (64-row tiles hold at most four 16-byte A vectors per thread; the
     // pooling prologue loads four pixels for each)
     if constexpr (small) return run_p1<CBW, 4, EK, PC, 64>(p, g, s, rows);
@@ -570,9 +595,14 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
                   (p.epi != EPI_STORE && p.epi != EPI_STATS) || p.accumulate || !p.p_mean || !p.p_gamma ||
                   !p.p_rstd || !p.p_beta))
         return hipErrorInvalidValue;
+    const bool bnadd = p.pro == PRO_BNADDRELU;
+    if (bnadd && (!p.a2 || !p.side || p.wtrans || (p.epi != EPI_STORE && p.epi != EPI_STATS) || p.accumulate ||
+                  !p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta))
+        return hipErrorInvalidValue;
     // 32-bit pixel indices and raw-buffer operand views: every span below 2^31 bytes
     const int64_t lim = (int64_t)1 << 31;
     const int64_t arows = poolf ? 4 * p.m : p.m;
+    if (bnadd && (p.m * p.side_ldc + p.K) * 2 >= lim) return hipErrorInvalidValue;
     if (p.m < 1 || arows >= (lim >> 1) || (arows * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
@@ -580,6 +610,8 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
     const int ek = epilogue_kind(p.epi, p.accumulate, p.e_scale);
     if (poolf) return ek == EK_STATS ? run_p1_nva<EK_STATS, PC_BNRELU_POOL>(p, g, s, rows)
                                      : run_p1_nva<EK_STORE, PC_BNRELU_POOL>(p, g, s, rows);
+    if (bnadd) return ek == EK_STATS ? run_p1_nva<EK_STATS, PC_BNADD>(p, g, s, rows)
+                                     : run_p1_nva<EK_STORE, PC_BNADD>(p, g, s, rows);
     if (p.pro == PRO_BNGRAD) return run_p1_ek<PC_BNGRAD>(p, g, ek, s, rows);
     if (p.pro == PRO_BNRELU && ek == EK_STATS) return run_p1_nva<EK_STATS, PC_BNRELU>(p, g, s, rows);
     return run_p1_ek<PC_RUNTIME>(p, g, ek, s, rows);

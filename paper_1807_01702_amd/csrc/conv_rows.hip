@@ -24,6 +24,9 @@
 //   PRO_BNRELU_POOL: row = 2x2 window; a = mean over its four pixels of
 //                max(gamma*(x-mean)*rstd + beta, 0)  (1x1 only, general
 //                staging loop)
+//   PRO_BNADDRELU: a = max(gamma*(x-mean)*rstd + beta + r0, 0), r0 the
+//                identity (a2); a is also stored to the side view (1x1 only,
+//                general staging loop, by the first column tile)
 // Epilogues (sub-BN1 side):
 //   EPI_STATS  : store y, per-channel sum(y), sum(y^2) of the stored values
 //   EPI_BNBWD  : dy = dz * [gamma*xhat+beta > 0] with xhat from the BN input,
@@ -97,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     const int arows = BM + 2 * halo;
 
     // per-channel prologue coefficients for all K channels
-    if (p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL) {
+    if (p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL || p.pro == PRO_BNADDRELU) {
         for (int c = tid; c < K; c += kThreads)             // y = x c0 + c1
             bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], coef[K + c], coef[2 * K + c]);
     } else if (p.pro == PRO_BNGRAD) {
@@ -319,6 +322,14 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
                     for (int e = 0; e < VEC; e++) f[e] = f[e] > 0.f ? f[e] : 0.f;
                     out = Elem<T>::pack(f);
+                } else if (p.pro == PRO_BNADDRELU) {
+                    float f[VEC], id[VEC];
+                    Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
+                    Elem<T>::unpack(ldg16(asrc2 + pp * p.a2_ldc + c), id);
+                    for (int e = 0; e < VEC; e++)
+                        f[e] = __builtin_fmaxf(bn_lin(f[e], coef[K + c + e], coef[2 * K + c + e]) + id[e], 0.f);
+                    out = Elem<T>::pack(f);
+                    if (nt == 0) stg16(reinterpret_cast<T *>(p.side) + pp * p.side_ldc + c, out);
                 } else if (p.pro == PRO_BNRELU_POOL) {
                     const int ho = H / 2, wo = W / 2;
                     const int64_t img = pp / ((int64_t)ho * wo);
@@ -528,6 +539,7 @@ static double rows_algorithmic_bytes(const RowsParams &p)
     if (p.pro == PRO_BNGRAD) a = 2.0 * m * K;                    // dy and x
     if (p.pro == PRO_POOLUP) a = m / 4.0 * K;                    // pooled gradient
     if (p.pro == PRO_BNRELU_POOL) a = 4.0 * m * K;               // four input pixels per window
+    if (p.pro == PRO_BNADDRELU) a = 3.0 * m * K;                 // y and the identity read, the result written
     double out = m * N;                                          // output write
     if (p.epi == EPI_STORE && p.accumulate) out += m * N;        // read-modify-write
     if (p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK) out += m * N;   // BN input / ReLU input read
@@ -547,14 +559,16 @@ static bool rows_spans_fit(int dtype, int64_t m, int K, int N, int64_t a_ldc, in
 
 bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro)
 {
-    return dtype == DT_BF16 && taps == 1 && pro != PRO_BNRELU_POOL && rows_spans_fit(dtype, m, K, N, a_ldc, a2_ldc, pro);
+    return dtype == DT_BF16 && taps == 1 && pro != PRO_BNRELU_POOL && pro != PRO_BNADDRELU &&
+           rows_spans_fit(dtype, m, K, N, a_ldc, a2_ldc, pro);
 }
 
 template <typename T, int TAPS, int BM, int BN, int WM, int WN, int SP = SP_RUNTIME>
 static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 {
     using Cfg = RowsCfg<T, TAPS, BM, BN>;
-    const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD || p.pro == PRO_BNRELU_POOL ? 3 : 0;
+    const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD || p.pro == PRO_BNRELU_POOL || p.pro == PRO_BNADDRELU
+                      ? 3 : 0;
     const size_t lds = Cfg::LDS + (size_t)P * p.K * sizeof(float);
     auto kern = k_conv_rows<T, TAPS, BM, BN, WM, WN, SP>;
     static bool attr_set = false;
@@ -567,7 +581,8 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     TraceScope tr(KC_CONV, TAPS == 9 ? KID_CONV_3X3 : KID_CONV_1X1, s, rows_algorithmic_bytes(p),
                   2.0 * (double)p.m * TAPS * p.K * p.N);
     RowsParams q = p;
-    q.buf32 = TAPS == 1 && p.pro != PRO_BNRELU_POOL && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
+    q.buf32 = TAPS == 1 && p.pro != PRO_BNRELU_POOL && p.pro != PRO_BNADDRELU &&
+              rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
     if (q.wdirect && (!q.buf32 || !p.wraw)) return hipErrorInvalidValue;   // unpacked weights need this path
     if (SP == SP_FWD_BNRELU && (!q.wdirect || p.wtrans || p.pro != PRO_BNRELU)) return hipErrorInvalidValue;
     if (SP == SP_DGRAD_BNGRAD && (!q.wdirect || !p.wtrans || p.pro != PRO_BNGRAD)) return hipErrorInvalidValue;
@@ -579,7 +594,10 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 static bool rows_operands_ok(const RowsParams &p)
 {
     if (!p.a || !(p.wdirect ? p.wraw : p.wpack) || !p.y) return false;
-    if ((p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL) && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta))
+    if ((p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL || p.pro == PRO_BNADDRELU) && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta))
+        return false;
+    if (p.pro == PRO_BNADDRELU && (p.taps != 1 || !p.a2 || !p.side || p.wtrans || p.epi == EPI_BNBWD ||
+                                   p.epi == EPI_RELUMASK))
         return false;
     if (p.pro == PRO_BNRELU_POOL && (p.taps != 1 || p.h % 2 || p.w % 2 || (int64_t)p.n * p.h * p.w != 4 * p.m ||
                                      p.wtrans || p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK))

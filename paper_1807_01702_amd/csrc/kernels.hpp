@@ -71,7 +71,12 @@ hipError_t launch_sum_partials(const float *part, int64_t S, int64_t len, float 
 // even; m = n h w / 4 rows); a row is the average of relu(bn(x)) over its
 // window's four pixels (BN, ReLU and the transition's average pooling applied
 // before the linear 1x1 CONV)
-enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 4, PRO_BNRELU_POOL = 5 };
+// PRO_BNADDRELU: a = max(gamma (x - mean) rstd + beta + r0, 0) with x the
+// residual branch's last CONV output and r0 (a2) the block's identity input;
+// a is also stored to the side view (the next block's identity and the
+// backward's ReLU operand)
+enum { PRO_NONE = 0, PRO_BNRELU = 1, PRO_BNGRAD = 2, PRO_POOLUP = 3, PRO_RELU = 4, PRO_BNRELU_POOL = 5,
+       PRO_BNADDRELU = 6 };
 enum { EPI_STORE = 0, EPI_STATS = 1, EPI_BNBWD = 2, EPI_RELUMASK = 3 };
 // Compile-time epilogue kinds of the persistent CONV kernels (EPI_STORE splits
 // into plain store and read-add-store).
@@ -109,6 +114,8 @@ struct RowsParams {
     int64_t ex_ldc;
     const float *e_gamma, *e_beta, *e_mean, *e_rstd;
     const float *e_shift;         // EPI_STATS: the sums are of (y - e_shift) (NULL: 0)
+    void *side;                   // PRO_BNADDRELU: the transformed A rows are stored here too
+    int64_t side_ldc;
     int buf32;                    // tiled 1x1 kernel: operand spans below 2^31 bytes (set by its launcher)
     int wdirect;                  // tiled bf16 1x1 kernel: weights read from wraw ([k][n], wtrans: [n][k]), no packing
 };

@@ -596,9 +596,11 @@ class ResNetStack:
 
     Fused: every BN's statistics come from the epilogue of the CONV that
     produces its input; BN1/BN2 + ReLU run in the next CONV's prologue; the
-    last BN of a block is followed by the residual addition, so it runs with
-    the addition and the ReLU as one element-wise sweep, and its input
-    gradient is consumed deferred by the third CONV's backward.  Unfused: the
+    last BN of a block, the residual addition and the ReLU run in the
+    prologue of the next block's first CONV, which also writes their result
+    (the next block's identity); only the last block of the stack runs them
+    as one element-wise sweep.  BN3's input gradient is consumed deferred by
+    the third CONV's backward.  Unfused: the
     reference chain (two-pass statistics, materialised normalised / ReLU
     tensors and gradients)."""
 
@@ -644,13 +646,19 @@ class ResNetStack:
             self.dzw = torch.empty_like(self.dyw)
 
     def forward(self):
-        for b in self.blocks:
+        for i, b in enumerate(self.blocks):
             u2, u3 = b["u2"], b["u3"]
             if self.fused:
-                B.bnr_conv_bn_stats_fwd(b["desc1"], b["xin"], b["w1"], b["y1"], u2.bn)
+                if i == 0:
+                    B.bnr_conv_bn_stats_fwd(b["desc1"], b["xin"], b["w1"], b["y1"], u2.bn)
+                else:                          # the previous block's BN3 + identity + ReLU on load
+                    pb = self.blocks[i - 1]
+                    B.bnr_bn_add_relu_conv_fwd(b["desc1"], pb["y3"], pb["bn3"], pb["xin"], pb["out"], b["w1"],
+                                               b["y1"], u2.bn)
                 B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out, u3.bn)
                 B.bnr_bn_relu_conv_fwd(u3.desc, u3.x, u3.bn, u3.wt, u3.out, b["bn3"])
-                B.bnr_bn_add_relu_fwd(b["y3"], b["bn3"], b["xin"], b["out"])
+                if i == len(self.blocks) - 1:
+                    B.bnr_bn_add_relu_fwd(b["y3"], b["bn3"], b["xin"], b["out"])
             else:
                 B.bnr_conv_fwd(b["desc1"], b["xin"], b["w1"], b["y1"])
                 u2.ref_fwd()

@@ -199,6 +199,48 @@ def test_bn_relu_conv_pool_fwd(B, case, stats):
         assert_stats("pooled output stats", host(ybn.mean), host(ybn.var), mr, vr, RTOL[bf16])
 
 
+# ----------------------------- residual boundary: BN-add-ReLU-CONV ----
+@pytest.mark.parametrize("case", [
+    # dtype, n, h, w, c (y, identity, r), c_out, r_ldc
+    (True, 2, 14, 14, 256, 64, 256),        # ResNet-50 conv2_x block boundary (persistent 1x1 kernel)
+    (True, 1, 9, 11, 136, 40, 144),         # ragged pixels and channels, r into a wider view
+    (False, 2, 5, 6, 24, 16, 24),           # fp32 (tiled kernel)
+])
+def test_bn_add_relu_conv_fwd(B, case):
+    """r = relu(bn(y) + identity) formed while the next block's first CONV
+    reads y and the identity, written as a side output, and out = conv(r)
+    with statistics: r equals the standalone element-wise pass bit for bit,
+    out and its statistics match the oracle."""
+    bf16, n, h, w, c, co, rldc = case
+    rnd = P.round_bf16 if bf16 else (lambda a: np.asarray(a, np.float64))
+    yf = synth.normal(12, "y", (n, h, w, c), bf16=bf16) * np.float32(1.3)
+    yf = synth.round_to_bf16(yf) if bf16 else yf
+    idf = synth.normal(12, "id", (n, h, w, c), bf16=bf16)
+    wt = synth.conv_weight(12, "w", 1, c, co, bf16)
+    bp = synth.bn_params(12, "bn", c)
+    y, ident = dev(yf, bf16), dev(idf, bf16)
+    ybn = _bn_dev(bp["gamma"], bp["beta"])
+    B.bnr_bn_stats(y, ybn)
+    rbuf = torch.zeros((n, h, w, rldc), dtype=y.dtype, device=y.device)
+    out = torch.empty((n, h, w, co), dtype=y.dtype, device=y.device)
+    obn = B.BN.stats_only(co, y.device)
+    desc = B.desc_for(y, out, 1, n, h, w)
+    B.bnr_bn_add_relu_conv_fwd(desc, y, ybn, ident, rbuf[..., :c], dev(wt, bf16), out, obn)
+    r_ew = torch.empty_like(y)
+    B.bnr_bn_add_relu_fwd(y, ybn, ident, r_ew)
+    torch.cuda.synchronize()
+    assert torch.equal(rbuf[..., :c], r_ew), "side output differs from the element-wise pass"
+    assert np.all(host(rbuf[..., c:]) == 0), "wrote outside the side view"
+    yr, _, _, _ = P.bn_fwd(yf.astype(np.float64), bp["gamma"], bp["beta"], 1e-5)
+    r_r = rnd(P.relu_fwd(yr + idf.astype(np.float64)))
+    amb = relu_ambiguous(yr + idf.astype(np.float64), bf16)
+    assert_close("r", host(rbuf[..., :c]), r_r, RTOL[bf16], exclude=amb)
+    out_r = rnd(P.conv_fwd(host(r_ew), wt.astype(np.float64)))
+    assert_close("out", host(out), out_r, RTOL[bf16])
+    mr, vr, _ = P.bn_stats(out_r, 1e-5)
+    assert_stats("out stats", host(obn.mean), host(obn.var), mr, vr, RTOL[bf16])
+
+
 # -------------------------------------------------------- fused backward ----
 BWD_CASES = [
     (False, 1, 8, 8, 8, 64, 32),
