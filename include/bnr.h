@@ -108,6 +108,19 @@ typedef struct {
     float *running_mean;   /* [C] or NULL                                          */
     float *running_var;    /* [C] or NULL                                          */
     float momentum;        /* in [0, 1]                                            */
+    /* Low part of the mean (optional).  When set, every statistics producer
+     * also writes mean_lo = mean64 - mean, the float32 rounding of what the
+     * float32 mean drops from the float64 value it was rounded from, and every
+     * consumer of float32 data normalises the centred value x - mean with it:
+     * y = (x - mean) c0 + beta - mean_lo c0 (c0 = gamma rstd), xhat and the
+     * deferred input gradient alike.  The plain form x c0 + beta - mean c0
+     * loses |mean| 2^-24 through the float32 mean and product, above 1e-4 of
+     * the normalised value once |mean| / std reaches about 10^3; x - mean is
+     * exact there (the operands are within a factor of two), so the centred
+     * form keeps float32 accuracy at any offset.  bf16 consumers use mean
+     * alone (the storage itself carries |x| 2^-9).  The same BN arrays must
+     * reach every consumer of one tensor (forward, ReLU mask, recompute). */
+    float *mean_lo;        /* [C] or NULL                                          */
 } bnr_bn;
 
 /* Where the gradient of a CONV's output comes from (backward entry points). */

@@ -38,7 +38,8 @@ class ConvDesc(ctypes.Structure):
 
 class BNStruct(ctypes.Structure):
     _fields_ = [("gamma", c_vp), ("beta", c_vp), ("mean", c_vp), ("var", c_vp), ("rstd", c_vp), ("eps", c_f),
-                ("shift", c_vp), ("running_mean", c_vp), ("running_var", c_vp), ("momentum", c_f)]
+                ("shift", c_vp), ("running_mean", c_vp), ("running_var", c_vp), ("momentum", c_f),
+                ("mean_lo", c_vp)]
 
 
 class GradSrc(ctypes.Structure):
@@ -217,9 +218,11 @@ class BN:
     Optional robust one-sweep statistics: ``shift`` (per-channel K: the
     one-sweep producers sum x - K and (x - K)^2) and running statistics
     (``running_mean``, ``running_var``, ``momentum``) updated by the producer;
-    set them with :meth:`robust`."""
+    set them with :meth:`robust`, which also allocates ``mean_lo`` (the low
+    part of the float64 mean, written by the producers; float32 consumers
+    normalise (x - mean) - mean_lo with it)."""
 
-    shift = running_mean = running_var = None
+    shift = running_mean = running_var = mean_lo = None
     momentum = 0.0
 
     def __init__(self, gamma, beta, eps=1e-5, mean=None, var=None, rstd=None):
@@ -233,6 +236,7 @@ class BN:
         """Sum around shift (may be running_mean itself) and/or update running statistics; returns self."""
         self.shift, self.running_mean, self.running_var = shift, running_mean, running_var
         self.momentum = float(momentum)
+        self.mean_lo = torch.empty_like(self.mean)
         return self
 
     @classmethod
@@ -259,7 +263,7 @@ class BN:
     def struct(self):
         return BNStruct(_ptr(self.gamma), _ptr(self.beta), _ptr(self.mean), _ptr(self.var), _ptr(self.rstd),
                         self.eps, _ptr(self.shift), _ptr(self.running_mean), _ptr(self.running_var),
-                        self.momentum)
+                        self.momentum, _ptr(self.mean_lo))
 
 
 def conv_desc(n, h, w, c_in, c_out, k, in_ldc, out_ldc, dtype):

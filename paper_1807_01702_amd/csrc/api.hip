@@ -106,8 +106,12 @@ bnr_status check_bn(const bnr_bn *bn, const char *name, bool need_affine, bool n
     if (need_stats_out && !(bn->eps > 0.0f)) return fail(BNR_ERR_SHAPE, "%s.eps must be > 0", name);
     if (need_stats_out) {
         const auto mis = [](const void *q) { return reinterpret_cast<uintptr_t>(q) % 4 != 0; };
-        if (mis(bn->shift) || mis(bn->running_mean) || mis(bn->running_var))
-            return fail(BNR_ERR_ALIGN, "%s shift / running statistics misaligned", name);
+        if (mis(bn->shift) || mis(bn->running_mean) || mis(bn->running_var) || mis(bn->mean_lo))
+            return fail(BNR_ERR_ALIGN, "%s shift / running statistics / mean_lo misaligned", name);
+        const float *mr = bn->mean_lo;
+        if (mr && (mr == bn->mean || mr == bn->shift || mr == bn->var || mr == bn->rstd || mr == bn->running_mean ||
+                   mr == bn->running_var))
+            return fail(BNR_ERR_ALIAS, "%s.mean_lo aliases another array of the BN", name);
         if (bn->running_var && !bn->running_mean)
             return fail(BNR_ERR_NULL, "%s.running_var set without running_mean", name);
         if (bn->running_mean && !(bn->momentum >= 0.0f && bn->momentum <= 1.0f))
@@ -121,8 +125,25 @@ bnr_status check_bn(const bnr_bn *bn, const char *name, bool need_affine, bool n
 SplitTerms fwd_terms(const bnr_bn *bn, bool one_sweep)
 {
     SplitTerms t{nullptr, nullptr, nullptr, nullptr, 0, one_sweep ? bn->shift : nullptr, bn->running_mean,
-                 bn->running_var, bn->momentum};
+                 bn->running_var, bn->momentum, one_sweep ? bn->mean_lo : nullptr};
     return t;
+}
+
+// terms of a two-pass mean combine (FIN_MEAN): the low part of the mean
+SplitTerms mean_terms(const bnr_bn *bn)
+{
+    SplitTerms t{nullptr, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0.f, bn->mean_lo};
+    return t;
+}
+
+// The mean a consumer of bn's input is given and the centre it subtracts from
+// the input first (bn_centre): float32 data with mean_lo set is normalised as
+// (x - mean) - mean_lo, everything else as x - mean.
+struct Centred { const float *mean, *ctr; };
+Centred centred(const bnr_bn *bn, int dtype)
+{
+    if (dtype == DT_F32 && bn->mean_lo) return Centred{bn->mean_lo, bn->mean};
+    return Centred{bn->mean, nullptr};
 }
 
 bnr_status check_desc(const bnr_conv_desc *d)
@@ -333,7 +354,11 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     rp.pro = x_bn ? (pool ? PRO_BNRELU_POOL : PRO_BNRELU) : PRO_NONE;
     rp.m = my;
     rp.a = x; rp.a_ldc = d->in_ldc;
-    if (x_bn) { rp.p_gamma = x_bn->gamma; rp.p_beta = x_bn->beta; rp.p_mean = x_bn->mean; rp.p_rstd = x_bn->rstd; }
+    if (x_bn) {
+        const Centred cx = centred(x_bn, rp.dtype);
+        rp.p_gamma = x_bn->gamma; rp.p_beta = x_bn->beta; rp.p_mean = cx.mean; rp.p_rstd = x_bn->rstd;
+        rp.p_ctr = cx.ctr;
+    }
     rp.epi = y_bn ? EPI_STATS : EPI_STORE;
     rp.y = y; rp.y_ldc = d->out_ldc;
     rp.part = part;
@@ -494,7 +519,9 @@ bnr_status bnr_bn_add_relu_conv_fwd(const bnr_conv_desc *d, const void *y, const
     rp.pro = PRO_BNADDRELU;
     rp.a = y; rp.a_ldc = d->in_ldc;
     rp.a2 = ident; rp.a2_ldc = ident_ldc;
-    rp.p_gamma = y_bn->gamma; rp.p_beta = y_bn->beta; rp.p_mean = y_bn->mean; rp.p_rstd = y_bn->rstd;
+    const Centred cy = centred(y_bn, rp.dtype);
+    rp.p_gamma = y_bn->gamma; rp.p_beta = y_bn->beta; rp.p_mean = cy.mean; rp.p_rstd = y_bn->rstd;
+    rp.p_ctr = cy.ctr;
     rp.side = r; rp.side_ldc = r_ldc;
     rp.epi = out_bn ? EPI_STATS : EPI_STORE;
     rp.y = out; rp.y_ldc = d->out_ldc;
@@ -583,11 +610,14 @@ static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn 
         rp.pro = PRO_NONE; rp.a = g->g; rp.a_ldc = g->g_ldc;
     } else if (g->kind == BNR_GRAD_BN) {
         rp.pro = PRO_BNGRAD; rp.a = g->dy; rp.a_ldc = d->c_out; rp.a2 = g->x; rp.a2_ldc = g->x_ldc;
-        rp.p_gamma = g->bn->gamma; rp.p_mean = g->bn->mean; rp.p_rstd = g->bn->rstd;
+        const Centred cg = centred(g->bn, rp.dtype);
+        rp.p_gamma = g->bn->gamma; rp.p_mean = cg.mean; rp.p_rstd = g->bn->rstd; rp.p_ctr = cg.ctr;
         rp.p_dgamma = g->dgamma; rp.p_dbeta = g->dbeta;
     } else if (g->kind == BNR_GRAD_SPLIT) {
         rp.pro = PRO_BNGRAD; rp.p_split = 1; rp.a = g->g; rp.a_ldc = g->g_ldc; rp.a2 = g->x; rp.a2_ldc = g->x_ldc;
-        rp.p_mean = g->bn->mean; rp.p_rstd = g->bn->rstd; rp.p_alpha = g->alpha; rp.p_betap = g->betap;
+        const Centred cg = centred(g->bn, rp.dtype);
+        rp.p_mean = cg.mean; rp.p_rstd = g->bn->rstd; rp.p_alpha = g->alpha; rp.p_betap = g->betap;
+        rp.p_ctr = cg.ctr;
     } else {
         rp.pro = PRO_POOLUP; rp.a = g->g; rp.a_ldc = g->g_ldc;
     }
@@ -595,7 +625,9 @@ static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn 
         rp.epi = EPI_BNBWD; rp.y = y; rp.y_ldc = y_ldc; rp.part = cp.part;
         rp.e_scale = y_scale; rp.accumulate = y_scale && y_acc ? 1 : 0;
         rp.ex = x; rp.ex_ldc = d->in_ldc;
-        rp.e_gamma = x_bn->gamma; rp.e_beta = x_bn->beta; rp.e_mean = x_bn->mean; rp.e_rstd = x_bn->rstd;
+        const Centred cx = centred(x_bn, rp.dtype);
+        rp.e_gamma = x_bn->gamma; rp.e_beta = x_bn->beta; rp.e_mean = cx.mean; rp.e_rstd = x_bn->rstd;
+        rp.e_ctr = cx.ctr;
     } else {
         rp.epi = EPI_STORE; rp.y = y; rp.y_ldc = y_ldc; rp.accumulate = y_acc ? 1 : 0;
     }
@@ -617,17 +649,22 @@ static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn 
     wp.x = x; wp.x_ldc = d->in_ldc;
     if (x_bn) {
         wp.a_mode = 1;
-        wp.a_gamma = x_bn->gamma; wp.a_beta = x_bn->beta; wp.a_mean = x_bn->mean; wp.a_rstd = x_bn->rstd;
+        const Centred cx = centred(x_bn, dt);
+        wp.a_gamma = x_bn->gamma; wp.a_beta = x_bn->beta; wp.a_mean = cx.mean; wp.a_rstd = x_bn->rstd;
+        wp.a_ctr = cx.ctr;
     }
     if (g->kind == BNR_GRAD_DENSE) {
         wp.gsrc = GB_DENSE; wp.g = g->g; wp.g_ldc = g->g_ldc;
     } else if (g->kind == BNR_GRAD_BN) {
+        const Centred cg = centred(g->bn, dt);
         wp.gsrc = GB_BNGRAD; wp.g = g->dy; wp.g_ldc = d->c_out; wp.gx = g->x; wp.gx_ldc = g->x_ldc;
-        wp.g_gamma = g->bn->gamma; wp.g_mean = g->bn->mean; wp.g_rstd = g->bn->rstd;
+        wp.g_gamma = g->bn->gamma; wp.g_mean = cg.mean; wp.g_rstd = g->bn->rstd; wp.g_ctr = cg.ctr;
         wp.g_dgamma = g->dgamma; wp.g_dbeta = g->dbeta;
     } else if (g->kind == BNR_GRAD_SPLIT) {
+        const Centred cg = centred(g->bn, dt);
         wp.gsrc = GB_BNGRAD; wp.g_split = 1; wp.g = g->g; wp.g_ldc = g->g_ldc; wp.gx = g->x; wp.gx_ldc = g->x_ldc;
-        wp.g_mean = g->bn->mean; wp.g_rstd = g->bn->rstd; wp.g_alpha = g->alpha; wp.g_betap = g->betap;
+        wp.g_mean = cg.mean; wp.g_rstd = g->bn->rstd; wp.g_alpha = g->alpha; wp.g_betap = g->betap;
+        wp.g_ctr = cg.ctr;
     } else {
         wp.gsrc = GB_POOLUP; wp.g = g->g; wp.g_ldc = g->g_ldc;
     }
@@ -711,8 +748,9 @@ static bnr_status bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn 
     else TRY(bwd_steps(d, x, nullptr, w, g, dw, nullptr, nullptr, dx, dx_ldc, 0, dx_accumulate, nullptr, ws, s, parts));
     // 4. optional standalone BN input gradient
     if ((parts & BWD_DATA) && x_bn && dx) {
+        const Centred cx = centred(x_bn, dt_of(d->dtype));
         TRY_HIP(launch_elementwise(dt_of(d->dtype), EW_DX, m, d->c_in, dy, d->c_in, x, d->in_ldc, x_bn->gamma, nullptr,
-                                   x_bn->mean, x_bn->rstd, dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, s),
+                                   cx.mean, x_bn->rstd, dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, s, cx.ctr),
                 "BN input gradient");
     }
     return ok();
@@ -817,8 +855,9 @@ bnr_status bnr_split_dx(int64_t m, int32_t c, bnr_dtype dtype, const void *gsum,
     if (overlap(rdx, view_range(x, m, c, x_ldc, es))) return fail(BNR_ERR_ALIAS, "dx overlaps x");
     if (overlap(rdx, view_range(gsum, m, c, gsum_ldc, es)) && !(gsum == dx && dx_ldc == gsum_ldc && !dx_accumulate))
         return fail(BNR_ERR_ALIAS, "dx overlaps gsum");
-    TRY_HIP(launch_elementwise(dt_of(dtype), EW_SPLITDX, m, c, gsum, gsum_ldc, x, x_ldc, nullptr, nullptr, bn->mean,
-                               bn->rstd, betap, alpha, dx, dx_ldc, dx_accumulate ? 1 : 0, (hipStream_t)stream),
+    const Centred cx = centred(bn, dt_of(dtype));
+    TRY_HIP(launch_elementwise(dt_of(dtype), EW_SPLITDX, m, c, gsum, gsum_ldc, x, x_ldc, nullptr, nullptr, cx.mean,
+                               bn->rstd, betap, alpha, dx, dx_ldc, dx_accumulate ? 1 : 0, (hipStream_t)stream, cx.ctr),
             "summed BN input gradient");
     return ok();
 }
@@ -844,8 +883,9 @@ bnr_status bnr_bn_dx(int64_t m, int32_t c, bnr_dtype dtype, const void *dy, cons
     const Range rdy = view_range(dy, m, c, c, es);
     if (overlap(rdx, rdy) && !(dy == dx && dx_ldc == c && !dx_accumulate))
         return fail(BNR_ERR_ALIAS, "dx overlaps dy");
-    TRY_HIP(launch_elementwise(dt_of(dtype), EW_DX, m, c, dy, c, x, x_ldc, bn->gamma, nullptr, bn->mean, bn->rstd,
-                               dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, (hipStream_t)stream),
+    const Centred cx = centred(bn, dt_of(dtype));
+    TRY_HIP(launch_elementwise(dt_of(dtype), EW_DX, m, c, dy, c, x, x_ldc, bn->gamma, nullptr, cx.mean, bn->rstd,
+                               dgamma, dbeta, dx, dx_ldc, dx_accumulate ? 1 : 0, (hipStream_t)stream, cx.ctr),
             "BN input gradient");
     return ok();
 }
@@ -890,16 +930,18 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
             // mean sweep, then variance sweep (two-pass, as the unfused BN layer)
             TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SUM, nullptr, nullptr, nullptr, 0, part,
                                          R, s), "mean sweep");
+            const SplitTerms mt = mean_terms(bn);
             TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_MEAN, bn->eps, bn->mean, nullptr, nullptr, nullptr,
-                                          nullptr, red, s), "mean combine");
+                                          nullptr, red, s, &mt), "mean combine");
             TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_SQDEV, bn->mean, nullptr, nullptr, 0,
                                          part, R, s), "variance sweep");
             const SplitTerms ft = fwd_terms(bn, false);
             TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_VAR, bn->eps, bn->mean, bn->var, bn->rstd, nullptr,
                                           nullptr, red, s, &ft), "variance combine");
         }
+        const Centred cx = centred(bn, dt);
         TRY_HIP(launch_elementwise(dt, EW_APPLY, m, d->c_in, a->x, d->in_ldc, nullptr, 0, bn->gamma, bn->beta,
-                                   bn->mean, bn->rstd, nullptr, nullptr, a->y, d->c_in, 0, s), "normalise");
+                                   cx.mean, bn->rstd, nullptr, nullptr, a->y, d->c_in, 0, s, cx.ctr), "normalise");
         if (base)
             TRY_HIP(launch_elementwise(dt, EW_RELU, m, d->c_in, a->y, d->c_in, nullptr, 0, nullptr, nullptr, nullptr,
                                        nullptr, nullptr, nullptr, a->z, d->c_in, 0, s), "relu");
@@ -948,13 +990,14 @@ bnr_status bnr_reference_path(bnr_ref_mode mode, int32_t backward, const bnr_con
         TRY_HIP(launch_elementwise(dt, EW_RELUBWD, m, d->c_in, a->dz, d->c_in, a->y, d->c_in, nullptr, nullptr, nullptr,
                                    nullptr, nullptr, nullptr, a->dy, d->c_in, 0, s), "relu backward");
     const int64_t R = stats_row_blocks(m, d->c_in, dt);
-    TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_DYX, bn->mean, bn->rstd, a->dy, d->c_in, part, R,
-                                 s), "BN backward sums sweep");
+    const Centred cx = centred(bn, dt);
+    TRY_HIP(launch_stats_partial(dt, a->x, d->in_ldc, m, d->c_in, ST_DYX, cx.mean, bn->rstd, a->dy, d->c_in, part, R,
+                                 s, cx.ctr), "BN backward sums sweep");
     TRY_HIP(launch_stats_finalize(part, R, d->c_in, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma,
                                   red, s),
             "BN backward sums combine");
-    TRY_HIP(launch_elementwise(dt, EW_DX, m, d->c_in, a->dy, d->c_in, a->x, d->in_ldc, bn->gamma, nullptr, bn->mean,
-                               bn->rstd, a->dgamma, a->dbeta, a->dx, a->dx_ldc, a->dx_accumulate ? 1 : 0, s),
+    TRY_HIP(launch_elementwise(dt, EW_DX, m, d->c_in, a->dy, d->c_in, a->x, d->in_ldc, bn->gamma, nullptr, cx.mean,
+                               bn->rstd, a->dgamma, a->dbeta, a->dx, a->dx_ldc, a->dx_accumulate ? 1 : 0, s, cx.ctr),
             "BN input gradient");
     return ok();
 }
@@ -989,8 +1032,9 @@ bnr_status bnr_bn_add_relu_fwd(int64_t m, int32_t c, bnr_dtype dtype, const void
     if (overlap(ro, view_range(y, m, c, y_ldc, es))) return fail(BNR_ERR_ALIAS, "out overlaps y");
     if (overlap(ro, view_range(id, m, c, id_ldc, es)) && !(out == id && out_ldc == id_ldc))
         return fail(BNR_ERR_ALIAS, "out overlaps id");
-    TRY_HIP(launch_elementwise(dt_of(dtype), EW_BNADDRELU, m, c, y, y_ldc, id, id_ldc, bn->gamma, bn->beta, bn->mean,
-                               bn->rstd, nullptr, nullptr, out, out_ldc, 0, (hipStream_t)stream),
+    const Centred cy = centred(bn, dt_of(dtype));
+    TRY_HIP(launch_elementwise(dt_of(dtype), EW_BNADDRELU, m, c, y, y_ldc, id, id_ldc, bn->gamma, bn->beta, cy.mean,
+                               bn->rstd, nullptr, nullptr, out, out_ldc, 0, (hipStream_t)stream, cy.ctr),
             "BN + add + ReLU");
     return ok();
 }
@@ -1023,7 +1067,9 @@ bnr_status bnr_bn_add_relu_bwd(int64_t m, int32_t c, bnr_dtype dtype, const void
     const int64_t R = stats_row_blocks(m, c, dt);
     float *part = (float *)ws;
     void *red = (char *)ws + stats_part_bytes(m, c);
-    TRY_HIP(launch_addrelu_bwd(dt, m, c, g, g_ldc, out, out_ldc, y, y_ldc, bn->mean, bn->rstd, gm, gm_ldc, part, R, s),
+    const Centred cy = centred(bn, dt);
+    TRY_HIP(launch_addrelu_bwd(dt, m, c, g, g_ldc, out, out_ldc, y, y_ldc, cy.mean, bn->rstd, gm, gm_ldc, part, R, s,
+                               cy.ctr),
             "ReLU mask + BN backward sums");
     TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, dbeta, dgamma, red, s),
             "backward sums combine");
@@ -1054,15 +1100,17 @@ bnr_status bnr_reference_bn_add_relu(int32_t backward, int64_t m, int32_t c, bnr
         // two-pass statistics, normalise (write tmp), add + ReLU (write out)
         TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_SUM, nullptr, nullptr, nullptr, 0, part, R, s),
                 "mean sweep");
+        const SplitTerms mt = mean_terms(bn);
         TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MEAN, bn->eps, bn->mean, nullptr, nullptr, nullptr, nullptr,
-                                      red, s), "mean combine");
+                                      red, s, &mt), "mean combine");
         TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_SQDEV, bn->mean, nullptr, nullptr, 0, part, R, s),
                 "variance sweep");
         const SplitTerms ft = fwd_terms(bn, false);
         TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr,
                                       red, s, &ft), "variance combine");
-        TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->y, a->y_ldc, nullptr, 0, bn->gamma, bn->beta, bn->mean,
-                                   bn->rstd, nullptr, nullptr, a->tmp, c, 0, s), "normalise");
+        const Centred cy = centred(bn, dt);
+        TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->y, a->y_ldc, nullptr, 0, bn->gamma, bn->beta, cy.mean,
+                                   bn->rstd, nullptr, nullptr, a->tmp, c, 0, s, cy.ctr), "normalise");
         TRY_HIP(launch_elementwise(dt, EW_ADDRELU, m, c, a->tmp, c, a->id, a->id_ldc, nullptr, nullptr, nullptr,
                                    nullptr, nullptr, nullptr, a->out, a->out_ldc, 0, s), "add + ReLU");
         return ok();
@@ -1078,12 +1126,13 @@ bnr_status bnr_reference_bn_add_relu(int32_t backward, int64_t m, int32_t c, bnr
     // ReLU backward (write gm), BN reductions sweep, BN input-gradient sweep (write dx)
     TRY_HIP(launch_elementwise(dt, EW_RELUBWD, m, c, a->g, a->g_ldc, a->out, a->out_ldc, nullptr, nullptr, nullptr,
                                nullptr, nullptr, nullptr, a->gm, c, 0, s), "ReLU backward");
-    TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_DYX, bn->mean, bn->rstd, a->gm, c, part, R, s),
+    const Centred cy = centred(bn, dt);
+    TRY_HIP(launch_stats_partial(dt, a->y, a->y_ldc, m, c, ST_DYX, cy.mean, bn->rstd, a->gm, c, part, R, s, cy.ctr),
             "BN backward sums");
     TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma, red, s),
             "backward sums combine");
-    TRY_HIP(launch_elementwise(dt, EW_DX, m, c, a->gm, c, a->y, a->y_ldc, bn->gamma, nullptr, bn->mean, bn->rstd,
-                               a->dgamma, a->dbeta, a->dx, a->dx_ldc, 0, s), "BN input gradient");
+    TRY_HIP(launch_elementwise(dt, EW_DX, m, c, a->gm, c, a->y, a->y_ldc, bn->gamma, nullptr, cy.mean, bn->rstd,
+                               a->dgamma, a->dbeta, a->dx, a->dx_ldc, 0, s, cy.ctr), "BN input gradient");
     return ok();
 }
 
@@ -1113,15 +1162,17 @@ bnr_status bnr_reference_bn_relu(int32_t backward, int64_t m, int32_t c, bnr_dty
         // two-pass statistics, normalise (write y), ReLU (write z)
         TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_SUM, nullptr, nullptr, nullptr, 0, part, R, s),
                 "mean sweep");
+        const SplitTerms mt = mean_terms(bn);
         TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_MEAN, bn->eps, bn->mean, nullptr, nullptr, nullptr, nullptr,
-                                      red, s), "mean combine");
+                                      red, s, &mt), "mean combine");
         TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_SQDEV, bn->mean, nullptr, nullptr, 0, part, R, s),
                 "variance sweep");
         const SplitTerms ft = fwd_terms(bn, false);
         TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_VAR, bn->eps, bn->mean, bn->var, bn->rstd, nullptr, nullptr,
                                       red, s, &ft), "variance combine");
-        TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->x, a->x_ldc, nullptr, 0, bn->gamma, bn->beta, bn->mean,
-                                   bn->rstd, nullptr, nullptr, a->y, c, 0, s), "normalise");
+        const Centred cx = centred(bn, dt);
+        TRY_HIP(launch_elementwise(dt, EW_APPLY, m, c, a->x, a->x_ldc, nullptr, 0, bn->gamma, bn->beta, cx.mean,
+                                   bn->rstd, nullptr, nullptr, a->y, c, 0, s, cx.ctr), "normalise");
         TRY_HIP(launch_elementwise(dt, EW_RELU, m, c, a->y, c, nullptr, 0, nullptr, nullptr, nullptr, nullptr, nullptr,
                                    nullptr, a->z, c, 0, s), "ReLU");
         return ok();
@@ -1140,12 +1191,13 @@ bnr_status bnr_reference_bn_relu(int32_t backward, int64_t m, int32_t c, bnr_dty
     // ReLU backward (write dy), BN reductions sweep, BN input-gradient sweep (write dx)
     TRY_HIP(launch_elementwise(dt, EW_RELUBWD, m, c, a->gz, a->gz_ldc, a->y, c, nullptr, nullptr, nullptr, nullptr,
                                nullptr, nullptr, a->dy, c, 0, s), "ReLU backward");
-    TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_DYX, bn->mean, bn->rstd, a->dy, c, part, R, s),
+    const Centred cx = centred(bn, dt);
+    TRY_HIP(launch_stats_partial(dt, a->x, a->x_ldc, m, c, ST_DYX, cx.mean, bn->rstd, a->dy, c, part, R, s, cx.ctr),
             "BN backward sums");
     TRY_HIP(launch_stats_finalize(part, R, c, m, FIN_BWD, 0.f, nullptr, nullptr, nullptr, a->dbeta, a->dgamma, red, s),
             "backward sums combine");
-    TRY_HIP(launch_elementwise(dt, EW_DX, m, c, a->dy, c, a->x, a->x_ldc, bn->gamma, nullptr, bn->mean, bn->rstd,
-                               a->dgamma, a->dbeta, a->dx, a->dx_ldc, 0, s), "BN input gradient");
+    TRY_HIP(launch_elementwise(dt, EW_DX, m, c, a->dy, c, a->x, a->x_ldc, bn->gamma, nullptr, cx.mean, bn->rstd,
+                               a->dgamma, a->dbeta, a->dx, a->dx_ldc, 0, s, cx.ctr), "BN input gradient");
     return ok();
 }
 
@@ -1248,13 +1300,14 @@ bnr_status check_head(int n, int h, int w, int c, int classes, bnr_dtype dtype, 
     return BNR_OK;
 }
 
-void head_params(HeadParams &p, int n, int h, int w, int c, int classes, const void *x, int x_ldc, const bnr_bn *bn,
-                 const void *wfc)
+void head_params(HeadParams &p, int dt, int n, int h, int w, int c, int classes, const void *x, int x_ldc,
+                 const bnr_bn *bn, const void *wfc)
 {
     memset(&p, 0, sizeof p);
     p.n = n; p.h = h; p.w = w; p.c = c; p.classes = classes;
     p.x = x; p.x_ldc = x_ldc;
-    p.gamma = bn->gamma; p.beta = bn->beta; p.mean = bn->mean; p.rstd = bn->rstd;
+    const Centred cx = centred(bn, dt);
+    p.gamma = bn->gamma; p.beta = bn->beta; p.mean = cx.mean; p.rstd = bn->rstd; p.ctr = cx.ctr;
     p.wfc = wfc;
 }
 
@@ -1331,7 +1384,8 @@ bnr_status bnr_stem_wgrad(const bnr_stem_desc *d, const void *img, const bnr_gra
         p.g_ldc = kStemCout;
         p.gx = g->x;
         p.gx_ldc = g->x_ldc;
-        p.g_gamma = g->bn->gamma; p.g_mean = g->bn->mean; p.g_rstd = g->bn->rstd;
+        const Centred cg = centred(g->bn, dt_of(d->dtype));
+        p.g_gamma = g->bn->gamma; p.g_mean = cg.mean; p.g_rstd = g->bn->rstd; p.g_ctr = cg.ctr;
         p.g_dgamma = g->dgamma; p.g_dbeta = g->dbeta;
     } else {
         return fail(BNR_ERR_UNSUPPORTED, "gradient kind %d (first CONV: dense or BN)", (int)g->kind);
@@ -1384,7 +1438,10 @@ bnr_status bnr_bn_relu_maxpool_fwd(int32_t n, int32_t h, int32_t w, int32_t c, b
     if (overlap(view_range(y, m_out, c, y_ldc, es), view_range(x, m, c, x_ldc, es)))
         return fail(BNR_ERR_ALIAS, "y overlaps x");
     p.x = x; p.x_ldc = x_ldc; p.y = y; p.y_ldc = y_ldc;
-    if (x_bn) { p.gamma = x_bn->gamma; p.beta = x_bn->beta; p.mean = x_bn->mean; p.rstd = x_bn->rstd; }
+    if (x_bn) {
+        const Centred cx = centred(x_bn, dt_of(dtype));
+        p.gamma = x_bn->gamma; p.beta = x_bn->beta; p.mean = cx.mean; p.rstd = x_bn->rstd; p.ctr = cx.ctr;
+    }
     p.part = (float *)ws;
     p.shift = y_bn ? y_bn->shift : nullptr;
     hipStream_t st = (hipStream_t)stream;
@@ -1434,7 +1491,10 @@ bnr_status bnr_maxpool_bn_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dt
     memset(&p, 0, sizeof p);
     p.n = n; p.h = h; p.w = w; p.c = c; p.ho = ho; p.wo = wo;
     p.x = x; p.x_ldc = x_ldc; p.g = gy; p.g_ldc = gy_ldc; p.y = dy; p.y_ldc = c;
-    if (x_bn) { p.gamma = x_bn->gamma; p.beta = x_bn->beta; p.mean = x_bn->mean; p.rstd = x_bn->rstd; }
+    if (x_bn) {
+        const Centred cx = centred(x_bn, dt_of(dtype));
+        p.gamma = x_bn->gamma; p.beta = x_bn->beta; p.mean = cx.mean; p.rstd = x_bn->rstd; p.ctr = cx.ctr;
+    }
     p.part = (float *)ws;
     hipStream_t st = (hipStream_t)stream;
     TRY_HIP(launch_maxpool_bwd(dt_of(dtype), p, x_bn != nullptr, st), "max-pooling backward");
@@ -1465,7 +1525,7 @@ bnr_status bnr_head_fwd(int32_t n, int32_t h, int32_t w, int32_t c, int32_t clas
     TRY(check_fptr(dlogits, "dlogits"));
     TRY(check_fptr(loss, "loss"));
     HeadParams p;
-    head_params(p, n, h, w, c, classes, x, x_ldc, x_bn, wfc);
+    head_params(p, dt_of(dtype), n, h, w, c, classes, x, x_ldc, x_bn, wfc);
     p.bfc = bfc; p.labels = labels; p.f = f; p.logits = logits; p.dlogits = dlogits; p.loss = loss;
     TRY_HIP(launch_head_fwd(dt_of(dtype), p, (hipStream_t)stream), "classifier head");
     return ok();
@@ -1497,7 +1557,7 @@ bnr_status bnr_head_bwd(int32_t n, int32_t h, int32_t w, int32_t c, int32_t clas
     if (overlap(view_range(gx, m, c, gx_ldc, es), view_range(x, m, c, x_ldc, es)))
         return fail(BNR_ERR_ALIAS, "gx overlaps x");
     HeadParams p;
-    head_params(p, n, h, w, c, classes, x, x_ldc, x_bn, wfc);
+    head_params(p, dt_of(dtype), n, h, w, c, classes, x, x_ldc, x_bn, wfc);
     p.f = const_cast<float *>(f);
     p.dlogits = const_cast<float *>(dlogits);
     p.df = df; p.dwfc = dwfc; p.dbfc = dbfc;

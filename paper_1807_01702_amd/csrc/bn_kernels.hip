@@ -21,11 +21,12 @@ namespace bnr {
 //              per-channel shift passed as `mean`, 0 if NULL)
 //   ST_SUM   : s1 = sum x                                 (unfused mean sweep)
 //   ST_SQDEV : s1 = sum (x - mean)^2                      (unfused variance sweep)
-//   ST_DYX   : s1 = sum dy,           s2 = sum dy * xhat  (BN backward sums)
+//   ST_DYX   : s1 = sum dy,           s2 = sum dy * xhat  (BN backward sums;
+//              xhat = ((x - ctr) - mean) rstd, ctr the float32 centre, bn_centre)
 // part[rb][0][c] = s1, part[rb][1][c] = s2 (float32).
 template <typename T, int MODE>
 __device__ __forceinline__ void stats_accum(const vec16 &v, const vec16 &d, const float *mu, const float *rs,
-                                            float *s1, float *s2)
+                                            const float *kc, float *s1, float *s2)
 {
     constexpr int VEC = Elem<T>::VEC;
     float f[VEC];
@@ -39,7 +40,7 @@ __device__ __forceinline__ void stats_accum(const vec16 &v, const vec16 &d, cons
     } else {
         float g[VEC];
         Elem<T>::unpack(d, g);
-        for (int i = 0; i < VEC; i++) { s1[i] += g[i]; s2[i] += g[i] * ((f[i] - mu[i]) * rs[i]); }
+        for (int i = 0; i < VEC; i++) { s1[i] += g[i]; s2[i] += g[i] * (((f[i] - kc[i]) - mu[i]) * rs[i]); }
     }
 }
 
@@ -47,7 +48,8 @@ template <typename T, int MODE>
 __global__ __launch_bounds__(kThreads) void k_stats_partial(
     const T *__restrict__ x, int64_t ldc, int64_t m, int C,
     const float *__restrict__ mean, const float *__restrict__ rstd,
-    const T *__restrict__ dy, int64_t dy_ldc, int64_t rows_per_block, float *__restrict__ part)
+    const T *__restrict__ dy, int64_t dy_ldc, int64_t rows_per_block, float *__restrict__ part,
+    const float *__restrict__ ctr)
 {
     constexpr int VEC = Elem<T>::VEC, U = 4;
     __shared__ float red[2][kThreads * VEC];
@@ -56,8 +58,10 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
     const int ry = kThreads / vb;
     const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
-    float s1[VEC], s2[VEC], mu[VEC], rs[VEC];
-    for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f; }
+    float s1[VEC], s2[VEC], mu[VEC], rs[VEC], kc[VEC];
+    for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f; kc[i] = 0.f; }
+    if (ty < ry && MODE == ST_DYX)
+        for (int i = 0; i < VEC; i++) kc[i] = bn_centre<T>(ctr, c0 + i);
     if (ty < ry && (MODE == ST_SQDEV || MODE == ST_DYX || (MODE == ST_SUMSQ && mean)))
         for (int i = 0; i < VEC; i++) mu[i] = mean[c0 + i];
     if (ty < ry && MODE == ST_DYX)
@@ -74,12 +78,12 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
                 d[u] = MODE == ST_DYX ? ldg16(dy + (r + u * ry) * dy_ldc + c0) : v[u];
             }
             #pragma unroll
-            for (int u = 0; u < U; u++) stats_accum<T, MODE>(v[u], d[u], mu, rs, s1, s2);
+            for (int u = 0; u < U; u++) stats_accum<T, MODE>(v[u], d[u], mu, rs, kc, s1, s2);
         }
         for (; r < r1; r += ry) {
             const vec16 v = ldg16(x + r * ldc + c0);
             const vec16 d = MODE == ST_DYX ? ldg16(dy + r * dy_ldc + c0) : v;
-            stats_accum<T, MODE>(v, d, mu, rs, s1, s2);
+            stats_accum<T, MODE>(v, d, mu, rs, kc, s1, s2);
         }
     }
     const int nch = vb * VEC;
@@ -105,6 +109,7 @@ __global__ __launch_bounds__(kThreads) void k_stats_partial(
 //   FIN_MVF   : with K = st.shift (0 if NULL; the sums are of x - K):
 //               mean = K + a/m, var = b/m - (a/m)^2 (clamped at 0), rstd
 //   FIN_MEAN  : mean = a/m
+//   (FIN_MVF, FIN_MEAN: st.mean_lo[c] = mean64 - (float)mean64, the low part)
 //   FIN_VAR   : var = a/m, rstd            (two-pass variance)
 //   (FIN_MVF, FIN_VAR: running statistics updated when st.rmean is set)
 //   FIN_BWD   : dbeta = a, dgamma = b, and the summed-gradient terms of st
@@ -121,7 +126,9 @@ __device__ __forceinline__ void stats_write(int mode, int c, double a, double b,
             v = b / dm - ms * ms;
             if (v < 0.0) v = 0.0;
             mu = (st.shift ? (double)st.shift[c] : 0.0) + ms;
-            mean[c] = (float)mu;
+            const float mf = (float)mu;
+            mean[c] = mf;
+            if (st.mean_lo) st.mean_lo[c] = (float)(mu - (double)mf);
         } else {                                  // two-pass: a = sum (x - mean)^2
             v = a / dm;
             mu = st.rmean ? (double)mean[c] : 0.0;
@@ -134,7 +141,10 @@ __device__ __forceinline__ void stats_write(int mode, int c, double a, double b,
             if (st.rvar) st.rvar[c] = (float)((1.0 - mo) * (double)st.rvar[c] + mo * v * (dm > 1.0 ? dm / (dm - 1.0) : 1.0));
         }
     } else if (mode == FIN_MEAN) {
-        mean[c] = (float)(a / dm);
+        const double mu = a / dm;
+        const float mf = (float)mu;
+        mean[c] = mf;
+        if (st.mean_lo) st.mean_lo[c] = (float)(mu - (double)mf);
     } else {
         dbeta[c] = (float)a;
         dgamma[c] = (float)b;
@@ -300,6 +310,8 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine2(const double *__res
 // and ACC are template arguments so each row batch of four rows issues all
 // its loads, including the accumulate read, before any arithmetic; the
 // operands are streamed once, so the loads are non-temporal).
+// (x - mean in every mode below stands for (x - ctr) - mean: ctr the float32
+// centre, bn_centre, with mean given relative to it)
 //   EW_DX      : out = gamma*rstd*(dy - dbeta/m - xhat*dgamma/m)  [+ out]
 //   EW_APPLY   : out = gamma*(x-mean)*rstd + beta                  (unfused BN)
 //   EW_RELU    : out = max(x, 0)                                   (unfused ReLU)
@@ -313,7 +325,8 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
     int64_t m, int C, const T *__restrict__ x, int64_t x_ldc, const T *__restrict__ x2,
     int64_t x2_ldc, const float *__restrict__ gamma, const float *__restrict__ beta,
     const float *__restrict__ mean, const float *__restrict__ rstd, const float *__restrict__ dgamma,
-    const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int64_t rows_per_block)
+    const float *__restrict__ dbeta, T *__restrict__ out, int64_t out_ldc, int64_t rows_per_block,
+    const float *__restrict__ ctr)
 {
     constexpr int VEC = Elem<T>::VEC, U = 4;
     constexpr bool TWO = MODE == EW_DX || MODE == EW_RELUBWD || MODE == EW_BNADDRELU || MODE == EW_ADDRELU ||
@@ -324,11 +337,13 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
     const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
     if (ty >= ry) return;
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
-    float p0[VEC], p1[VEC], p2[VEC], p3[VEC], p4[VEC];
+    float p0[VEC], p1[VEC], p2[VEC], p3[VEC], p4[VEC], kc[VEC];
     const float inv_m = 1.0f / (float)m;
     for (int i = 0; i < VEC; i++) {
         const int c = c0 + i;
         p0[i] = p1[i] = p2[i] = p3[i] = p4[i] = 0.f;
+        kc[i] = MODE == EW_DX || MODE == EW_APPLY || MODE == EW_BNADDRELU || MODE == EW_SPLITDX
+                    ? bn_centre<T>(ctr, c) : 0.f;
         if (MODE == EW_DX) {
             p0[i] = gamma[c] * rstd[c];          // k
             p1[i] = dbeta[c] * inv_m;            // a
@@ -354,7 +369,7 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
         if (MODE == EW_DX) {
             // f = dy, g = x
             for (int i = 0; i < VEC; i++) {
-                const float xh = (g[i] - p3[i]) * p4[i];
+                const float xh = ((g[i] - kc[i]) - p3[i]) * p4[i];
                 o[i] = p0[i] * (f[i] - p1[i] - xh * p2[i]);
             }
             if (ACC) {
@@ -363,12 +378,12 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
                 for (int i = 0; i < VEC; i++) o[i] += old[i];
             }
         } else if (MODE == EW_APPLY) {
-            for (int i = 0; i < VEC; i++) o[i] = p0[i] * ((f[i] - p3[i]) * p2[i]) + p1[i];
+            for (int i = 0; i < VEC; i++) o[i] = p0[i] * (((f[i] - kc[i]) - p3[i]) * p2[i]) + p1[i];
         } else if (MODE == EW_RELU) {
             for (int i = 0; i < VEC; i++) o[i] = f[i] > 0.f ? f[i] : 0.f;
         } else if (MODE == EW_BNADDRELU) {
             for (int i = 0; i < VEC; i++) {
-                const float t = bn_lin(f[i], p0[i], p1[i]) + g[i];
+                const float t = bn_lin(f[i] - kc[i], p0[i], p1[i]) + g[i];
                 o[i] = t > 0.f ? t : 0.f;
             }
         } else if (MODE == EW_ADDRELU) {
@@ -378,7 +393,7 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
             }
         } else if (MODE == EW_SPLITDX) {
             // f = summed gradient, g = x
-            for (int i = 0; i < VEC; i++) o[i] = f[i] + __builtin_fmaf(p0[i], g[i], p1[i]);
+            for (int i = 0; i < VEC; i++) o[i] = f[i] + __builtin_fmaf(p0[i], g[i] - kc[i], p1[i]);
             if (ACC) {
                 float old[VEC];
                 Elem<T>::unpack(vo, old);
@@ -415,13 +430,13 @@ __global__ __launch_bounds__(kThreads) void k_elementwise(
 // --------------------------------------------------------------------------
 // Backward of out = relu(bn(y) + identity) up to the BN reductions, in one
 // sweep: gm = g * [out > 0] (the gradient of both the identity and the BN
-// output), s1 = sum gm, s2 = sum gm * (y - mean) * rstd.  Row blocks as in
-// k_stats_partial.
+// output), s1 = sum gm, s2 = sum gm * ((y - ctr) - mean) * rstd (ctr: the
+// float32 centre, bn_centre).  Row blocks as in k_stats_partial.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_addrelu_bwd(
     const T *g, int64_t g_ldc, const T *__restrict__ out, int64_t out_ldc, const T *__restrict__ y,
     int64_t y_ldc, int64_t m, int C, const float *__restrict__ mean, const float *__restrict__ rstd, T *gm,
-    int64_t gm_ldc, int64_t rows_per_block, float *__restrict__ part)
+    int64_t gm_ldc, int64_t rows_per_block, float *__restrict__ part, const float *__restrict__ ctr)
 {
     constexpr int VEC = Elem<T>::VEC, U = 2;
     __shared__ float red[2][kThreads * VEC];
@@ -430,10 +445,12 @@ __global__ __launch_bounds__(kThreads) void k_addrelu_bwd(
     const int ry = kThreads / vb;
     const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
-    float s1[VEC], s2[VEC], mu[VEC], rs[VEC];
-    for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 0.f; }
+    float s1[VEC], s2[VEC], mu[VEC], rs[VEC], kc[VEC];
+    for (int i = 0; i < VEC; i++) { s1[i] = 0.f; s2[i] = 0.f; mu[i] = 0.f; rs[i] = 0.f; kc[i] = 0.f; }
     if (ty < ry)
-        for (int i = 0; i < VEC; i++) { mu[i] = mean[c0 + i]; rs[i] = rstd[c0 + i]; }
+        for (int i = 0; i < VEC; i++) {
+            mu[i] = mean[c0 + i]; rs[i] = rstd[c0 + i]; kc[i] = bn_centre<T>(ctr, c0 + i);
+        }
     auto row = [&](const vec16 &vg, const vec16 &vo, const vec16 &vy, T *dst) __attribute__((always_inline)) {
         float fg[VEC], fo[VEC], fy[VEC];
         Elem<T>::unpack(vg, fg);
@@ -443,7 +460,7 @@ __global__ __launch_bounds__(kThreads) void k_addrelu_bwd(
             const float d = fo[i] > 0.f ? fg[i] : 0.f;
             fg[i] = d;
             s1[i] += d;
-            s2[i] += d * ((fy[i] - mu[i]) * rs[i]);
+            s2[i] += d * (((fy[i] - kc[i]) - mu[i]) * rs[i]);
         }
         stg16(dst, Elem<T>::pack(fg));
     };
@@ -608,7 +625,7 @@ static inline int grid_cap(int64_t want) { return (int)(want < 4096 ? (want < 1 
 
 hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
                                 const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
-                                float *part, int64_t R, hipStream_t s)
+                                float *part, int64_t R, hipStream_t s, const float *ctr)
 {
     // operands each mode reads: refuse a launch that would dereference NULL
     if (!x || !part || ((mode == ST_SQDEV || mode == ST_DYX) && !mean) || (mode == ST_DYX && (!rstd || !dy)))
@@ -621,7 +638,7 @@ hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m
     auto go = [&](auto kern, auto tag) {
         using T = decltype(tag);
         hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, (const T *)x, ldc, m, C, mean, rstd, (const T *)dy,
-                           dy_ldc, rpb, part);
+                           dy_ldc, rpb, part, ctr);
     };
     if (dtype == DT_BF16) {
         switch (mode) {
@@ -654,16 +671,18 @@ hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m,
     if (!part || !red || (mode == FIN_MVF && (!mean || !rstd)) || (mode == FIN_MEAN && !mean) ||
         (mode == FIN_VAR && !rstd) || (mode == FIN_BWD && (!dbeta || !dgamma)))
         return hipErrorInvalidValue;
-    SplitTerms st{nullptr, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0.f};
+    SplitTerms st{nullptr, nullptr, nullptr, nullptr, 0, nullptr, nullptr, nullptr, 0.f, nullptr};
     if (split && split->alpha) {
         if (mode != FIN_BWD || !split->gamma || !split->rstd || !split->betap) return hipErrorInvalidValue;
         st = *split;
     }
-    if (split && (split->shift || split->rmean)) {
-        if ((split->shift && mode != FIN_MVF) || (split->rmean && mode != FIN_MVF && mode != FIN_VAR) ||
+    if (split && (split->shift || split->rmean || split->mean_lo)) {
+        if ((split->shift && mode != FIN_MVF) || (split->mean_lo && mode != FIN_MVF && mode != FIN_MEAN) ||
+            (split->rmean && mode != FIN_MVF && mode != FIN_VAR) ||
             (!split->rmean && split->rvar) || split->alpha || (mode == FIN_VAR && split->rmean && !mean))
             return hipErrorInvalidValue;
         st.shift = split->shift; st.rmean = split->rmean; st.rvar = split->rvar; st.momentum = split->momentum;
+        st.mean_lo = split->mean_lo;
     }
     if (R <= kCombineOneMaxRows) {
         TraceScope tr(KC_SMALL, KID_COMBINE, s, (double)R * 2 * C * 4 + 3.0 * C * 4, 0.0);
@@ -687,7 +706,7 @@ hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m,
 hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void *x, int64_t x_ldc, const void *x2,
                               int64_t x2_ldc, const float *gamma, const float *beta, const float *mean,
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
-                              int64_t out_ldc, int accumulate, hipStream_t s)
+                              int64_t out_ldc, int accumulate, hipStream_t s, const float *ctr)
 {
     const bool two = mode == EW_DX || mode == EW_RELUBWD || mode == EW_BNADDRELU || mode == EW_ADDRELU ||
                      mode == EW_SPLITDX;
@@ -705,7 +724,7 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
     auto go = [&](auto kern, auto tag) {
         using T = decltype(tag);
         hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, s, m, C, (const T *)x, x_ldc, (const T *)x2, x2_ldc, gamma,
-                           beta, mean, rstd, dgamma, dbeta, (T *)out, out_ldc, rpb);
+                           beta, mean, rstd, dgamma, dbeta, (T *)out, out_ldc, rpb, ctr);
     };
     if (dtype == DT_BF16) {
         if (mode == EW_DX) {
@@ -737,7 +756,7 @@ hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void 
 
 hipError_t launch_addrelu_bwd(int dtype, int64_t m, int C, const void *g, int64_t g_ldc, const void *out,
                               int64_t out_ldc, const void *y, int64_t y_ldc, const float *mean, const float *rstd,
-                              void *gm, int64_t gm_ldc, float *part, int64_t R, hipStream_t s)
+                              void *gm, int64_t gm_ldc, float *part, int64_t R, hipStream_t s, const float *ctr)
 {
     if (!g || !out || !y || !mean || !rstd || !gm || !part) return hipErrorInvalidValue;
     const int cb = (int)ceil_div(C, stats_ch_per_block(dtype));
@@ -747,11 +766,11 @@ hipError_t launch_addrelu_bwd(int dtype, int64_t m, int C, const void *g, int64_
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_addrelu_bwd<bf16_t>, grid, dim3(kThreads), 0, s, (const bf16_t *)g, g_ldc,
                            (const bf16_t *)out, out_ldc, (const bf16_t *)y, y_ldc, m, C, mean, rstd, (bf16_t *)gm,
-                           gm_ldc, rpb, part);
+                           gm_ldc, rpb, part, ctr);
     else
         hipLaunchKernelGGL(k_addrelu_bwd<float>, grid, dim3(kThreads), 0, s, (const float *)g, g_ldc,
                            (const float *)out, out_ldc, (const float *)y, y_ldc, m, C, mean, rstd, (float *)gm, gm_ldc,
-                           rpb, part);
+                           rpb, part, ctr);
     return hipGetLastError();
 }
 

@@ -137,6 +137,23 @@ __device__ __forceinline__ void bn_coef(float gamma, float beta, float mean, flo
 }
 __device__ __forceinline__ float bn_lin(float x, float c0, float c1) { return __builtin_fmaf(x, c0, c1); }
 
+// Normalisation centre of a BN input held in float32.  A consumer may be given
+// a centre K (the float32 mean) and the mean relative to it (mean - K: the low
+// part of the float64 mean), and then normalises the centred value x - K:
+//   y = (x - K) c0 + (beta - (mean - K) c0),  xhat = ((x - K) - (mean - K)) rstd,
+// the deferred gradient d = A dy + B (x - K) + C with deferred_coef given
+// mean - K.  Evaluated on x itself with the float32 mean, c1 = beta - mean c0
+// and the product x c0 would carry |mean| 2^-24 of absolute error, more than
+// the normalised value can afford once |mean| / std reaches 10^3; x - K is
+// exact there (Sterbenz: operands within a factor of two).  bf16 storage
+// already carries |x| 2^-9, so its consumers take K = 0: a compile-time zero,
+// and x - 0 = x exactly (also for -0), so the subtraction folds away.
+template <typename T>
+__device__ __forceinline__ float bn_centre(const float *ctr, int c) {
+    if constexpr (sizeof(T) == 4) return ctr ? ctr[c] : 0.f;
+    else return 0.f;
+}
+
 // Deferred input gradient of a BN-fed tensor, formed on load as
 //   d = A dy + B x + C  per channel (dy the loaded gradient, x the BN input).
 // One BN (split = 0):  d = gamma rstd (dy - dbeta/m - xhat dgamma/m), i.e.

@@ -33,6 +33,9 @@
 //                store dy (e_scale: store or add gamma*rstd*dy), per-channel
 //                sum(dy), sum(dy*xhat)
 //   EPI_RELUMASK: dy = dz * [y > 0] from a stored y (ReLU-CONV fusion alone)
+// float32 data: x - mean in the prologues and the BN-backward epilogue is
+// (x - K) - (mean - K) with the BN's centre K (bn_centre), x in PRO_BNGRAD is
+// x - K with the coefficients formed from mean - K.
 // The epilogue goes through LDS so that every global access is a 16-byte
 // vector of one pixel row.
 #include <type_traits>
@@ -99,15 +102,25 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     const int halo = TAPS == 9 ? W + 1 : 0;
     const int arows = BM + 2 * halo;
 
-    // per-channel prologue coefficients for all K channels
+    // per-channel prologue coefficients for all K channels; float32 data also
+    // keeps the centre K (bn_centre) in coef[3 K + c]: x stands for x - K below
+    constexpr bool kF32 = sizeof(T) == 4;
+    auto kcen = [&](int c) __attribute__((always_inline)) {
+        if constexpr (kF32) return coef[3 * K + c];
+        else return 0.f;
+    };
     if (p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL || p.pro == PRO_BNADDRELU) {
-        for (int c = tid; c < K; c += kThreads)             // y = x c0 + c1
+        for (int c = tid; c < K; c += kThreads) {           // y = x c0 + c1
             bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], coef[K + c], coef[2 * K + c]);
+            if constexpr (kF32) coef[3 * K + c] = bn_centre<T>(p.p_ctr, c);
+        }
     } else if (p.pro == PRO_BNGRAD) {
         const float inv_m = 1.0f / (float)m;
-        for (int c = tid; c < K; c += kThreads)
+        for (int c = tid; c < K; c += kThreads) {
             deferred_coef(p.p_split, c, inv_m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta, p.p_alpha,
                           p.p_betap, coef[c], coef[K + c], coef[2 * K + c]);
+            if constexpr (kF32) coef[3 * K + c] = bn_centre<T>(p.p_ctr, c);
+        }
     }
 
     // geometry of this lane's output rows
@@ -212,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                         Elem<T>::unpack(ra[j], f);
                         #pragma unroll
                         for (int e = 0; e < VEC; e++) {
-                            const float t = bn_lin(f[e], coef[K + cc + e], coef[2 * K + cc + e]);
+                            const float t = bn_lin(f[e] - kcen(cc + e), coef[K + cc + e], coef[2 * K + cc + e]);
                             f[e] = t > 0.f ? t : 0.f;
                         }
                         out = Elem<T>::pack(f);
@@ -223,7 +236,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                         Elem<T>::unpack(rx[j], x);
                         #pragma unroll
                         for (int e = 0; e < VEC; e++)
-                            d[e] = __builtin_fmaf(coef[cc + e], d[e], __builtin_fmaf(coef[K + cc + e], x[e], coef[2 * K + cc + e]));
+                            d[e] = __builtin_fmaf(coef[cc + e], d[e],
+                                                  __builtin_fmaf(coef[K + cc + e], x[e] - kcen(cc + e), coef[2 * K + cc + e]));
                         out = Elem<T>::pack(d);
                     } else if (pro == PRO_RELU) {
                         float f[VEC];
@@ -306,7 +320,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     float f[VEC];
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
                     for (int e = 0; e < VEC; e++) {
-                        const float t = bn_lin(f[e], coef[K + c + e], coef[2 * K + c + e]);
+                        const float t = bn_lin(f[e] - kcen(c + e), coef[K + c + e], coef[2 * K + c + e]);
                         f[e] = t > 0.f ? t : 0.f;
                     }
                     out = Elem<T>::pack(f);
@@ -315,7 +329,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), d);
                     Elem<T>::unpack(ldg16(asrc2 + pp * p.a2_ldc + c), x);
                     for (int e = 0; e < VEC; e++)
-                        d[e] = __builtin_fmaf(coef[c + e], d[e], __builtin_fmaf(coef[K + c + e], x[e], coef[2 * K + c + e]));
+                        d[e] = __builtin_fmaf(coef[c + e], d[e],
+                                              __builtin_fmaf(coef[K + c + e], x[e] - kcen(c + e), coef[2 * K + c + e]));
                     out = Elem<T>::pack(d);
                 } else if (p.pro == PRO_RELU) {
                     float f[VEC];
@@ -327,7 +342,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), f);
                     Elem<T>::unpack(ldg16(asrc2 + pp * p.a2_ldc + c), id);
                     for (int e = 0; e < VEC; e++)
-                        f[e] = __builtin_fmaxf(bn_lin(f[e], coef[K + c + e], coef[2 * K + c + e]) + id[e], 0.f);
+                        f[e] = __builtin_fmaxf(bn_lin(f[e] - kcen(c + e), coef[K + c + e], coef[2 * K + c + e]) + id[e], 0.f);
                     out = Elem<T>::pack(f);
                     if (nt == 0) stg16(reinterpret_cast<T *>(p.side) + pp * p.side_ldc + c, out);
                 } else if (p.pro == PRO_BNRELU_POOL) {
@@ -342,7 +357,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                         float f[VEC];
                         Elem<T>::unpack(ldg16(asrc + (p00 + (f4 >> 1) * W + (f4 & 1)) * p.a_ldc + c), f);
                         for (int e = 0; e < VEC; e++)
-                            acc[e] += __builtin_fmaxf(bn_lin(f[e], coef[K + c + e], coef[2 * K + c + e]), 0.f);
+                            acc[e] += __builtin_fmaxf(bn_lin(f[e] - kcen(c + e), coef[K + c + e], coef[2 * K + c + e]), 0.f);
                     }
                     for (int e = 0; e < VEC; e++) acc[e] *= 0.25f;
                     out = Elem<T>::pack(acc);
@@ -403,11 +418,12 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     const int v = tid % VPRO, r0 = tid / VPRO;
     const int n = n0 + v * VEC;
     const bool col_ok = n < N;
-    float s1[VEC], s2[VEC], emu[VEC], ers[VEC], eg[VEC], eb[VEC];
-    for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
+    float s1[VEC], s2[VEC], emu[VEC], ers[VEC], eg[VEC], eb[VEC], ek[VEC];
+    for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; ek[e] = 0.f; }
     if (p.epi == EPI_BNBWD && col_ok)
         for (int e = 0; e < VEC; e++) {
             emu[e] = p.e_mean[n + e]; ers[e] = p.e_rstd[n + e];
+            ek[e] = bn_centre<T>(p.e_ctr, n + e);
             bn_coef(p.e_gamma[n + e], p.e_beta[n + e], emu[e], ers[e], eg[e], eb[e]);   // the forward's c0, c1
         }
     if (p.epi == EPI_STATS)                       // statistics of y - shift
@@ -447,8 +463,9 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 Elem<T>::unpack(ldg16(exs + pp * p.ex_ldc + n), x);
                 if (p.e_scale && p.accumulate) Elem<T>::unpack(ldg16(dst), old);
                 for (int e = 0; e < VEC; e++) {
-                    const float xh = (x[e] - emu[e]) * ers[e];
-                    const float d = bn_lin(x[e], eg[e], eb[e]) > 0.f ? f[e] : 0.f;
+                    const float xc = x[e] - ek[e];
+                    const float xh = (xc - emu[e]) * ers[e];
+                    const float d = bn_lin(xc, eg[e], eb[e]) > 0.f ? f[e] : 0.f;
                     s1[e] += d;
                     s2[e] += d * xh;
                     // summed-gradient form: gamma*rstd*dy, stored or added
@@ -568,7 +585,7 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 {
     using Cfg = RowsCfg<T, TAPS, BM, BN>;
     const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD || p.pro == PRO_BNRELU_POOL || p.pro == PRO_BNADDRELU
-                      ? 3 : 0;
+                      ? (sizeof(T) == 4 ? 4 : 3) : 0;
     const size_t lds = Cfg::LDS + (size_t)P * p.K * sizeof(float);
     auto kern = k_conv_rows<T, TAPS, BM, BN, WM, WN, SP>;
     static bool attr_set = false;

@@ -113,8 +113,8 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
     static_assert(WR * WC == 4, "four waves");
     __shared__ __align__(16) T Zt[kWgCIT * ZSTR];
     __shared__ __align__(16) T Gt[COT * GSTR];
-    __shared__ float zc[2][kWgCIT];
-    __shared__ float gc[3][COT];
+    __shared__ float zc[3][kWgCIT];           // c0, c1, centre (float32 data: x - K below)
+    __shared__ float gc[4][COT];              // A, B, C, centre of gx
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wr = wave / WC, wc = wave % WC;
@@ -130,14 +130,18 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
 
     if (tid < kWgCIT) {
         const int c = ci0 + tid;
-        if (p.a_mode == 1 && c < C_in)          // the forward's y = x c0 + c1
+        if (p.a_mode == 1 && c < C_in) {        // the forward's y = x c0 + c1
             bn_coef(p.a_gamma[c], p.a_beta[c], p.a_mean[c], p.a_rstd[c], zc[0][tid], zc[1][tid]);
+            zc[2][tid] = bn_centre<T>(p.a_ctr, c);
+        }
     }
     if (tid < COT) {
         const int c = co0 + tid;
-        if (p.gsrc == GB_BNGRAD && c < C_out)
+        if (p.gsrc == GB_BNGRAD && c < C_out) {
             deferred_coef(p.g_split, c, 1.0f / (float)m, p.g_gamma, p.g_mean, p.g_rstd, p.g_dgamma, p.g_dbeta,
                           p.g_alpha, p.g_betap, gc[0][tid], gc[1][tid], gc[2][tid]);
+            gc[3][tid] = bn_centre<T>(p.g_ctr, c);
+        }
     }
     // zero the G guards and the columns beyond gcols once; staging never writes them
     for (int i = tid; i < COT * GSTR; i += kThreads) {
@@ -221,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
                 const bool valid = g.zpix(2 * pr + h2) >= 0 && ci0 + cl < C_in;
                 if (p.a_mode == 1)
                     for (int e = 0; e < VEC; e++) {
-                        const float t = bn_lin(f[h2][e], zc[0][cl + e], zc[1][cl + e]);
+                        const float t = bn_lin(f[h2][e] - zc[2][cl + e], zc[0][cl + e], zc[1][cl + e]);
                         f[h2][e] = valid && t > 0.f ? t : 0.f;
                     }
                 else if (p.a_mode == 2)
@@ -243,7 +247,7 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgradParams p, WgradPlan pl)
                     Elem<T>::unpack(gx[j][h2], x);
                     for (int e = 0; e < VEC; e++) {
                         const float d = __builtin_fmaf(gc[0][cl + e], f[h2][e],
-                                                       __builtin_fmaf(gc[1][cl + e], x[e], gc[2][cl + e]));
+                                                       __builtin_fmaf(gc[1][cl + e], x[e] - gc[3][cl + e], gc[2][cl + e]));
                         f[h2][e] = valid ? d : 0.f;
                     }
                 } else if (p.gsrc == GB_POOLUP) {

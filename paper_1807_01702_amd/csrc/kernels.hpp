@@ -26,6 +26,10 @@ struct SplitTerms {
     const float *shift;
     float *rmean, *rvar;
     float momentum;
+    // FIN_MVF, FIN_MEAN: also write the low part of the float64 mean,
+    // mean64 - (float)mean64 (float32 consumers centre x on the float32 mean
+    // and are given this as the mean relative to it)
+    float *mean_lo;
 };
 
 // Reduction scratch ("red") of a statistics combine: the float64 level-1
@@ -37,19 +41,23 @@ inline size_t stats_red_bytes(int C) { return (size_t)kRedMaxRS * 2 * C * sizeof
 int stats_combine_splits(int64_t R);
 hipError_t launch_stats_partial(int dtype, const void *x, int64_t ldc, int64_t m, int C, int mode,
                                 const float *mean, const float *rstd, const void *dy, int64_t dy_ldc,
-                                float *part, int64_t R, hipStream_t s);
+                                float *part, int64_t R, hipStream_t s, const float *ctr = nullptr);
 hipError_t launch_stats_finalize(const float *part, int64_t R, int C, int64_t m, int mode, float eps, float *mean,
                                  float *var, float *rstd, float *dbeta, float *dgamma, void *red, hipStream_t s,
                                  const SplitTerms *split = nullptr);
 hipError_t launch_elementwise(int dtype, int mode, int64_t m, int C, const void *x, int64_t x_ldc, const void *x2,
                               int64_t x2_ldc, const float *gamma, const float *beta, const float *mean,
                               const float *rstd, const float *dgamma, const float *dbeta, void *out,
-                              int64_t out_ldc, int accumulate, hipStream_t s);
+                              int64_t out_ldc, int accumulate, hipStream_t s, const float *ctr = nullptr);
 // Residual-block backward sweep: gm = g * [out > 0], per-channel sum(gm) and
 // sum(gm * (y - mean) * rstd) partials [R][2][C].
+// ctr (the statistics sweep's ST_DYX, the elementwise BN modes, this sweep):
+// the float32 centre of the BN input (NULL: 0), mean given relative to it
+// (bn_centre).
 hipError_t launch_addrelu_bwd(int dtype, int64_t m, int C, const void *g, int64_t g_ldc, const void *out,
                               int64_t out_ldc, const void *y, int64_t y_ldc, const float *mean, const float *rstd,
-                              void *gm, int64_t gm_ldc, float *part, int64_t R, hipStream_t s);
+                              void *gm, int64_t gm_ldc, float *part, int64_t R, hipStream_t s,
+                              const float *ctr = nullptr);
 hipError_t launch_avgpool2(int dtype, int n, int h, int w, int C, const void *x, int64_t ldc, void *y, int64_t y_ldc,
                            hipStream_t s);
 hipError_t launch_avgpool2_bwd(int dtype, int n, int h, int w, int C, const void *g, int64_t g_ldc, void *gx,
@@ -101,6 +109,7 @@ struct RowsParams {
     const float *p_gamma, *p_beta, *p_mean, *p_rstd, *p_dgamma, *p_dbeta;
     int p_split;                  // PRO_BNGRAD: 1 = summed gradient of several BNs (deferred_coef)
     const float *p_alpha, *p_betap;
+    const float *p_ctr;           // float32 centre of the prologue BN's input (NULL: 0; p_mean relative to it)
     const void *wpack;            // weights packed by launch_pack_weights (conv_rows)
     const void *wraw;             // weights in their [k][k][c_in][c_out] layout (persistent kernels)
     int wtrans;                   // 1: data-gradient operand (GEMM K = c_out, N = c_in)
@@ -113,6 +122,7 @@ struct RowsParams {
     const void *ex;               // EPI_BNBWD: BN input (N channels); EPI_RELUMASK: ReLU input
     int64_t ex_ldc;
     const float *e_gamma, *e_beta, *e_mean, *e_rstd;
+    const float *e_ctr;           // EPI_BNBWD: float32 centre of ex (NULL: 0; e_mean relative to it)
     const float *e_shift;         // EPI_STATS: the sums are of (y - e_shift) (NULL: 0)
     void *side;                   // PRO_BNADDRELU: the transformed A rows are stored here too
     int64_t side_ldc;
@@ -148,6 +158,7 @@ struct WgradParams {
     int64_t x_ldc;
     int a_mode;                   // 0: x as is, 1: relu(bn(x)) recomputed on load, 2: relu(x)
     const float *a_gamma, *a_beta, *a_mean, *a_rstd;
+    const float *a_ctr;           // a_mode 1: float32 centre of x (NULL: 0; a_mean relative to it)
     int gsrc;                     // GB_*
     const void *g;                // DENSE: [m][c_out] view; POOLUP: pooled gradient; BNGRAD: dy (dense)
     int64_t g_ldc;
@@ -156,6 +167,7 @@ struct WgradParams {
     const float *g_gamma, *g_mean, *g_rstd, *g_dgamma, *g_dbeta;
     int g_split;                  // GB_BNGRAD: 1 = summed gradient of several BNs (deferred_coef)
     const float *g_alpha, *g_betap;
+    const float *g_ctr;           // GB_BNGRAD: float32 centre of gx (NULL: 0; g_mean relative to it)
     float *dw;                    // [k][k][c_in][c_out]
     float *part;                  // workspace for split partial tiles
     void *red;                    // split-K sum scratch (sum_partials_red_bytes)
@@ -186,6 +198,7 @@ struct StemParams {
     const void *gx;               // BNGRAD: the BN input (the CONV output) view
     int64_t gx_ldc;
     const float *g_gamma, *g_mean, *g_rstd, *g_dgamma, *g_dbeta;
+    const float *g_ctr;           // BNGRAD, float32: centre of gx (NULL: 0; g_mean relative to it)
     float *dwpart;                // weight-gradient partials [splits][7][7][c_in][64]
 };
 int64_t stem_groups(int64_t items);
@@ -202,6 +215,7 @@ struct MaxPoolParams {
     const void *x;                // input view [n][h][w][c]
     int64_t x_ldc;
     const float *gamma, *beta, *mean, *rstd;   // BN of x (NULL: plain pooling)
+    const float *ctr;             // float32 centre of x (NULL: 0; mean relative to it)
     void *y;                      // forward: output view; backward: dy / dz (dense [n*h*w][c])
     int64_t y_ldc;
     const void *g;                // backward: gradient of the pooled output (view)
@@ -221,6 +235,7 @@ struct HeadParams {
     const void *x;                // [n*h*w][c] view
     int64_t x_ldc;
     const float *gamma, *beta, *mean, *rstd;
+    const float *ctr;             // float32 centre of x (NULL: 0; mean relative to it)
     float *f;                     // pooled features [n][c]
     const void *wfc;              // [c][classes] (dtype)
     const float *bfc;             // [classes]

@@ -363,10 +363,12 @@ __global__ __launch_bounds__(kThreads) void k_stem_wgrad_f32(StemParams p)
     const int co = i % kStemCout, r = i / kStemCout;
     const int ci = r % p.c_in, kw = (r / p.c_in) % kSK, kh = r / (p.c_in * kSK);
     const int64_t m_out = (int64_t)p.n * p.ho * p.wo;
-    float A = 1.f, B = 0.f, C = 0.f;
-    if (GS == GB_BNGRAD)
+    float A = 1.f, B = 0.f, C = 0.f, K = 0.f;
+    if (GS == GB_BNGRAD) {
         deferred_coef(0, co, 1.0f / (float)m_out, p.g_gamma, p.g_mean, p.g_rstd, p.g_dgamma, p.g_dbeta, nullptr,
                       nullptr, A, B, C);
+        K = bn_centre<float>(p.g_ctr, co);      // d = A dy + B (x - K) + C
+    }
     const float *img = reinterpret_cast<const float *>(p.img);
     const float *g = reinterpret_cast<const float *>(p.g), *gx = reinterpret_cast<const float *>(p.gx);
     float acc = 0.f;
@@ -377,7 +379,7 @@ __global__ __launch_bounds__(kThreads) void k_stem_wgrad_f32(StemParams p)
         const int64_t n = t / p.ho;
         const int ih = 2 * oh - kStemPad + kh, iw = 2 * ow - kStemPad + kw;
         if (ih < 0 || ih >= p.h || iw < 0 || iw >= p.w) continue;
-        const float gv = GS == GB_BNGRAD ? __builtin_fmaf(A, g[q * kStemCout + co], __builtin_fmaf(B, gx[q * p.gx_ldc + co], C))
+        const float gv = GS == GB_BNGRAD ? __builtin_fmaf(A, g[q * kStemCout + co], __builtin_fmaf(B, gx[q * p.gx_ldc + co] - K, C))
                                          : g[q * p.g_ldc + co];
         acc = __builtin_fmaf(img[((n * p.h + ih) * p.w + iw) * kStemPix + ci], gv, acc);
     }
@@ -405,16 +407,17 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
     const int ry = kThreads / vb;
     const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
-    float sg[VEC], k[VEC], b[VEC], s1[VEC], s2[VEC], sh[VEC];
+    float sg[VEC], k[VEC], b[VEC], kc[VEC], s1[VEC], s2[VEC], sh[VEC];
     #pragma unroll
     for (int i = 0; i < VEC; i++) {
         s1[i] = s2[i] = 0.f;
         sh[i] = STATS && p.shift && ty < ry ? p.shift[c0 + i] : 0.f;     // statistics of y - shift
-        sg[i] = 1.f; k[i] = 1.f; b[i] = 0.f;
+        sg[i] = 1.f; k[i] = 1.f; b[i] = 0.f; kc[i] = 0.f;
         if (BN && ty < ry) {
             const float g = p.gamma[c0 + i];
             sg[i] = g > 0.f ? 1.f : (g < 0.f ? -1.f : 0.f);
             bn_coef(g, p.beta[c0 + i], p.mean[c0 + i], p.rstd[c0 + i], k[i], b[i]);
+            kc[i] = bn_centre<T>(p.ctr, c0 + i);
         }
     }
     const T *x = reinterpret_cast<const T *>(p.x);
@@ -452,7 +455,7 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
             for (int i = 0; i < VEC; i++) {
                 o[i] = bv[i];
                 if (BN) {
-                    const float v = bn_lin(bv[i], k[i], b[i]);
+                    const float v = bn_lin(bv[i] - kc[i], k[i], b[i]);
                     o[i] = v > 0.f ? v : 0.f;
                 }
             }
@@ -507,16 +510,17 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_bwd(MaxPoolParams p)
     const int tid = threadIdx.x, cv = tid % cvec;
     const int hp = (h + 1) / 2;
     const int64_t items = (int64_t)p.n * hp;
-    float k[VEC], b[VEC], mu[VEC], rs[VEC], s1[VEC], s2[VEC];
+    float k[VEC], b[VEC], mu[VEC], rs[VEC], kc[VEC], s1[VEC], s2[VEC];
     #pragma unroll
     for (int i = 0; i < VEC; i++) {
         s1[i] = s2[i] = 0.f;
-        k[i] = 1.f; b[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f;
+        k[i] = 1.f; b[i] = 0.f; mu[i] = 0.f; rs[i] = 1.f; kc[i] = 0.f;
         if (BN) {
             const int c = cv * VEC + i;
             const float g = p.gamma[c];
             mu[i] = p.mean[c];
             rs[i] = p.rstd[c];
+            kc[i] = bn_centre<T>(p.ctr, c);
             bn_coef(g, p.beta[c], mu[i], rs[i], k[i], b[i]);
         }
     }
@@ -589,14 +593,14 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_bwd(MaxPoolParams p)
                 float f[VEC];
                 Elem<T>::unpack(ldg16(x + q * p.x_ldc + cv * VEC), f);
                 #pragma unroll
-                for (int i = 0; i < VEC; i++) o[i] = bn_lin(f[i], k[i], b[i]) > 0.f ? dz[i] : 0.f;
+                for (int i = 0; i < VEC; i++) o[i] = bn_lin(f[i] - kc[i], k[i], b[i]) > 0.f ? dz[i] : 0.f;
                 const vec16 ov = Elem<T>::pack(o);
                 stg16(dy + q * C + cv * VEC, ov);
                 Elem<T>::unpack(ov, o);
                 #pragma unroll
                 for (int i = 0; i < VEC; i++) {
                     s1[i] += o[i];
-                    s2[i] += o[i] * ((f[i] - mu[i]) * rs[i]);
+                    s2[i] += o[i] * (((f[i] - kc[i]) - mu[i]) * rs[i]);
                 }
             } else {
                 stg16(dy + q * C + cv * VEC, Elem<T>::pack(dz));
@@ -635,10 +639,11 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
     const int i = blockIdx.x * kThreads + threadIdx.x;
     if (i >= p.n * cvec) return;
     const int n = i / cvec, c0 = (i - n * cvec) * VEC;
-    float k[VEC], b[VEC], acc[VEC];
+    float k[VEC], b[VEC], kc[VEC], acc[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) {
         bn_coef(p.gamma[c0 + e], p.beta[c0 + e], p.mean[c0 + e], p.rstd[c0 + e], k[e], b[e]);
+        kc[e] = bn_centre<T>(p.ctr, c0 + e);
         acc[e] = 0.f;
     }
     const T *x = reinterpret_cast<const T *>(p.x);
@@ -647,7 +652,7 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
         Elem<T>::unpack(ldg16(x + ((int64_t)n * hw + q) * p.x_ldc + c0), f);
         #pragma unroll
         for (int e = 0; e < VEC; e++) {
-            const float v = bn_lin(f[e], k[e], b[e]);
+            const float v = bn_lin(f[e] - kc[e], k[e], b[e]);
             acc[e] += v > 0.f ? v : 0.f;
         }
     }
@@ -781,17 +786,18 @@ __global__ __launch_bounds__(kThreads) void k_head_bn_bwd(HeadParams p, int64_t 
     const int ry = kThreads / vb;
     const int tid = threadIdx.x, tx = tid % vb, ty = tid / vb;
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
-    float k[VEC], b[VEC], mu[VEC], rs[VEC], gk[VEC], s1[VEC], s2[VEC], da[VEC], db[VEC];
+    float k[VEC], b[VEC], mu[VEC], rs[VEC], kc[VEC], gk[VEC], s1[VEC], s2[VEC], da[VEC], db[VEC];
     const float inv_hw = 1.0f / (float)hw, inv_m = 1.0f / (float)m;
     #pragma unroll
     for (int i = 0; i < VEC; i++) {
         s1[i] = s2[i] = 0.f;
-        k[i] = b[i] = mu[i] = gk[i] = da[i] = db[i] = 0.f;
+        k[i] = b[i] = mu[i] = gk[i] = da[i] = db[i] = kc[i] = 0.f;
         rs[i] = 1.f;
         if (ty < ry) {
             const int c = c0 + i;
             mu[i] = p.mean[c];
             rs[i] = p.rstd[c];
+            kc[i] = bn_centre<T>(p.ctr, c);
             bn_coef(p.gamma[c], p.beta[c], mu[i], rs[i], k[i], b[i]);
             gk[i] = k[i];
             if (MODE == HB_DX) { da[i] = p.dbeta[c] * inv_m; db[i] = p.dgamma[c] * inv_m; }
@@ -809,8 +815,9 @@ __global__ __launch_bounds__(kThreads) void k_head_bn_bwd(HeadParams p, int64_t 
             #pragma unroll
             for (int i = 0; i < VEC; i++) {
                 const float dz = p.df[n * C + c0 + i] * inv_hw;
-                const float dyv = bn_lin(f[i], k[i], b[i]) > 0.f ? dz : 0.f;
-                const float xh = (f[i] - mu[i]) * rs[i];
+                const float xc = f[i] - kc[i];
+                const float dyv = bn_lin(xc, k[i], b[i]) > 0.f ? dz : 0.f;
+                const float xh = (xc - mu[i]) * rs[i];
                 if (MODE == HB_DX) {
                     o[i] = gk[i] * (dyv - da[i] - xh * db[i]);
                 } else {

@@ -187,3 +187,198 @@ def test_reference_two_pass_running(B):
     mean_r, var_r, _ = P.bn_stats(full.astype(np.float64), 0.0)
     assert_stats("two-pass stats", host(bn.mean), host(bn.var), mean_r, var_r, TOL)
     _check_running(bn, rmean0, rvar0, mean_r, var_r, m, momentum=0.25)
+
+
+# ------------------------------------------------ consumers at large offsets ----
+@pytest.mark.parametrize("offset", [1.0e3, 1.0e4])
+@pytest.mark.parametrize("k", [1, 3])
+def test_consumers_at_large_offset(B, offset, k):
+    """fp32 data whose channels sit at |mean| / std = offset: the robust
+    statistics of x (summed around a shift near the mean), the BN+ReLU
+    prologue of the CONV that reads x, the BN-backward epilogue of its data
+    gradient and the deferred input gradient of a BN on a large-offset CONV
+    output, each against the oracle at the fp32 tolerance."""
+    from helpers import assert_close, relu_ambiguous
+    n, h, w, ci, co = 2, 6, 7, 16, 24
+    xf = synth.normal(21, "x", (n, h, w, ci)) + np.float32(offset)
+    wt = synth.conv_weight(21, "w", k, ci, co, False)
+    bp = synth.bn_params(21, "bn", ci)
+    x64 = xf.astype(np.float64)
+    mean_r, var_r, _ = P.bn_stats(x64, 0.0)
+    x = dev(xf, False)
+    bn = B.BN(f32dev(bp["gamma"]), f32dev(bp["beta"]), 1e-5)
+    bn.robust(shift=f32dev(mean_r + synth.normal(21, "shift", (ci,))))
+    B.bnr_bn_stats(x, bn)
+    y = torch.empty((n, h, w, co), dtype=torch.float32, device="cuda")
+    desc = B.desc_for(x, y, k, n, h, w)
+    B.bnr_bn_relu_conv_fwd(desc, x, bn, dev(wt, False), y)
+    # backward: dense upstream gradient; BN-backward epilogue, dW with the recompute
+    gf = synth.normal(21, "g", (n, h, w, co))
+    dw = torch.empty(wt.shape, dtype=torch.float32, device="cuda")
+    dg = torch.empty(ci, dtype=torch.float32, device="cuda")
+    db = torch.empty_like(dg)
+    dy = torch.empty_like(x)
+    dx = torch.empty_like(x)
+    B.bnr_bwd_fused(desc, x, bn, dev(wt, False), B.grad_dense(dev(gf, False)), dw, dg, db, dy, dx)
+    torch.cuda.synchronize()
+    yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    amb = relu_ambiguous(yr, False)
+    z = P.relu_fwd(yr)
+    assert_close("conv out", host(y), P.conv_fwd(z, wt.astype(np.float64)), 1e-4)
+    dz = P.conv_dgrad(gf.astype(np.float64), wt.astype(np.float64), (h, w))
+    dyr = P.relu_bwd(dz, yr)
+    dxr, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, rstd)
+    assert_close("dy", host(dy), dyr, 1e-4, exclude=amb)
+    assert_close("dx", host(dx), dxr, 1e-4, exclude=amb)
+    assert_close("dW", host(dw), P.conv_wgrad(z, gf.astype(np.float64), k), 1e-4)
+    assert_close("dgamma", host(dg), dgr, 1e-4)
+    # the deferred input gradient of a BN whose input is this large-offset x,
+    # formed on load by the backward of the CONV that produced x (input xin)
+    xin_f = synth.normal(21, "xin", (n, h, w, co))
+    wp = synth.conv_weight(21, "wp", k, co, ci, False)
+    dwp = torch.empty(wp.shape, dtype=torch.float32, device="cuda")
+    dxin = torch.empty((n, h, w, co), dtype=torch.float32, device="cuda")
+    descp = B.desc_for(dev(xin_f, False), x, k, n, h, w)
+    B.bnr_bwd_fused(descp, dev(xin_f, False), None, dev(wp, False), B.grad_bn(dy, x, bn, dg, db), dwp, dx=dxin)
+    torch.cuda.synchronize()
+    g_r = P.bn_bwd(x64, host(dy), bp["gamma"], mu, rstd)[0]
+    assert_close("deferred dx -> producer dx", host(dxin), P.conv_dgrad(g_r, wp.astype(np.float64), (h, w)), 1e-4)
+    assert_close("deferred dx -> producer dW", host(dwp), P.conv_wgrad(xin_f.astype(np.float64), g_r, k), 1e-4)
+
+
+@pytest.mark.parametrize("offset", [1.0e4])
+def test_sweeps_at_large_offset(B, offset):
+    """The standalone float32 BN sweeps on data at |mean| / std = offset: BN
+    input gradient, summed-gradient input gradient and the summed gradient
+    formed in a CONV prologue, BN + add + ReLU forward and backward, and the
+    unfused (two-pass) BN -> ReLU layer, each against the oracle."""
+    from helpers import assert_close, relu_ambiguous
+    n, h, w, c, co = 2, 5, 9, 32, 16
+    m = n * h * w
+    xf = synth.normal(22, "x", (n, h, w, c)) + np.float32(offset)
+    x64 = xf.astype(np.float64)
+    bp = synth.bn_params(22, "bn", c)
+    x = dev(xf, False)
+
+    def robust_bn():
+        bn = B.BN(f32dev(bp["gamma"]), f32dev(bp["beta"]), 1e-5)
+        return bn.robust(shift=f32dev(P.bn_stats(x64, 0.0)[0] + synth.normal(22, "shift", (c,))))
+
+    yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    amb = relu_ambiguous(yr, False)
+    bn = robust_bn()
+    B.bnr_bn_stats(x, bn)
+    # BN input gradient from dy and the sums
+    dyf = synth.normal(22, "dy", (n, h, w, c))
+    dxr, dgr, dbr = P.bn_bwd(x64, dyf.astype(np.float64), bp["gamma"], mu, rstd)
+    dx = torch.empty_like(x)
+    B.bnr_bn_dx(dev(dyf, False), x, bn, f32dev(dgr), f32dev(dbr), dx)
+    torch.cuda.synchronize()
+    assert_close("bn dx", host(dx), dxr, 1e-4)
+    # summed gradient: dx = gsum + alpha + betap xhat, and the same term in a CONV prologue
+    gs = synth.normal(22, "gsum", (n, h, w, c))
+    al, bt = synth.normal(22, "alpha", (c,)), synth.normal(22, "betap", (c,))
+    xh = (x64 - mu) * rstd
+    dsr = gs + al + bt * xh
+    B.bnr_split_dx(dev(gs, False), x, bn, f32dev(al), f32dev(bt), dx)
+    xin = synth.normal(22, "xin", (n, h, w, co))
+    wp = synth.conv_weight(22, "wp", 1, co, c, False)
+    dxin = torch.empty((n, h, w, co), dtype=torch.float32, device="cuda")
+    dwp = torch.empty(wp.shape, dtype=torch.float32, device="cuda")
+    desc = B.desc_for(dev(xin, False), x, 1, n, h, w)
+    B.bnr_bwd_fused(desc, dev(xin, False), None, dev(wp, False),
+                    B.grad_split(dev(gs, False), x, bn, f32dev(al), f32dev(bt)), dwp, dx=dxin)
+    torch.cuda.synchronize()
+    assert_close("split dx", host(dx), dsr, 1e-4)
+    assert_close("summed gradient prologue -> dx", host(dxin), P.conv_dgrad(dsr, wp.astype(np.float64), (h, w)), 1e-4)
+    assert_close("summed gradient prologue -> dW", host(dwp), P.conv_wgrad(xin.astype(np.float64), dsr, 1), 1e-4)
+    # BN + add + ReLU and its backward
+    idf = synth.normal(22, "id", (n, h, w, c))
+    t = yr + idf
+    amb_t = relu_ambiguous(t, False)
+    outr = P.relu_fwd(t)
+    out = torch.empty_like(x)
+    B.bnr_bn_add_relu_fwd(x, bn, dev(idf, False), out)
+    g = synth.normal(22, "g", (n, h, w, c))
+    gm = torch.empty_like(x)
+    dg = torch.empty(c, dtype=torch.float32, device="cuda")
+    db = torch.empty_like(dg)
+    B.bnr_bn_add_relu_bwd(dev(g, False), out, x, bn, gm, dg, db)
+    torch.cuda.synchronize()
+    assert_close("bn+add+relu", host(out), outr, 1e-4, exclude=amb_t)
+    gmr = P.relu_bwd(g.astype(np.float64), t)
+    _, dg2, db2 = P.bn_bwd(x64, gmr, bp["gamma"], mu, rstd)
+    assert_close("bn+add+relu bwd dgamma", host(dg), dg2, 1e-4)
+    assert_close("bn+add+relu bwd dbeta", host(db), db2, 1e-4)
+    # unfused BN -> ReLU (two-pass statistics) forward and backward.  Its mean
+    # is a plain float32 sum of x (the two-pass layer takes no shift), good to
+    # about 1e-3 std at this offset; the consumers are checked against the
+    # oracle's formulas at the statistics the GPU produced (mean + mean_lo in
+    # float64, rstd), which is what they can be held to.
+    bn2 = robust_bn()
+    y = torch.empty_like(x)
+    z = torch.empty_like(x)
+    B.bnr_reference_bn_relu(False, x, bn2, y, z)
+    gz = synth.normal(22, "gz", (n, h, w, c))
+    dy = torch.empty_like(x)
+    dx2 = torch.empty_like(x)
+    torch.cuda.synchronize()
+    mu2 = host(bn2.mean).astype(np.float64) + host(bn2.mean_lo).astype(np.float64)
+    rs2 = host(bn2.rstd).astype(np.float64)
+    assert np.max(np.abs(mu2 - mu) * rstd) < 1e-2, "two-pass mean"
+    y2r = bp["gamma"] * ((x64 - mu2) * rs2) + bp["beta"]
+    amb2 = relu_ambiguous(y2r, False)
+    B.bnr_reference_bn_relu(True, x, bn2, y, z, gz=dev(gz, False), dy=dy, dgamma=dg, dbeta=db, dx=dx2)
+    torch.cuda.synchronize()
+    assert_close("two-pass y", host(y), y2r, 1e-4)
+    dyr = P.relu_bwd(gz.astype(np.float64), y2r)
+    dxr2, dgr2, _ = P.bn_bwd(x64, dyr, bp["gamma"], mu2, rs2)
+    assert_close("two-pass dx", host(dx2), dxr2, 1e-4, exclude=amb2)
+    assert_close("two-pass dgamma", host(dg), dgr2, 1e-4)
+    # one-sweep statistics around the shift: mean + mean_lo is the float64 mean
+    full = host(bn.mean).astype(np.float64) + host(bn.mean_lo).astype(np.float64)
+    assert np.max(np.abs(full - mu) * rstd) < 1e-6, "mean + mean_lo"
+
+
+def test_net_ends_at_large_offset(B):
+    """BN-ReLU-max-pooling forward and backward and the classifier head's
+    pooled features on float32 data at |mean| / std = 1e4, with the mean
+    given as its float32 value plus the low part, against the oracle."""
+    from helpers import assert_close
+    n, h, w, c = 2, 14, 14, 32
+    xf = synth.normal(23, "x", (n, h, w, c)) + np.float32(1.0e4)
+    x64 = xf.astype(np.float64)
+    bp = synth.bn_params(23, "bn", c)
+    yr, mu, var, rstd = P.bn_fwd(x64, bp["gamma"], bp["beta"], 1e-5)
+    m32 = mu.astype(np.float32)
+    lo32 = (mu - m32.astype(np.float64)).astype(np.float32)
+    r32 = rstd.astype(np.float32)
+    bn = B.BN(f32dev(bp["gamma"]), f32dev(bp["beta"]), 1e-5, mean=f32dev(m32), rstd=f32dev(r32))
+    bn.mean_lo = f32dev(lo32)
+    y = bp["gamma"] * ((x64 - mu) * r32.astype(np.float64)) + bp["beta"]
+    z = P.relu_fwd(y)
+    x = dev(xf, False)
+    ho, wo = (h - 1) // 2 + 1, (w - 1) // 2 + 1
+    out = torch.empty((n, ho, wo, c), dtype=torch.float32, device="cuda")
+    B.bnr_bn_relu_maxpool_fwd(x, bn, out, n, h, w)
+    gy = synth.normal(23, "gy", (n, ho, wo, c))
+    dy = torch.empty_like(x)
+    dg = torch.empty(c, dtype=torch.float32, device="cuda")
+    db = torch.empty_like(dg)
+    B.bnr_maxpool_bn_bwd(x, bn, dev(gy, False), dy, n, h, w, dg, db)
+    # head: pooled features of relu(bn(x))
+    K = 10
+    wfc = synth.normal(23, "wfc", (c, K)) * np.float32(0.1)
+    bfc = synth.normal(23, "bfc", (K,))
+    labels = synth._gen(23, "labels").integers(0, K, size=n).astype(np.int32)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    ft, lg, dl, ls = torch.empty((n, c), **f32), torch.empty((n, K), **f32), torch.empty((n, K), **f32), torch.empty(1 + n, **f32)
+    B.bnr_head_fwd(x, bn, dev(wfc, False), f32dev(bfc), torch.from_numpy(labels).cuda(), ft, lg, dl, ls, n, h, w)
+    torch.cuda.synchronize()
+    assert_close("BN-ReLU-max-pool", host(out), P.maxpool_fwd(z, 3, 2, 1), 1e-5)
+    dyr = P.relu_bwd(P.maxpool_bwd(z, gy.astype(np.float64), 3, 2, 1), y)
+    _, dgr, dbr = P.bn_bwd(x64, dyr, bp["gamma"], mu, r32.astype(np.float64))
+    assert_close("max-pool BN backward dy", host(dy), dyr, 1e-5)
+    assert_close("max-pool BN backward dgamma", host(dg), dgr, 1e-5)
+    assert_close("max-pool BN backward dbeta", host(db), dbr, 1e-5)
+    assert_close("head features", host(ft), P.global_avgpool_fwd(z), 1e-5)
