@@ -6,8 +6,10 @@ A step is one forward + backward pass of the whole block (six composite
 layers + transition) over one batch of synthetic inputs already resident in
 HBM.  Each variant's step is captured once in a HIP graph and replayed.
 Variants: fused (BN fission/fusion + inter-composite-layer fusion: the
-headline value), fused_no_icf (fission/fusion inside composite layers only)
-and unfused (the reference layer chain).
+headline value), fused_no_icf (fission/fusion inside composite layers only),
+fused_o2 (that, with the paper's stored O2' sweep: the backward reads the
+stored BN+ReLU outputs instead of recomputing them) and unfused (the
+reference layer chain).
 
 Prints one JSON line (rank 0).  Options: --gpus (1 only), --steps, --warmup,
 --workload {dense_block,bottleneck,single_layer,resnet_stack,densenet121}, --no-graph,
@@ -60,7 +62,7 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true")
-    ap.add_argument("--only", choices=["fused", "fused_no_icf", "fused_overlap", "fused_robust", "unfused",
+    ap.add_argument("--only", choices=["fused", "fused_no_icf", "fused_o2", "fused_overlap", "fused_robust", "unfused",
                                        "unfused_rcf",
                                        "unfused_rcf_mvf"],
                     default=None)
@@ -86,6 +88,8 @@ def build_workloads(args, torch):
         variants.insert(2, ("fused_overlap", dict(fused=True, overlap=True)))
         # the same fused step with robust one-sweep statistics (sums around the running mean)
         variants.insert(3, ("fused_robust", dict(fused=True, robust=True)))
+        # BNFF with the paper's stored O2' sweep (the backward reads relu(bn(x)) instead of recomputing it)
+        variants.insert(2, ("fused_o2", dict(fused=True, icf=False, o2=True)))
     if args.workload in ("dense_block", "resnet_stack", "densenet121") and not args.no_ablation:
         # the paper's intermediate endpoints (Sec. 5): ReLU-CONV fusion, then + mean/variance fusion
         from paper_1807_01702_amd import bnr as B
@@ -515,7 +519,8 @@ def main():
         "fused_no_icf": ({"images_per_s": noicf["images"] / (noicf["ms"] / 1e3), "ms_per_step": noicf["ms"],
                           "algorithmic_bytes": model.get("fused_no_icf")} if noicf else None),
         "speedup_vs_unfused": (unf["ms"] / fused["ms"]) if (fused and unf) else None,
-        "ablation": {k: {"images_per_s": v["images"] / (v["ms"] / 1e3), "ms_per_step": v["ms"]}
+        "ablation": {k: {"images_per_s": v["images"] / (v["ms"] / 1e3), "ms_per_step": v["ms"],
+                         **({"algorithmic_bytes": model[k]} if k in model else {})}
                      for k, v in res.items()},
         "hbm_bytes_per_step": {"algorithmic_fused": model["fused"], "algorithmic_unfused": model["unfused"]},
         "roofline": roofline(kernels, dtype, args.workload) if kernels else None,

@@ -189,6 +189,19 @@ bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr
                                 const void *w, void *y, bnr_bn *y_bn,
                                 void *ws, size_t ws_bytes, void *stream);
 
+/* bnr_bn_relu_conv_fwd that also writes the BN+ReLU output it feeds to the
+ * CONV, z = relu(gamma*(x-mean)*rstd+beta), to the view z[m][c_in] (pixel
+ * stride z_ldc): the O2' sweep of the paper's fused (sub-BN2)-ReLU-CONV layer
+ * (Sec. 3.2), materialised for the BN backward.  z holds exactly the values
+ * the CONV multiplies (in the storage type).  The backward that reads it is
+ * bnr_bwd_fused_o2; bnr_bn_relu_conv_fwd + bnr_bwd_fused is the same
+ * computation with z recomputed from x instead (one sweep fewer).
+ * Workspace: bnr_workspace_size(d).  Errors as bnr_bn_relu_conv_fwd, plus
+ * BNR_ERR_NULL for z NULL, BNR_ERR_ALIAS if z overlaps x, y or w. */
+bnr_status bnr_bn_relu_conv_fwd_o2(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn,
+                                   const void *w, void *y, bnr_bn *y_bn, void *z, int32_t z_ldc,
+                                   void *ws, size_t ws_bytes, void *stream);
+
 /* DenseNet transition layer, fused (Sec. 2.3 transition layer; Sec. 3.2
  * (sub-BN2)-ReLU-CONV fusion): y = avgpool2x2(conv1x1(relu(bn(x)))) computed
  * as conv1x1(avgpool2x2(relu(bn(x)))) -- both operations are linear, so the
@@ -280,6 +293,21 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
                          const bnr_grad_src *g_src, float *dw, float *dgamma, float *dbeta, void *dy,
                          void *dx, int32_t dx_ldc, int32_t dx_accumulate,
                          void *ws, size_t ws_bytes, void *stream);
+
+/* bnr_bwd_fused for a forward run by bnr_bn_relu_conv_fwd_o2 (the paper's
+ * O2' structure, Sec. 3.2): z is that forward's stored BN+ReLU output (view
+ * [m][c_in], pixel stride z_ldc).  Step 1's epilogue reads z in place of x:
+ * dy = dz*[z>0] and xhat = (z - beta)/gamma wherever dy can be non-zero (so
+ * z's rounding enters dgamma through xhat); a thread whose 16-byte channel
+ * vector holds a channel with gamma = 0 (xhat not recoverable from z) reads x
+ * there instead, with the formulas of bnr_bwd_fused.  Step 3 multiplies z as
+ * it is (no recompute).  Step 4 and the outputs are those of bnr_bwd_fused
+ * (x is still the BN input).  Errors as bnr_bwd_fused, plus BNR_ERR_NULL for
+ * x_bn or z NULL and BNR_ERR_ALIAS if z overlaps dy or dx. */
+bnr_status bnr_bwd_fused_o2(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *z,
+                            int32_t z_ldc, const void *w, const bnr_grad_src *g_src, float *dw, float *dgamma,
+                            float *dbeta, void *dy, void *dx, int32_t dx_ldc, int32_t dx_accumulate,
+                            void *ws, size_t ws_bytes, void *stream);
 
 /* The two independent halves of bnr_bwd_fused (and of bnr_bwd_fused_split
  * below), for callers that overlap a layer's weight gradient with the data

@@ -92,6 +92,10 @@ _lib_fns = dict(
                                   c_i32, c_vp, c_i32, c_vp, c_vp, _P(BNStruct), c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_pool_fwd=_sig("bnr_bn_relu_conv_pool_fwd", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
                                    c_vp, _P(BNStruct), c_vp, c_sz, c_vp),
+    bnr_bn_relu_conv_fwd_o2=_sig("bnr_bn_relu_conv_fwd_o2", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp,
+                                 c_vp, _P(BNStruct), c_vp, c_i32, c_vp, c_sz, c_vp),
+    bnr_bwd_fused_o2=_sig("bnr_bwd_fused_o2", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct), c_vp, c_i32, c_vp,
+                          _P(GradSrc), c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_i32, c_vp, c_sz, c_vp),
     bnr_bn_relu_conv_fwd_static=_sig("bnr_bn_relu_conv_fwd_static", ctypes.c_int, _P(ConvDesc), c_vp, _P(BNStruct),
                                      c_vp, c_vp, _P(BNStruct), c_vp),
     bnr_avgpool2_fwd=_sig("bnr_avgpool2_fwd", ctypes.c_int, c_i32, c_i32, c_i32, c_i32, ctypes.c_int, c_vp, c_i32,
@@ -331,6 +335,17 @@ def bnr_bn_relu_conv_pool_fwd(desc, x, x_bn, w, y, y_bn=None):
                                                  ctypes.byref(ys) if ys is not None else None, ws, wsb, _stream()))
 
 
+def bnr_bn_relu_conv_fwd_o2(desc, x, x_bn, w, y, z, y_bn=None):
+    """bnr_bn_relu_conv_fwd that also writes z = relu(bn(x)) (the O2' sweep) to the view z."""
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    xs = x_bn.struct()
+    ys = y_bn.struct() if y_bn is not None else None
+    pz, _, _, ldz = view(z)
+    _check(_lib_fns["bnr_bn_relu_conv_fwd_o2"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), _ptr(w), _ptr(y),
+                                               ctypes.byref(ys) if ys is not None else None, pz, ldz, ws, wsb,
+                                               _stream()))
+
+
 def bnr_bn_relu_conv_fwd_static(desc, x, x_bn, w, y, y_bn=None):
     """bnr_bn_relu_conv_fwd on the library's static per-GPU scratch (no workspace, no allocation)."""
     xs = x_bn.struct()
@@ -395,6 +410,21 @@ def bnr_bwd_fused(desc, x, x_bn, w, g_src, dw, dgamma=None, dbeta=None, dy=None,
     _check(_lib_fns["bnr_bwd_fused"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs) if xs is not None else None,
                                      _ptr(w), ctypes.byref(gs), _ptr(dw), _ptr(dgamma), _ptr(dbeta), _ptr(dy), dxp,
                                      dx_ldc, 1 if dx_accumulate else 0, ws, wsb, _stream()))
+    del keep
+
+
+def bnr_bwd_fused_o2(desc, x, x_bn, z, w, g_src, dw, dgamma, dbeta, dy, dx=None, dx_accumulate=False):
+    """bnr_bwd_fused reading the forward's stored z (O2') instead of recomputing it from x."""
+    ws, wsb = workspace(bnr_workspace_size(desc), x.device)
+    gs, keep = _grad_struct(g_src)
+    xs = x_bn.struct()
+    pz, _, _, ldz = view(z)
+    dxp, dx_ldc = (None, 0)
+    if dx is not None:
+        dxp, _, _, dx_ldc = view(dx)
+    _check(_lib_fns["bnr_bwd_fused_o2"](ctypes.byref(desc), _ptr(x), ctypes.byref(xs), pz, ldz, _ptr(w),
+                                        ctypes.byref(gs), _ptr(dw), _ptr(dgamma), _ptr(dbeta), _ptr(dy), dxp, dx_ldc,
+                                        1 if dx_accumulate else 0, ws, wsb, _stream()))
     del keep
 
 

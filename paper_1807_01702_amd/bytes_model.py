@@ -34,7 +34,8 @@ byte traffic of each driver's kernel sequence.
 
 
 def sweeps_per_bn():
-    return {"fwd_unfused": 8, "fwd_fused": 2, "bwd_unfused": 12, "bwd_fused": 7}
+    # fwd_fused_o2: the paper's fused layer also writes the BN+ReLU output (O2')
+    return {"fwd_unfused": 8, "fwd_fused": 2, "fwd_fused_o2": 3, "bwd_unfused": 12, "bwd_fused": 7}
 
 
 class _Acc:
@@ -46,11 +47,13 @@ class _Acc:
         return self
 
 
-def _unit_fused_fwd(a, m, ci, co, k, e, stats_sweep, out_stats=True):
+def _unit_fused_fwd(a, m, ci, co, k, e, stats_sweep, out_stats=True, save_z=False):
     if stats_sweep:
         a += m * ci * e                       # standalone sub-BN1: one read sweep
     a += m * ci * e + k * k * ci * co * e     # CONV reads x (normalise + ReLU on load) and weights
     a += m * co * e                           # writes its output (statistics of it in the epilogue)
+    if save_z:
+        a += m * ci * e                       # O2': also writes relu(bn(x)) (the backward reads it in place of x)
 
 
 def _unit_fused_bwd(a, m, ci, co, k, e, g_bytes, dx_mode):
@@ -119,8 +122,9 @@ def bottleneck(m, ci, width, k, e):
 
 def _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode, in_sweep=True):
     """Forward of a dense block (+ transition) in mode 'icf' (fused with
-    inter-composite-layer fusion), 'fused' or 'unfused'; in_sweep (icf): the
-    block input's statistics need their own sweep."""
+    inter-composite-layer fusion), 'fused', 'o2' (fused, the composite layers'
+    BN+ReLU outputs stored: the paper's O2' sweep) or 'unfused'; in_sweep
+    (icf): the block input's statistics need their own sweep."""
     c = c0
     if mode == "icf" and in_sweep:
         a += m * c0 * e                                          # the one statistics sweep (block input)
@@ -129,8 +133,8 @@ def _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode, in_sweep=True):
             _unit_ref_fwd(a, m, c, width, 1, e)
             _unit_ref_fwd(a, m, width, k, 3, e)
         else:
-            _unit_fused_fwd(a, m, c, width, 1, e, mode == "fused")
-            _unit_fused_fwd(a, m, width, k, 3, e, False)
+            _unit_fused_fwd(a, m, c, width, 1, e, mode in ("fused", "o2"), save_z=mode == "o2")
+            _unit_fused_fwd(a, m, width, k, 3, e, False, save_z=mode == "o2")
         c += k
     if trans_out:
         if mode == "unfused":
@@ -139,7 +143,7 @@ def _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode, in_sweep=True):
         else:
             # BN, ReLU and the 2x2 average in the CONV's prologue: read x,
             # write only the pooled output
-            if mode == "fused":
+            if mode in ("fused", "o2"):
                 a += m * c * e                                   # the transition BN's statistics sweep
             a += m * c * e + c * trans_out * e + m // 4 * trans_out * e
     return c
@@ -152,7 +156,7 @@ def _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode):
     if trans_out:
         if mode == "icf":
             _unit_split_bwd(a, m, ct, trans_out, 1, e, m // 4 * trans_out * e, False)
-        elif mode == "fused":
+        elif mode in ("fused", "o2"):
             _unit_fused_bwd(a, m, ct, trans_out, 1, e, m // 4 * trans_out * e, "write")
         else:
             a += m // 4 * trans_out * e + m * trans_out * e      # unfused: materialised pooling gradient
@@ -162,7 +166,7 @@ def _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode):
         if mode == "icf":
             _unit_fused_bwd(a, m, width, k, 3, e, 2 * m * k * e, None)     # summed gradient + slice on load
             _unit_split_bwd(a, m, c, width, 1, e, 2 * m * width * e, True)
-        elif mode == "fused":
+        elif mode in ("fused", "o2"):             # (o2: the epilogue and wgrad read z in place of x)
             _unit_fused_bwd(a, m, width, k, 3, e, m * k * e, None)
             _unit_fused_bwd(a, m, c, width, 1, e, 2 * m * width * e, "accumulate")
         else:
@@ -174,12 +178,12 @@ def _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode):
 
 def dense_block(m, c0, layers, width, k, trans_out, e):
     out = {}
-    for mode in ("icf", "fused", "unfused"):
+    for mode in ("icf", "fused", "o2", "unfused"):
         a = _Acc()
         _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode)
         _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode)
         out[mode] = a.total
-    return {"fused": out["icf"], "fused_no_icf": out["fused"], "unfused": out["unfused"]}
+    return {"fused": out["icf"], "fused_no_icf": out["fused"], "fused_o2": out["o2"], "unfused": out["unfused"]}
 
 
 def densenet(n, hw, c_in, c_stem, blocks, classes, e):

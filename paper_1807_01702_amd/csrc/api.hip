@@ -301,7 +301,7 @@ bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w
         TRY_HIP(launch_conv3x3(rp, s), transpose ? "conv data gradient" : "conv forward");
         return BNR_OK;
     }
-    if (rows_direct_weights(rp.dtype, rp.taps, rp.m, rp.K, rp.N, rp.a_ldc, rp.a2_ldc, rp.pro)) {
+    if (rows_direct_weights(rp.dtype, rp.taps, rp.m, rp.K, rp.N, rp.a_ldc, rp.a2_ldc, rp.pro, rp.side != nullptr)) {
         rp.wdirect = 1;                 // bf16 1x1: the tiled kernel reads the caller's weights, no packing
         rp.wraw = w;
         rp.wtrans = transpose;
@@ -321,11 +321,15 @@ size_t conv_fwd_ws(const ConvWs &w) { return w.pack + w.part + w.red; }
 // forward CONV with optional BN+ReLU prologue and optional statistics epilogue
 // (need: the workspace bytes checked; 0 = the whole conv workspace).  pool:
 // the BN+ReLU output is averaged over 2x2 windows before the 1x1 CONV, whose
-// output y is the pooled [n][h/2][w/2][c_out] view.
+// output y is the pooled [n][h/2][w/2][c_out] view.  z (BN+ReLU forward,
+// not pooled): the BN+ReLU output is also written to the view z (pixel stride
+// z_ldc), the materialised O2' sweep.
 bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w, void *y,
-                    bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream, size_t need = 0, bool pool = false)
+                    bnr_bn *y_bn, void *ws, size_t ws_bytes, void *stream, size_t need = 0, bool pool = false,
+                    void *z = nullptr, int32_t z_ldc = 0)
 {
     TRY(check_desc(d));
+    if (z && (pool || !x_bn)) return fail(BNR_ERR_UNSUPPORTED, "z is written by the BN+ReLU forward only");
     if (pool && (d->k != 1 || d->h % 2 || d->w % 2 || !x_bn))
         return fail(d->k != 1 ? BNR_ERR_UNSUPPORTED : BNR_ERR_SHAPE,
                     "pooled forward: 1x1 CONV with BN, even h and w (k %d, h %d, w %d)", d->k, d->h, d->w);
@@ -344,6 +348,12 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
     const int64_t wbytes = (int64_t)d->k * d->k * d->c_in * d->c_out * es;
     Range rw{reinterpret_cast<uintptr_t>(w), reinterpret_cast<uintptr_t>(w) + (uintptr_t)wbytes};
     if (overlap(ry, rw)) return fail(BNR_ERR_ALIAS, "y overlaps w");
+    if (z) {
+        TRY(check_channels(d->c_in, z_ldc, d->dtype, "z"));
+        const Range rz = view_range(z, m, d->c_in, z_ldc, es);
+        if (overlap(rz, view_range(x, m, d->c_in, d->in_ldc, es)) || overlap(rz, ry) || overlap(rz, rw))
+            return fail(BNR_ERR_ALIAS, "z overlaps x, y or w");
+    }
 
     hipStream_t s = (hipStream_t)stream;
     const ConvPtrs wp = conv_ptrs(ws, cw);
@@ -359,6 +369,7 @@ bnr_status conv_fwd(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, c
         rp.p_gamma = x_bn->gamma; rp.p_beta = x_bn->beta; rp.p_mean = cx.mean; rp.p_rstd = x_bn->rstd;
         rp.p_ctr = cx.ctr;
     }
+    rp.side = z; rp.side_ldc = z_ldc;
     rp.epi = y_bn ? EPI_STATS : EPI_STORE;
     rp.y = y; rp.y_ldc = d->out_ldc;
     rp.part = part;
@@ -468,6 +479,15 @@ bnr_status bnr_bn_relu_conv_fwd(const bnr_conv_desc *d, const void *x, const bnr
 {
     if (!x_bn) return fail(BNR_ERR_NULL, "x_bn is NULL");
     return conv_fwd(d, x, x_bn, w, y, y_bn, ws, ws_bytes, stream);
+}
+
+bnr_status bnr_bn_relu_conv_fwd_o2(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
+                                   void *y, bnr_bn *y_bn, void *z, int32_t z_ldc, void *ws, size_t ws_bytes,
+                                   void *stream)
+{
+    if (!x_bn) return fail(BNR_ERR_NULL, "x_bn is NULL");
+    if (!z) return fail(BNR_ERR_NULL, "z is NULL");
+    return conv_fwd(d, x, x_bn, w, y, y_bn, ws, ws_bytes, stream, 0, false, z, z_ldc);
 }
 
 bnr_status bnr_bn_relu_conv_fwd_static(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
@@ -588,10 +608,12 @@ bnr_status bnr_avgpool2_bwd(int32_t n, int32_t h, int32_t w, int32_t c, bnr_dtyp
 // the dbeta/dgamma combine (with split: also alpha/betap), the weight gradient.
 enum { BWD_DATA = 1, BWD_WEIGHTS = 2 };
 
+// z (with x_bn): the stored BN+ReLU output of the forward (O2'), read by the
+// BN-backward epilogue in place of x and by the weight gradient as its operand.
 static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
                             const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *y, int64_t y_ldc,
                             int y_scale, int y_acc, const SplitTerms *split, void *ws, hipStream_t s,
-                            int parts = BWD_DATA | BWD_WEIGHTS)
+                            int parts = BWD_DATA | BWD_WEIGHTS, const void *z = nullptr, int64_t z_ldc = 0)
 {
     const ConvWs cw = conv_ws(d);
     const ConvPtrs cp = conv_ptrs(ws, cw);
@@ -628,6 +650,7 @@ static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn 
         const Centred cx = centred(x_bn, rp.dtype);
         rp.e_gamma = x_bn->gamma; rp.e_beta = x_bn->beta; rp.e_mean = cx.mean; rp.e_rstd = x_bn->rstd;
         rp.e_ctr = cx.ctr;
+        if (z) { rp.e_zsrc = 1; rp.ex = z; rp.ex_ldc = z_ldc; rp.ex2 = x; rp.ex2_ldc = d->in_ldc; }
     } else {
         rp.epi = EPI_STORE; rp.y = y; rp.y_ldc = y_ldc; rp.accumulate = y_acc ? 1 : 0;
     }
@@ -641,13 +664,13 @@ static bnr_status bwd_steps(const bnr_conv_desc *d, const void *x, const bnr_bn 
     }
     }
     if (!(parts & BWD_WEIGHTS)) return BNR_OK;
-    // 3. weight gradient, both operands recomputed on load
+    // 3. weight gradient, both operands recomputed on load (z: read as it is)
     WgradParams wp;
     memset(&wp, 0, sizeof wp);
     wp.dtype = dt; wp.k = d->k; wp.n = d->n; wp.h = d->h; wp.w = d->w; wp.m = m;
     wp.c_in = d->c_in; wp.c_out = d->c_out;
-    wp.x = x; wp.x_ldc = d->in_ldc;
-    if (x_bn) {
+    wp.x = z ? z : x; wp.x_ldc = z ? z_ldc : d->in_ldc;
+    if (x_bn && !z) {
         wp.a_mode = 1;
         const Centred cx = centred(x_bn, dt);
         wp.a_gamma = x_bn->gamma; wp.a_beta = x_bn->beta; wp.a_mean = cx.mean; wp.a_rstd = x_bn->rstd;
@@ -703,7 +726,8 @@ static bool grad_src_overlaps(const bnr_conv_desc *d, const bnr_grad_src *g, Ran
 
 static bnr_status bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,
                             const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy, void *dx,
-                            int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream, int parts)
+                            int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream, int parts,
+                            const void *z = nullptr, int32_t z_ldc = 0)
 {
     TRY(check_desc(d));
     TRY(check_ptr(x, "x"));
@@ -742,9 +766,18 @@ static bnr_status bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn 
         if (grad_src_overlaps(d, g, rdx)) return fail(BNR_ERR_ALIAS, "dx overlaps a view g_src reads");
         if (!x_bn && overlap(rdx, rx)) return fail(BNR_ERR_ALIAS, "dx overlaps x");
     }
+    if (z) {
+        if (!x_bn) return fail(BNR_ERR_NULL, "z needs x_bn");
+        TRY(check_ptr(z, "z"));
+        TRY(check_channels(d->c_in, z_ldc, d->dtype, "z"));
+        const Range rz = view_range(z, m, d->c_in, z_ldc, es);
+        if (overlap(rz, view_range(dy, m, d->c_in, d->c_in, es)) ||
+            (dx && overlap(rz, view_range(dx, m, d->c_in, dx_ldc, es))))
+            return fail(BNR_ERR_ALIAS, "z overlaps dy or dx");
+    }
 
     hipStream_t s = (hipStream_t)stream;
-    if (x_bn) TRY(bwd_steps(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, d->c_in, 0, 0, nullptr, ws, s, parts));
+    if (x_bn) TRY(bwd_steps(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, d->c_in, 0, 0, nullptr, ws, s, parts, z, z_ldc));
     else TRY(bwd_steps(d, x, nullptr, w, g, dw, nullptr, nullptr, dx, dx_ldc, 0, dx_accumulate, nullptr, ws, s, parts));
     // 4. optional standalone BN input gradient
     if ((parts & BWD_DATA) && x_bn && dx) {
@@ -762,6 +795,16 @@ bnr_status bnr_bwd_fused(const bnr_conv_desc *d, const void *x, const bnr_bn *x_
 {
     return bwd_fused(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, dx, dx_ldc, dx_accumulate, ws, ws_bytes, stream,
                      BWD_DATA | BWD_WEIGHTS);
+}
+
+bnr_status bnr_bwd_fused_o2(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *z, int32_t z_ldc,
+                            const void *w, const bnr_grad_src *g, float *dw, float *dgamma, float *dbeta, void *dy,
+                            void *dx, int32_t dx_ldc, int32_t dx_accumulate, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!x_bn) return fail(BNR_ERR_NULL, "x_bn is NULL");
+    if (!z) return fail(BNR_ERR_NULL, "z is NULL");
+    return bwd_fused(d, x, x_bn, w, g, dw, dgamma, dbeta, dy, dx, dx_ldc, dx_accumulate, ws, ws_bytes, stream,
+                     BWD_DATA | BWD_WEIGHTS, z, z_ldc);
 }
 
 bnr_status bnr_bwd_data(const bnr_conv_desc *d, const void *x, const bnr_bn *x_bn, const void *w,

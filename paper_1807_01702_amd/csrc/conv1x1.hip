@@ -59,19 +59,24 @@ static P1Geom p1_geom(int K, int N)
 // BN+ReLU with the statistics epilogue), PC_BNRELU_POOL (BN+ReLU and the 2x2
 // average of each window: a tile row loads four input pixels), PC_BNADD (the
 // residual block's BN + identity + ReLU: a second operand, and the result is
-// stored as a side output), PC_RUNTIME (PRO_NONE / PRO_BNRELU / PRO_RELU /
-// PRO_POOLUP chosen at run time).
-enum { PC_RUNTIME = 0, PC_BNGRAD = 1, PC_BNRELU = 2, PC_BNRELU_POOL = 3, PC_BNADD = 4 };
+// stored as a side output), PC_BNRELU_SAVE (BN+ReLU whose result z is also
+// stored as a side output: the materialised O2' sweep), PC_RUNTIME (PRO_NONE /
+// PRO_BNRELU / PRO_RELU / PRO_POOLUP chosen at run time).
+// The BN-backward epilogues read z instead of x when p.e_zsrc is set (see
+// the epilogue parameters below).
+enum { PC_RUNTIME = 0, PC_BNGRAD = 1, PC_BNRELU = 2, PC_BNRELU_POOL = 3, PC_BNADD = 4, PC_BNRELU_SAVE = 5 };
 
 template <int CBW, int NVA, int EK, int PC, int BM>
 __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 {
     constexpr bool BNADD = PC == PC_BNADD;
+    constexpr bool SAVE = PC == PC_BNRELU_SAVE;
+    constexpr bool SIDE = BNADD || SAVE;                  // the transformed A rows are also stored
     constexpr bool BNG = PC == PC_BNGRAD;
     constexpr bool TWO = BNG || BNADD;                     // the prologue reads a second operand
     constexpr bool POOLF = PC == PC_BNRELU_POOL;          // rows are 2x2 windows of the input
     constexpr int PF = POOLF ? 4 : 1;                      // input pixels per A row
-    const int pro = PC == PC_BNRELU || POOLF || BNADD ? PRO_BNRELU : (PC == PC_BNGRAD ? PRO_BNGRAD : p.pro);
+    const int pro = PC == PC_BNRELU || POOLF || SIDE ? PRO_BNRELU : (PC == PC_BNGRAD ? PRO_BNGRAD : p.pro);
     using T = bf16_t;
     using M = Mfma<T>;
     constexpr int VEC = 8;
@@ -101,11 +106,14 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((arows - 1) * a_ldc + K) * 2));
     const __amdgpu_buffer_rsrc_t a2buf = buf_view(TWO ? p.a2 : p.a, TWO ? (uint32_t)(((int64_t)(m - 1) * a2_ldc + K) * 2) : 0u);
     const int side_ldc = (int)p.side_ldc;
-    const __amdgpu_buffer_rsrc_t sbuf = buf_view(BNADD ? p.side : p.a,
-                                                 BNADD ? (uint32_t)(((int64_t)(m - 1) * side_ldc + K) * 2) : 0u);
+    const __amdgpu_buffer_rsrc_t sbuf = buf_view(SIDE ? p.side : p.a,
+                                                 SIDE ? (uint32_t)(((int64_t)(m - 1) * side_ldc + K) * 2) : 0u);
     const __amdgpu_buffer_rsrc_t ybuf = buf_view(p.y, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * 2));
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * 2) : 0u);
+    const int ex2_ldc = (int)p.ex2_ldc;
+    const __amdgpu_buffer_rsrc_t x2buf = buf_view(p.ex2 ? p.ex2 : p.y,
+                                                  p.ex2 ? (uint32_t)(((int64_t)(m - 1) * ex2_ldc + N) * 2) : 0u);
 
     // ---- weights -> LDS as Ws[n][k] (zero outside K x N), in batches of
     // kWB vectors per thread whose loads are all in flight before any write ----
@@ -278,7 +286,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 for (int e = 0; e < VEC; e++) acc[e] *= 0.25f;
                 put(j, Elem<T>::pack(acc));
             }
-        } else if (pro == PRO_BNRELU) {                   // z = max(x c0 + c1, 0)
+        } else if (pro == PRO_BNRELU) {                   // z = max(x c0 + c1, 0)   (SAVE: also stored)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int c = sc[j] < KP ? sc[j] : 0;
@@ -291,7 +299,12 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                     const float t = bn_lin(f[e], ca[e], cb[e]);
                     f[e] = t > 0.f ? t : 0.f;
                 }
-                put(j, Elem<T>::pack(f));
+                const vec16 v = Elem<T>::pack(f);
+                put(j, v);
+                if (SAVE) {
+                    const int pp = p0 + sr[j];
+                    bst16(sbuf, j < nva && sc[j] < K && pp < lim ? (uint32_t)(pp * side_ldc + sc[j]) * 2u : kBufOff, v);
+                }
             }
         } else if (pro == PRO_RELU) {
             #pragma unroll
@@ -327,26 +340,46 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
     T *yout = reinterpret_cast<T *>(p.y);
+
+    __syncthreads();
+    // this thread's epilogue channels are fixed: keep their BN parameters in registers
+    float eM[VEC], eR[VEC], eG[VEC], eB[VEC], eC0[VEC], eC1[VEC], eS[VEC];
+    #pragma unroll
+    for (int e = 0; e < VEC; e++) {
+        eM[e] = epi[n + e]; eR[e] = epi[NP + n + e]; eG[e] = epi[2 * NP + n + e]; eB[e] = epi[3 * NP + n + e];
+        bn_coef(eG[e], eB[e], eM[e], eR[e], eC0[e], eC1[e]);     // the forward prologue's y = x c0 + c1
+        eS[e] = eC0[e];                                           // summed-gradient scale gamma rstd
+    }
+    // e_zsrc: the BN-backward operand is the stored z = relu(y) (the O2' sweep):
+    // mask [z > 0] (as fma(z, 1, 0) > 0) and xhat = (z - beta) / gamma where the
+    // mask passes; a thread whose channel vector holds a gamma = 0 channel
+    // (xhat not recoverable from z) reads x (ex2) with the usual parameters.
+    const bool zsrc = BNBWD && p.e_zsrc;
+    bool zs = zsrc && col_ok;
+    #pragma unroll
+    for (int e = 0; e < VEC; e++) zs = zs && eG[e] != 0.f;
+    if (zs)
+        #pragma unroll
+        for (int e = 0; e < VEC; e++) { eM[e] = eB[e]; eR[e] = 1.0f / eG[e]; eC0[e] = 1.f; eC1[e] = 0.f; }
     auto load_epi = [&](int p0, int lim) __attribute__((always_inline)) {
         if (!READS) return;
         #pragma unroll
         for (int j = 0; j < NVX; j++) {
             const int r = r0 + j * RSTEP, pp = p0 + r;
             const bool ok = col_ok && r < BM && pp < lim;
-            if (EK == EK_STORE_ACC) rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
-            else rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
+            if (EK == EK_STORE_ACC) {
+                rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
+            } else if (BNBWD && zsrc) {   // z, or x for a vector holding a gamma = 0 channel (one load is empty)
+                const vec16 a = bld16(xbuf, ok && zs ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
+                const vec16 b = bld16(x2buf, ok && !zs ? (uint32_t)(pp * ex2_ldc + n) * 2u : kBufOff);
+                #pragma unroll
+                for (int i = 0; i < 4; i++) rx[j].u[i] = a.u[i] | b.u[i];
+            } else {
+                rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
+            }
             if (EK == EK_BNBWD_SCACC) rd[j < NVD ? j : 0] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
         }
     };
-
-    __syncthreads();
-    // this thread's epilogue channels are fixed: keep their BN parameters in registers
-    float eM[VEC], eR[VEC], eG[VEC], eB[VEC], eC0[VEC], eC1[VEC];
-    #pragma unroll
-    for (int e = 0; e < VEC; e++) {
-        eM[e] = epi[n + e]; eR[e] = epi[NP + n + e]; eG[e] = epi[2 * NP + n + e]; eB[e] = epi[3 * NP + n + e];
-        bn_coef(eG[e], eB[e], eM[e], eR[e], eC0[e], eC1[e]);     // the forward prologue's y = x c0 + c1
-    }
     // work items: F rounds of whole tiles (item k < F is tile k*G + gi, rows
     // [p0, p0 + BM)), then this workgroup's share [lo, hi) of the R rows left
     const int G = gridDim.x, gi = blockIdx.x;
@@ -439,8 +472,8 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                     s1[e] += d;
                     s2[e] += d * xh;
                     if (EK == EK_BNBWD) f[e] = d;
-                    else if (EK == EK_BNBWD_SC) f[e] = d * eC0[e];
-                    else f[e] = __builtin_fmaf(d, eC0[e], old[e]);
+                    else if (EK == EK_BNBWD_SC) f[e] = d * eS[e];
+                    else f[e] = __builtin_fmaf(d, eS[e], old[e]);
                 }
                 vo[j] = Elem<T>::pack(f);
             }
@@ -521,6 +554,7 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
     double a = m * p.K;
     if (BNG) a *= 2.0;
     if (PC == PC_BNADD) a *= 3.0;                   // y and the identity read, the result written
+    if (PC == PC_BNRELU_SAVE) a *= 2.0;             // x read, z written
     if (p.pro == PRO_POOLUP) a /= 4.0;
     if (PC == PC_BNRELU_POOL) a *= 4.0;             // four input pixels per row
     double out = m * p.N;
@@ -599,10 +633,15 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
     if (bnadd && (!p.a2 || !p.side || p.wtrans || (p.epi != EPI_STORE && p.epi != EPI_STATS) || p.accumulate ||
                   !p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta))
         return hipErrorInvalidValue;
+    const bool save = p.pro == PRO_BNRELU && p.side;
+    if (save && (p.wtrans || (p.epi != EPI_STORE && p.epi != EPI_STATS) || p.accumulate)) return hipErrorInvalidValue;
+    if (p.side && !bnadd && !save) return hipErrorInvalidValue;
+    if (p.e_zsrc && (p.epi != EPI_BNBWD || !p.ex2)) return hipErrorInvalidValue;
     // 32-bit pixel indices and raw-buffer operand views: every span below 2^31 bytes
     const int64_t lim = (int64_t)1 << 31;
     const int64_t arows = poolf ? 4 * p.m : p.m;
-    if (bnadd && (p.m * p.side_ldc + p.K) * 2 >= lim) return hipErrorInvalidValue;
+    if ((bnadd || save) && (p.m * p.side_ldc + p.K) * 2 >= lim) return hipErrorInvalidValue;
+    if (p.ex2 && (p.m * p.ex2_ldc + p.N) * 2 >= lim) return hipErrorInvalidValue;
     if (p.m < 1 || arows >= (lim >> 1) || (arows * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
@@ -612,6 +651,8 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
                                      : run_p1_nva<EK_STORE, PC_BNRELU_POOL>(p, g, s, rows);
     if (bnadd) return ek == EK_STATS ? run_p1_nva<EK_STATS, PC_BNADD>(p, g, s, rows)
                                      : run_p1_nva<EK_STORE, PC_BNADD>(p, g, s, rows);
+    if (save) return ek == EK_STATS ? run_p1_nva<EK_STATS, PC_BNRELU_SAVE>(p, g, s, rows)
+                                    : run_p1_nva<EK_STORE, PC_BNRELU_SAVE>(p, g, s, rows);
     if (p.pro == PRO_BNGRAD) return run_p1_ek<PC_BNGRAD>(p, g, ek, s, rows);
     if (p.pro == PRO_BNRELU && ek == EK_STATS) return run_p1_nva<EK_STATS, PC_BNRELU>(p, g, s, rows);
     return run_p1_ek<PC_RUNTIME>(p, g, ek, s, rows);

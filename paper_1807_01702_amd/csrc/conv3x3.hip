@@ -138,13 +138,17 @@ __device__ __forceinline__ int p3_pixel(int P, const P3Geom &g, int H, int W)
 // BN input gradient, which reads a second operand), PC3_BNRELU (the forward
 // BN+ReLU with the statistics epilogue), PC3_RUNTIME (PRO_NONE / PRO_BNRELU /
 // PRO_RELU chosen at run time).
-enum { PC3_RUNTIME = 0, PC3_BNGRAD = 1, PC3_BNRELU = 2 };
+// PC3_BNRELU_SAVE: BN+ReLU whose result z is also stored (the materialised
+// O2' sweep; each workgroup stores the positions of its own range once).
+// The BN-backward epilogue reads z instead of x when p.e_zsrc is set.
+enum { PC3_RUNTIME = 0, PC3_BNGRAD = 1, PC3_BNRELU = 2, PC3_BNRELU_SAVE = 3 };
 
 template <int WK, int WN, int EK, int PC>
 __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
 {
     constexpr bool BNG = PC == PC3_BNGRAD;
-    const int pro = PC == PC3_BNRELU ? PRO_BNRELU : (PC == PC3_BNGRAD ? PRO_BNGRAD : p.pro);
+    constexpr bool SAVE = PC == PC3_BNRELU_SAVE;
+    const int pro = PC == PC3_BNRELU || SAVE ? PRO_BNRELU : (PC == PC3_BNGRAD ? PRO_BNGRAD : p.pro);
     using T = bf16_t;
     using M = Mfma<T>;
     constexpr int VEC = 8;
@@ -182,6 +186,11 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const __amdgpu_buffer_rsrc_t abuf = buf_view(p.a, (uint32_t)(((int64_t)(m - 1) * a_ldc + K) * ES));
     const __amdgpu_buffer_rsrc_t a2buf = buf_view(BNG ? p.a2 : p.a, BNG ? (uint32_t)(((int64_t)(m - 1) * a2_ldc + K) * ES) : 0u);
     const __amdgpu_buffer_rsrc_t ybuf = buf_view(p.y, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * ES));
+    const int side_ldc = (int)p.side_ldc, ex2_ldc = (int)p.ex2_ldc;
+    const __amdgpu_buffer_rsrc_t sbuf = buf_view(SAVE ? p.side : p.a,
+                                                 SAVE ? (uint32_t)(((int64_t)(m - 1) * side_ldc + K) * ES) : 0u);
+    const __amdgpu_buffer_rsrc_t x2buf = buf_view(p.ex2 ? p.ex2 : p.y,
+                                                  p.ex2 ? (uint32_t)(((int64_t)(m - 1) * ex2_ldc + N) * ES) : 0u);
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * ES) : 0u);
 
@@ -193,12 +202,14 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     // replaces ring rows in phase B of tile t; it is loaded AHEAD tiles
     // earlier into one of two register buffers, so its loads are in flight
     // for AHEAD tile periods.
-    struct Batch { vec16 a[NVA]; vec16 b[NVB]; int pix; };
+    // own: the position lies in this workgroup's range (SAVE stores it)
+    struct Batch { vec16 a[NVA]; vec16 b[NVB]; int pix; bool own; };
     auto load_rows = [&](int q0, int cnt, Batch &bt) __attribute__((always_inline)) {
         const int arow = tid >> 2;
         const P3Base b = p3_base(q0, g);
         const int pp = p3_pixel_at(b, q0 + arow, g, H, W);
         bt.pix = arow < cnt ? pp : -1;
+        bt.own = q0 + arow >= P0 && q0 + arow < P1;
         #pragma unroll
         for (int j = 0; j < NVA; j++) {
             const int c = (4 * j + (tid & 3)) * VEC;
@@ -276,6 +287,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         if (c < N && EK == EK_BNBWD) {      // mean, rstd and the forward's y = x c0 + c1
             e0 = p.e_mean[c]; e1 = p.e_rstd[c];
             bn_coef(p.e_gamma[c], p.e_beta[c], e0, e1, e2, e3);
+            // e_zsrc: the operand is the stored z = relu(y): mask [z > 0] as
+            // fma(z, 1, 0) > 0, xhat = (z - beta) / gamma, unless the channel's
+            // vector holds a gamma = 0 channel (its threads read x: ex2)
+            bool zv = p.e_zsrc != 0;
+            for (int i = c & ~(VEC - 1); i < (c & ~(VEC - 1)) + VEC; i++) zv = zv && p.e_gamma[i] != 0.f;
+            if (zv) { e0 = p.e_beta[c]; e1 = 1.0f / p.e_gamma[c]; e2 = 1.f; e3 = 0.f; }
         }
         if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[c];     // statistics of y - shift
         epi[c] = e0; epi[NPC + c] = e1; epi[2 * NPC + c] = e2; epi[3 * NPC + c] = e3;
@@ -294,6 +311,10 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const int v = tid % VPRO, r0 = tid / VPRO;
     const int n = v * VEC;
     const bool col_ok = n < N;
+    const bool zsrc = EK == EK_BNBWD && p.e_zsrc;
+    bool zs = zsrc && col_ok;                      // this thread's vector reads z (else x)
+    #pragma unroll
+    for (int e = 0; e < VEC; e++) zs = zs && p.e_gamma[col_ok ? n + e : 0] != 0.f;
 
     // ---- prologue transform of a batch, then the ring writes.  The mode
     // switch is wave-uniform and outside the vector loop; invalid rows are
@@ -340,6 +361,9 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                 outv[j] = Elem<T>::pack(f);
                 #pragma unroll
                 for (int i = 0; i < 4; i++) outv[j].u[i] &= keep;
+                if (SAVE)
+                    bst16(sbuf, live && bt.own && bt.pix >= 0 && c < K ? (uint32_t)(bt.pix * side_ldc + c) * ES : kBufOff,
+                          outv[j]);
             }
         } else if (pro == PRO_RELU) {                     // (padding rows load zeros)
             #pragma unroll
@@ -381,8 +405,16 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         for (int j = 0; j < NVX; j++) {
             const int pp = epix[j];
             const bool ok = pp >= 0;
-            if (EK == EK_STORE_ACC) rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * ES : kBufOff);
-            else rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * ES : kBufOff);
+            if (EK == EK_STORE_ACC) {
+                rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * ES : kBufOff);
+            } else if (EK == EK_BNBWD && zsrc) {   // z, or x (gamma = 0 in the vector): one load is empty
+                const vec16 a = bld16(xbuf, ok && zs ? (uint32_t)(pp * ex_ldc + n) * ES : kBufOff);
+                const vec16 b = bld16(x2buf, ok && !zs ? (uint32_t)(pp * ex2_ldc + n) * ES : kBufOff);
+                #pragma unroll
+                for (int i = 0; i < 4; i++) rx[j].u[i] = a.u[i] | b.u[i];
+            } else {
+                rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * ES : kBufOff);
+            }
         }
     };
 
@@ -594,7 +626,7 @@ static hipError_t run_p3(const RowsParams &p, const P3Geom &g, hipStream_t s)
     const int grid = (int)conv3x3_partial_rows(p.m);
     const double e = 2.0, m = (double)p.m;
     double a = m * p.K;
-    if (BNG) a *= 2.0;
+    if (BNG || PC == PC3_BNRELU_SAVE) a *= 2.0;     // second operand read / z written
     double out = m * p.N;
     if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD) out += m * p.N;
     TraceScope tr(KC_CONV, KID_CONV_3X3, s, e * (a + out + 9.0 * p.K * p.N), 2.0 * m * 9.0 * p.K * p.N);
@@ -643,10 +675,15 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
     if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return hipErrorInvalidValue;
     if (p.epi == EPI_RELUMASK && !p.ex) return hipErrorInvalidValue;
     if ((int64_t)p.n * p.h * p.w != p.m || p.m < 1) return hipErrorInvalidValue;
+    const bool save = p.pro == PRO_BNRELU && p.side;
+    if (p.side && (!save || p.wtrans || (p.epi != EPI_STORE && p.epi != EPI_STATS) || p.accumulate))
+        return hipErrorInvalidValue;
+    if (p.e_zsrc && (p.epi != EPI_BNBWD || !p.ex2)) return hipErrorInvalidValue;
     // 32-bit pixel indices and raw-buffer operand views: every span below 2^31 bytes
     const int64_t lim = (int64_t)1 << 31;
     if (p.m >= (lim >> 1) || (p.m * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
-        (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
+        (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim) ||
+        (save && (p.m * p.side_ldc + p.K) * 2 >= lim) || (p.ex2 && (p.m * p.ex2_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
     P3Geom g = p3_geom(p.K, p.N, p.w);
     g.PH = p.h + 2;
@@ -657,6 +694,8 @@ hipError_t launch_conv3x3(const RowsParams &p, hipStream_t s)
     if (mp >= (lim >> 1)) return hipErrorInvalidValue;
     g.MP = (int)mp;
     const int ek = epilogue_kind(p.epi, p.accumulate, 0);
+    if (save) return ek == EK_STATS ? run_p3_shape<EK_STATS, PC3_BNRELU_SAVE>(p, g, s)
+                                    : run_p3_shape<EK_STORE, PC3_BNRELU_SAVE>(p, g, s);
     if (p.pro == PRO_BNGRAD) return run_p3_ek<PC3_BNGRAD>(p, g, ek, s);
     if (p.pro == PRO_BNRELU && ek == EK_STATS) return run_p3_shape<EK_STATS, PC3_BNRELU>(p, g, s);
     return run_p3_ek<PC3_RUNTIME>(p, g, ek, s);

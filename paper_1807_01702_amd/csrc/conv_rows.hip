@@ -17,7 +17,9 @@
 //
 // Prologues (sub-BN2 side, Sec. 3.2):
 //   PRO_RELU   : a = max(x, 0)   (ReLU-CONV fusion alone, unfused-BN modes)
-//   PRO_BNRELU : a = max(gamma*(x-mean)*rstd + beta, 0)
+//   PRO_BNRELU : a = max(gamma*(x-mean)*rstd + beta, 0); with p.side set, a
+//                is also stored there (the materialised O2' sweep; general
+//                staging loop, by the first column tile, the tile's own rows)
 //   PRO_BNGRAD : a = A dy + B x + C  (deferred BN input gradient from dy and
 //                the BN input x; coefficients by deferred_coef)
 //   PRO_POOLUP : a = g[n][y/2][x/2] / 4   (2x2 average-pooling gradient)
@@ -31,7 +33,10 @@
 //   EPI_STATS  : store y, per-channel sum(y), sum(y^2) of the stored values
 //   EPI_BNBWD  : dy = dz * [gamma*xhat+beta > 0] with xhat from the BN input,
 //                store dy (e_scale: store or add gamma*rstd*dy), per-channel
-//                sum(dy), sum(dy*xhat)
+//                sum(dy), sum(dy*xhat); with e_zsrc, ex is the stored
+//                z = relu(y): mask [z > 0], xhat = (z - beta)/gamma, and a
+//                thread whose channel vector holds a gamma = 0 channel reads
+//                x (ex2) with the usual formulas instead
 //   EPI_RELUMASK: dy = dz * [y > 0] from a stored y (ReLU-CONV fusion alone)
 // float32 data: x - mean in the prologues and the BN-backward epilogue is
 // (x - K) - (mean - K) with the BN's centre K (bn_centre), x in PRO_BNGRAD is
@@ -324,6 +329,8 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                         f[e] = t > 0.f ? t : 0.f;
                     }
                     out = Elem<T>::pack(f);
+                    if (p.side && nt == 0 && r >= halo && r < halo + BM)
+                        stg16(reinterpret_cast<T *>(p.side) + pp * p.side_ldc + c, out);
                 } else if (p.pro == PRO_BNGRAD) {
                     float d[VEC], x[VEC];
                     Elem<T>::unpack(ldg16(asrc + pp * p.a_ldc + c), d);
@@ -418,14 +425,24 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     const int v = tid % VPRO, r0 = tid / VPRO;
     const int n = n0 + v * VEC;
     const bool col_ok = n < N;
-    float s1[VEC], s2[VEC], emu[VEC], ers[VEC], eg[VEC], eb[VEC], ek[VEC];
+    float s1[VEC], s2[VEC], emu[VEC], ers[VEC], eg[VEC], eb[VEC], ek[VEC], es[VEC];
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; ek[e] = 0.f; }
-    if (p.epi == EPI_BNBWD && col_ok)
+    const bool zsrc = p.epi == EPI_BNBWD && p.e_zsrc;
+    bool zs = zsrc && col_ok;                     // this thread's vector reads z (else x)
+    if (p.epi == EPI_BNBWD && col_ok) {
+        for (int e = 0; e < VEC; e++) zs = zs && p.e_gamma[n + e] != 0.f;
         for (int e = 0; e < VEC; e++) {
             emu[e] = p.e_mean[n + e]; ers[e] = p.e_rstd[n + e];
             ek[e] = bn_centre<T>(p.e_ctr, n + e);
             bn_coef(p.e_gamma[n + e], p.e_beta[n + e], emu[e], ers[e], eg[e], eb[e]);   // the forward's c0, c1
+            es[e] = eg[e];                                                             // summed-form scale
+            if (zs) {                             // mask fma(z, 1, 0) > 0, xhat = (z - beta) / gamma
+                emu[e] = p.e_beta[n + e]; ers[e] = 1.0f / p.e_gamma[n + e];
+                eg[e] = 1.f; eb[e] = 0.f; ek[e] = 0.f;
+            }
         }
+    }
+    const T *ex2s = reinterpret_cast<const T *>(p.ex2);
     if (p.epi == EPI_STATS)                       // statistics of y - shift
         for (int e = 0; e < VEC; e++) emu[e] = p.e_shift && col_ok ? p.e_shift[n + e] : 0.f;
     T *yout = reinterpret_cast<T *>(p.y);
@@ -460,7 +477,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             } else {
                 float f[VEC], x[VEC], old[VEC];
                 Elem<T>::unpack(cv, f);
-                Elem<T>::unpack(ldg16(exs + pp * p.ex_ldc + n), x);
+                Elem<T>::unpack(ldg16(zsrc && !zs ? ex2s + pp * p.ex2_ldc + n : exs + pp * p.ex_ldc + n), x);
                 if (p.e_scale && p.accumulate) Elem<T>::unpack(ldg16(dst), old);
                 for (int e = 0; e < VEC; e++) {
                     const float xc = x[e] - ek[e];
@@ -469,7 +486,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     s1[e] += d;
                     s2[e] += d * xh;
                     // summed-gradient form: gamma*rstd*dy, stored or added
-                    f[e] = !p.e_scale ? d : (p.accumulate ? __builtin_fmaf(d, eg[e], old[e]) : d * eg[e]);
+                    f[e] = !p.e_scale ? d : (p.accumulate ? __builtin_fmaf(d, es[e], old[e]) : d * es[e]);
                 }
                 stg16(dst, Elem<T>::pack(f));
             }
@@ -557,6 +574,7 @@ static double rows_algorithmic_bytes(const RowsParams &p)
     if (p.pro == PRO_POOLUP) a = m / 4.0 * K;                    // pooled gradient
     if (p.pro == PRO_BNRELU_POOL) a = 4.0 * m * K;               // four input pixels per window
     if (p.pro == PRO_BNADDRELU) a = 3.0 * m * K;                 // y and the identity read, the result written
+    if (p.pro == PRO_BNRELU && p.side) a = 2.0 * m * K;          // x read, z written
     double out = m * N;                                          // output write
     if (p.epi == EPI_STORE && p.accumulate) out += m * N;        // read-modify-write
     if (p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK) out += m * N;   // BN input / ReLU input read
@@ -574,9 +592,10 @@ static bool rows_spans_fit(int dtype, int64_t m, int K, int N, int64_t a_ldc, in
            ceil_div(N, 32) * 32 * ceil_div(K, kRowsBK) * kRowsBK * es < lim;
 }
 
-bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro)
+bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro,
+                         bool side)
 {
-    return dtype == DT_BF16 && taps == 1 && pro != PRO_BNRELU_POOL && pro != PRO_BNADDRELU &&
+    return dtype == DT_BF16 && taps == 1 && pro != PRO_BNRELU_POOL && pro != PRO_BNADDRELU && !side &&
            rows_spans_fit(dtype, m, K, N, a_ldc, a2_ldc, pro);
 }
 
@@ -598,7 +617,7 @@ static hipError_t run_rows(const RowsParams &p, hipStream_t s)
     TraceScope tr(KC_CONV, TAPS == 9 ? KID_CONV_3X3 : KID_CONV_1X1, s, rows_algorithmic_bytes(p),
                   2.0 * (double)p.m * TAPS * p.K * p.N);
     RowsParams q = p;
-    q.buf32 = TAPS == 1 && p.pro != PRO_BNRELU_POOL && p.pro != PRO_BNADDRELU &&
+    q.buf32 = TAPS == 1 && p.pro != PRO_BNRELU_POOL && p.pro != PRO_BNADDRELU && !p.side &&
               rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
     if (q.wdirect && (!q.buf32 || !p.wraw)) return hipErrorInvalidValue;   // unpacked weights need this path
     if (SP == SP_FWD_BNRELU && (!q.wdirect || p.wtrans || p.pro != PRO_BNRELU)) return hipErrorInvalidValue;
@@ -625,6 +644,10 @@ static bool rows_operands_ok(const RowsParams &p)
     if ((p.epi == EPI_STATS || p.epi == EPI_BNBWD) && !p.part) return false;
     if (p.epi == EPI_BNBWD && (!p.ex || !p.e_mean || !p.e_rstd || !p.e_gamma || !p.e_beta)) return false;
     if (p.epi == EPI_RELUMASK && !p.ex) return false;
+    if (p.side && p.pro != PRO_BNADDRELU &&
+        (p.pro != PRO_BNRELU || p.wtrans || p.epi == EPI_BNBWD || p.epi == EPI_RELUMASK || p.wdirect))
+        return false;
+    if (p.e_zsrc && (p.epi != EPI_BNBWD || !p.ex2)) return false;
     if (p.taps == 9 && p.w > kRowsMaxW3) return false;
     return true;
 }

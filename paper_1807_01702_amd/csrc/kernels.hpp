@@ -123,8 +123,14 @@ struct RowsParams {
     int64_t ex_ldc;
     const float *e_gamma, *e_beta, *e_mean, *e_rstd;
     const float *e_ctr;           // EPI_BNBWD: float32 centre of ex (NULL: 0; e_mean relative to it)
+    int e_zsrc;                   // EPI_BNBWD: ex is the stored z = relu(y) of the forward (O2'): mask
+                                  // [z > 0], xhat = (z - beta) / gamma; channel vectors holding a
+                                  // gamma = 0 channel read ex2 (the BN input x) instead
+    const void *ex2;              // e_zsrc: the BN input x (N channels)
+    int64_t ex2_ldc;
     const float *e_shift;         // EPI_STATS: the sums are of (y - e_shift) (NULL: 0)
-    void *side;                   // PRO_BNADDRELU: the transformed A rows are stored here too
+    void *side;                   // PRO_BNADDRELU, PRO_BNRELU (forward, optional): the transformed
+                                  // A rows are stored here too
     int64_t side_ldc;
     int buf32;                    // tiled 1x1 kernel: operand spans below 2^31 bytes (set by its launcher)
     int wdirect;                  // tiled bf16 1x1 kernel: weights read from wraw ([k][n], wtrans: [n][k]), no packing
@@ -133,7 +139,8 @@ int64_t rows_mtiles(int dtype, int taps, int64_t m, int n_out);
 size_t rows_pack_bytes(int dtype, int taps, int K, int N);
 // transpose = 0: forward packing of W[kh][kw][ci][co] (GEMM K = ci, N = co);
 // transpose = 1: data-gradient packing, flipped taps, GEMM K = co, N = ci.
-bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro);
+bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a_ldc, int64_t a2_ldc, int pro,
+                         bool side);
 hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_out, int transpose, void *wpack,
                                hipStream_t s);
 hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s);

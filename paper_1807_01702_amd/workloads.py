@@ -198,10 +198,16 @@ class _DenseStage:
     alpha/betap; each 3x3 CONV's backward forms its slice's gradient on load,
     and one pass materialises the block input's gradient at the end.  Without
     ICF each BN1 sweeps its input for statistics and its input gradient is
-    formed by a separate pass accumulating into G."""
+    formed by a separate pass accumulating into G.
+
+    ``o2`` (fused without ICF only): the paper's own sweep structure -- each
+    composite layer's fused forwards also store the BN+ReLU output they feed
+    to their CONV (O2'), and the backwards read it in place of recomputing it
+    from the BN input (bnr_bn_relu_conv_fwd_o2 / bnr_bwd_fused_o2); every
+    layer keeps its two stored tensors from forward to backward."""
 
     def __init__(self, n, h, w, c0, ct, cpls, trans, eps, dev, bf16, fused, icf, ref_mode=MODE, overlap=False,
-                 robust=False):
+                 robust=False, o2=False):
         dt = torch.bfloat16 if bf16 else torch.float32
         self.n, self.h, self.w, self.c0, self.ct = n, h, w, c0, ct
         self.X = torch.zeros((n, h, w, ct), dtype=dt, device=dev)
@@ -255,6 +261,14 @@ class _DenseStage:
         self.icf = bool(icf)
         if self.icf and not fused:
             raise ValueError("inter-composite-layer fusion needs the fused path")
+        self.o2 = bool(o2)
+        if self.o2 and (not fused or self.icf or self.overlap):
+            raise ValueError("the stored-O2' variant is wired for the fused path without inter-composite-layer "
+                             "fusion or overlap")
+        # per layer: relu(bn1(X[..., :c_l])) and relu(bn2(x1)), written by the forward, read by the backward
+        self.z = ([(torch.empty((n, h, w, c_l), dtype=dt, device=dev),
+                    torch.empty((n, h, w, u2.x.shape[-1]), dtype=dt, device=dev)) for c_l, k, u1, u2 in self.cpl]
+                  if self.o2 else None)
         if self.icf:
             f32 = dict(dtype=torch.float32, device=dev)
             self.mu, self.var, self.rstd = (torch.empty(ct, **f32) for _ in range(3))
@@ -311,8 +325,13 @@ class _DenseStage:
             if ut is not None:
                 B.bnr_bn_relu_conv_pool_fwd(self._pool_desc(pooled), ut.x, ut.bn, ut.wt, pooled, pooled_bn)
         elif self.fused:
-            for c_l, k, u1, u2 in self.cpl:
+            for i, (c_l, k, u1, u2) in enumerate(self.cpl):
                 B.bnr_bn_stats(u1.x, u1.bn)                                    # sub-BN1 of a concat: own sweep
+                if self.o2:
+                    z1, z2 = self.z[i]
+                    B.bnr_bn_relu_conv_fwd_o2(u1.desc, u1.x, u1.bn, u1.wt, u1.out, z1, u2.bn)
+                    B.bnr_bn_relu_conv_fwd_o2(u2.desc, u2.x, u2.bn, u2.wt, u2.out, z2)
+                    continue
                 B.bnr_bn_relu_conv_fwd(u1.desc, u1.x, u1.bn, u1.wt, u1.out, u2.bn)
                 B.bnr_bn_relu_conv_fwd(u2.desc, u2.x, u2.bn, u2.wt, u2.out)
             ut = self.ut
@@ -361,7 +380,16 @@ class _DenseStage:
             if ut is not None:
                 B.bnr_bwd_fused(ut.desc, ut.x, ut.bn, ut.wt, B.grad_avgpool2(dpool), ut.dw, ut.g.dgamma,
                                 ut.g.dbeta, self.dy_t, self.G)
-            for c_l, k, u1, u2 in reversed(self.cpl):
+            for i, (c_l, k, u1, u2) in reversed(list(enumerate(self.cpl))):
+                if self.o2:
+                    z1, z2 = self.z[i]
+                    B.bnr_bwd_fused_o2(u2.desc, u2.x, u2.bn, z2, u2.wt, B.grad_dense(self.G[..., c_l:c_l + k]),
+                                       u2.dw, u2.g.dgamma, u2.g.dbeta, self.dy2)
+                    B.bnr_bwd_fused_o2(u1.desc, u1.x, u1.bn, z1, u1.wt,
+                                       B.grad_bn(self.dy2, u2.x, u2.bn, u2.g.dgamma, u2.g.dbeta),
+                                       u1.dw, u1.g.dgamma, u1.g.dbeta, _dense(self.dy1_flat, n, h, w, c_l),
+                                       self.G[..., :c_l], dx_accumulate=True)
+                    continue
                 B.bnr_bwd_fused(u2.desc, u2.x, u2.bn, u2.wt, B.grad_dense(self.G[..., c_l:c_l + k]), u2.dw,
                                 u2.g.dgamma, u2.g.dbeta, self.dy2)
                 B.bnr_bwd_fused(u1.desc, u1.x, u1.bn, u1.wt,
@@ -433,13 +461,14 @@ class DenseBlock(_DenseStage):
     input; upstream gradient: dpool of the pooled output.  ``icf`` defaults
     to on for the fused path (see _DenseStage)."""
 
-    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None, overlap=False, robust=False):
+    def __init__(self, data, device="cuda", fused=True, ref_mode=MODE, icf=None, overlap=False, robust=False,
+                 o2=False):
         bf16 = data["bf16"]
         dev = torch.device(device)
         dt = torch.bfloat16 if bf16 else torch.float32
         n, h, w, c0 = data["x"].shape
         super().__init__(n, h, w, c0, data["c_total"], data["cpls"], data["trans"], data["eps"], dev, bf16, fused,
-                         fused if icf is None else icf, ref_mode, overlap, robust)
+                         fused if icf is None else icf, ref_mode, overlap, robust, o2)
         self.X[..., :c0] = _t(data["x"], dev, bf16)
         to = data["trans"]["w"].shape[3]
         self.pooled = torch.empty((n, h // 2, w // 2, to), dtype=dt, device=dev)

@@ -35,7 +35,8 @@ from paper_1807_01702_amd import synth
 pytestmark = pytest.mark.gpu
 
 MODES = ["fused", "baseline", "rcf", "rcf_mvf"]
-BLOCK_MODES = ["fused", "fused_overlap", "fused_no_icf", "baseline", "rcf", "rcf_mvf"]   # fused = BNFF + ICF
+# fused = BNFF + ICF; fused_o2 = BNFF with the stored O2' sweep
+BLOCK_MODES = ["fused", "fused_overlap", "fused_no_icf", "fused_o2", "baseline", "rcf", "rcf_mvf"]
 
 
 def _make(cls, data, mode):
@@ -45,6 +46,8 @@ def _make(cls, data, mode):
         return getattr(W, cls)(data, fused=True)
     if mode == "fused_no_icf":
         return getattr(W, cls)(data, fused=True, icf=False)
+    if mode == "fused_o2":              # the backward reads the stored relu(bn(x)) (O2')
+        return getattr(W, cls)(data, fused=True, icf=False, o2=True)
     if mode == "fused_overlap":         # weight gradients on a side stream
         return getattr(W, cls)(data, fused=True, overlap=True)
     ref = {"baseline": B.MODE_BASELINE, "rcf": B.MODE_RCF, "rcf_mvf": B.MODE_RCF_MVF}[mode]
@@ -201,7 +204,7 @@ def test_dense_block_bf16():
     rnd = OC.storage(True)
     rt = RTOL[True]
     errs = {}
-    for mode in ("fused", "fused_no_icf", "baseline"):
+    for mode in ("fused", "fused_no_icf", "fused_o2", "baseline"):
         pooled, c = OC.block_fwd(d["x"], d["cpls"], d["trans"], d["eps"], rnd, d["c_total"],
                                  pool_first=mode != "baseline")
         dX0, g = OC.block_bwd(c, d["dpool"].astype(np.float64), rnd)
@@ -222,7 +225,7 @@ def test_dense_block_bf16():
         errs[mode] = np.array(e)
         del wl
     unfused = errs["baseline"]
-    for mode in ("fused", "fused_no_icf"):
+    for mode in ("fused", "fused_no_icf", "fused_o2"):
         assert np.all(errs[mode] <= 1.25 * unfused + 2e-3), (mode, errs[mode], unfused)
         assert np.all(errs[mode] <= 0.2), (mode, errs[mode])      # gross-error guard: a wrong term is O(1)
 
