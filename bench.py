@@ -67,12 +67,21 @@ def parse():
                                        "unfused_rcf_mvf"],
                     default=None)
     ap.add_argument("--no-ablation", action="store_true")
+    ap.add_argument("--flush-mb", type=int, default=512,
+                    help="MiB copied before every library call in the cold-cache trace (0: no cold-cache trace)")
+    ap.add_argument("--bn-passes", type=int, default=0, metavar="MB",
+                    help="time the standalone BN sweeps on tensors of about MB megabytes and exit")
     ap.add_argument("--summarize-step-bytes", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None)
+    ap.add_argument("--summarize-ablation", metavar="RUN_DIR", default=None,
+                    help="RUN_DIR/sb_f_V, RUN_DIR/sb_w_V of each variant V (profile-only runs, --steps 2 --warmup 1) "
+                         "-> profiles/hbm_bytes_per_step_<workload>.json and a markdown table (with --bench-json)")
     ap.add_argument("--summarize-mfma", metavar="PMC_DIR", default=None)
     ap.add_argument("--calib-copy-mb", type=int, default=0)
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None)
     ap.add_argument("--summarize-trace", nargs=2, metavar=("KERNEL_STATS_CSV", "STEPS"), default=None)
     ap.add_argument("--bench-json", default=None)
+    ap.add_argument("--summarize-bench", metavar="BENCH_JSON", default=None,
+                    help="markdown: the bench line's figures, per-class event timings, warm and cold cache")
     return ap.parse_args()
 
 
@@ -141,19 +150,45 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 PEAK_MFMA_TFS = {"bf16": 2500.0, "f32": 157.3}
 
 
-def traced_kernels(torch, wl, steps):
+def traced_kernels(torch, wl, steps, flush_mb=0):
     """Per-kernel totals over `steps` eager steps, each launch bracketed by
-    HIP events on its own stream inside the library."""
+    HIP events on its own stream inside the library.  flush_mb > 0: before
+    every library call of the step a copy of flush_mb MiB (read and written)
+    evicts the L2 caches and the Infinity Cache (256 MB), so every kernel
+    starts cold; the copies themselves are not counted."""
     from paper_1807_01702_amd import bnr as B
     wl.step()
     torch.cuda.synchronize()
-    B.bnr_trace_begin(0xF, 200000)
-    for _ in range(steps):
-        wl.step()
-    torch.cuda.synchronize()
-    recs = B.bnr_trace_end(200000)
+    saved = {}
+    if flush_mb > 0:
+        n = flush_mb * 1024 * 1024 // 4
+        fsrc = torch.ones(n, dtype=torch.float32, device="cuda")
+        fdst = torch.empty_like(fsrc)
+        copy = B.bnr_hbm_copy
+
+        def cold(f):
+            def g(*a, **k):
+                copy(fsrc, fdst)
+                return f(*a, **k)
+            return g
+        for name in dir(B):
+            if name.startswith("bnr_") and name not in ("bnr_hbm_copy", "bnr_trace_begin", "bnr_trace_end") and \
+                    callable(getattr(B, name)) and not name.endswith("_size"):
+                saved[name] = getattr(B, name)
+                setattr(B, name, cold(saved[name]))
+    try:
+        B.bnr_trace_begin(0xF, 200000)
+        for _ in range(steps):
+            wl.step()
+        torch.cuda.synchronize()
+        recs = B.bnr_trace_end(200000)
+    finally:
+        for name, f in saved.items():
+            setattr(B, name, f)
     agg = {}
     for name, ms, by, fl in recs:
+        if flush_mb > 0 and name == "copy":
+            continue
         a = agg.setdefault(name, [0, 0.0, 0.0, 0.0])
         a[0] += 1
         a[1] += ms
@@ -241,8 +276,10 @@ def _counter_rows(d, counter):
     return out
 
 
-def summarize_pmc(fetch_dir, write_dir, workload, copy_mb):
-    """Per kernel class: counter bytes per launch, scaled by the calibration copy."""
+def summarize_pmc(fetch_dir, write_dir, workload, copy_mb, bench_json=None):
+    """Per kernel class: counter bytes per launch, scaled by the calibration
+    copy, and (bench_json: a bench line of the same tree) the algorithmic
+    bytes per launch the library's launchers account and the ratio."""
     fetch, write = _counter_rows(fetch_dir, "FETCH_SIZE"), _counter_rows(write_dir, "WRITE_SIZE")
     expected = copy_mb * 1024.0 * 1024.0
     fc = [v for n, v in fetch if kernel_class(n) == "copy"]
@@ -266,6 +303,13 @@ def summarize_pmc(fetch_dir, write_dir, workload, copy_mb):
         wb = sum(a["write"]) / len(a["write"]) * w_scale
         classes[c] = {"launches": len(a["fetch"]), "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
                       "bytes_per_launch": fb + wb, "sources_sha256": sources_sha(c)}
+    if bench_json:
+        with open(bench_json) as fh:
+            kern = json.loads(fh.read().strip().splitlines()[-1])["kernels"]
+        for c, v in classes.items():
+            if c in kern:
+                v["algorithmic_bytes_per_launch"] = kern[c]["algorithmic_bytes_per_launch"]
+                v["counter_over_algorithmic"] = v["bytes_per_launch"] / kern[c]["algorithmic_bytes_per_launch"]
     return {"workload": workload, "calibration": {"copy_bytes": expected, "fetch_counted": fc[-1],
                                                   "write_counted": wc[-1], "fetch_scale": f_scale,
                                                   "write_scale": w_scale},
@@ -292,6 +336,94 @@ def summarize_step_bytes(fetch_dir, write_dir, copy_mb, steps):
         out[counter] = {"bytes_per_step": sum(v for _, v in lib[:-1]) * scale / steps, "scale": scale}
     out["total_bytes_per_step"] = out["FETCH_SIZE"]["bytes_per_step"] + out["WRITE_SIZE"]["bytes_per_step"]
     return out
+
+
+ABLATION_ROWS = [("unfused", "unfused chain (BASELINE: two-pass statistics, BN, ReLU, CONV sweeps)"),
+                 ("unfused_rcf", "ReLU-CONV fusion (RCF)"),
+                 ("unfused_rcf_mvf", "RCF + mean/variance fusion (MVF)"),
+                 ("fused_o2", "BN fission-n-fusion with the stored O2' sweep (the paper's BNFF)"),
+                 ("fused_no_icf", "BN fission-n-fusion, z recomputed from x (BNFF)"),
+                 ("fused", "BNFF + inter-composite-layer fusion (ICF)")]
+
+
+def summarize_ablation(run_dir, workload, copy_mb, steps, bench_json=None):
+    """HBM bytes per step of every variant with counter runs under run_dir,
+    beside the bytes model and (bench_json) the variant's time: writes
+    profiles/hbm_bytes_per_step_<workload>.json (with the SHA-256 of all
+    kernel sources) and returns a markdown table."""
+    from paper_1807_01702_amd import bytes_model, synth
+    cls, recipe, kw = WORKLOADS[workload]
+    model = bytes_model.for_workload(workload, getattr(synth, recipe)(seed=0, **kw))
+    abl = {}
+    if bench_json:
+        with open(bench_json) as fh:
+            abl = json.loads(fh.read().strip().splitlines()[-1])["ablation"]
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    out = {"workload": workload, "sources_sha256": h.hexdigest(), "variants": {}}
+    for v, _ in ABLATION_ROWS:
+        fd, wd = os.path.join(run_dir, "sb_f_" + v), os.path.join(run_dir, "sb_w_" + v)
+        if not (os.path.isdir(fd) and os.path.isdir(wd)):
+            continue
+        sb = summarize_step_bytes(fd, wd, copy_mb, steps)
+        out["variants"][v] = {"counter_bytes_per_step": sb["total_bytes_per_step"],
+                              "fetch_bytes_per_step": sb["FETCH_SIZE"]["bytes_per_step"],
+                              "write_bytes_per_step": sb["WRITE_SIZE"]["bytes_per_step"],
+                              "model_bytes_per_step": model.get(v),
+                              "ms_per_step": abl.get(v, {}).get("ms_per_step")}
+    with open(os.path.join(ROOT, "profiles", "hbm_bytes_per_step_%s.json" % workload), "w") as fh:
+        json.dump(out, fh, indent=1, sort_keys=True)
+    base = out["variants"].get("unfused", {})
+    rows = ["| variant | HBM GB/step (counters) | model GB/step | counters / model | vs unfused | ms/step | "
+            "speedup vs unfused |", "|---|---|---|---|---|---|---|"]
+    for v, label in ABLATION_ROWS:
+        r = out["variants"].get(v)
+        if not r:
+            continue
+        mb, ms = r["model_bytes_per_step"], r["ms_per_step"]
+        rows.append("| %s | %.2f | %s | %s | %.2f | %s | %s |" % (
+            label, r["counter_bytes_per_step"] / 1e9, "%.2f" % (mb / 1e9) if mb else "-",
+            "%.2f" % (r["counter_bytes_per_step"] / mb) if mb else "-",
+            r["counter_bytes_per_step"] / base["counter_bytes_per_step"] if base else float("nan"),
+            "%.3f" % ms if ms else "-",
+            "%.2fx" % (base["ms_per_step"] / ms) if (ms and base.get("ms_per_step")) else "-"))
+    return "\n".join(rows)
+
+
+def summarize_bench(bench_json):
+    """Markdown: headline figures of a bench line, and per kernel class the
+    HIP-event timings of the traced eager steps, warm and with every library
+    call preceded by a copy that evicts L2 and the Infinity Cache."""
+    with open(bench_json) as fh:
+        b = json.loads(fh.read().strip().splitlines()[-1])
+    r = b["roofline"]
+    out = ["Workload: %s, batch %d." % (b["config"]["workload"], b["config"]["global_batch"]),
+           "Bench line: %s = %.0f %s (%.3f ms/step, %s); unfused %.3f ms/step (%.2fx)." % (
+        b["metric"], b["value"], b["unit"], b["ms_per_step"], "graph replay" if b["config"].get("graph") else "eager",
+        b["unfused"]["ms_per_step"], b["speedup_vs_unfused"]),
+        "Dominant kernel class `%s`: %.1f us per launch, %.1f MB algorithmic -> %.0f GB/s = %.3f of %.0f GB/s%s." % (
+        r["kernel"], r["avg_launch_us"], r.get("algorithmic_bytes_per_launch", 0) / 1e6, r["achieved"], r["frac"],
+        r["peak"], "; counters %.1f MB per launch" % (r["traffic"] / 1e6) if r.get("traffic") else "")]
+    cpu = b.get("cpu_baseline")
+    if cpu:
+        out.append("CPU baseline (the fp64 oracle): %.2f %s on %d threads (%s)." % (cpu["value"], cpu["unit"],
+                                                                                  cpu["cores"], cpu["sample"]))
+    cold = (b.get("cold_cache") or {}).get("kernels", {})
+    out += ["", "| class | launches/step | ms/step | avg us | algorithmic MB | GB/s | of 8 TB/s | cold avg us | "
+            "cold / warm |", "|---|---|---|---|---|---|---|---|---|"]
+    for k, v in sorted(b["kernels"].items(), key=lambda kv: -kv[1]["ms_per_step"]):
+        c = cold.get(k)
+        out.append("| %s | %.1f | %.3f | %.1f | %.1f | %.0f | %.2f | %s | %s |" % (
+            k, v["launches_per_step"], v["ms_per_step"], v["avg_launch_us"], v["algorithmic_bytes_per_launch"] / 1e6,
+            v["achieved_GBps"] or 0, (v["achieved_GBps"] or 0) / PEAK_HBM_GBS,
+            "%.1f" % c["avg_launch_us"] if c else "-", "%.3f" % (c["avg_launch_us"] / v["avg_launch_us"]) if c else "-"))
+    if cold:
+        out.append("")
+        out.append("Cold: %d MiB copied (read and written) before every library call of the step, so no operand is "
+                   "in L2 or the 256 MB Infinity Cache when a kernel starts." % b["cold_cache"]["flush_mb"])
+    return "\n".join(out)
 
 
 def summarize_mfma(pmc_dir, dtype="bf16"):
@@ -393,6 +525,52 @@ def summarize_trace(stats_csv, steps, workload, bench_json=None):
     return "\n".join(out)
 
 
+def bn_passes(torch, mb, reps):
+    """Markdown table: the standalone BN sweeps (the passes BN fission/fusion
+    keeps where a BN's producer or reader is not a CONV) on bf16 tensors of
+    about `mb` MB ([m][256]), each launch timed by the library's HIP events,
+    achieved rate = the launcher's algorithmic bytes / event time, against
+    8 TB/s; the calibration copy beside them."""
+    from paper_1807_01702_amd import bnr as B
+    c = 256
+    m = mb * 1000 * 1000 // (2 * c)
+    bf = dict(dtype=torch.bfloat16, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    x, y, g = (torch.randn((m, c), generator=gen, **f32).to(torch.bfloat16) for _ in range(3))
+    out, gm, dx = (torch.empty((m, c), **bf) for _ in range(3))
+    bn = B.BN(torch.ones(c, **f32), torch.zeros(c, **f32), 1e-5)
+    dg, db, al, bp = (torch.randn(c, generator=gen, **f32) * 0.01 for _ in range(4))
+    cs, cd = torch.empty((m, c), **bf), torch.empty((m, c), **bf)
+    passes = [("statistics sweep (sum x, sum x^2)", lambda: B.bnr_bn_stats(x, bn)),
+              ("BN input gradient (dy, x -> dx)", lambda: B.bnr_bn_dx(g, x, bn, dg, db, dx)),
+              ("summed-gradient input gradient (G, x -> dX)", lambda: B.bnr_split_dx(g, x, bn, al, bp, dx)),
+              ("BN + add + ReLU (y, id -> out)", lambda: B.bnr_bn_add_relu_fwd(y, bn, x, out)),
+              ("its backward (g, out, y -> gm, sums)", lambda: B.bnr_bn_add_relu_bwd(g, out, y, bn, gm, dg, db)),
+              ("calibration copy", lambda: B.bnr_hbm_copy(cs, cd))]
+    rows = ["| pass | kernel | launches | avg us | algorithmic MB | TB/s | of 8 TB/s |", "|---|---|---|---|---|---|---|"]
+    for label, f in passes:
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        B.bnr_trace_begin(0xF, 100000)
+        for _ in range(reps):
+            f()
+        torch.cuda.synchronize()
+        agg = {}
+        for name, ms, by, fl in B.bnr_trace_end(100000):
+            a = agg.setdefault(name, [0, 0.0, 0.0])
+            a[0] += 1
+            a[1] += ms
+            a[2] += by
+        for name, (n, ms, by) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+            rate = by / (ms * 1e-3) / 1e12
+            rows.append("| %s | %s | %d | %.1f | %.1f | %.2f | %.2f |" % (label, name, n, 1e3 * ms / n, by / n / 1e6,
+                                                                       rate, rate * 1e3 / PEAK_HBM_GBS))
+    return ("Tensors [%d][%d] bf16 (%.1f MB each); %d timed calls per pass after 3 warm-up calls.\n\n" %
+            (m, c, m * c * 2 / 1e6, reps)) + "\n".join(rows)
+
+
 def cpu_baseline(args):
     """The fp64 oracle, as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -448,7 +626,8 @@ def main():
     if args.summarize_pmc:
         if args.calib_copy_mb <= 0:
             raise SystemExit("--summarize-pmc needs the --calib-copy-mb value the counter runs used")
-        out = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload, args.calib_copy_mb)
+        out = summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload, args.calib_copy_mb,
+                            args.bench_json)
         path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % args.workload)
         with open(path, "w") as fh:
             json.dump(out, fh, indent=1, sort_keys=True)
@@ -463,6 +642,15 @@ def main():
         print(json.dumps(summarize_step_bytes(args.summarize_step_bytes[0], args.summarize_step_bytes[1],
                                               args.calib_copy_mb, args.steps + args.warmup)))
         return
+    if args.summarize_ablation:
+        if args.calib_copy_mb <= 0:
+            raise SystemExit("--summarize-ablation needs the --calib-copy-mb value the counter runs used")
+        print(summarize_ablation(args.summarize_ablation, args.workload, args.calib_copy_mb, args.steps + args.warmup,
+                                 args.bench_json))
+        return
+    if args.summarize_bench:
+        print(summarize_bench(args.summarize_bench))
+        return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace[0], int(args.summarize_trace[1]), args.workload, args.bench_json))
         return
@@ -470,6 +658,9 @@ def main():
         print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
     import torch
+    if args.bn_passes:
+        print(bn_passes(torch, args.bn_passes, args.steps))
+        return
     from paper_1807_01702_amd import bytes_model
     torch.cuda.set_device(0)
     data, wls = build_workloads(args, torch)
@@ -490,6 +681,8 @@ def main():
         return
     dtype = "bf16" if data.get("bf16") else "f32"
     kernels = traced_kernels(torch, wls["fused"], args.steps) if "fused" in wls else None
+    cold = (traced_kernels(torch, wls["fused"], min(args.steps, 5), args.flush_mb)
+            if "fused" in wls and args.flush_mb > 0 else None)
     fused = res.get("fused")
     unf = res.get("unfused")
     noicf = res.get("fused_no_icf")
@@ -525,6 +718,11 @@ def main():
         "hbm_bytes_per_step": {"algorithmic_fused": model["fused"], "algorithmic_unfused": model["unfused"]},
         "roofline": roofline(kernels, dtype, args.workload) if kernels else None,
         "kernels": kernels,
+        # every library call preceded by a copy that evicts L2 and the Infinity Cache
+        "cold_cache": ({"flush_mb": args.flush_mb, "roofline": roofline(cold, dtype, args.workload),
+                        "kernels": {k: {"avg_launch_us": v["avg_launch_us"], "ms_per_step": v["ms_per_step"],
+                                        "achieved_GBps": v["achieved_GBps"]} for k, v in cold.items()}}
+                       if cold else None),
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(args),
     }
     print(json.dumps(line))

@@ -80,17 +80,24 @@ def _unit_split_bwd(a, m, ci, co, k, e, g_bytes, accumulate):
     a += k * k * ci * co * 4                  # dW (fp32)
 
 
-def _unit_ref_fwd(a, m, ci, co, k, e):
-    a += 2 * m * ci * e                       # mean sweep, variance sweep
+def _unit_ref_fwd(a, m, ci, co, k, e, ref="baseline"):
+    """Unfused chain; ref 'rcf': the ReLU applied while the CONV reads y (no
+    z), 'rcf_mvf': that with one statistics sweep (mean/variance fusion)."""
+    a += (1 if ref == "rcf_mvf" else 2) * m * ci * e     # statistics: mean and variance sweeps (MVF: one)
     a += 2 * m * ci * e                       # normalise: read x, write y
-    a += 2 * m * ci * e                       # ReLU: read y, write z
-    a += m * ci * e + k * k * ci * co * e + m * co * e   # CONV: read z, weights, write out
+    if ref == "baseline":
+        a += 2 * m * ci * e                   # ReLU: read y, write z
+    a += m * ci * e + k * k * ci * co * e + m * co * e   # CONV: read z (RCF: y), weights, write out
 
 
-def _unit_ref_bwd(a, m, ci, co, k, e, g_bytes, accumulate):
-    a += g_bytes + k * k * ci * co * e + m * ci * e      # dgrad: read g, weights, write dz
-    a += m * ci * e + g_bytes + k * k * ci * co * 4      # wgrad: read z, g, write dW
-    a += 3 * m * ci * e                                  # ReLU backward: read dz, y, write dy
+def _unit_ref_bwd(a, m, ci, co, k, e, g_bytes, accumulate, ref="baseline"):
+    if ref == "baseline":
+        a += g_bytes + k * k * ci * co * e + m * ci * e  # dgrad: read g, weights, write dz
+        a += m * ci * e + g_bytes + k * k * ci * co * 4  # wgrad: read z, g, write dW
+        a += 3 * m * ci * e                              # ReLU backward: read dz, y, write dy
+    else:
+        a += g_bytes + k * k * ci * co * e + 2 * m * ci * e   # dgrad with the ReLU mask: read g, weights, y; write dy
+        a += m * ci * e + g_bytes + k * k * ci * co * 4  # wgrad: read y (ReLU on load), g, write dW
     a += 2 * m * ci * e                                  # reductions: read dy, x
     a += 3 * m * ci * e + (m * ci * e if accumulate else 0)   # dx: read dy, x (+dx), write dx
 
@@ -123,22 +130,25 @@ def bottleneck(m, ci, width, k, e):
 def _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode, in_sweep=True):
     """Forward of a dense block (+ transition) in mode 'icf' (fused with
     inter-composite-layer fusion), 'fused', 'o2' (fused, the composite layers'
-    BN+ReLU outputs stored: the paper's O2' sweep) or 'unfused'; in_sweep
-    (icf): the block input's statistics need their own sweep."""
+    BN+ReLU outputs stored: the paper's O2' sweep), 'unfused', 'rcf' or
+    'rcf_mvf' (the unfused chain with ReLU-CONV fusion, and with mean/variance
+    fusion too); in_sweep (icf): the block input's statistics need their own
+    sweep."""
+    ref = {"unfused": "baseline", "rcf": "rcf", "rcf_mvf": "rcf_mvf"}.get(mode)
     c = c0
     if mode == "icf" and in_sweep:
         a += m * c0 * e                                          # the one statistics sweep (block input)
     for _ in range(layers):
-        if mode == "unfused":
-            _unit_ref_fwd(a, m, c, width, 1, e)
-            _unit_ref_fwd(a, m, width, k, 3, e)
+        if ref:
+            _unit_ref_fwd(a, m, c, width, 1, e, ref)
+            _unit_ref_fwd(a, m, width, k, 3, e, ref)
         else:
             _unit_fused_fwd(a, m, c, width, 1, e, mode in ("fused", "o2"), save_z=mode == "o2")
             _unit_fused_fwd(a, m, width, k, 3, e, False, save_z=mode == "o2")
         c += k
     if trans_out:
-        if mode == "unfused":
-            _unit_ref_fwd(a, m, c, trans_out, 1, e)
+        if ref:
+            _unit_ref_fwd(a, m, c, trans_out, 1, e, ref)
             a += m * trans_out * e + m // 4 * trans_out * e      # avgpool forward
         else:
             # BN, ReLU and the 2x2 average in the CONV's prologue: read x,
@@ -153,6 +163,7 @@ def _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode):
     """Backward of _block_fwd; without a transition the block's gradient
     buffer was written by the BN that reads the whole block (the head)."""
     ct = c0 + layers * k
+    ref = {"unfused": "baseline", "rcf": "rcf", "rcf_mvf": "rcf_mvf"}.get(mode)
     if trans_out:
         if mode == "icf":
             _unit_split_bwd(a, m, ct, trans_out, 1, e, m // 4 * trans_out * e, False)
@@ -160,7 +171,7 @@ def _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode):
             _unit_fused_bwd(a, m, ct, trans_out, 1, e, m // 4 * trans_out * e, "write")
         else:
             a += m // 4 * trans_out * e + m * trans_out * e      # unfused: materialised pooling gradient
-            _unit_ref_bwd(a, m, ct, trans_out, 1, e, m * trans_out * e, False)
+            _unit_ref_bwd(a, m, ct, trans_out, 1, e, m * trans_out * e, False, ref)
     for layer in reversed(range(layers)):
         c = c0 + layer * k
         if mode == "icf":
@@ -170,20 +181,21 @@ def _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode):
             _unit_fused_bwd(a, m, width, k, 3, e, m * k * e, None)
             _unit_fused_bwd(a, m, c, width, 1, e, 2 * m * width * e, "accumulate")
         else:
-            _unit_ref_bwd(a, m, width, k, 3, e, m * k * e, False)
-            _unit_ref_bwd(a, m, c, width, 1, e, m * width * e, True)
+            _unit_ref_bwd(a, m, width, k, 3, e, m * k * e, False, ref)
+            _unit_ref_bwd(a, m, c, width, 1, e, m * width * e, True, ref)
     if mode == "icf":
         a += 3 * m * c0 * e                                      # block-input gradient: read sum, x; write
 
 
 def dense_block(m, c0, layers, width, k, trans_out, e):
     out = {}
-    for mode in ("icf", "fused", "o2", "unfused"):
+    for mode in ("icf", "fused", "o2", "unfused", "rcf", "rcf_mvf"):
         a = _Acc()
         _block_fwd(a, m, c0, layers, width, k, trans_out, e, mode)
         _block_bwd(a, m, c0, layers, width, k, trans_out, e, mode)
         out[mode] = a.total
-    return {"fused": out["icf"], "fused_no_icf": out["fused"], "fused_o2": out["o2"], "unfused": out["unfused"]}
+    return {"fused": out["icf"], "fused_no_icf": out["fused"], "fused_o2": out["o2"], "unfused": out["unfused"],
+            "unfused_rcf": out["rcf"], "unfused_rcf_mvf": out["rcf_mvf"]}
 
 
 def densenet(n, hw, c_in, c_stem, blocks, classes, e):
