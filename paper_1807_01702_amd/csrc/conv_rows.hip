@@ -535,7 +535,7 @@ __global__ __launch_bounds__(kThreads) void k_pack_weights(const T *__restrict__
 // ------------------------------------------------------------- launchers ---
 int64_t rows_mtiles(int dtype, int taps, int64_t m, int n_out)
 {
-    return ceil_div(m, rows_tile(dtype, taps, n_out).bm);
+    return ceil_div(m, rows_tile(dtype, taps, n_out, m).bm);
 }
 
 size_t rows_pack_bytes(int dtype, int taps, int K, int N)
@@ -655,22 +655,25 @@ static bool rows_operands_ok(const RowsParams &p)
 hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s)
 {
     if (!rows_operands_ok(p)) return hipErrorInvalidValue;
-    const RowsTile t = rows_tile(p.dtype, p.taps, p.N);
+    const RowsTile t = rows_tile(p.dtype, p.taps, p.N, p.m);
     if (p.dtype == DT_BF16) {
         if (p.taps == 1) {
             const bool dw = p.wdirect && rows_spans_fit(p.dtype, p.m, p.K, p.N, p.a_ldc, p.a2_ldc, p.pro);
             if (dw && p.pro == PRO_BNRELU && !p.wtrans) {
                 if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1, SP_FWD_BNRELU>(p, s);
                 if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1, SP_FWD_BNRELU>(p, s);
+                if (t.bm == 64) return run_rows<bf16_t, 1, 64, 128, 2, 2, SP_FWD_BNRELU>(p, s);
                 return run_rows<bf16_t, 1, 128, 128, 2, 2, SP_FWD_BNRELU>(p, s);
             }
             if (dw && p.pro == PRO_BNGRAD && p.wtrans) {
                 if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1, SP_DGRAD_BNGRAD>(p, s);
                 if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1, SP_DGRAD_BNGRAD>(p, s);
+                if (t.bm == 64) return run_rows<bf16_t, 1, 64, 128, 2, 2, SP_DGRAD_BNGRAD>(p, s);
                 return run_rows<bf16_t, 1, 128, 128, 2, 2, SP_DGRAD_BNGRAD>(p, s);
             }
             if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1>(p, s);
             if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1>(p, s);
+            if (t.bm == 64) return run_rows<bf16_t, 1, 64, 128, 2, 2>(p, s);
             return run_rows<bf16_t, 1, 128, 128, 2, 2>(p, s);
         }
         if (t.bn == 32) return run_rows<bf16_t, 9, 128, 32, 4, 1>(p, s);

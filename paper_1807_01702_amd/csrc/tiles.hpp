@@ -37,9 +37,15 @@ inline int64_t stats_row_blocks(int64_t m, int c, int dtype) {
 constexpr int kRowsBK = 32;
 constexpr int kRowsMaxW3 = 62;             // largest image width for 3x3 (halo = W+1 rows)
 struct RowsTile { int bm, bn; };
-inline RowsTile rows_tile(int dtype, int taps, int n_out) {
+// m > 0: a bf16 1x1 grid of 128-row tiles that would leave CUs idle (the
+// late DenseNet blocks: 14x14 and 7x7 images) takes 64-row tiles instead
+inline RowsTile rows_tile(int dtype, int taps, int n_out, int64_t m = 0) {
     if (dtype == DT_F32) return RowsTile{64, n_out <= 32 ? 32 : 64};
-    if (taps == 1) return RowsTile{128, n_out <= 64 ? (n_out <= 32 ? 32 : 64) : 128};
+    if (taps == 1) {
+        const int bn = n_out <= 64 ? (n_out <= 32 ? 32 : 64) : 128;
+        const int64_t tiles128 = (m + 127) / 128 * ((n_out + bn - 1) / bn);
+        return RowsTile{bn == 128 && m > 0 && tiles128 < 256 ? 64 : 128, bn};
+    }
     return RowsTile{128, n_out <= 32 ? 32 : 64};
 }
 
