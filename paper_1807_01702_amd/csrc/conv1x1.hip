@@ -34,11 +34,14 @@ struct P1Geom {
     size_t region, lds;
 };
 
-static P1Geom p1_geom(int K, int N)
+// fine: the output columns rounded up to a multiple of 32 (the data gradients
+// with the BN-backward epilogue, whose widths are concatenation prefixes:
+// 96, 160, 192, 224 channels); otherwise to 32, 64, 128 or 256.
+static P1Geom p1_geom(int K, int N, bool fine = false)
 {
     P1Geom g;
     g.KP = (K + 31) / 32 * 32;
-    g.NP = N <= 32 ? 32 : (N <= 64 ? 64 : (N <= 128 ? 128 : 256));
+    g.NP = fine ? (N + 31) / 32 * 32 : (N <= 32 ? 32 : (N <= 64 ? 64 : (N <= 128 ? 128 : 256)));
     g.lda = g.KP + 8;
     g.ldw = g.KP + 8;
     g.ldc = g.NP + 8;
@@ -80,8 +83,8 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     using T = bf16_t;
     using M = Mfma<T>;
     constexpr int VEC = 8;
-    constexpr int RPT0 = BM * (32 * CBW / VEC) / kP1Threads;
-    constexpr int RPT = RPT0 > 0 ? RPT0 : 1;                     // epilogue rows per thread
+    constexpr int RSTEP_C = kP1Threads / (32 * CBW / VEC);     // epilogue rows per pass
+    constexpr int RPT = (BM + RSTEP_C - 1) / RSTEP_C;            // epilogue rows per thread
     constexpr int RB = BM / 64;                                  // 16-row MFMA blocks per wave
     constexpr bool BNBWD = EK == EK_BNBWD || EK == EK_BNBWD_SC || EK == EK_BNBWD_SCACC;
     constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || BNBWD;
@@ -330,11 +333,13 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
         }
     };
 
-    // ---- epilogue mapping: thread = one channel vector of rows r0, r0+RSTEP, ... ----
-    const int VPRO = NP / VEC, RSTEP = kP1Threads / VPRO;
+    // ---- epilogue mapping: thread = one channel vector of rows r0, r0+RSTEP, ...
+    // (a width that does not divide the workgroup leaves its last threads idle) ----
+    const int VPRO = NP / VEC, RSTEP = RSTEP_C;
     const int v = tid % VPRO, r0 = tid / VPRO;
     const int n = v * VEC;
-    const bool col_ok = n < N;
+    const bool act = r0 < RSTEP;
+    const bool col_ok = act && n < N;
     vec16 rx[NVX], rd[NVD];
     float s1[VEC], s2[VEC];
     #pragma unroll
@@ -489,11 +494,12 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     // ---- per-workgroup statistics partial row ----
     if (EK == EK_STATS || BNBWD) {
         float *red = reinterpret_cast<float *>(As);
-        #pragma unroll
-        for (int e = 0; e < VEC; e++) {
-            red[r0 * NP + n + e] = s1[e];
-            red[(RSTEP + r0) * NP + n + e] = s2[e];
-        }
+        if (act)
+            #pragma unroll
+            for (int e = 0; e < VEC; e++) {
+                red[r0 * NP + n + e] = s1[e];
+                red[(RSTEP + r0) * NP + n + e] = s2[e];
+            }
         lds_colsum2(red, RSTEP, NP, NP, kP1Threads, tid, p.part + (int64_t)blockIdx.x * 2 * N,
                     p.part + (int64_t)blockIdx.x * 2 * N + N, N);
     }
@@ -572,7 +578,7 @@ template <int CBW, int NVA128, int EK, int PC>
 static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
     constexpr bool reads = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK >= EK_BNBWD;
-    constexpr bool small = (CBW == 8 && reads) || (NVA128 == 8 && (PC == PC_BNGRAD || PC == PC_BNADD)) ||
+    constexpr bool small = (CBW >= 5 && reads) || (NVA128 == 8 && (PC == PC_BNGRAD || PC == PC_BNADD)) ||
                            PC == PC_BNRELU_POOL;
     // (64-row tiles hold at most four 16-byte A vectors per thread; the
     // pooling prologue loads four pixels for each)
@@ -583,12 +589,24 @@ static hipError_t run_p1_bm(const RowsParams &p, const P1Geom &g, hipStream_t s,
 template <int NVA128, int EK, int PC>
 static hipError_t run_p1_cbw(const RowsParams &p, const P1Geom &g, hipStream_t s, int64_t *rows)
 {
+    constexpr bool FINE = EK == EK_BNBWD || EK == EK_BNBWD_SC || EK == EK_BNBWD_SCACC;
     switch (g.NP / 32) {
     case 1: return run_p1_bm<1, NVA128, EK, PC>(p, g, s, rows);
     case 2: return run_p1_bm<2, NVA128, EK, PC>(p, g, s, rows);
     case 4: return run_p1_bm<4, NVA128, EK, PC>(p, g, s, rows);
-    default: return run_p1_bm<8, NVA128, EK, PC>(p, g, s, rows);
+    case 8: return run_p1_bm<8, NVA128, EK, PC>(p, g, s, rows);
+    default: break;
     }
+    if constexpr (FINE) {
+        switch (g.NP / 32) {
+        case 3: return run_p1_bm<3, NVA128, EK, PC>(p, g, s, rows);
+        case 5: return run_p1_bm<5, NVA128, EK, PC>(p, g, s, rows);
+        case 6: return run_p1_bm<6, NVA128, EK, PC>(p, g, s, rows);
+        case 7: return run_p1_bm<7, NVA128, EK, PC>(p, g, s, rows);
+        default: break;
+        }
+    }
+    return hipErrorInvalidValue;
 }
 
 template <int EK, int PC>
@@ -645,7 +663,7 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
     if (p.m < 1 || arows >= (lim >> 1) || (arows * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
-    const P1Geom g = p1_geom(p.K, p.N);
+    const P1Geom g = p1_geom(p.K, p.N, p.epi == EPI_BNBWD);
     const int ek = epilogue_kind(p.epi, p.accumulate, p.e_scale);
     if (poolf) return ek == EK_STATS ? run_p1_nva<EK_STATS, PC_BNRELU_POOL>(p, g, s, rows)
                                      : run_p1_nva<EK_STORE, PC_BNRELU_POOL>(p, g, s, rows);
