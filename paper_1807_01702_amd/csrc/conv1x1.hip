@@ -398,11 +398,13 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     for (int k = 0; k < nitems; k++) {
         int p0, lim;
         item(k, p0, lim);
+        // epilogue operand first, before this tile's staging: it then has the
+        // staging, the matrix cores and the output staging to arrive, and the
+        // staging's wait for this tile's rows (issued earlier) leaves it in
+        // flight; the next tile's rows follow it
+        load_epi(p0, lim);
         store_a(p0, lim);
         __syncthreads();
-        // epilogue operand first: the epilogue waits for it while the next
-        // tile's rows (issued after it) may still be in flight
-        load_epi(p0, lim);
         if (k + 1 < nitems) { int q0, ql; item(k + 1, q0, ql); load_a(q0, ql); }
         // ---- matrix cores: 16 RB rows x NP/2 columns per wave ----
         f32x4 acc[RB][CBW];
