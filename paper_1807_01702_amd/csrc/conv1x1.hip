@@ -423,20 +423,21 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             for (int cb = 0; cb < CBW; cb++) {
                 const typename M::frag b = M::load(brow + cb * 16 * g.ldw + k0);
                 #pragma unroll
-                for (int ib = 0; ib < RB; ib++) M::mma(acc[ib][cb], a[ib], b);
+                for (int ib = 0; ib < RB; ib++) M::mma(acc[ib][cb], b, a[ib]);
             }
         }
         __syncthreads();
+        // (the weights are the matrix cores' first operand, so a lane holds
+        // four consecutive channels of one pixel row: one 8-byte write)
         #pragma unroll
         for (int ib = 0; ib < RB; ib++)
             #pragma unroll
-            for (int cb = 0; cb < CBW; cb++)
-                #pragma unroll
-                for (int i = 0; i < 4; i++) {
-                    const int row = wm * (16 * RB) + ib * 16 + (lane >> 4) * 4 + i;
-                    const int col = wn * (NP / 2) + cb * 16 + (lane & 15);
-                    Cs[row * g.ldc + col] = f2bf(acc[ib][cb][i]);
-                }
+            for (int cb = 0; cb < CBW; cb++) {
+                const int row = wm * (16 * RB) + ib * 16 + (lane & 15);
+                const int col = wn * (NP / 2) + cb * 16 + (lane >> 4) * 4;
+                const uint2 w = make_uint2(pack2bf(acc[ib][cb][0], acc[ib][cb][1]), pack2bf(acc[ib][cb][2], acc[ib][cb][3]));
+                *reinterpret_cast<uint2 *>(Cs + row * g.ldc + col) = w;
+            }
         __syncthreads();
         // ---- epilogue row pass: all outputs of this thread first (invalid rows
         // contribute zeros), then the stores back to back ----

@@ -468,25 +468,25 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             #pragma unroll
             for (int ib = 0; ib < RB; ib++) {
                 if (tap == 0) {
-                    M::mma0(acc[ib][0], af[0][ib], bfr[0][0]);
-                    M::mma0(acc[ib][1], af[0][ib], bfr[0][1]);
+                    M::mma0(acc[ib][0], bfr[0][0], af[0][ib]);
+                    M::mma0(acc[ib][1], bfr[0][1], af[0][ib]);
                 } else {
-                    M::mma(acc[ib][0], af[tap % NB][ib], bfr[tap][0]);
-                    M::mma(acc[ib][1], af[tap % NB][ib], bfr[tap][1]);
+                    M::mma(acc[ib][0], bfr[tap][0], af[tap % NB][ib]);
+                    M::mma(acc[ib][1], bfr[tap][1], af[tap % NB][ib]);
                 }
             }
         }
-        // ---- float32 partial tile of this K slice -> LDS ----
+        // ---- float32 partial tile of this K slice -> LDS (the weights are
+        // the matrix cores' first operand, so a lane holds four consecutive
+        // channels of one position: one 16-byte write) ----
         #pragma unroll
         for (int ib = 0; ib < RB; ib++)
             #pragma unroll
-            for (int cb = 0; cb < 2; cb++)
-                #pragma unroll
-                for (int i = 0; i < 4; i++) {
-                    const int row = wr * 16 * RB + ib * 16 + (lane >> 4) * 4 + i;
-                    const int col = wn * 32 + cb * 16 + (lane & 15);
-                    red[(wk * kP3BM + row) * ldr + col] = acc[ib][cb][i];
-                }
+            for (int cb = 0; cb < 2; cb++) {
+                const int row = wr * 16 * RB + ib * 16 + (lane & 15);
+                const int col = wn * 32 + cb * 16 + (lane >> 4) * 4;
+                *reinterpret_cast<f32x4 *>(red + (wk * kP3BM + row) * ldr + col) = acc[ib][cb];
+            }
         __syncthreads();
         // ---- (B) ring rows of the tile after next, then this tile's epilogue ----
         store_rows(batch_rows(tt), (tt * kP3BM) % RING, bt);
