@@ -55,6 +55,7 @@ constexpr int kP3MaxH = 896;        // tallest image (exact multiply-shift row q
 struct P3Geom {
     int KP, NP, lda, ldw, ldr, ring;
     int PW, PH, MP;                 // padded row length W + 2, image height H + 2, positions n PH PW
+    int grid, mp_q, mp_r;           // workgroups and MP = mp_q grid + mp_r (set by the launcher)
     double inv_pw, inv_ph;
     uint32_t rpw, rph;              // ceil(2^20 / PW), ceil(2^20 / PH): multiply-shift quotients
     size_t ring_bytes, stage_bytes, lds;
@@ -72,6 +73,7 @@ static P3Geom p3_geom(int K, int N, int W)
     g.ring_bytes = (size_t)(g.ring + 17) * g.lda * 2;   // + copies of the first 16 rows + a junk row
     g.PW = W + 2;
     g.PH = 0; g.MP = 0; g.inv_pw = 1.0 / g.PW; g.inv_ph = 0.0;   // set by the launcher
+    g.grid = 1; g.mp_q = 0; g.mp_r = 0;
     const size_t wst = (size_t)9 * g.NP * g.ldw * 2;
     const size_t red = (size_t)(g.KP / 32) * kP3BM * g.ldr * 4;
     const size_t stats = (size_t)2 * (kP3Threads / (g.NP / 8)) * g.NP * 4;
@@ -177,8 +179,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const int K = p.K, N = p.N, RING = g.ring, lda = g.lda, ldr = g.ldr;
     const int m = (int)p.m;                                      // launcher: m < 2^30
     const int H = p.h, W = p.w, PW = g.PW;
-    const int P0 = (int)((int64_t)blockIdx.x * g.MP / gridDim.x);
-    const int P1 = (int)((int64_t)(blockIdx.x + 1) * g.MP / gridDim.x);
+    // range [floor(b MP / G), floor((b + 1) MP / G)) in 32-bit arithmetic
+    // (b mp_q <= MP < 2^30, b mp_r < G^2): no 64-bit division, whose branches
+    // would serialise the kernel-argument loads around it
+    const int bid = blockIdx.x;
+    const int P0 = bid * g.mp_q + (int)((uint32_t)(bid * g.mp_r) / (uint32_t)g.grid);
+    const int P1 = (bid + 1) * g.mp_q + (int)((uint32_t)((bid + 1) * g.mp_r) / (uint32_t)g.grid);
     const T *wsrc = reinterpret_cast<const T *>(p.wraw);
     constexpr uint32_t ES = sizeof(T);
     // operand views as raw buffers (launcher guarantees each spans < 2^31 bytes)
@@ -439,7 +445,6 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     // epilogue of this tile runs, and the next batch and epilogue operand are
     // loaded.
     auto tile = [&](int p0, Batch &bt) __attribute__((always_inline)) {
-        const int nrows = P1 - p0 < kP3BM ? P1 - p0 : kP3BM;
         const int tt = (p0 - P0) / kP3BM;
 
         // ---- (A) matrix cores: 16 RB rows x 32 columns x 32 K per wave, nine taps ----
@@ -613,7 +618,7 @@ int64_t conv3x3_partial_rows(int64_t m)
 }
 
 template <int WK, int WN, int EK, int PC>
-static hipError_t run_p3(const RowsParams &p, const P3Geom &g, hipStream_t s)
+static hipError_t run_p3(const RowsParams &p, const P3Geom &g0, hipStream_t s)
 {
     constexpr bool BNG = PC == PC3_BNGRAD;
     auto kern = k_conv3x3<WK, WN, EK, PC>;
@@ -624,6 +629,10 @@ static hipError_t run_p3(const RowsParams &p, const P3Geom &g, hipStream_t s)
         attr_set = true;
     }
     const int grid = (int)conv3x3_partial_rows(p.m);
+    P3Geom g = g0;
+    g.grid = grid;
+    g.mp_q = g.MP / grid;
+    g.mp_r = g.MP % grid;
     const double e = 2.0, m = (double)p.m;
     double a = m * p.K;
     if (BNG || PC == PC3_BNRELU_SAVE) a *= 2.0;     // second operand read / z written

@@ -406,7 +406,7 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
         if (TAPS == 1) {
             const int q = tid / (zside ? VZ : VG) + j * (kThreads / (zside ? VZ : VG));
             const int pp = base + q;
-            return (q < KQ) & (pp < (int)m) ? pp : -1;
+            return ((q < KQ) & (pp < (int)m)) ? pp : -1;
         }
         const int r = zside ? zrr[j] : grr[j];
         const int o = zside ? zro[j] : gro[j];
