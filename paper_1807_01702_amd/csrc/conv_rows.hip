@@ -53,15 +53,18 @@
 
 namespace bnr {
 
-template <typename T, int TAPS, int BM, int BN>
+// BK: input channels per K chunk (kRowsBK, or kRowsBKDirect for the
+// specialised bf16 1x1 cases below, whose weights are staged either as rows
+// of n ([n][k], pitch ASTR) or as rows of k ([k][n], pitch BN + 8)).
+template <typename T, int TAPS, int BM, int BN, int BK = kRowsBK>
 struct RowsCfg {
     static constexpr int VEC = Elem<T>::VEC;
     static constexpr int PAD = 16 / (int)sizeof(T);
-    static constexpr int ASTR = kRowsBK + PAD;                 // staged row stride (elements)
+    static constexpr int ASTR = BK + PAD;                      // staged row stride (elements)
     static constexpr int HALO_MAX = TAPS == 9 ? kRowsMaxW3 + 1 : 0;
     static constexpr int AROWS = BM + 2 * HALO_MAX;
     static constexpr int A_ELEMS = AROWS * ASTR;
-    static constexpr int B_ELEMS = TAPS * BN * ASTR;
+    static constexpr int B_ELEMS = TAPS * (BN * ASTR > BK * (BN + 8) ? BN * ASTR : BK * (BN + 8));
     static constexpr int CSTR = BN + PAD;
     static constexpr size_t STAGE_BYTES = (size_t)(A_ELEMS + B_ELEMS) * sizeof(T);
     static constexpr size_t EPI_BYTES = (size_t)BM * CSTR * sizeof(T);
@@ -79,15 +82,22 @@ struct RowsCfg {
 // in late dense blocks, the mode branches are on the critical path (forward
 // about 20% of the launch, data gradient about 6%).
 enum { SP_RUNTIME = 0, SP_FWD_BNRELU = 1, SP_DGRAD_BNGRAD = 2 };
+// K chunk of the forward case: a wider chunk means fewer load round trips and
+// barriers per tile (K up to 1024 in late DenseNet blocks).  The data
+// gradient (K = 128, N up to 1024, epilogue-bound) keeps 32: wider chunks
+// made it slower.
+constexpr int kRowsBKDirect = 64;
+template <int SP> constexpr int rows_bk() { return SP == SP_FWD_BNRELU ? kRowsBKDirect : kRowsBK; }
 
 template <typename T, int TAPS, int BM, int BN, int WM, int WN, int SP>
 __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
 {
     static_assert(SP == SP_RUNTIME || (TAPS == 1 && sizeof(T) == 2), "specialised cases are bf16 1x1");
-    using Cfg = RowsCfg<T, TAPS, BM, BN>;
+    constexpr int BK = rows_bk<SP>();
+    using Cfg = RowsCfg<T, TAPS, BM, BN, BK>;
     using M = Mfma<T>;
     constexpr int TM = BM / (WM * 16), TN = BN / (WN * 16);
-    constexpr int VEC = Cfg::VEC, ASTR = Cfg::ASTR, VPR = kRowsBK / VEC;
+    constexpr int VEC = Cfg::VEC, ASTR = Cfg::ASTR, VPR = BK / VEC;
     static_assert(WM * WN == 4, "four waves");
     static_assert(TM * WM * 16 == BM && TN * WN * 16 == BN, "tile");
 
@@ -142,7 +152,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     for (int rb = 0; rb < TM; rb++)
         for (int cb = 0; cb < TN; cb++) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nchunks = (K + kRowsBK - 1) / kRowsBK;
+    const int nchunks = (K + BK - 1) / BK;
     const T *asrc = reinterpret_cast<const T *>(p.a);
     const T *asrc2 = reinterpret_cast<const T *>(p.a2);
     __syncthreads();
@@ -172,7 +182,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             constexpr int BP = BN + 8;                                // pitch of the [k][n] staging
             const __amdgpu_buffer_rsrc_t wbuf =
                 direct ? buf_view(p.wraw, (uint32_t)((int64_t)K * N * sizeof(T)))
-                       : buf_view(p.wpack, (uint32_t)((int64_t)gridDim.y * nchunks * BN * kRowsBK * sizeof(T)));
+                       : buf_view(p.wpack, (uint32_t)((int64_t)gridDim.y * nchunks * BN * BK * sizeof(T)));
             const int a_ldc = (int)p.a_ldc, a2_ldc = (int)p.a2_ldc;
             int apix[NA], arow[NA], avec[NA];
             #pragma unroll
@@ -192,7 +202,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             }
             vec16 ra[NA], rx[NA], rw[NB];
             auto load_chunk = [&](int ch) __attribute__((always_inline)) {
-                const int c0 = ch * kRowsBK;
+                const int c0 = ch * BK;
                 #pragma unroll
                 for (int j = 0; j < NA; j++) {
                     const int c = c0 + avec[j] * VEC;
@@ -201,7 +211,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     if (pro == PRO_BNGRAD)
                         rx[j] = bld16(a2buf, ok ? (uint32_t)(apix[j] * a2_ldc + c) * (uint32_t)sizeof(T) : kBufOff);
                 }
-                const uint32_t wofs = (uint32_t)(((int64_t)nt * nchunks + ch) * (BN * kRowsBK));
+                const uint32_t wofs = (uint32_t)(((int64_t)nt * nchunks + ch) * (BN * BK));
                 #pragma unroll
                 for (int j = 0; j < NB; j++) {
                     const int i = tid + j * kThreads;
@@ -213,13 +223,13 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                         const int nn = n0 + i / VPR, k = c0 + (i % VPR) * VEC;
                         if (i < BN * VPR && nn < N && k < K) off = (uint32_t)(nn * K + k) * (uint32_t)sizeof(T);
                     } else if (i < BN * VPR) {
-                        off = (wofs + (uint32_t)((i / VPR) * kRowsBK + (i % VPR) * VEC)) * (uint32_t)sizeof(T);
+                        off = (wofs + (uint32_t)((i / VPR) * BK + (i % VPR) * VEC)) * (uint32_t)sizeof(T);
                     }
                     rw[j] = bld16(wbuf, off);
                 }
             };
             auto store_chunk = [&](int ch) __attribute__((always_inline)) {
-                const int c0 = ch * kRowsBK;
+                const int c0 = ch * BK;
                 #pragma unroll
                 for (int j = 0; j < NA; j++) {
                     const int c = c0 + avec[j] * VEC;
@@ -279,7 +289,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                 store_chunk(ch);
                 __syncthreads();
                 if (ch + 1 < nchunks) load_chunk(ch + 1);
-                for (int ks = 0; ks < kRowsBK / M::KSTEP; ks++) {
+                for (int ks = 0; ks < BK / M::KSTEP; ks++) {
                     const int kofs = ks * M::KSTEP + (lane >> 4) * M::KPL;
                     typename M::frag b[TN];
                     if constexpr (kTr) {
@@ -311,7 +321,7 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
         }
     }
     for (int ch = 0; ch < ((TAPS == 1 && (SP != SP_RUNTIME || p.buf32)) ? 0 : nchunks); ch++) {
-        const int c0 = ch * kRowsBK;
+        const int c0 = ch * BK;
         // ---- stage A (prologue applied, zero outside the tensor) ----
         for (int i = tid; i < arows * VPR; i += kThreads) {
             const int r = i / VPR, v = i % VPR;
@@ -382,17 +392,17 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
             *reinterpret_cast<vec16 *>(As + r * ASTR + v * VEC) = out;
         }
         // ---- stage B: all taps of this chunk (packed, zero-padded) ----
-        const T *wsrc = reinterpret_cast<const T *>(p.wpack) + ((int64_t)nt * nchunks + ch) * (TAPS * BN * kRowsBK);
+        const T *wsrc = reinterpret_cast<const T *>(p.wpack) + ((int64_t)nt * nchunks + ch) * (TAPS * BN * BK);
         for (int i = tid; i < TAPS * BN * VPR; i += kThreads) {
             const int row = i / VPR, v = i % VPR;
-            *reinterpret_cast<vec16 *>(Bs + row * ASTR + v * VEC) = ldg16(wsrc + row * kRowsBK + v * VEC);
+            *reinterpret_cast<vec16 *>(Bs + row * ASTR + v * VEC) = ldg16(wsrc + row * BK + v * VEC);
         }
         __syncthreads();
         // ---- matrix cores ----
         for (int tap = 0; tap < TAPS; tap++) {
             const int dh = TAPS == 9 ? tap / 3 - 1 : 0, dw = TAPS == 9 ? tap % 3 - 1 : 0;
             const int off = dh * W + dw;
-            for (int ks = 0; ks < kRowsBK / M::KSTEP; ks++) {
+            for (int ks = 0; ks < BK / M::KSTEP; ks++) {
                 const int kofs = ks * M::KSTEP + (lane >> 4) * M::KPL;
                 typename M::frag b[TN];
                 for (int cb = 0; cb < TN; cb++)
@@ -602,7 +612,7 @@ bool rows_direct_weights(int dtype, int taps, int64_t m, int K, int N, int64_t a
 template <typename T, int TAPS, int BM, int BN, int WM, int WN, int SP = SP_RUNTIME>
 static hipError_t run_rows(const RowsParams &p, hipStream_t s)
 {
-    using Cfg = RowsCfg<T, TAPS, BM, BN>;
+    using Cfg = RowsCfg<T, TAPS, BM, BN, rows_bk<SP>()>;
     const int P = p.pro == PRO_BNRELU || p.pro == PRO_BNGRAD || p.pro == PRO_BNRELU_POOL || p.pro == PRO_BNADDRELU
                       ? (sizeof(T) == 4 ? 4 : 3) : 0;
     const size_t lds = Cfg::LDS + (size_t)P * p.K * sizeof(float);
