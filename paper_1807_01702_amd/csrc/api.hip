@@ -288,7 +288,7 @@ void fill_rows(RowsParams &rp, const bnr_conv_desc *d, int K, int N)
 bnr_status launch_conv_any(RowsParams &rp, const bnr_conv_desc *d, const void *w, int transpose, void *wpack,
                            int64_t *rows, hipStream_t s)
 {
-    if (rp.taps == 1 && conv1x1_supported(rp.dtype, rp.K, rp.N)) {
+    if (rp.taps == 1 && conv1x1_supported(rp.dtype, rp.K, rp.N, rp.epi)) {
         rp.wraw = w;
         rp.wtrans = transpose;
         TRY_HIP(launch_conv1x1(rp, s, rows), transpose ? "conv data gradient" : "conv forward");

@@ -29,8 +29,12 @@ constexpr int kP1Threads = 512;
 constexpr int kP1BM = 128;     // largest tile height (rows = pixels)
 constexpr int kP1NV = 8;       // 16-byte vectors per thread for a tile operand
 
+// Output columns in ncg groups of ncol (the last one may be shorter), each
+// computed by gcw workgroups; ncg > 1 only for widths past 256 (the data
+// gradient of a wide concatenation), one group per 256 columns at most.
 struct P1Geom {
     int KP, NP, lda, ldw, ldc;
+    int ncg, ncol, gcw;
     size_t region, lds;
 };
 
@@ -42,6 +46,7 @@ static P1Geom p1_geom(int K, int N, bool fine = false)
     P1Geom g;
     g.KP = (K + 31) / 32 * 32;
     g.NP = fine ? (N + 31) / 32 * 32 : (N <= 32 ? 32 : (N <= 64 ? 64 : (N <= 128 ? 128 : 256)));
+    g.ncg = 1; g.ncol = N; g.gcw = 1;
     g.lda = g.KP + 8;
     g.ldw = g.KP + 8;
     g.ldc = g.NP + 8;
@@ -98,7 +103,11 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;              // 4 x 2 waves: 16 RB rows x NP/2 columns each
-    const int K = p.K, N = p.N, KP = g.KP, NP = g.NP;
+    // column group cg: this workgroup's output columns [col0, col0 + N) of NT
+    const int cg = (int)blockIdx.x / g.gcw;
+    const int col0 = cg * g.ncol, NT = p.N;
+    const int N = NT - col0 < g.ncol ? NT - col0 : g.ncol;
+    const int K = p.K, KP = g.KP, NP = g.NP;
     const int m = (int)p.m;                               // launcher: m < 2^30
     const int H = p.h, W = p.w;
     const T *wsrc = reinterpret_cast<const T *>(p.wraw);
@@ -111,18 +120,19 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     const int side_ldc = (int)p.side_ldc;
     const __amdgpu_buffer_rsrc_t sbuf = buf_view(SIDE ? p.side : p.a,
                                                  SIDE ? (uint32_t)(((int64_t)(m - 1) * side_ldc + K) * 2) : 0u);
-    const __amdgpu_buffer_rsrc_t ybuf = buf_view(p.y, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * 2));
-    const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
+    const T *ycol = reinterpret_cast<const T *>(p.y) + col0;
+    const __amdgpu_buffer_rsrc_t ybuf = buf_view(ycol, (uint32_t)(((int64_t)(m - 1) * y_ldc + N) * 2));
+    const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? reinterpret_cast<const T *>(p.ex) + col0 : ycol,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * 2) : 0u);
     const int ex2_ldc = (int)p.ex2_ldc;
-    const __amdgpu_buffer_rsrc_t x2buf = buf_view(p.ex2 ? p.ex2 : p.y,
+    const __amdgpu_buffer_rsrc_t x2buf = buf_view(p.ex2 ? reinterpret_cast<const T *>(p.ex2) + col0 : ycol,
                                                   p.ex2 ? (uint32_t)(((int64_t)(m - 1) * ex2_ldc + N) * 2) : 0u);
 
     // ---- weights -> LDS as Ws[n][k] (zero outside K x N), in batches of
     // kWB vectors per thread whose loads are all in flight before any write ----
     {
         constexpr int kWB = 8;
-        const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(K * N * 2));
+        const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(K * NT * 2));
         const int total = KP * NP / VEC;
         for (int base = 0; base < total; base += kWB * kP1Threads) {
             vec16 v[kWB];
@@ -132,10 +142,10 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 int off;
                 if (!p.wtrans) {  // forward: W[k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k
                     const int n0 = (i / KP) * VEC, k = i % KP;
-                    off = i < total && k < K && n0 < N ? (k * N + n0) * 2 : (int)kBufOff;
+                    off = i < total && k < K && n0 < N ? (k * NT + col0 + n0) * 2 : (int)kBufOff;
                 } else {          // data gradient: W[n][k] (n = c_in, k = c_out), rows of k
                     const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
-                    off = i < total && n < N && k0 < K ? (n * K + k0) * 2 : (int)kBufOff;
+                    off = i < total && n < N && k0 < K ? ((col0 + n) * K + k0) * 2 : (int)kBufOff;
                 }
                 v[u] = bld16(wbuf, (uint32_t)off);
             }
@@ -170,8 +180,9 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     }
     for (int c = tid; c < NP; c += kP1Threads) {
         float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
-        if (c < N && BNBWD) { e0 = p.e_mean[c]; e1 = p.e_rstd[c]; e2 = p.e_gamma[c]; e3 = p.e_beta[c]; }
-        if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[c];     // statistics of y - shift
+        const int cc = col0 + c;
+        if (c < N && BNBWD) { e0 = p.e_mean[cc]; e1 = p.e_rstd[cc]; e2 = p.e_gamma[cc]; e3 = p.e_beta[cc]; }
+        if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[cc];     // statistics of y - shift
         epi[c] = e0; epi[NP + c] = e1; epi[2 * NP + c] = e2; epi[3 * NP + c] = e3;
     }
 
@@ -344,7 +355,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     float s1[VEC], s2[VEC];
     #pragma unroll
     for (int e = 0; e < VEC; e++) { s1[e] = 0.f; s2[e] = 0.f; }
-    T *yout = reinterpret_cast<T *>(p.y);
+    T *yout = reinterpret_cast<T *>(p.y) + col0;
 
     __syncthreads();
     // this thread's epilogue channels are fixed: keep their BN parameters in registers
@@ -387,7 +398,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     };
     // work items: F rounds of whole tiles (item k < F is tile k*G + gi, rows
     // [p0, p0 + BM)), then this workgroup's share [lo, hi) of the R rows left
-    const int G = gridDim.x, gi = blockIdx.x;
+    const int G = g.gcw, gi = (int)blockIdx.x - cg * g.gcw;
     const int F = m / (G * BM), R = m - F * G * BM;         // R < G*BM <= 2^16, so gi*R fits
     const int lo = F * G * BM + gi * R / G, hi = F * G * BM + (gi + 1) * R / G;
     const int nitems = F + (hi > lo ? 1 : 0);
@@ -503,8 +514,8 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                 red[r0 * NP + n + e] = s1[e];
                 red[(RSTEP + r0) * NP + n + e] = s2[e];
             }
-        lds_colsum2(red, RSTEP, NP, NP, kP1Threads, tid, p.part + (int64_t)blockIdx.x * 2 * N,
-                    p.part + (int64_t)blockIdx.x * 2 * N + N, N);
+        lds_colsum2(red, RSTEP, NP, NP, kP1Threads, tid, p.part + (int64_t)gi * 2 * NT + col0,
+                    p.part + (int64_t)gi * 2 * NT + NT + col0, N);
     }
 }
 
@@ -521,10 +532,23 @@ static int device_cus()
     return cus;
 }
 
-bool conv1x1_supported(int dtype, int K, int N)
+// Column groups: one up to 256 output columns; the data gradient with the
+// BN-backward epilogue (the gradient of a wide concatenation) takes up to
+// kP1MaxN columns in groups of at most 256, equal widths rounded up to 32.
+// Every group re-reads the A rows (K <= 256 channels, small beside the
+// epilogue's three N-wide sweeps).
+constexpr int kP1MaxN = 2048;
+static int p1_group_cols(int N)
 {
-    if (dtype != DT_BF16 || K > 256 || N > 256) return false;
-    const P1Geom g = p1_geom(K, N);
+    if (N <= 256) return N;
+    const int64_t ncg = ceil_div(N, 256);
+    return (int)(ceil_div(ceil_div(N, ncg), 32) * 32);
+}
+
+bool conv1x1_supported(int dtype, int K, int N, int epi)
+{
+    if (dtype != DT_BF16 || K > 256 || N < 1 || N > kP1MaxN || (N > 256 && epi != EPI_BNBWD)) return false;
+    const P1Geom g = p1_geom(K, p1_group_cols(N));
     if (g.lds > 150 * 1024) return false;
     if ((int64_t)kP1BM * (g.KP / 8) > (int64_t)kP1NV * kP1Threads) return false;      // A tile registers
     if (kP1BM / (kP1Threads / (g.NP / 8)) > kP1NV) return false;                       // epilogue registers
@@ -557,8 +581,11 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
         per_cu < 1)
         per_cu = 1;
     const int64_t gmax = (int64_t)device_cus() * (per_cu < 2 ? per_cu : 2);
-    const int grid = (int)(ntiles < gmax ? ntiles : gmax);
-    *rows = grid;
+    const int64_t per_group = gmax / g.ncg > 1 ? gmax / g.ncg : 1;
+    P1Geom gg = g;
+    gg.gcw = (int)(ntiles < per_group ? ntiles : per_group);
+    const int grid = gg.gcw * g.ncg;
+    *rows = gg.gcw;
     const double m = (double)p.m;
     double a = m * p.K;
     if (BNG) a *= 2.0;
@@ -570,7 +597,7 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
     if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD || EK == EK_BNBWD_SC) out += m * p.N;
     if (EK == EK_BNBWD_SCACC) out += 2.0 * m * p.N;
     TraceScope tr(KC_CONV, KID_CONV_1X1, s, 2.0 * (a + out + (double)p.K * p.N), 2.0 * m * p.K * p.N);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kP1Threads), g.lds, s, p, g);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kP1Threads), g.lds, s, p, gg);
     return hipGetLastError();
 }
 
@@ -636,7 +663,7 @@ static hipError_t run_p1_ek(const RowsParams &p, const P1Geom &g, int ek, hipStr
 
 hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
 {
-    if (!p.a || !p.wraw || !p.y || p.taps != 1 || !conv1x1_supported(p.dtype, p.K, p.N)) return hipErrorInvalidValue;
+    if (!p.a || !p.wraw || !p.y || p.taps != 1 || !conv1x1_supported(p.dtype, p.K, p.N, p.epi)) return hipErrorInvalidValue;
     if (p.pro == PRO_BNRELU && (!p.p_mean || !p.p_gamma || !p.p_rstd || !p.p_beta)) return hipErrorInvalidValue;
     if (p.pro == PRO_BNGRAD && (!p.a2 || !p.p_mean || !p.p_rstd ||
                                 (p.p_split ? (!p.p_alpha || !p.p_betap) : (!p.p_gamma || !p.p_dbeta || !p.p_dgamma))))
@@ -666,7 +693,10 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
     if (p.m < 1 || arows >= (lim >> 1) || (arows * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
-    const P1Geom g = p1_geom(p.K, p.N, p.epi == EPI_BNBWD);
+    const int ncol = p1_group_cols(p.N);
+    P1Geom g = p1_geom(p.K, ncol, p.epi == EPI_BNBWD);
+    g.ncg = (int)ceil_div(p.N, ncol);
+    g.ncol = ncol;
     const int ek = epilogue_kind(p.epi, p.accumulate, p.e_scale);
     if (poolf) return ek == EK_STATS ? run_p1_nva<EK_STATS, PC_BNRELU_POOL>(p, g, s, rows)
                                      : run_p1_nva<EK_STORE, PC_BNRELU_POOL>(p, g, s, rows);

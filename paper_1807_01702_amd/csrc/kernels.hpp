@@ -146,7 +146,7 @@ hipError_t launch_pack_weights(int dtype, const void *w, int k, int c_in, int c_
 hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s);
 
 // ---- persistent 1x1 CONV (weights resident in LDS, one workgroup per CU) ----
-bool conv1x1_supported(int dtype, int K, int N);
+bool conv1x1_supported(int dtype, int K, int N, int epi);
 int64_t conv1x1_partial_rows(int64_t m);      // upper bound of the statistics partial rows it writes
 hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows);   // *rows: partial rows written
 

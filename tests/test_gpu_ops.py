@@ -256,6 +256,7 @@ BWD_CASES = [
     (True, 1, 2, 7, 7, 512, 128),               # tiled 1x1 forward weights [k][n] and data gradient [n][k] unpacked
     (True, 1, 1, 9, 11, 288, 40),               # ragged: K and N past the 256-channel persistent kernel
     (True, 1, 1, 6, 7, 264, 24),                # tiled 1x1: one 8-channel tail chunk, 32-channel output tile
+    (True, 1, 1, 5, 7, 1000, 128),              # persistent 1x1 data gradient in four column groups (256 x 3 + 232)
     (True, 3, 4, 56, 56, 128, 32),              # 3x3 weight gradient: 5 chunks per split, Z rows carried between
                                                 # chunks, splits crossing image boundaries
     (True, 3, 8, 30, 7, 64, 32),                # same with 14-row chunks of 7-pixel rows
@@ -461,6 +462,7 @@ def test_bn_dx_and_avgpool(B, bf16):
     (False, 3, 2, 6, 7, 24, 40, (16, 40), 12),     # fp32: tiled kernels, ragged
     (True, 3, 2, 10, 12, 32, 96, (128, 64), 128),  # bf16: persistent 1x1 readers, 3x3 producer
     (True, 1, 1, 9, 11, 136, 160, (128, 256), 64),  # bf16: wide slice, 1x1 producer
+    (True, 1, 1, 9, 11, 288, 320, (128, 64), 64),  # slice past 256 channels: readers' data gradients in two column groups
 ])
 def test_split_fusion_two_readers(B, case):
     """A concatenation slice x read by two BN-ReLU-CONV1x1 layers that share
