@@ -534,22 +534,27 @@ static int device_cus()
 
 // Column groups: one up to 256 output columns; the data gradient with the
 // BN-backward epilogue (the gradient of a wide concatenation) takes up to
-// kP1MaxN columns in groups of at most 256, equal widths rounded up to 32.
-// Every group re-reads the A rows (K <= 256 channels, small beside the
-// epilogue's three N-wide sweeps).
+// kP1MaxN columns in the fewest groups of equal width (rounded up to 32, at
+// most 256) whose weight columns and staging fit the LDS.  Every group
+// re-reads the A rows (K <= 256 channels, small beside the epilogue's three
+// N-wide sweeps).
 constexpr int kP1MaxN = 2048;
-static int p1_group_cols(int N)
+constexpr size_t kP1MaxLds = 150 * 1024;
+static int p1_group_cols(int K, int N)
 {
     if (N <= 256) return N;
-    const int64_t ncg = ceil_div(N, 256);
-    return (int)(ceil_div(ceil_div(N, ncg), 32) * 32);
+    for (int64_t ncg = ceil_div(N, 256); ncg <= ceil_div(N, 32); ncg++) {
+        const int ncol = (int)(ceil_div(ceil_div(N, ncg), 32) * 32);
+        if (p1_geom(K, ncol).lds <= kP1MaxLds) return ncol;
+    }
+    return 32;
 }
 
 bool conv1x1_supported(int dtype, int K, int N, int epi)
 {
     if (dtype != DT_BF16 || K > 256 || N < 1 || N > kP1MaxN || (N > 256 && epi != EPI_BNBWD)) return false;
-    const P1Geom g = p1_geom(K, p1_group_cols(N));
-    if (g.lds > 150 * 1024) return false;
+    const P1Geom g = p1_geom(K, p1_group_cols(K, N));
+    if (g.lds > kP1MaxLds) return false;
     if ((int64_t)kP1BM * (g.KP / 8) > (int64_t)kP1NV * kP1Threads) return false;      // A tile registers
     if (kP1BM / (kP1Threads / (g.NP / 8)) > kP1NV) return false;                       // epilogue registers
     return true;
@@ -693,7 +698,7 @@ hipError_t launch_conv1x1(const RowsParams &p, hipStream_t s, int64_t *rows)
     if (p.m < 1 || arows >= (lim >> 1) || (arows * p.a_ldc + p.K) * 2 >= lim || (p.m * p.y_ldc + p.N) * 2 >= lim ||
         (p.a2 && (p.m * p.a2_ldc + p.K) * 2 >= lim) || (p.ex && (p.m * p.ex_ldc + p.N) * 2 >= lim))
         return hipErrorInvalidValue;
-    const int ncol = p1_group_cols(p.N);
+    const int ncol = p1_group_cols(p.K, p.N);
     P1Geom g = p1_geom(p.K, ncol, p.epi == EPI_BNBWD);
     g.ncg = (int)ceil_div(p.N, ncol);
     g.ncol = ncol;

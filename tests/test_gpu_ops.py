@@ -257,6 +257,7 @@ BWD_CASES = [
     (True, 1, 1, 9, 11, 288, 40),               # ragged: K and N past the 256-channel persistent kernel
     (True, 1, 1, 6, 7, 264, 24),                # tiled 1x1: one 8-channel tail chunk, 32-channel output tile
     (True, 1, 1, 5, 7, 1000, 128),              # persistent 1x1 data gradient in four column groups (256 x 3 + 232)
+    (True, 1, 1, 6, 10, 512, 256),              # K = 256: four 128-column groups (256-column groups exceed the LDS)
     (True, 3, 4, 56, 56, 128, 32),              # 3x3 weight gradient: 5 chunks per split, Z rows carried between
                                                 # chunks, splits crossing image boundaries
     (True, 3, 8, 30, 7, 64, 32),                # same with 14-row chunks of 7-pixel rows
