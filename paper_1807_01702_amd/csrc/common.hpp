@@ -163,20 +163,28 @@ __device__ __forceinline__ float bn_centre(const float *ctr, int c) {
 // holds D = sum_l gamma_l rstd dy_l and the per-channel sums
 // alpha = -sum_l gamma_l rstd dbeta_l/m, betap = -sum_l gamma_l rstd dgamma_l/m,
 // so d = D + alpha + betap xhat: A = 1, B = betap rstd, C = alpha - B mean.
+// The same from the channel's values: split = 1 takes (alpha, betap) in the
+// places of (gamma, dgamma) and ignores dbeta.
+__device__ __forceinline__ void deferred_coef_of(int split, float inv_m, float gamma, float mean, float rstd,
+                                                 float dgamma, float dbeta, float &A, float &B, float &C)
+{
+    if (split) {
+        A = 1.f;
+        B = dgamma * rstd;
+        C = gamma - B * mean;
+    } else {
+        const float k = gamma * rstd, b = dgamma * inv_m * rstd;
+        A = k;
+        B = -k * b;
+        C = k * (b * mean - dbeta * inv_m);
+    }
+}
 __device__ __forceinline__ void deferred_coef(int split, int c, float inv_m, const float *gamma, const float *mean,
                                               const float *rstd, const float *dgamma, const float *dbeta,
                                               const float *alpha, const float *betap, float &A, float &B, float &C)
 {
-    if (split) {
-        A = 1.f;
-        B = betap[c] * rstd[c];
-        C = alpha[c] - B * mean[c];
-    } else {
-        const float k = gamma[c] * rstd[c], b = dgamma[c] * inv_m * rstd[c];
-        A = k;
-        B = -k * b;
-        C = k * (b * mean[c] - dbeta[c] * inv_m);
-    }
+    if (split) deferred_coef_of(1, inv_m, alpha[c], mean[c], rstd[c], betap[c], 0.f, A, B, C);
+    else deferred_coef_of(0, inv_m, gamma[c], mean[c], rstd[c], dgamma[c], dbeta[c], A, B, C);
 }
 
 // Eight consecutive floats from a 32-byte aligned LDS address (two 16-byte reads).

@@ -560,12 +560,11 @@ bool conv1x1_supported(int dtype, int K, int N, int epi)
     return true;
 }
 
-// Up to two workgroups per CU (when a variant's LDS and registers allow it,
-// the second hides the first's load / epilogue latency).
+// One workgroup per CU (see run_p1): at most one partial row per CU.
 int64_t conv1x1_partial_rows(int64_t m)
 {
     const int64_t tiles = ceil_div(m, 64);
-    const int64_t g = 2 * (int64_t)device_cus();
+    const int64_t g = device_cus();
     return tiles < g ? tiles : g;
 }
 
@@ -580,12 +579,10 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
         if (e != hipSuccess) return e;
         attr_set = true;
     }
+    // one workgroup per CU: a second one (where registers and LDS would allow
+    // it) measured no faster and doubles the statistics partial rows
     const int ntiles = (int)ceil_div(p.m, BM);
-    int per_cu = 1;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)kern, kP1Threads, g.lds) != hipSuccess ||
-        per_cu < 1)
-        per_cu = 1;
-    const int64_t gmax = (int64_t)device_cus() * (per_cu < 2 ? per_cu : 2);
+    const int64_t gmax = device_cus();
     const int64_t per_group = gmax / g.ncg > 1 ? gmax / g.ncg : 1;
     P1Geom gg = g;
     gg.gcw = (int)(ntiles < per_group ? ntiles : per_group);

@@ -224,75 +224,92 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             if (BNG) bt.b[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(bt.pix * a2_ldc + c) * ES : kBufOff);
         }
     };
-    // ring fill: the first tile's window, positions [P0 - H1, P0 + 128 + H1)
-    // = RING rows in two batches, loaded before the weights are staged
+    // ---- prologue loads, in the order they are needed: the per-channel
+    // parameters (thread c holds channel c; KPC, NPC <= 128), the weights,
+    // then the ring fill (the first tile's window, positions
+    // [P0 - H1, P0 + 128 + H1) = RING rows in two batches).  Loads complete
+    // in issue order for the wait counter, so the weight staging waits only
+    // for the parameters and the weights, and the fill stays in flight.
+    //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
+    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef_of)
+    float q0 = 0.f, q1 = 0.f, q2 = 0.f, q3 = 0.f, q4 = 0.f;
+    if (tid < K && pro == PRO_BNRELU) {
+        q0 = p.p_gamma[tid]; q1 = p.p_beta[tid]; q2 = p.p_mean[tid]; q3 = p.p_rstd[tid];
+    } else if (tid < K && pro == PRO_BNGRAD) {
+        q1 = p.p_mean[tid]; q2 = p.p_rstd[tid];
+        if (p.p_split) { q0 = p.p_alpha[tid]; q3 = p.p_betap[tid]; }
+        else { q0 = p.p_gamma[tid]; q3 = p.p_dgamma[tid]; q4 = p.p_dbeta[tid]; }
+    }
+    float ep0 = 0.f, ep1 = 1.f, epg = 0.f, epb = 0.f;
+    if (tid < N && EK == EK_BNBWD) { ep0 = p.e_mean[tid]; ep1 = p.e_rstd[tid]; epg = p.e_gamma[tid]; epb = p.e_beta[tid]; }
+    if (tid < N && EK == EK_STATS && p.e_shift) ep0 = p.e_shift[tid];     // statistics of y - shift
+
+    // weights -> LDS stage as Ws[tap][n][k] (zero outside K x N), in batches
+    // of kWB vectors per thread whose loads are all in flight before any write
+    constexpr int kWB = 16;
+    const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(9 * K * N * ES));
+    constexpr int wtotal = 9 * KPC * NPC / VEC;
+    constexpr int VPK = KPC / VEC;
+    vec16 wv[kWB];
+    auto load_w = [&](int base) __attribute__((always_inline)) {
+        #pragma unroll
+        for (int u = 0; u < kWB; u++) {
+            const int i = base + u * kP3Threads + tid;
+            int off;
+            if (!p.wtrans) {  // forward: W[tap][k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k
+                const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
+                const int n0 = (rem / KPC) * VEC, k = rem % KPC;
+                off = i < wtotal && k < K && n0 < N ? ((tap * K + k) * N + n0) * (int)ES : (int)kBufOff;
+            } else {          // data gradient: W[8 - tap][n][k] (n = c_in, k = c_out), rows of k
+                const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
+                const int n = rem / VPK, k0 = (rem % VPK) * VEC;
+                off = i < wtotal && n < N && k0 < K ? (((8 - tap) * N + n) * K + k0) * (int)ES : (int)kBufOff;
+            }
+            wv[u] = bld16(wbuf, (uint32_t)off);
+        }
+    };
+    auto write_w = [&](int base) __attribute__((always_inline)) {
+        #pragma unroll
+        for (int u = 0; u < kWB; u++) {
+            const int i = base + u * kP3Threads + tid;
+            if (i >= wtotal) break;
+            if (!p.wtrans) {  // scatter the n row to columns (a wave writes 64 consecutive k of a column)
+                const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
+                const int n0 = (rem / KPC) * VEC, k = rem % KPC;
+                #pragma unroll
+                for (int e = 0; e < VEC; e++)
+                    Ws[(tap * NPC + n0 + e) * g.ldw + k] =
+                        (T)((e & 1) ? (wv[u].u[e >> 1] >> 16) : (wv[u].u[e >> 1] & 0xffffu));
+            } else {          // rows copy straight
+                const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
+                const int n = rem / VPK, k0 = (rem % VPK) * VEC;
+                *reinterpret_cast<vec16 *>(Ws + (tap * NPC + n) * g.ldw + k0) = wv[u];
+            }
+        }
+    };
+    load_w(0);
     const int H1 = g.PW + 1;
     Batch bt0, bt1;
     load_rows(P0 - H1, kP3BM, bt0);
     load_rows(P0 - H1 + kP3BM, RING - kP3BM, bt1);
-
-    // ---- weights -> LDS stage as Ws[tap][n][k] (zero outside K x N), in
-    // batches of kWB vectors per thread whose loads are all in flight before
-    // any write ----
-    {
-        constexpr int kWB = 8;
-        const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(9 * K * N * ES));
-        constexpr int total = 9 * KPC * NPC / VEC;
-        constexpr int VPK = KPC / VEC;
-        for (int base = 0; base < total; base += kWB * kP3Threads) {
-            vec16 v[kWB];
-            #pragma unroll
-            for (int u = 0; u < kWB; u++) {
-                const int i = base + u * kP3Threads + tid;
-                int off;
-                if (!p.wtrans) {  // forward: W[tap][k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k
-                    const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
-                    const int n0 = (rem / KPC) * VEC, k = rem % KPC;
-                    off = i < total && k < K && n0 < N ? ((tap * K + k) * N + n0) * (int)ES : (int)kBufOff;
-                } else {          // data gradient: W[8 - tap][n][k] (n = c_in, k = c_out), rows of k
-                    const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
-                    const int n = rem / VPK, k0 = (rem % VPK) * VEC;
-                    off = i < total && n < N && k0 < K ? (((8 - tap) * N + n) * K + k0) * (int)ES : (int)kBufOff;
-                }
-                v[u] = bld16(wbuf, (uint32_t)off);
-            }
-            #pragma unroll
-            for (int u = 0; u < kWB; u++) {
-                const int i = base + u * kP3Threads + tid;
-                if (i >= total) break;
-                if (!p.wtrans) {  // scatter the n row to columns (a wave writes 64 consecutive k of a column)
-                    const int tap = i / (KPC * VPRO), rem = i % (KPC * VPRO);
-                    const int n0 = (rem / KPC) * VEC, k = rem % KPC;
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++)
-                        Ws[(tap * NPC + n0 + e) * g.ldw + k] =
-                            (T)((e & 1) ? (v[u].u[e >> 1] >> 16) : (v[u].u[e >> 1] & 0xffffu));
-                } else {          // rows copy straight
-                    const int tap = i / (NPC * VPK), rem = i % (NPC * VPK);
-                    const int n = rem / VPK, k0 = (rem % VPK) * VEC;
-                    *reinterpret_cast<vec16 *>(Ws + (tap * NPC + n) * g.ldw + k0) = v[u];
-                }
-            }
-        }
+    write_w(0);
+    for (int base = kWB * kP3Threads; base < wtotal; base += kWB * kP3Threads) {
+        load_w(base);
+        write_w(base);
     }
-    // ---- per-channel prologue / epilogue parameters ----
-    //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
-    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef)
-    for (int c = tid; c < KPC; c += kP3Threads) {
+    // ---- per-channel prologue / epilogue parameters -> LDS ----
+    if (tid < KPC) {
+        const int c = tid;
         float c0 = 0.f, c1 = 0.f, c2 = 0.f;
-        if (c < K && pro == PRO_BNRELU) {
-            bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], c0, c1);
-        } else if (c < K && pro == PRO_BNGRAD) {
-            deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
-                          p.p_alpha, p.p_betap, c0, c1, c2);
-        }
+        if (c < K && pro == PRO_BNRELU) bn_coef(q0, q1, q2, q3, c0, c1);
+        else if (c < K && pro == PRO_BNGRAD) deferred_coef_of(p.p_split, 1.0f / (float)m, q0, q1, q2, q3, q4, c0, c1, c2);
         coef[c] = c0; coef[KPC + c] = c1; coef[2 * KPC + c] = c2;
     }
-    for (int c = tid; c < NPC; c += kP3Threads) {
-        float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
+    if (tid < NPC) {
+        const int c = tid;
+        float e0 = ep0, e1 = ep1, e2 = 0.f, e3 = 0.f;
         if (c < N && EK == EK_BNBWD) {      // mean, rstd and the forward's y = x c0 + c1
-            e0 = p.e_mean[c]; e1 = p.e_rstd[c];
-            bn_coef(p.e_gamma[c], p.e_beta[c], e0, e1, e2, e3);
+            bn_coef(epg, epb, e0, e1, e2, e3);
             // e_zsrc: the operand is the stored z = relu(y): mask [z > 0] as
             // fma(z, 1, 0) > 0, xhat = (z - beta) / gamma, unless the channel's
             // vector holds a gamma = 0 channel (its threads read x: ex2)
@@ -300,7 +317,6 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             for (int i = c & ~(VEC - 1); i < (c & ~(VEC - 1)) + VEC; i++) zv = zv && p.e_gamma[i] != 0.f;
             if (zv) { e0 = p.e_beta[c]; e1 = 1.0f / p.e_gamma[c]; e2 = 1.f; e3 = 0.f; }
         }
-        if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[c];     // statistics of y - shift
         epi[c] = e0; epi[NPC + c] = e1; epi[2 * NPC + c] = e2; epi[3 * NPC + c] = e3;
     }
     __syncthreads();
