@@ -345,20 +345,33 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
     const int vz = tid % VZ, vg = tid % VG;
     const int cz = ci0 + vz * VEC, cg = co0 + vg * VEC;
     const bool zc_ok = cz < C_in, gc_ok = cg < C_out;
+    // (the deferred-gradient parameters first, then one branch around all 32
+    // operand parameters, so every load is in flight together: a branch per
+    // channel made eight round trips)
+    float gq0 = 0.f, gq1 = 0.f, gq2 = 0.f, gq3 = 0.f, gq4 = 0.f;
+    const bool gco_ld = GS == GB_BNGRAD && tid < COT && co0 + tid < C_out;
+    if (gco_ld) {
+        const int c = co0 + tid;
+        gq1 = p.g_mean[c]; gq2 = p.g_rstd[c];
+        if (p.g_split) { gq0 = p.g_alpha[c]; gq3 = p.g_betap[c]; }
+        else { gq0 = p.g_gamma[c]; gq3 = p.g_dgamma[c]; gq4 = p.g_dbeta[c]; }
+    }
     float za[VEC], zb[VEC];
     #pragma unroll
-    for (int e = 0; e < VEC; e++) {
-        za[e] = 1.f; zb[e] = 0.f;
-        if (p.a_mode == 1 && zc_ok) {
-            bn_coef(p.a_gamma[cz + e], p.a_beta[cz + e], p.a_mean[cz + e], p.a_rstd[cz + e], za[e], zb[e]);
+    for (int e = 0; e < VEC; e++) { za[e] = 1.f; zb[e] = 0.f; }
+    if (p.a_mode == 1 && zc_ok) {
+        float ga[VEC], be[VEC], mu[VEC], rs[VEC];
+        #pragma unroll
+        for (int e = 0; e < VEC; e++) {
+            ga[e] = p.a_gamma[cz + e]; be[e] = p.a_beta[cz + e]; mu[e] = p.a_mean[cz + e]; rs[e] = p.a_rstd[cz + e];
         }
+        #pragma unroll
+        for (int e = 0; e < VEC; e++) bn_coef(ga[e], be[e], mu[e], rs[e], za[e], zb[e]);
     }
     // deferred-gradient coefficients in LDS (registers are the occupancy limit of the 3x3 variants)
     if (GS == GB_BNGRAD && tid < COT) {
         float A = 0.f, Bc = 0.f, Cc = 0.f;
-        if (co0 + tid < C_out)
-            deferred_coef(p.g_split, co0 + tid, 1.0f / (float)m, p.g_gamma, p.g_mean, p.g_rstd, p.g_dgamma,
-                          p.g_dbeta, p.g_alpha, p.g_betap, A, Bc, Cc);
+        if (gco_ld) deferred_coef_of(p.g_split, 1.0f / (float)m, gq0, gq1, gq2, gq3, gq4, A, Bc, Cc);
         gco[tid] = A; gco[COT + tid] = Bc; gco[2 * COT + tid] = Cc;
     }
     __syncthreads();
