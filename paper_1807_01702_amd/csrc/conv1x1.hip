@@ -128,6 +128,24 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     const __amdgpu_buffer_rsrc_t x2buf = buf_view(p.ex2 ? reinterpret_cast<const T *>(p.ex2) + col0 : ycol,
                                                   p.ex2 ? (uint32_t)(((int64_t)(m - 1) * ex2_ldc + N) * 2) : 0u);
 
+    // ---- per-channel parameters, loaded first so their round trip overlaps
+    // the weights' (KP, NP <= 256 < kP1Threads: thread c holds channel c)
+    //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
+    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef_of)
+    float q0 = 0.f, q1 = 0.f, q2 = 0.f, q3 = 0.f, q4 = 0.f;
+    if (tid < K && pro == PRO_BNRELU) {
+        q0 = p.p_gamma[tid]; q1 = p.p_beta[tid]; q2 = p.p_mean[tid]; q3 = p.p_rstd[tid];
+    } else if (tid < K && pro == PRO_BNGRAD) {
+        q1 = p.p_mean[tid]; q2 = p.p_rstd[tid];
+        if (p.p_split) { q0 = p.p_alpha[tid]; q3 = p.p_betap[tid]; }
+        else { q0 = p.p_gamma[tid]; q3 = p.p_dgamma[tid]; q4 = p.p_dbeta[tid]; }
+    }
+    float ep0 = 0.f, ep1 = 1.f, ep2 = 0.f, ep3 = 0.f;
+    if (tid < N && BNBWD) {
+        ep0 = p.e_mean[col0 + tid]; ep1 = p.e_rstd[col0 + tid]; ep2 = p.e_gamma[col0 + tid]; ep3 = p.e_beta[col0 + tid];
+    }
+    if (tid < N && EK == EK_STATS && p.e_shift) ep0 = p.e_shift[col0 + tid];     // statistics of y - shift
+
     // ---- weights -> LDS as Ws[n][k] (zero outside K x N), in batches of
     // kWB vectors per thread whose loads are all in flight before any write ----
     {
@@ -165,26 +183,14 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             }
         }
     }
-    // ---- per-channel prologue / epilogue parameters ----
-    //   BNRELU: z = max(x * c0 + c1, 0) with c0 = gamma*rstd, c1 = beta - mean*gamma*rstd
-    //   BNGRAD: d = c0 * dy + c1 * x + c2  (the deferred BN input gradient: deferred_coef)
-    for (int c = tid; c < KP; c += kP1Threads) {
+    // ---- per-channel prologue / epilogue parameters -> LDS ----
+    if (tid < KP) {
         float c0 = 0.f, c1 = 0.f, c2 = 0.f;
-        if (c < K && pro == PRO_BNRELU) {
-            bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], c0, c1);
-        } else if (c < K && pro == PRO_BNGRAD) {
-            deferred_coef(p.p_split, c, 1.0f / (float)m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta,
-                          p.p_alpha, p.p_betap, c0, c1, c2);
-        }
-        coef[c] = c0; coef[KP + c] = c1; coef[2 * KP + c] = c2;
+        if (tid < K && pro == PRO_BNRELU) bn_coef(q0, q1, q2, q3, c0, c1);
+        else if (tid < K && pro == PRO_BNGRAD) deferred_coef_of(p.p_split, 1.0f / (float)m, q0, q1, q2, q3, q4, c0, c1, c2);
+        coef[tid] = c0; coef[KP + tid] = c1; coef[2 * KP + tid] = c2;
     }
-    for (int c = tid; c < NP; c += kP1Threads) {
-        float e0 = 0.f, e1 = 1.f, e2 = 0.f, e3 = 0.f;
-        const int cc = col0 + c;
-        if (c < N && BNBWD) { e0 = p.e_mean[cc]; e1 = p.e_rstd[cc]; e2 = p.e_gamma[cc]; e3 = p.e_beta[cc]; }
-        if (c < N && EK == EK_STATS && p.e_shift) e0 = p.e_shift[cc];     // statistics of y - shift
-        epi[c] = e0; epi[NP + c] = e1; epi[2 * NP + c] = e2; epi[3 * NP + c] = e3;
-    }
+    if (tid < NP) { epi[tid] = ep0; epi[NP + tid] = ep1; epi[2 * NP + tid] = ep2; epi[3 * NP + tid] = ep3; }
 
     // ---- tile operand registers ----
     const int VPR = KP / VEC;                          // A vectors per row

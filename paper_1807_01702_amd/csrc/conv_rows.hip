@@ -124,17 +124,50 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
         if constexpr (kF32) return coef[3 * K + c];
         else return 0.f;
     };
+    // (CU channels per thread per pass, their loads at clamped indices issued
+    // together before any use: one memory round trip per pass)
+    constexpr int CU = 4;
     if (p.pro == PRO_BNRELU || p.pro == PRO_BNRELU_POOL || p.pro == PRO_BNADDRELU) {
-        for (int c = tid; c < K; c += kThreads) {           // y = x c0 + c1
-            bn_coef(p.p_gamma[c], p.p_beta[c], p.p_mean[c], p.p_rstd[c], coef[K + c], coef[2 * K + c]);
-            if constexpr (kF32) coef[3 * K + c] = bn_centre<T>(p.p_ctr, c);
+        for (int cb = tid; cb < K; cb += CU * kThreads) {   // y = x c0 + c1
+            float g[CU], b[CU], mu[CU], rs[CU], kc[CU];
+            #pragma unroll
+            for (int u = 0; u < CU; u++) {
+                const int c = min(cb + u * kThreads, K - 1);
+                g[u] = p.p_gamma[c]; b[u] = p.p_beta[c]; mu[u] = p.p_mean[c]; rs[u] = p.p_rstd[c];
+                kc[u] = bn_centre<T>(p.p_ctr, c);
+            }
+            #pragma unroll
+            for (int u = 0; u < CU; u++) {
+                const int c = cb + u * kThreads;
+                if (c < K) {
+                    bn_coef(g[u], b[u], mu[u], rs[u], coef[K + c], coef[2 * K + c]);
+                    if constexpr (kF32) coef[3 * K + c] = kc[u];
+                }
+            }
         }
     } else if (p.pro == PRO_BNGRAD) {
         const float inv_m = 1.0f / (float)m;
-        for (int c = tid; c < K; c += kThreads) {
-            deferred_coef(p.p_split, c, inv_m, p.p_gamma, p.p_mean, p.p_rstd, p.p_dgamma, p.p_dbeta, p.p_alpha,
-                          p.p_betap, coef[c], coef[K + c], coef[2 * K + c]);
-            if constexpr (kF32) coef[3 * K + c] = bn_centre<T>(p.p_ctr, c);
+        const bool split = p.p_split != 0;
+        for (int cb = tid; cb < K; cb += CU * kThreads) {
+            float g[CU], mu[CU], rs[CU], dg[CU], db[CU], kc[CU];
+            #pragma unroll
+            for (int u = 0; u < CU; u++) {
+                const int c = min(cb + u * kThreads, K - 1);
+                mu[u] = p.p_mean[c]; rs[u] = p.p_rstd[c];
+                g[u] = split ? p.p_alpha[c] : p.p_gamma[c];
+                dg[u] = split ? p.p_betap[c] : p.p_dgamma[c];
+                db[u] = split ? 0.f : p.p_dbeta[c];
+                kc[u] = bn_centre<T>(p.p_ctr, c);
+            }
+            #pragma unroll
+            for (int u = 0; u < CU; u++) {
+                const int c = cb + u * kThreads;
+                if (c < K) {
+                    deferred_coef_of(p.p_split, inv_m, g[u], mu[u], rs[u], dg[u], db[u], coef[c], coef[K + c],
+                                     coef[2 * K + c]);
+                    if constexpr (kF32) coef[3 * K + c] = kc[u];
+                }
+            }
         }
     }
 
@@ -440,14 +473,19 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
     const bool zsrc = p.epi == EPI_BNBWD && p.e_zsrc;
     bool zs = zsrc && col_ok;                     // this thread's vector reads z (else x)
     if (p.epi == EPI_BNBWD && col_ok) {
-        for (int e = 0; e < VEC; e++) zs = zs && p.e_gamma[n + e] != 0.f;
+        // every parameter load first (a load inside a per-channel branch
+        // becomes one memory round trip per channel)
+        float ga[VEC], be[VEC];
         for (int e = 0; e < VEC; e++) {
-            emu[e] = p.e_mean[n + e]; ers[e] = p.e_rstd[n + e];
+            emu[e] = p.e_mean[n + e]; ers[e] = p.e_rstd[n + e]; ga[e] = p.e_gamma[n + e]; be[e] = p.e_beta[n + e];
             ek[e] = bn_centre<T>(p.e_ctr, n + e);
-            bn_coef(p.e_gamma[n + e], p.e_beta[n + e], emu[e], ers[e], eg[e], eb[e]);   // the forward's c0, c1
-            es[e] = eg[e];                                                             // summed-form scale
+        }
+        for (int e = 0; e < VEC; e++) zs = zs && ga[e] != 0.f;
+        for (int e = 0; e < VEC; e++) {
+            bn_coef(ga[e], be[e], emu[e], ers[e], eg[e], eb[e]);     // the forward's c0, c1
+            es[e] = eg[e];                                          // summed-form scale
             if (zs) {                             // mask fma(z, 1, 0) > 0, xhat = (z - beta) / gamma
-                emu[e] = p.e_beta[n + e]; ers[e] = 1.0f / p.e_gamma[n + e];
+                emu[e] = be[e]; ers[e] = 1.0f / ga[e];
                 eg[e] = 1.f; eb[e] = 0.f; ek[e] = 0.f;
             }
         }

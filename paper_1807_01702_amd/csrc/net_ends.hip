@@ -409,15 +409,21 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
     const int c0 = ((int)blockIdx.y * kStatsMaxVec + tx) * VEC;
     float sg[VEC], k[VEC], b[VEC], kc[VEC], s1[VEC], s2[VEC], sh[VEC];
     #pragma unroll
-    for (int i = 0; i < VEC; i++) {
-        s1[i] = s2[i] = 0.f;
-        sh[i] = STATS && p.shift && ty < ry ? p.shift[c0 + i] : 0.f;     // statistics of y - shift
-        sg[i] = 1.f; k[i] = 1.f; b[i] = 0.f; kc[i] = 0.f;
-        if (BN && ty < ry) {
-            const float g = p.gamma[c0 + i];
-            sg[i] = g > 0.f ? 1.f : (g < 0.f ? -1.f : 0.f);
-            bn_coef(g, p.beta[c0 + i], p.mean[c0 + i], p.rstd[c0 + i], k[i], b[i]);
+    for (int i = 0; i < VEC; i++) { s1[i] = s2[i] = 0.f; sh[i] = 0.f; sg[i] = 1.f; k[i] = 1.f; b[i] = 0.f; kc[i] = 0.f; }
+    if (STATS && p.shift && ty < ry)                                      // statistics of y - shift
+        #pragma unroll
+        for (int i = 0; i < VEC; i++) sh[i] = p.shift[c0 + i];
+    if (BN && ty < ry) {            // (all loads in one branch: one memory round trip)
+        float g[VEC], be[VEC], mu[VEC], rs[VEC];
+        #pragma unroll
+        for (int i = 0; i < VEC; i++) {
+            g[i] = p.gamma[c0 + i]; be[i] = p.beta[c0 + i]; mu[i] = p.mean[c0 + i]; rs[i] = p.rstd[c0 + i];
             kc[i] = bn_centre<T>(p.ctr, c0 + i);
+        }
+        #pragma unroll
+        for (int i = 0; i < VEC; i++) {
+            sg[i] = g[i] > 0.f ? 1.f : (g[i] < 0.f ? -1.f : 0.f);
+            bn_coef(g[i], be[i], mu[i], rs[i], k[i], b[i]);
         }
     }
     const T *x = reinterpret_cast<const T *>(p.x);
@@ -793,14 +799,21 @@ __global__ __launch_bounds__(kThreads) void k_head_bn_bwd(HeadParams p, int64_t 
         s1[i] = s2[i] = 0.f;
         k[i] = b[i] = mu[i] = gk[i] = da[i] = db[i] = kc[i] = 0.f;
         rs[i] = 1.f;
-        if (ty < ry) {
+    }
+    if (ty < ry) {                  // (all loads in one branch: one memory round trip)
+        float g[VEC], be[VEC];
+        #pragma unroll
+        for (int i = 0; i < VEC; i++) {
             const int c = c0 + i;
-            mu[i] = p.mean[c];
-            rs[i] = p.rstd[c];
+            mu[i] = p.mean[c]; rs[i] = p.rstd[c]; g[i] = p.gamma[c]; be[i] = p.beta[c];
             kc[i] = bn_centre<T>(p.ctr, c);
-            bn_coef(p.gamma[c], p.beta[c], mu[i], rs[i], k[i], b[i]);
+            if (MODE == HB_DX) { da[i] = p.dbeta[c]; db[i] = p.dgamma[c]; }
+        }
+        #pragma unroll
+        for (int i = 0; i < VEC; i++) {
+            bn_coef(g[i], be[i], mu[i], rs[i], k[i], b[i]);
             gk[i] = k[i];
-            if (MODE == HB_DX) { da[i] = p.dbeta[c] * inv_m; db[i] = p.dgamma[c] * inv_m; }
+            if (MODE == HB_DX) { da[i] *= inv_m; db[i] *= inv_m; }
         }
     }
     const T *x = reinterpret_cast<const T *>(p.x);
