@@ -149,9 +149,12 @@ __device__ __forceinline__ void stats_write(int mode, int c, double a, double b,
         dbeta[c] = (float)a;
         dgamma[c] = (float)b;
         if (st.alpha) {
-            const double k = (double)st.gamma[c] * (double)st.rstd[c];
+            float al0 = 0.f, bp0 = 0.f;           // (every load before any use: one round trip)
+            const float g = st.gamma[c], r = st.rstd[c];
+            if (st.accumulate) { al0 = st.alpha[c]; bp0 = st.betap[c]; }
+            const double k = (double)g * (double)r;
             float al = (float)(-k * a / dm), bp = (float)(-k * b / dm);
-            if (st.accumulate) { al += st.alpha[c]; bp += st.betap[c]; }
+            if (st.accumulate) { al += al0; bp += bp0; }
             st.alpha[c] = al;
             st.betap[c] = bp;
         }
@@ -171,14 +174,23 @@ __device__ __forceinline__ void combine_one_block(int bid, const float *__restri
     const int c = bid * 8 + cl;
     double a = 0.0, b = 0.0;
     if (c < C) {
+        // rows past the last are read at the last row and selected away: no
+        // branch around a load, so the 16 loads of a pass are in flight
+        // together (a branch per load made one round trip each)
         const float *p = part + c;
         for (int64_t r = g; r < R; r += 8 * 32) {
             float va[8], vb[8];
             #pragma unroll
             for (int u = 0; u < 8; u++) {
-                const int64_t rr = r + 32 * u;
-                va[u] = rr < R ? p[rr * 2 * C] : 0.f;
-                vb[u] = rr < R ? p[rr * 2 * C + C] : 0.f;
+                const int64_t rr = r + 32 * u, rc = rr < R ? rr : R - 1;
+                va[u] = p[rc * 2 * C];
+                vb[u] = p[rc * 2 * C + C];
+            }
+            #pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const bool ok = r + 32 * u < R;
+                va[u] = ok ? va[u] : 0.f;
+                vb[u] = ok ? vb[u] : 0.f;
             }
             #pragma unroll
             for (int u = 0; u < 8; u++) { a += (double)va[u]; b += (double)vb[u]; }
@@ -230,16 +242,22 @@ __global__ __launch_bounds__(kThreads) void k_bwd_tail(const float *__restrict__
     const int64_t st4 = len / 4;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     if (i4 < st4) {
+        // splits past the last are read at the last split and selected away:
+        // no branch around a load, so the eight loads of a pass are in flight
+        // together
         const float4 *p = reinterpret_cast<const float4 *>(wpart) + i4;
         for (int64_t r = q; r < S; r += 8 * QN) {
             float4 v[8];
             #pragma unroll
             for (int u = 0; u < 8; u++) {
                 const int64_t rr = r + (int64_t)u * QN;
-                v[u] = rr < S ? p[rr * st4] : make_float4(0.f, 0.f, 0.f, 0.f);
+                v[u] = p[(rr < S ? rr : S - 1) * st4];
             }
             #pragma unroll
-            for (int u = 0; u < 8; u++) { acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w; }
+            for (int u = 0; u < 8; u++) {
+                if (r + (int64_t)u * QN >= S) v[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+                acc.x += v[u].x; acc.y += v[u].y; acc.z += v[u].z; acc.w += v[u].w;
+            }
         }
     }
     red[q][f] = acc;
@@ -267,13 +285,22 @@ __global__ __launch_bounds__(kThreads) void k_stats_combine1(const float *__rest
     const int64_t r0 = rs * R / RS, r1 = (rs + 1) * R / RS;
     double a = 0.0, b = 0.0;
     if (c < C) {
+        // rows past the range are read at its last row and selected away (no
+        // branch around a load)
         const float *p = part + c;
         for (int64_t r = r0 + wv; r < r1; r += 32) {
             float va[8], vb[8];
+            #pragma unroll
             for (int u = 0; u < 8; u++) {
-                const int64_t rr = r + 4 * u;
-                va[u] = rr < r1 ? p[rr * 2 * C] : 0.f;
-                vb[u] = rr < r1 ? p[rr * 2 * C + C] : 0.f;
+                const int64_t rr = r + 4 * u, rc = rr < r1 ? rr : r1 - 1;
+                va[u] = p[rc * 2 * C];
+                vb[u] = p[rc * 2 * C + C];
+            }
+            #pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const bool ok = r + 4 * u < r1;
+                va[u] = ok ? va[u] : 0.f;
+                vb[u] = ok ? vb[u] : 0.f;
             }
             for (int u = 0; u < 8; u++) { a += (double)va[u]; b += (double)vb[u]; }
         }
