@@ -104,10 +104,13 @@ __global__ __launch_bounds__(kThreads, 2) void k_stem_conv(StemParams p)
                 uint32_t h2[2];
                 #pragma unroll
                 for (int u = 0; u < 2; u++) {
+                    // (an unconditional load at a clamped index, then a select:
+                    // a load under a branch costs one memory round trip each)
                     const int e = 2 * e2 + u, kw = 2 * g16 + e / 4, ci = e % 4;
-                    h2[u] = kw < kSK && ci < p.c_in
-                                ? (uint32_t)wt[((kh * kSK + kw) * p.c_in + ci) * kStemCout + nb * 16 + l16]
-                                : 0u;
+                    const bool ok = kw < kSK && ci < p.c_in;
+                    const uint32_t v =
+                        wt[ok ? ((kh * kSK + kw) * p.c_in + ci) * kStemCout + nb * 16 + l16 : nb * 16 + l16];
+                    h2[u] = ok ? v : 0u;
                 }
                 wd[e2] = h2[0] | (h2[1] << 16);
             }
@@ -439,21 +442,27 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_fwd(MaxPoolParams p, int64
             float best[VEC], bv[VEC];
             #pragma unroll
             for (int i = 0; i < VEC; i++) { best[i] = -INFINITY; bv[i] = 0.f; }
+            // the nine taps' loads first, at clamped positions (a load under a
+            // bounds branch costs one memory round trip each), then the
+            // first-maximum scan in tap order over the taps inside the image
+            vec16 tv[9];
+            bool tin[9];
             #pragma unroll
-            for (int kh = 0; kh < 3; kh++) {
-                const int ih = 2 * oh - 1 + kh;
-                if (ih < 0 || ih >= p.h) continue;
+            for (int t9 = 0; t9 < 9; t9++) {
+                const int ih = 2 * oh - 1 + t9 / 3, iw = 2 * ow - 1 + t9 % 3;
+                tin[t9] = ih >= 0 && ih < p.h && iw >= 0 && iw < p.w;
+                const int ihc = ih < 0 ? 0 : (ih >= p.h ? p.h - 1 : ih), iwc = iw < 0 ? 0 : (iw >= p.w ? p.w - 1 : iw);
+                tv[t9] = ldg16(x + ((n * p.h + ihc) * p.w + iwc) * p.x_ldc + c0);
+            }
+            #pragma unroll
+            for (int t9 = 0; t9 < 9; t9++) {
+                if (!tin[t9]) continue;
+                float f[VEC];
+                Elem<T>::unpack(tv[t9], f);
                 #pragma unroll
-                for (int kw = 0; kw < 3; kw++) {
-                    const int iw = 2 * ow - 1 + kw;
-                    if (iw < 0 || iw >= p.w) continue;
-                    float f[VEC];
-                    Elem<T>::unpack(ldg16(x + ((n * p.h + ih) * p.w + iw) * p.x_ldc + c0), f);
-                    #pragma unroll
-                    for (int i = 0; i < VEC; i++) {
-                        const float key = BN ? sg[i] * f[i] : f[i];
-                        if (key > best[i]) { best[i] = key; bv[i] = f[i]; }
-                    }
+                for (int i = 0; i < VEC; i++) {
+                    const float key = BN ? sg[i] * f[i] : f[i];
+                    if (key > best[i]) { best[i] = key; bv[i] = f[i]; }
                 }
             }
             float o[VEC];
@@ -551,21 +560,26 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_bwd(MaxPoolParams p)
             uint32_t code[VEC];
             #pragma unroll
             for (int i = 0; i < VEC; i++) { best[i] = -INFINITY; code[i] = 0; }
+            // the nine taps' loads first at clamped positions, then the scan
+            // in tap order (as in the forward pass)
+            vec16 tv[9];
+            bool tin[9];
             #pragma unroll
-            for (int kh = 0; kh < 3; kh++) {
-                const int ih = 2 * oh - 1 + kh;
-                if (ih < 0 || ih >= h) continue;
+            for (int t9 = 0; t9 < 9; t9++) {
+                const int ih = 2 * oh - 1 + t9 / 3, iw = 2 * ow - 1 + t9 % 3;
+                tin[t9] = ih >= 0 && ih < h && iw >= 0 && iw < w;
+                const int ihc = ih < 0 ? 0 : (ih >= h ? h - 1 : ih), iwc = iw < 0 ? 0 : (iw >= w ? w - 1 : iw);
+                tv[t9] = ldg16(x + ((n * h + ihc) * w + iwc) * p.x_ldc + v * VEC);
+            }
+            #pragma unroll
+            for (int t9 = 0; t9 < 9; t9++) {
+                if (!tin[t9]) continue;
+                float f[VEC];
+                Elem<T>::unpack(tv[t9], f);
                 #pragma unroll
-                for (int kw = 0; kw < 3; kw++) {
-                    const int iw = 2 * ow - 1 + kw;
-                    if (iw < 0 || iw >= w) continue;
-                    float f[VEC];
-                    Elem<T>::unpack(ldg16(x + ((n * h + ih) * w + iw) * p.x_ldc + v * VEC), f);
-                    #pragma unroll
-                    for (int i = 0; i < VEC; i++) {
-                        const float kk = BN ? sgn_s[v * VEC + i] * f[i] : f[i];
-                        if (kk > best[i]) { best[i] = kk; code[i] = (uint32_t)(kh * 3 + kw); }
-                    }
+                for (int i = 0; i < VEC; i++) {
+                    const float kk = BN ? sgn_s[v * VEC + i] * f[i] : f[i];
+                    if (kk > best[i]) { best[i] = kk; code[i] = (uint32_t)t9; }
                 }
             }
             uint8_t *cp = &codes[orow][ow * C + v * VEC];
@@ -583,21 +597,36 @@ __global__ __launch_bounds__(kThreads) void k_maxpool_bwd(MaxPoolParams p)
             for (int i = 0; i < VEC; i++) dz[i] = 0.f;
             const int oh_lo = j, oh_hi = ir ? j + 1 : j;
             const int ow_lo = col >> 1, ow_hi = (col & 1) ? (col + 1) >> 1 : col >> 1;
-            for (int oh = oh_lo; oh <= oh_hi && oh < ho; oh++)
-                for (int ow = ow_lo; ow <= ow_hi && ow < wo; ow++) {
-                    const uint32_t tap = (uint32_t)((row - (2 * oh - 1)) * 3 + (col - (2 * ow - 1)));
-                    float g[VEC];
-                    Elem<T>::unpack(ldg16(gy + ((n * ho + oh) * wo + ow) * p.g_ldc + cv * VEC), g);
-                    const uint8_t *cp = &codes[oh - j][ow * C + cv * VEC];
-                    #pragma unroll
-                    for (int i = 0; i < VEC; i++)
-                        if (cp[i] == tap) dz[i] += g[i];
-                }
+            // the (at most 2 x 2) covering windows' gradients and the BN input
+            // loaded first at clamped positions, then summed in row-major
+            // window order
             const int64_t q = (n * h + row) * w + col;
+            vec16 gv[4], xv = zero16();
+            bool win[4];
+            #pragma unroll
+            for (int w4 = 0; w4 < 4; w4++) {
+                const int oh = oh_lo + (w4 >> 1), ow = ow_lo + (w4 & 1);
+                win[w4] = oh <= oh_hi && oh < ho && ow <= ow_hi && ow < wo;
+                const int ohc = oh < ho ? oh : ho - 1, owc = ow < wo ? ow : wo - 1;
+                gv[w4] = ldg16(gy + ((n * ho + ohc) * wo + owc) * p.g_ldc + cv * VEC);
+            }
+            if (BN) xv = ldg16(x + q * p.x_ldc + cv * VEC);
+            #pragma unroll
+            for (int w4 = 0; w4 < 4; w4++) {
+                if (!win[w4]) continue;
+                const int oh = oh_lo + (w4 >> 1), ow = ow_lo + (w4 & 1);
+                const uint32_t tap = (uint32_t)((row - (2 * oh - 1)) * 3 + (col - (2 * ow - 1)));
+                float g[VEC];
+                Elem<T>::unpack(gv[w4], g);
+                const uint8_t *cp = &codes[oh - j][ow * C + cv * VEC];
+                #pragma unroll
+                for (int i = 0; i < VEC; i++)
+                    if (cp[i] == tap) dz[i] += g[i];
+            }
             float o[VEC];
             if (BN) {
                 float f[VEC];
-                Elem<T>::unpack(ldg16(x + q * p.x_ldc + cv * VEC), f);
+                Elem<T>::unpack(xv, f);
                 #pragma unroll
                 for (int i = 0; i < VEC; i++) o[i] = bn_lin(f[i] - kc[i], k[i], b[i]) > 0.f ? dz[i] : 0.f;
                 const vec16 ov = Elem<T>::pack(o);
@@ -684,25 +713,46 @@ __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const
     const int tid = threadIdx.x, tr = tid / 16, tc = tid % 16;
     const int i0 = blockIdx.y * BM, j0 = blockIdx.x * BN;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    constexpr int NA = BK * BM / kThreads, NB = BK * BN / kThreads;
     for (int k0 = 0; k0 < K; k0 += BK) {
+        // every load of the chunk at a clamped index first, then the LDS
+        // writes with the out-of-range elements selected to zero (a load
+        // under a bounds branch costs one memory round trip each)
+        float av[NA];
+        TB bv[NB];                                   // raw: converted after every load is issued
+        bool aok[NA], bok[NB];
         #pragma unroll
-        for (int u = 0; u < BK * BM / kThreads; u++) {
+        for (int u = 0; u < NA; u++) {
             const int e = tid + u * kThreads;
             const int kk = sak == 1 ? e % BK : e / BM, ii = sak == 1 ? e / BK : e % BM;
             const int gi = i0 + ii, gk = k0 + kk;
-            As[kk][ii] = gi < M && gk < K ? a[gi * sai + gk * sak] : 0.f;
+            aok[u] = gi < M && gk < K;
+            av[u] = a[(aok[u] ? gi : 0) * sai + (aok[u] ? gk : 0) * sak];
         }
         #pragma unroll
-        for (int u = 0; u < BK * BN / kThreads; u++) {
+        for (int u = 0; u < NB; u++) {
             const int e = tid + u * kThreads;
             const int kk = sbk == 1 ? e % BK : e / BN, jj = sbk == 1 ? e / BK : e % BN;
             const int gj = j0 + jj, gk = k0 + kk;
-            float bv = 0.f;
-            if (gj < N && gk < K) {
-                if constexpr (sizeof(TB) == 2) bv = bf2f(b[gk * sbk + gj * sbj]);
-                else bv = b[gk * sbk + gj * sbj];
-            }
-            Bs[kk][jj] = bv;
+            bok[u] = gj < N && gk < K;
+            const int64_t off = (int64_t)(bok[u] ? gk : 0) * sbk + (int64_t)(bok[u] ? gj : 0) * sbj;
+            bv[u] = b[off];
+        }
+        __builtin_amdgcn_sched_barrier(0);   // keep every load above the writes (the scheduler sinks them)
+        #pragma unroll
+        for (int u = 0; u < NA; u++) {
+            const int e = tid + u * kThreads;
+            const int kk = sak == 1 ? e % BK : e / BM, ii = sak == 1 ? e / BK : e % BM;
+            As[kk][ii] = aok[u] ? av[u] : 0.f;
+        }
+        #pragma unroll
+        for (int u = 0; u < NB; u++) {
+            const int e = tid + u * kThreads;
+            const int kk = sbk == 1 ? e % BK : e / BN, jj = sbk == 1 ? e / BK : e % BN;
+            float f;
+            if constexpr (sizeof(TB) == 2) f = bf2f(bv[u]);
+            else f = bv[u];
+            Bs[kk][jj] = bok[u] ? f : 0.f;
         }
         __syncthreads();
         #pragma unroll 16
