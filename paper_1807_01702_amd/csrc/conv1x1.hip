@@ -125,8 +125,6 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? reinterpret_cast<const T *>(p.ex) + col0 : ycol,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * 2) : 0u);
     const int ex2_ldc = (int)p.ex2_ldc;
-    const __amdgpu_buffer_rsrc_t x2buf = buf_view(p.ex2 ? reinterpret_cast<const T *>(p.ex2) + col0 : ycol,
-                                                  p.ex2 ? (uint32_t)(((int64_t)(m - 1) * ex2_ldc + N) * 2) : 0u);
 
     // ---- per-channel parameters, loaded first so their round trip overlaps
     // the weights' (KP, NP <= 256 < kP1Threads: thread c holds channel c)
@@ -383,6 +381,11 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     if (zs)
         #pragma unroll
         for (int e = 0; e < VEC; e++) { eM[e] = eB[e]; eR[e] = 1.0f / eG[e]; eC0[e] = 1.f; eC1[e] = 0.f; }
+    // (the z / x source of this thread's channel vector as a plain pointer:
+    // the choice is per lane, so one load replaces two raw-buffer loads merged
+    // after both arrive)
+    const T *zsrc_col = reinterpret_cast<const T *>(zs ? p.ex : (p.ex2 ? p.ex2 : p.ex)) + col0 + (col_ok ? n : 0);
+    const int zsrc_ldc = zs ? ex_ldc : ex2_ldc;
     auto load_epi = [&](int p0, int lim) __attribute__((always_inline)) {
         if (!READS) return;
         #pragma unroll
@@ -391,11 +394,9 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             const bool ok = col_ok && r < BM && pp < lim;
             if (EK == EK_STORE_ACC) {
                 rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * 2u : kBufOff);
-            } else if (BNBWD && zsrc) {   // z, or x for a vector holding a gamma = 0 channel (one load is empty)
-                const vec16 a = bld16(xbuf, ok && zs ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
-                const vec16 b = bld16(x2buf, ok && !zs ? (uint32_t)(pp * ex2_ldc + n) * 2u : kBufOff);
-                #pragma unroll
-                for (int i = 0; i < 4; i++) rx[j].u[i] = a.u[i] | b.u[i];
+            } else if (BNBWD && zsrc) {   // z, or x for a vector holding a gamma = 0 channel: one load
+                // from this thread's source at a clamped row (a row past the tile is not used)
+                rx[j] = ldg16(zsrc_col + (int64_t)(ok ? pp : 0) * zsrc_ldc);
             } else {
                 rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * 2u : kBufOff);
             }

@@ -314,7 +314,13 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             // fma(z, 1, 0) > 0, xhat = (z - beta) / gamma, unless the channel's
             // vector holds a gamma = 0 channel (its threads read x: ex2)
             bool zv = p.e_zsrc != 0;
-            for (int i = c & ~(VEC - 1); i < (c & ~(VEC - 1)) + VEC; i++) zv = zv && p.e_gamma[i] != 0.f;
+            if (zv) {                              // (the eight loads together, then the test)
+                float ga[VEC];
+                #pragma unroll
+                for (int i = 0; i < VEC; i++) ga[i] = p.e_gamma[(c & ~(VEC - 1)) + i];
+                #pragma unroll
+                for (int i = 0; i < VEC; i++) zv = zv && ga[i] != 0.f;
+            }
             if (zv) { e0 = p.e_beta[c]; e1 = 1.0f / p.e_gamma[c]; e2 = 1.f; e3 = 0.f; }
         }
         epi[c] = e0; epi[NPC + c] = e1; epi[2 * NPC + c] = e2; epi[3 * NPC + c] = e3;
@@ -335,8 +341,13 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const bool col_ok = n < N;
     const bool zsrc = EK == EK_BNBWD && p.e_zsrc;
     bool zs = zsrc && col_ok;                      // this thread's vector reads z (else x)
-    #pragma unroll
-    for (int e = 0; e < VEC; e++) zs = zs && p.e_gamma[col_ok ? n + e : 0] != 0.f;
+    if (zsrc) {                                    // (the eight loads together, then the test)
+        float ga[VEC];
+        #pragma unroll
+        for (int e = 0; e < VEC; e++) ga[e] = p.e_gamma[col_ok ? n + e : 0];
+        #pragma unroll
+        for (int e = 0; e < VEC; e++) zs = zs && ga[e] != 0.f;
+    }
 
     // ---- prologue transform of a batch, then the ring writes.  The mode
     // switch is wave-uniform and outside the vector loop; invalid rows are
