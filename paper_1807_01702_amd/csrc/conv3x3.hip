@@ -142,13 +142,17 @@ __device__ __forceinline__ int p3_pixel(int P, const P3Geom &g, int H, int W)
 // PRO_RELU chosen at run time).
 // PC3_BNRELU_SAVE: BN+ReLU whose result z is also stored (the materialised
 // O2' sweep; each workgroup stores the positions of its own range once).
-// The BN-backward epilogue reads z instead of x when p.e_zsrc is set.
 enum { PC3_RUNTIME = 0, PC3_BNGRAD = 1, PC3_BNRELU = 2, PC3_BNRELU_SAVE = 3 };
+// The BN-backward epilogue reading the stored z (p.e_zsrc) is an epilogue kind
+// of its own, so the plain BN-backward epilogue carries none of its code.
+constexpr int EK3_BNBWD_Z = 7;
 
 template <int WK, int WN, int EK, int PC>
 __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
 {
     constexpr bool BNG = PC == PC3_BNGRAD;
+    constexpr bool ZK = EK == EK3_BNBWD_Z;                        // BN backward from the stored z
+    constexpr bool BNB = EK == EK_BNBWD || ZK;                    // BN-backward epilogue
     constexpr bool SAVE = PC == PC3_BNRELU_SAVE;
     const int pro = PC == PC3_BNRELU || SAVE ? PRO_BNRELU : (PC == PC3_BNGRAD ? PRO_BNGRAD : p.pro);
     using T = bf16_t;
@@ -159,7 +163,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     constexpr int RB = kP3BM / (16 * WR);                        // 16-row blocks per wave
     constexpr int VPRO = NPC / VEC, RSTEP = kP3Threads / VPRO;
     constexpr int RPT = kP3BM / RSTEP;                           // epilogue rows per thread
-    constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD;
+    constexpr bool READS = EK == EK_STORE_ACC || EK == EK_RELUMASK || BNB;
     constexpr int NVA = (kP3BM * (KPC / VEC) + kP3Threads - 1) / kP3Threads;
     constexpr int NVB = BNG ? NVA : 1, NVX = READS ? RPT : 1;
     // batches in flight: one (a second register buffer is merged back into
@@ -195,8 +199,6 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const int side_ldc = (int)p.side_ldc, ex2_ldc = (int)p.ex2_ldc;
     const __amdgpu_buffer_rsrc_t sbuf = buf_view(SAVE ? p.side : p.a,
                                                  SAVE ? (uint32_t)(((int64_t)(m - 1) * side_ldc + K) * ES) : 0u);
-    const __amdgpu_buffer_rsrc_t x2buf = buf_view(p.ex2 ? p.ex2 : p.y,
-                                                  p.ex2 ? (uint32_t)(((int64_t)(m - 1) * ex2_ldc + N) * ES) : 0u);
     const __amdgpu_buffer_rsrc_t xbuf = buf_view(p.ex ? p.ex : p.y,
                                                  p.ex ? (uint32_t)(((int64_t)(m - 1) * ex_ldc + N) * ES) : 0u);
 
@@ -241,7 +243,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         else { q0 = p.p_gamma[tid]; q3 = p.p_dgamma[tid]; q4 = p.p_dbeta[tid]; }
     }
     float ep0 = 0.f, ep1 = 1.f, epg = 0.f, epb = 0.f;
-    if (tid < N && EK == EK_BNBWD) { ep0 = p.e_mean[tid]; ep1 = p.e_rstd[tid]; epg = p.e_gamma[tid]; epb = p.e_beta[tid]; }
+    if (tid < N && BNB) { ep0 = p.e_mean[tid]; ep1 = p.e_rstd[tid]; epg = p.e_gamma[tid]; epb = p.e_beta[tid]; }
     if (tid < N && EK == EK_STATS && p.e_shift) ep0 = p.e_shift[tid];     // statistics of y - shift
 
     // weights -> LDS stage as Ws[tap][n][k] (zero outside K x N), in batches
@@ -308,12 +310,12 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     if (tid < NPC) {
         const int c = tid;
         float e0 = ep0, e1 = ep1, e2 = 0.f, e3 = 0.f;
-        if (c < N && EK == EK_BNBWD) {      // mean, rstd and the forward's y = x c0 + c1
+        if (c < N && BNB) {      // mean, rstd and the forward's y = x c0 + c1
             bn_coef(epg, epb, e0, e1, e2, e3);
             // e_zsrc: the operand is the stored z = relu(y): mask [z > 0] as
             // fma(z, 1, 0) > 0, xhat = (z - beta) / gamma, unless the channel's
             // vector holds a gamma = 0 channel (its threads read x: ex2)
-            bool zv = p.e_zsrc != 0;
+            bool zv = ZK;
             if (zv) {                              // (the eight loads together, then the test)
                 float ga[VEC];
                 #pragma unroll
@@ -339,7 +341,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     const int v = tid % VPRO, r0 = tid / VPRO;
     const int n = v * VEC;
     const bool col_ok = n < N;
-    const bool zsrc = EK == EK_BNBWD && p.e_zsrc;
+    constexpr bool zsrc = ZK;
     bool zs = zsrc && col_ok;                      // this thread's vector reads z (else x)
     if (zsrc) {                                    // (the eight loads together, then the test)
         float ga[VEC];
@@ -348,6 +350,8 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         #pragma unroll
         for (int e = 0; e < VEC; e++) zs = zs && ga[e] != 0.f;
     }
+    const T *zsrc_col = reinterpret_cast<const T *>(zs ? p.ex : (p.ex2 ? p.ex2 : p.ex)) + (col_ok ? n : 0);
+    const int zsrc_ldc = zs ? ex_ldc : ex2_ldc;
 
     // ---- prologue transform of a batch, then the ring writes.  The mode
     // switch is wave-uniform and outside the vector loop; invalid rows are
@@ -440,11 +444,9 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             const bool ok = pp >= 0;
             if (EK == EK_STORE_ACC) {
                 rx[j] = bld16(ybuf, ok ? (uint32_t)(pp * y_ldc + n) * ES : kBufOff);
-            } else if (EK == EK_BNBWD && zsrc) {   // z, or x (gamma = 0 in the vector): one load is empty
-                const vec16 a = bld16(xbuf, ok && zs ? (uint32_t)(pp * ex_ldc + n) * ES : kBufOff);
-                const vec16 b = bld16(x2buf, ok && !zs ? (uint32_t)(pp * ex2_ldc + n) * ES : kBufOff);
-                #pragma unroll
-                for (int i = 0; i < 4; i++) rx[j].u[i] = a.u[i] | b.u[i];
+            } else if (ZK) {   // z, or x (gamma = 0 in the vector): one load from this thread's
+                // source at a clamped pixel (a padding or past-the-end row is not used)
+                rx[j] = ldg16(zsrc_col + (int64_t)(ok ? pp : 0) * zsrc_ldc);
             } else {
                 rx[j] = bld16(xbuf, ok ? (uint32_t)(pp * ex_ldc + n) * ES : kBufOff);
             }
@@ -529,7 +531,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
             vec16 vo[RPT];
             float eM[VEC], eR[VEC], eC0[VEC], eC1[VEC];
             if (EK == EK_STATS) lds_f8(epi + n, eM);                  // shift
-            if (EK == EK_BNBWD) {
+            if (BNB) {
                 lds_f8(epi + n, eM);
                 lds_f8(epi + NPC + n, eR);
                 lds_f8(epi + 2 * NPC + n, eC0);
@@ -571,7 +573,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
                     #pragma unroll
                     for (int e = 0; e < VEC; e++) f[e] = yv[e] > 0.f ? f[e] : 0.f;
                     vo[j] = Elem<T>::pack(f);
-                } else if (EK == EK_BNBWD) {
+                } else if (BNB) {
                     float x[VEC];
                     Elem<T>::unpack(rx[j < NVX ? j : 0], x);
                     #pragma unroll
@@ -604,7 +606,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     }
 
     // ---- per-workgroup statistics partial row ----
-    if (EK == EK_STATS || EK == EK_BNBWD) {
+    if (EK == EK_STATS || BNB) {
         #pragma unroll
         for (int e = 0; e < VEC; e++) {
             red[r0 * NPC + n + e] = s1[e];
@@ -664,7 +666,7 @@ static hipError_t run_p3(const RowsParams &p, const P3Geom &g0, hipStream_t s)
     double a = m * p.K;
     if (BNG || PC == PC3_BNRELU_SAVE) a *= 2.0;     // second operand read / z written
     double out = m * p.N;
-    if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD) out += m * p.N;
+    if (EK == EK_STORE_ACC || EK == EK_RELUMASK || EK == EK_BNBWD || EK == EK3_BNBWD_Z) out += m * p.N;
     TraceScope tr(KC_CONV, KID_CONV_3X3, s, e * (a + out + 9.0 * p.K * p.N), 2.0 * m * 9.0 * p.K * p.N);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kP3Threads), g.lds, s, p, g);
     return hipGetLastError();
@@ -694,7 +696,7 @@ static hipError_t run_p3_ek(const RowsParams &p, const P3Geom &g, int ek, hipStr
     case EK_STORE_ACC: return run_p3_shape<EK_STORE_ACC, PC>(p, g, s);
     case EK_STATS: return run_p3_shape<EK_STATS, PC>(p, g, s);
     case EK_RELUMASK: return run_p3_shape<EK_RELUMASK, PC>(p, g, s);
-    default: return run_p3_shape<EK_BNBWD, PC>(p, g, s);
+    default: return p.e_zsrc ? run_p3_shape<EK3_BNBWD_Z, PC>(p, g, s) : run_p3_shape<EK_BNBWD, PC>(p, g, s);
     }
 }
 
