@@ -154,6 +154,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             vec16 v[kWB];
             #pragma unroll
             for (int u = 0; u < kWB; u++) {
+                if (base + u * kP1Threads >= total) break;   // (uniform: no empty loads issued)
                 const int i = base + u * kP1Threads + tid;
                 int off;
                 if (!p.wtrans) {  // forward: W[k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k

@@ -256,6 +256,7 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
     auto load_w = [&](int base) __attribute__((always_inline)) {
         #pragma unroll
         for (int u = 0; u < kWB; u++) {
+            if (base + u * kP3Threads >= wtotal) break;      // (uniform: no empty loads issued)
             const int i = base + u * kP3Threads + tid;
             int off;
             if (!p.wtrans) {  // forward: W[tap][k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k
