@@ -640,9 +640,13 @@ bool conv3x3_supported(int dtype, int K, int N, int H, int W)
     return g.lds <= 160 * 1024;
 }
 
+// One workgroup per 32 pixels, at most one per CU: a small image (14 x 14,
+// 7 x 7) would otherwise leave most CUs idle, and each workgroup's launch
+// prologue (weights, parameters, ring fill) is a fixed cost that more
+// workgroups share out; a range shorter than a tile is a masked tile.
 int64_t conv3x3_partial_rows(int64_t m)
 {
-    const int64_t tiles = ceil_div(m, kP3BM);
+    const int64_t tiles = ceil_div(m, 32);
     const int64_t g = p3_cus();
     return tiles < g ? tiles : g;
 }

@@ -59,6 +59,7 @@ constexpr int kWgKC = 64;                  // K positions per chunk
 constexpr int kWgCIT = 64;                 // input channels per tile
 constexpr int kWgMaxW3 = 62;               // widest 3x3 image row (PW <= 64)
 constexpr int kWgTrKQ1 = 64;               // pixels per chunk of the bf16 1x1 weight gradient (128: slower)
+constexpr int64_t kWgTrSmallPartBytes = 16ll << 20;   // partial-tile budget of small bf16 weight gradients
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct WgradPlan {
@@ -143,9 +144,12 @@ inline WgTrPlan wgrad_tr_plan(int64_t m, int n, int h, int w, int c_in, int c_ou
     const int64_t n_out = (int64_t)p.ci_tiles * p.co_tiles;
     int64_t s = ceil_div(512, n_out);                 // two workgroups per CU
     // partial tiles (S * |dW| float32, written and read once) kept below the
-    // operand bytes
+    // operand bytes, or below kWgTrSmallPartBytes for small operands (late
+    // DenseNet blocks: a launch of a few dozen workgroups is latency-bound,
+    // and a few MB more of partial tiles cost less than the idle CUs)
     const int64_t dw_bytes = (int64_t)k * k * c_in * c_out * 4;
-    const int64_t in_bytes = m * (int64_t)(c_in + c_out) * 2;
+    int64_t in_bytes = m * (int64_t)(c_in + c_out) * 2;
+    if (in_bytes < kWgTrSmallPartBytes) in_bytes = kWgTrSmallPartBytes;
     int64_t cap = in_bytes / (dw_bytes > 0 ? dw_bytes : 1);
     if (cap < 1) cap = 1;
     if (s > cap) s = cap;
