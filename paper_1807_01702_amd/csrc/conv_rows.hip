@@ -710,17 +710,20 @@ hipError_t launch_conv_rows(const RowsParams &p, hipStream_t s)
             if (dw && p.pro == PRO_BNRELU && !p.wtrans) {
                 if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1, SP_FWD_BNRELU>(p, s);
                 if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1, SP_FWD_BNRELU>(p, s);
+                if (t.bm == 32) return run_rows<bf16_t, 1, 32, 128, 2, 2, SP_FWD_BNRELU>(p, s);
                 if (t.bm == 64) return run_rows<bf16_t, 1, 64, 128, 2, 2, SP_FWD_BNRELU>(p, s);
                 return run_rows<bf16_t, 1, 128, 128, 2, 2, SP_FWD_BNRELU>(p, s);
             }
             if (dw && p.pro == PRO_BNGRAD && p.wtrans) {
                 if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1, SP_DGRAD_BNGRAD>(p, s);
                 if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1, SP_DGRAD_BNGRAD>(p, s);
+                if (t.bm == 32) return run_rows<bf16_t, 1, 32, 128, 2, 2, SP_DGRAD_BNGRAD>(p, s);
                 if (t.bm == 64) return run_rows<bf16_t, 1, 64, 128, 2, 2, SP_DGRAD_BNGRAD>(p, s);
                 return run_rows<bf16_t, 1, 128, 128, 2, 2, SP_DGRAD_BNGRAD>(p, s);
             }
             if (t.bn == 32) return run_rows<bf16_t, 1, 128, 32, 4, 1>(p, s);
             if (t.bn == 64) return run_rows<bf16_t, 1, 128, 64, 4, 1>(p, s);
+            if (t.bm == 32) return run_rows<bf16_t, 1, 32, 128, 2, 2>(p, s);
             if (t.bm == 64) return run_rows<bf16_t, 1, 64, 128, 2, 2>(p, s);
             return run_rows<bf16_t, 1, 128, 128, 2, 2>(p, s);
         }

@@ -38,13 +38,16 @@ constexpr int kRowsBK = 32;
 constexpr int kRowsMaxW3 = 62;             // largest image width for 3x3 (halo = W+1 rows)
 struct RowsTile { int bm, bn; };
 // m > 0: a bf16 1x1 grid of 128-row tiles that would leave CUs idle (the
-// late DenseNet blocks: 14x14 and 7x7 images) takes 64-row tiles instead
+// late DenseNet blocks: 14x14 and 7x7 images) takes 64-row tiles instead,
+// and 32-row tiles below 128 tiles of 64 rows (7x7 images at batch 128)
 inline RowsTile rows_tile(int dtype, int taps, int n_out, int64_t m = 0) {
     if (dtype == DT_F32) return RowsTile{64, n_out <= 32 ? 32 : 64};
     if (taps == 1) {
         const int bn = n_out <= 64 ? (n_out <= 32 ? 32 : 64) : 128;
-        const int64_t tiles128 = (m + 127) / 128 * ((n_out + bn - 1) / bn);
-        return RowsTile{bn == 128 && m > 0 && tiles128 < 256 ? 64 : 128, bn};
+        const int64_t nt = (n_out + bn - 1) / bn;
+        const int64_t tiles128 = (m + 127) / 128 * nt, tiles64 = (m + 63) / 64 * nt;
+        if (bn != 128 || m <= 0 || tiles128 >= 256) return RowsTile{128, bn};
+        return RowsTile{tiles64 >= 128 ? 64 : 32, bn};
     }
     return RowsTile{128, n_out <= 32 ? 32 : 64};
 }
@@ -59,7 +62,7 @@ constexpr int kWgKC = 64;                  // K positions per chunk
 constexpr int kWgCIT = 64;                 // input channels per tile
 constexpr int kWgMaxW3 = 62;               // widest 3x3 image row (PW <= 64)
 constexpr int kWgTrKQ1 = 64;               // pixels per chunk of the bf16 1x1 weight gradient (128: slower)
-constexpr int64_t kWgTrSmallPartBytes = 16ll << 20;   // partial-tile budget of small bf16 weight gradients
+constexpr int64_t kWgTrSmallPartBytes = 32ll << 20;   // partial-tile budget of small bf16 weight gradients
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct WgradPlan {
