@@ -655,7 +655,7 @@ def main():
         print(summarize_trace(args.summarize_trace[0], int(args.summarize_trace[1]), args.workload, args.bench_json))
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
     import torch
     if args.bn_passes:
