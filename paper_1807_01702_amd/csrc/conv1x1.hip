@@ -192,20 +192,24 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     if (tid < NP) { epi[tid] = ep0; epi[NP + tid] = ep1; epi[2 * NP + tid] = ep2; epi[3 * NP + tid] = ep3; }
 
     // ---- tile operand registers ----
+    // A slot j of this thread: channel vector av of row ar0 + j RPS, with
+    // VPR vectors per row and RPS = kP1Threads / VPR rows per step (the
+    // launcher checks that NVA slots cover a tile).  Consecutive lanes read
+    // consecutive 16-byte vectors of one pixel row (whole rows per wave), and
+    // a thread's channels are the same in every slot and every tile, so its
+    // prologue coefficients are read from LDS once per launch, not per tile.
     const int VPR = KP / VEC;                          // A vectors per row
-    const int nva = (BM * VPR + kP1Threads - 1) / kP1Threads;
-    // A slot j of this thread: 4 consecutive lanes cover 4 channel vectors (64
-    // contiguous bytes of one pixel row), 16 lane groups cover 16 rows, so a
-    // wave touches only 4 distinct prologue-coefficient addresses (LDS
-    // broadcast, no bank conflicts).
+    const int RPS = kP1Threads / VPR;
+    const int av = tid % VPR, ar0 = tid / VPR;
     int sr[NVA], sc[NVA];
+    bool sv[NVA];
     #pragma unroll
     for (int j = 0; j < NVA; j++) {
-        const int i = tid + j * kP1Threads;
-        const int q = i >> 2;
-        sr[j] = q % BM;
-        sc[j] = ((q / BM) * 4 + (i & 3)) * VEC;
+        sr[j] = ar0 + j * RPS;
+        sc[j] = av * VEC;
+        sv[j] = ar0 < RPS && sr[j] < BM;
     }
+    float kc0[VEC], kc1[VEC], kc2[VEC];                // its prologue coefficients (set below)
     vec16 ra[NVA * PF], rb[NVB];
     // the wave-uniform mode switches sit outside the slot loops, so each
     // mode's slots are straight-line code
@@ -215,7 +219,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int q = p0 + sr[j], c = sc[j];
-                const bool ok = j < nva && c < K && q < lim;
+                const bool ok = sv[j] && c < K && q < lim;
                 const int img = q / (ho * wo);
                 const int rem = q - img * ho * wo;
                 const int y = rem / wo, x = rem - y * wo;
@@ -230,7 +234,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int pp = p0 + sr[j], c = sc[j];
-                const bool ok = j < nva && c < K && pp < lim;
+                const bool ok = sv[j] && c < K && pp < lim;
                 const int img = pp / (H * W);
                 const int rem = pp - img * H * W;
                 const int y = rem / W, x = rem - y * W;
@@ -241,7 +245,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
                 const int pp = p0 + sr[j], c = sc[j];
-                const bool ok = j < nva && c < K && pp < lim;
+                const bool ok = sv[j] && c < K && pp < lim;
                 ra[j] = bld16(abuf, ok ? (uint32_t)(pp * a_ldc + c) * 2u : kBufOff);
                 if (TWO) rb[j < NVB ? j : 0] = bld16(a2buf, ok ? (uint32_t)(pp * a2_ldc + c) * 2u : kBufOff);
             }
@@ -253,45 +257,35 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     // coefficients and zero weights.
     auto store_a = [&](int p0, int lim) __attribute__((always_inline)) {
         auto put = [&](int j, const vec16 &v) __attribute__((always_inline)) {
-            if (j < nva && sc[j] < KP) *reinterpret_cast<vec16 *>(As + sr[j] * g.lda + sc[j]) = v;
+            if (sv[j]) *reinterpret_cast<vec16 *>(As + sr[j] * g.lda + sc[j]) = v;
         };
         if (BNADD) {                                      // r = max(y c0 + c1 + identity, 0), also stored
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
-                const int c = sc[j] < KP ? sc[j] : 0;
-                float f[VEC], id[VEC], ca[VEC], cb[VEC];
+                float f[VEC], id[VEC];
                 Elem<T>::unpack(ra[j], f);
                 Elem<T>::unpack(rb[j < NVB ? j : 0], id);
-                lds_f8(coef + c, ca);
-                lds_f8(coef + KP + c, cb);
                 #pragma unroll
-                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(bn_lin(f[e], ca[e], cb[e]) + id[e], 0.f);
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaxf(bn_lin(f[e], kc0[e], kc1[e]) + id[e], 0.f);
                 const vec16 v = Elem<T>::pack(f);
                 put(j, v);
                 const int pp = p0 + sr[j];
-                bst16(sbuf, j < nva && sc[j] < K && pp < lim ? (uint32_t)(pp * side_ldc + sc[j]) * 2u : kBufOff, v);
+                bst16(sbuf, sv[j] && sc[j] < K && pp < lim ? (uint32_t)(pp * side_ldc + sc[j]) * 2u : kBufOff, v);
             }
         } else if (BNG) {                                        // PRO_BNGRAD: d = c0 dy + c1 x + c2
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
-                const int c = sc[j] < KP ? sc[j] : 0;
-                float f[VEC], x[VEC], c0[VEC], c1[VEC], c2[VEC];
+                float f[VEC], x[VEC];
                 Elem<T>::unpack(ra[j], f);
                 Elem<T>::unpack(rb[j < NVB ? j : 0], x);
-                lds_f8(coef + c, c0);
-                lds_f8(coef + KP + c, c1);
-                lds_f8(coef + 2 * KP + c, c2);
                 #pragma unroll
-                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaf(c0[e], f[e], __builtin_fmaf(c1[e], x[e], c2[e]));
+                for (int e = 0; e < VEC; e++) f[e] = __builtin_fmaf(kc0[e], f[e], __builtin_fmaf(kc1[e], x[e], kc2[e]));
                 put(j, Elem<T>::pack(f));
             }
         } else if (POOLF) {                               // z = mean over the window of max(x c0 + c1, 0)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
-                const int c = sc[j] < KP ? sc[j] : 0;
-                float acc[VEC], ca[VEC], cb[VEC];
-                lds_f8(coef + c, ca);
-                lds_f8(coef + KP + c, cb);
+                float acc[VEC];
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) acc[e] = 0.f;
                 #pragma unroll
@@ -299,7 +293,7 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
                     float f[VEC];
                     Elem<T>::unpack(ra[j * PF + f4], f);
                     #pragma unroll
-                    for (int e = 0; e < VEC; e++) acc[e] += __builtin_fmaxf(bn_lin(f[e], ca[e], cb[e]), 0.f);
+                    for (int e = 0; e < VEC; e++) acc[e] += __builtin_fmaxf(bn_lin(f[e], kc0[e], kc1[e]), 0.f);
                 }
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) acc[e] *= 0.25f;
@@ -308,21 +302,18 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
         } else if (pro == PRO_BNRELU) {                   // z = max(x c0 + c1, 0)   (SAVE: also stored)
             #pragma unroll
             for (int j = 0; j < NVA; j++) {
-                const int c = sc[j] < KP ? sc[j] : 0;
-                float f[VEC], ca[VEC], cb[VEC];
+                float f[VEC];
                 Elem<T>::unpack(ra[j], f);
-                lds_f8(coef + c, ca);
-                lds_f8(coef + KP + c, cb);
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) {
-                    const float t = bn_lin(f[e], ca[e], cb[e]);
+                    const float t = bn_lin(f[e], kc0[e], kc1[e]);
                     f[e] = t > 0.f ? t : 0.f;
                 }
                 const vec16 v = Elem<T>::pack(f);
                 put(j, v);
                 if (SAVE) {
                     const int pp = p0 + sr[j];
-                    bst16(sbuf, j < nva && sc[j] < K && pp < lim ? (uint32_t)(pp * side_ldc + sc[j]) * 2u : kBufOff, v);
+                    bst16(sbuf, sv[j] && sc[j] < K && pp < lim ? (uint32_t)(pp * side_ldc + sc[j]) * 2u : kBufOff, v);
                 }
             }
         } else if (pro == PRO_RELU) {
@@ -363,6 +354,18 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
     T *yout = reinterpret_cast<T *>(p.y) + col0;
 
     __syncthreads();
+    // this thread's prologue channels are fixed too: their coefficients in registers
+    if (pro == PRO_BNRELU || pro == PRO_BNGRAD) {
+        lds_f8(coef + av * VEC, kc0);
+        lds_f8(coef + KP + av * VEC, kc1);
+        if (pro == PRO_BNGRAD) lds_f8(coef + 2 * KP + av * VEC, kc2);
+        else
+            #pragma unroll
+            for (int e = 0; e < VEC; e++) kc2[e] = 0.f;
+    } else {
+        #pragma unroll
+        for (int e = 0; e < VEC; e++) { kc0[e] = 0.f; kc1[e] = 0.f; kc2[e] = 0.f; }
+    }
     // this thread's epilogue channels are fixed: keep their BN parameters in registers
     float eM[VEC], eR[VEC], eG[VEC], eB[VEC], eC0[VEC], eC1[VEC], eS[VEC];
     #pragma unroll
@@ -594,6 +597,9 @@ static hipError_t run_p1(const RowsParams &p, const P1Geom &g, hipStream_t s, in
     const int64_t per_group = gmax / g.ncg > 1 ? gmax / g.ncg : 1;
     P1Geom gg = g;
     gg.gcw = (int)(ntiles < per_group ? ntiles : per_group);
+    // a thread's NVA A slots step over rows kP1Threads / (KP / 8) apart: they must cover a tile
+    const int rps = kP1Threads / (g.KP / 8);
+    if ((BM + rps - 1) / rps > NVA) return hipErrorInvalidValue;
     const int grid = gg.gcw * g.ncg;
     *rows = gg.gcw;
     const double m = (double)p.m;
