@@ -479,18 +479,23 @@ __global__ __launch_bounds__(kThreads, (TAPS == 3 && COT == 64) ? 1 : 2) void k_
             for (int i = 0; i < 4; i++) out.u[i] = valid ? out.u[i] : 0u;
             *reinterpret_cast<vec16 *>(Zs + (row < ZR ? row : ZR) * ZP + vz * VEC) = out;
         }
+        // (this thread's G channel vector is the same in every slot: its
+        // deferred-gradient coefficients are read once per chunk)
+        float gA[VEC], gB[VEC], gC[VEC];
+        if (GS == GB_BNGRAD) {
+            lds_f8(gco + vg * VEC, gA);
+            lds_f8(gco + COT + vg * VEC, gB);
+            lds_f8(gco + 2 * COT + vg * VEC, gC);
+        }
         #pragma unroll
         for (int j = 0; j < NG; j++) {
             const int row = tid / VG + j * (kThreads / VG);
             vec16 out = gr[j];
             if (GS == GB_BNGRAD) {
                 const bool valid = (row < KQ) & (pix(base, h0, j, false) >= 0) & gc_ok;
-                float d[VEC], x[VEC], gA[VEC], gB[VEC], gC[VEC];
+                float d[VEC], x[VEC];
                 Elem<T>::unpack(gr[j], d);
                 Elem<T>::unpack(gx[j < NGX ? j : 0], x);
-                lds_f8(gco + vg * VEC, gA);
-                lds_f8(gco + COT + vg * VEC, gB);
-                lds_f8(gco + 2 * COT + vg * VEC, gC);
                 #pragma unroll
                 for (int e = 0; e < VEC; e++) d[e] = __builtin_fmaf(gA[e], d[e], __builtin_fmaf(gB[e], x[e], gC[e]));
                 out = Elem<T>::pack(d);
