@@ -261,31 +261,43 @@ __global__ __launch_bounds__(kThreads) void k_conv_rows(RowsParams p)
                     rw[j] = bld16(wbuf, off);
                 }
             };
+            // every slot of a thread holds the same channel vector of a chunk
+            // (kThreads is a multiple of VPR): its coefficients are read once
+            // per chunk, not once per slot
+            static_assert(kThreads % VPR == 0, "slot channels");
             auto store_chunk = [&](int ch) __attribute__((always_inline)) {
                 const int c0 = ch * BK;
+                const int cv = c0 + (tid % VPR) * VEC, cc = cv < K ? cv : 0;
+                float k0[VEC], k1[VEC], k2[VEC], kc[VEC];
+                if (pro == PRO_BNRELU || pro == PRO_BNGRAD) {
+                    #pragma unroll
+                    for (int e = 0; e < VEC; e++) {
+                        k0[e] = coef[cc + e];
+                        k1[e] = coef[K + cc + e];
+                        k2[e] = coef[2 * K + cc + e];
+                        kc[e] = kcen(cc + e);
+                    }
+                }
                 #pragma unroll
                 for (int j = 0; j < NA; j++) {
                     const int c = c0 + avec[j] * VEC;
                     vec16 out = ra[j];
                     if (pro == PRO_BNRELU) {
-                        const int cc = c < K ? c : 0;
                         float f[VEC];
                         Elem<T>::unpack(ra[j], f);
                         #pragma unroll
                         for (int e = 0; e < VEC; e++) {
-                            const float t = bn_lin(f[e] - kcen(cc + e), coef[K + cc + e], coef[2 * K + cc + e]);
+                            const float t = bn_lin(f[e] - kc[e], k1[e], k2[e]);
                             f[e] = t > 0.f ? t : 0.f;
                         }
                         out = Elem<T>::pack(f);
                     } else if (pro == PRO_BNGRAD) {
-                        const int cc = c < K ? c : 0;
                         float d[VEC], x[VEC];
                         Elem<T>::unpack(ra[j], d);
                         Elem<T>::unpack(rx[j], x);
                         #pragma unroll
                         for (int e = 0; e < VEC; e++)
-                            d[e] = __builtin_fmaf(coef[cc + e], d[e],
-                                                  __builtin_fmaf(coef[K + cc + e], x[e] - kcen(cc + e), coef[2 * K + cc + e]));
+                            d[e] = __builtin_fmaf(k0[e], d[e], __builtin_fmaf(k1[e], x[e] - kc[e], k2[e]));
                         out = Elem<T>::pack(d);
                     } else if (pro == PRO_RELU) {
                         float f[VEC];
