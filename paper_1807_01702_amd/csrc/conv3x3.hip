@@ -420,8 +420,15 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
         for (int j = 0; j < NVA; j++) {
             const int c = (4 * j + (tid & 3)) * VEC;
             *reinterpret_cast<vec16 *>(ring + s1 * lda + c) = outv[j];
-            *reinterpret_cast<vec16 *>(ring + s2 * lda + c) = outv[j];
         }
+        // the copies of the first 16 ring rows: a branch around stores only
+        // (most waves hold none of those rows and skip the writes)
+        if (s2 != RING + 16)
+            #pragma unroll
+            for (int j = 0; j < NVA; j++) {
+                const int c = (4 * j + (tid & 3)) * VEC;
+                *reinterpret_cast<vec16 *>(ring + s2 * lda + c) = outv[j];
+            }
     };
 
     // ---- epilogue operand: thread = one channel vector of rows r0, r0+RSTEP, ... ----
