@@ -356,9 +356,10 @@ __global__ __launch_bounds__(kP3Threads) void k_conv3x3(RowsParams p, P3Geom g)
 
     // ---- prologue transform of a batch, then the ring writes.  The mode
     // switch is wave-uniform and outside the vector loop; invalid rows are
-    // zeroed on the packed words and rows past the batch (and the copies of
-    // rows beyond the first 16) go to a junk row, so each mode's vectors are
-    // straight-line code.  32 NVA = KPC: every channel vector is in range. ----
+    // zeroed on the packed words and rows past the batch go to a junk row, so
+    // each mode's vectors are straight-line code; only the copies of the first
+    // 16 ring rows are written under a branch (around stores, no loads).
+    // 32 NVA = KPC: every channel vector is in range. ----
     static_assert(32 * NVA == KPC, "batch vectors");
     auto store_rows = [&](int cnt, int slot0, Batch &bt) __attribute__((always_inline)) {
         const int arow = tid >> 2;

@@ -127,6 +127,8 @@ FWD_CASES = [
     (True, 1, 1, 9, 11, 320, 96, 320, 104),      # same, partial output tile, output view
     (True, 1, 1, 5, 13, 296, 24, 304, 24),       # tiled 1x1: ragged last 64-channel chunk, 32-channel output tile
     (True, 1, 1, 3, 5, 1000, 64, 1000, 64),      # tiled 1x1: 16 chunks, 64-channel output tile
+    (True, 1, 128, 7, 7, 992, 128, 992, 128),    # DenseNet-121 block 4 at batch 128: tiled 1x1 in 32-row tiles
+    (True, 3, 128, 7, 7, 128, 32, 128, 32),      # its 3x3 at batch 128: one persistent workgroup per 32 pixels
 ]
 
 
@@ -261,6 +263,9 @@ BWD_CASES = [
     (True, 3, 4, 56, 56, 128, 32),              # 3x3 weight gradient: 5 chunks per split, Z rows carried between
                                                 # chunks, splits crossing image boundaries
     (True, 3, 8, 30, 7, 64, 32),                # same with 14-row chunks of 7-pixel rows
+    (True, 3, 128, 7, 7, 128, 32),              # DenseNet-121 block 4 at batch 128: 196 persistent 3x3
+                                                # workgroups, 64-way split-K weight gradient (small-operand budget)
+    (True, 1, 128, 7, 7, 992, 128),             # its 1x1: data gradient in four column groups, wide split-K dW
 ]
 
 
