@@ -21,7 +21,8 @@ steps, the byte-counter calibration reference), --only VARIANT, --no-ablation
 Counter summaries (no GPU needed): --summarize-pmc (per-class bytes of the
 dominant-kernel roofline), --summarize-step-bytes FETCH_DIR WRITE_DIR (HBM bytes
 per step of a profile-only run), --summarize-mfma PMC_DIR (matrix-core rate and
-busy fraction per kernel class), --summarize-trace (rocprofv3 --stats tables).
+busy fraction per kernel class), --summarize-lds PMC_DIR (LDS instructions and
+bank-conflict cycles per kernel class), --summarize-trace (rocprofv3 --stats tables).
 
 HBM traffic of the dominant kernel (`roofline.traffic`): two rocprofv3
 counter runs of the profile-only command, one with FETCH_SIZE and one with
@@ -76,6 +77,7 @@ def parse():
                     help="RUN_DIR/sb_f_V, RUN_DIR/sb_w_V of each variant V (profile-only runs, --steps 2 --warmup 1) "
                          "-> profiles/hbm_bytes_per_step_<workload>.json and a markdown table (with --bench-json)")
     ap.add_argument("--summarize-mfma", metavar="PMC_DIR", default=None)
+    ap.add_argument("--summarize-lds", metavar="PMC_DIR", default=None)
     ap.add_argument("--calib-copy-mb", type=int, default=0)
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"), default=None)
     ap.add_argument("--summarize-trace", nargs=2, metavar=("KERNEL_STATS_CSV", "STEPS"), default=None)
@@ -464,6 +466,35 @@ def summarize_mfma(pmc_dir, dtype="bf16"):
     return "\n".join(out)
 
 
+def summarize_lds(pmc_dir):
+    """Markdown table per kernel class from a rocprofv3 --pmc run with
+    SQ_INSTS_LDS and SQ_LDS_BANK_CONFLICT: LDS instructions and bank-conflict
+    cycles per dispatch (summed over the dispatch's waves), and conflict
+    cycles per LDS instruction."""
+    disp = {}
+    for path in glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                d = disp.setdefault((path, r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
+                d[r["Counter_Name"]] = float(r["Counter_Value"])
+    agg = {}
+    for d in disp.values():
+        c = kernel_class(d["name"])
+        if c is None or "SQ_INSTS_LDS" not in d:
+            continue
+        a = agg.setdefault(c, [0, 0.0, 0.0])
+        a[0] += 1
+        a[1] += d["SQ_INSTS_LDS"]
+        a[2] += d.get("SQ_LDS_BANK_CONFLICT", 0.0)
+    out = ["| class | dispatches | LDS instructions per dispatch | bank-conflict cycles per dispatch | "
+           "conflict cycles per LDS instruction |", "|---|---|---|---|---|"]
+    for c, (n, li, bc) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        if li <= 0:
+            continue
+        out.append("| %s | %d | %.0f | %.0f | %.2f |" % (c, n, li / n, bc / n, bc / li))
+    return "\n".join(out)
+
+
 def traffic_for(workload, cls):
     """Counter bytes per launch of a kernel class, if measured on the current sources."""
     path = os.path.join(ROOT, "profiles", "hbm_traffic_%s.json" % workload)
@@ -635,6 +666,9 @@ def main():
         return
     if args.summarize_mfma:
         print(summarize_mfma(args.summarize_mfma))
+        return
+    if args.summarize_lds:
+        print(summarize_lds(args.summarize_lds))
         return
     if args.summarize_step_bytes:
         if args.calib_copy_mb <= 0:
