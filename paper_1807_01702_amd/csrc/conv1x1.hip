@@ -146,7 +146,43 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
 
     // ---- weights -> LDS as Ws[n][k] (zero outside K x N), in batches of
     // kWB vectors per thread whose loads are all in flight before any write ----
-    {
+    if (!p.wtrans) {
+        // forward W[k][n] -> Ws[n][k]: an item is four consecutive k of one
+        // 8-column group (four 16-byte loads), written as one 8-byte word per
+        // column (a quarter of the LDS writes of single elements)
+        constexpr int kWB = 8, kIB = kWB / 4;
+        const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(K * NT * 2));
+        const int KQ = KP / 4, items = KQ * (NP / VEC);
+        for (int base = 0; base < items; base += kIB * kP1Threads) {
+            vec16 v[kWB];
+            #pragma unroll
+            for (int u = 0; u < kWB; u++) {
+                if (base + (u >> 2) * kP1Threads >= items) break;   // (uniform: no empty loads issued)
+                const int it = base + (u >> 2) * kP1Threads + tid;
+                const int n0 = (it / KQ) * VEC, k = (it % KQ) * 4 + (u & 3);
+                const int off = it < items && k < K && n0 < N ? (k * NT + col0 + n0) * 2 : (int)kBufOff;
+                v[u] = bld16(wbuf, (uint32_t)off);
+            }
+            #pragma unroll
+            for (int ui = 0; ui < kIB; ui++) {
+                const int it = base + ui * kP1Threads + tid;
+                if (base + ui * kP1Threads >= items) break;
+                if (it < items) {
+                    const int n0 = (it / KQ) * VEC, k0 = (it % KQ) * 4;
+                    #pragma unroll
+                    for (int e = 0; e < VEC; e++) {
+                        uint32_t h[4];
+                        #pragma unroll
+                        for (int q = 0; q < 4; q++)
+                            h[q] = (e & 1) ? (v[ui * 4 + q].u[e >> 1] >> 16) : (v[ui * 4 + q].u[e >> 1] & 0xffffu);
+                        *reinterpret_cast<uint2 *>(Ws + (n0 + e) * g.ldw + k0) =
+                            make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                    }
+                }
+            }
+        }
+    } else {
+        // data gradient: W[n][k] (n = c_in, k = c_out), rows of k copied straight
         constexpr int kWB = 8;
         const __amdgpu_buffer_rsrc_t wbuf = buf_view(wsrc, (uint32_t)(K * NT * 2));
         const int total = KP * NP / VEC;
@@ -156,29 +192,16 @@ __global__ __launch_bounds__(kP1Threads) void k_conv1x1(RowsParams p, P1Geom g)
             for (int u = 0; u < kWB; u++) {
                 if (base + u * kP1Threads >= total) break;   // (uniform: no empty loads issued)
                 const int i = base + u * kP1Threads + tid;
-                int off;
-                if (!p.wtrans) {  // forward: W[k][n] (k = c_in, n = c_out); consecutive lanes take consecutive k
-                    const int n0 = (i / KP) * VEC, k = i % KP;
-                    off = i < total && k < K && n0 < N ? (k * NT + col0 + n0) * 2 : (int)kBufOff;
-                } else {          // data gradient: W[n][k] (n = c_in, k = c_out), rows of k
-                    const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
-                    off = i < total && n < N && k0 < K ? ((col0 + n) * K + k0) * 2 : (int)kBufOff;
-                }
+                const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
+                const int off = i < total && n < N && k0 < K ? ((col0 + n) * K + k0) * 2 : (int)kBufOff;
                 v[u] = bld16(wbuf, (uint32_t)off);
             }
             #pragma unroll
             for (int u = 0; u < kWB; u++) {
                 const int i = base + u * kP1Threads + tid;
                 if (i >= total) break;
-                if (!p.wtrans) {  // scatter the n row to columns (a wave writes 64 consecutive k of a column)
-                    const int n0 = (i / KP) * VEC, k = i % KP;
-                    #pragma unroll
-                    for (int e = 0; e < VEC; e++)
-                        Ws[(n0 + e) * g.ldw + k] = (T)((e & 1) ? (v[u].u[e >> 1] >> 16) : (v[u].u[e >> 1] & 0xffffu));
-                } else {          // rows copy straight
-                    const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
-                    *reinterpret_cast<vec16 *>(Ws + n * g.ldw + k0) = v[u];
-                }
+                const int n = i / (KP / VEC), k0 = (i % (KP / VEC)) * VEC;
+                *reinterpret_cast<vec16 *>(Ws + n * g.ldw + k0) = v[u];
             }
         }
     }
