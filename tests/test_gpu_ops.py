@@ -129,6 +129,8 @@ FWD_CASES = [
     (True, 1, 1, 3, 5, 1000, 64, 1000, 64),      # tiled 1x1: 16 chunks, 64-channel output tile
     (True, 1, 128, 7, 7, 992, 128, 992, 128),    # DenseNet-121 block 4 at batch 128: tiled 1x1 in 32-row tiles
     (True, 3, 128, 7, 7, 128, 32, 128, 32),      # its 3x3 at batch 128: one persistent workgroup per 32 pixels
+    (True, 1, 5, 120, 110, 96, 128, 104, 128),   # persistent 1x1 forward over 66000 pixels: two whole rounds
+                                                 # of 128-row tiles, then the 464 rows left split over the grid
 ]
 
 
