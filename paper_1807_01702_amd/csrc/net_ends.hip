@@ -700,8 +700,9 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
 // A(i,k) = a[i*sai + k*sak] (float32), B(k,j) = b[k*sbk + j*sbj] (TB).  16x64
 // output tiles (enough workgroups for the 128-image batch), K in chunks of 64
 // staged in LDS with the operand's contiguous index running across the
-// threads (coalesced for either orientation), 4 outputs per thread, k summed
-// in order (deterministic).
+// threads (coalesced for either orientation), 4 consecutive outputs of one
+// row per thread (A staged [i][k]: four k of its row in one 16-byte LDS read;
+// B: the four columns of a k in one), k summed in order (deterministic).
 template <typename TB>
 __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const float *__restrict__ a, int64_t sai,
                                                       int64_t sak, const TB *__restrict__ b, int64_t sbk,
@@ -709,7 +710,8 @@ __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const
                                                       float *__restrict__ out)
 {
     constexpr int BM = 16, BN = 64, BK = 64;
-    __shared__ float As[BK][BM + 1], Bs[BK][BN + 4];
+    __shared__ __align__(16) float As[BM][BK + 4];
+    __shared__ __align__(16) float Bs[BK][BN + 4];
     const int tid = threadIdx.x, tr = tid / 16, tc = tid % 16;
     const int i0 = blockIdx.y * BM, j0 = blockIdx.x * BN;
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
@@ -743,7 +745,7 @@ __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const
         for (int u = 0; u < NA; u++) {
             const int e = tid + u * kThreads;
             const int kk = sak == 1 ? e % BK : e / BM, ii = sak == 1 ? e / BK : e % BM;
-            As[kk][ii] = aok[u] ? av[u] : 0.f;
+            As[ii][kk] = aok[u] ? av[u] : 0.f;
         }
         #pragma unroll
         for (int u = 0; u < NB; u++) {
@@ -755,17 +757,24 @@ __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const
             Bs[kk][jj] = bok[u] ? f : 0.f;
         }
         __syncthreads();
-        #pragma unroll 16
-        for (int kk = 0; kk < BK; kk++) {
-            const float av = As[kk][tr];
+        #pragma unroll 4
+        for (int k4 = 0; k4 < BK; k4 += 4) {
+            const float4 a4 = *reinterpret_cast<const float4 *>(&As[tr][k4]);
+            const float ak[4] = {a4.x, a4.y, a4.z, a4.w};
             #pragma unroll
-            for (int v = 0; v < 4; v++) acc[v] = __builtin_fmaf(av, Bs[kk][tc + 16 * v], acc[v]);
+            for (int q = 0; q < 4; q++) {
+                const float4 b4 = *reinterpret_cast<const float4 *>(&Bs[k4 + q][4 * tc]);
+                acc[0] = __builtin_fmaf(ak[q], b4.x, acc[0]);
+                acc[1] = __builtin_fmaf(ak[q], b4.y, acc[1]);
+                acc[2] = __builtin_fmaf(ak[q], b4.z, acc[2]);
+                acc[3] = __builtin_fmaf(ak[q], b4.w, acc[3]);
+            }
         }
         __syncthreads();
     }
     #pragma unroll
     for (int v = 0; v < 4; v++) {
-        const int gi = i0 + tr, gj = j0 + tc + 16 * v;
+        const int gi = i0 + tr, gj = j0 + 4 * tc + v;
         if (gi < M && gj < N) out[(int64_t)gi * N + gj] = acc[v] + (bias ? bias[gj] : 0.f);
     }
 }
