@@ -697,24 +697,26 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
 }
 
 // Small float32 GEMM for the FC layer: out[i][j] = sum_k A(i,k) B(k,j) (+ bias[j]),
-// A(i,k) = a[i*sai + k*sak] (float32), B(k,j) = b[k*sbk + j*sbj] (TB).  16x64
-// output tiles (enough workgroups for the 128-image batch), K in chunks of 64
-// staged in LDS with the operand's contiguous index running across the
-// threads (coalesced for either orientation), 4 consecutive outputs of one
-// row per thread (A staged [i][k]: four k of its row in one 16-byte LDS read;
-// B: the four columns of a k in one), k summed in order (deterministic).
+// A(i,k) = a[i*sai + k*sak] (float32), B(k,j) = b[k*sbk + j*sbj] (TB).  16 x
+// kFcBN output tiles (two workgroups per CU for the 128-image batch), K in
+// chunks of 64 staged in LDS with the operand's contiguous index running
+// across the threads (coalesced for either orientation), 2 consecutive
+// outputs of one row per thread (A staged [i][k]: four k of its row in one
+// 16-byte LDS read; B: the two columns of a k in one), k summed in order
+// (deterministic).
+constexpr int kFcBN = 32;                 // output columns per workgroup tile
 template <typename TB>
 __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const float *__restrict__ a, int64_t sai,
                                                       int64_t sak, const TB *__restrict__ b, int64_t sbk,
                                                       int64_t sbj, const float *__restrict__ bias,
                                                       float *__restrict__ out)
 {
-    constexpr int BM = 16, BN = 64, BK = 64;
+    constexpr int BM = 16, BN = kFcBN, BK = 64;
     __shared__ __align__(16) float As[BM][BK + 4];
     __shared__ __align__(16) float Bs[BK][BN + 4];
     const int tid = threadIdx.x, tr = tid / 16, tc = tid % 16;
     const int i0 = blockIdx.y * BM, j0 = blockIdx.x * BN;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    float acc[2] = {0.f, 0.f};
     constexpr int NA = BK * BM / kThreads, NB = BK * BN / kThreads;
     for (int k0 = 0; k0 < K; k0 += BK) {
         // every load of the chunk at a clamped index first, then the LDS
@@ -763,18 +765,16 @@ __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const
             const float ak[4] = {a4.x, a4.y, a4.z, a4.w};
             #pragma unroll
             for (int q = 0; q < 4; q++) {
-                const float4 b4 = *reinterpret_cast<const float4 *>(&Bs[k4 + q][4 * tc]);
-                acc[0] = __builtin_fmaf(ak[q], b4.x, acc[0]);
-                acc[1] = __builtin_fmaf(ak[q], b4.y, acc[1]);
-                acc[2] = __builtin_fmaf(ak[q], b4.z, acc[2]);
-                acc[3] = __builtin_fmaf(ak[q], b4.w, acc[3]);
+                const float2 b2 = *reinterpret_cast<const float2 *>(&Bs[k4 + q][2 * tc]);
+                acc[0] = __builtin_fmaf(ak[q], b2.x, acc[0]);
+                acc[1] = __builtin_fmaf(ak[q], b2.y, acc[1]);
             }
         }
         __syncthreads();
     }
     #pragma unroll
-    for (int v = 0; v < 4; v++) {
-        const int gi = i0 + tr, gj = j0 + 4 * tc + v;
+    for (int v = 0; v < 2; v++) {
+        const int gi = i0 + tr, gj = j0 + 2 * tc + v;
         if (gi < M && gj < N) out[(int64_t)gi * N + gj] = acc[v] + (bias ? bias[gj] : 0.f);
     }
 }
@@ -1048,7 +1048,7 @@ hipError_t launch_head_fwd(int dtype, const HeadParams &p, hipStream_t s)
     const int nt = p.n * (p.c / vec);
     if (dtype == DT_BF16) hipLaunchKernelGGL(k_head_pool<bf16_t>, dim3((unsigned)ceil_div(nt, kThreads)), dim3(kThreads), 0, s, p);
     else hipLaunchKernelGGL(k_head_pool<float>, dim3((unsigned)ceil_div(nt, kThreads)), dim3(kThreads), 0, s, p);
-    dim3 grid((unsigned)ceil_div(p.classes, 64), (unsigned)ceil_div(p.n, 16));
+    dim3 grid((unsigned)ceil_div(p.classes, kFcBN), (unsigned)ceil_div(p.n, 16));
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_fc_gemm<bf16_t>, grid, dim3(kThreads), 0, s, p.n, p.classes, p.c, p.f, (int64_t)p.c,
                            (int64_t)1, (const bf16_t *)p.wfc, (int64_t)p.classes, (int64_t)1, p.bfc, p.logits);
@@ -1069,7 +1069,7 @@ hipError_t launch_head_bwd_fc(int dtype, const HeadParams &p, hipStream_t s)
     TraceScope tr(KC_SMALL, KID_HEAD, s, 4.0 * ((double)p.n * p.classes + 2.0 * p.n * p.c + (double)p.c * p.classes),
                   4.0 * p.n * p.c * p.classes);
     // df = dlogits W^T: A = dlogits [n][K], B(k=j, col=c) = W[c][j]
-    dim3 g1((unsigned)ceil_div(p.c, 64), (unsigned)ceil_div(p.n, 16));
+    dim3 g1((unsigned)ceil_div(p.c, kFcBN), (unsigned)ceil_div(p.n, 16));
     if (dtype == DT_BF16)
         hipLaunchKernelGGL(k_fc_gemm<bf16_t>, g1, dim3(kThreads), 0, s, p.n, p.c, p.classes, p.dlogits,
                            (int64_t)p.classes, (int64_t)1, (const bf16_t *)p.wfc, (int64_t)1, (int64_t)p.classes,
@@ -1079,7 +1079,7 @@ hipError_t launch_head_bwd_fc(int dtype, const HeadParams &p, hipStream_t s)
                            (int64_t)p.classes, (int64_t)1, (const float *)p.wfc, (int64_t)1, (int64_t)p.classes,
                            (const float *)nullptr, p.df);
     // dW = f^T dlogits: A(i=c, k=n) = f[n][c], B(k=n, j) = dlogits[n][j]
-    dim3 g2((unsigned)ceil_div(p.classes, 64), (unsigned)ceil_div(p.c, 16));
+    dim3 g2((unsigned)ceil_div(p.classes, kFcBN), (unsigned)ceil_div(p.c, 16));
     hipLaunchKernelGGL(k_fc_gemm<float>, g2, dim3(kThreads), 0, s, p.c, p.classes, p.n, p.f, (int64_t)1,
                        (int64_t)p.c, p.dlogits, (int64_t)p.classes, (int64_t)1, (const float *)nullptr, p.dwfc);
     hipLaunchKernelGGL(k_colsum, dim3((unsigned)ceil_div(p.classes, kThreads)), dim3(kThreads), 0, s, p.n, p.classes,
