@@ -698,13 +698,12 @@ __global__ __launch_bounds__(kThreads) void k_head_pool(HeadParams p)
 
 // Small float32 GEMM for the FC layer: out[i][j] = sum_k A(i,k) B(k,j) (+ bias[j]),
 // A(i,k) = a[i*sai + k*sak] (float32), B(k,j) = b[k*sbk + j*sbj] (TB).  16 x
-// kFcBN output tiles (two workgroups per CU for the 128-image batch), K in
-// chunks of 64 staged in LDS with the operand's contiguous index running
-// across the threads (coalesced for either orientation), 2 consecutive
-// outputs of one row per thread (A staged [i][k]: four k of its row in one
-// 16-byte LDS read; B: the two columns of a k in one), k summed in order
-// (deterministic).
-constexpr int kFcBN = 32;                 // output columns per workgroup tile
+// kFcBN output tiles (for the 128-image batch: 8 x 63 workgroups, two per CU
+// and more), K in chunks of 64 staged in LDS with the operand's contiguous
+// index running across the threads (coalesced for either orientation),
+// kFcBN / 16 consecutive outputs of one row per thread (A staged [i][k]: four
+// k of its row in one 16-byte LDS read), k summed in order (deterministic).
+constexpr int kFcBN = 16;                 // output columns per workgroup tile
 template <typename TB>
 __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const float *__restrict__ a, int64_t sai,
                                                       int64_t sak, const TB *__restrict__ b, int64_t sbk,
@@ -716,7 +715,10 @@ __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const
     __shared__ __align__(16) float Bs[BK][BN + 4];
     const int tid = threadIdx.x, tr = tid / 16, tc = tid % 16;
     const int i0 = blockIdx.y * BM, j0 = blockIdx.x * BN;
-    float acc[2] = {0.f, 0.f};
+    constexpr int OPT = BN / 16;                     // consecutive outputs per thread
+    float acc[OPT];
+    #pragma unroll
+    for (int v = 0; v < OPT; v++) acc[v] = 0.f;
     constexpr int NA = BK * BM / kThreads, NB = BK * BN / kThreads;
     for (int k0 = 0; k0 < K; k0 += BK) {
         // every load of the chunk at a clamped index first, then the LDS
@@ -765,16 +767,15 @@ __global__ __launch_bounds__(kThreads) void k_fc_gemm(int M, int N, int K, const
             const float ak[4] = {a4.x, a4.y, a4.z, a4.w};
             #pragma unroll
             for (int q = 0; q < 4; q++) {
-                const float2 b2 = *reinterpret_cast<const float2 *>(&Bs[k4 + q][2 * tc]);
-                acc[0] = __builtin_fmaf(ak[q], b2.x, acc[0]);
-                acc[1] = __builtin_fmaf(ak[q], b2.y, acc[1]);
+                #pragma unroll
+                for (int v = 0; v < OPT; v++) acc[v] = __builtin_fmaf(ak[q], Bs[k4 + q][OPT * tc + v], acc[v]);
             }
         }
         __syncthreads();
     }
     #pragma unroll
-    for (int v = 0; v < 2; v++) {
-        const int gi = i0 + tr, gj = j0 + 2 * tc + v;
+    for (int v = 0; v < OPT; v++) {
+        const int gi = i0 + tr, gj = j0 + OPT * tc + v;
         if (gi < M && gj < N) out[(int64_t)gi * N + gj] = acc[v] + (bias ? bias[gj] : 0.f);
     }
 }
